@@ -1,0 +1,367 @@
+"""ClusterAttention oracle: a plain, slow, fp64 CPU implementation of the method.
+
+TEST INFRASTRUCTURE ONLY. Nothing in the product path imports this module; only
+the tests, the smoke check and the bench's CPU-baseline leg may call it. It
+shares no code with the HIP library.
+
+Every function works on one attention head (2-D arrays, rows = tokens) in fp64
+and cites the passage of the paper it follows. Where the paper leaves a choice
+open, the reading taken is stated in the docstring (the same readings are
+listed in the design doc). Inputs are the exact values the GPU receives (float32 or
+bf16-representable), upcast to fp64.
+
+Pins: see tests/test_oracle_*.py. Parts with no independent pin are marked
+"parity unpinned" below (none at present).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+F64 = np.float64
+
+# ---------------------------------------------------------------------------
+# Dense attention (Preliminaries: error in sparse attention, o = sum_i w_i v_i)
+# ---------------------------------------------------------------------------
+
+
+def dense_attention(Q, K, V, tau):
+    """o_i = sum_j softmax_j(tau q_i.k_j) v_j, and lse_i = log sum_j exp(tau q_i.k_j).
+
+    Preliminaries (error in sparse attention): the output of a query is the
+    attention-weighted sum of all values.
+    """
+    Q, K, V = (np.asarray(x, F64) for x in (Q, K, V))
+    S = tau * (Q @ K.T)
+    m = S.max(axis=1, keepdims=True)
+    E = np.exp(S - m)
+    l = E.sum(axis=1, keepdims=True)
+    return (E @ V) / l, (m + np.log(l))[:, 0]
+
+
+# ---------------------------------------------------------------------------
+# Moments, eigendecompositions and the split spaces (Method: Transforms;
+# Method: Diagonalized recursive splitting; App. B.2)
+# ---------------------------------------------------------------------------
+
+
+def second_moment(X):
+    """M = X^T X / n (Method, key clustering: the metric matrix Q^T Q / n)."""
+    X = np.asarray(X, F64)
+    return X.T @ X / X.shape[0]
+
+
+def centred_cov(X):
+    """X_c^T X_c / n with X_c the column-centred matrix (Method, query clustering;
+    App. B: the covariance of the keys)."""
+    X = np.asarray(X, F64)
+    Xc = X - X.mean(axis=0)
+    return Xc.T @ Xc / X.shape[0]
+
+
+def eigh_desc(A):
+    """Eigenpairs of a symmetric matrix, eigenvalues in descending order."""
+    lam, U = np.linalg.eigh(np.asarray(A, F64))
+    order = np.argsort(-lam, kind="stable")
+    return lam[order], U[:, order]
+
+
+def psd_root(A):
+    """Root factor S = E diag(sqrt(max(lambda, 0))) of a PSD matrix, so that
+    S S^T = A with negative eigenvalues clamped to zero (Method, key clustering:
+    small negative eigenvalues are clamped to 0; x^T A y = (x S).(y S))."""
+    lam, E = eigh_desc(A)
+    return E * np.sqrt(np.maximum(lam, 0.0))[None, :]
+
+
+def orient(U, mean_row):
+    """Flip each column u_j of U so that mean_row . u_j >= 0 (the mean of the
+    projected coordinate is non-negative; exactly 0 keeps the sign). The paper
+    does not fix eigenvector signs; this reading makes the split coordinates
+    independent of the eigensolver's arbitrary sign choice."""
+    s = np.asarray(mean_row, F64) @ U
+    return U * np.where(s < 0.0, -1.0, 1.0)[None, :]
+
+
+def pca_basis(X):
+    """Principal axes of X: eigenvectors of the centred covariance, descending,
+    oriented by the data mean (Method: diagonalized recursive splitting
+    projects the data onto its principal components)."""
+    X = np.asarray(X, F64)
+    _, U = eigh_desc(centred_cov(X))
+    return orient(U, X.mean(axis=0))
+
+
+def key_split_space(Q, K, mode):
+    """Split coordinates Y_K of the keys.
+
+    none:   Y_K = K.
+    pca:    Y_K = K U, U the principal axes of K.
+    metric: keys are mapped into the query-aware metric M = Q^T Q / n (Method,
+            key clustering): K -> K S_q with S_q S_q^T = M, then projected on
+            the principal axes of K S_q (diagonalized splitting). The principal
+            axes of K S_q are the eigenvectors of S_q^T C_K S_q.
+    """
+    Q, K = np.asarray(Q, F64), np.asarray(K, F64)
+    if mode == "none":
+        return K.copy()
+    if mode == "pca":
+        return K @ pca_basis(K)
+    if mode == "metric":
+        S_q = psd_root(second_moment(Q))
+        Z = K @ S_q
+        return Z @ pca_basis(Z)
+    raise ValueError(mode)
+
+
+def query_representation(Q, K):
+    """r(q) = q S_k / |q S_k| with S_k S_k^T = K_c^T K_c / n (Method, query
+    clustering for top-k selection; App. B.2). A query with |q S_k| = 0 maps
+    to r = 0 (the paper leaves this case open)."""
+    Q, K = np.asarray(Q, F64), np.asarray(K, F64)
+    S_k = psd_root(centred_cov(K))
+    rho = Q @ S_k
+    nrm = np.sqrt((rho * rho).sum(axis=1))
+    safe = np.where(nrm > 0.0, nrm, 1.0)
+    return np.where(nrm[:, None] > 0.0, rho / safe[:, None], 0.0)
+
+
+def query_split_space(Q, K, mode):
+    """Split coordinates Y_Q of the queries: none -> Q; pca -> Q on its principal
+    axes; metric -> r(q) (top-k representation) on its principal axes."""
+    Q = np.asarray(Q, F64)
+    if mode == "none":
+        return Q.copy()
+    if mode == "pca":
+        return Q @ pca_basis(Q)
+    if mode == "metric":
+        R = query_representation(Q, K)
+        return R @ pca_basis(R)
+    raise ValueError(mode)
+
+
+# ---------------------------------------------------------------------------
+# Diagonalized recursive splitting (Method: recursive splitting; App. D.2)
+# ---------------------------------------------------------------------------
+
+
+def subsample_positions(s, m):
+    """Positions of the m-point subsample inside a node of s members (in the
+    node's order): p_j = floor((2j + 1) s / (2m)). The paper samples
+    min(a d, |S|) points with a = 1 but gives no sampling rule; this evenly
+    strided, deterministic rule is the reading taken. For m = s it is every
+    member."""
+    return [((2 * j + 1) * s) // (2 * m) for j in range(m)]
+
+
+def sequential_variance(rows):
+    """Population variance of each column of ``rows`` (m x d), fp64, two passes,
+    rows summed strictly in order, no fused multiply-add: the mean first, then
+    the mean of squared deviations. (The paper asks for the highest-variance
+    coordinate without fixing an estimator; this exact order is the reading.)"""
+    rows = np.asarray(rows, F64)
+    m = rows.shape[0]
+    acc = np.zeros(rows.shape[1], F64)
+    for j in range(m):
+        acc = acc + rows[j]
+    mean = acc / F64(m)
+    acc = np.zeros(rows.shape[1], F64)
+    for j in range(m):
+        dev = rows[j] - mean
+        acc = acc + dev * dev
+    return acc / F64(m)
+
+
+def left_size(s, c):
+    """Members sent left when splitting s points with cluster size c: the
+    multiple of c closest to half of s, taking the smaller one on a tie, i.e.
+    c * floor(ceil(s / c) / 2) (Method: basic recursive splitting)."""
+    return c * ((-(-s // c)) // 2)
+
+
+def split(Y, c, trace=None):
+    """Diagonalized recursive splitting of the rows of Y into clusters of size c.
+
+    Method: recursive splitting (basic: split so the part below the threshold
+    is the multiple of c closest to half; diagonalized: at each split pick the
+    global principal coordinate of highest variance on a subsample of min(d, s)
+    points). A node of s <= c points is a leaf. Otherwise:
+
+      1. subsample m = min(d, s) members at ``subsample_positions``;
+      2. j* = argmax of ``sequential_variance`` (ties -> lowest coordinate);
+      3. the left child gets the ``left_size(s, c)`` members with the smallest
+         (Y[i, j*], i) pairs (-0.0 counts as +0.0; equal values go by original
+         index), the right child the rest; both keep ascending index order;
+      4. recurse on the left child, then on the right child.
+
+    Returns (perm, cid, counts): perm lists the original token indices cluster
+    by cluster (leaves left to right, ascending index inside a leaf); cid[i] is
+    the cluster of token i; counts[a] the size of cluster a. If ``trace`` is a
+    list, one (members, j_star, m_left, left, right) tuple per split is
+    appended.
+    """
+    Y = np.asarray(Y, F64)
+    n, d = Y.shape
+    if c < 1:
+        raise ValueError("cluster size must be positive")
+    leaves = []
+
+    def rec(members):
+        s = len(members)
+        if s <= c:
+            leaves.append(members)
+            return
+        m = min(d, s)
+        sub = Y[members[subsample_positions(s, m)]]
+        jstar = int(np.argmax(sequential_variance(sub)))
+        mL = left_size(s, c)
+        vals = Y[members, jstar] + 0.0  # -0.0 -> +0.0
+        order = np.argsort(vals, kind="stable")  # members are in ascending index order
+        left = np.sort(members[order[:mL]])
+        right = np.sort(members[order[mL:]])
+        if trace is not None:
+            trace.append((members, jstar, mL, left, right))
+        rec(left)
+        rec(right)
+
+    rec(np.arange(n, dtype=np.int64))
+    perm = np.concatenate(leaves)
+    counts = np.array([len(x) for x in leaves], dtype=np.int64)
+    cid = np.empty(n, dtype=np.int64)
+    for a, x in enumerate(leaves):
+        cid[x] = a
+    return perm, cid, counts
+
+
+# ---------------------------------------------------------------------------
+# Centroids, scoring, selection (Method: cluster assignment)
+# ---------------------------------------------------------------------------
+
+
+def cluster_members(perm, counts):
+    starts = np.concatenate([[0], np.cumsum(counts)[:-1]])
+    return [perm[s:s + n] for s, n in zip(starts, counts)]
+
+
+def centroids(X, perm, counts):
+    """Mean of the original (untransformed) vectors of each cluster's real
+    members (Method, scoring: centroid of a cluster; App. A: centroid keys and
+    values)."""
+    X = np.asarray(X, F64)
+    return np.stack([X[mem].mean(axis=0) for mem in cluster_members(perm, counts)])
+
+
+def centroid_scores(qbar, kbar):
+    """score(a, b) = qbar_a . kbar_b, the average logit between the two clusters
+    (Method: scoring). The 1/sqrt(d) factor does not change the ranking and is
+    left out."""
+    return np.asarray(qbar, F64) @ np.asarray(kbar, F64).T
+
+
+def topk(S, k):
+    """For each query cluster, the k key clusters with the largest score (ties
+    to the lower index), listed in ascending order (Method: selection, top-k)."""
+    S = np.asarray(S, F64)
+    out = np.empty((S.shape[0], k), dtype=np.int64)
+    for a in range(S.shape[0]):
+        order = np.argsort(-S[a], kind="stable")
+        out[a] = np.sort(order[:k])
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Block-sparse attention and striped mean-compensation (Method: overview;
+# Preliminaries: error in sparse attention; App. A)
+# ---------------------------------------------------------------------------
+
+
+def sparse_attention(Q, K, V, perm_q, counts_q, perm_k, counts_k, lists, tau):
+    """o_S and lse_S for every query: softmax attention restricted to the real
+    keys of the selected key clusters of the query's cluster (Method: overview,
+    the attention step returns the output and the softmax denominator).
+    Returned in original query order."""
+    Q, K, V = (np.asarray(x, F64) for x in (Q, K, V))
+    qmem = cluster_members(perm_q, counts_q)
+    kmem = cluster_members(perm_k, counts_k)
+    o = np.zeros_like(Q)
+    lse = np.zeros(Q.shape[0])
+    for a, rows in enumerate(qmem):
+        keys = np.concatenate([kmem[b] for b in lists[a]])
+        o[rows], lse[rows] = dense_attention(Q[rows], K[keys], V[keys], tau)
+    return o, lse
+
+
+def compensate(Q, kbar, vbar, counts_k, perm_q, counts_q, lists, o_s, lse_s, tau, enable=True):
+    """Striped mean-compensation (Preliminaries: error in sparse attention; App. A).
+
+    Each key cluster b not selected for the query's cluster enters the
+    query's softmax through its centroid key and value, weighted by its size:
+    logit tau q.kbar_b + ln|b|, value vbar_b. Merged with the sparse part in
+    log-sum-exp form this equals
+        (sum_{i in S} w_i v_i + sum_b |b| w_b vbar_b) / (w_S + sum_b |b| w_b).
+    With compensation off, or all clusters selected, the output is o_S.
+    """
+    Q = np.asarray(Q, F64)
+    kbar, vbar = np.asarray(kbar, F64), np.asarray(vbar, F64)
+    out = np.array(o_s, F64, copy=True)
+    lse = np.array(lse_s, F64, copy=True)
+    if not enable:
+        return out, lse
+    n_kc = kbar.shape[0]
+    logc = np.log(np.asarray(counts_k, F64))
+    for a, rows in enumerate(cluster_members(perm_q, counts_q)):
+        excl = np.setdiff1d(np.arange(n_kc), lists[a])
+        if excl.size == 0:
+            continue
+        t = tau * (Q[rows] @ kbar[excl].T) + logc[excl][None, :]
+        m = t.max(axis=1, keepdims=True)
+        e = np.exp(t - m)
+        l = e.sum(axis=1, keepdims=True)
+        o_c = (e @ vbar[excl]) / l
+        lse_c = (m + np.log(l))[:, 0]
+        both = np.logaddexp(lse[rows], lse_c)
+        out[rows] = (np.exp(lse[rows] - both)[:, None] * out[rows]
+                     + np.exp(lse_c - both)[:, None] * o_c)
+        lse[rows] = both
+    return out, lse
+
+
+# ---------------------------------------------------------------------------
+# The whole forward pass of one head
+# ---------------------------------------------------------------------------
+
+
+def forward(Q, K, V, cq, ck, k, mode="metric", enable_comp=True, tau=None,
+            perm_q=None, perm_k=None, lists=None, scores=None):
+    """ClusterAttention for one head: clustering -> centroids -> scores ->
+    top-k -> block-sparse attention -> compensation (Method: overview).
+
+    perm_q / perm_k / scores / lists may be supplied from outside (parity hooks:
+    the checker then follows the given permutation or ranking instead of its
+    own). Returns a dict with every intermediate; ``out`` and ``lse`` are in
+    original query order.
+    """
+    Q, K, V = (np.asarray(x, F64) for x in (Q, K, V))
+    d = Q.shape[1]
+    tau = 1.0 / np.sqrt(d) if tau is None else tau
+    r = {}
+    if perm_q is None:
+        r["yq"] = query_split_space(Q, K, mode)
+        perm_q, _, _ = split(r["yq"], cq)
+    if perm_k is None:
+        r["yk"] = key_split_space(Q, K, mode)
+        perm_k, _, _ = split(r["yk"], ck)
+    nq, nk = Q.shape[0], K.shape[0]
+    counts_q = np.array([min(cq, nq - a * cq) for a in range(-(-nq // cq))])
+    counts_k = np.array([min(ck, nk - b * ck) for b in range(-(-nk // ck))])
+    r.update(perm_q=np.asarray(perm_q), perm_k=np.asarray(perm_k),
+             counts_q=counts_q, counts_k=counts_k)
+    r["qbar"] = centroids(Q, perm_q, counts_q)
+    r["kbar"] = centroids(K, perm_k, counts_k)
+    r["vbar"] = centroids(V, perm_k, counts_k)
+    r["scores"] = centroid_scores(r["qbar"], r["kbar"]) if scores is None else np.asarray(scores, F64)
+    r["lists"] = topk(r["scores"], k) if lists is None else np.asarray(lists)
+    o_s, lse_s = sparse_attention(Q, K, V, perm_q, counts_q, perm_k, counts_k, r["lists"], tau)
+    r["o_s"], r["lse_s"] = o_s, lse_s
+    r["out"], r["lse"] = compensate(Q, r["kbar"], r["vbar"], counts_k, perm_q, counts_q,
+                                    r["lists"], o_s, lse_s, tau, enable_comp)
+    return r

@@ -1,0 +1,110 @@
+"""Pins of the oracle's split spaces (Method: transforms; App. B) against the
+properties the paper derives for them."""
+import numpy as np
+import pytest
+
+from oracle import ref
+
+
+def _mix(seed, n=400, d=6, low_rank=False):
+    rng = np.random.default_rng(seed)
+    cen = rng.standard_normal((5, d)) * 2
+    Q = cen[rng.integers(0, 5, n)] + 0.5 * rng.standard_normal((n, d)) + 0.7
+    K = cen[rng.integers(0, 5, n)] + 0.5 * rng.standard_normal((n, d)) - 0.3
+    if low_rank:
+        Q[:, -2:] = 0.0  # queries span a subspace: M is singular
+    return Q, K
+
+
+@pytest.mark.parametrize("low_rank", [False, True])
+def test_key_metric_distances(low_rank):
+    """Method, key clustering: |y_a - y_b|^2 = (k_a - k_b)^T (Q^T Q / n) (k_a - k_b),
+    i.e. the mean squared difference of the two keys' logits over all queries."""
+    Q, K = _mix(0, low_rank=low_rank)
+    Y = ref.key_split_space(Q, K, "metric")
+    rng = np.random.default_rng(1)
+    for _ in range(50):
+        a, b = rng.integers(0, len(K), 2)
+        want = ((Q @ (K[a] - K[b])) ** 2).mean()
+        got = ((Y[a] - Y[b]) ** 2).sum()
+        assert abs(got - want) <= 1e-10 * max(1.0, want)
+
+
+def test_query_representation_properties():
+    """App. B.2: r(q) = R_k q / |R_k q| with R_k^T R_k = K_c^T K_c: unit norm, and
+    r_a . r_b = q_a^T C q_b / sqrt(q_a^T C q_a q_b^T C q_b), C the key covariance."""
+    Q, K = _mix(2)
+    R = ref.query_representation(Q, K)
+    C = np.cov(K.T, bias=True)
+    assert np.abs((R * R).sum(axis=1) - 1).max() < 1e-12
+    G = Q @ C @ Q.T
+    nrm = np.sqrt(np.diag(G))
+    assert np.abs(R @ R.T - G / np.outer(nrm, nrm)).max() < 1e-11
+    Y = ref.query_split_space(Q, K, "metric")
+    assert np.abs(Y @ Y.T - R @ R.T).max() < 1e-11  # rotation only
+
+
+def test_zero_query_maps_to_zero():
+    Q, K = _mix(3)
+    Q[7] = 0.0
+    assert (ref.query_representation(Q, K)[7] == 0).all()
+
+
+def test_pairwise_difference_gram_is_2n_covariance():
+    """App. B.2: D^T D = 2n K_c^T K_c for D the matrix of all ordered key differences."""
+    rng = np.random.default_rng(4)
+    K = rng.standard_normal((30, 4)) + 1.5
+    n = len(K)
+    D = (K[:, None, :] - K[None, :, :]).reshape(n * n, -1)
+    assert np.abs(D.T @ D - 2 * n * n * ref.centred_cov(K)).max() < 1e-10
+
+
+@pytest.mark.parametrize("mode", ["pca", "metric"])
+def test_split_space_is_decorrelated_sorted_and_oriented(mode):
+    """Diagonalized splitting works on principal coordinates: the covariance of
+    Y is diagonal with non-increasing variances, and (orientation reading) every
+    coordinate has a non-negative mean."""
+    Q, K = _mix(5)
+    for Y in (ref.key_split_space(Q, K, mode), ref.query_split_space(Q, K, mode)):
+        C = np.cov(Y.T, bias=True)
+        off = C - np.diag(np.diag(C))
+        assert np.abs(off).max() < 1e-10 * np.abs(C).max()
+        assert (np.diff(np.diag(C)) <= 1e-12).all()
+        assert (Y.mean(axis=0) >= -1e-12).all()
+
+
+def test_query_space_is_invariant_to_key_shift():
+    """App. B.1/B.2: the centred key metric quotients out the softmax shift, so
+    shifting every key by one vector leaves the query split space unchanged."""
+    Q, K = _mix(6)
+    a = ref.query_split_space(Q, K, "metric")
+    b = ref.query_split_space(Q, K + np.array([3.0, -1, 2, 0.5, 0, 1]), "metric")
+    assert np.abs(a - b).max() < 1e-9
+
+
+def test_metric_key_space_independent_of_root_choice():
+    """Any factor S with S S^T = M gives the same split coordinates (up to the
+    orientation rule): compare E sqrt(L) with the symmetric root E sqrt(L) E^T."""
+    Q, K = _mix(7)
+    M = ref.second_moment(Q)
+    lam, E = np.linalg.eigh(M)
+    Rsym = E @ np.diag(np.sqrt(np.maximum(lam, 0))) @ E.T
+    Z = K @ Rsym
+    Ysym = Z @ ref.pca_basis(Z)
+    assert np.abs(Ysym - ref.key_split_space(Q, K, "metric")).max() < 1e-10
+
+
+def test_none_mode_is_identity():
+    Q, K = _mix(8)
+    assert np.array_equal(ref.key_split_space(Q, K, "none"), K)
+    assert np.array_equal(ref.query_split_space(Q, K, "none"), Q)
+
+
+def test_clamped_root_of_indefinite_matrix():
+    """Method, key clustering: negative eigenvalues are clamped to zero."""
+    rng = np.random.default_rng(10)
+    E, _ = np.linalg.qr(rng.standard_normal((3, 3)))
+    A = E @ np.diag([4.0, 1.0, -0.25]) @ E.T
+    S = ref.psd_root(A)
+    want = E @ np.diag([4.0, 1.0, 0.0]) @ E.T
+    assert np.abs(S @ S.T - want).max() < 1e-13
