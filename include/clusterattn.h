@@ -1,0 +1,212 @@
+/*
+ * clusterattn.h - C ABI of the ClusterAttention hot path on MI355X (gfx950).
+ *
+ * ClusterAttention replaces bidirectional softmax attention, per head, by four
+ * steps (paper: Method, Overview; Preliminaries, motivation for sparse
+ * attention):
+ *   1. ca_cluster            split queries and keys into clusters of a fixed
+ *                            power-of-two size (Method: Clustering), and form
+ *                            the permuted Q/K/V and the cluster centroids;
+ *   2. ca_select             score every query cluster against every key
+ *                            cluster by centroid dot products and keep the top-k
+ *                            key clusters (Method: Cluster assignment);
+ *   3. ca_block_sparse_attn  softmax attention of each query cluster onto the
+ *                            keys of its selected clusters, returning the output
+ *                            and the softmax denominator (Method: Overview);
+ *   4. ca_compensate         striped mean-compensation: every skipped key
+ *                            cluster enters through its centroid key and value
+ *                            weighted by its size, merged with step 3, and the
+ *                            rows restored to the original token order
+ *                            (Preliminaries: error in sparse attention; App. A).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - All data pointers are DEVICE pointers (hipMalloc'd or equivalent) on the
+ *   current HIP device. The caller owns every buffer; the library never
+ *   allocates, frees or synchronises. Work is enqueued on `stream` (a
+ *   hipStream_t; NULL = the default stream) and buffers must stay alive until
+ *   the stream has passed it.
+ * - Q/K/V and the final output use the problem's layout (ca_layout) with the
+ *   last dimension contiguous. Every other array is dense, row-major, with the
+ *   shape given in its comment; BH = batch * heads, heads vary fastest.
+ * - Derived sizes: nqc = ceil(nq/cq), nkc = ceil(nk/ck), nq_pad = nqc*cq,
+ *   nk_pad = nkc*ck. Clusters hold exactly cq (ck) tokens except the last one,
+ *   which holds the remainder; its missing rows are zero-filled padding that
+ *   never influences a result.
+ * - Every call validates its arguments before touching the GPU. On any status
+ *   other than CA_OK nothing has been enqueued. CA_E_DEVICE means a HIP launch
+ *   error after validation; ca_last_error() then gives the HIP error text.
+ *   No C++ exception crosses this interface.
+ * - Every output element is written (including padding rows). Outputs must not
+ *   alias inputs. Results are deterministic: two identical calls give
+ *   bit-identical outputs.
+ * - Non-finite inputs (NaN/Inf) are not checked: the calls stay memory-safe
+ *   but the results are unspecified.
+ * - Calls on different streams may run concurrently if their outputs and
+ *   workspaces do not overlap.
+ */
+#ifndef CLUSTERATTN_H_
+#define CLUSTERATTN_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CA_ABI_VERSION 1
+
+#if defined(__GNUC__) || defined(__clang__)
+#define CA_API __attribute__((visibility("default")))
+#else
+#define CA_API
+#endif
+
+typedef enum {
+  CA_OK = 0,
+  CA_E_INVALID = 1,     /* bad argument: null pointer, size out of range, c not a power of two, k not in [1, nkc] */
+  CA_E_UNSUPPORTED = 2, /* valid but not built: e.g. bf16 attention with d not in {64, 128} */
+  CA_E_WORKSPACE = 3,   /* workspace smaller than ca_workspace_size() */
+  CA_E_DEVICE = 4       /* HIP reported an error while enqueueing */
+} ca_status;
+
+typedef enum { CA_F32 = 0, CA_BF16 = 1 } ca_dtype;
+
+/* Space in which the recursive split is done (Method: Transforms).
+ *   CA_XF_NONE:   the raw coordinates.
+ *   CA_XF_PCA:    principal coordinates of the raw vectors (diagonalized
+ *                 splitting without the attention-aware metrics).
+ *   CA_XF_METRIC: keys in the query-induced metric Q^T Q / n, queries through
+ *                 r(q) = q S_k / |q S_k| with S_k S_k^T = the key covariance
+ *                 (top-k representation, App. B.2), each side then on its own
+ *                 principal coordinates. This is the evaluated method. */
+typedef enum { CA_XF_NONE = 0, CA_XF_PCA = 1, CA_XF_METRIC = 2 } ca_transform;
+
+/* Layout of Q, K, V and the final output: BHND = [B][H][N][d],
+ * BNHD = [B][N][H][d] (the usual activation layout of a transformer). */
+typedef enum { CA_LAYOUT_BHND = 0, CA_LAYOUT_BNHD = 1 } ca_layout;
+
+typedef struct {
+  int32_t batch, heads;  /* >= 1 */
+  int32_t nq, nk;        /* real query / key tokens per head, >= 1 */
+  int32_t d;             /* head dimension, 1..128 (attention: see below) */
+  int32_t cq, ck;        /* cluster sizes, powers of two in [1, 256] */
+  int32_t dtype;         /* ca_dtype of Q/K/V, permuted copies and output */
+  int32_t transform;     /* ca_transform (ca_cluster only) */
+  int32_t layout;        /* ca_layout of Q/K/V/out */
+} ca_problem;
+
+/* Outputs of ca_cluster. Required unless marked optional. */
+typedef struct {
+  int32_t* perm_q;   /* [BH][nq]  original query index at each cluster-ordered position */
+  int32_t* perm_k;   /* [BH][nk]  same for keys */
+  int32_t* cid_q;    /* [BH][nq]  cluster of original query i (optional, may be NULL) */
+  int32_t* cid_k;    /* [BH][nk]  cluster of original key i (optional, may be NULL) */
+  int32_t* count_q;  /* [BH][nqc] real members per query cluster */
+  int32_t* count_k;  /* [BH][nkc] real members per key cluster */
+  float* cent_q;     /* [BH][nqc][d] fp32 mean of the ORIGINAL query vectors of each cluster */
+  float* cent_k;     /* [BH][nkc][d] same for keys */
+  float* cent_v;     /* [BH][nkc][d] same for values (values follow the key clusters);
+                        optional: NULL (with v == NULL) skips values */
+  void* qp;          /* [BH][nq_pad][d] dtype: queries in cluster order, pad rows zero */
+  void* kp;          /* [BH][nk_pad][d] dtype: keys in cluster order, pad rows zero */
+  void* vp;          /* [BH][nkc][d][ck] dtype: value tiles. For every key cluster the ck value
+                        rows in cluster order, stored transposed (dimension-major, ck
+                        contiguous), pad columns zero. This is the operand layout of the
+                        value product in the attention calls. Optional: NULL with v. */
+  float* yq_dbg;     /* [BH][nq][d] optional: the query split coordinates (original order) */
+  float* yk_dbg;     /* [BH][nk][d] optional: the key split coordinates (original order) */
+} ca_cluster_out;
+
+/* ABI version compiled into the library (CA_ABI_VERSION). */
+CA_API int ca_abi_version(void);
+
+/* Static text for a status code. */
+CA_API const char* ca_status_str(int status);
+
+/* Detail of the last non-OK status returned on the calling thread ("" if none). */
+CA_API const char* ca_last_error(void);
+
+/* Bytes of workspace ca_cluster and ca_select need for this problem with k
+ * kept key clusters (k is only used for validation; the size does not depend
+ * on it). Host-only; enqueues nothing. Workspace must be 256-byte aligned. */
+CA_API int ca_workspace_size(const ca_problem* p, int32_t k, size_t* bytes);
+
+/* Step 1: clustering (Method: Clustering, Recursive splitting - diagonalized
+ * variant; Transforms).
+ *
+ * Per head, queries and keys are each mapped to their split space (transform)
+ * and recursively split: at a node of s > c tokens, a subsample of
+ * m = min(d, s) members at positions floor((2j+1)s/(2m)) of the node (in
+ * ascending original-index order) picks the coordinate of highest fp64
+ * population variance (two-pass, sequential, ties to the lower coordinate);
+ * the node's c*floor(ceil(s/c)/2) members with the smallest (coordinate value,
+ * original index) go left, the rest right, both keeping index order; leaves
+ * are numbered left to right. This is deterministic: given the split
+ * coordinates (exported through yq_dbg / yk_dbg) the permutation is exact.
+ *
+ * q, k: [B,H,nq|nk,d] in the problem layout and dtype. v: same shape as k, or
+ * NULL to skip the value outputs. ws: device workspace of ws_bytes >=
+ * ca_workspace_size(). */
+CA_API int ca_cluster(const ca_problem* p, const void* q, const void* k, const void* v,
+               const ca_cluster_out* out, void* ws, size_t ws_bytes, void* stream);
+
+/* Step 2: assignment (Method: Cluster assignment - scoring and top-k
+ * selection). scores[a][b] = cent_q[a] . cent_k[b] (fp32, the mean pairwise
+ * logit up to the 1/sqrt(d) factor); lists[a] = the k key clusters with the
+ * largest scores, ties to the lower index, in ascending order.
+ *
+ * cent_q: [BH][nqc][d], cent_k: [BH][nkc][d] fp32. scores_in: optional
+ * [BH][nqc][nkc] fp32 scores to rank instead of computing them (NULL:
+ * compute). scores_out: optional [BH][nqc][nkc] export of the ranked scores.
+ * lists: [BH][nqc][k] int32 output. 1 <= k <= nkc. */
+CA_API int ca_select(const ca_problem* p, const float* cent_q, const float* cent_k,
+              const float* scores_in, float* scores_out, int32_t k, int32_t* lists,
+              void* ws, size_t ws_bytes, void* stream);
+
+/* Step 3: block-sparse attention (Method: Overview - attention over the
+ * selected clusters, returning the softmax denominator).
+ *
+ * For query row p of cluster a (permuted order), over the real keys j of the
+ * clusters in lists[a]:  s_j = scale * qp[p] . kp[j],
+ *   op[p]  = sum_j e^{s_j - m} vp[j] / sum_j e^{s_j - m},
+ *   lse[p] = m + ln sum_j e^{s_j - m}   (natural log; m = max_j s_j).
+ * Key rows past count_k[b] in a cluster are padding and are excluded.
+ *
+ * qp: [BH][nq_pad][d], kp: [BH][nk_pad][d], vp: [BH][nkc][d][ck] value tiles
+ * as written by ca_cluster (all dtype), count_k: [BH][nkc],
+ * lists: [BH][nqc][k] with entries in [0, nkc) (not checked on the device;
+ * out-of-range entries are clamped), op: [BH][nq_pad][d] dtype, lse:
+ * [BH][nq_pad] fp32. scale <= 0 selects 1/sqrt(d). Padding query rows get
+ * defined values that callers ignore. bf16: d in {64, 128}, cq and ck in
+ * {64, 128}; fp32: d % 4 == 0, any cq, ck. */
+CA_API int ca_block_sparse_attn(const ca_problem* p, const void* qp, const void* kp, const void* vp,
+                         const int32_t* count_k, const int32_t* lists, int32_t k, float scale,
+                         void* op, float* lse, void* stream);
+
+/* Step 4: striped mean-compensation and un-permutation (Preliminaries: error
+ * in sparse attention; App. A).
+ *
+ * For query row p of cluster a: every key cluster b NOT in lists[a] adds the
+ * logit t_b = scale * qp[p] . cent_k[b] + ln count_k[b] with value cent_v[b];
+ *   lse_c = ln sum_b e^{t_b},  o_c = sum_b e^{t_b - lse_c} cent_v[b],
+ *   lse   = ln(e^{lse[p]} + e^{lse_c}),
+ *   out   = e^{lse[p] - lse} op[p] + e^{lse_c - lse} o_c,
+ * written to out[perm_q[p]] (original token order, problem layout). With
+ * enable == 0, or when every cluster is selected, out = op[p], lse = lse[p].
+ *
+ * qp, op: [BH][nq_pad][d] dtype; cent_k, cent_v: [BH][nkc][d] fp32; count_k:
+ * [BH][nkc]; lists: [BH][nqc][k]; lse: [BH][nq_pad] fp32; perm_q: [BH][nq];
+ * out: [B,H,nq,d] in the problem layout and dtype; lse_out: optional
+ * [BH][nq] fp32 in original order. */
+CA_API int ca_compensate(const ca_problem* p, const void* qp, const float* cent_k, const float* cent_v,
+                  const int32_t* count_k, const int32_t* lists, int32_t k, float scale,
+                  int32_t enable, const void* op, const float* lse, const int32_t* perm_q,
+                  void* out, float* lse_out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CLUSTERATTN_H_ */

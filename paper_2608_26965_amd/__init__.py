@@ -1,0 +1,202 @@
+"""ClusterAttention on MI355X: Python binding of libclusterattn (HIP, gfx950).
+
+Every step runs in the HIP library; this module only allocates tensors with
+torch and passes their device pointers and the current stream to the four
+C-ABI calls (see include/clusterattn.h):
+
+    cluster -> select -> block_sparse_attn -> compensate
+
+``forward`` chains them for one attention layer. There is no CPU fallback: if
+the library is not built, importing the calls raises.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+
+import torch
+
+from . import _lib
+from ._lib import (CA_BF16, CA_F32, CA_LAYOUT_BHND, CA_LAYOUT_BNHD, CA_XF_METRIC, CA_XF_NONE,
+                   CA_XF_PCA, CAError)
+
+__all__ = ["Problem", "workspace_size", "cluster", "select", "block_sparse_attn", "compensate",
+           "forward", "CAError", "abi_version"]
+
+_XF = {"none": CA_XF_NONE, "pca": CA_XF_PCA, "metric": CA_XF_METRIC}
+_LAYOUT = {"bhnd": CA_LAYOUT_BHND, "bnhd": CA_LAYOUT_BNHD}
+_DT = {torch.float32: CA_F32, torch.bfloat16: CA_BF16}
+
+
+def abi_version() -> int:
+    return _lib.load().ca_abi_version()
+
+
+@dataclass(frozen=True)
+class Problem:
+    batch: int
+    heads: int
+    nq: int
+    nk: int
+    d: int
+    cq: int
+    ck: int
+    dtype: torch.dtype = torch.bfloat16
+    transform: str = "metric"
+    layout: str = "bhnd"
+
+    @property
+    def bh(self):
+        return self.batch * self.heads
+
+    @property
+    def nqc(self):
+        return -(-self.nq // self.cq)
+
+    @property
+    def nkc(self):
+        return -(-self.nk // self.ck)
+
+    @property
+    def nq_pad(self):
+        return self.nqc * self.cq
+
+    @property
+    def nk_pad(self):
+        return self.nkc * self.ck
+
+    def c(self) -> _lib.CaProblem:
+        return _lib.CaProblem(self.batch, self.heads, self.nq, self.nk, self.d, self.cq, self.ck,
+                              _DT[self.dtype], _XF[self.transform], _LAYOUT[self.layout])
+
+    def shape(self, n):
+        if self.layout == "bhnd":
+            return (self.batch, self.heads, n, self.d)
+        return (self.batch, n, self.heads, self.d)
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(device):
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def workspace_size(p: Problem, k: int = 1) -> int:
+    n = __import__("ctypes").c_size_t(0)
+    _lib.check(_lib.load().ca_workspace_size(p.c(), k, n), "ca_workspace_size")
+    return n.value
+
+
+def workspace(p: Problem, device, k: int = 1) -> torch.Tensor:
+    return torch.empty(max(workspace_size(p, k), 256), dtype=torch.uint8, device=device)
+
+
+def cluster(p: Problem, q, k, v=None, *, export_y=False, ws=None):
+    """Step 1. Returns a dict of device tensors: perm_q/perm_k [BH,n],
+    cid_q/cid_k [BH,n], count_q/count_k [BH,nc], cent_q/cent_k/cent_v [BH,nc,d],
+    qp/kp [BH,n_pad,d], vp [BH,nkc,d,ck] (value tiles), and yq/yk [BH,n,d] if
+    export_y."""
+    dev = q.device
+    i32 = dict(dtype=torch.int32, device=dev)
+    f32 = dict(dtype=torch.float32, device=dev)
+    BH, d = p.bh, p.d
+    r = dict(
+        perm_q=torch.empty(BH, p.nq, **i32), perm_k=torch.empty(BH, p.nk, **i32),
+        cid_q=torch.empty(BH, p.nq, **i32), cid_k=torch.empty(BH, p.nk, **i32),
+        count_q=torch.empty(BH, p.nqc, **i32), count_k=torch.empty(BH, p.nkc, **i32),
+        cent_q=torch.empty(BH, p.nqc, d, **f32), cent_k=torch.empty(BH, p.nkc, d, **f32),
+        qp=torch.empty(BH, p.nq_pad, d, dtype=p.dtype, device=dev),
+        kp=torch.empty(BH, p.nk_pad, d, dtype=p.dtype, device=dev),
+    )
+    if v is not None:
+        r["cent_v"] = torch.empty(BH, p.nkc, d, **f32)
+        r["vp"] = torch.empty(BH, p.nkc, d, p.ck, dtype=p.dtype, device=dev)
+    if export_y:
+        r["yq"] = torch.empty(BH, p.nq, d, **f32)
+        r["yk"] = torch.empty(BH, p.nk, d, **f32)
+    out = _lib.CaClusterOut(*(_ptr(r.get(n)) for n in (
+        "perm_q", "perm_k", "cid_q", "cid_k", "count_q", "count_k", "cent_q", "cent_k", "cent_v",
+        "qp", "kp", "vp", "yq", "yk")))
+    if ws is None:
+        ws = workspace(p, dev)
+    st = _lib.load().ca_cluster(p.c(), _ptr(q), _ptr(k), _ptr(v), out, _ptr(ws), ws.numel(),
+                                _stream(dev))
+    _lib.check(st, "ca_cluster")
+    return r
+
+
+def select(p: Problem, cent_q, cent_k, keep_k: int, *, scores_in=None, export_scores=False,
+           ws=None):
+    """Step 2. Returns (lists [BH,nqc,k] int32 ascending, scores or None)."""
+    dev = (cent_q if cent_q is not None else scores_in).device
+    lists = torch.empty(p.bh, p.nqc, keep_k, dtype=torch.int32, device=dev)
+    scores = None
+    if export_scores:
+        scores = torch.empty(p.bh, p.nqc, p.nkc, dtype=torch.float32, device=dev)
+    if ws is None and scores_in is None and scores is None:
+        ws = workspace(p, dev, keep_k)
+    st = _lib.load().ca_select(p.c(), _ptr(cent_q), _ptr(cent_k), _ptr(scores_in), _ptr(scores),
+                               keep_k, _ptr(lists), _ptr(ws), 0 if ws is None else ws.numel(),
+                               _stream(dev))
+    _lib.check(st, "ca_select")
+    return lists, scores
+
+
+def block_sparse_attn(p: Problem, qp, kp, vp, count_k, lists, keep_k: int, scale: float = 0.0):
+    """Step 3. Returns (op [BH,nq_pad,d] dtype, lse [BH,nq_pad] fp32)."""
+    dev = qp.device
+    op = torch.empty(p.bh, p.nq_pad, p.d, dtype=p.dtype, device=dev)
+    lse = torch.empty(p.bh, p.nq_pad, dtype=torch.float32, device=dev)
+    st = _lib.load().ca_block_sparse_attn(p.c(), _ptr(qp), _ptr(kp), _ptr(vp), _ptr(count_k),
+                                          _ptr(lists), keep_k, float(scale), _ptr(op), _ptr(lse),
+                                          _stream(dev))
+    _lib.check(st, "ca_block_sparse_attn")
+    return op, lse
+
+
+def compensate(p: Problem, qp, cent_k, cent_v, count_k, lists, keep_k: int, op, lse, perm_q,
+               scale: float = 0.0, enable: bool = True, want_lse: bool = False, out=None):
+    """Step 4. Returns (out in the problem layout, lse [BH,nq] or None)."""
+    dev = op.device
+    if out is None:
+        out = torch.empty(p.shape(p.nq), dtype=p.dtype, device=dev)
+    lse_out = torch.empty(p.bh, p.nq, dtype=torch.float32, device=dev) if want_lse else None
+    st = _lib.load().ca_compensate(p.c(), _ptr(qp), _ptr(cent_k), _ptr(cent_v), _ptr(count_k),
+                                   _ptr(lists), keep_k, float(scale), int(bool(enable)), _ptr(op),
+                                   _ptr(lse), _ptr(perm_q), _ptr(out), _ptr(lse_out),
+                                   _stream(dev))
+    _lib.check(st, "ca_compensate")
+    return out, lse_out
+
+
+def keep_to_k(keep: float, n_kc: int) -> int:
+    """Kept key clusters for a keep fraction: ceil(keep * n_kc), in [1, n_kc]."""
+    return max(1, min(n_kc, int(math.ceil(keep * n_kc - 1e-9))))
+
+
+def forward(q, k, v, cq=128, ck=None, keep=None, keep_k=None, transform="metric",
+            compensation=True, scale=None, layout="bhnd", return_parts=False):
+    """ClusterAttention for one layer. q, k, v: [B,H,N,d] ("bhnd") or [B,N,H,d]
+    ("bnhd"), bf16 or fp32, on one GPU. Keep either a fraction (``keep``) or a
+    count (``keep_k``) of key clusters per query cluster."""
+    ck = cq if ck is None else ck
+    if layout == "bhnd":
+        B, H, nq, d = q.shape
+        nk = k.shape[2]
+    else:
+        B, nq, H, d = q.shape
+        nk = k.shape[1]
+    p = Problem(B, H, nq, nk, d, cq, ck, q.dtype, transform, layout)
+    if keep_k is None:
+        keep_k = keep_to_k(1.0 / 8 if keep is None else keep, p.nkc)
+    sc = 0.0 if scale is None else float(scale)
+    c = cluster(p, q, k, v)
+    lists, _ = select(p, c["cent_q"], c["cent_k"], keep_k)
+    op, lse = block_sparse_attn(p, c["qp"], c["kp"], c["vp"], c["count_k"], lists, keep_k, sc)
+    out, lse_out = compensate(p, c["qp"], c["cent_k"], c["cent_v"], c["count_k"], lists, keep_k,
+                              op, lse, c["perm_q"], sc, compensation, want_lse=return_parts)
+    if return_parts:
+        return out, dict(c, lists=lists, op=op, lse_s=lse, lse=lse_out, problem=p)
+    return out

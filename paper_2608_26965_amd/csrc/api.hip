@@ -1,0 +1,244 @@
+// C ABI of libclusterattn: argument validation, workspace planning and dispatch.
+// Every entry point validates completely before the first HIP call, so a
+// non-OK status means nothing was enqueued.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "common.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+int ok() {
+  g_err[0] = '\0';
+  return CA_OK;
+}
+
+int device_status(hipError_t e, const char* where) {
+  if (e == hipSuccess) return ok();
+  return fail(CA_E_DEVICE, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool pow2(int x) { return x >= 1 && (x & (x - 1)) == 0; }
+
+// Validates the problem descriptor and fills the derived sizes.
+int check_problem(const ca_problem* p, ca::Prob* P) {
+  if (!p) return fail(CA_E_INVALID, "problem is NULL");
+  if (p->batch < 1 || p->heads < 1) return fail(CA_E_INVALID, "batch and heads must be >= 1");
+  if (p->nq < 1 || p->nk < 1) return fail(CA_E_INVALID, "nq and nk must be >= 1");
+  if ((int64_t)p->batch * p->heads > (1 << 20)) return fail(CA_E_INVALID, "batch*heads too large");
+  if (p->nq > (1 << 26) || p->nk > (1 << 26)) return fail(CA_E_INVALID, "nq/nk above 2^26");
+  if (p->d < 1 || p->d > ca::kMaxD) return fail(CA_E_INVALID, "d must be in [1, %d]", ca::kMaxD);
+  if (!pow2(p->cq) || !pow2(p->ck) || p->cq > ca::kMaxC || p->ck > ca::kMaxC)
+    return fail(CA_E_INVALID, "cluster sizes must be powers of two in [1, %d]", ca::kMaxC);
+  if (p->dtype != CA_F32 && p->dtype != CA_BF16) return fail(CA_E_INVALID, "unknown dtype");
+  if (p->transform < CA_XF_NONE || p->transform > CA_XF_METRIC)
+    return fail(CA_E_INVALID, "unknown transform");
+  if (p->layout != CA_LAYOUT_BHND && p->layout != CA_LAYOUT_BNHD)
+    return fail(CA_E_INVALID, "unknown layout");
+  P->B = p->batch;
+  P->H = p->heads;
+  P->BH = p->batch * p->heads;
+  P->nq = p->nq;
+  P->nk = p->nk;
+  P->d = p->d;
+  P->cq = p->cq;
+  P->ck = p->ck;
+  P->dtype = p->dtype;
+  P->xf = p->transform;
+  P->layout = p->layout;
+  P->nqc = (p->nq + p->cq - 1) / p->cq;
+  P->nkc = (p->nk + p->ck - 1) / p->ck;
+  P->nq_pad = P->nqc * p->cq;
+  P->nk_pad = P->nkc * p->ck;
+  P->esize = p->dtype == CA_BF16 ? 2 : 4;
+  return CA_OK;
+}
+
+int check_k(const ca::Prob& P, int32_t k) {
+  if (k < 1 || k > P.nkc) return fail(CA_E_INVALID, "k=%d not in [1, nkc=%d]", k, P.nkc);
+  return CA_OK;
+}
+
+int check_ws(const ca::Workspace& W, const void* ws, size_t ws_bytes) {
+  if (ws_bytes < W.total)
+    return fail(CA_E_WORKSPACE, "workspace of %zu bytes, need %zu", ws_bytes, W.total);
+  if (W.total > 0 && !ws) return fail(CA_E_INVALID, "workspace is NULL");
+  if (((uintptr_t)ws & 255u) != 0) return fail(CA_E_INVALID, "workspace must be 256-byte aligned");
+  return CA_OK;
+}
+
+int check_attn_shape(const ca::Prob& P) {
+  if (P.dtype == CA_BF16) {
+    if (P.d != 64 && P.d != 128)
+      return fail(CA_E_UNSUPPORTED, "bf16 attention needs d in {64, 128}, got %d", P.d);
+    if ((P.cq != 64 && P.cq != 128) || (P.ck != 64 && P.ck != 128))
+      return fail(CA_E_UNSUPPORTED, "bf16 attention needs cq, ck in {64, 128}");
+  } else if (P.d % 4 != 0) {
+    return fail(CA_E_UNSUPPORTED, "fp32 attention needs d %% 4 == 0, got %d", P.d);
+  }
+  return CA_OK;
+}
+
+}  // namespace
+
+namespace ca {
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+void plan_workspace(const Prob& P, Workspace* W) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off += align256(bytes);
+    return o;
+  };
+  const size_t BH = P.BH, d = P.d;
+  const int nmax = P.nq > P.nk ? P.nq : P.nk;
+  W->nblk_mom = (nmax + kMomRows - 1) / kMomRows;
+  W->levels_q = num_levels(P.nq, P.cq);
+  W->levels_k = num_levels(P.nk, P.ck);
+  W->big_q = split_big_levels(P.nq, P.cq, W->levels_q);
+  W->big_k = split_big_levels(P.nk, P.ck, W->levels_k);
+  int bigmax = W->big_q > W->big_k ? W->big_q : W->big_k;
+  W->max_big_nodes = bigmax > 0 ? (1 << (bigmax - 1)) : 1;
+  W->max_chunks = (nmax + kChunk - 1) / kChunk;
+
+  W->y_q = take(BH * P.nq * d * 4);
+  W->y_k = take(BH * P.nk * d * 4);
+  W->idx0 = take(2 * BH * nmax * 4);
+  W->idx1 = take(2 * BH * nmax * 4);
+  W->keys = take(2 * BH * nmax * 4);
+  W->mom_part = take(2 * BH * W->nblk_mom * (d * d + d) * 4);
+  W->mats = take(BH * kMats * d * d * 4);
+  W->vecs = take(BH * kVecs * d * 4);
+  W->inv_q = take(BH * P.nq * 4);
+  W->qn_part = take(BH * W->nblk_mom * (d * d + d) * 4);
+  W->node_state = take(2 * BH * W->max_big_nodes * kNodeInts * 4);
+  W->hist = take(2 * BH * W->max_big_nodes * kRadixBins * 4);
+  W->chunk_cnt = take(2 * BH * W->max_big_nodes * W->max_chunks * 2 * 4);
+  W->scores = take(BH * P.nqc * P.nkc * 4);
+  W->total = off;
+}
+
+}  // namespace ca
+
+extern "C" {
+
+int ca_abi_version(void) { return CA_ABI_VERSION; }
+
+const char* ca_status_str(int status) {
+  switch (status) {
+    case CA_OK: return "CA_OK";
+    case CA_E_INVALID: return "CA_E_INVALID: invalid argument";
+    case CA_E_UNSUPPORTED: return "CA_E_UNSUPPORTED: combination not built";
+    case CA_E_WORKSPACE: return "CA_E_WORKSPACE: workspace too small";
+    case CA_E_DEVICE: return "CA_E_DEVICE: HIP error";
+    default: return "unknown status";
+  }
+}
+
+const char* ca_last_error(void) { return g_err; }
+
+int ca_workspace_size(const ca_problem* p, int32_t k, size_t* bytes) {
+  ca::Prob P;
+  int s = check_problem(p, &P);
+  if (s) return s;
+  if ((s = check_k(P, k))) return s;
+  if (!bytes) return fail(CA_E_INVALID, "bytes is NULL");
+  ca::Workspace W;
+  ca::plan_workspace(P, &W);
+  *bytes = W.total;
+  return ok();
+}
+
+int ca_cluster(const ca_problem* p, const void* q, const void* k, const void* v,
+               const ca_cluster_out* out, void* ws, size_t ws_bytes, void* stream) {
+  ca::Prob P;
+  int s = check_problem(p, &P);
+  if (s) return s;
+  if (!q || !k) return fail(CA_E_INVALID, "q and k are required");
+  if (!out) return fail(CA_E_INVALID, "out is NULL");
+  if (!out->perm_q || !out->perm_k || !out->count_q || !out->count_k || !out->cent_q ||
+      !out->cent_k || !out->qp || !out->kp)
+    return fail(CA_E_INVALID, "a required output of ca_cluster is NULL");
+  bool want_v = v != nullptr;
+  if (want_v && (!out->cent_v || !out->vp))
+    return fail(CA_E_INVALID, "v given but cent_v or vp is NULL");
+  ca::Workspace W;
+  ca::plan_workspace(P, &W);
+  if ((s = check_ws(W, ws, ws_bytes))) return s;
+  return device_status(
+      ca::launch_cluster(P, q, k, v, out, (char*)ws, W, (hipStream_t)stream), "ca_cluster");
+}
+
+int ca_select(const ca_problem* p, const float* cent_q, const float* cent_k,
+              const float* scores_in, float* scores_out, int32_t k, int32_t* lists, void* ws,
+              size_t ws_bytes, void* stream) {
+  ca::Prob P;
+  int s = check_problem(p, &P);
+  if (s) return s;
+  if ((s = check_k(P, k))) return s;
+  if (!lists) return fail(CA_E_INVALID, "lists is NULL");
+  if (!scores_in && (!cent_q || !cent_k))
+    return fail(CA_E_INVALID, "cent_q and cent_k are required when scores_in is NULL");
+  float* scores = scores_out;
+  if (!scores_in && !scores) {
+    ca::Workspace W;
+    ca::plan_workspace(P, &W);
+    if ((s = check_ws(W, ws, ws_bytes))) return s;
+    scores = (float*)((char*)ws + W.scores);
+  }
+  return device_status(ca::launch_select(P, cent_q, cent_k, scores_in, scores, k, lists,
+                                         (hipStream_t)stream),
+                       "ca_select");
+}
+
+int ca_block_sparse_attn(const ca_problem* p, const void* qp, const void* kp, const void* vp,
+                         const int32_t* count_k, const int32_t* lists, int32_t k, float scale,
+                         void* op, float* lse, void* stream) {
+  ca::Prob P;
+  int s = check_problem(p, &P);
+  if (s) return s;
+  if ((s = check_k(P, k))) return s;
+  if (!qp || !kp || !vp || !count_k || !lists || !op || !lse)
+    return fail(CA_E_INVALID, "a required pointer of ca_block_sparse_attn is NULL");
+  if ((s = check_attn_shape(P))) return s;
+  if (!(scale > 0.0f)) scale = 1.0f / sqrtf((float)P.d);
+  return device_status(
+      ca::launch_attn(P, qp, kp, vp, count_k, lists, k, scale, op, lse, (hipStream_t)stream),
+      "ca_block_sparse_attn");
+}
+
+int ca_compensate(const ca_problem* p, const void* qp, const float* cent_k, const float* cent_v,
+                  const int32_t* count_k, const int32_t* lists, int32_t k, float scale,
+                  int32_t enable, const void* op, const float* lse, const int32_t* perm_q,
+                  void* out, float* lse_out, void* stream) {
+  ca::Prob P;
+  int s = check_problem(p, &P);
+  if (s) return s;
+  if ((s = check_k(P, k))) return s;
+  if (!op || !lse || !perm_q || !out)
+    return fail(CA_E_INVALID, "a required pointer of ca_compensate is NULL");
+  if (enable && (!qp || !cent_k || !cent_v || !count_k || !lists))
+    return fail(CA_E_INVALID, "compensation needs qp, cent_k, cent_v, count_k and lists");
+  if ((s = check_attn_shape(P))) return s;
+  if (!(scale > 0.0f)) scale = 1.0f / sqrtf((float)P.d);
+  return device_status(ca::launch_comp(P, qp, cent_k, cent_v, count_k, lists, k, scale, enable,
+                                       op, lse, perm_q, out, lse_out, (hipStream_t)stream),
+                       "ca_compensate");
+}
+
+}  // extern "C"

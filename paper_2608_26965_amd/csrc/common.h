@@ -1,0 +1,148 @@
+// Internal declarations shared by the HIP translation units of libclusterattn.
+// Not part of the public ABI (see include/clusterattn.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/clusterattn.h"
+
+namespace ca {
+
+typedef __bf16 bf16;
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+
+constexpr int kMaxD = 128;
+constexpr int kMaxC = 256;
+
+// ---- scalar conversions -------------------------------------------------
+
+__device__ __forceinline__ float bf2f(bf16 x) {
+  return __uint_as_float(((uint32_t)__builtin_bit_cast(uint16_t, x)) << 16);
+}
+// Round to nearest even (finite inputs).
+__device__ __forceinline__ bf16 f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return __builtin_bit_cast(bf16, (uint16_t)(u >> 16));
+}
+__device__ __forceinline__ float load_elem(const void* base, size_t idx, int dtype) {
+  return dtype == CA_BF16 ? bf2f(((const bf16*)base)[idx]) : ((const float*)base)[idx];
+}
+__device__ __forceinline__ void store_elem(void* base, size_t idx, int dtype, float v) {
+  if (dtype == CA_BF16)
+    ((bf16*)base)[idx] = f2bf(v);
+  else
+    ((float*)base)[idx] = v;
+}
+
+// Order-preserving map of a float to uint32 (ascending float -> ascending
+// unsigned); -0.0 is first turned into +0.0 so that the two compare equal.
+__device__ __forceinline__ uint32_t ordered_bits(float f) {
+  uint32_t u = __float_as_uint(f + 0.0f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// ---- problem description ---------------------------------------------------
+
+struct Prob {
+  int B, H, BH, nq, nk, d, cq, ck, dtype, xf, layout;
+  int nqc, nkc, nq_pad, nk_pad;
+  size_t esize;
+};
+
+// Element offset of (bh, token i, dim 0) in a [B,H,N,d] tensor of the given layout.
+__host__ __device__ __forceinline__ size_t row_off(int bh, int i, int N, int H, int d, int layout) {
+  if (layout == CA_LAYOUT_BHND) return ((size_t)bh * N + i) * d;
+  int b = bh / H, h = bh - b * H;
+  return (((size_t)b * N + i) * H + h) * d;
+}
+
+// ---- the split tree -----------------------------------------------------------
+// Node sizes depend only on (n, c): a node of s > c tokens sends
+// c*floor(ceil(s/c)/2) tokens left and the rest right. A node of s <= c is a
+// leaf and is carried down a level as (left = itself, right = empty), so level
+// l has 2^l slots. Every node starts at a multiple of c.
+
+__host__ __device__ __forceinline__ int left_size(int s, int c) {
+  return c * (((s + c - 1) / c) / 2);
+}
+// Range [start, start+size) of slot `node` at level `lvl` of a tree over n tokens.
+__host__ __device__ __forceinline__ void node_range(int n, int c, int lvl, int node, int* start,
+                                                     int* size) {
+  int st = 0, s = n;
+  for (int b = lvl - 1; b >= 0; --b) {
+    int bit = (node >> b) & 1;
+    int mL = s > c ? left_size(s, c) : s;
+    if (bit) {
+      st += mL;
+      s -= mL;
+    } else {
+      s = mL;
+    }
+  }
+  *start = st;
+  *size = s;
+}
+inline int num_levels(int n, int c) {
+  int nc = (n + c - 1) / c, L = 0;
+  while ((1 << L) < nc) ++L;
+  return L;
+}
+
+// ---- workspace layout ---------------------------------------------------------
+
+struct Workspace {
+  // clustering
+  size_t y_q, y_k;          // fp32 [BH][n][d] split coordinates (unless exported)
+  size_t idx0, idx1, keys;  // int32 / uint32 [2][BH][nmax]
+  size_t mom_part;          // fp32 [2][BH][nblk][d*d + d]
+  size_t mats;              // fp32 [BH][kMats][d][d]
+  size_t vecs;              // fp32 [BH][kVecs][d]
+  size_t inv_q;             // fp32 [BH][nq]
+  size_t qn_part;           // fp32 [BH][nblk_q][d*d + d]
+  size_t node_state;        // int32 [2][BH][max_big_nodes][kNodeInts]
+  size_t hist;              // uint32 [2][BH][max_big_nodes][kRadixBins]
+  size_t chunk_cnt;         // int32 [2][BH][max_big_nodes][max_chunks][2]
+  // selection
+  size_t scores;            // fp32 [BH][nqc][nkc]
+  size_t total;
+  // derived split parameters
+  int nblk_mom;             // row blocks per tensor for moment partials
+  int levels_q, levels_k;   // split levels per side
+  int big_q, big_k;         // levels done by the multi-block kernels
+  int max_big_nodes, max_chunks;
+};
+
+constexpr int kMats = 8;
+constexpr int kVecs = 8;
+constexpr int kNodeInts = 8;
+constexpr int kRadixBins = 2048;
+constexpr int kChunk = 4096;      // tokens per block in the multi-block split passes
+constexpr int kTail = 4096;       // nodes of at most this size finish in one workgroup
+constexpr int kMomRows = 2048;    // rows per moment-partial block
+
+void plan_workspace(const Prob& P, Workspace* W);
+// Number of split levels done by the multi-block kernels (nodes above the tail size).
+int split_big_levels(int n, int c, int levels);
+
+// ---- launchers (return hipError_t of the last launch) ----------------------
+
+hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const void* v,
+                          const ca_cluster_out* out, char* ws, const Workspace& W,
+                          hipStream_t st);
+hipError_t launch_select(const Prob& P, const float* cq, const float* ck, const float* scores_in,
+                         float* scores, int k, int32_t* lists, hipStream_t st);
+hipError_t launch_attn(const Prob& P, const void* qp, const void* kp, const void* vp,
+                       const int32_t* count_k, const int32_t* lists, int k, float scale, void* op,
+                       float* lse, hipStream_t st);
+hipError_t launch_comp(const Prob& P, const void* qp, const float* cent_k, const float* cent_v,
+                       const int32_t* count_k, const int32_t* lists, int k, float scale,
+                       int enable, const void* op, const float* lse, const int32_t* perm_q,
+                       void* out, float* lse_out, hipStream_t st);
+
+}  // namespace ca

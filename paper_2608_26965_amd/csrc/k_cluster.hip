@@ -1,0 +1,1336 @@
+// Clustering (paper: Method, Clustering): split spaces (Transforms), the
+// diagonalized recursive split, and the permuted copies plus centroids.
+//
+// Pipeline per head, both sides batched in every launch:
+//   moments      X^T X and column sums (fp32 partials, fp64 reduction)
+//   eigh         cyclic Jacobi on d x d matrices, one workgroup per matrix
+//   transforms   metric roots, the key-side covariance in the query metric,
+//                the normalised query representation and its covariance
+//   project      Y = X T (queries additionally scaled by 1/|q S_k|)
+//   split        levels with nodes larger than the tail size: multi-block
+//                radix select (11/11/10-bit digits) + stable partition;
+//                remaining levels: one workgroup per node, in LDS
+//   gather       permuted Q/K/V, centroids of the original vectors, counts
+//
+// The split is exact integer work on order-preserving images of the fp32
+// coordinates; the only floating-point decision, the highest-variance
+// coordinate of a node's subsample, is taken in fp64 with a fixed operation
+// order and no contraction, so it is reproducible bit for bit.
+#include <math.h>
+
+#include "common.h"
+
+namespace ca {
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// Parameters of the two sides (0 = queries, 1 = keys)
+// ---------------------------------------------------------------------------
+
+struct Side {
+  const void* x;    // input tensor, problem layout
+  float* y;         // split coordinates [BH][n][d]
+  int32_t* perm;    // [BH][n]
+  int32_t* cid;     // [BH][n] (may be null)
+  int32_t* count;   // [BH][nc]
+  float* cent;      // [BH][nc][d]
+  void* xp;         // permuted copy [BH][npad][d]
+  int n, c, nc, npad, levels, big, tail;
+};
+
+struct Ctx {
+  Side s[2];
+  const void* v;    // values (may be null)
+  float* cent_v;
+  void* vp;         // value tiles [BH][nkc][d][ck]
+  int BH, H, d, dtype, layout, xf, nmax, nblk;
+  float* mats;      // [BH][kMats][d][d]
+  float* vecs;      // [BH][kVecs][d]
+  float* inv_q;     // [BH][nq]
+  float* mom_part;  // [2][BH][nblk][d*d + d]
+  float* qn_part;   // [BH][nblk][d*d + d]
+  int32_t* idx0;
+  int32_t* idx1;
+  uint32_t* keys;
+  int32_t* node_state;
+  uint32_t* hist;
+  int32_t* chunk_cnt;
+  int max_nodes, max_chunks;
+};
+
+// Matrix slots
+enum { M_A0 = 0, M_CK = 1, M_E0 = 2, M_EK = 3, M_C2 = 4, M_C3 = 5, M_TK = 6, M_TQ = 7 };
+// Vector slots
+enum { V_L0 = 0, V_LK = 1, V_MUQ = 2, V_MUK = 3, V_L2 = 4, V_L3 = 5, V_MUR = 6, V_KQ = 7 };
+
+__device__ __forceinline__ float* mat(const Ctx& C, int bh, int slot) {
+  return C.mats + ((size_t)bh * kMats + slot) * C.d * C.d;
+}
+__device__ __forceinline__ float* vec(const Ctx& C, int bh, int slot) {
+  return C.vecs + ((size_t)bh * kVecs + slot) * C.d;
+}
+
+__device__ __forceinline__ float load_x(const void* x, int bh, int i, int n, int H, int d, int t,
+                                        int dtype, int layout) {
+  return load_elem(x, row_off(bh, i, n, H, d, layout) + t, dtype);
+}
+
+// ---------------------------------------------------------------------------
+// Second moments: part[pid][blk] = (sum_rows x x^T, sum_rows x) over a row block
+// ---------------------------------------------------------------------------
+
+constexpr int kStage = 32;  // rows staged in LDS at a time
+constexpr int kDP = kMaxD + 4;
+
+// Accumulates sum_r a_r b_r^T for the rows staged in A/B into per-thread 4x4
+// blocks (up to 4 blocks per thread: d <= 128).
+__device__ __forceinline__ void acc_outer(float (*A)[kDP], float (*B)[kDP], int rows, int d4,
+                                          float acc[4][16]) {
+  const int nb = d4 * d4;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int blk = threadIdx.x + 256 * q;
+    if (blk >= nb) break;
+    const int bi = blk / d4, bj = blk % d4;
+    for (int r = 0; r < rows; ++r) {
+      const float4 a = *(const float4*)&A[r][4 * bi];
+      const float4 b = *(const float4*)&B[r][4 * bj];
+      const float av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[q][4 * i + j] = __builtin_fmaf(av[i], bv[j], acc[q][4 * i + j]);
+    }
+  }
+}
+
+__device__ __forceinline__ void write_outer(float* out, int d, int d4, float acc[4][16]) {
+  const int nb = d4 * d4;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int blk = threadIdx.x + 256 * q;
+    if (blk >= nb) break;
+    const int bi = blk / d4, bj = blk % d4;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = 4 * bi + i, c = 4 * bj + j;
+        if (r < d && c < d) out[r * d + c] = acc[q][4 * i + j];
+      }
+  }
+}
+
+__global__ __launch_bounds__(256) void moments_partial_kernel(Ctx C) {
+  __shared__ __attribute__((aligned(16))) float X[kStage][kDP];
+  const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH, blk = blockIdx.x;
+  const Side& S = C.s[side];
+  const int d = C.d, d4 = (d + 3) / 4;
+  const int r0 = blk * kMomRows, r1 = min(S.n, r0 + kMomRows);
+  float acc[4][16];
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[q][e] = 0.f;
+  float csum = 0.f;
+  for (int rs = r0; rs < r1; rs += kStage) {
+    const int rows = min(kStage, r1 - rs);
+    __syncthreads();
+    for (int e = threadIdx.x; e < kStage * 4 * d4; e += 256) {
+      const int r = e / (4 * d4), t = e % (4 * d4);
+      X[r][t] = (r < rows && t < d)
+                    ? load_x(S.x, bh, rs + r, S.n, C.H, d, t, C.dtype, C.layout)
+                    : 0.f;
+    }
+    __syncthreads();
+    acc_outer(X, X, rows, d4, acc);
+    if (threadIdx.x < d)
+      for (int r = 0; r < rows; ++r) csum += X[r][threadIdx.x];
+  }
+  float* out = C.mom_part + ((size_t)pid * C.nblk + blk) * (d * d + d);
+  write_outer(out, d, d4, acc);
+  if (threadIdx.x < d) out[d * d + threadIdx.x] = csum;
+}
+
+// Reduces the partials of both sides of one head in fp64 and writes the
+// matrices the eigensolver starts from:
+//   queries: metric -> Q^T Q / n;  pca -> centred covariance of Q
+//   keys:    centred covariance of K (both modes)
+__global__ __launch_bounds__(256) void moments_finish_kernel(Ctx C) {
+  __shared__ double mu[kMaxD];
+  const int bh = blockIdx.x, d = C.d;
+  for (int side = 0; side < 2; ++side) {
+    const int pid = side * C.BH + bh;
+    const Side& S = C.s[side];
+    const float* part = C.mom_part + (size_t)pid * C.nblk * (d * d + d);
+    const double n = (double)S.n;
+    __syncthreads();
+    for (int t = threadIdx.x; t < d; t += 256) {
+      double s = 0.0;
+      for (int b = 0; b < C.nblk; ++b) s += (double)part[(size_t)b * (d * d + d) + d * d + t];
+      mu[t] = s / n;
+      vec(C, bh, side == 0 ? V_MUQ : V_MUK)[t] = (float)(s / n);
+    }
+    __syncthreads();
+    const bool centred = side == 1 || C.xf == CA_XF_PCA;
+    float* M = mat(C, bh, side == 0 ? M_A0 : M_CK);
+    for (int e = threadIdx.x; e < d * d; e += 256) {
+      double s = 0.0;
+      for (int b = 0; b < C.nblk; ++b) s += (double)part[(size_t)b * (d * d + d) + e];
+      double v = s / n;
+      if (centred) v -= mu[e / d] * mu[e % d];
+      M[e] = (float)v;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Symmetric eigensolver: parallel cyclic Jacobi, one workgroup per matrix.
+// Rotations use the round-robin ordering, d/2 disjoint pairs per step, each
+// step applied as 2x2 blocks of J^T A J (Golub & Van Loan, parallel Jacobi).
+// Output: eigenvalues in descending order and the matching eigenvectors as
+// columns.
+// ---------------------------------------------------------------------------
+
+struct EighJobs {
+  int n;
+  int in[2], vecs[2], vals[2];
+};
+
+constexpr int kEP = kMaxD + 1;
+
+__global__ __launch_bounds__(256) void eigh_kernel(Ctx C, EighJobs J) {
+  extern __shared__ float esh[];
+  float* A = esh;                       // [d][kEP]
+  float* V = esh + kMaxD * kEP;         // [d][kEP]
+  __shared__ float rc[kMaxD / 2 + 1], rs[kMaxD / 2 + 1];
+  __shared__ int rp[kMaxD / 2 + 1], rq[kMaxD / 2 + 1];
+  __shared__ float red[256];
+  __shared__ int sh_stop;
+  const int bh = blockIdx.x, job = blockIdx.y, d = C.d, tid = threadIdx.x;
+  const float* Min = mat(C, bh, J.in[job]);
+  for (int e = tid; e < d * d; e += 256) {
+    const int i = e / d, j = e % d;
+    A[i * kEP + j] = Min[e];
+    V[i * kEP + j] = i == j ? 1.f : 0.f;
+  }
+  if (tid == 0) sh_stop = 0;
+  const int m = (d + 1) & ~1;  // players (a phantom one when d is odd)
+  const int np = m / 2;
+  for (int sweep = 0; sweep < 30; ++sweep) {
+    __syncthreads();
+    // convergence: off-diagonal mass relative to the total
+    float off = 0.f, tot = 0.f;
+    for (int e = tid; e < d * d; e += 256) {
+      const int i = e / d, j = e % d;
+      const float a = A[i * kEP + j];
+      tot += a * a;
+      if (i != j) off += a * a;
+    }
+    red[tid] = off;
+    __syncthreads();
+    for (int s = 128; s > 0; s >>= 1) {
+      if (tid < s) red[tid] += red[tid + s];
+      __syncthreads();
+    }
+    const float offs = red[0];
+    __syncthreads();
+    red[tid] = tot;
+    __syncthreads();
+    for (int s = 128; s > 0; s >>= 1) {
+      if (tid < s) red[tid] += red[tid + s];
+      __syncthreads();
+    }
+    // Stop one sweep after the off-diagonal mass falls below 1e-11 of the total
+    // (quadratic convergence then reaches the fp32 rounding floor).
+    if (tid == 0) sh_stop = (offs <= 1e-11f * red[0]) ? sh_stop + 1 : 0;
+    __syncthreads();
+    if (sh_stop >= 2 || offs == 0.f) break;
+    for (int step = 0; step < m - 1; ++step) {
+      if (tid < np) {
+        auto player = [&](int pos) { return pos == 0 ? 0 : 1 + (pos - 1 + step) % (m - 1); };
+        int p = player(tid), q = player(m - 1 - tid);
+        if (p > q) {
+          int t = p;
+          p = q;
+          q = t;
+        }
+        float c = 1.f, s = 0.f;
+        if (q < d) {
+          const double apq = A[p * kEP + q];
+          if (apq != 0.0) {
+            const double app = A[p * kEP + p], aqq = A[q * kEP + q];
+            const double tau = (aqq - app) / (2.0 * apq);
+            const double t = (tau >= 0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
+            const double cc = 1.0 / sqrt(1.0 + t * t);
+            c = (float)cc;
+            s = (float)(t * cc);
+          }
+        }
+        rp[tid] = p;
+        rq[tid] = q;
+        rc[tid] = c;
+        rs[tid] = s;
+      }
+      __syncthreads();
+      // A <- J^T A J, one 2x2 block per (row pair, column pair)
+      for (int e = tid; e < np * np; e += 256) {
+        const int k1 = e / np, k2 = e % np;
+        const int p1 = rp[k1], q1 = rq[k1], p2 = rp[k2], q2 = rq[k2];
+        const float c1 = rc[k1], s1 = rs[k1], c2 = rc[k2], s2 = rs[k2];
+        const bool hq1 = q1 < d, hq2 = q2 < d;
+        const float a = A[p1 * kEP + p2];
+        const float b = hq2 ? A[p1 * kEP + q2] : 0.f;
+        const float cc = hq1 ? A[q1 * kEP + p2] : 0.f;
+        const float dd = (hq1 && hq2) ? A[q1 * kEP + q2] : 0.f;
+        // rows: p' = c p - s q, q' = s p + c q
+        const float r00 = c1 * a - s1 * cc, r01 = c1 * b - s1 * dd;
+        const float r10 = s1 * a + c1 * cc, r11 = s1 * b + c1 * dd;
+        // columns
+        float n00 = c2 * r00 - s2 * r01, n01 = s2 * r00 + c2 * r01;
+        float n10 = c2 * r10 - s2 * r11, n11 = s2 * r10 + c2 * r11;
+        if (k1 == k2) {
+          n01 = 0.f;
+          n10 = 0.f;
+        }
+        A[p1 * kEP + p2] = n00;
+        if (hq2) A[p1 * kEP + q2] = n01;
+        if (hq1) A[q1 * kEP + p2] = n10;
+        if (hq1 && hq2) A[q1 * kEP + q2] = n11;
+      }
+      // V <- V J
+      for (int e = tid; e < d * np; e += 256) {
+        const int i = e / np, kk = e % np;
+        const int p = rp[kk], q = rq[kk];
+        if (q >= d) continue;
+        const float c = rc[kk], s = rs[kk];
+        const float vp = V[i * kEP + p], vq = V[i * kEP + q];
+        V[i * kEP + p] = c * vp - s * vq;
+        V[i * kEP + q] = s * vp + c * vq;
+      }
+      __syncthreads();
+    }
+  }
+  __syncthreads();
+  // sort descending (ties by index) and write
+  float* vals = vec(C, bh, J.vals[job]);
+  float* vecs = mat(C, bh, J.vecs[job]);
+  for (int i = tid; i < d; i += 256) {
+    const float li = A[i * kEP + i];
+    int rank = 0;
+    for (int j = 0; j < d; ++j) {
+      const float lj = A[j * kEP + j];
+      rank += (lj > li) || (lj == li && j < i);
+    }
+    vals[rank] = li;
+    for (int r = 0; r < d; ++r) vecs[r * d + rank] = V[r * kEP + i];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Small dense products inside one workgroup (d x d, fp32 FMA):
+// Cm = op(A) * B with op(A) = A or A^T.
+// ---------------------------------------------------------------------------
+
+__device__ void wg_matmul(const float* Am, bool transA, const float* Bm, float* Cm, int d,
+                          float (*As)[kDP], float (*Bs)[kDP]) {
+  const int d4 = (d + 3) / 4;
+  float acc[4][16];
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[q][e] = 0.f;
+  for (int t0 = 0; t0 < d; t0 += kStage) {
+    const int tn = min(kStage, d - t0);
+    __syncthreads();
+    // As[t][i] = op(A)[i][t0 + t],  Bs[t][j] = B[t0 + t][j]
+    for (int e = threadIdx.x; e < kStage * 4 * d4; e += 256) {
+      const int t = e / (4 * d4), i = e % (4 * d4);
+      const bool in = t < tn && i < d;
+      As[t][i] = in ? (transA ? Am[(t0 + t) * d + i] : Am[i * d + t0 + t]) : 0.f;
+      Bs[t][i] = in ? Bm[(t0 + t) * d + i] : 0.f;
+    }
+    __syncthreads();
+    acc_outer(As, Bs, tn, d4, acc);
+  }
+  __syncthreads();
+  write_outer(Cm, d, d4, acc);
+  __threadfence_block();
+  __syncthreads();
+}
+
+// Metric mode, after the first eigensolves: roots S_q (of Q^T Q/n) and S_k (of
+// the key covariance), and C2 = S_q^T C_K S_q, the covariance of K S_q.
+__global__ __launch_bounds__(256) void prep_metric_kernel(Ctx C) {
+  __shared__ __attribute__((aligned(16))) float As[kStage][kDP];
+  __shared__ __attribute__((aligned(16))) float Bs[kStage][kDP];
+  const int bh = blockIdx.x, d = C.d;
+  float* Sq = mat(C, bh, M_E0);
+  float* Sk = mat(C, bh, M_EK);
+  const float* lq = vec(C, bh, V_L0);
+  const float* lk = vec(C, bh, V_LK);
+  for (int e = threadIdx.x; e < d * d; e += 256) {
+    const int j = e % d;
+    Sq[e] *= sqrtf(fmaxf(lq[j], 0.f));
+    Sk[e] *= sqrtf(fmaxf(lk[j], 0.f));
+  }
+  __threadfence_block();
+  __syncthreads();
+  float* tmp = mat(C, bh, M_TK);
+  wg_matmul(mat(C, bh, M_CK), false, Sq, tmp, d, As, Bs);  // C_K S_q
+  wg_matmul(Sq, true, tmp, mat(C, bh, M_C2), d, As, Bs);   // S_q^T C_K S_q
+  // kq = mu_K^T S_q (for orienting the key axes)
+  const float* muk = vec(C, bh, V_MUK);
+  for (int j = threadIdx.x; j < d; j += 256) {
+    float s = 0.f;
+    for (int t = 0; t < d; ++t) s = __builtin_fmaf(muk[t], Sq[t * d + j], s);
+    vec(C, bh, V_KQ)[j] = s;
+  }
+}
+
+// Metric mode, queries: rho = q S_k, inv = 1/|rho| (0 if rho = 0), r = rho*inv;
+// partial sums of r r^T and r per row block; inv is kept for the projection.
+__global__ __launch_bounds__(256) void qnorm_partial_kernel(Ctx C) {
+  extern __shared__ float qsh[];
+  float* Sk = qsh;                                        // [d][kDP]
+  float (*X)[kDP] = (float(*)[kDP])(qsh + kMaxD * kDP);   // [kStage][kDP]
+  float (*R)[kDP] = (float(*)[kDP])(qsh + (kMaxD + kStage) * kDP);
+  __shared__ float invs[kStage];
+  const int bh = blockIdx.y, blk = blockIdx.x, d = C.d, d4 = (d + 3) / 4;
+  const Side& S = C.s[0];
+  const float* Skg = mat(C, bh, M_EK);
+  for (int e = threadIdx.x; e < d * 4 * d4; e += 256) {
+    const int t = e / (4 * d4), j = e % (4 * d4);
+    Sk[t * kDP + j] = j < d ? Skg[t * d + j] : 0.f;
+  }
+  const int r0 = blk * kMomRows, r1 = min(S.n, r0 + kMomRows);
+  float acc[4][16];
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[q][e] = 0.f;
+  float csum = 0.f;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  for (int rs = r0; rs < r1; rs += kStage) {
+    const int rows = min(kStage, r1 - rs);
+    __syncthreads();
+    for (int e = threadIdx.x; e < kStage * 4 * d4; e += 256) {
+      const int r = e / (4 * d4), t = e % (4 * d4);
+      X[r][t] = (r < rows && t < d) ? load_x(S.x, bh, rs + r, S.n, C.H, d, t, C.dtype, C.layout)
+                                    : 0.f;
+    }
+    __syncthreads();
+    // rho for the staged rows
+    for (int e = threadIdx.x; e < kStage * d4; e += 256) {
+      const int r = e / d4, j4 = e % d4;
+      float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+      for (int t = 0; t < d; ++t) {
+        const float xv = X[r][t];
+        const float4 s4 = *(const float4*)&Sk[t * kDP + 4 * j4];
+        a0 = __builtin_fmaf(xv, s4.x, a0);
+        a1 = __builtin_fmaf(xv, s4.y, a1);
+        a2 = __builtin_fmaf(xv, s4.z, a2);
+        a3 = __builtin_fmaf(xv, s4.w, a3);
+      }
+      *(float4*)&R[r][4 * j4] = make_float4(a0, a1, a2, a3);
+    }
+    __syncthreads();
+    // one wave per row: 1/|rho|
+    for (int r = w; r < kStage; r += 4) {
+      float s = 0.f;
+      for (int t = lane; t < d; t += 64) s = __builtin_fmaf(R[r][t], R[r][t], s);
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+      if (lane == 0) {
+        const float inv = s > 0.f ? 1.f / sqrtf(s) : 0.f;
+        invs[r] = inv;
+        if (r < rows) C.inv_q[(size_t)bh * S.n + rs + r] = inv;
+      }
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < kStage * 4 * d4; e += 256) {
+      const int r = e / (4 * d4), t = e % (4 * d4);
+      R[r][t] = r < rows ? R[r][t] * invs[r] : 0.f;
+    }
+    __syncthreads();
+    acc_outer(R, R, rows, d4, acc);
+    if (threadIdx.x < d)
+      for (int r = 0; r < rows; ++r) csum += R[r][threadIdx.x];
+  }
+  float* out = C.qn_part + ((size_t)bh * C.nblk + blk) * (d * d + d);
+  write_outer(out, d, d4, acc);
+  if (threadIdx.x < d) out[d * d + threadIdx.x] = csum;
+}
+
+// Covariance of r(q) (fp64 reduction) and its mean.
+__global__ __launch_bounds__(256) void qnorm_finish_kernel(Ctx C) {
+  __shared__ double mu[kMaxD];
+  const int bh = blockIdx.x, d = C.d;
+  const float* part = C.qn_part + (size_t)bh * C.nblk * (d * d + d);
+  const double n = (double)C.s[0].n;
+  for (int t = threadIdx.x; t < d; t += 256) {
+    double s = 0.0;
+    for (int b = 0; b < C.nblk; ++b) s += (double)part[(size_t)b * (d * d + d) + d * d + t];
+    mu[t] = s / n;
+    vec(C, bh, V_MUR)[t] = (float)(s / n);
+  }
+  __syncthreads();
+  float* M = mat(C, bh, M_C3);
+  for (int e = threadIdx.x; e < d * d; e += 256) {
+    double s = 0.0;
+    for (int b = 0; b < C.nblk; ++b) s += (double)part[(size_t)b * (d * d + d) + e];
+    M[e] = (float)(s / n - mu[e / d] * mu[e % d]);
+  }
+}
+
+// Final projection matrices with the orientation rule (every split coordinate
+// gets a non-negative mean):
+//   metric: T_K = S_q U2, W_Q = S_k U3     pca: T_K = U_K, W_Q = U_Q
+__global__ __launch_bounds__(256) void prep_final_kernel(Ctx C) {
+  __shared__ __attribute__((aligned(16))) float As[kStage][kDP];
+  __shared__ __attribute__((aligned(16))) float Bs[kStage][kDP];
+  __shared__ float sgn[2][kMaxD];
+  const int bh = blockIdx.x, d = C.d;
+  const bool metric = C.xf == CA_XF_METRIC;
+  float* Uk = mat(C, bh, metric ? M_C2 : M_EK);
+  float* Uq = mat(C, bh, metric ? M_C3 : M_E0);
+  const float* mk = vec(C, bh, metric ? V_KQ : V_MUK);
+  const float* mq = vec(C, bh, metric ? V_MUR : V_MUQ);
+  for (int j = threadIdx.x; j < d; j += 256) {
+    float sk = 0.f, sq = 0.f;
+    for (int t = 0; t < d; ++t) {
+      sk = __builtin_fmaf(mk[t], Uk[t * d + j], sk);
+      sq = __builtin_fmaf(mq[t], Uq[t * d + j], sq);
+    }
+    sgn[0][j] = sk < 0.f ? -1.f : 1.f;
+    sgn[1][j] = sq < 0.f ? -1.f : 1.f;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < d * d; e += 256) {
+    const int j = e % d;
+    Uk[e] *= sgn[0][j];
+    Uq[e] *= sgn[1][j];
+  }
+  __threadfence_block();
+  __syncthreads();
+  float* Tk = mat(C, bh, M_TK);
+  float* Tq = mat(C, bh, M_TQ);
+  if (metric) {
+    wg_matmul(mat(C, bh, M_E0), false, Uk, Tk, d, As, Bs);
+    wg_matmul(mat(C, bh, M_EK), false, Uq, Tq, d, As, Bs);
+  } else {
+    for (int e = threadIdx.x; e < d * d; e += 256) {
+      Tk[e] = Uk[e];
+      Tq[e] = Uq[e];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Projection Y = X T (fp32), or Y = X for the raw-coordinate mode.
+// ---------------------------------------------------------------------------
+
+constexpr int kProjRows = 256;
+
+__global__ __launch_bounds__(256) void project_kernel(Ctx C) {
+  extern __shared__ float psh[];
+  float* T = psh;                                        // [d][kDP]
+  float (*X)[kDP] = (float(*)[kDP])(psh + kMaxD * kDP);  // [kStage][kDP]
+  const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH;
+  const Side& S = C.s[side];
+  const int d = C.d, d4 = (d + 3) / 4;
+  const int r0 = blockIdx.x * kProjRows, r1 = min(S.n, r0 + kProjRows);
+  if (r0 >= r1) return;
+  float* Y = S.y + (size_t)bh * S.n * d;
+  if (C.xf == CA_XF_NONE) {
+    for (int e = threadIdx.x; e < (r1 - r0) * d; e += 256) {
+      const int r = r0 + e / d, t = e % d;
+      Y[(size_t)r * d + t] = load_x(S.x, bh, r, S.n, C.H, d, t, C.dtype, C.layout);
+    }
+    return;
+  }
+  const float* Tg = mat(C, bh, side == 0 ? M_TQ : M_TK);
+  for (int e = threadIdx.x; e < d * 4 * d4; e += 256) {
+    const int t = e / (4 * d4), j = e % (4 * d4);
+    T[t * kDP + j] = j < d ? Tg[t * d + j] : 0.f;
+  }
+  const bool scale = side == 0 && C.xf == CA_XF_METRIC;
+  for (int rs = r0; rs < r1; rs += kStage) {
+    const int rows = min(kStage, r1 - rs);
+    __syncthreads();
+    for (int e = threadIdx.x; e < kStage * 4 * d4; e += 256) {
+      const int r = e / (4 * d4), t = e % (4 * d4);
+      X[r][t] = (r < rows && t < d) ? load_x(S.x, bh, rs + r, S.n, C.H, d, t, C.dtype, C.layout)
+                                    : 0.f;
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < rows * d4; e += 256) {
+      const int r = e / d4, j4 = e % d4;
+      float a[4] = {0.f, 0.f, 0.f, 0.f};
+      for (int t = 0; t < d; ++t) {
+        const float xv = X[r][t];
+        const float4 t4 = *(const float4*)&T[t * kDP + 4 * j4];
+        a[0] = __builtin_fmaf(xv, t4.x, a[0]);
+        a[1] = __builtin_fmaf(xv, t4.y, a[1]);
+        a[2] = __builtin_fmaf(xv, t4.z, a[2]);
+        a[3] = __builtin_fmaf(xv, t4.w, a[3]);
+      }
+      const float sc = scale ? C.inv_q[(size_t)bh * S.n + rs + r] : 1.f;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (4 * j4 + j < d) Y[(size_t)(rs + r) * d + 4 * j4 + j] = a[j] * sc;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Recursive split
+// ---------------------------------------------------------------------------
+
+// Highest-variance coordinate of the node's subsample, computed by one
+// wavefront: lane t owns coordinates t and t + 64. fp64, two passes over the
+// rows in order, mean = sum/m, variance = sum((y - mean)^2)/m, no contraction;
+// ties go to the lowest coordinate.
+__device__ int choose_coordinate(const float* __restrict__ Y, int d, const int32_t* idx,
+                                 bool identity, int start, int size, int lane) {
+#pragma clang fp contract(off)
+  const int m = size < d ? size : d;
+  double best = -1.0;
+  int bt = 0x7fffffff;
+  for (int half = 0; half < 2; ++half) {
+    const int t = lane + 64 * half;
+    if (t >= d) break;
+    double acc = 0.0;
+    for (int j = 0; j < m; ++j) {
+      const int p = start + (int)(((int64_t)(2 * j + 1) * size) / (2 * m));
+      const int i = identity ? p : idx[p];
+      acc = acc + (double)Y[(size_t)i * d + t];
+    }
+    const double mean = acc / (double)m;
+    double acc2 = 0.0;
+    for (int j = 0; j < m; ++j) {
+      const int p = start + (int)(((int64_t)(2 * j + 1) * size) / (2 * m));
+      const int i = identity ? p : idx[p];
+      const double dv = (double)Y[(size_t)i * d + t] - mean;
+      const double sq = dv * dv;
+      acc2 = acc2 + sq;
+    }
+    const double var = acc2 / (double)m;
+    if (var > best || (var == best && t < bt)) {
+      best = var;
+      bt = t;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const double ob = __shfl_xor(best, o, 64);
+    const int ot = __shfl_xor(bt, o, 64);
+    if (ob > best || (ob == best && ot < bt)) {
+      best = ob;
+      bt = ot;
+    }
+  }
+  return bt;
+}
+
+// Node state layout (int32): 0 j*, 1 threshold prefix, 2 rank among the
+// remaining candidates, 3 left size, 4 start, 5 size, 6 arrival counter,
+// 7 number of chunks.
+__device__ __forceinline__ int32_t* node_ptr(const Ctx& C, int pid, int node) {
+  return C.node_state + ((size_t)pid * C.max_nodes + node) * kNodeInts;
+}
+
+struct LevelArgs {
+  int level;
+  int first;  // input permutation is the identity
+  const int32_t* idx_in;
+  int32_t* idx_out;
+};
+
+__global__ __launch_bounds__(64) void split_choose_kernel(Ctx C, LevelArgs L) {
+  const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH, node = blockIdx.x;
+  const Side& S = C.s[side];
+  if (L.level >= S.big) return;
+  int start, size;
+  node_range(S.n, S.c, L.level, node, &start, &size);
+  int32_t* ns = node_ptr(C, pid, node);
+  const int lane = threadIdx.x;
+  if (size <= S.c) {
+    if (lane == 0) ns[0] = -1;
+    return;
+  }
+  const int32_t* idx = L.idx_in + (size_t)pid * C.nmax;
+  const int js = choose_coordinate(S.y + (size_t)bh * S.n * C.d, C.d, idx, L.first, start, size,
+                                   lane);
+  uint32_t* hist = C.hist + ((size_t)pid * C.max_nodes + node) * kRadixBins;
+  for (int b = lane; b < kRadixBins; b += 64) hist[b] = 0u;
+  if (lane == 0) {
+    const int mL = left_size(size, S.c);
+    ns[0] = js;
+    ns[1] = 0;
+    ns[2] = mL - 1;
+    ns[3] = mL;
+    ns[4] = start;
+    ns[5] = size;
+    ns[6] = 0;
+    ns[7] = (size + kChunk - 1) / kChunk;
+  }
+}
+
+// Block-wide exclusive scan (256 threads).
+__device__ __forceinline__ int scan256(int x, int* wsum, int* total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int v = x;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(v, o, 64);
+    if (lane >= o) v += y;
+  }
+  if (lane == 63) wsum[w] = v;
+  __syncthreads();
+  int base = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if (i < w) base += wsum[i];
+    tot += wsum[i];
+  }
+  __syncthreads();
+  *total = tot;
+  return base + v - x;
+}
+
+// Digit pass `pass` (0: bits 31..21, 1: bits 20..10, 2: bits 9..0) of the
+// radix select of the node's (m_L)-th smallest key. Pass 0 also materialises
+// the keys. The last block to finish a node picks the digit.
+__global__ __launch_bounds__(256) void split_hist_kernel(Ctx C, LevelArgs L, int pass) {
+  __shared__ int lh[kRadixBins];
+  __shared__ int wsum[4];
+  __shared__ int sh_last;
+  const int pid = blockIdx.z, side = pid / C.BH, bh = pid % C.BH, node = blockIdx.y;
+  const Side& S = C.s[side];
+  if (L.level >= S.big) return;
+  int32_t* ns = node_ptr(C, pid, node);
+  const int js = ns[0];
+  if (js < 0) return;
+  const int start = ns[4], size = ns[5], nch = ns[7];
+  const int c0 = blockIdx.x * kChunk;
+  if (c0 >= size) return;
+  const int c1 = min(size, c0 + kChunk);
+  const int shift = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
+  const uint32_t dmask = pass == 2 ? 1023u : 2047u;
+  const int mshift = pass == 0 ? 32 : (pass == 1 ? 21 : 10);
+  const uint32_t prefix = (uint32_t)ns[1];
+  for (int b = threadIdx.x; b < kRadixBins; b += 256) lh[b] = 0;
+  __syncthreads();
+  const float* Y = S.y + (size_t)bh * S.n * C.d;
+  const int32_t* idx = L.idx_in + (size_t)pid * C.nmax;
+  uint32_t* keys = C.keys + (size_t)pid * C.nmax;
+  for (int o = c0 + threadIdx.x; o < c1; o += 256) {
+    const int p = start + o;
+    uint32_t key;
+    if (pass == 0) {
+      const int i = L.first ? p : idx[p];
+      key = ordered_bits(Y[(size_t)i * C.d + js]);
+      keys[p] = key;
+    } else {
+      key = keys[p];
+    }
+    if (mshift == 32 || (key >> mshift) == (prefix >> mshift))
+      atomicAdd(&lh[(key >> shift) & dmask], 1);
+  }
+  __syncthreads();
+  uint32_t* gh = C.hist + ((size_t)pid * C.max_nodes + node) * kRadixBins;
+  for (int b = threadIdx.x; b < kRadixBins; b += 256)
+    if (lh[b]) atomicAdd(&gh[b], (uint32_t)lh[b]);
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) sh_last = atomicAdd(&ns[6], 1) == nch - 1;
+  __syncthreads();
+  if (!sh_last) return;
+  __threadfence();
+  // Last block of this node: find the digit holding the wanted rank.
+  const int rank = ns[2];
+  int cnt[8], sum = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int b = threadIdx.x * 8 + i;
+    cnt[i] = (int)__hip_atomic_load(&gh[b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    gh[b] = 0u;
+    sum += cnt[i];
+  }
+  int tot;
+  const int before = scan256(sum, wsum, &tot);
+  if (rank >= before && rank < before + sum) {
+    int acc = before;
+    for (int i = 0; i < 8; ++i) {
+      if (rank < acc + cnt[i]) {
+        ns[1] = (int)(prefix | ((uint32_t)(threadIdx.x * 8 + i) << shift));
+        ns[2] = rank - acc;
+        break;
+      }
+      acc += cnt[i];
+    }
+  }
+  if (threadIdx.x == 0) ns[6] = 0;
+}
+
+// Per-chunk counts of keys below / equal to the threshold; the last block
+// turns them into exclusive prefixes over the node's chunks.
+__global__ __launch_bounds__(256) void split_count_kernel(Ctx C, LevelArgs L) {
+  __shared__ int wsum[4];
+  __shared__ int sh_last;
+  const int pid = blockIdx.z, side = pid / C.BH, node = blockIdx.y;
+  const Side& S = C.s[side];
+  if (L.level >= S.big) return;
+  int32_t* ns = node_ptr(C, pid, node);
+  if (ns[0] < 0) return;
+  const int start = ns[4], size = ns[5], nch = ns[7];
+  const int c0 = blockIdx.x * kChunk;
+  if (c0 >= size) return;
+  const int c1 = min(size, c0 + kChunk);
+  const uint32_t thr = (uint32_t)ns[1];
+  const uint32_t* keys = C.keys + (size_t)pid * C.nmax;
+  int less = 0, eq = 0;
+  for (int o = c0 + threadIdx.x; o < c1; o += 256) {
+    const uint32_t key = keys[start + o];
+    less += key < thr;
+    eq += key == thr;
+  }
+  int tl, te;
+  scan256(less, wsum, &tl);
+  scan256(eq, wsum, &te);
+  int32_t* cc = C.chunk_cnt + ((size_t)pid * C.max_nodes + node) * C.max_chunks * 2;
+  if (threadIdx.x == 0) {
+    cc[2 * blockIdx.x] = tl;
+    cc[2 * blockIdx.x + 1] = te;
+  }
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) sh_last = atomicAdd(&ns[6], 1) == nch - 1;
+  __syncthreads();
+  if (!sh_last) return;
+  __threadfence();
+  if (threadIdx.x == 0) {
+    int sl = 0, se = 0;
+    for (int ch = 0; ch < nch; ++ch) {
+      const int l = __hip_atomic_load(&cc[2 * ch], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int e = __hip_atomic_load(&cc[2 * ch + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      cc[2 * ch] = sl;
+      cc[2 * ch + 1] = se;
+      sl += l;
+      se += e;
+    }
+    ns[6] = 0;
+  }
+}
+
+// Stable partition of every node: the m_L smallest (key, index) pairs go left
+// in node order, the rest right in node order. Nodes that are already leaves
+// are copied.
+__global__ __launch_bounds__(256) void split_scatter_kernel(Ctx C, LevelArgs L) {
+  __shared__ int wsum[4];
+  const int pid = blockIdx.z, side = pid / C.BH, node = blockIdx.y;
+  const Side& S = C.s[side];
+  if (L.level >= S.big) return;
+  int start, size;
+  node_range(S.n, S.c, L.level, node, &start, &size);
+  const int c0 = blockIdx.x * kChunk;
+  if (c0 >= size) return;
+  const int c1 = min(size, c0 + kChunk);
+  const int32_t* idx_in = L.idx_in + (size_t)pid * C.nmax;
+  int32_t* idx_out = L.idx_out + (size_t)pid * C.nmax;
+  const int32_t* ns = node_ptr(C, pid, node);
+  if (size <= S.c) {
+    for (int o = c0 + threadIdx.x; o < c1; o += 256)
+      idx_out[start + o] = L.first ? start + o : idx_in[start + o];
+    return;
+  }
+  const uint32_t thr = (uint32_t)ns[1];
+  const int need_eq = ns[2] + 1, mL = ns[3];
+  const int32_t* cc = C.chunk_cnt + ((size_t)pid * C.max_nodes + node) * C.max_chunks * 2;
+  const int less0 = cc[2 * blockIdx.x], eq0 = cc[2 * blockIdx.x + 1];
+  const uint32_t* keys = C.keys + (size_t)pid * C.nmax;
+  constexpr int per = kChunk / 256;
+  const int o0 = c0 + threadIdx.x * per, o1 = min(c1, o0 + per);
+  int less = 0, eq = 0;
+  for (int o = o0; o < o1; ++o) {
+    const uint32_t key = keys[start + o];
+    less += key < thr;
+    eq += key == thr;
+  }
+  int tot;
+  const int packed = scan256((less << 16) | eq, wsum, &tot);
+  int lb = less0 + (packed >> 16), eb = eq0 + (packed & 0xFFFF);
+  for (int o = o0; o < o1; ++o) {
+    const uint32_t key = keys[start + o];
+    const int Lo = lb + min(eb, need_eq);
+    const bool left = key < thr || (key == thr && eb < need_eq);
+    const int dst = left ? Lo : mL + (o - Lo);
+    if (dst >= 0 && dst < size) idx_out[start + dst] = L.first ? start + o : idx_in[start + o];
+    lb += key < thr;
+    eb += key == thr;
+  }
+}
+
+// Remaining levels of one node (at most the side's tail size) in one
+// workgroup: per level every active sub-node picks its coordinate (one
+// wavefront each), keys are gathered, a four-pass 8-bit radix select runs on
+// per-sub-node LDS histograms, and a block-wide scan partitions stably.
+constexpr int kTailThreads = 512;
+constexpr int kMaxSub = 32;
+
+__device__ __forceinline__ int scan512(int x, int* wsum) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int v = x;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(v, o, 64);
+    if (lane >= o) v += y;
+  }
+  if (lane == 63) wsum[w] = v;
+  __syncthreads();
+  int base = 0;
+#pragma unroll
+  for (int i = 0; i < kTailThreads / 64; ++i)
+    if (i < w) base += wsum[i];
+  __syncthreads();
+  return base + v - x;
+}
+
+__global__ __launch_bounds__(kTailThreads) void split_tail_kernel(Ctx C, int parity0, int parity1) {
+  __shared__ int32_t ia[kTail], ib[kTail];
+  __shared__ uint32_t keys[kTail];
+  __shared__ int scan[kTail + 1];
+  __shared__ int hist[kMaxSub][256];
+  __shared__ int sub_start[2 * kMaxSub + 2], sub_size[2 * kMaxSub + 2];
+  __shared__ int sub_js[2 * kMaxSub + 2], sub_thr[2 * kMaxSub + 2], sub_rank[2 * kMaxSub + 2];
+  __shared__ int act_list[kMaxSub], act_of[2 * kMaxSub + 2];
+  __shared__ int wsum[kTailThreads / 64];
+  __shared__ int sh_nact;
+  const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH, node = blockIdx.x;
+  const Side& S = C.s[side];
+  if (node >= (1 << S.big)) return;
+  int start, size;
+  node_range(S.n, S.c, S.big, node, &start, &size);
+  const int par = side == 0 ? parity0 : parity1;
+  const bool identity = S.big == 0;
+  const int32_t* src = (par ? C.idx1 : C.idx0) + (size_t)pid * C.nmax;
+  for (int o = threadIdx.x; o < size; o += kTailThreads) ia[o] = identity ? start + o : src[start + o];
+  const float* Y = S.y + (size_t)bh * S.n * C.d;
+  const int d = C.d, c = S.c;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int32_t* cur = ia;
+  int32_t* nxt = ib;
+  const int nsub_levels = S.levels - S.big;
+  for (int r = 0; r < nsub_levels; ++r) {
+    const int nslots = 1 << r;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      // Sub-node ranges at this level (relative to the node) and the active list.
+      int nact = 0;
+      for (int sl = 0; sl < nslots; ++sl) {
+        int st = 0, s = size;
+        for (int b = r - 1; b >= 0; --b) {
+          const int bit = (sl >> b) & 1;
+          const int mL = s > c ? left_size(s, c) : s;
+          if (bit) {
+            st += mL;
+            s -= mL;
+          } else {
+            s = mL;
+          }
+        }
+        sub_start[sl] = st;
+        sub_size[sl] = s;
+        act_of[sl] = -1;
+        if (s > c) {
+          act_of[sl] = nact;
+          act_list[nact++] = sl;
+        }
+      }
+      sub_start[nslots] = size;
+      sh_nact = nact;
+    }
+    __syncthreads();
+    const int nact = sh_nact;
+    if (nact == 0) break;
+    // coordinate choice: one wavefront per active sub-node
+    for (int a = w; a < nact; a += kTailThreads / 64) {
+      const int sl = act_list[a];
+      const int js = choose_coordinate(Y, d, cur, false, sub_start[sl], sub_size[sl], lane);
+      if (lane == 0) {
+        sub_js[sl] = js;
+        sub_thr[sl] = 0;
+        sub_rank[sl] = left_size(sub_size[sl], c) - 1;
+      }
+    }
+    __syncthreads();
+    // keys; slot of position o by binary search over the sub-node starts
+    for (int o = threadIdx.x; o < size; o += kTailThreads) {
+      // The last slot starting at or before o is the non-empty slot holding o:
+      // empty slots start where the next non-empty slot starts.
+      int lo = 0, hi = nslots - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (sub_start[mid] <= o)
+          lo = mid;
+        else
+          hi = mid - 1;
+      }
+      scan[o] = lo;  // slot id (temporarily)
+      keys[o] = act_of[lo] >= 0 ? ordered_bits(Y[(size_t)cur[o] * d + sub_js[lo]]) : 0u;
+    }
+    // four 8-bit digit passes
+    for (int pass = 0; pass < 4; ++pass) {
+      const int shift = 24 - 8 * pass;
+      const int mshift = shift + 8;
+      __syncthreads();
+      for (int e = threadIdx.x; e < nact * 256; e += kTailThreads) hist[e / 256][e % 256] = 0;
+      __syncthreads();
+      for (int o = threadIdx.x; o < size; o += kTailThreads) {
+        const int sl = scan[o], a = act_of[sl];
+        if (a < 0) continue;
+        const uint32_t key = keys[o];
+        const uint32_t pre = (uint32_t)sub_thr[sl];
+        if (mshift == 32 || (key >> mshift) == (pre >> mshift))
+          atomicAdd(&hist[a][(key >> shift) & 255], 1);
+      }
+      __syncthreads();
+      for (int a = w; a < nact; a += kTailThreads / 64) {
+        const int sl = act_list[a];
+        const int rank = sub_rank[sl];
+        int cnt[4], sum = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          cnt[i] = hist[a][4 * lane + i];
+          sum += cnt[i];
+        }
+        int incl = sum;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(incl, o, 64);
+          if (lane >= o) incl += y;
+        }
+        const int before = incl - sum;
+        if (rank >= before && rank < incl) {
+          int acc = before;
+          for (int i = 0; i < 4; ++i) {
+            if (rank < acc + cnt[i]) {
+              sub_thr[sl] = (int)((uint32_t)sub_thr[sl] | ((uint32_t)(4 * lane + i) << shift));
+              sub_rank[sl] = rank - acc;
+              break;
+            }
+            acc += cnt[i];
+          }
+        }
+      }
+    }
+    __syncthreads();
+    // stable partition: scan of packed (less, equal) counts in position order
+    constexpr int per = kTail / kTailThreads;
+    const int o0 = threadIdx.x * per;
+    int less = 0, eq = 0;
+    for (int o = o0; o < o0 + per && o < size; ++o) {
+      const int sl = scan[o];
+      if (act_of[sl] < 0) continue;
+      const uint32_t thr = (uint32_t)sub_thr[sl];
+      less += keys[o] < thr;
+      eq += keys[o] == thr;
+    }
+    const int packed0 = scan512((less << 16) | eq, wsum);
+    // exclusive prefix at every position (packed), then per-sub-node offsets
+    int run = packed0;
+    int slots_local[per];
+    for (int u = 0; u < per; ++u) {
+      const int o = o0 + u;
+      if (o >= size) break;
+      const int sl = scan[o];
+      slots_local[u] = sl;
+      const uint32_t thr = (uint32_t)sub_thr[sl];
+      const bool act = act_of[sl] >= 0;
+      const int inc = act ? (((keys[o] < thr) ? 1 : 0) << 16) | ((keys[o] == thr) ? 1 : 0) : 0;
+      scan[o] = run;  // overwrite slot id by the exclusive prefix
+      run += inc;
+    }
+    __syncthreads();
+    int newpos[per];
+    for (int u = 0; u < per; ++u) {
+      const int o = o0 + u;
+      if (o >= size) break;
+      const int sl = slots_local[u];
+      const int st = sub_start[sl];
+      if (act_of[sl] < 0) {
+        newpos[u] = o;
+        continue;
+      }
+      const int base = scan[st];
+      const int rel = scan[o] - base;
+      const int lb = rel >> 16, eb = rel & 0xFFFF;
+      const uint32_t thr = (uint32_t)sub_thr[sl];
+      const int need_eq = sub_rank[sl] + 1;
+      const int mL = left_size(sub_size[sl], c);
+      const int Lo = lb + min(eb, need_eq);
+      const bool left = keys[o] < thr || (keys[o] == thr && eb < need_eq);
+      const int rel_dst = left ? Lo : mL + (o - st - Lo);
+      newpos[u] = (rel_dst >= 0 && rel_dst < sub_size[sl]) ? st + rel_dst : -1;
+    }
+    __syncthreads();
+    for (int u = 0; u < per; ++u) {
+      const int o = o0 + u;
+      if (o >= size) break;
+      if (newpos[u] >= 0) nxt[newpos[u]] = cur[o];
+    }
+    int32_t* t = cur;
+    cur = nxt;
+    nxt = t;
+  }
+  __syncthreads();
+  int32_t* perm = S.perm + (size_t)bh * S.n;
+  for (int o = threadIdx.x; o < size; o += kTailThreads) perm[start + o] = cur[o];
+}
+
+// ---------------------------------------------------------------------------
+// Gather: permuted copies (pad rows zero), centroids of the original vectors,
+// counts, cluster ids. Values follow the key permutation and are stored per
+// key cluster as a d x c tile (dimension-major), which is the operand layout
+// of the value product in the attention kernels.
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(128) void gather_kernel(Ctx C) {
+  extern __shared__ float gsh[];  // value tile staging [c][d]
+  const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH, a = blockIdx.x;
+  const Side& S = C.s[side];
+  if (a >= S.nc) return;
+  const int d = C.d, c = S.c, t = threadIdx.x;
+  const int cnt = min(c, S.n - a * c);
+  const int32_t* perm = S.perm + (size_t)bh * S.n + (size_t)a * c;
+  if (t == 0) S.count[(size_t)bh * S.nc + a] = cnt;
+  if (S.cid)
+    for (int r = t; r < cnt; r += 128) S.cid[(size_t)bh * S.n + perm[r]] = a;
+  const size_t xrow0 = ((size_t)bh * S.npad + (size_t)a * c) * d;
+  const bool vals = side == 1 && C.v != nullptr;
+  for (int tt = t; tt < d; tt += 128) {
+    float s = 0.f, sv = 0.f;
+    for (int r = 0; r < c; ++r) {
+      float x = 0.f, xv = 0.f;
+      if (r < cnt) {
+        const int i = perm[r];
+        x = load_x(S.x, bh, i, S.n, C.H, d, tt, C.dtype, C.layout);
+        s += x;
+        if (vals) {
+          xv = load_x(C.v, bh, i, S.n, C.H, d, tt, C.dtype, C.layout);
+          sv += xv;
+        }
+      }
+      store_elem(S.xp, xrow0 + (size_t)r * d + tt, C.dtype, x);
+      if (vals) gsh[r * d + tt] = xv;
+    }
+    S.cent[((size_t)bh * S.nc + a) * d + tt] = s / (float)cnt;
+    if (vals) C.cent_v[((size_t)bh * S.nc + a) * d + tt] = sv / (float)cnt;
+  }
+  if (vals) {
+    __syncthreads();
+    const size_t vt0 = ((size_t)bh * S.nc + a) * (size_t)d * c;
+    for (int e = t; e < d * c; e += 128) {
+      const int dd = e / c, r = e % c;
+      store_elem(C.vp, vt0 + e, C.dtype, gsh[r * d + dd]);
+    }
+  }
+}
+
+int tail_size(int c) { return c * 64 < kTail ? c * 64 : kTail; }
+
+}  // namespace
+
+int split_big_levels(int n, int c, int L) {
+  const int tail = tail_size(c);
+  int l = 0;
+  while (l < L) {
+    int maxs = 0;
+    for (int node = 0; node < (1 << l); ++node) {
+      int st, s;
+      node_range(n, c, l, node, &st, &s);
+      if (s > maxs) maxs = s;
+    }
+    if (maxs <= tail) break;
+    ++l;
+  }
+  return l;
+}
+
+namespace {
+// Kernels that use more than 64 KiB of dynamic LDS declare their size once. A
+// refusal is not fatal here: the launch itself reports a real limit.
+constexpr size_t kEighLds = 2 * kMaxD * kEP * sizeof(float);
+constexpr size_t kQnormLds = (size_t)(kMaxD + 2 * kStage) * kDP * sizeof(float);
+constexpr size_t kProjLds = (size_t)(kMaxD + kStage) * kDP * sizeof(float);
+constexpr size_t kGatherLds = (size_t)kMaxC * kMaxD * sizeof(float);
+hipError_t set_lds_limits() {
+  static bool done = [] {
+    hipFuncSetAttribute((const void*)eigh_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                        (int)kEighLds);
+    hipFuncSetAttribute((const void*)qnorm_partial_kernel,
+                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)kQnormLds);
+    hipFuncSetAttribute((const void*)project_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                        (int)kProjLds);
+    hipFuncSetAttribute((const void*)gather_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                        (int)kGatherLds);
+    (void)hipGetLastError();
+    return true;
+  }();
+  (void)done;
+  return hipSuccess;
+}
+}  // namespace
+
+hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const void* v,
+                          const ca_cluster_out* out, char* ws, const Workspace& W,
+                          hipStream_t st) {
+  {
+    hipError_t le = set_lds_limits();
+    if (le != hipSuccess) return le;
+  }
+  Ctx C = {};
+  const int d = P.d;
+  C.BH = P.BH;
+  C.H = P.H;
+  C.d = d;
+  C.dtype = P.dtype;
+  C.layout = P.layout;
+  C.xf = P.xf;
+  C.nmax = P.nq > P.nk ? P.nq : P.nk;
+  C.nblk = W.nblk_mom;
+  C.v = v;
+  C.cent_v = out->cent_v;
+  C.vp = out->vp;
+  C.mats = (float*)(ws + W.mats);
+  C.vecs = (float*)(ws + W.vecs);
+  C.inv_q = (float*)(ws + W.inv_q);
+  C.mom_part = (float*)(ws + W.mom_part);
+  C.qn_part = (float*)(ws + W.qn_part);
+  C.idx0 = (int32_t*)(ws + W.idx0);
+  C.idx1 = (int32_t*)(ws + W.idx1);
+  C.keys = (uint32_t*)(ws + W.keys);
+  C.node_state = (int32_t*)(ws + W.node_state);
+  C.hist = (uint32_t*)(ws + W.hist);
+  C.chunk_cnt = (int32_t*)(ws + W.chunk_cnt);
+  C.max_nodes = W.max_big_nodes;
+  C.max_chunks = W.max_chunks;
+  Side& Sq = C.s[0];
+  Side& Sk = C.s[1];
+  Sq.x = q;
+  Sk.x = k;
+  Sq.y = out->yq_dbg ? out->yq_dbg : (float*)(ws + W.y_q);
+  Sk.y = out->yk_dbg ? out->yk_dbg : (float*)(ws + W.y_k);
+  Sq.perm = out->perm_q;
+  Sk.perm = out->perm_k;
+  Sq.cid = out->cid_q;
+  Sk.cid = out->cid_k;
+  Sq.count = out->count_q;
+  Sk.count = out->count_k;
+  Sq.cent = out->cent_q;
+  Sk.cent = out->cent_k;
+  Sq.xp = out->qp;
+  Sk.xp = out->kp;
+  Sq.n = P.nq;
+  Sk.n = P.nk;
+  Sq.c = P.cq;
+  Sk.c = P.ck;
+  Sq.nc = P.nqc;
+  Sk.nc = P.nkc;
+  Sq.npad = P.nq_pad;
+  Sk.npad = P.nk_pad;
+  Sq.levels = W.levels_q;
+  Sk.levels = W.levels_k;
+  Sq.big = W.big_q;
+  Sk.big = W.big_k;
+  Sq.tail = tail_size(P.cq);
+  Sk.tail = tail_size(P.ck);
+  const int BH = P.BH;
+  hipError_t e;
+#define CA_CHECK()                          \
+  do {                                      \
+    e = hipGetLastError();                  \
+    if (e != hipSuccess) return e;          \
+  } while (0)
+
+  if (P.xf != CA_XF_NONE) {
+    hipLaunchKernelGGL(moments_partial_kernel, dim3(C.nblk, 2 * BH), dim3(256), 0, st, C);
+    CA_CHECK();
+    hipLaunchKernelGGL(moments_finish_kernel, dim3(BH), dim3(256), 0, st, C);
+    CA_CHECK();
+    const size_t eigh_lds = kEighLds;
+    EighJobs J1 = {2, {M_A0, M_CK}, {M_E0, M_EK}, {V_L0, V_LK}};
+    hipLaunchKernelGGL(eigh_kernel, dim3(BH, 2), dim3(256), eigh_lds, st, C, J1);
+    CA_CHECK();
+    if (P.xf == CA_XF_METRIC) {
+      hipLaunchKernelGGL(prep_metric_kernel, dim3(BH), dim3(256), 0, st, C);
+      CA_CHECK();
+      const size_t qlds = kQnormLds;
+      hipLaunchKernelGGL(qnorm_partial_kernel, dim3(C.nblk, BH), dim3(256), qlds, st, C);
+      CA_CHECK();
+      hipLaunchKernelGGL(qnorm_finish_kernel, dim3(BH), dim3(256), 0, st, C);
+      CA_CHECK();
+      EighJobs J2 = {2, {M_C2, M_C3}, {M_C2, M_C3}, {V_L2, V_L3}};
+      hipLaunchKernelGGL(eigh_kernel, dim3(BH, 2), dim3(256), eigh_lds, st, C, J2);
+      CA_CHECK();
+    }
+    hipLaunchKernelGGL(prep_final_kernel, dim3(BH), dim3(256), 0, st, C);
+    CA_CHECK();
+  }
+  {
+    const int nmax = C.nmax;
+    const size_t plds = kProjLds;
+    hipLaunchKernelGGL(project_kernel, dim3((nmax + kProjRows - 1) / kProjRows, 2 * BH),
+                       dim3(256), plds, st, C);
+    CA_CHECK();
+  }
+  const int big = W.big_q > W.big_k ? W.big_q : W.big_k;
+  for (int l = 0; l < big; ++l) {
+    LevelArgs L;
+    L.level = l;
+    L.first = l == 0;
+    L.idx_in = (l & 1) ? C.idx1 : C.idx0;
+    L.idx_out = (l & 1) ? C.idx0 : C.idx1;
+    int maxs = 0;
+    for (int side = 0; side < 2; ++side) {
+      const Side& S = C.s[side];
+      if (l >= S.big) continue;
+      for (int node = 0; node < (1 << l); ++node) {
+        int s0, sz;
+        node_range(S.n, S.c, l, node, &s0, &sz);
+        if (sz > maxs) maxs = sz;
+      }
+    }
+    const int cpn = (maxs + kChunk - 1) / kChunk;
+    hipLaunchKernelGGL(split_choose_kernel, dim3(1 << l, 2 * BH), dim3(64), 0, st, C, L);
+    CA_CHECK();
+    for (int pass = 0; pass < 3; ++pass) {
+      hipLaunchKernelGGL(split_hist_kernel, dim3(cpn, 1 << l, 2 * BH), dim3(256), 0, st, C, L,
+                         pass);
+      CA_CHECK();
+    }
+    hipLaunchKernelGGL(split_count_kernel, dim3(cpn, 1 << l, 2 * BH), dim3(256), 0, st, C, L);
+    CA_CHECK();
+    hipLaunchKernelGGL(split_scatter_kernel, dim3(cpn, 1 << l, 2 * BH), dim3(256), 0, st, C, L);
+    CA_CHECK();
+  }
+  {
+    // After its last multi-block level, side s holds its order in idx[(big_s) & 1].
+    const int nodes = 1 << big;
+    hipLaunchKernelGGL(split_tail_kernel, dim3(nodes, 2 * BH), dim3(kTailThreads), 0, st, C,
+                       W.big_q & 1, W.big_k & 1);
+    CA_CHECK();
+  }
+  {
+    const int maxc = P.nqc > P.nkc ? P.nqc : P.nkc;
+    const size_t glds = v ? (size_t)P.ck * d * sizeof(float) : 0;
+    hipLaunchKernelGGL(gather_kernel, dim3(maxc, 2 * BH), dim3(128), glds, st, C);
+    CA_CHECK();
+  }
+#undef CA_CHECK
+  return hipSuccess;
+}
+
+}  // namespace ca

@@ -1,0 +1,92 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every symbol the header declares, and rejects invalid arguments before
+touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _lib():
+    from paper_2608_26965_amd import _lib as L
+    try:
+        return L, L.load()
+    except ImportError as e:  # pragma: no cover
+        pytest.skip(str(e))
+
+
+def test_header_symbols_exported():
+    L, lib = _lib()
+    hdr = open(os.path.join(ROOT, "include", "clusterattn.h")).read()
+    declared = set(re.findall(r"CA_API\s+[\w\s\*]+?\b(ca_\w+)\s*\(", hdr))
+    assert declared == set(L.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name)
+    assert lib.ca_abi_version() == 1
+
+
+def _prob(**kw):
+    from paper_2608_26965_amd import _lib as L
+    base = dict(batch=1, heads=2, nq=1000, nk=1000, d=64, cq=64, ck=64, dtype=L.CA_BF16,
+                transform=L.CA_XF_METRIC, layout=L.CA_LAYOUT_BHND)
+    base.update(kw)
+    return L.CaProblem(**base)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(cq=48), 1), (dict(ck=512), 1), (dict(d=0), 1), (dict(d=129), 1), (dict(nq=0), 1),
+    (dict(dtype=7), 1), (dict(transform=3), 1), (dict(layout=2), 1), (dict(heads=0), 1),
+])
+def test_invalid_problem(kw, status):
+    L, lib = _lib()
+    n = ctypes.c_size_t(0)
+    assert lib.ca_workspace_size(_prob(**kw), 1, n) == status
+    assert L.last_error() != ""
+
+
+def test_workspace_and_k_validation():
+    L, lib = _lib()
+    n = ctypes.c_size_t(0)
+    assert lib.ca_workspace_size(_prob(), 16, n) == 0 and n.value > 0
+    assert lib.ca_workspace_size(_prob(), 17, n) == L.CA_E_INVALID  # nkc = 16
+    assert lib.ca_workspace_size(_prob(), 0, n) == L.CA_E_INVALID
+    assert "k=0" in L.last_error()
+
+
+def test_calls_reject_before_enqueue():
+    L, lib = _lib()
+    p = _prob()
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+    out = L.CaClusterOut()
+    assert lib.ca_cluster(p, None, fake, None, out, None, 0, None) == L.CA_E_INVALID
+    assert lib.ca_cluster(p, fake, fake, None, out, None, 0, None) == L.CA_E_INVALID
+    full = L.CaClusterOut(*([0x1000] * 14))
+    assert lib.ca_cluster(p, fake, fake, None, full, fake, 16, None) == L.CA_E_WORKSPACE
+    assert lib.ca_select(p, None, None, None, None, 4, fake, None, 0, None) == L.CA_E_INVALID
+    assert lib.ca_select(p, fake, fake, None, None, 4, fake, None, 0, None) == L.CA_E_WORKSPACE
+    args = [fake] * 5
+    assert lib.ca_block_sparse_attn(p, *args, 0, 0.0, fake, fake, None) == L.CA_E_INVALID
+    assert lib.ca_block_sparse_attn(p, *args, 99, 0.0, fake, fake, None) == L.CA_E_INVALID
+    assert lib.ca_block_sparse_attn(_prob(d=48), *args, 2, 0.0, fake, fake, None) == \
+        L.CA_E_UNSUPPORTED
+    assert lib.ca_block_sparse_attn(_prob(cq=32), *args, 2, 0.0, fake, fake, None) == \
+        L.CA_E_UNSUPPORTED
+    assert lib.ca_compensate(p, fake, fake, fake, fake, fake, 2, 0.0, 1, None, fake, fake, fake,
+                             None, None) == L.CA_E_INVALID
+    assert lib.ca_compensate(p, None, None, None, None, None, 2, 0.0, 1, fake, fake, fake, fake,
+                             None, None) == L.CA_E_INVALID
+    ws_misaligned = ctypes.c_void_p(0x1001)
+    need = ctypes.c_size_t(0)
+    lib.ca_workspace_size(p, 1, need)
+    assert lib.ca_cluster(p, fake, fake, None, full, ws_misaligned, need.value, None) == \
+        L.CA_E_INVALID
+    assert "aligned" in L.last_error()
+
+
+def test_status_strings():
+    L, lib = _lib()
+    for s in range(5):
+        assert lib.ca_status_str(s).decode().startswith("CA_")

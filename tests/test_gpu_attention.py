@@ -1,0 +1,145 @@
+"""GPU parity of the attention calls against the oracle, through the C ABI.
+
+Inputs are seeded synthetic mixtures; permutations and selection lists are
+drawn at random so that the attention kernels are checked on their own
+(independently of the clustering). Sizes span several tiles and a ragged last
+cluster."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import ref
+from synth import mixture_inputs
+
+pytestmark = pytest.mark.gpu
+
+CASES = [
+    # dtype, d, cq, ck, n, k
+    ("bf16", 64, 128, 128, 1000, 3),
+    ("bf16", 64, 64, 64, 700, 5),
+    ("bf16", 128, 64, 64, 650, 4),
+    ("bf16", 128, 128, 128, 1111, 2),
+    ("bf16", 64, 128, 64, 900, 6),
+    ("bf16", 128, 64, 128, 777, 7),
+    ("f32", 64, 64, 64, 1000, 4),
+    ("f32", 32, 32, 16, 333, 5),
+    ("f32", 128, 16, 64, 300, 2),
+]
+
+
+def _setup(dt, d, cq, ck, n, k, seed=0, heads=2):
+    from tests import gpu_util as G
+    Q, K, V = mixture_inputs(seed, heads, n, d, dt, centres=8, sigma=0.4)
+    rng = np.random.default_rng(seed + 1)
+    perm_q = np.stack([rng.permutation(n) for _ in range(heads)]).astype(np.int32)
+    perm_k = np.stack([rng.permutation(n) for _ in range(heads)]).astype(np.int32)
+    nqc, nkc = -(-n // cq), -(-n // ck)
+    k = min(k, nkc)
+    lists = G.random_lists(rng, heads, nqc, nkc, k)
+    return Q, K, V, perm_q, perm_k, lists, k
+
+
+@pytest.mark.parametrize("dt,d,cq,ck,n,k", CASES)
+def test_block_sparse_attention_parity(dt, d, cq, ck, n, k):
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    G.flush(f"attn case dt={dt} d={d} cq={cq} ck={ck} n={n} k={k}")
+    Q, K, V, perm_q, perm_k, lists, k = _setup(dt, d, cq, ck, n, k)
+    H = Q.shape[0]
+    p = ca.Problem(1, H, n, n, d, cq, ck, G.tdtype(dt))
+    tq = G.permuted_rows(Q, perm_q, cq, G.tdtype(dt))
+    tk = G.permuted_rows(K, perm_k, ck, G.tdtype(dt))
+    tv = G.value_tiles(V, perm_k, ck, G.tdtype(dt))
+    cnt = G.dev(np.stack([G.counts(n, ck)] * H), torch.int32)
+    op, lse = ca.block_sparse_attn(p, tq, tk, tv, cnt, G.dev(lists, torch.int32), k)
+    torch.cuda.synchronize()
+    op, lse = G.host(op), G.host(lse)
+    tau = 1 / math.sqrt(d)
+    worst = 0.0
+    for h in range(H):
+        o, l = ref.sparse_attention(Q[h], K[h], V[h], perm_q[h], G.counts(n, cq), perm_k[h],
+                                    G.counts(n, ck), lists[h], tau)
+        got = op[h, :n]
+        want = o[perm_q[h]]
+        err = np.abs(got - want).max()
+        worst = max(worst, err)
+        assert err <= G.TOL[dt], (h, err)
+        lerr = np.abs(lse[h, :n] - l[perm_q[h]]).max()
+        assert lerr <= (1e-5 if dt == "f32" else 1e-3) * max(1.0, np.abs(l).max()), lerr
+    G.flush(f"  max abs err {worst:.3g}")
+
+
+@pytest.mark.parametrize("dt,d,cq,ck,n,k", CASES)
+@pytest.mark.parametrize("enable", [True, False])
+def test_compensation_parity(dt, d, cq, ck, n, k, enable):
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    G.flush(f"comp case dt={dt} d={d} cq={cq} ck={ck} n={n} k={k} enable={enable}")
+    Q, K, V, perm_q, perm_k, lists, k = _setup(dt, d, cq, ck, n, k, seed=3)
+    H = Q.shape[0]
+    p = ca.Problem(1, H, n, n, d, cq, ck, G.tdtype(dt))
+    tau = 1 / math.sqrt(d)
+    cq_n, ck_n = G.counts(n, cq), G.counts(n, ck)
+    # sparse part from the oracle, handed over in the GPU's storage precision
+    op = np.zeros((H, p.nq_pad, d), np.float32)
+    lse = np.zeros((H, p.nq_pad), np.float32)
+    kbar = np.zeros((H, p.nkc, d), np.float32)
+    vbar = np.zeros((H, p.nkc, d), np.float32)
+    want = []
+    for h in range(H):
+        o, l = ref.sparse_attention(Q[h], K[h], V[h], perm_q[h], cq_n, perm_k[h], ck_n, lists[h],
+                                    tau)
+        if dt == "bf16":
+            from synth import bf16_round
+            o = bf16_round(o.astype(np.float32)).astype(np.float64)
+        op[h, :n] = o[perm_q[h]]
+        lse[h, :n] = l[perm_q[h]]
+        kb = ref.centroids(K[h], perm_k[h], ck_n).astype(np.float32)
+        vb = ref.centroids(V[h], perm_k[h], ck_n).astype(np.float32)
+        kbar[h], vbar[h] = kb, vb
+        want.append(ref.compensate(Q[h], kb, vb, ck_n, perm_q[h], cq_n, lists[h], o,
+                                   lse[h, :n][np.argsort(perm_q[h])].astype(np.float64), tau,
+                                   enable))
+    tq = G.permuted_rows(Q, perm_q, cq, G.tdtype(dt))
+    out, lse_out = ca.compensate(p, tq, G.dev(kbar), G.dev(vbar),
+                                 G.dev(np.stack([ck_n] * H), torch.int32),
+                                 G.dev(lists, torch.int32), k, G.dev(op, G.tdtype(dt)),
+                                 G.dev(lse), G.dev(perm_q, torch.int32), enable=enable,
+                                 want_lse=True)
+    torch.cuda.synchronize()
+    out, lse_out = G.host(out)[0], G.host(lse_out)
+    for h in range(H):
+        o_w, l_w = want[h]
+        err = np.abs(out[h] - o_w).max()
+        assert err <= G.TOL[dt], (h, err)
+        assert np.abs(lse_out[h] - l_w).max() <= 1e-4 * max(1.0, np.abs(l_w).max())
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_all_kept_equals_dense(dt):
+    """Every key cluster selected: the two calls give dense attention."""
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    d, c, n = 64, 64, 1000
+    Q, K, V = mixture_inputs(11, 1, n, d, dt, centres=8, sigma=0.4)
+    rng = np.random.default_rng(5)
+    perm_q = rng.permutation(n)[None].astype(np.int32)
+    perm_k = rng.permutation(n)[None].astype(np.int32)
+    p = ca.Problem(1, 1, n, n, d, c, c, G.tdtype(dt))
+    k = p.nkc
+    lists = np.arange(k, dtype=np.int32)[None, None].repeat(p.nqc, 1)
+    tq = G.permuted_rows(Q, perm_q, c, G.tdtype(dt))
+    cnt = G.dev(G.counts(n, c)[None], torch.int32)
+    L = G.dev(lists, torch.int32)
+    op, lse = ca.block_sparse_attn(p, tq, G.permuted_rows(K, perm_k, c, G.tdtype(dt)),
+                                   G.value_tiles(V, perm_k, c, G.tdtype(dt)), cnt, L, k)
+    kbar = np.zeros((1, p.nkc, d), np.float32)
+    out, _ = ca.compensate(p, tq, G.dev(kbar), G.dev(kbar), cnt, L, k, op, lse,
+                           G.dev(perm_q, torch.int32))
+    torch.cuda.synchronize()
+    o, _ = ref.dense_attention(Q[0], K[0], V[0], 1 / 8)
+    assert np.abs(G.host(out)[0, 0] - o).max() <= G.TOL[dt]

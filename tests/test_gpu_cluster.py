@@ -1,0 +1,147 @@
+"""GPU parity of ca_cluster.
+
+* Raw-coordinate mode: the permutation is compared end to end with the
+  oracle's split of the same inputs, bit for bit.
+* PCA / metric modes: the split coordinates are exported; the permutation must
+  equal the oracle's split of exactly those coordinates, and the coordinates
+  themselves must satisfy the properties the paper gives for the split spaces
+  (metric distances, unit-norm query representation, decorrelated and
+  descending principal coordinates with non-negative means) to fp32 accuracy.
+* Permuted copies, value tiles, counts, cluster ids and centroids are checked
+  against the permutation.
+"""
+import numpy as np
+import pytest
+
+from oracle import ref
+from synth import mixture_inputs
+
+pytestmark = pytest.mark.gpu
+
+SPLIT_CASES = [
+    # dtype, n, d, c, transform
+    ("f32", 1024, 64, 64, "none"),
+    ("bf16", 1000, 64, 64, "none"),
+    ("bf16", 5000, 32, 16, "none"),
+    ("bf16", 20000, 64, 128, "none"),
+    ("f32", 9000, 16, 32, "none"),
+    ("bf16", 3001, 128, 64, "none"),
+    ("f32", 1024, 64, 64, "pca"),
+    ("bf16", 6000, 64, 128, "pca"),
+    ("f32", 1024, 64, 64, "metric"),
+    ("bf16", 20000, 64, 128, "metric"),
+    ("bf16", 12345, 128, 64, "metric"),
+    ("bf16", 100, 64, 128, "metric"),
+]
+
+
+def _run(dt, n, d, c, xf, seed=0, heads=2, layout="bhnd"):
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    Q, K, V = mixture_inputs(seed, heads, n, d, dt, centres=12, sigma=0.5)
+    p = ca.Problem(1, heads, n, n, d, c, c, G.tdtype(dt), xf, layout)
+    if layout == "bhnd":
+        tq, tk, tv = (G.dev(x[None], G.tdtype(dt)) for x in (Q, K, V))
+    else:
+        tq, tk, tv = (G.dev(x[None].transpose(0, 2, 1, 3), G.tdtype(dt)) for x in (Q, K, V))
+    r = ca.cluster(p, tq, tk, tv, export_y=True)
+    torch.cuda.synchronize()
+    return Q, K, V, p, {k: v.cpu() for k, v in r.items()}
+
+
+def _check_copies(X, perm, cnt, cent, xp, c, dt):
+    from tests import gpu_util as G
+    n = X.shape[0]
+    assert cnt.tolist() == G.counts(n, c).tolist()
+    xp = xp.float().numpy()
+    assert np.array_equal(xp[:n], X[perm].astype(np.float32))
+    assert (xp[n:] == 0).all()
+    want = ref.centroids(X, perm, cnt)
+    assert np.abs(cent.numpy() - want).max() <= 1e-5 * max(1.0, np.abs(want).max())
+
+
+@pytest.mark.parametrize("dt,n,d,c,xf", SPLIT_CASES)
+def test_cluster_parity(dt, n, d, c, xf):
+    from tests import gpu_util as G
+    G.flush(f"cluster case dt={dt} n={n} d={d} c={c} xf={xf}")
+    Q, K, V, p, r = _run(dt, n, d, c, xf)
+    for h in range(Q.shape[0]):
+        yq = r["yq"][h].numpy().astype(np.float64)
+        yk = r["yk"][h].numpy().astype(np.float64)
+        if xf == "none":
+            assert np.array_equal(yq, Q[h]) and np.array_equal(yk, K[h])
+        pq, cidq, cntq = ref.split(yq, c)
+        pk, cidk, cntk = ref.split(yk, c)
+        assert np.array_equal(r["perm_q"][h].numpy(), pq), "query permutation"
+        assert np.array_equal(r["perm_k"][h].numpy(), pk), "key permutation"
+        assert np.array_equal(r["cid_q"][h].numpy(), cidq)
+        assert np.array_equal(r["cid_k"][h].numpy(), cidk)
+        _check_copies(Q[h], pq, r["count_q"][h], r["cent_q"][h], r["qp"][h], c, dt)
+        _check_copies(K[h], pk, r["count_k"][h], r["cent_k"][h], r["kp"][h], c, dt)
+        # value tiles follow the key permutation, transposed per cluster
+        nkc = p.nkc
+        rows = np.zeros((nkc * c, d))
+        rows[:n] = V[h][pk]
+        tiles = rows.reshape(nkc, c, d).transpose(0, 2, 1)
+        assert np.array_equal(r["vp"][h].float().numpy(), tiles.astype(np.float32))
+        wantv = ref.centroids(V[h], pk, cntk)
+        assert np.abs(r["cent_v"][h].numpy() - wantv).max() <= 1e-5 * max(1, np.abs(wantv).max())
+        if xf != "none":
+            _check_split_space(Q[h], K[h], yq, yk, xf)
+
+
+def _check_split_space(Q, K, yq, yk, xf):
+    """Properties of the split coordinates that do not depend on the
+    eigensolver's basis choice."""
+    rtol = 2e-4
+    for Y in (yq, yk):
+        C = np.cov(Y.T, bias=True)
+        scale = np.abs(C).max()
+        off = C - np.diag(np.diag(C))
+        assert np.abs(off).max() <= 5e-4 * scale, "decorrelated"
+        dg = np.diag(C)
+        assert (np.diff(dg) <= 1e-4 * scale).all(), "descending variances"
+        assert (Y.mean(axis=0) >= -1e-4 * np.sqrt(scale)).all(), "oriented"
+    rng = np.random.default_rng(0)
+    pairs = rng.integers(0, len(K), size=(200, 2))
+    if xf == "metric":
+        for a, b in pairs:
+            want = ((Q @ (K[a] - K[b])) ** 2).mean()
+            got = ((yk[a] - yk[b]) ** 2).sum()
+            assert abs(got - want) <= rtol * ((yk[a] ** 2).sum() + (yk[b] ** 2).sum()) + 1e-9
+        R = ref.query_representation(Q, K)
+        assert np.abs((yq * yq).sum(axis=1) - (R * R).sum(axis=1)).max() <= 1e-4
+        G1 = yq[pairs[:, 0]] * yq[pairs[:, 1]]
+        G2 = R[pairs[:, 0]] * R[pairs[:, 1]]
+        assert np.abs(G1.sum(axis=1) - G2.sum(axis=1)).max() <= 1e-4
+    else:
+        for X, Y in ((Q, yq), (K, yk)):
+            for a, b in pairs:
+                want = ((X[a] - X[b]) ** 2).sum()
+                got = ((Y[a] - Y[b]) ** 2).sum()
+                assert abs(got - want) <= rtol * ((X[a] ** 2).sum() + (X[b] ** 2).sum()) + 1e-9
+
+
+def test_layout_bnhd_matches_bhnd():
+    from tests import gpu_util as G
+    Q, K, V, p, r1 = _run("bf16", 3000, 64, 64, "metric", layout="bhnd")
+    _, _, _, _, r2 = _run("bf16", 3000, 64, 64, "metric", layout="bnhd")
+    for key in ("perm_q", "perm_k", "qp", "kp", "vp", "cent_q", "cent_k", "yq", "yk"):
+        assert np.array_equal(r1[key].float().numpy(), r2[key].float().numpy()), key
+
+
+def test_cluster_deterministic():
+    _, _, _, _, r1 = _run("bf16", 20000, 64, 128, "metric", seed=4)
+    _, _, _, _, r2 = _run("bf16", 20000, 64, 128, "metric", seed=4)
+    for key in r1:
+        assert np.array_equal(r1[key].float().numpy(), r2[key].float().numpy()), key
+
+
+def test_single_cluster_and_tiny():
+    """n <= c: one cluster, identity order; n = 1."""
+    for n in (1, 37, 64):
+        Q, K, V, p, r = _run("f32", n, 16, 64, "pca", seed=n)
+        for h in range(2):
+            assert r["perm_q"][h].tolist() == list(range(n))
+            assert r["count_k"][h].tolist() == [n]
