@@ -1,0 +1,162 @@
+#!/usr/bin/env python3
+"""Throughput of the ClusterAttention hot path on one MI355X.
+
+One step = one whole layer: ca_cluster -> ca_select -> ca_block_sparse_attn ->
+ca_compensate over all heads of the tabular-attention workload (batch 1, 8
+heads, 65,536 tokens, d = 64, bf16, clusters of 128, top 1/8 of key
+clusters, compensation on), inputs resident in HBM.
+
+Reported value: dense-equivalent attention TFLOP/s = 4 * heads * N^2 * d /
+(end-to-end time per layer). Alongside: ms per layer, per-call ms from HIP
+events, the roofline position of the dominant kernel (block-sparse attention,
+bf16 MFMA) and the CPU oracle timed on one head.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+WORKLOAD = dict(cfg=2, name="tabular-8h-n65536-d64-bf16-c128-keep1/8", heads=8, n=65536, d=64,
+                c=128, keep=1 / 8)
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def time_oracle(Q, K, V, c, k):
+    """The oracle, as it stands, on one head of the workload (full pipeline)."""
+    from oracle import ref
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    t0 = time.perf_counter()
+    ref.forward(Q, K, V, c, c, k, "metric", True)
+    dt = time.perf_counter() - t0
+    return dt, threads
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: ClusterAttention's heads are independent, so a "
+              "multi-GPU layer shards heads with no communication; run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2608_26965_amd as ca
+    from synth import make_config
+
+    W = WORKLOAD
+    H, n, d, c = W["heads"], W["n"], W["d"], W["c"]
+    Qh, Kh, Vh = make_config(W["cfg"])
+    dev = torch.device("cuda:0")
+    q = torch.from_numpy(Qh[None]).to(dev).to(torch.bfloat16)
+    k = torch.from_numpy(Kh[None]).to(dev).to(torch.bfloat16)
+    v = torch.from_numpy(Vh[None]).to(dev).to(torch.bfloat16)
+    p = ca.Problem(1, H, n, n, d, c, c, torch.bfloat16, "metric", "bhnd")
+    keep_k = ca.keep_to_k(W["keep"], p.nkc)
+    ws = ca.workspace(p, dev, keep_k)
+    out = torch.empty(p.shape(n), dtype=torch.bfloat16, device=dev)
+
+    def step(ev=None):
+        if ev:
+            ev[0].record()
+        r = ca.cluster(p, q, k, v, ws=ws)
+        if ev:
+            ev[1].record()
+        lists, _ = ca.select(p, r["cent_q"], r["cent_k"], keep_k, ws=ws)
+        if ev:
+            ev[2].record()
+        op, lse = ca.block_sparse_attn(p, r["qp"], r["kp"], r["vp"], r["count_k"], lists, keep_k)
+        if ev:
+            ev[3].record()
+        ca.compensate(p, r["qp"], r["cent_k"], r["cent_v"], r["count_k"], lists, keep_k, op, lse,
+                      r["perm_q"], out=out)
+        if ev:
+            ev[4].record()
+
+    for _ in range(args.warmup):
+        step()
+    # HIP events on the stream the calls are enqueued on (torch's current
+    # stream), one set per step, read back after the timed region.
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(evs[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / args.steps
+    calls = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(4)] for e in evs])
+    call_ms = calls.mean(axis=0)
+
+    f_dense = 4.0 * H * n * n * d
+    value = f_dense / (ms_step * 1e-3) / 1e12
+    f_attn = 4.0 * d * c * c * keep_k * p.nqc * H
+    attn_tflops = f_attn / (call_ms[2] * 1e-3) / 1e12
+    f_comp = 4.0 * d * p.nq_pad * p.nkc * H
+    rec = {
+        "metric": "dense-equivalent attention TFLOP/s + end-to-end ms/layer (clustering incl.)",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": W["name"], "batch": 1, "heads": H, "seq_len": n, "head_dim": d,
+                   "cluster_size": c, "keep": W["keep"], "kept_clusters": keep_k,
+                   "transform": "metric", "compensation": True},
+        "breakdown_ms": {"cluster": round(call_ms[0], 4), "select": round(call_ms[1], 4),
+                         "block_sparse_attn": round(call_ms[2], 4),
+                         "compensate": round(call_ms[3], 4)},
+        "roofline": {"kernel": "attn_bf16_kernel<64,128,128>", "bound": "mfma",
+                     "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None},
+        "compensate_tflops": round(f_comp / (call_ms[3] * 1e-3) / 1e12, 2),
+    }
+    if not args.no_cpu_baseline:
+        t_head, threads = time_oracle(Qh[0], Kh[0], Vh[0], c, keep_k)
+        rec["cpu_baseline"] = {
+            "value": round(4.0 * n * n * d / t_head / 1e12, 5), "unit": "TFLOP/s",
+            "cores": threads, "kind": "oracle",
+            "sample": f"head 0 of {H}, full pipeline (clustering, selection, sparse attention, "
+                      f"compensation), fp64 NumPy, {t_head:.1f} s; {cpu_model()}"}
+    print(json.dumps(rec))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,143 @@
+"""End-to-end GPU parity of the four calls chained, at the workloads' full
+per-head sizes (the tabular workload at all 8 heads, in the launch
+configuration the bench times).
+
+Per checked head: permutations bit-exact against the oracle's split of the
+exported split coordinates; lists bit-exact against the oracle's top-k of the
+exported scores; scores within fp32 rounding of the oracle's centroid scores;
+outputs of sampled query clusters within the tolerance against the oracle's
+compensated sparse attention given the GPU's permutation and lists."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import ref
+from synth import CONFIGS, keep_to_k, make_config
+
+pytestmark = pytest.mark.gpu
+
+
+def _pipeline(p, q, k, v, keep_k, comp=True):
+    import paper_2608_26965_amd as ca
+    r = ca.cluster(p, q, k, v, export_y=True)
+    lists, scores = ca.select(p, r["cent_q"], r["cent_k"], keep_k, export_scores=True)
+    op, lse = ca.block_sparse_attn(p, r["qp"], r["kp"], r["vp"], r["count_k"], lists, keep_k)
+    out, lse_out = ca.compensate(p, r["qp"], r["cent_k"], r["cent_v"], r["count_k"], lists, keep_k,
+                                 op, lse, r["perm_q"], enable=comp, want_lse=True)
+    return r, lists, scores, out, lse_out
+
+
+def _check_head(Q, K, V, r, lists, scores, out, h, c, k, dt, nsample, comp, seed):
+    from tests import gpu_util as G
+    n, d = Q.shape
+    tau = 1 / math.sqrt(d)
+    yq = r["yq"][h].double().cpu().numpy()
+    yk = r["yk"][h].double().cpu().numpy()
+    perm_q = r["perm_q"][h].cpu().numpy()
+    perm_k = r["perm_k"][h].cpu().numpy()
+    assert np.array_equal(perm_q, ref.split(yq, c)[0]), "query permutation"
+    assert np.array_equal(perm_k, ref.split(yk, c)[0]), "key permutation"
+    cq_n, ck_n = G.counts(n, c), G.counts(n, c)
+    S = scores[h].double().cpu().numpy()
+    L = lists[h].cpu().numpy()
+    assert np.array_equal(L, ref.topk(S, k)), "lists"
+    qbar = ref.centroids(Q, perm_q, cq_n)
+    kbar = ref.centroids(K, perm_k, ck_n)
+    vbar = ref.centroids(V, perm_k, ck_n)
+    S_or = ref.centroid_scores(qbar, kbar)
+    assert np.abs(S - S_or).max() <= 1e-4 * max(1.0, np.abs(S_or).max()), "scores"
+    rng = np.random.default_rng(seed)
+    nqc = len(cq_n)
+    sample = np.unique(np.concatenate([[nqc - 1], rng.choice(nqc, min(nsample, nqc), replace=False)]))
+    mem = ref.cluster_members(perm_q, cq_n)
+    rows = np.concatenate([mem[a] for a in sample])
+    sub_counts = cq_n[sample]
+    sub_perm = np.arange(len(rows))
+    o_s, l_s = ref.sparse_attention(Q[rows], K, V, sub_perm, sub_counts, perm_k, ck_n, L[sample],
+                                    tau)
+    o, l = ref.compensate(Q[rows], kbar, vbar, ck_n, sub_perm, sub_counts, L[sample], o_s, l_s,
+                          tau, comp)
+    got = out[h][rows]
+    err = np.abs(got - o).max()
+    assert err <= G.TOL[dt], f"head {h}: output error {err}"
+    return err
+
+
+def _run_config(cid, heads, c, keep, comp=True, check_heads=None, nsample=12):
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    cfg = CONFIGS[cid]
+    G.flush(f"e2e config {cid} heads={len(heads)} c={c} keep={keep} comp={comp}")
+    Q, K, V = make_config(cid, heads=heads)
+    H, n, d = Q.shape
+    dt = cfg.dtype
+    p = ca.Problem(1, H, n, n, d, c, c, G.tdtype(dt), "metric")
+    k = keep_to_k(keep, p.nkc)
+    tq, tk, tv = (G.dev(x[None], G.tdtype(dt)) for x in (Q, K, V))
+    r, lists, scores, out, lse = _pipeline(p, tq, tk, tv, k, comp)
+    torch.cuda.synchronize()
+    outh = G.host(out)[0]
+    worst = 0.0
+    for h in (check_heads if check_heads is not None else range(H)):
+        worst = max(worst, _check_head(Q[h], K[h], V[h], r, lists, scores, outh, h, c, k, dt,
+                                       nsample, comp, seed=cid * 100 + h))
+    G.flush(f"  worst sampled error {worst:.3g}")
+    return r, lists, out
+
+
+def test_small_fp32_config_full():
+    """The 1-head fp32 workload: every query cluster checked."""
+    _run_config(1, [0], 64, 0.25, nsample=16)
+
+
+def test_small_fp32_all_kept_is_dense():
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    Q, K, V = make_config(1)
+    n, d = Q.shape[1:]
+    p = ca.Problem(1, 1, n, n, d, 64, 64, torch.float32, "metric")
+    tq, tk, tv = (G.dev(x[None]) for x in (Q, K, V))
+    _, _, _, out, _ = _pipeline(p, tq, tk, tv, p.nkc)
+    torch.cuda.synchronize()
+    o, _ = ref.dense_attention(Q[0], K[0], V[0], 1 / 8)
+    assert np.abs(G.host(out)[0, 0] - o).max() <= 1e-5
+
+
+def test_tabular_bench_workload_all_heads():
+    """The benchmarked workload at full size, all 8 heads."""
+    _run_config(2, list(range(8)), 128, 1 / 8, check_heads=[0, 3, 7])
+
+
+@pytest.mark.parametrize("keep", [1 / 16, 1 / 4])
+def test_large_tabular_one_head(keep):
+    _run_config(3, [0], 128, keep, nsample=6)
+
+
+def test_video_480p_two_heads():
+    _run_config(4, [0, 1], 64, 1 / 4, nsample=8)
+
+
+@pytest.mark.parametrize("c,keep,comp", [(64, 1 / 16, True), (128, 1 / 4, False),
+                                         (128, 1 / 8, True)])
+def test_video_720p_one_head(c, keep, comp):
+    _run_config(5, [0], c, keep, comp=comp, nsample=8)
+
+
+def test_pipeline_deterministic():
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    Q, K, V = make_config(2, heads=[1, 2])
+    H, n, d = Q.shape
+    p = ca.Problem(1, H, n, n, d, 128, 128, torch.bfloat16, "metric")
+    tq, tk, tv = (G.dev(x[None], torch.bfloat16) for x in (Q, K, V))
+    a = _pipeline(p, tq, tk, tv, 64)
+    b = _pipeline(p, tq, tk, tv, 64)
+    torch.cuda.synchronize()
+    for x, y in zip(a[1:], b[1:]):
+        assert torch.equal(x, y)
+    for key in a[0]:
+        assert torch.equal(a[0][key], b[0][key]), key
