@@ -24,12 +24,8 @@ constexpr int kMaxC = 256;
 __device__ __forceinline__ float bf2f(bf16 x) {
   return __uint_as_float(((uint32_t)__builtin_bit_cast(uint16_t, x)) << 16);
 }
-// Round to nearest even (finite inputs).
-__device__ __forceinline__ bf16 f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return __builtin_bit_cast(bf16, (uint16_t)(u >> 16));
-}
+// Round to nearest even (the hardware conversion, v_cvt_pk_bf16_f32).
+__device__ __forceinline__ bf16 f2bf(float f) { return (bf16)f; }
 __device__ __forceinline__ float load_elem(const void* base, size_t idx, int dtype) {
   return dtype == CA_BF16 ? bf2f(((const bf16*)base)[idx]) : ((const float*)base)[idx];
 }

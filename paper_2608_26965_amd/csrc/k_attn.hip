@@ -7,6 +7,8 @@
 // queries. fp32: plain FMA, one thread per query.
 #include <math.h>
 
+#include <type_traits>
+
 #include "attn_tile.h"
 
 namespace ca {
@@ -15,6 +17,8 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
+// s_waitcnt immediate (gfx9 encoding) waiting for vmcnt = 0 only.
+constexpr int kVmcnt0 = 0x0F70;
 
 // Workgroup w of a 1-D grid runs on XCD w % 8. Renumber so that each XCD gets
 // one contiguous range of (head, query cluster) items: neighbouring query
@@ -26,23 +30,40 @@ __device__ __forceinline__ int xcd_remap(int wg, int total) {
   return xcd < rem ? xcd * (per + 1) + loc : rem * (per + 1) + (xcd - rem) * per + loc;
 }
 
+// Waves per SIMD the bf16 kernel is compiled for: two when the double-buffered
+// tiles of two workgroups fit in LDS (so MFMA of one wave overlaps the softmax
+// of another), else one.
+// Workgroups per CU the bf16 kernel is compiled for: as many double-buffered
+// tile pairs as fit in LDS (so the MFMA of one wave overlaps the softmax of
+// another), capped at two waves per SIMD.
 template <int D, int CQ, int CK>
-__global__ __launch_bounds__(CQ * 2) void attn_bf16_kernel(
+constexpr int attn_blocks_per_cu() {
+  constexpr int by_lds = (160 * 1024) / (8 * D * CK);
+  constexpr int by_waves = 8 / (CQ / 32);
+  return by_lds < by_waves ? (by_lds < 1 ? 1 : by_lds) : by_waves;
+}
+
+template <int D, int CQ, int CK>
+__global__ __launch_bounds__(CQ * 2, (attn_blocks_per_cu<D, CQ, CK>())) void attn_bf16_kernel(
     const bf16* __restrict__ qp, const bf16* __restrict__ kp, const bf16* __restrict__ vp,
     const int32_t* __restrict__ count_k, const int32_t* __restrict__ lists, int nqc, int nkc,
     int k, float sl2, bf16* __restrict__ op, float* __restrict__ lse, int total) {
   constexpr int NW = CQ / 32;
-  constexpr int T = NW * 64;
   constexpr int MT = CK / 32;
   constexpr int KS = D / 16;
   constexpr int DT = D / 32;
-  constexpr int KP = D + 8;   // LDS pitch of a K row (bf16), +16 bytes against bank conflicts
-  constexpr int VP = CK + 8;  // LDS pitch of a V^T row
-  constexpr int KCH = CK * D / 8 / T;  // 16-byte chunks per thread per tile
-  constexpr int VCH = D * CK / 8 / T;
-  static_assert(KCH * T * 8 == CK * D && VCH * T * 8 == D * CK, "tile split");
-  __shared__ __attribute__((aligned(16))) bf16 Ks[2][CK * KP];
-  __shared__ __attribute__((aligned(16))) bf16 Vs[2][D * VP];
+  constexpr int KROW = 2 * D;   // bytes per K row
+  constexpr int VROW = 2 * CK;  // bytes per V^T row
+  constexpr int KBYTES = CK * KROW, VBYTES = D * VROW;
+  constexpr int STAGE = KBYTES + VBYTES;
+  constexpr int KLD = KBYTES / 1024 / NW;  // direct-to-LDS instructions per wave
+  constexpr int VLD = VBYTES / 1024 / NW;
+  constexpr int NL = KLD + VLD;
+  static_assert(KLD * 1024 * NW == KBYTES && VLD * 1024 * NW == VBYTES, "tile split");
+  // Rescale the running output only when a query's maximum logit grows by more
+  // than 2^8 (log2 units): exponentials then stay below 256, exact in fp32.
+  constexpr float kLazy = 8.0f;
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
   const int item = xcd_remap(blockIdx.x, total);
   const int bh = item / nqc, a = item - bh * nqc;
@@ -54,34 +75,38 @@ __global__ __launch_bounds__(CQ * 2) void attn_bf16_kernel(
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks)
     qreg[ks] = *(const bf16x8*)(qp + qrow * D + 16 * ks + 8 * h);
+  // Retire the query loads here (a wait the compiler sees), so that no
+  // compiler-inserted vmcnt wait lands inside the loop, where it would also
+  // wait for the in-flight copy of the next tile.
+  __builtin_amdgcn_s_waitcnt(kVmcnt0);
 
   const int32_t* lst = lists + ((size_t)bh * nqc + a) * k;
+  const int32_t* cnth = count_k + (size_t)bh * nkc;
   auto tile_id = [&](int t) {
     int b = lst[t];
     return b < 0 ? 0 : (b >= nkc ? nkc - 1 : b);
   };
-
-  uint4 kreg[KCH], vreg[VCH];
-  auto fetch = [&](int b) {
+  const TileCopy<KROW, KLD, NW> kcopy(w, lane);
+  const TileCopy<VROW, VLD, NW> vcopy(w, lane);
+  const uint32_t lds0 = lds_addr(smem);
+  auto issue = [&](int b, int stage) {
     const bf16* kt = kp + ((size_t)bh * nk_pad + (size_t)b * CK) * D;
     const bf16* vt = vp + ((size_t)bh * nkc + b) * (size_t)D * CK;
-#pragma unroll
-    for (int i = 0; i < KCH; ++i) kreg[i] = ((const uint4*)kt)[tid + i * T];
-#pragma unroll
-    for (int i = 0; i < VCH; ++i) vreg[i] = ((const uint4*)vt)[tid + i * T];
+    kcopy.issue(kt, lds0 + stage * STAGE, w);
+    vcopy.issue(vt, lds0 + stage * STAGE + KBYTES, w);
   };
-  auto stash = [&](int buf) {
+  // Loop-invariant LDS read offsets (rows r and r + 32 share the swizzle key).
+  int koff[KS];
+  {
+    const int row = kswz(l32);
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      int c = tid + i * T, row = c / (D / 8), c8 = c % (D / 8);
-      *(uint4*)&Ks[buf][row * KP + c8 * 8] = kreg[i];
-    }
+    for (int kk = 0; kk < KS; ++kk) koff[kk] = swz_off<KROW>(row, 2 * kk + h);
+  }
+  int voff[MT][2];
 #pragma unroll
-    for (int i = 0; i < VCH; ++i) {
-      int c = tid + i * T, row = c / (CK / 8), c8 = c % (CK / 8);
-      *(uint4*)&Vs[buf][row * VP + c8 * 8] = vreg[i];
-    }
-  };
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) voff[mt][s2] = swz_off<VROW>(l32, 4 * mt + 2 * s2 + h);
 
   f32x16 oacc[DT];
 #pragma unroll
@@ -90,25 +115,26 @@ __global__ __launch_bounds__(CQ * 2) void attn_bf16_kernel(
     for (int r = 0; r < 16; ++r) oacc[dt][r] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
-  fetch(tile_id(0));
-  stash(0);
-  __syncthreads();
-
-  for (int t = 0; t < k; ++t) {
-    const int cur = t & 1;
-    if (t + 1 < k) fetch(tile_id(t + 1));
-    const int cnt = count_k[(size_t)bh * nkc + tile_id(t)];
+  auto body = [&](auto stage_tag, int t) {
+    constexpr int S = decltype(stage_tag)::value;
+    if (t + 1 < k)
+      wait_vmcnt<NL>();
+    else
+      wait_vmcnt<0>();
+    raw_barrier();
+    const char* ks = smem + S * STAGE;
+    const char* vs = ks + KBYTES;
+    const int cnt = cnth[tile_id(t)];
 
     f32x16 sacc[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) sacc[mt][r] = 0.f;
-      const bf16* krow = &Ks[cur][(32 * mt + kswz(l32)) * KP + 8 * h];
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        bf16x8 av = *(const bf16x8*)(krow + 16 * ks);
-        sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qreg[ks], sacc[mt], 0, 0, 0);
+      for (int kk = 0; kk < KS; ++kk) {
+        const bf16x8 av = *(const bf16x8*)(ks + 32 * mt * KROW + koff[kk]);
+        sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qreg[kk], sacc[mt], 0, 0, 0);
       }
     }
     if (cnt < CK) {
@@ -123,40 +149,50 @@ __global__ __launch_bounds__(CQ * 2) void attn_bf16_kernel(
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[mt][r]);
-    mx = fmaxf(mx, wave_xor32(mx));
-    const float m_new = fmaxf(m_run, mx * sl2);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    mx = fmaxf(mx, wave_xor32(mx)) * sl2;
+    if (__builtin_amdgcn_ballot_w64(mx > m_run + kLazy)) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
+      m_run = m_new;
+    }
     float lsum = 0.f;
     bf16x8 pb[MT][2];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int s = 0; s < 2; ++s) {
+      for (int s2 = 0; s2 < 2; ++s2) {
         float pv[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          pv[j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[mt][8 * s + j], sl2, -m_new));
-          lsum += pv[j];
-        }
-        pb[mt][s] = pack8(pv);
+        for (int j = 0; j < 8; ++j)
+          pv[j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[mt][8 * s2 + j], sl2, -m_run));
+        pb[mt][s2] = pack8(pv);
+        lsum = sum8(pb[mt][s2], lsum);
       }
-    l_run = l_run * alpha + lsum;
-    m_run = m_new;
+    l_run += lsum;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
-      const bf16* vrow = &Vs[cur][(32 * dt + l32) * VP + 8 * h];
+    for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          bf16x8 av = *(const bf16x8*)(vrow + 32 * mt + 16 * s);
-          oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[mt][s], oacc[dt], 0, 0, 0);
+        for (int s2 = 0; s2 < 2; ++s2) {
+          const bf16x8 av = *(const bf16x8*)(vs + 32 * dt * VROW + voff[mt][s2]);
+          oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[mt][s2], oacc[dt], 0, 0, 0);
         }
-    }
-    if (t + 1 < k) stash(cur ^ 1);
-    __syncthreads();
+    wait_lgkm();
+    raw_barrier();  // every wave is done with this stage
+    if (t + 2 < k) issue(tile_id(t + 2), S);
+  };
+
+  issue(tile_id(0), 0);
+  if (k > 1) issue(tile_id(1), 1);
+  for (int t = 0; t < k; t += 2) {
+    body(std::integral_constant<int, 0>{}, t);
+    if (t + 1 < k) body(std::integral_constant<int, 1>{}, t + 1);
   }
 
   const float l_tot = l_run + wave_xor32(l_run);
