@@ -126,6 +126,7 @@ void plan_workspace(const Prob& P, Workspace* W) {
   W->vecs = take(BH * kVecs * d * 4);
   W->inv_q = take(BH * P.nq * 4);
   W->qn_part = take(BH * W->nblk_mom * (d * d + d) * 4);
+  W->wops = take(BH * 3 * 2 * d * d * 2);
   W->node_state = take(2 * BH * W->max_big_nodes * kNodeInts * 4);
   W->hist = take(2 * BH * W->max_big_nodes * kRadixBins * 4);
   W->chunk_cnt = take(2 * BH * W->max_big_nodes * W->max_chunks * 2 * 4);

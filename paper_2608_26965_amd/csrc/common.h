@@ -101,6 +101,7 @@ struct Workspace {
   size_t vecs;              // fp32 [BH][kVecs][d]
   size_t inv_q;             // fp32 [BH][nq]
   size_t qn_part;           // fp32 [BH][nblk_q][d*d + d]
+  size_t wops;              // bf16 [BH][3][2][d][d] MFMA operands (transposed hi/lo)
   size_t node_state;        // int32 [2][BH][max_big_nodes][kNodeInts]
   size_t hist;              // uint32 [2][BH][max_big_nodes][kRadixBins]
   size_t chunk_cnt;         // int32 [2][BH][max_big_nodes][max_chunks][2]

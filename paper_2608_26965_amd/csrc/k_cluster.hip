@@ -18,6 +18,7 @@
 // order and no contraction, so it is reproducible bit for bit.
 #include <math.h>
 
+#include "attn_tile.h"
 #include "common.h"
 
 namespace ca {
@@ -50,6 +51,7 @@ struct Ctx {
   float* inv_q;     // [BH][nq]
   float* mom_part;  // [2][BH][nblk][d*d + d]
   float* qn_part;   // [BH][nblk][d*d + d]
+  bf16* wops;       // [BH][3][2][d][d] transposed hi/lo bf16 operands
   int32_t* idx0;
   int32_t* idx1;
   uint32_t* keys;
@@ -61,11 +63,16 @@ struct Ctx {
 
 // Matrix slots
 enum { M_A0 = 0, M_CK = 1, M_E0 = 2, M_EK = 3, M_C2 = 4, M_C3 = 5, M_TK = 6, M_TQ = 7 };
+// Operand slots (MFMA A operands W^T, split in bf16 hi + lo)
+enum { O_FK = 0, O_TK = 1, O_TQ = 2 };
 // Vector slots
 enum { V_L0 = 0, V_LK = 1, V_MUQ = 2, V_MUK = 3, V_L2 = 4, V_L3 = 5, V_MUR = 6, V_KQ = 7 };
 
 __device__ __forceinline__ float* mat(const Ctx& C, int bh, int slot) {
   return C.mats + ((size_t)bh * kMats + slot) * C.d * C.d;
+}
+__device__ __forceinline__ bf16* wop(const Ctx& C, int bh, int slot) {
+  return C.wops + ((size_t)bh * 3 + slot) * 2 * C.d * C.d;
 }
 __device__ __forceinline__ float* vec(const Ctx& C, int bh, int slot) {
   return C.vecs + ((size_t)bh * kVecs + slot) * C.d;
@@ -153,6 +160,19 @@ __global__ __launch_bounds__(256) void moments_partial_kernel(Ctx C) {
   if (threadIdx.x < d) out[d * d + threadIdx.x] = csum;
 }
 
+// Sum of nb partials p[0], p[stride], ... in fp64: eight independent running
+// sums (so the loads overlap), combined in a fixed order (deterministic).
+__device__ __forceinline__ double sum_partials(const float* p, size_t stride, int nb) {
+  double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  int b = 0;
+  for (; b + 8 <= nb; b += 8) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc[u] += (double)p[(size_t)(b + u) * stride];
+  }
+  for (; b < nb; ++b) acc[b & 7] += (double)p[(size_t)b * stride];
+  return ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
+}
+
 // Reduces the partials of both sides of one head in fp64 and writes the
 // matrices the eigensolver starts from:
 //   queries: metric -> Q^T Q / n;  pca -> centred covariance of Q
@@ -167,8 +187,7 @@ __global__ __launch_bounds__(256) void moments_finish_kernel(Ctx C) {
     const double n = (double)S.n;
     __syncthreads();
     for (int t = threadIdx.x; t < d; t += 256) {
-      double s = 0.0;
-      for (int b = 0; b < C.nblk; ++b) s += (double)part[(size_t)b * (d * d + d) + d * d + t];
+      const double s = sum_partials(part + d * d + t, (size_t)(d * d + d), C.nblk);
       mu[t] = s / n;
       vec(C, bh, side == 0 ? V_MUQ : V_MUK)[t] = (float)(s / n);
     }
@@ -176,8 +195,7 @@ __global__ __launch_bounds__(256) void moments_finish_kernel(Ctx C) {
     const bool centred = side == 1 || C.xf == CA_XF_PCA;
     float* M = mat(C, bh, side == 0 ? M_A0 : M_CK);
     for (int e = threadIdx.x; e < d * d; e += 256) {
-      double s = 0.0;
-      for (int b = 0; b < C.nblk; ++b) s += (double)part[(size_t)b * (d * d + d) + e];
+      const double s = sum_partials(part + e, (size_t)(d * d + d), C.nblk);
       double v = s / n;
       if (centred) v -= mu[e / d] * mu[e % d];
       M[e] = (float)v;
@@ -199,115 +217,192 @@ struct EighJobs {
 };
 
 constexpr int kEP = kMaxD + 1;
+constexpr int kEighThreads = 512;
 
-__global__ __launch_bounds__(256) void eigh_kernel(Ctx C, EighJobs J) {
+// Round-robin pairing of m players at a step: pair k joins positions k and
+// m-1-k; position 0 is fixed and the others rotate by one place per step, so
+// every pair meets once per m-1 steps. Returns p < q.
+__device__ __forceinline__ void rr_pair(int k, int step, int m, int* p, int* q) {
+  int x = k - 1 + step;
+  x -= x >= m - 1 ? m - 1 : 0;
+  const int a = k == 0 ? 0 : 1 + x;
+  int y = m - 2 - k + step;
+  y -= y >= m - 1 ? m - 1 : 0;
+  const int b = 1 + y;
+  *p = a < b ? a : b;
+  *q = a < b ? b : a;
+}
+
+template <int DM>
+__global__ __launch_bounds__(kEighThreads) void eigh_kernel(Ctx C, EighJobs J) {
   extern __shared__ float esh[];
   float* A = esh;                       // [d][kEP]
   float* V = esh + kMaxD * kEP;         // [d][kEP]
   __shared__ float rc[kMaxD / 2 + 1], rs[kMaxD / 2 + 1];
-  __shared__ int rp[kMaxD / 2 + 1], rq[kMaxD / 2 + 1];
-  __shared__ float red[256];
+  __shared__ float red[2][kEighThreads / 64];
   __shared__ int sh_stop;
   const int bh = blockIdx.x, job = blockIdx.y, d = C.d, tid = threadIdx.x;
+  const int lane = tid & 63, wv = tid >> 6;
   const float* Min = mat(C, bh, J.in[job]);
-  for (int e = tid; e < d * d; e += 256) {
-    const int i = e / d, j = e % d;
-    A[i * kEP + j] = Min[e];
-    V[i * kEP + j] = i == j ? 1.f : 0.f;
-  }
+  for (int i = wv; i < d; i += kEighThreads / 64)
+    for (int j = lane; j < d; j += 64) {
+      A[i * kEP + j] = Min[i * d + j];
+      V[i * kEP + j] = i == j ? 1.f : 0.f;
+    }
   if (tid == 0) sh_stop = 0;
   const int m = (d + 1) & ~1;  // players (a phantom one when d is odd)
   const int np = m / 2;
-  for (int sweep = 0; sweep < 30; ++sweep) {
+  for (int sweep = 0; sweep < 40; ++sweep) {
     __syncthreads();
-    // convergence: off-diagonal mass relative to the total
+    // Convergence: off-diagonal mass relative to the total.
     float off = 0.f, tot = 0.f;
-    for (int e = tid; e < d * d; e += 256) {
-      const int i = e / d, j = e % d;
-      const float a = A[i * kEP + j];
-      tot += a * a;
-      if (i != j) off += a * a;
+    for (int i = wv; i < d; i += kEighThreads / 64)
+      for (int j = lane; j < d; j += 64) {
+        const float a = A[i * kEP + j];
+        tot += a * a;
+        if (i != j) off += a * a;
+      }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      off += __shfl_xor(off, o, 64);
+      tot += __shfl_xor(tot, o, 64);
     }
-    red[tid] = off;
-    __syncthreads();
-    for (int s = 128; s > 0; s >>= 1) {
-      if (tid < s) red[tid] += red[tid + s];
-      __syncthreads();
+    if (lane == 0) {
+      red[0][wv] = off;
+      red[1][wv] = tot;
     }
-    const float offs = red[0];
     __syncthreads();
-    red[tid] = tot;
-    __syncthreads();
-    for (int s = 128; s > 0; s >>= 1) {
-      if (tid < s) red[tid] += red[tid + s];
-      __syncthreads();
+    if (tid == 0) {
+      float so = 0.f, st = 0.f;
+      for (int i = 0; i < kEighThreads / 64; ++i) {
+        so += red[0][i];
+        st += red[1][i];
+      }
+      // Stop one sweep after the off-diagonal mass falls below (d * 2e-6)^2 of
+      // the total: above the fp32 rounding floor (about (d * eps)^2), and
+      // quadratic convergence makes the extra sweep reach that floor.
+      const float thr = (float)d * 2e-6f;
+      sh_stop = (so <= thr * thr * st) ? sh_stop + 1 : 0;
+      if (so == 0.f) sh_stop = 2;
     }
-    // Stop one sweep after the off-diagonal mass falls below 1e-11 of the total
-    // (quadratic convergence then reaches the fp32 rounding floor).
-    if (tid == 0) sh_stop = (offs <= 1e-11f * red[0]) ? sh_stop + 1 : 0;
     __syncthreads();
-    if (sh_stop >= 2 || offs == 0.f) break;
+    if (sh_stop >= 2) break;
     for (int step = 0; step < m - 1; ++step) {
       if (tid < np) {
-        auto player = [&](int pos) { return pos == 0 ? 0 : 1 + (pos - 1 + step) % (m - 1); };
-        int p = player(tid), q = player(m - 1 - tid);
-        if (p > q) {
-          int t = p;
-          p = q;
-          q = t;
-        }
-        float c = 1.f, s = 0.f;
+        int p, q;
+        rr_pair(tid, step, m, &p, &q);
+        float c = 1.f, sn = 0.f;
         if (q < d) {
-          const double apq = A[p * kEP + q];
-          if (apq != 0.0) {
-            const double app = A[p * kEP + p], aqq = A[q * kEP + q];
-            const double tau = (aqq - app) / (2.0 * apq);
-            const double t = (tau >= 0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
-            const double cc = 1.0 / sqrt(1.0 + t * t);
-            c = (float)cc;
-            s = (float)(t * cc);
+          const float apq = A[p * kEP + q];
+          if (apq != 0.f) {
+            const float app = A[p * kEP + p], aqq = A[q * kEP + q];
+            const float tau = (aqq - app) / (2.f * apq);
+            const float t = copysignf(1.f, tau) / (fabsf(tau) + sqrtf(1.f + tau * tau));
+            c = 1.f / sqrtf(1.f + t * t);
+            sn = t * c;
           }
         }
-        rp[tid] = p;
-        rq[tid] = q;
         rc[tid] = c;
-        rs[tid] = s;
+        rs[tid] = sn;
       }
       __syncthreads();
-      // A <- J^T A J, one 2x2 block per (row pair, column pair)
-      for (int e = tid; e < np * np; e += 256) {
-        const int k1 = e / np, k2 = e % np;
-        const int p1 = rp[k1], q1 = rq[k1], p2 = rp[k2], q2 = rq[k2];
-        const float c1 = rc[k1], s1 = rs[k1], c2 = rc[k2], s2 = rs[k2];
-        const bool hq1 = q1 < d, hq2 = q2 < d;
-        const float a = A[p1 * kEP + p2];
-        const float b = hq2 ? A[p1 * kEP + q2] : 0.f;
-        const float cc = hq1 ? A[q1 * kEP + p2] : 0.f;
-        const float dd = (hq1 && hq2) ? A[q1 * kEP + q2] : 0.f;
-        // rows: p' = c p - s q, q' = s p + c q
-        const float r00 = c1 * a - s1 * cc, r01 = c1 * b - s1 * dd;
-        const float r10 = s1 * a + c1 * cc, r11 = s1 * b + c1 * dd;
-        // columns
-        float n00 = c2 * r00 - s2 * r01, n01 = s2 * r00 + c2 * r01;
-        float n10 = c2 * r10 - s2 * r11, n11 = s2 * r10 + c2 * r11;
-        if (k1 == k2) {
-          n01 = 0.f;
-          n10 = 0.f;
-        }
-        A[p1 * kEP + p2] = n00;
-        if (hq2) A[p1 * kEP + q2] = n01;
-        if (hq1) A[q1 * kEP + p2] = n10;
-        if (hq1 && hq2) A[q1 * kEP + q2] = n11;
+      // This thread's items: blocks (k1, k2), k1 = (tid >> 5) + 16 a, k2 = (tid & 31) + 32 b,
+      // kept when k1 <= k2 < np; value rows i = lane for pairs kk = wv + 8 c.
+      constexpr int KA = DM / 2 / 16, KB = DM / 2 / 32 > 0 ? DM / 2 / 32 : 1, KV = DM / 2 / 8;
+      int bp1[KA], bq1[KA], bp2[KB], bq2[KB];
+      float bc1[KA], bs1[KA], bc2[KB], bs2[KB];
+#pragma unroll
+      for (int a1 = 0; a1 < KA; ++a1) {
+        const int k1 = (tid >> 5) + 16 * a1;
+        rr_pair(k1 < np ? k1 : 0, step, m, &bp1[a1], &bq1[a1]);
+        bc1[a1] = k1 < np ? rc[k1] : 1.f;
+        bs1[a1] = k1 < np ? rs[k1] : 0.f;
       }
-      // V <- V J
-      for (int e = tid; e < d * np; e += 256) {
-        const int i = e / np, kk = e % np;
-        const int p = rp[kk], q = rq[kk];
-        if (q >= d) continue;
-        const float c = rc[kk], s = rs[kk];
-        const float vp = V[i * kEP + p], vq = V[i * kEP + q];
-        V[i * kEP + p] = c * vp - s * vq;
-        V[i * kEP + q] = s * vp + c * vq;
+#pragma unroll
+      for (int b2 = 0; b2 < KB; ++b2) {
+        const int k2 = (tid & 31) + 32 * b2;
+        rr_pair(k2 < np ? k2 : 0, step, m, &bp2[b2], &bq2[b2]);
+        bc2[b2] = k2 < np ? rc[k2] : 1.f;
+        bs2[b2] = k2 < np ? rs[k2] : 0.f;
+      }
+      float va[KA][KB][4];
+#pragma unroll
+      for (int a1 = 0; a1 < KA; ++a1)
+#pragma unroll
+        for (int b2 = 0; b2 < KB; ++b2) {
+          const int k1 = (tid >> 5) + 16 * a1, k2 = (tid & 31) + 32 * b2;
+          const bool live = k1 <= k2 && k2 < np;
+          const int p1 = bp1[a1], q1 = bq1[a1], p2 = bp2[b2], q2 = bq2[b2];
+          const bool hq1 = q1 < d, hq2 = q2 < d;
+          va[a1][b2][0] = live ? A[p1 * kEP + p2] : 0.f;
+          va[a1][b2][1] = live && hq2 ? A[p1 * kEP + q2] : 0.f;
+          va[a1][b2][2] = live && hq1 ? A[q1 * kEP + p2] : 0.f;
+          va[a1][b2][3] = live && hq1 && hq2 ? A[q1 * kEP + q2] : 0.f;
+        }
+      float vv[KV][2];
+      int vpq[KV][2];
+      float vcs[KV][2];
+#pragma unroll
+      for (int cc = 0; cc < KV; ++cc) {
+        const int kk = wv + 8 * cc;
+        int p = 0, q = 0;
+        rr_pair(kk < np ? kk : 0, step, m, &p, &q);
+        const bool live = kk < np && q < d && lane < d;
+        vpq[cc][0] = live ? p : -1;
+        vpq[cc][1] = q;
+        vcs[cc][0] = kk < np ? rc[kk] : 1.f;
+        vcs[cc][1] = kk < np ? rs[kk] : 0.f;
+        vv[cc][0] = live ? V[lane * kEP + p] : 0.f;
+        vv[cc][1] = live ? V[lane * kEP + q] : 0.f;
+      }
+      // (rows of value pairs beyond lane 63 when d > 64)
+      float vv2[KV][2];
+#pragma unroll
+      for (int cc = 0; cc < KV; ++cc) {
+        const bool live = vpq[cc][0] >= 0 && lane + 64 < d;
+        vv2[cc][0] = live ? V[(lane + 64) * kEP + vpq[cc][0]] : 0.f;
+        vv2[cc][1] = live ? V[(lane + 64) * kEP + vpq[cc][1]] : 0.f;
+      }
+#pragma unroll
+      for (int a1 = 0; a1 < KA; ++a1)
+#pragma unroll
+        for (int b2 = 0; b2 < KB; ++b2) {
+          const int k1 = (tid >> 5) + 16 * a1, k2 = (tid & 31) + 32 * b2;
+          if (!(k1 <= k2 && k2 < np)) continue;
+          const int p1 = bp1[a1], q1 = bq1[a1], p2 = bp2[b2], q2 = bq2[b2];
+          const float c1 = bc1[a1], s1 = bs1[a1], c2 = bc2[b2], s2 = bs2[b2];
+          const bool hq1 = q1 < d, hq2 = q2 < d;
+          const float a = va[a1][b2][0], b = va[a1][b2][1], cc = va[a1][b2][2], dd = va[a1][b2][3];
+          const float r00 = c1 * a - s1 * cc, r01 = c1 * b - s1 * dd;
+          const float r10 = s1 * a + c1 * cc, r11 = s1 * b + c1 * dd;
+          float n00 = c2 * r00 - s2 * r01, n01 = s2 * r00 + c2 * r01;
+          float n10 = c2 * r10 - s2 * r11, n11 = s2 * r10 + c2 * r11;
+          if (k1 == k2) {
+            n01 = 0.f;
+            n10 = 0.f;
+          }
+          A[p1 * kEP + p2] = n00;
+          if (hq2) A[p1 * kEP + q2] = n01;
+          if (hq1) A[q1 * kEP + p2] = n10;
+          if (hq1 && hq2) A[q1 * kEP + q2] = n11;
+          if (k1 != k2) {
+            A[p2 * kEP + p1] = n00;
+            if (hq2) A[q2 * kEP + p1] = n01;
+            if (hq1) A[p2 * kEP + q1] = n10;
+            if (hq1 && hq2) A[q2 * kEP + q1] = n11;
+          }
+        }
+#pragma unroll
+      for (int cc = 0; cc < KV; ++cc) {
+        const int p = vpq[cc][0], q = vpq[cc][1];
+        if (p < 0) continue;
+        const float c = vcs[cc][0], sn = vcs[cc][1];
+        V[lane * kEP + p] = c * vv[cc][0] - sn * vv[cc][1];
+        V[lane * kEP + q] = sn * vv[cc][0] + c * vv[cc][1];
+        if (lane + 64 < d) {
+          V[(lane + 64) * kEP + p] = c * vv2[cc][0] - sn * vv2[cc][1];
+          V[(lane + 64) * kEP + q] = sn * vv2[cc][0] + c * vv2[cc][1];
+        }
       }
       __syncthreads();
     }
@@ -316,7 +411,7 @@ __global__ __launch_bounds__(256) void eigh_kernel(Ctx C, EighJobs J) {
   // sort descending (ties by index) and write
   float* vals = vec(C, bh, J.vals[job]);
   float* vecs = mat(C, bh, J.vecs[job]);
-  for (int i = tid; i < d; i += 256) {
+  for (int i = tid; i < d; i += kEighThreads) {
     const float li = A[i * kEP + i];
     int rank = 0;
     for (int j = 0; j < d; ++j) {
@@ -326,6 +421,59 @@ __global__ __launch_bounds__(256) void eigh_kernel(Ctx C, EighJobs J) {
     vals[rank] = li;
     for (int r = 0; r < d; ++r) vecs[r * d + rank] = V[r * kEP + i];
   }
+}
+
+// ---------------------------------------------------------------------------
+// Metric roots: a factor F with F F^T = M. Any such factor gives the same
+// split coordinates after the principal-axis step (F = E sqrt(L) R for an
+// orthogonal R, which the principal axes absorb), so the root of each metric
+// is taken as its Cholesky factor, in fp64; pivots below a relative threshold
+// are treated as zero (positive semi-definite metrics; this equals clamping
+// the eigenvalues at zero up to rounding).
+// ---------------------------------------------------------------------------
+
+constexpr int kCholThreads = 256;
+constexpr int kCP = kMaxD + 1;
+
+__global__ __launch_bounds__(kCholThreads) void cholesky_kernel(Ctx C, int in0, int out0, int in1,
+                                                                 int out1) {
+  extern __shared__ double csh[];  // [d][kCP]
+  __shared__ double sh_tol;
+  const int bh = blockIdx.x, job = blockIdx.y, d = C.d, tid = threadIdx.x;
+  const int tr = tid >> 4, tc = tid & 15;  // 16 x 16 thread grid
+  const float* M = mat(C, bh, job == 0 ? in0 : in1);
+  float* F = mat(C, bh, job == 0 ? out0 : out1);
+  double* A = csh;
+  for (int i = tr; i < d; i += 16)
+    for (int k = tc; k < d; k += 16) A[i * kCP + k] = (double)M[i * d + k];
+  __syncthreads();
+  if (tid < 64) {
+    double mx = 0.0;
+    for (int i = tid; i < d; i += 64) mx = fmax(mx, A[i * kCP + i]);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) mx = fmax(mx, __shfl_xor(mx, o, 64));
+    if (tid == 0) sh_tol = mx * 1e-12;
+  }
+  __syncthreads();
+  const double tol = sh_tol;
+  for (int j = 0; j < d; ++j) {
+    // every thread derives the pivot from the same LDS value
+    const double dj = A[j * kCP + j];
+    const double piv = dj > tol ? sqrt(dj) : 0.0;
+    const double ip = piv > 0.0 ? 1.0 / piv : 0.0;
+    __syncthreads();
+    for (int i = j + 1 + tid; i < d; i += kCholThreads) A[i * kCP + j] *= ip;
+    if (tid == 0) A[j * kCP + j] = piv;
+    __syncthreads();
+    // trailing update of the lower triangle, rows i > j, columns j < k <= i
+    for (int i = j + 1 + tr; i < d; i += 16) {
+      const double lij = A[i * kCP + j];
+      for (int k = j + 1 + tc; k <= i; k += 16) A[i * kCP + k] -= lij * A[k * kCP + j];
+    }
+    __syncthreads();
+  }
+  for (int i = tr; i < d; i += 16)
+    for (int k = tc; k < d; k += 16) F[i * d + k] = k <= i ? (float)A[i * kCP + k] : 0.f;
 }
 
 // ---------------------------------------------------------------------------
@@ -360,21 +508,25 @@ __device__ void wg_matmul(const float* Am, bool transA, const float* Bm, float* 
   __syncthreads();
 }
 
-// Metric mode, after the first eigensolves: roots S_q (of Q^T Q/n) and S_k (of
-// the key covariance), and C2 = S_q^T C_K S_q, the covariance of K S_q.
+// W (d x d, fp32) -> W^T as two bf16 matrices hi + lo with hi + lo = W^T to
+// about 2^-16 relative: the A operands of the MFMA projections.
+__device__ void pack_wops(const float* W, bf16* out, int d) {
+  for (int e = threadIdx.x; e < d * d; e += 256) {
+    const int i = e / d, k = e % d;  // out row i (output dim), column k (input dim)
+    const float w = W[k * d + i];
+    const bf16 hi = (bf16)w;
+    out[e] = hi;
+    out[d * d + e] = (bf16)(w - (float)hi);
+  }
+}
+
+// Metric mode, after the factorizations: S_q (F F^T = Q^T Q/n) and S_k
+// (F F^T = key covariance); C2 = S_q^T C_K S_q, the covariance of K S_q.
 __global__ __launch_bounds__(256) void prep_metric_kernel(Ctx C) {
   __shared__ __attribute__((aligned(16))) float As[kStage][kDP];
   __shared__ __attribute__((aligned(16))) float Bs[kStage][kDP];
   const int bh = blockIdx.x, d = C.d;
   float* Sq = mat(C, bh, M_E0);
-  float* Sk = mat(C, bh, M_EK);
-  const float* lq = vec(C, bh, V_L0);
-  const float* lk = vec(C, bh, V_LK);
-  for (int e = threadIdx.x; e < d * d; e += 256) {
-    const int j = e % d;
-    Sq[e] *= sqrtf(fmaxf(lq[j], 0.f));
-    Sk[e] *= sqrtf(fmaxf(lk[j], 0.f));
-  }
   __threadfence_block();
   __syncthreads();
   float* tmp = mat(C, bh, M_TK);
@@ -387,6 +539,7 @@ __global__ __launch_bounds__(256) void prep_metric_kernel(Ctx C) {
     for (int t = 0; t < d; ++t) s = __builtin_fmaf(muk[t], Sq[t * d + j], s);
     vec(C, bh, V_KQ)[j] = s;
   }
+  if (C.dtype == CA_BF16) pack_wops(mat(C, bh, M_EK), wop(C, bh, O_FK), d);
 }
 
 // Metric mode, queries: rho = q S_k, inv = 1/|rho| (0 if rho = 0), r = rho*inv;
@@ -463,24 +616,46 @@ __global__ __launch_bounds__(256) void qnorm_partial_kernel(Ctx C) {
   if (threadIdx.x < d) out[d * d + threadIdx.x] = csum;
 }
 
-// Covariance of r(q) (fp64 reduction) and its mean.
-__global__ __launch_bounds__(256) void qnorm_finish_kernel(Ctx C) {
+// Covariance of r(q) (fp64 reduction) and its mean. Partials either hold
+// sums of r r^T and r directly (weighted == 0), or sums of inv^2 x x^T and
+// inv x (weighted != 0), from which cov(r) = S_k^T (sum inv^2 x x^T / n) S_k -
+// mu_r mu_r^T with mu_r = S_k^T (sum inv x) / n.
+__global__ __launch_bounds__(256) void qnorm_finish_kernel(Ctx C, int weighted) {
   __shared__ double mu[kMaxD];
+  __shared__ __attribute__((aligned(16))) float As[kStage][kDP];
+  __shared__ __attribute__((aligned(16))) float Bs[kStage][kDP];
   const int bh = blockIdx.x, d = C.d;
   const float* part = C.qn_part + (size_t)bh * C.nblk * (d * d + d);
   const double n = (double)C.s[0].n;
+  float* M = mat(C, bh, M_C3);
+  float* mur = vec(C, bh, V_MUR);
   for (int t = threadIdx.x; t < d; t += 256) {
-    double s = 0.0;
-    for (int b = 0; b < C.nblk; ++b) s += (double)part[(size_t)b * (d * d + d) + d * d + t];
+    const double s = sum_partials(part + d * d + t, (size_t)(d * d + d), C.nblk);
     mu[t] = s / n;
-    vec(C, bh, V_MUR)[t] = (float)(s / n);
   }
   __syncthreads();
-  float* M = mat(C, bh, M_C3);
-  for (int e = threadIdx.x; e < d * d; e += 256) {
-    double s = 0.0;
-    for (int b = 0; b < C.nblk; ++b) s += (double)part[(size_t)b * (d * d + d) + e];
-    M[e] = (float)(s / n - mu[e / d] * mu[e % d]);
+  if (weighted) {
+    const float* Sk = mat(C, bh, M_EK);
+    // mu_r = S_k^T m
+    for (int j = threadIdx.x; j < d; j += 256) {
+      double acc = 0.0;
+      for (int t = 0; t < d; ++t) acc += (double)Sk[t * d + j] * mu[t];
+      mur[j] = (float)acc;
+    }
+    for (int e = threadIdx.x; e < d * d; e += 256)
+      M[e] = (float)(sum_partials(part + e, (size_t)(d * d + d), C.nblk) / n);
+    __threadfence_block();
+    __syncthreads();
+    float* tmp = mat(C, bh, M_TQ);
+    wg_matmul(M, false, Sk, tmp, d, As, Bs);   // W2 S_k
+    wg_matmul(Sk, true, tmp, M, d, As, Bs);    // S_k^T W2 S_k
+    for (int e = threadIdx.x; e < d * d; e += 256) M[e] -= mur[e / d] * mur[e % d];
+  } else {
+    for (int t = threadIdx.x; t < d; t += 256) mur[t] = (float)mu[t];
+    for (int e = threadIdx.x; e < d * d; e += 256) {
+      const double s = sum_partials(part + e, (size_t)(d * d + d), C.nblk);
+      M[e] = (float)(s / n - mu[e / d] * mu[e % d]);
+    }
   }
 }
 
@@ -524,6 +699,12 @@ __global__ __launch_bounds__(256) void prep_final_kernel(Ctx C) {
       Tk[e] = Uk[e];
       Tq[e] = Uq[e];
     }
+  }
+  __threadfence_block();
+  __syncthreads();
+  if (C.dtype == CA_BF16) {
+    pack_wops(Tk, wop(C, bh, O_TK), d);
+    pack_wops(Tq, wop(C, bh, O_TQ), d);
   }
 }
 
@@ -580,6 +761,293 @@ __global__ __launch_bounds__(256) void project_kernel(Ctx C) {
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         if (4 * j4 + j < d) Y[(size_t)(rs + r) * d + 4 * j4 + j] = a[j] * sc;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// MFMA versions of the dense passes (bf16 inputs, d in {64, 128}).
+//
+// A 32-token tile of X is held as MFMA operands: lane l owns token l % 32 and
+// features 16 ks + 8 (l / 32) + [0, 8) for k-step ks, loaded with 16-byte
+// reads straight from the rows. With X as the B operand and W^T as the A
+// operand, (X W)^T comes out with one token per lane (column = token), so
+// per-token scalings stay in the lane. For the second moments X^T X the tile
+// is first transposed on the matrix core by multiplying with an identity
+// operand (exact for bf16 data), which leaves one feature per lane.
+// ---------------------------------------------------------------------------
+
+template <int D>
+__device__ __forceinline__ void load_xtile(const bf16* __restrict__ x, int bh, int tok0, int lim,
+                                           int n, int H, int layout, int l32, int h,
+                                           bf16x8 (&xop)[D / 16]) {
+  const int tok = tok0 + l32;
+  if (tok < lim) {
+    const bf16* row = x + row_off(bh, tok, n, H, D, layout);
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) xop[ks] = *(const bf16x8*)(row + 16 * ks + 8 * h);
+  } else {
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks)
+#pragma unroll
+      for (int u = 0; u < 8; ++u) xop[ks][u] = (bf16)0.f;
+  }
+}
+
+// Identity operands: B[k][n] = 1 iff k == n for the two 16-row halves of a
+// 32-wide feature tile.
+__device__ __forceinline__ void ident_ops(int l32, int h, bf16x8 (&id)[2]) {
+#pragma unroll
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int u = 0; u < 8; ++u) id[s][u] = (bf16)((l32 == 16 * s + 8 * h + u) ? 1.f : 0.f);
+}
+
+// xT[ft]: lane l holds feature 32 ft + l % 32 of tokens 8 (r/4) + 4 h + r % 4.
+template <int D>
+__device__ __forceinline__ void transpose_tile(const bf16x8 (&xop)[D / 16], const bf16x8 (&id)[2],
+                                               f32x16 (&xT)[D / 32]) {
+#pragma unroll
+  for (int ft = 0; ft < D / 32; ++ft) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) xT[ft][r] = 0.f;
+    xT[ft] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xop[2 * ft], id[0], xT[ft], 0, 0, 0);
+    xT[ft] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xop[2 * ft + 1], id[1], xT[ft], 0, 0, 0);
+  }
+}
+
+__device__ __forceinline__ bf16x8 pack_half(const f32x16& v, int s) {
+  float t[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) t[j] = v[8 * s + j];
+  return pack8(t);
+}
+
+// Stages the hi/lo W^T operands of one head into LDS (row = output dim,
+// 2D-byte rows, chunk-swizzled).
+template <int D>
+__device__ __forceinline__ void stage_wops(const bf16* __restrict__ src, char* lds) {
+  constexpr int ROWB = 2 * D, NCH = ROWB / 16;
+  for (int c = threadIdx.x; c < 2 * D * NCH; c += 256) {
+    const int m = c / (D * NCH), rem = c % (D * NCH);
+    const int r = rem / NCH, lc = rem % NCH;
+    *(uint4*)(lds + m * D * ROWB + swz_off<ROWB>(r, lc)) =
+        *(const uint4*)(src + (size_t)m * D * D + r * D + lc * 8);
+  }
+}
+
+// acc[ot] = (X W)^T tile ot (output dims 32 ot.., tokens = lanes) with W = hi + lo.
+template <int D>
+__device__ __forceinline__ void project_tile(const char* wl, const bf16x8 (&xop)[D / 16], int l32,
+                                             int h, f32x16 (&acc)[D / 32]) {
+  constexpr int ROWB = 2 * D;
+#pragma unroll
+  for (int ot = 0; ot < D / 32; ++ot) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[ot][r] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) {
+      const int off = swz_off<ROWB>(32 * ot + l32, 2 * ks + h);
+      const bf16x8 ahi = *(const bf16x8*)(wl + off);
+      const bf16x8 alo = *(const bf16x8*)(wl + D * ROWB + off);
+      acc[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ahi, xop[ks], acc[ot], 0, 0, 0);
+      acc[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(alo, xop[ks], acc[ot], 0, 0, 0);
+    }
+  }
+}
+
+// Adds the symmetric Gram tiles (it <= jt) of one wave into red[d][d] (and
+// the mirror), waves in a fixed order.
+template <int D>
+__device__ __forceinline__ void reduce_gram(float* red, const f32x16* g, int w, int l32, int h) {
+  constexpr int FT = D / 32;
+  for (int wv = 0; wv < 4; ++wv) {
+    if (w == wv) {
+      int t = 0;
+#pragma unroll
+      for (int it = 0; it < FT; ++it)
+#pragma unroll
+        for (int jt = it; jt < FT; ++jt, ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int i = 32 * it + 8 * (r >> 2) + 4 * h + (r & 3), j = 32 * jt + l32;
+            const float v = g[t][r];
+            red[i * D + j] = wv == 0 ? v : red[i * D + j] + v;
+            if (it != jt) red[j * D + i] = wv == 0 ? v : red[j * D + i] + v;
+          }
+    }
+    __syncthreads();
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void moments_mfma_kernel(Ctx C) {
+  constexpr int FT = D / 32, KS = D / 16, NT = FT * (FT + 1) / 2;
+  __shared__ float red[D * D];
+  __shared__ float csr[4][D];
+  const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH, blk = blockIdx.x;
+  const Side& S = C.s[side];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
+  const int r0 = blk * kMomRows, r1 = min(S.n, r0 + kMomRows);
+  bf16x8 id[2];
+  ident_ops(l32, h, id);
+  f32x16 g[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) g[t][r] = 0.f;
+  float cs[FT];
+#pragma unroll
+  for (int ft = 0; ft < FT; ++ft) cs[ft] = 0.f;
+  for (int tok0 = r0 + 32 * w; tok0 < r1; tok0 += 128) {
+    bf16x8 xop[KS];
+    load_xtile<D>((const bf16*)S.x, bh, tok0, r1, S.n, C.H, C.layout, l32, h, xop);
+    f32x16 xT[FT];
+    transpose_tile<D>(xop, id, xT);
+#pragma unroll
+    for (int ft = 0; ft < FT; ++ft)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) cs[ft] += xT[ft][r];
+    int t = 0;
+#pragma unroll
+    for (int it = 0; it < FT; ++it)
+#pragma unroll
+      for (int jt = it; jt < FT; ++jt, ++t)
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2)
+          g[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pack_half(xT[it], s2),
+                                                          pack_half(xT[jt], s2), g[t], 0, 0, 0);
+  }
+  reduce_gram<D>(red, g, w, l32, h);
+#pragma unroll
+  for (int ft = 0; ft < FT; ++ft) {
+    const float v = cs[ft] + __shfl_xor(cs[ft], 32, 64);
+    if (h == 0) csr[w][32 * ft + l32] = v;
+  }
+  __syncthreads();
+  float* out = C.mom_part + ((size_t)pid * C.nblk + blk) * (D * D + D);
+  for (int e = tid; e < D * D; e += 256) out[e] = red[e];
+  for (int f = tid; f < D; f += 256) out[D * D + f] = ((csr[0][f] + csr[1][f]) + csr[2][f]) + csr[3][f];
+}
+
+// Metric mode, queries: rho = q S_k (MFMA, lane = token), inv = 1/|rho| (0 if
+// rho = 0) kept for the projection, and per row block the partial sums of
+// inv^2 x x^T and inv x (r r^T = S_k^T (inv^2 x x^T) S_k is formed after the
+// reduction).
+template <int D>
+__global__ __launch_bounds__(256) void qnorm_mfma_kernel(Ctx C) {
+  constexpr int FT = D / 32, KS = D / 16, NT = FT * (FT + 1) / 2;
+  __shared__ __attribute__((aligned(16))) char wl[2 * D * 2 * D];
+  __shared__ float red[D * D];
+  __shared__ float csr[4][D];
+  __shared__ float sinv[4][32];
+  const int bh = blockIdx.y, blk = blockIdx.x;
+  const Side& S = C.s[0];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
+  stage_wops<D>(wop(C, bh, O_FK), wl);
+  __syncthreads();
+  const int r0 = blk * kMomRows, r1 = min(S.n, r0 + kMomRows);
+  bf16x8 id[2];
+  ident_ops(l32, h, id);
+  f32x16 g[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) g[t][r] = 0.f;
+  float cs[FT];
+#pragma unroll
+  for (int ft = 0; ft < FT; ++ft) cs[ft] = 0.f;
+  for (int tok0 = r0 + 32 * w; tok0 < r1; tok0 += 128) {
+    bf16x8 xop[KS];
+    load_xtile<D>((const bf16*)S.x, bh, tok0, r1, S.n, C.H, C.layout, l32, h, xop);
+    f32x16 acc[FT];
+    project_tile<D>(wl, xop, l32, h, acc);
+    float nrm = 0.f;
+#pragma unroll
+    for (int ot = 0; ot < FT; ++ot)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) nrm = __builtin_fmaf(acc[ot][r], acc[ot][r], nrm);
+    nrm += __shfl_xor(nrm, 32, 64);
+    const float inv = nrm > 0.f ? 1.f / sqrtf(nrm) : 0.f;
+    if (h == 0) {
+      sinv[w][l32] = inv;
+      if (tok0 + l32 < r1) C.inv_q[(size_t)bh * S.n + tok0 + l32] = inv;
+    }
+    __builtin_amdgcn_wave_barrier();
+    f32x16 xT[FT];
+    transpose_tile<D>(xop, id, xT);
+    float wt[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) wt[r] = sinv[w][8 * (r >> 2) + 4 * h + (r & 3)];
+#pragma unroll
+    for (int ft = 0; ft < FT; ++ft)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) cs[ft] = __builtin_fmaf(wt[r], xT[ft][r], cs[ft]);
+    int t = 0;
+#pragma unroll
+    for (int it = 0; it < FT; ++it)
+#pragma unroll
+      for (int jt = it; jt < FT; ++jt, ++t)
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) {
+          float bw[8], bl[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const float v = wt[8 * s2 + j] * wt[8 * s2 + j] * xT[jt][8 * s2 + j];
+            bw[j] = v;
+          }
+          const bf16x8 bhi = pack8(bw);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) bl[j] = bw[j] - (float)bhi[j];
+          const bf16x8 a = pack_half(xT[it], s2);
+          g[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bhi, g[t], 0, 0, 0);
+          g[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pack8(bl), g[t], 0, 0, 0);
+        }
+    __builtin_amdgcn_wave_barrier();
+  }
+  reduce_gram<D>(red, g, w, l32, h);
+#pragma unroll
+  for (int ft = 0; ft < FT; ++ft) {
+    const float v = cs[ft] + __shfl_xor(cs[ft], 32, 64);
+    if (h == 0) csr[w][32 * ft + l32] = v;
+  }
+  __syncthreads();
+  float* out = C.qn_part + ((size_t)bh * C.nblk + blk) * (D * D + D);
+  for (int e = tid; e < D * D; e += 256) out[e] = red[e];
+  for (int f = tid; f < D; f += 256) out[D * D + f] = ((csr[0][f] + csr[1][f]) + csr[2][f]) + csr[3][f];
+}
+
+// Y = X T (keys) or inv * (X W_Q) (metric queries), lane = token, fp32 rows.
+template <int D>
+__global__ __launch_bounds__(256) void project_mfma_kernel(Ctx C) {
+  constexpr int FT = D / 32, KS = D / 16;
+  __shared__ __attribute__((aligned(16))) char wl[2 * D * 2 * D];
+  const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH;
+  const Side& S = C.s[side];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
+  const int r0 = blockIdx.x * kProjRows, r1 = min(S.n, r0 + kProjRows);
+  if (r0 >= r1) return;
+  stage_wops<D>(wop(C, bh, side == 0 ? O_TQ : O_TK), wl);
+  __syncthreads();
+  const bool scale = side == 0 && C.xf == CA_XF_METRIC;
+  float* Y = S.y + (size_t)bh * S.n * D;
+  for (int tok0 = r0 + 32 * w; tok0 < r1; tok0 += 128) {
+    bf16x8 xop[KS];
+    load_xtile<D>((const bf16*)S.x, bh, tok0, r1, S.n, C.H, C.layout, l32, h, xop);
+    f32x16 acc[FT];
+    project_tile<D>(wl, xop, l32, h, acc);
+    const int tok = tok0 + l32;
+    if (tok < r1) {
+      const float sc = scale ? C.inv_q[(size_t)bh * S.n + tok] : 1.f;
+      float* yrow = Y + (size_t)tok * D;
+#pragma unroll
+      for (int ot = 0; ot < FT; ++ot)
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          const int col = 32 * ot + 8 * g4 + 4 * h;
+          *(float4*)(yrow + col) = make_float4(acc[ot][4 * g4] * sc, acc[ot][4 * g4 + 1] * sc,
+                                               acc[ot][4 * g4 + 2] * sc, acc[ot][4 * g4 + 3] * sc);
+        }
     }
   }
 }
@@ -1139,6 +1607,90 @@ __global__ __launch_bounds__(128) void gather_kernel(Ctx C) {
   }
 }
 
+// Fast gather for rows that are a whole number of 16-byte chunks: one
+// workgroup per cluster copies the cluster's rows chunk by chunk (coalesced
+// on both sides), sums the centroids in registers and then across the
+// workgroup in a fixed order (deterministic), and transposes the value rows
+// through LDS so that the value tiles are written 16 bytes at a time.
+template <typename T>
+__global__ __launch_bounds__(256) void gather_fast_kernel(Ctx C) {
+  extern __shared__ float gfs[];
+  constexpr int EPC = 16 / sizeof(T);  // elements per 16-byte chunk
+  const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH, a = blockIdx.x;
+  const Side& S = C.s[side];
+  if (a >= S.nc) return;
+  const int d = C.d, c = S.c, tid = threadIdx.x;
+  const int cpr = d / EPC;        // chunks per row (divides 256: d <= 128)
+  const int rstep = 256 / cpr;    // row stride of one thread
+  const int col = tid % cpr, r0 = tid / cpr;
+  const int cnt = min(c, S.n - a * c);
+  const int32_t* perm = S.perm + (size_t)bh * S.n + (size_t)a * c;
+  const bool vals = side == 1 && C.v != nullptr;
+  float* part = gfs;                            // [rstep][d] partial sums of x
+  float* partv = gfs + rstep * d;               // [rstep][d] partial sums of v
+  T* vstage = (T*)(gfs + 2 * rstep * d);        // [c][d] value rows
+  if (tid == 0) S.count[(size_t)bh * S.nc + a] = cnt;
+  if (S.cid)
+    for (int r = tid; r < cnt; r += 256) S.cid[(size_t)bh * S.n + perm[r]] = a;
+  float acc[EPC], accv[EPC];
+#pragma unroll
+  for (int u = 0; u < EPC; ++u) acc[u] = accv[u] = 0.f;
+  T* dst = (T*)S.xp + ((size_t)bh * S.npad + (size_t)a * c) * d;
+  for (int r = r0; r < c; r += rstep) {
+    uint4 chunk = make_uint4(0u, 0u, 0u, 0u), vchunk = chunk;
+    if (r < cnt) {
+      const int i = perm[r];
+      chunk = *(const uint4*)((const T*)S.x + row_off(bh, i, S.n, C.H, d, C.layout) + col * EPC);
+      if (vals)
+        vchunk = *(const uint4*)((const T*)C.v + row_off(bh, i, S.n, C.H, d, C.layout) + col * EPC);
+    }
+    *(uint4*)(dst + (size_t)r * d + col * EPC) = chunk;
+    union {
+      uint4 v;
+      T e[EPC];
+    } cx, cv;
+    cx.v = chunk;
+#pragma unroll
+    for (int u = 0; u < EPC; ++u) acc[u] += (float)cx.e[u];
+    if (vals) {
+      *(uint4*)(vstage + r * d + col * EPC) = vchunk;
+      cv.v = vchunk;
+#pragma unroll
+      for (int u = 0; u < EPC; ++u) accv[u] += (float)cv.e[u];
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < EPC; ++u) {
+    part[r0 * d + col * EPC + u] = acc[u];
+    if (vals) partv[r0 * d + col * EPC + u] = accv[u];
+  }
+  __syncthreads();
+  for (int f = tid; f < d; f += 256) {
+    float sx = 0.f, sv = 0.f;
+    for (int g = 0; g < rstep; ++g) {
+      sx += part[g * d + f];
+      if (vals) sv += partv[g * d + f];
+    }
+    S.cent[((size_t)bh * S.nc + a) * d + f] = sx / (float)cnt;
+    if (vals) C.cent_v[((size_t)bh * S.nc + a) * d + f] = sv / (float)cnt;
+  }
+  if (vals) {
+    // value tile [d][c]: chunk = EPC consecutive rows of one dimension
+    T* vt = (T*)C.vp + ((size_t)bh * S.nc + a) * (size_t)d * c;
+    const int cpc = c / EPC;  // chunks per tile row (c >= EPC)
+    for (int e = tid; e < d * cpc; e += 256) {
+      const int f = e / cpc, rr = (e % cpc) * EPC;
+      union {
+        uint4 v;
+        T e[EPC];
+      } tmp;
+#pragma unroll
+      for (int u = 0; u < EPC; ++u) tmp.e[u] = vstage[(rr + u) * d + f];
+      *(uint4*)(vt + (size_t)f * c + rr) = tmp.v;
+    }
+  }
+}
+
 int tail_size(int c) { return c * 64 < kTail ? c * 64 : kTail; }
 
 }  // namespace
@@ -1163,19 +1715,28 @@ namespace {
 // Kernels that use more than 64 KiB of dynamic LDS declare their size once. A
 // refusal is not fatal here: the launch itself reports a real limit.
 constexpr size_t kEighLds = 2 * kMaxD * kEP * sizeof(float);
+constexpr size_t kCholLds = (size_t)kMaxD * kCP * sizeof(double);
 constexpr size_t kQnormLds = (size_t)(kMaxD + 2 * kStage) * kDP * sizeof(float);
 constexpr size_t kProjLds = (size_t)(kMaxD + kStage) * kDP * sizeof(float);
 constexpr size_t kGatherLds = (size_t)kMaxC * kMaxD * sizeof(float);
 hipError_t set_lds_limits() {
   static bool done = [] {
-    hipFuncSetAttribute((const void*)eigh_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                        (int)kEighLds);
-    hipFuncSetAttribute((const void*)qnorm_partial_kernel,
+    (void)hipFuncSetAttribute((const void*)eigh_kernel<64>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)kEighLds);
+    (void)hipFuncSetAttribute((const void*)eigh_kernel<128>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)kEighLds);
+    (void)hipFuncSetAttribute((const void*)cholesky_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                        (int)kCholLds);
+    (void)hipFuncSetAttribute((const void*)qnorm_partial_kernel,
                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)kQnormLds);
-    hipFuncSetAttribute((const void*)project_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+    (void)hipFuncSetAttribute((const void*)project_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
                         (int)kProjLds);
-    hipFuncSetAttribute((const void*)gather_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+    (void)hipFuncSetAttribute((const void*)gather_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
                         (int)kGatherLds);
+    (void)hipFuncSetAttribute((const void*)gather_fast_kernel<bf16>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    (void)hipFuncSetAttribute((const void*)gather_fast_kernel<float>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     (void)hipGetLastError();
     return true;
   }();
@@ -1209,6 +1770,7 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
   C.inv_q = (float*)(ws + W.inv_q);
   C.mom_part = (float*)(ws + W.mom_part);
   C.qn_part = (float*)(ws + W.qn_part);
+  C.wops = (bf16*)(ws + W.wops);
   C.idx0 = (int32_t*)(ws + W.idx0);
   C.idx1 = (int32_t*)(ws + W.idx1);
   C.keys = (uint32_t*)(ws + W.keys);
@@ -1255,25 +1817,48 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
     if (e != hipSuccess) return e;          \
   } while (0)
 
+  const bool mfma = P.dtype == CA_BF16 && (d == 64 || d == 128);
   if (P.xf != CA_XF_NONE) {
-    hipLaunchKernelGGL(moments_partial_kernel, dim3(C.nblk, 2 * BH), dim3(256), 0, st, C);
+    if (mfma && d == 64)
+      hipLaunchKernelGGL(moments_mfma_kernel<64>, dim3(C.nblk, 2 * BH), dim3(256), 0, st, C);
+    else if (mfma)
+      hipLaunchKernelGGL(moments_mfma_kernel<128>, dim3(C.nblk, 2 * BH), dim3(256), 0, st, C);
+    else
+      hipLaunchKernelGGL(moments_partial_kernel, dim3(C.nblk, 2 * BH), dim3(256), 0, st, C);
     CA_CHECK();
     hipLaunchKernelGGL(moments_finish_kernel, dim3(BH), dim3(256), 0, st, C);
     CA_CHECK();
     const size_t eigh_lds = kEighLds;
-    EighJobs J1 = {2, {M_A0, M_CK}, {M_E0, M_EK}, {V_L0, V_LK}};
-    hipLaunchKernelGGL(eigh_kernel, dim3(BH, 2), dim3(256), eigh_lds, st, C, J1);
-    CA_CHECK();
+    if (P.xf == CA_XF_PCA) {
+      EighJobs J1 = {2, {M_A0, M_CK}, {M_E0, M_EK}, {V_L0, V_LK}};
+      if (d <= 64)
+        hipLaunchKernelGGL(eigh_kernel<64>, dim3(BH, 2), dim3(kEighThreads), eigh_lds, st, C, J1);
+      else
+        hipLaunchKernelGGL(eigh_kernel<128>, dim3(BH, 2), dim3(kEighThreads), eigh_lds, st, C, J1);
+      CA_CHECK();
+    } else {
+      hipLaunchKernelGGL(cholesky_kernel, dim3(BH, 2), dim3(kCholThreads), kCholLds, st, C,
+                         (int)M_A0, (int)M_E0, (int)M_CK, (int)M_EK);
+      CA_CHECK();
+    }
     if (P.xf == CA_XF_METRIC) {
       hipLaunchKernelGGL(prep_metric_kernel, dim3(BH), dim3(256), 0, st, C);
       CA_CHECK();
       const size_t qlds = kQnormLds;
-      hipLaunchKernelGGL(qnorm_partial_kernel, dim3(C.nblk, BH), dim3(256), qlds, st, C);
+      if (mfma && d == 64)
+        hipLaunchKernelGGL(qnorm_mfma_kernel<64>, dim3(C.nblk, BH), dim3(256), 0, st, C);
+      else if (mfma)
+        hipLaunchKernelGGL(qnorm_mfma_kernel<128>, dim3(C.nblk, BH), dim3(256), 0, st, C);
+      else
+        hipLaunchKernelGGL(qnorm_partial_kernel, dim3(C.nblk, BH), dim3(256), qlds, st, C);
       CA_CHECK();
-      hipLaunchKernelGGL(qnorm_finish_kernel, dim3(BH), dim3(256), 0, st, C);
+      hipLaunchKernelGGL(qnorm_finish_kernel, dim3(BH), dim3(256), 0, st, C, (int)mfma);
       CA_CHECK();
       EighJobs J2 = {2, {M_C2, M_C3}, {M_C2, M_C3}, {V_L2, V_L3}};
-      hipLaunchKernelGGL(eigh_kernel, dim3(BH, 2), dim3(256), eigh_lds, st, C, J2);
+      if (d <= 64)
+        hipLaunchKernelGGL(eigh_kernel<64>, dim3(BH, 2), dim3(kEighThreads), eigh_lds, st, C, J2);
+      else
+        hipLaunchKernelGGL(eigh_kernel<128>, dim3(BH, 2), dim3(kEighThreads), eigh_lds, st, C, J2);
       CA_CHECK();
     }
     hipLaunchKernelGGL(prep_final_kernel, dim3(BH), dim3(256), 0, st, C);
@@ -1282,8 +1867,13 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
   {
     const int nmax = C.nmax;
     const size_t plds = kProjLds;
-    hipLaunchKernelGGL(project_kernel, dim3((nmax + kProjRows - 1) / kProjRows, 2 * BH),
-                       dim3(256), plds, st, C);
+    const dim3 pgrid((nmax + kProjRows - 1) / kProjRows, 2 * BH);
+    if (mfma && P.xf != CA_XF_NONE && d == 64)
+      hipLaunchKernelGGL(project_mfma_kernel<64>, pgrid, dim3(256), 0, st, C);
+    else if (mfma && P.xf != CA_XF_NONE)
+      hipLaunchKernelGGL(project_mfma_kernel<128>, pgrid, dim3(256), 0, st, C);
+    else
+      hipLaunchKernelGGL(project_kernel, pgrid, dim3(256), plds, st, C);
     CA_CHECK();
   }
   const int big = W.big_q > W.big_k ? W.big_q : W.big_k;
@@ -1325,8 +1915,19 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
   }
   {
     const int maxc = P.nqc > P.nkc ? P.nqc : P.nkc;
-    const size_t glds = v ? (size_t)P.ck * d * sizeof(float) : 0;
-    hipLaunchKernelGGL(gather_kernel, dim3(maxc, 2 * BH), dim3(128), glds, st, C);
+    const int epc = 16 / (int)P.esize;
+    const bool fast = (d % epc == 0) && (P.ck % epc == 0) && ((256 / (d / epc)) * (d / epc) == 256);
+    if (fast) {
+      const int rstep = 256 / (d / epc);
+      const size_t glds = (size_t)2 * rstep * d * sizeof(float) + (v ? (size_t)P.ck * d * P.esize : 0);
+      if (P.dtype == CA_BF16)
+        hipLaunchKernelGGL(gather_fast_kernel<bf16>, dim3(maxc, 2 * BH), dim3(256), glds, st, C);
+      else
+        hipLaunchKernelGGL(gather_fast_kernel<float>, dim3(maxc, 2 * BH), dim3(256), glds, st, C);
+    } else {
+      const size_t glds = v ? (size_t)P.ck * d * sizeof(float) : 0;
+      hipLaunchKernelGGL(gather_kernel, dim3(maxc, 2 * BH), dim3(128), glds, st, C);
+    }
     CA_CHECK();
   }
 #undef CA_CHECK
