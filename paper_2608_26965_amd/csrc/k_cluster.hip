@@ -205,10 +205,16 @@ __global__ __launch_bounds__(256) void moments_finish_kernel(Ctx C) {
 
 // ---------------------------------------------------------------------------
 // Symmetric eigensolver: parallel cyclic Jacobi, one workgroup per matrix.
-// Rotations use the round-robin ordering, d/2 disjoint pairs per step, each
-// step applied as 2x2 blocks of J^T A J (Golub & Van Loan, parallel Jacobi).
-// Output: eigenvalues in descending order and the matching eigenvectors as
-// columns.
+// The DM players of a round-robin tournament (rows beyond d are zero padding,
+// so any pair that touches one is an identity rotation) give DM/2 disjoint
+// pairs per step; every pair of indices meets once per sweep of DM-1 steps
+// (Golub & Van Loan, parallel Jacobi). A step is applied as J^T A J in two
+// passes over LDS: first the rows p, q of A and of V^T (one column per lane),
+// then the columns p, q of A (one row per lane). Each wavefront owns the same
+// DM/16 pairs in both passes and computes their rotations itself, so a step
+// costs two barriers and every LDS access is a conflict-free row or column
+// sweep. Output: eigenvalues in descending order and the matching eigenvectors
+// as columns.
 // ---------------------------------------------------------------------------
 
 struct EighJobs {
@@ -216,8 +222,11 @@ struct EighJobs {
   int in[2], vecs[2], vals[2];
 };
 
-constexpr int kEP = kMaxD + 1;
 constexpr int kEighThreads = 512;
+
+__host__ __device__ constexpr size_t eigh_lds_bytes(int dm) {
+  return 2 * (size_t)dm * (dm + 1) * sizeof(float);
+}
 
 // Round-robin pairing of m players at a step: pair k joins positions k and
 // m-1-k; position 0 is fixed and the others rotate by one place per step, so
@@ -233,34 +242,62 @@ __device__ __forceinline__ void rr_pair(int k, int step, int m, int* p, int* q) 
   *q = a < b ? b : a;
 }
 
+// Rotation (c, s) that zeroes entry (p, q) of J^T A J, J = [[c, s], [-s, c]]
+// on rows/columns (p, q): t = tan(theta) is the smaller root of
+// t^2 + 2 tau t - 1 = 0, tau = (a_qq - a_pp) / (2 a_pq). Hardware reciprocal
+// and square-root approximations are enough: any (c, s) with c^2 + s^2 = 1 to
+// rounding keeps the transform orthogonal, and a slightly inexact angle only
+// leaves a tiny off-diagonal that later sweeps remove.
+__device__ __forceinline__ void jacobi_rotation(float app, float aqq, float apq, float* c,
+                                                float* s) {
+  if (!(fabsf(apq) > 1e-30f)) {
+    *c = 1.f;
+    *s = 0.f;
+    return;
+  }
+  const float tau = 0.5f * (aqq - app) * __builtin_amdgcn_rcpf(apq);
+  const float den = fabsf(tau) + __builtin_amdgcn_sqrtf(1.f + tau * tau);
+  const float t = copysignf(__builtin_amdgcn_rcpf(den), tau);
+  const float cc = __builtin_amdgcn_rsqf(1.f + t * t);
+  *c = cc;
+  *s = t * cc;
+}
+
 template <int DM>
 __global__ __launch_bounds__(kEighThreads) void eigh_kernel(Ctx C, EighJobs J) {
+  constexpr int EP = DM + 1;               // odd row stride: column sweeps hit distinct banks
+  constexpr int NW = kEighThreads / 64;
+  constexpr int PPW = DM / 2 / NW;         // pairs per wavefront and step
+  constexpr int CPL = DM / 64;             // columns (rows) per lane in a row (column) pass
+  static_assert(PPW >= 1 && CPL >= 1, "matrix size");
   extern __shared__ float esh[];
-  float* A = esh;                       // [d][kEP]
-  float* V = esh + kMaxD * kEP;         // [d][kEP]
-  __shared__ float rc[kMaxD / 2 + 1], rs[kMaxD / 2 + 1];
-  __shared__ float red[2][kEighThreads / 64];
+  float* A = esh;             // [DM][EP]
+  float* Vt = esh + DM * EP;  // [DM][EP], Vt[i][j] = V[j][i]
+  __shared__ float red[2][NW];
   __shared__ int sh_stop;
   const int bh = blockIdx.x, job = blockIdx.y, d = C.d, tid = threadIdx.x;
-  const int lane = tid & 63, wv = tid >> 6;
+  const int lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const float* Min = mat(C, bh, J.in[job]);
-  for (int i = wv; i < d; i += kEighThreads / 64)
-    for (int j = lane; j < d; j += 64) {
-      A[i * kEP + j] = Min[i * d + j];
-      V[i * kEP + j] = i == j ? 1.f : 0.f;
+  for (int i = wv; i < DM; i += NW)
+#pragma unroll
+    for (int cc = 0; cc < CPL; ++cc) {
+      const int j = lane + 64 * cc;
+      A[i * EP + j] = i < d && j < d ? Min[i * d + j] : 0.f;
+      Vt[i * EP + j] = i == j ? 1.f : 0.f;
     }
   if (tid == 0) sh_stop = 0;
-  const int m = (d + 1) & ~1;  // players (a phantom one when d is odd)
-  const int np = m / 2;
   for (int sweep = 0; sweep < 40; ++sweep) {
     __syncthreads();
     // Convergence: off-diagonal mass relative to the total.
     float off = 0.f, tot = 0.f;
-    for (int i = wv; i < d; i += kEighThreads / 64)
-      for (int j = lane; j < d; j += 64) {
-        const float a = A[i * kEP + j];
+    for (int i = wv; i < d; i += NW)
+#pragma unroll
+      for (int cc = 0; cc < CPL; ++cc) {
+        const int j = lane + 64 * cc;
+        const float a = A[i * EP + j];
         tot += a * a;
-        if (i != j) off += a * a;
+        off += i != j ? a * a : 0.f;
       }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
@@ -274,7 +311,7 @@ __global__ __launch_bounds__(kEighThreads) void eigh_kernel(Ctx C, EighJobs J) {
     __syncthreads();
     if (tid == 0) {
       float so = 0.f, st = 0.f;
-      for (int i = 0; i < kEighThreads / 64; ++i) {
+      for (int i = 0; i < NW; ++i) {
         so += red[0][i];
         st += red[1][i];
       }
@@ -287,123 +324,67 @@ __global__ __launch_bounds__(kEighThreads) void eigh_kernel(Ctx C, EighJobs J) {
     }
     __syncthreads();
     if (sh_stop >= 2) break;
-    for (int step = 0; step < m - 1; ++step) {
-      if (tid < np) {
-        int p, q;
-        rr_pair(tid, step, m, &p, &q);
-        float c = 1.f, sn = 0.f;
-        if (q < d) {
-          const float apq = A[p * kEP + q];
-          if (apq != 0.f) {
-            const float app = A[p * kEP + p], aqq = A[q * kEP + q];
-            const float tau = (aqq - app) / (2.f * apq);
-            const float t = copysignf(1.f, tau) / (fabsf(tau) + sqrtf(1.f + tau * tau));
-            c = 1.f / sqrtf(1.f + t * t);
-            sn = t * c;
-          }
-        }
-        rc[tid] = c;
-        rs[tid] = sn;
+    for (int step = 0; step < DM - 1; ++step) {
+      // This wavefront's pairs k = wv + NW t; lane t (mod PPW) derives pair t's
+      // rotation, then every lane reads it back as a wave-uniform value.
+      int pl, ql;
+      rr_pair(wv + NW * (lane % PPW), step, DM, &pl, &ql);
+      float cl, sl;
+      jacobi_rotation(A[pl * EP + pl], A[ql * EP + ql], A[pl * EP + ql], &cl, &sl);
+      int P[PPW], Q[PPW];
+      float Cs[PPW], Ss[PPW];
+#pragma unroll
+      for (int t = 0; t < PPW; ++t) {
+        P[t] = __builtin_amdgcn_readlane(pl, t);
+        Q[t] = __builtin_amdgcn_readlane(ql, t);
+        Cs[t] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cl), t));
+        Ss[t] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sl), t));
       }
+      // Row pass: rows p, q of A and of V^T.
+      float ra[PPW][CPL][4];
+#pragma unroll
+      for (int t = 0; t < PPW; ++t)
+#pragma unroll
+        for (int cc = 0; cc < CPL; ++cc) {
+          const int j = lane + 64 * cc;
+          ra[t][cc][0] = A[P[t] * EP + j];
+          ra[t][cc][1] = A[Q[t] * EP + j];
+          ra[t][cc][2] = Vt[P[t] * EP + j];
+          ra[t][cc][3] = Vt[Q[t] * EP + j];
+        }
+#pragma unroll
+      for (int t = 0; t < PPW; ++t)
+#pragma unroll
+        for (int cc = 0; cc < CPL; ++cc) {
+          const int j = lane + 64 * cc;
+          const float c = Cs[t], s = Ss[t];
+          A[P[t] * EP + j] = c * ra[t][cc][0] - s * ra[t][cc][1];
+          A[Q[t] * EP + j] = s * ra[t][cc][0] + c * ra[t][cc][1];
+          Vt[P[t] * EP + j] = c * ra[t][cc][2] - s * ra[t][cc][3];
+          Vt[Q[t] * EP + j] = s * ra[t][cc][2] + c * ra[t][cc][3];
+        }
       __syncthreads();
-      // This thread's items: blocks (k1, k2), k1 = (tid >> 5) + 16 a, k2 = (tid & 31) + 32 b,
-      // kept when k1 <= k2 < np; value rows i = lane for pairs kk = wv + 8 c.
-      constexpr int KA = DM / 2 / 16, KB = DM / 2 / 32 > 0 ? DM / 2 / 32 : 1, KV = DM / 2 / 8;
-      int bp1[KA], bq1[KA], bp2[KB], bq2[KB];
-      float bc1[KA], bs1[KA], bc2[KB], bs2[KB];
+      // Column pass: columns p, q of A; the (p, q) entries become exact zeros.
+      float ca[PPW][CPL][2];
 #pragma unroll
-      for (int a1 = 0; a1 < KA; ++a1) {
-        const int k1 = (tid >> 5) + 16 * a1;
-        rr_pair(k1 < np ? k1 : 0, step, m, &bp1[a1], &bq1[a1]);
-        bc1[a1] = k1 < np ? rc[k1] : 1.f;
-        bs1[a1] = k1 < np ? rs[k1] : 0.f;
-      }
+      for (int t = 0; t < PPW; ++t)
 #pragma unroll
-      for (int b2 = 0; b2 < KB; ++b2) {
-        const int k2 = (tid & 31) + 32 * b2;
-        rr_pair(k2 < np ? k2 : 0, step, m, &bp2[b2], &bq2[b2]);
-        bc2[b2] = k2 < np ? rc[k2] : 1.f;
-        bs2[b2] = k2 < np ? rs[k2] : 0.f;
-      }
-      float va[KA][KB][4];
-#pragma unroll
-      for (int a1 = 0; a1 < KA; ++a1)
-#pragma unroll
-        for (int b2 = 0; b2 < KB; ++b2) {
-          const int k1 = (tid >> 5) + 16 * a1, k2 = (tid & 31) + 32 * b2;
-          const bool live = k1 <= k2 && k2 < np;
-          const int p1 = bp1[a1], q1 = bq1[a1], p2 = bp2[b2], q2 = bq2[b2];
-          const bool hq1 = q1 < d, hq2 = q2 < d;
-          va[a1][b2][0] = live ? A[p1 * kEP + p2] : 0.f;
-          va[a1][b2][1] = live && hq2 ? A[p1 * kEP + q2] : 0.f;
-          va[a1][b2][2] = live && hq1 ? A[q1 * kEP + p2] : 0.f;
-          va[a1][b2][3] = live && hq1 && hq2 ? A[q1 * kEP + q2] : 0.f;
-        }
-      float vv[KV][2];
-      int vpq[KV][2];
-      float vcs[KV][2];
-#pragma unroll
-      for (int cc = 0; cc < KV; ++cc) {
-        const int kk = wv + 8 * cc;
-        int p = 0, q = 0;
-        rr_pair(kk < np ? kk : 0, step, m, &p, &q);
-        const bool live = kk < np && q < d && lane < d;
-        vpq[cc][0] = live ? p : -1;
-        vpq[cc][1] = q;
-        vcs[cc][0] = kk < np ? rc[kk] : 1.f;
-        vcs[cc][1] = kk < np ? rs[kk] : 0.f;
-        vv[cc][0] = live ? V[lane * kEP + p] : 0.f;
-        vv[cc][1] = live ? V[lane * kEP + q] : 0.f;
-      }
-      // (rows of value pairs beyond lane 63 when d > 64)
-      float vv2[KV][2];
-#pragma unroll
-      for (int cc = 0; cc < KV; ++cc) {
-        const bool live = vpq[cc][0] >= 0 && lane + 64 < d;
-        vv2[cc][0] = live ? V[(lane + 64) * kEP + vpq[cc][0]] : 0.f;
-        vv2[cc][1] = live ? V[(lane + 64) * kEP + vpq[cc][1]] : 0.f;
-      }
-#pragma unroll
-      for (int a1 = 0; a1 < KA; ++a1)
-#pragma unroll
-        for (int b2 = 0; b2 < KB; ++b2) {
-          const int k1 = (tid >> 5) + 16 * a1, k2 = (tid & 31) + 32 * b2;
-          if (!(k1 <= k2 && k2 < np)) continue;
-          const int p1 = bp1[a1], q1 = bq1[a1], p2 = bp2[b2], q2 = bq2[b2];
-          const float c1 = bc1[a1], s1 = bs1[a1], c2 = bc2[b2], s2 = bs2[b2];
-          const bool hq1 = q1 < d, hq2 = q2 < d;
-          const float a = va[a1][b2][0], b = va[a1][b2][1], cc = va[a1][b2][2], dd = va[a1][b2][3];
-          const float r00 = c1 * a - s1 * cc, r01 = c1 * b - s1 * dd;
-          const float r10 = s1 * a + c1 * cc, r11 = s1 * b + c1 * dd;
-          float n00 = c2 * r00 - s2 * r01, n01 = s2 * r00 + c2 * r01;
-          float n10 = c2 * r10 - s2 * r11, n11 = s2 * r10 + c2 * r11;
-          if (k1 == k2) {
-            n01 = 0.f;
-            n10 = 0.f;
-          }
-          A[p1 * kEP + p2] = n00;
-          if (hq2) A[p1 * kEP + q2] = n01;
-          if (hq1) A[q1 * kEP + p2] = n10;
-          if (hq1 && hq2) A[q1 * kEP + q2] = n11;
-          if (k1 != k2) {
-            A[p2 * kEP + p1] = n00;
-            if (hq2) A[q2 * kEP + p1] = n01;
-            if (hq1) A[p2 * kEP + q1] = n10;
-            if (hq1 && hq2) A[q2 * kEP + q1] = n11;
-          }
+        for (int cc = 0; cc < CPL; ++cc) {
+          const int i = lane + 64 * cc;
+          ca[t][cc][0] = A[i * EP + P[t]];
+          ca[t][cc][1] = A[i * EP + Q[t]];
         }
 #pragma unroll
-      for (int cc = 0; cc < KV; ++cc) {
-        const int p = vpq[cc][0], q = vpq[cc][1];
-        if (p < 0) continue;
-        const float c = vcs[cc][0], sn = vcs[cc][1];
-        V[lane * kEP + p] = c * vv[cc][0] - sn * vv[cc][1];
-        V[lane * kEP + q] = sn * vv[cc][0] + c * vv[cc][1];
-        if (lane + 64 < d) {
-          V[(lane + 64) * kEP + p] = c * vv2[cc][0] - sn * vv2[cc][1];
-          V[(lane + 64) * kEP + q] = sn * vv2[cc][0] + c * vv2[cc][1];
+      for (int t = 0; t < PPW; ++t)
+#pragma unroll
+        for (int cc = 0; cc < CPL; ++cc) {
+          const int i = lane + 64 * cc;
+          const float c = Cs[t], s = Ss[t];
+          const float np_ = c * ca[t][cc][0] - s * ca[t][cc][1];
+          const float nq_ = s * ca[t][cc][0] + c * ca[t][cc][1];
+          A[i * EP + P[t]] = i == Q[t] ? 0.f : np_;
+          A[i * EP + Q[t]] = i == P[t] ? 0.f : nq_;
         }
-      }
       __syncthreads();
     }
   }
@@ -412,14 +393,14 @@ __global__ __launch_bounds__(kEighThreads) void eigh_kernel(Ctx C, EighJobs J) {
   float* vals = vec(C, bh, J.vals[job]);
   float* vecs = mat(C, bh, J.vecs[job]);
   for (int i = tid; i < d; i += kEighThreads) {
-    const float li = A[i * kEP + i];
+    const float li = A[i * EP + i];
     int rank = 0;
     for (int j = 0; j < d; ++j) {
-      const float lj = A[j * kEP + j];
+      const float lj = A[j * EP + j];
       rank += (lj > li) || (lj == li && j < i);
     }
     vals[rank] = li;
-    for (int r = 0; r < d; ++r) vecs[r * d + rank] = V[r * kEP + i];
+    for (int r = 0; r < d; ++r) vecs[r * d + rank] = Vt[i * EP + r];
   }
 }
 
@@ -1714,15 +1695,13 @@ int split_big_levels(int n, int c, int L) {
 namespace {
 // Kernels that use more than 64 KiB of dynamic LDS declare their size once. A
 // refusal is not fatal here: the launch itself reports a real limit.
-constexpr size_t kEighLds = 2 * kMaxD * kEP * sizeof(float);
+constexpr size_t kEighLds = eigh_lds_bytes(kMaxD);
 constexpr size_t kCholLds = (size_t)kMaxD * kCP * sizeof(double);
 constexpr size_t kQnormLds = (size_t)(kMaxD + 2 * kStage) * kDP * sizeof(float);
 constexpr size_t kProjLds = (size_t)(kMaxD + kStage) * kDP * sizeof(float);
 constexpr size_t kGatherLds = (size_t)kMaxC * kMaxD * sizeof(float);
 hipError_t set_lds_limits() {
   static bool done = [] {
-    (void)hipFuncSetAttribute((const void*)eigh_kernel<64>,
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)kEighLds);
     (void)hipFuncSetAttribute((const void*)eigh_kernel<128>,
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)kEighLds);
     (void)hipFuncSetAttribute((const void*)cholesky_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -1828,13 +1807,12 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
     CA_CHECK();
     hipLaunchKernelGGL(moments_finish_kernel, dim3(BH), dim3(256), 0, st, C);
     CA_CHECK();
-    const size_t eigh_lds = kEighLds;
     if (P.xf == CA_XF_PCA) {
       EighJobs J1 = {2, {M_A0, M_CK}, {M_E0, M_EK}, {V_L0, V_LK}};
       if (d <= 64)
-        hipLaunchKernelGGL(eigh_kernel<64>, dim3(BH, 2), dim3(kEighThreads), eigh_lds, st, C, J1);
+        hipLaunchKernelGGL(eigh_kernel<64>, dim3(BH, 2), dim3(kEighThreads), eigh_lds_bytes(64), st, C, J1);
       else
-        hipLaunchKernelGGL(eigh_kernel<128>, dim3(BH, 2), dim3(kEighThreads), eigh_lds, st, C, J1);
+        hipLaunchKernelGGL(eigh_kernel<128>, dim3(BH, 2), dim3(kEighThreads), kEighLds, st, C, J1);
       CA_CHECK();
     } else {
       hipLaunchKernelGGL(cholesky_kernel, dim3(BH, 2), dim3(kCholThreads), kCholLds, st, C,
@@ -1856,9 +1834,9 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
       CA_CHECK();
       EighJobs J2 = {2, {M_C2, M_C3}, {M_C2, M_C3}, {V_L2, V_L3}};
       if (d <= 64)
-        hipLaunchKernelGGL(eigh_kernel<64>, dim3(BH, 2), dim3(kEighThreads), eigh_lds, st, C, J2);
+        hipLaunchKernelGGL(eigh_kernel<64>, dim3(BH, 2), dim3(kEighThreads), eigh_lds_bytes(64), st, C, J2);
       else
-        hipLaunchKernelGGL(eigh_kernel<128>, dim3(BH, 2), dim3(kEighThreads), eigh_lds, st, C, J2);
+        hipLaunchKernelGGL(eigh_kernel<128>, dim3(BH, 2), dim3(kEighThreads), kEighLds, st, C, J2);
       CA_CHECK();
     }
     hipLaunchKernelGGL(prep_final_kernel, dim3(BH), dim3(256), 0, st, C);
