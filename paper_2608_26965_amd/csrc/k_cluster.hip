@@ -1040,33 +1040,64 @@ __global__ __launch_bounds__(256) void project_mfma_kernel(Ctx C) {
 // Highest-variance coordinate of the node's subsample, computed by one
 // wavefront: lane t owns coordinates t and t + 64. fp64, two passes over the
 // rows in order, mean = sum/m, variance = sum((y - mean)^2)/m, no contraction;
-// ties go to the lowest coordinate.
+// ties go to the lowest coordinate. The sample rows are located first (lane j
+// holds the row of sample j and j + 64), then read in batches of independent
+// loads, so a pass costs m/16 memory round trips rather than m.
 __device__ int choose_coordinate(const float* __restrict__ Y, int d, const int32_t* idx,
                                  bool identity, int start, int size, int lane) {
 #pragma clang fp contract(off)
+  constexpr int B = 16;
   const int m = size < d ? size : d;
+  int row[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int j = lane + 64 * h;
+    int r = 0;
+    if (j < m) {
+      const int p = start + (int)(((int64_t)(2 * j + 1) * size) / (2 * m));
+      r = identity ? p : idx[p];
+    }
+    row[h] = r;
+  }
   double best = -1.0;
   int bt = 0x7fffffff;
-  for (int half = 0; half < 2; ++half) {
+  for (int half = 0; half * 64 < d; ++half) {
     const int t = lane + 64 * half;
-    if (t >= d) break;
+    const bool tv = t < d;
+    const float* Yt = Y + (tv ? t : 0);
     double acc = 0.0;
-    for (int j = 0; j < m; ++j) {
-      const int p = start + (int)(((int64_t)(2 * j + 1) * size) / (2 * m));
-      const int i = identity ? p : idx[p];
-      acc = acc + (double)Y[(size_t)i * d + t];
+    for (int j0 = 0; j0 < m; j0 += B) {
+      float v[B];
+#pragma unroll
+      for (int u = 0; u < B; ++u) {
+        const int j = j0 + u;
+        const int r = __builtin_amdgcn_readlane(j < 64 ? row[0] : row[1], j & 63);
+        v[u] = Yt[(size_t)r * d];
+      }
+#pragma unroll
+      for (int u = 0; u < B; ++u)
+        if (j0 + u < m) acc = acc + (double)v[u];
     }
     const double mean = acc / (double)m;
     double acc2 = 0.0;
-    for (int j = 0; j < m; ++j) {
-      const int p = start + (int)(((int64_t)(2 * j + 1) * size) / (2 * m));
-      const int i = identity ? p : idx[p];
-      const double dv = (double)Y[(size_t)i * d + t] - mean;
-      const double sq = dv * dv;
-      acc2 = acc2 + sq;
+    for (int j0 = 0; j0 < m; j0 += B) {
+      float v[B];
+#pragma unroll
+      for (int u = 0; u < B; ++u) {
+        const int j = j0 + u;
+        const int r = __builtin_amdgcn_readlane(j < 64 ? row[0] : row[1], j & 63);
+        v[u] = Yt[(size_t)r * d];
+      }
+#pragma unroll
+      for (int u = 0; u < B; ++u)
+        if (j0 + u < m) {
+          const double dv = (double)v[u] - mean;
+          const double sq = dv * dv;
+          acc2 = acc2 + sq;
+        }
     }
     const double var = acc2 / (double)m;
-    if (var > best || (var == best && t < bt)) {
+    if (tv && (var > best || (var == best && t < bt))) {
       best = var;
       bt = t;
     }
