@@ -39,7 +39,7 @@ int check_problem(const ca_problem* p, ca::Prob* P) {
   if (p->batch < 1 || p->heads < 1) return fail(CA_E_INVALID, "batch and heads must be >= 1");
   if (p->nq < 1 || p->nk < 1) return fail(CA_E_INVALID, "nq and nk must be >= 1");
   if ((int64_t)p->batch * p->heads > (1 << 20)) return fail(CA_E_INVALID, "batch*heads too large");
-  if (p->nq > (1 << 26) || p->nk > (1 << 26)) return fail(CA_E_INVALID, "nq/nk above 2^26");
+  if (p->nq > (1 << 22) || p->nk > (1 << 22)) return fail(CA_E_INVALID, "nq/nk above 2^22");
   if (p->d < 1 || p->d > ca::kMaxD) return fail(CA_E_INVALID, "d must be in [1, %d]", ca::kMaxD);
   if (!pow2(p->cq) || !pow2(p->ck) || p->cq > ca::kMaxC || p->ck > ca::kMaxC)
     return fail(CA_E_INVALID, "cluster sizes must be powers of two in [1, %d]", ca::kMaxC);
@@ -114,7 +114,7 @@ void plan_workspace(const Prob& P, Workspace* W) {
   W->big_k = split_big_levels(P.nk, P.ck, W->levels_k);
   int bigmax = W->big_q > W->big_k ? W->big_q : W->big_k;
   W->max_big_nodes = bigmax > 0 ? (1 << (bigmax - 1)) : 1;
-  W->max_chunks = (nmax + kChunk - 1) / kChunk;
+  W->hist_slots = split_hist_slots(P, W->big_q, W->big_k);
 
   W->y_q = take(BH * P.nq * d * 4);
   W->y_k = take(BH * P.nk * d * 4);
@@ -128,8 +128,8 @@ void plan_workspace(const Prob& P, Workspace* W) {
   W->qn_part = take(BH * W->nblk_mom * (d * d + d) * 4);
   W->wops = take(BH * 3 * 2 * d * d * 2);
   W->node_state = take(2 * BH * W->max_big_nodes * kNodeInts * 4);
-  W->hist = take(2 * BH * W->max_big_nodes * kRadixBins * 4);
-  W->chunk_cnt = take(2 * BH * W->max_big_nodes * W->max_chunks * 2 * 4);
+  W->hist = take(2 * BH * W->hist_slots * kBins * 4);
+  W->chunk_cnt = take(2 * BH * W->hist_slots * 2 * 4);
   W->scores = take(BH * P.nqc * P.nkc * 4);
   W->total = off;
 }

@@ -103,8 +103,8 @@ struct Workspace {
   size_t qn_part;           // fp32 [BH][nblk_q][d*d + d]
   size_t wops;              // bf16 [BH][3][2][d][d] MFMA operands (transposed hi/lo)
   size_t node_state;        // int32 [2][BH][max_big_nodes][kNodeInts]
-  size_t hist;              // uint32 [2][BH][max_big_nodes][kRadixBins]
-  size_t chunk_cnt;         // int32 [2][BH][max_big_nodes][max_chunks][2]
+  size_t hist;              // uint32 [2][BH][hist_slots][kBins] chunk histograms
+  size_t chunk_cnt;         // int32 [2][BH][hist_slots][2] chunk prefixes (less, equal)
   // selection
   size_t scores;            // fp32 [BH][nqc][nkc]
   size_t total;
@@ -112,13 +112,14 @@ struct Workspace {
   int nblk_mom;             // row blocks per tensor for moment partials
   int levels_q, levels_k;   // split levels per side
   int big_q, big_k;         // levels done by the multi-block kernels
-  int max_big_nodes, max_chunks;
+  int max_big_nodes;        // nodes at the deepest multi-block level
+  int hist_slots;           // chunk slots of the busiest multi-block level
 };
 
 constexpr int kMats = 8;
 constexpr int kVecs = 8;
-constexpr int kNodeInts = 8;
-constexpr int kRadixBins = 2048;
+constexpr int kNodeInts = 16;
+constexpr int kBins = 4096;       // linear bins of the multi-block split select
 constexpr int kChunk = 4096;      // tokens per block in the multi-block split passes
 constexpr int kTail = 4096;       // nodes of at most this size finish in one workgroup
 constexpr int kMomRows = 2048;    // rows per moment-partial block
@@ -126,6 +127,11 @@ constexpr int kMomRows = 2048;    // rows per moment-partial block
 void plan_workspace(const Prob& P, Workspace* W);
 // Number of split levels done by the multi-block kernels (nodes above the tail size).
 int split_big_levels(int n, int c, int levels);
+// Chunk blocks per node at multi-block level l (largest node of either side
+// still split by the multi-block kernels there), and the most chunk slots any
+// multi-block level needs.
+int split_level_cpn(const Prob& P, int big_q, int big_k, int l);
+int split_hist_slots(const Prob& P, int big_q, int big_k);
 
 // ---- launchers (return hipError_t of the last launch) ----------------------
 

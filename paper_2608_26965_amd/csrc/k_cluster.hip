@@ -58,7 +58,7 @@ struct Ctx {
   int32_t* node_state;
   uint32_t* hist;
   int32_t* chunk_cnt;
-  int max_nodes, max_chunks;
+  int max_nodes, hist_slots;
 };
 
 // Matrix slots
@@ -1042,11 +1042,12 @@ __global__ __launch_bounds__(256) void project_mfma_kernel(Ctx C) {
 // rows in order, mean = sum/m, variance = sum((y - mean)^2)/m, no contraction;
 // ties go to the lowest coordinate. The sample rows are located first (lane j
 // holds the row of sample j and j + 64), then read in batches of independent
-// loads, so a pass costs m/16 memory round trips rather than m.
+// loads, so a pass costs m/32 memory round trips rather than m.
 __device__ int choose_coordinate(const float* __restrict__ Y, int d, const int32_t* idx,
-                                 bool identity, int start, int size, int lane) {
+                                 bool identity, int start, int size, int lane,
+                                 double* mean_out = nullptr, double* var_out = nullptr) {
 #pragma clang fp contract(off)
-  constexpr int B = 16;
+  constexpr int B = 32;
   const int m = size < d ? size : d;
   int row[2];
 #pragma unroll
@@ -1059,7 +1060,7 @@ __device__ int choose_coordinate(const float* __restrict__ Y, int d, const int32
     }
     row[h] = r;
   }
-  double best = -1.0;
+  double best = -1.0, bmean = 0.0;
   int bt = 0x7fffffff;
   for (int half = 0; half * 64 < d; ++half) {
     const int t = lane + 64 * half;
@@ -1099,31 +1100,66 @@ __device__ int choose_coordinate(const float* __restrict__ Y, int d, const int32
     const double var = acc2 / (double)m;
     if (tv && (var > best || (var == best && t < bt))) {
       best = var;
+      bmean = mean;
       bt = t;
     }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
     const double ob = __shfl_xor(best, o, 64);
+    const double om = __shfl_xor(bmean, o, 64);
     const int ot = __shfl_xor(bt, o, 64);
     if (ob > best || (ob == best && ot < bt)) {
       best = ob;
+      bmean = om;
       bt = ot;
     }
   }
+  if (mean_out) *mean_out = bmean;
+  if (var_out) *var_out = best;
   return bt;
 }
 
-// Node state layout (int32): 0 j*, 1 threshold prefix, 2 rank among the
-// remaining candidates, 3 left size, 4 start, 5 size, 6 arrival counter,
-// 7 number of chunks.
+// Multi-block levels. A node's split threshold is its m_L-th smallest key,
+// found exactly in two steps:
+//   keys:   every chunk block gathers its keys and counts them into kBins
+//           linear bins over [mean - 4 sd, mean + 4 sd] of the node's sample
+//           (the clamped linear map is monotone, so each bin is a contiguous
+//           key range); the chunk's histogram goes to its own slot.
+//   select: one workgroup per node sums the chunk histograms, finds the bin
+//           holding the wanted rank, collects that bin's keys (typically a
+//           few hundred) and selects exactly among them with an 8-bit radix
+//           select; it also turns the per-chunk counts below / equal to the
+//           threshold into exclusive prefixes for the stable scatter.
+// Kernel boundaries order the steps: no grid-wide fences or arrival counters.
+//
+// Node state (int32): 0 j* (-1: leaf), 1 threshold key, 2 rank among keys
+// equal to the threshold, 3 left size, 4 start, 5 size, 6 bin origin (float),
+// 7 number of chunks, 8 bin scale (float), 9 rank of the threshold.
 __device__ __forceinline__ int32_t* node_ptr(const Ctx& C, int pid, int node) {
   return C.node_state + ((size_t)pid * C.max_nodes + node) * kNodeInts;
 }
 
+__device__ __forceinline__ float key_value(uint32_t key) {
+  return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
+}
+
+// Bin of a key: floor((v - lo) * scale) clamped to [0, kBins); infinities and
+// NaNs go to the end bin their key order puts them in.
+__device__ __forceinline__ int lin_bin(uint32_t key, float lo, float scale) {
+  if (key >= 0xFF800000u) return kBins - 1;  // +inf, positive NaNs
+  if (key <= 0x007FFFFFu) return 0;          // -inf, negative NaNs
+  float t = (key_value(key) - lo) * scale;
+  t = fminf(fmaxf(t, 0.f), (float)(kBins - 1));
+  return (int)t;
+}
+
+constexpr int kPer = kChunk / 256;  // positions per thread in a 256-thread chunk block
+
 struct LevelArgs {
   int level;
   int first;  // input permutation is the identity
+  int cpn;    // chunk slots per node at this level
   const int32_t* idx_in;
   int32_t* idx_out;
 };
@@ -1141,25 +1177,33 @@ __global__ __launch_bounds__(64) void split_choose_kernel(Ctx C, LevelArgs L) {
     return;
   }
   const int32_t* idx = L.idx_in + (size_t)pid * C.nmax;
+  double mean, var;
   const int js = choose_coordinate(S.y + (size_t)bh * S.n * C.d, C.d, idx, L.first, start, size,
-                                   lane);
-  uint32_t* hist = C.hist + ((size_t)pid * C.max_nodes + node) * kRadixBins;
-  for (int b = lane; b < kRadixBins; b += 64) hist[b] = 0u;
+                                   lane, &mean, &var);
   if (lane == 0) {
+    const double sd = sqrt(var);
+    float lo = (float)(mean - 4.0 * sd), scale = (float)((double)kBins / (8.0 * sd));
+    if (!(sd > 0.0) || !isfinite(lo) || !isfinite(scale)) {
+      lo = 0.f;
+      scale = 0.f;  // one bin: the select step falls back to streaming
+    }
     const int mL = left_size(size, S.c);
     ns[0] = js;
     ns[1] = 0;
-    ns[2] = mL - 1;
+    ns[2] = 0;
     ns[3] = mL;
     ns[4] = start;
     ns[5] = size;
-    ns[6] = 0;
+    ns[6] = __float_as_int(lo);
     ns[7] = (size + kChunk - 1) / kChunk;
+    ns[8] = __float_as_int(scale);
+    ns[9] = mL - 1;
   }
 }
 
-// Block-wide exclusive scan (256 threads).
-__device__ __forceinline__ int scan256(int x, int* wsum, int* total) {
+// Block-wide exclusive scan (NT threads).
+template <int NT>
+__device__ __forceinline__ int block_scan(int x, int* wsum, int* total) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   int v = x;
 #pragma unroll
@@ -1171,143 +1215,261 @@ __device__ __forceinline__ int scan256(int x, int* wsum, int* total) {
   __syncthreads();
   int base = 0, tot = 0;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    if (i < w) base += wsum[i];
-    tot += wsum[i];
+  for (int i = 0; i < NT / 64; ++i) {
+    const int ws = wsum[i];
+    base += i < w ? ws : 0;
+    tot += ws;
   }
   __syncthreads();
   *total = tot;
   return base + v - x;
 }
 
-// Digit pass `pass` (0: bits 31..21, 1: bits 20..10, 2: bits 9..0) of the
-// radix select of the node's (m_L)-th smallest key. Pass 0 also materialises
-// the keys. The last block to finish a node picks the digit.
-__global__ __launch_bounds__(256) void split_hist_kernel(Ctx C, LevelArgs L, int pass) {
-  __shared__ int lh[kRadixBins];
-  __shared__ int wsum[4];
-  __shared__ int sh_last;
+__device__ __forceinline__ int scan256(int x, int* wsum, int* total) {
+  return block_scan<256>(x, wsum, total);
+}
+
+// Keys of one chunk and its linear-bin histogram.
+__global__ __launch_bounds__(256) void split_keys_kernel(Ctx C, LevelArgs L) {
+  __shared__ int lh[kBins];
   const int pid = blockIdx.z, side = pid / C.BH, bh = pid % C.BH, node = blockIdx.y;
   const Side& S = C.s[side];
   if (L.level >= S.big) return;
-  int32_t* ns = node_ptr(C, pid, node);
+  const int32_t* ns = node_ptr(C, pid, node);
   const int js = ns[0];
   if (js < 0) return;
-  const int start = ns[4], size = ns[5], nch = ns[7];
+  const int start = ns[4], size = ns[5];
+  const float lo = __int_as_float(ns[6]), scale = __int_as_float(ns[8]);
   const int c0 = blockIdx.x * kChunk;
   if (c0 >= size) return;
   const int c1 = min(size, c0 + kChunk);
-  const int shift = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
-  const uint32_t dmask = pass == 2 ? 1023u : 2047u;
-  const int mshift = pass == 0 ? 32 : (pass == 1 ? 21 : 10);
-  const uint32_t prefix = (uint32_t)ns[1];
-  for (int b = threadIdx.x; b < kRadixBins; b += 256) lh[b] = 0;
-  __syncthreads();
+  for (int b = threadIdx.x; b < kBins; b += 256) lh[b] = 0;
   const float* Y = S.y + (size_t)bh * S.n * C.d;
   const int32_t* idx = L.idx_in + (size_t)pid * C.nmax;
   uint32_t* keys = C.keys + (size_t)pid * C.nmax;
-  for (int o = c0 + threadIdx.x; o < c1; o += 256) {
-    const int p = start + o;
-    uint32_t key;
-    if (pass == 0) {
-      const int i = L.first ? p : idx[p];
-      key = ordered_bits(Y[(size_t)i * C.d + js]);
-      keys[p] = key;
-    } else {
-      key = keys[p];
-    }
-    if (mshift == 32 || (key >> mshift) == (prefix >> mshift))
-      atomicAdd(&lh[(key >> shift) & dmask], 1);
-  }
-  __syncthreads();
-  uint32_t* gh = C.hist + ((size_t)pid * C.max_nodes + node) * kRadixBins;
-  for (int b = threadIdx.x; b < kRadixBins; b += 256)
-    if (lh[b]) atomicAdd(&gh[b], (uint32_t)lh[b]);
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) sh_last = atomicAdd(&ns[6], 1) == nch - 1;
-  __syncthreads();
-  if (!sh_last) return;
-  __threadfence();
-  // Last block of this node: find the digit holding the wanted rank.
-  const int rank = ns[2];
-  int cnt[8], sum = 0;
+  // All of a thread's loads are issued before any is used.
+  int rows[kPer];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int b = threadIdx.x * 8 + i;
-    cnt[i] = (int)__hip_atomic_load(&gh[b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    gh[b] = 0u;
-    sum += cnt[i];
+  for (int u = 0; u < kPer; ++u) {
+    const int o = c0 + threadIdx.x + 256 * u;
+    rows[u] = o < c1 ? (L.first ? start + o : idx[start + o]) : 0;
   }
-  int tot;
-  const int before = scan256(sum, wsum, &tot);
-  if (rank >= before && rank < before + sum) {
-    int acc = before;
-    for (int i = 0; i < 8; ++i) {
-      if (rank < acc + cnt[i]) {
-        ns[1] = (int)(prefix | ((uint32_t)(threadIdx.x * 8 + i) << shift));
-        ns[2] = rank - acc;
-        break;
-      }
-      acc += cnt[i];
+  uint32_t kv[kPer];
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) kv[u] = ordered_bits(Y[(size_t)rows[u] * C.d + js]);
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int o = c0 + threadIdx.x + 256 * u;
+    if (o < c1) {
+      keys[start + o] = kv[u];
+      atomicAdd(&lh[lin_bin(kv[u], lo, scale)], 1);
     }
   }
-  if (threadIdx.x == 0) ns[6] = 0;
+  __syncthreads();
+  uint4* gh = reinterpret_cast<uint4*>(
+      C.hist + ((size_t)pid * C.hist_slots + (size_t)node * L.cpn + blockIdx.x) * kBins);
+  for (int b = threadIdx.x; b < kBins / 4; b += 256)
+    gh[b] = make_uint4((uint32_t)lh[4 * b], (uint32_t)lh[4 * b + 1], (uint32_t)lh[4 * b + 2],
+                       (uint32_t)lh[4 * b + 3]);
 }
 
-// Per-chunk counts of keys below / equal to the threshold; the last block
-// turns them into exclusive prefixes over the node's chunks.
-__global__ __launch_bounds__(256) void split_count_kernel(Ctx C, LevelArgs L) {
-  __shared__ int wsum[4];
-  __shared__ int sh_last;
-  const int pid = blockIdx.z, side = pid / C.BH, node = blockIdx.y;
+constexpr int kSelThreads = 1024;
+constexpr int kCand = 8192;         // candidates held in LDS
+constexpr int kMaxNodeChunks = 1024;  // chunks of one node (4M positions)
+static_assert(kBins == 4 * kSelThreads, "one uint4 of bins per select thread");
+
+__global__ __launch_bounds__(kSelThreads) void split_select_kernel(Ctx C, LevelArgs L) {
+  __shared__ uint32_t ckey[kCand];
+  __shared__ uint16_t cchunk[kCand];
+  __shared__ int below_ch[kMaxNodeChunks], less_ch[kMaxNodeChunks], eq_ch[kMaxNodeChunks];
+  __shared__ int rh[256];
+  __shared__ int wsum[kSelThreads / 64];
+  __shared__ int sh_bin, sh_below, sh_ncand, sh_digit, sh_rank;
+  const int pid = blockIdx.y, node = blockIdx.x, side = pid / C.BH;
   const Side& S = C.s[side];
   if (L.level >= S.big) return;
   int32_t* ns = node_ptr(C, pid, node);
   if (ns[0] < 0) return;
   const int start = ns[4], size = ns[5], nch = ns[7];
-  const int c0 = blockIdx.x * kChunk;
-  if (c0 >= size) return;
-  const int c1 = min(size, c0 + kChunk);
-  const uint32_t thr = (uint32_t)ns[1];
-  const uint32_t* keys = C.keys + (size_t)pid * C.nmax;
-  int less = 0, eq = 0;
-  for (int o = c0 + threadIdx.x; o < c1; o += 256) {
-    const uint32_t key = keys[start + o];
-    less += key < thr;
-    eq += key == thr;
+  const float lo = __int_as_float(ns[6]), scale = __int_as_float(ns[8]);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const uint4* H = reinterpret_cast<const uint4*>(
+      C.hist + ((size_t)pid * C.hist_slots + (size_t)node * L.cpn) * kBins);
+  const uint32_t* keys = C.keys + (size_t)pid * C.nmax + start;
+  for (int ch = tid; ch < nch; ch += kSelThreads) {
+    below_ch[ch] = 0;
+    less_ch[ch] = 0;
+    eq_ch[ch] = 0;
   }
-  int tl, te;
-  scan256(less, wsum, &tl);
-  scan256(eq, wsum, &te);
-  int32_t* cc = C.chunk_cnt + ((size_t)pid * C.max_nodes + node) * C.max_chunks * 2;
-  if (threadIdx.x == 0) {
-    cc[2 * blockIdx.x] = tl;
-    cc[2 * blockIdx.x + 1] = te;
-  }
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) sh_last = atomicAdd(&ns[6], 1) == nch - 1;
-  __syncthreads();
-  if (!sh_last) return;
-  __threadfence();
-  if (threadIdx.x == 0) {
-    int sl = 0, se = 0;
-    for (int ch = 0; ch < nch; ++ch) {
-      const int l = __hip_atomic_load(&cc[2 * ch], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const int e = __hip_atomic_load(&cc[2 * ch + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      cc[2 * ch] = sl;
-      cc[2 * ch + 1] = se;
-      sl += l;
-      se += e;
+  if (tid == 0) sh_ncand = 0;
+  // 1. node histogram: thread t owns bins 4t .. 4t+3
+  uint32_t nb[4] = {0u, 0u, 0u, 0u};
+  for (int ch0 = 0; ch0 < nch; ch0 += 8) {
+    uint4 hv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      hv[u] = ch0 + u < nch ? H[(size_t)(ch0 + u) * (kBins / 4) + tid] : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      nb[0] += hv[u].x;
+      nb[1] += hv[u].y;
+      nb[2] += hv[u].z;
+      nb[3] += hv[u].w;
     }
-    ns[6] = 0;
+  }
+  const int rank = ns[9];
+  int tot;
+  const int before = block_scan<kSelThreads>((int)(nb[0] + nb[1] + nb[2] + nb[3]), wsum, &tot);
+  {
+    int acc = before;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (rank >= acc && rank < acc + (int)nb[i]) {
+        sh_bin = 4 * tid + i;
+        sh_below = acc;
+      }
+      acc += (int)nb[i];
+    }
+  }
+  __syncthreads();
+  const int bstar = sh_bin, below = sh_below;
+  // 2. per-chunk counts of keys in bins below b*
+  for (int ch0 = 0; ch0 < nch; ch0 += 8) {
+    uint4 hv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      hv[u] = ch0 + u < nch && 4 * tid < bstar ? H[(size_t)(ch0 + u) * (kBins / 4) + tid]
+                                                : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      int part = (int)hv[u].x + (4 * tid + 1 < bstar ? (int)hv[u].y : 0) +
+                 (4 * tid + 2 < bstar ? (int)hv[u].z : 0) +
+                 (4 * tid + 3 < bstar ? (int)hv[u].w : 0);
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) part += __shfl_xor(part, o, 64);
+      if (lane == 0 && part) atomicAdd(&below_ch[ch0 + u], part);
+    }
+  }
+  // 3. collect the keys of bin b*
+  constexpr int B = 16;
+  for (int o0 = 0; o0 < size; o0 += B * kSelThreads) {
+    uint32_t kv[B];
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const int o = o0 + tid + kSelThreads * u;
+      kv[u] = o < size ? keys[o] : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+      const int o = o0 + tid + kSelThreads * u;
+      const bool hit = o < size && lin_bin(kv[u], lo, scale) == bstar;
+      const uint64_t m = __ballot(hit);
+      if (m == 0) continue;
+      int base = 0;
+      if (lane == 0) base = atomicAdd(&sh_ncand, __popcll(m));
+      base = __shfl(base, 0, 64);
+      if (hit) {
+        const int slot = base + (int)__popcll(m & ((1ull << lane) - 1ull));
+        if (slot < kCand) {
+          ckey[slot] = kv[u];
+          cchunk[slot] = (uint16_t)(o / kChunk);
+        }
+      }
+    }
+  }
+  __syncthreads();
+  const int ncand = sh_ncand;
+  const bool in_lds = ncand <= kCand;
+  // 4. exact select among the candidates: four 8-bit digits, high first
+  uint32_t thr = 0u;
+  int r = rank - below;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    if (tid < 256) rh[tid] = 0;
+    __syncthreads();
+    auto count = [&](uint32_t key) {
+      if (pass == 0 || (key >> (shift + 8)) == (thr >> (shift + 8)))
+        atomicAdd(&rh[(key >> shift) & 255u], 1);
+    };
+    if (in_lds) {
+      for (int i = tid; i < ncand; i += kSelThreads) count(ckey[i]);
+    } else {
+      for (int o = tid; o < size; o += kSelThreads) {
+        const uint32_t key = keys[o];
+        if (lin_bin(key, lo, scale) == bstar) count(key);
+      }
+    }
+    __syncthreads();
+    if (tid < 64) {
+      int cnt[4], sum = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        cnt[i] = rh[4 * tid + i];
+        sum += cnt[i];
+      }
+      int incl = sum;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += y;
+      }
+      int acc = incl - sum;
+      if (r >= acc && r < incl) {
+        for (int i = 0; i < 4; ++i) {
+          if (r < acc + cnt[i]) {
+            sh_digit = 4 * tid + i;
+            sh_rank = r - acc;
+            break;
+          }
+          acc += cnt[i];
+        }
+      }
+    }
+    __syncthreads();
+    thr |= (uint32_t)sh_digit << shift;
+    r = sh_rank;
+    __syncthreads();
+  }
+  // 5. per-chunk counts of candidates below / equal to the threshold
+  auto tally = [&](uint32_t key, int ch) {
+    if (key < thr) atomicAdd(&less_ch[ch], 1);
+    else if (key == thr) atomicAdd(&eq_ch[ch], 1);
+  };
+  if (in_lds) {
+    for (int i = tid; i < ncand; i += kSelThreads) tally(ckey[i], cchunk[i]);
+  } else {
+    for (int o = tid; o < size; o += kSelThreads) {
+      const uint32_t key = keys[o];
+      if (lin_bin(key, lo, scale) == bstar) tally(key, o / kChunk);
+    }
+  }
+  __syncthreads();
+  // 6. exclusive prefixes over the node's chunks
+  int32_t* cc = C.chunk_cnt + ((size_t)pid * C.hist_slots + (size_t)node * L.cpn) * 2;
+  int base_l = 0, base_e = 0;
+  for (int g = 0; g < nch; g += kSelThreads) {
+    const int ch = g + tid;
+    const int l = ch < nch ? below_ch[ch] + less_ch[ch] : 0, e = ch < nch ? eq_ch[ch] : 0;
+    int sl, se;
+    const int xl = block_scan<kSelThreads>(l, wsum, &sl);
+    const int xe = block_scan<kSelThreads>(e, wsum, &se);
+    if (ch < nch) {
+      cc[2 * ch] = base_l + xl;
+      cc[2 * ch + 1] = base_e + xe;
+    }
+    base_l += sl;
+    base_e += se;
+  }
+  if (tid == 0) {
+    ns[1] = (int)thr;
+    ns[2] = r;
   }
 }
 
-// Stable partition of every node: the m_L smallest (key, index) pairs go left
-// in node order, the rest right in node order. Nodes that are already leaves
-// are copied.
+// Stable partition of every node: the m_L smallest (key, position) pairs go
+// left in node order, the rest right in node order. Nodes that are already
+// leaves are copied.
 __global__ __launch_bounds__(256) void split_scatter_kernel(Ctx C, LevelArgs L) {
   __shared__ int wsum[4];
   const int pid = blockIdx.z, side = pid / C.BH, node = blockIdx.y;
@@ -1322,32 +1484,48 @@ __global__ __launch_bounds__(256) void split_scatter_kernel(Ctx C, LevelArgs L) 
   int32_t* idx_out = L.idx_out + (size_t)pid * C.nmax;
   const int32_t* ns = node_ptr(C, pid, node);
   if (size <= S.c) {
-    for (int o = c0 + threadIdx.x; o < c1; o += 256)
-      idx_out[start + o] = L.first ? start + o : idx_in[start + o];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int o = c0 + threadIdx.x + 256 * u;
+      if (o < c1) idx_out[start + o] = L.first ? start + o : idx_in[start + o];
+    }
     return;
   }
   const uint32_t thr = (uint32_t)ns[1];
   const int need_eq = ns[2] + 1, mL = ns[3];
-  const int32_t* cc = C.chunk_cnt + ((size_t)pid * C.max_nodes + node) * C.max_chunks * 2;
-  const int less0 = cc[2 * blockIdx.x], eq0 = cc[2 * blockIdx.x + 1];
+  const int32_t* cc =
+      C.chunk_cnt + ((size_t)pid * C.hist_slots + (size_t)node * L.cpn + blockIdx.x) * 2;
+  const int less0 = cc[0], eq0 = cc[1];
   const uint32_t* keys = C.keys + (size_t)pid * C.nmax;
-  constexpr int per = kChunk / 256;
-  const int o0 = c0 + threadIdx.x * per, o1 = min(c1, o0 + per);
+  // Each thread owns kPer consecutive positions; keys and rows are loaded
+  // together before the scan.
+  const int o0 = c0 + threadIdx.x * kPer;
+  uint32_t kv[kPer];
+  int rows[kPer];
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int o = o0 + u;
+    kv[u] = o < c1 ? keys[start + o] : 0xFFFFFFFFu;
+    rows[u] = o < c1 ? (L.first ? start + o : idx_in[start + o]) : 0;
+  }
   int less = 0, eq = 0;
-  for (int o = o0; o < o1; ++o) {
-    const uint32_t key = keys[start + o];
-    less += key < thr;
-    eq += key == thr;
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    less += o0 + u < c1 && kv[u] < thr;
+    eq += o0 + u < c1 && kv[u] == thr;
   }
   int tot;
   const int packed = scan256((less << 16) | eq, wsum, &tot);
   int lb = less0 + (packed >> 16), eb = eq0 + (packed & 0xFFFF);
-  for (int o = o0; o < o1; ++o) {
-    const uint32_t key = keys[start + o];
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int o = o0 + u;
+    if (o >= c1) break;
+    const uint32_t key = kv[u];
     const int Lo = lb + min(eb, need_eq);
     const bool left = key < thr || (key == thr && eb < need_eq);
     const int dst = left ? Lo : mL + (o - Lo);
-    if (dst >= 0 && dst < size) idx_out[start + dst] = L.first ? start + o : idx_in[start + o];
+    if (dst >= 0 && dst < size) idx_out[start + dst] = rows[u];
     lb += key < thr;
     eb += key == thr;
   }
@@ -1447,19 +1625,37 @@ __global__ __launch_bounds__(kTailThreads) void split_tail_kernel(Ctx C, int par
     }
     __syncthreads();
     // keys; slot of position o by binary search over the sub-node starts
-    for (int o = threadIdx.x; o < size; o += kTailThreads) {
-      // The last slot starting at or before o is the non-empty slot holding o:
-      // empty slots start where the next non-empty slot starts.
-      int lo = 0, hi = nslots - 1;
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (sub_start[mid] <= o)
-          lo = mid;
-        else
-          hi = mid - 1;
+    {
+      constexpr int PT = kTail / kTailThreads;
+      int gsl[PT], grow[PT];
+#pragma unroll
+      for (int u = 0; u < PT; ++u) {
+        const int o = threadIdx.x + kTailThreads * u;
+        // The last slot starting at or before o is the non-empty slot holding
+        // o: empty slots start where the next non-empty slot starts.
+        int lo = 0, hi = nslots - 1;
+        while (lo < hi) {
+          const int mid = (lo + hi + 1) >> 1;
+          if (sub_start[mid] <= o)
+            lo = mid;
+          else
+            hi = mid - 1;
+        }
+        gsl[u] = lo;
+        grow[u] = o < size && act_of[lo] >= 0 ? cur[o] : -1;
       }
-      scan[o] = lo;  // slot id (temporarily)
-      keys[o] = act_of[lo] >= 0 ? ordered_bits(Y[(size_t)cur[o] * d + sub_js[lo]]) : 0u;
+      float gv[PT];
+#pragma unroll
+      for (int u = 0; u < PT; ++u)
+        gv[u] = grow[u] >= 0 ? Y[(size_t)grow[u] * d + sub_js[gsl[u]]] : 0.f;
+#pragma unroll
+      for (int u = 0; u < PT; ++u) {
+        const int o = threadIdx.x + kTailThreads * u;
+        if (o < size) {
+          scan[o] = gsl[u];  // slot id (temporarily)
+          keys[o] = grow[u] >= 0 ? ordered_bits(gv[u]) : 0u;
+        }
+      }
     }
     // four 8-bit digit passes
     for (int pass = 0; pass < 4; ++pass) {
@@ -1707,6 +1903,30 @@ int tail_size(int c) { return c * 64 < kTail ? c * 64 : kTail; }
 
 }  // namespace
 
+int split_level_cpn(const Prob& P, int big_q, int big_k, int l) {
+  int maxs = 0;
+  for (int side = 0; side < 2; ++side) {
+    const int n = side == 0 ? P.nq : P.nk, c = side == 0 ? P.cq : P.ck;
+    if (l >= (side == 0 ? big_q : big_k)) continue;
+    for (int node = 0; node < (1 << l); ++node) {
+      int st, s;
+      node_range(n, c, l, node, &st, &s);
+      if (s > maxs) maxs = s;
+    }
+  }
+  return (maxs + kChunk - 1) / kChunk;
+}
+
+int split_hist_slots(const Prob& P, int big_q, int big_k) {
+  const int big = big_q > big_k ? big_q : big_k;
+  int slots = 1;
+  for (int l = 0; l < big; ++l) {
+    const int s = (1 << l) * split_level_cpn(P, big_q, big_k, l);
+    if (s > slots) slots = s;
+  }
+  return slots;
+}
+
 int split_big_levels(int n, int c, int L) {
   const int tail = tail_size(c);
   int l = 0;
@@ -1788,7 +2008,7 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
   C.hist = (uint32_t*)(ws + W.hist);
   C.chunk_cnt = (int32_t*)(ws + W.chunk_cnt);
   C.max_nodes = W.max_big_nodes;
-  C.max_chunks = W.max_chunks;
+  C.hist_slots = W.hist_slots;
   Side& Sq = C.s[0];
   Side& Sk = C.s[1];
   Sq.x = q;
@@ -1892,25 +2112,13 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
     L.first = l == 0;
     L.idx_in = (l & 1) ? C.idx1 : C.idx0;
     L.idx_out = (l & 1) ? C.idx0 : C.idx1;
-    int maxs = 0;
-    for (int side = 0; side < 2; ++side) {
-      const Side& S = C.s[side];
-      if (l >= S.big) continue;
-      for (int node = 0; node < (1 << l); ++node) {
-        int s0, sz;
-        node_range(S.n, S.c, l, node, &s0, &sz);
-        if (sz > maxs) maxs = sz;
-      }
-    }
-    const int cpn = (maxs + kChunk - 1) / kChunk;
+    const int cpn = split_level_cpn(P, W.big_q, W.big_k, l);
+    L.cpn = cpn;
     hipLaunchKernelGGL(split_choose_kernel, dim3(1 << l, 2 * BH), dim3(64), 0, st, C, L);
     CA_CHECK();
-    for (int pass = 0; pass < 3; ++pass) {
-      hipLaunchKernelGGL(split_hist_kernel, dim3(cpn, 1 << l, 2 * BH), dim3(256), 0, st, C, L,
-                         pass);
-      CA_CHECK();
-    }
-    hipLaunchKernelGGL(split_count_kernel, dim3(cpn, 1 << l, 2 * BH), dim3(256), 0, st, C, L);
+    hipLaunchKernelGGL(split_keys_kernel, dim3(cpn, 1 << l, 2 * BH), dim3(256), 0, st, C, L);
+    CA_CHECK();
+    hipLaunchKernelGGL(split_select_kernel, dim3(1 << l, 2 * BH), dim3(kSelThreads), 0, st, C, L);
     CA_CHECK();
     hipLaunchKernelGGL(split_scatter_kernel, dim3(cpn, 1 << l, 2 * BH), dim3(256), 0, st, C, L);
     CA_CHECK();
