@@ -173,34 +173,33 @@ __device__ __forceinline__ double sum_partials(const float* p, size_t stride, in
   return ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
 }
 
-// Reduces the partials of both sides of one head in fp64 and writes the
-// matrices the eigensolver starts from:
+// Reduces the moment partials in fp64, one element per thread, and writes
+// the matrices the eigensolver starts from:
 //   queries: metric -> Q^T Q / n;  pca -> centred covariance of Q
 //   keys:    centred covariance of K (both modes)
+// plus the means. Grid: (element blocks, BH, side).
 __global__ __launch_bounds__(256) void moments_finish_kernel(Ctx C) {
-  __shared__ double mu[kMaxD];
-  const int bh = blockIdx.x, d = C.d;
-  for (int side = 0; side < 2; ++side) {
-    const int pid = side * C.BH + bh;
-    const Side& S = C.s[side];
-    const float* part = C.mom_part + (size_t)pid * C.nblk * (d * d + d);
-    const double n = (double)S.n;
-    __syncthreads();
-    for (int t = threadIdx.x; t < d; t += 256) {
-      const double s = sum_partials(part + d * d + t, (size_t)(d * d + d), C.nblk);
-      mu[t] = s / n;
-      vec(C, bh, side == 0 ? V_MUQ : V_MUK)[t] = (float)(s / n);
-    }
-    __syncthreads();
-    const bool centred = side == 1 || C.xf == CA_XF_PCA;
-    float* M = mat(C, bh, side == 0 ? M_A0 : M_CK);
-    for (int e = threadIdx.x; e < d * d; e += 256) {
-      const double s = sum_partials(part + e, (size_t)(d * d + d), C.nblk);
-      double v = s / n;
-      if (centred) v -= mu[e / d] * mu[e % d];
-      M[e] = (float)v;
-    }
+  const int side = blockIdx.z, bh = blockIdx.y, d = C.d;
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= d * d + d) return;
+  const int pid = side * C.BH + bh;
+  const size_t stride = (size_t)d * d + d;
+  const float* part = C.mom_part + (size_t)pid * C.nblk * stride;
+  const double n = (double)C.s[side].n;
+  if (e >= d * d) {
+    const int t = e - d * d;
+    vec(C, bh, side == 0 ? V_MUQ : V_MUK)[t] = (float)(sum_partials(part + e, stride, C.nblk) / n);
+    return;
   }
+  const bool centred = side == 1 || C.xf == CA_XF_PCA;
+  const int i = e / d, j = e % d;
+  double v = sum_partials(part + e, stride, C.nblk) / n;
+  if (centred) {
+    const double mi = sum_partials(part + d * d + i, stride, C.nblk) / n;
+    const double mj = sum_partials(part + d * d + j, stride, C.nblk) / n;
+    v -= mi * mj;
+  }
+  mat(C, bh, side == 0 ? M_A0 : M_CK)[e] = (float)v;
 }
 
 // ---------------------------------------------------------------------------
@@ -217,9 +216,22 @@ __global__ __launch_bounds__(256) void moments_finish_kernel(Ctx C) {
 // as columns.
 // ---------------------------------------------------------------------------
 
+// One eigenproblem: A = B, A = B - m m^T, or A = S^T B S (- u u^T with
+// u = S^T m); the eigenvectors are oriented so that o . U[:, j] >= 0 with
+// o = u (when u is formed) or a given vector, and the split projection
+// T = F U (or U) is written in fp32 and, for bf16 inputs, as the transposed
+// hi/lo bf16 MFMA operand.
+struct EighJob {
+  int b, s, m;     // matrix B, factor S (-1: none), vector m (-1: none)
+  int rank1;       // subtract u u^T
+  int u_out;       // vector slot for u (-1: none)
+  int orient;      // orientation vector slot, used when u is not formed
+  int vecs, vals;  // oriented eigenvectors (columns, descending) and eigenvalues
+  int t_f;         // factor F of the projection T = F U (-1: T = U)
+  int t_out, wop_out;
+};
 struct EighJobs {
-  int n;
-  int in[2], vecs[2], vals[2];
+  EighJob j[2];
 };
 
 constexpr int kEighThreads = 512;
@@ -263,6 +275,54 @@ __device__ __forceinline__ void jacobi_rotation(float app, float aqq, float apq,
   *s = t * cc;
 }
 
+// 4x4 register blocks of a d x d product (d <= 128, kEighThreads threads: at
+// most two blocks per thread): acc = op(X) op(Y), op(Z) = Z or Z^T, with X, Y
+// in LDS at row stride ld and zero padding up to a multiple of 4.
+struct MMAcc {
+  float v[2][16];
+};
+
+__device__ __forceinline__ void lds_mm(const float* X, bool tX, const float* Y, bool tY, int ld,
+                                       int d, MMAcc& acc) {
+  const int d4 = (d + 3) >> 2, nb = d4 * d4;
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc.v[u][e] = 0.f;
+    const int blk = threadIdx.x + kEighThreads * u;
+    if (blk >= nb) continue;
+    const int i0 = 4 * (blk / d4), j0 = 4 * (blk % d4);
+    for (int t = 0; t < d; ++t) {
+      float x[4], y[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        x[k] = tX ? X[t * ld + i0 + k] : X[(i0 + k) * ld + t];
+        y[k] = tY ? Y[(j0 + k) * ld + t] : Y[t * ld + j0 + k];
+      }
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc.v[u][4 * a + b] = __builtin_fmaf(x[a], y[b], acc.v[u][4 * a + b]);
+    }
+  }
+}
+
+// Writes acc to an LDS matrix (stride ld); entries outside d x d stay zero.
+__device__ __forceinline__ void lds_mm_store(const MMAcc& acc, float* Z, int ld, int d) {
+  const int d4 = (d + 3) >> 2, nb = d4 * d4;
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int blk = threadIdx.x + kEighThreads * u;
+    if (blk >= nb) continue;
+    const int i0 = 4 * (blk / d4), j0 = 4 * (blk % d4);
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+        Z[(i0 + a) * ld + j0 + b] = i0 + a < d && j0 + b < d ? acc.v[u][4 * a + b] : 0.f;
+  }
+}
+
 template <int DM>
 __global__ __launch_bounds__(kEighThreads) void eigh_kernel(Ctx C, EighJobs J) {
   constexpr int EP = DM + 1;               // odd row stride: column sweeps hit distinct banks
@@ -274,18 +334,71 @@ __global__ __launch_bounds__(kEighThreads) void eigh_kernel(Ctx C, EighJobs J) {
   float* A = esh;             // [DM][EP]
   float* Vt = esh + DM * EP;  // [DM][EP], Vt[i][j] = V[j][i]
   __shared__ float red[2][NW];
+  __shared__ float uvec[DM], ovec[DM], lam[DM], sgn[DM];
+  __shared__ int rnk[DM];
   __shared__ int sh_stop;
-  const int bh = blockIdx.x, job = blockIdx.y, d = C.d, tid = threadIdx.x;
+  const int bh = blockIdx.x, d = C.d, tid = threadIdx.x;
+  const EighJob& jb = J.j[blockIdx.y];
   const int lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const float* Min = mat(C, bh, J.in[job]);
-  for (int i = wv; i < DM; i += NW)
+  // ---- prologue: the matrix to diagonalize
+  {
+    const float* Bg = mat(C, bh, jb.b);
+    const float* Sg = jb.s >= 0 ? mat(C, bh, jb.s) : nullptr;
+    for (int i = wv; i < DM; i += NW)
 #pragma unroll
-    for (int cc = 0; cc < CPL; ++cc) {
-      const int j = lane + 64 * cc;
-      A[i * EP + j] = i < d && j < d ? Min[i * d + j] : 0.f;
-      Vt[i * EP + j] = i == j ? 1.f : 0.f;
+      for (int cc = 0; cc < CPL; ++cc) {
+        const int j = lane + 64 * cc;
+        const bool in = i < d && j < d;
+        A[i * EP + j] = in ? Bg[i * d + j] : 0.f;
+        Vt[i * EP + j] = Sg ? (in ? Sg[i * d + j] : 0.f) : 0.f;  // S while it is needed
+      }
+    if (tid < DM) ovec[tid] = 0.f;
+    __syncthreads();
+    if (jb.m >= 0) {
+      // u = S^T m (or m)
+      const float* mg = vec(C, bh, jb.m);
+      if (tid < d) {
+        float u;
+        if (Sg) {
+          u = 0.f;
+          for (int t = 0; t < d; ++t) u = __builtin_fmaf(Vt[t * EP + tid], mg[t], u);
+        } else {
+          u = mg[tid];
+        }
+        uvec[tid] = u;
+        ovec[tid] = u;
+      }
+    } else if (tid < d) {
+      ovec[tid] = vec(C, bh, jb.orient)[tid];
     }
+    if (Sg) {
+      // A = S^T (B S)
+      MMAcc acc;
+      lds_mm(A, false, Vt, false, EP, d, acc);  // T1 = B S
+      __syncthreads();
+      lds_mm_store(acc, A, EP, d);
+      __syncthreads();
+      lds_mm(Vt, true, A, false, EP, d, acc);   // S^T T1
+      __syncthreads();
+      lds_mm_store(acc, A, EP, d);
+    }
+    __syncthreads();
+    if (jb.rank1)
+      for (int i = wv; i < d; i += NW)
+#pragma unroll
+        for (int cc = 0; cc < CPL; ++cc) {
+          const int j = lane + 64 * cc;
+          if (j < d) A[i * EP + j] -= uvec[i] * uvec[j];
+        }
+    if (jb.u_out >= 0 && tid < d) vec(C, bh, jb.u_out)[tid] = uvec[tid];
+    for (int i = wv; i < DM; i += NW)
+#pragma unroll
+      for (int cc = 0; cc < CPL; ++cc) {
+        const int j = lane + 64 * cc;
+        Vt[i * EP + j] = i == j ? 1.f : 0.f;
+      }
+  }
   if (tid == 0) sh_stop = 0;
   for (int sweep = 0; sweep < 40; ++sweep) {
     __syncthreads();
@@ -389,18 +502,77 @@ __global__ __launch_bounds__(kEighThreads) void eigh_kernel(Ctx C, EighJobs J) {
     }
   }
   __syncthreads();
-  // sort descending (ties by index) and write
-  float* vals = vec(C, bh, J.vals[job]);
-  float* vecs = mat(C, bh, J.vecs[job]);
-  for (int i = tid; i < d; i += kEighThreads) {
-    const float li = A[i * EP + i];
-    int rank = 0;
+  // ---- epilogue: eigenvalues, ranks (descending, ties by index), orientation
+  if (tid < d) {
+    lam[tid] = A[tid * EP + tid];
+    float o = 0.f;
+    for (int t = 0; t < d; ++t) o = __builtin_fmaf(ovec[t], Vt[tid * EP + t], o);
+    sgn[tid] = o < 0.f ? -1.f : 1.f;
+  }
+  __syncthreads();
+  if (tid < d) {
+    const float li = lam[tid];
+    int r = 0;
     for (int j = 0; j < d; ++j) {
-      const float lj = A[j * EP + j];
-      rank += (lj > li) || (lj == li && j < i);
+      const float lj = lam[j];
+      r += (lj > li) || (lj == li && j < tid);
     }
-    vals[rank] = li;
-    for (int r = 0; r < d; ++r) vecs[r * d + rank] = Vt[i * EP + r];
+    rnk[tid] = r;
+    vec(C, bh, jb.vals)[r] = li;
+  }
+  __syncthreads();
+  float* U = mat(C, bh, jb.vecs);
+  float* T = mat(C, bh, jb.t_out);
+  bf16* W = jb.wop_out >= 0 ? wop(C, bh, jb.wop_out) : nullptr;
+  // Eigenvector i becomes column rnk[i]: U[r][rnk[i]] = sgn[i] Vt[i][r].
+  for (int i = wv; i < d; i += NW)
+#pragma unroll
+    for (int cc = 0; cc < CPL; ++cc) {
+      const int r = lane + 64 * cc;
+      if (r < d) U[r * d + rnk[i]] = sgn[i] * Vt[i * EP + r];
+    }
+  auto put_t = [&](int r, int i, float v) {  // T[r][rnk[i]] = v
+    const int j = rnk[i];
+    T[r * d + j] = v;
+    if (W) {
+      const bf16 hi = (bf16)v;
+      W[j * d + r] = hi;
+      W[d * d + j * d + r] = (bf16)(v - (float)hi);
+    }
+  };
+  if (jb.t_f >= 0) {
+    // T'[r][i] = sum_t F[r][t] Vt[i][t]; F goes into the A region.
+    const float* Sg = mat(C, bh, jb.t_f);
+    for (int i = wv; i < DM; i += NW)
+#pragma unroll
+      for (int cc = 0; cc < CPL; ++cc) {
+        const int j = lane + 64 * cc;
+        A[i * EP + j] = i < d && j < d ? Sg[i * d + j] : 0.f;
+      }
+    __syncthreads();
+    MMAcc acc;
+    lds_mm(A, false, Vt, true, EP, d, acc);
+    const int d4 = (d + 3) >> 2, nb = d4 * d4;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int blk = tid + kEighThreads * u;
+      if (blk >= nb) continue;
+      const int i0 = 4 * (blk / d4), j0 = 4 * (blk % d4);
+#pragma unroll
+      for (int a2 = 0; a2 < 4; ++a2)
+#pragma unroll
+        for (int b2 = 0; b2 < 4; ++b2) {
+          const int r = i0 + a2, i = j0 + b2;
+          if (r < d && i < d) put_t(r, i, sgn[i] * acc.v[u][4 * a2 + b2]);
+        }
+    }
+  } else {
+    for (int i = wv; i < d; i += NW)
+#pragma unroll
+      for (int cc = 0; cc < CPL; ++cc) {
+        const int r = lane + 64 * cc;
+        if (r < d) put_t(r, i, sgn[i] * Vt[i * EP + r]);
+      }
   }
 }
 
@@ -417,13 +589,14 @@ constexpr int kCholThreads = 256;
 constexpr int kCP = kMaxD + 1;
 
 __global__ __launch_bounds__(kCholThreads) void cholesky_kernel(Ctx C, int in0, int out0, int in1,
-                                                                 int out1) {
+                                                                 int out1, int pack1) {
   extern __shared__ double csh[];  // [d][kCP]
   __shared__ double sh_tol;
   const int bh = blockIdx.x, job = blockIdx.y, d = C.d, tid = threadIdx.x;
   const int tr = tid >> 4, tc = tid & 15;  // 16 x 16 thread grid
   const float* M = mat(C, bh, job == 0 ? in0 : in1);
   float* F = mat(C, bh, job == 0 ? out0 : out1);
+  const int pack = job == 1 ? pack1 : -1;
   double* A = csh;
   for (int i = tr; i < d; i += 16)
     for (int k = tc; k < d; k += 16) A[i * kCP + k] = (double)M[i * d + k];
@@ -455,72 +628,17 @@ __global__ __launch_bounds__(kCholThreads) void cholesky_kernel(Ctx C, int in0, 
   }
   for (int i = tr; i < d; i += 16)
     for (int k = tc; k < d; k += 16) F[i * d + k] = k <= i ? (float)A[i * kCP + k] : 0.f;
-}
-
-// ---------------------------------------------------------------------------
-// Small dense products inside one workgroup (d x d, fp32 FMA):
-// Cm = op(A) * B with op(A) = A or A^T.
-// ---------------------------------------------------------------------------
-
-__device__ void wg_matmul(const float* Am, bool transA, const float* Bm, float* Cm, int d,
-                          float (*As)[kDP], float (*Bs)[kDP]) {
-  const int d4 = (d + 3) / 4;
-  float acc[4][16];
-#pragma unroll
-  for (int q = 0; q < 4; ++q)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) acc[q][e] = 0.f;
-  for (int t0 = 0; t0 < d; t0 += kStage) {
-    const int tn = min(kStage, d - t0);
-    __syncthreads();
-    // As[t][i] = op(A)[i][t0 + t],  Bs[t][j] = B[t0 + t][j]
-    for (int e = threadIdx.x; e < kStage * 4 * d4; e += 256) {
-      const int t = e / (4 * d4), i = e % (4 * d4);
-      const bool in = t < tn && i < d;
-      As[t][i] = in ? (transA ? Am[(t0 + t) * d + i] : Am[i * d + t0 + t]) : 0.f;
-      Bs[t][i] = in ? Bm[(t0 + t) * d + i] : 0.f;
+  if (pack >= 0) {
+    // transposed hi/lo bf16 operand of the factor (the MFMA query pass)
+    bf16* out = wop(C, bh, pack);
+    for (int e = tid; e < d * d; e += kCholThreads) {
+      const int i = e / d, k = e % d;  // out row i (output dim), column k (input dim)
+      const float w = i <= k ? (float)A[k * kCP + i] : 0.f;
+      const bf16 hi = (bf16)w;
+      out[e] = hi;
+      out[d * d + e] = (bf16)(w - (float)hi);
     }
-    __syncthreads();
-    acc_outer(As, Bs, tn, d4, acc);
   }
-  __syncthreads();
-  write_outer(Cm, d, d4, acc);
-  __threadfence_block();
-  __syncthreads();
-}
-
-// W (d x d, fp32) -> W^T as two bf16 matrices hi + lo with hi + lo = W^T to
-// about 2^-16 relative: the A operands of the MFMA projections.
-__device__ void pack_wops(const float* W, bf16* out, int d) {
-  for (int e = threadIdx.x; e < d * d; e += 256) {
-    const int i = e / d, k = e % d;  // out row i (output dim), column k (input dim)
-    const float w = W[k * d + i];
-    const bf16 hi = (bf16)w;
-    out[e] = hi;
-    out[d * d + e] = (bf16)(w - (float)hi);
-  }
-}
-
-// Metric mode, after the factorizations: S_q (F F^T = Q^T Q/n) and S_k
-// (F F^T = key covariance); C2 = S_q^T C_K S_q, the covariance of K S_q.
-__global__ __launch_bounds__(256) void prep_metric_kernel(Ctx C) {
-  __shared__ __attribute__((aligned(16))) float As[kStage][kDP];
-  __shared__ __attribute__((aligned(16))) float Bs[kStage][kDP];
-  const int bh = blockIdx.x, d = C.d;
-  float* Sq = mat(C, bh, M_E0);
-  __threadfence_block();
-  __syncthreads();
-  float* tmp = mat(C, bh, M_TK);
-  wg_matmul(mat(C, bh, M_CK), false, Sq, tmp, d, As, Bs);  // C_K S_q
-  wg_matmul(Sq, true, tmp, mat(C, bh, M_C2), d, As, Bs);   // S_q^T C_K S_q
-  // kq = mu_K^T S_q (for orienting the key axes)
-  const float* muk = vec(C, bh, V_MUK);
-  for (int j = threadIdx.x; j < d; j += 256) {
-    float s = 0.f;
-    for (int t = 0; t < d; ++t) s = __builtin_fmaf(muk[t], Sq[t * d + j], s);
-    vec(C, bh, V_KQ)[j] = s;
-  }
-  if (C.dtype == CA_BF16) pack_wops(mat(C, bh, M_EK), wop(C, bh, O_FK), d);
 }
 
 // Metric mode, queries: rho = q S_k, inv = 1/|rho| (0 if rho = 0), r = rho*inv;
@@ -597,96 +715,22 @@ __global__ __launch_bounds__(256) void qnorm_partial_kernel(Ctx C) {
   if (threadIdx.x < d) out[d * d + threadIdx.x] = csum;
 }
 
-// Covariance of r(q) (fp64 reduction) and its mean. Partials either hold
-// sums of r r^T and r directly (weighted == 0), or sums of inv^2 x x^T and
-// inv x (weighted != 0), from which cov(r) = S_k^T (sum inv^2 x x^T / n) S_k -
-// mu_r mu_r^T with mu_r = S_k^T (sum inv x) / n.
-__global__ __launch_bounds__(256) void qnorm_finish_kernel(Ctx C, int weighted) {
-  __shared__ double mu[kMaxD];
-  __shared__ __attribute__((aligned(16))) float As[kStage][kDP];
-  __shared__ __attribute__((aligned(16))) float Bs[kStage][kDP];
-  const int bh = blockIdx.x, d = C.d;
-  const float* part = C.qn_part + (size_t)bh * C.nblk * (d * d + d);
-  const double n = (double)C.s[0].n;
-  float* M = mat(C, bh, M_C3);
-  float* mur = vec(C, bh, V_MUR);
-  for (int t = threadIdx.x; t < d; t += 256) {
-    const double s = sum_partials(part + d * d + t, (size_t)(d * d + d), C.nblk);
-    mu[t] = s / n;
-  }
-  __syncthreads();
-  if (weighted) {
-    const float* Sk = mat(C, bh, M_EK);
-    // mu_r = S_k^T m
-    for (int j = threadIdx.x; j < d; j += 256) {
-      double acc = 0.0;
-      for (int t = 0; t < d; ++t) acc += (double)Sk[t * d + j] * mu[t];
-      mur[j] = (float)acc;
-    }
-    for (int e = threadIdx.x; e < d * d; e += 256)
-      M[e] = (float)(sum_partials(part + e, (size_t)(d * d + d), C.nblk) / n);
-    __threadfence_block();
-    __syncthreads();
-    float* tmp = mat(C, bh, M_TQ);
-    wg_matmul(M, false, Sk, tmp, d, As, Bs);   // W2 S_k
-    wg_matmul(Sk, true, tmp, M, d, As, Bs);    // S_k^T W2 S_k
-    for (int e = threadIdx.x; e < d * d; e += 256) M[e] -= mur[e / d] * mur[e % d];
-  } else {
-    for (int t = threadIdx.x; t < d; t += 256) mur[t] = (float)mu[t];
-    for (int e = threadIdx.x; e < d * d; e += 256) {
-      const double s = sum_partials(part + e, (size_t)(d * d + d), C.nblk);
-      M[e] = (float)(s / n - mu[e / d] * mu[e % d]);
-    }
-  }
-}
-
-// Final projection matrices with the orientation rule (every split coordinate
-// gets a non-negative mean):
-//   metric: T_K = S_q U2, W_Q = S_k U3     pca: T_K = U_K, W_Q = U_Q
-__global__ __launch_bounds__(256) void prep_final_kernel(Ctx C) {
-  __shared__ __attribute__((aligned(16))) float As[kStage][kDP];
-  __shared__ __attribute__((aligned(16))) float Bs[kStage][kDP];
-  __shared__ float sgn[2][kMaxD];
-  const int bh = blockIdx.x, d = C.d;
-  const bool metric = C.xf == CA_XF_METRIC;
-  float* Uk = mat(C, bh, metric ? M_C2 : M_EK);
-  float* Uq = mat(C, bh, metric ? M_C3 : M_E0);
-  const float* mk = vec(C, bh, metric ? V_KQ : V_MUK);
-  const float* mq = vec(C, bh, metric ? V_MUR : V_MUQ);
-  for (int j = threadIdx.x; j < d; j += 256) {
-    float sk = 0.f, sq = 0.f;
-    for (int t = 0; t < d; ++t) {
-      sk = __builtin_fmaf(mk[t], Uk[t * d + j], sk);
-      sq = __builtin_fmaf(mq[t], Uq[t * d + j], sq);
-    }
-    sgn[0][j] = sk < 0.f ? -1.f : 1.f;
-    sgn[1][j] = sq < 0.f ? -1.f : 1.f;
-  }
-  __syncthreads();
-  for (int e = threadIdx.x; e < d * d; e += 256) {
-    const int j = e % d;
-    Uk[e] *= sgn[0][j];
-    Uq[e] *= sgn[1][j];
-  }
-  __threadfence_block();
-  __syncthreads();
-  float* Tk = mat(C, bh, M_TK);
-  float* Tq = mat(C, bh, M_TQ);
-  if (metric) {
-    wg_matmul(mat(C, bh, M_E0), false, Uk, Tk, d, As, Bs);
-    wg_matmul(mat(C, bh, M_EK), false, Uq, Tq, d, As, Bs);
-  } else {
-    for (int e = threadIdx.x; e < d * d; e += 256) {
-      Tk[e] = Uk[e];
-      Tq[e] = Uq[e];
-    }
-  }
-  __threadfence_block();
-  __syncthreads();
-  if (C.dtype == CA_BF16) {
-    pack_wops(Tk, wop(C, bh, O_TK), d);
-    pack_wops(Tq, wop(C, bh, O_TQ), d);
-  }
+// Means of the query-representation partials (fp64 reduction, one element
+// per thread): M_C3 <- sum/n of the d x d part, V_MUR <- sum/n of the vector
+// part. The partials hold either r r^T and r (then cov(r) = M_C3 - mu mu^T),
+// or inv^2 x x^T and inv x (then cov(r) = S_k^T M_C3 S_k - u u^T with
+// u = S_k^T V_MUR); the eigensolver's prologue forms cov(r).
+__global__ __launch_bounds__(256) void qnorm_finish_kernel(Ctx C) {
+  const int bh = blockIdx.y, d = C.d;
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= d * d + d) return;
+  const size_t stride = (size_t)d * d + d;
+  const float* part = C.qn_part + (size_t)bh * C.nblk * stride;
+  const double v = sum_partials(part + e, stride, C.nblk) / (double)C.s[0].n;
+  if (e < d * d)
+    mat(C, bh, M_C3)[e] = (float)v;
+  else
+    vec(C, bh, V_MUR)[e - d * d] = (float)v;
 }
 
 // ---------------------------------------------------------------------------
@@ -2056,22 +2100,19 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
     else
       hipLaunchKernelGGL(moments_partial_kernel, dim3(C.nblk, 2 * BH), dim3(256), 0, st, C);
     CA_CHECK();
-    hipLaunchKernelGGL(moments_finish_kernel, dim3(BH), dim3(256), 0, st, C);
+    const dim3 fgrid((d * d + d + 255) / 256, BH, 2);
+    hipLaunchKernelGGL(moments_finish_kernel, fgrid, dim3(256), 0, st, C);
     CA_CHECK();
+    const int wq = P.dtype == CA_BF16 ? (int)O_TQ : -1, wk = P.dtype == CA_BF16 ? (int)O_TK : -1;
+    EighJobs J;
     if (P.xf == CA_XF_PCA) {
-      EighJobs J1 = {2, {M_A0, M_CK}, {M_E0, M_EK}, {V_L0, V_LK}};
-      if (d <= 64)
-        hipLaunchKernelGGL(eigh_kernel<64>, dim3(BH, 2), dim3(kEighThreads), eigh_lds_bytes(64), st, C, J1);
-      else
-        hipLaunchKernelGGL(eigh_kernel<128>, dim3(BH, 2), dim3(kEighThreads), kEighLds, st, C, J1);
-      CA_CHECK();
+      // principal axes of the centred queries and keys, oriented by the means
+      J.j[0] = {M_A0, -1, -1, 0, -1, V_MUQ, M_E0, V_L0, -1, M_TQ, wq};
+      J.j[1] = {M_CK, -1, -1, 0, -1, V_MUK, M_EK, V_LK, -1, M_TK, wk};
     } else {
       hipLaunchKernelGGL(cholesky_kernel, dim3(BH, 2), dim3(kCholThreads), kCholLds, st, C,
-                         (int)M_A0, (int)M_E0, (int)M_CK, (int)M_EK);
-      CA_CHECK();
-    }
-    if (P.xf == CA_XF_METRIC) {
-      hipLaunchKernelGGL(prep_metric_kernel, dim3(BH), dim3(256), 0, st, C);
+                         (int)M_A0, (int)M_E0, (int)M_CK, (int)M_EK,
+                         P.dtype == CA_BF16 ? (int)O_FK : -1);
       CA_CHECK();
       const size_t qlds = kQnormLds;
       if (mfma && d == 64)
@@ -2081,16 +2122,20 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
       else
         hipLaunchKernelGGL(qnorm_partial_kernel, dim3(C.nblk, BH), dim3(256), qlds, st, C);
       CA_CHECK();
-      hipLaunchKernelGGL(qnorm_finish_kernel, dim3(BH), dim3(256), 0, st, C, (int)mfma);
+      hipLaunchKernelGGL(qnorm_finish_kernel, dim3((d * d + d + 255) / 256, BH), dim3(256), 0, st, C);
       CA_CHECK();
-      EighJobs J2 = {2, {M_C2, M_C3}, {M_C2, M_C3}, {V_L2, V_L3}};
-      if (d <= 64)
-        hipLaunchKernelGGL(eigh_kernel<64>, dim3(BH, 2), dim3(kEighThreads), eigh_lds_bytes(64), st, C, J2);
+      // keys: C2 = S_q^T C_K S_q, oriented by S_q^T mu_K, T_K = S_q U2
+      J.j[0] = {M_CK, M_E0, V_MUK, 0, V_KQ, -1, M_C2, V_L2, M_E0, M_TK, wk};
+      // queries: cov(r(q)), oriented by mu_r, W_Q = S_k U3
+      if (mfma)
+        J.j[1] = {M_C3, M_EK, V_MUR, 1, V_MUR, -1, M_C3, V_L3, M_EK, M_TQ, wq};
       else
-        hipLaunchKernelGGL(eigh_kernel<128>, dim3(BH, 2), dim3(kEighThreads), kEighLds, st, C, J2);
-      CA_CHECK();
+        J.j[1] = {M_C3, -1, V_MUR, 1, -1, -1, M_C3, V_L3, M_EK, M_TQ, wq};
     }
-    hipLaunchKernelGGL(prep_final_kernel, dim3(BH), dim3(256), 0, st, C);
+    if (d <= 64)
+      hipLaunchKernelGGL(eigh_kernel<64>, dim3(BH, 2), dim3(kEighThreads), eigh_lds_bytes(64), st, C, J);
+    else
+      hipLaunchKernelGGL(eigh_kernel<128>, dim3(BH, 2), dim3(kEighThreads), kEighLds, st, C, J);
     CA_CHECK();
   }
   {
