@@ -31,7 +31,7 @@ __device__ __forceinline__ size_t out_row(int bh, int i, int nq, int H, int d, i
 }
 
 template <int D, int CQ>
-__global__ __launch_bounds__(CQ * 2) void comp_bf16_kernel(
+__global__ __launch_bounds__(CQ * 2, (D == 64 ? 2 : 1)) void comp_bf16_kernel(
     const bf16* __restrict__ qp, const float* __restrict__ cent_k,
     const float* __restrict__ cent_v, const int32_t* __restrict__ count_k,
     const int32_t* __restrict__ lists, int nq, int H, int nqc, int nkc, int k, float sl2,
@@ -48,7 +48,7 @@ __global__ __launch_bounds__(CQ * 2) void comp_bf16_kernel(
   constexpr int VP = CT + 8;
   __shared__ __attribute__((aligned(16))) bf16 Ks[CT * KP];
   __shared__ __attribute__((aligned(16))) bf16 Vs[D * VP];
-  __shared__ float bias[CT];
+  __shared__ __attribute__((aligned(16))) float bias[CT];
   __shared__ uint32_t selmask[kMaskWords];
 
   const int item = xcd_remap(blockIdx.x, total);
@@ -83,36 +83,109 @@ __global__ __launch_bounds__(CQ * 2) void comp_bf16_kernel(
     const float* ckh = cent_k + (size_t)bh * nkc * D;
     const float* cvh = cent_v + (size_t)bh * nkc * D;
     const int32_t* cnth = count_k + (size_t)bh * nkc;
-    for (int b0 = 0; b0 < nkc; b0 += CT) {
-      __syncthreads();  // previous tile fully consumed; selmask complete
-      // Stage centroid keys (rows) and values (transposed) as bf16.
-      for (int e = tid; e < CT * (D / 4); e += T) {
-        const int row = e / (D / 4), c4 = (e % (D / 4)) * 4, b = b0 + row;
-        float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), vv = kv;
-        if (b < nkc) {
-          kv = *(const float4*)(ckh + (size_t)b * D + c4);
-          vv = *(const float4*)(cvh + (size_t)b * D + c4);
-        }
-        bf16x4 k4 = {f2bf(kv.x), f2bf(kv.y), f2bf(kv.z), f2bf(kv.w)};
-        *(bf16x4*)&Ks[row * KP + c4] = k4;
-        Vs[(c4 + 0) * VP + row] = f2bf(vv.x);
-        Vs[(c4 + 1) * VP + row] = f2bf(vv.y);
-        Vs[(c4 + 2) * VP + row] = f2bf(vv.z);
-        Vs[(c4 + 3) * VP + row] = f2bf(vv.w);
+    // Staging tasks: K rows as 8-column chunks (one 16-byte LDS store each);
+    // V as 8-centroid x 4-column blocks, transposed in registers into four
+    // 16-byte stores. The global loads of tile t+1 are issued before the
+    // products of tile t, so their latency hides behind the matrix work.
+    constexpr int NKT = CT * (D / 8) / T;
+    constexpr int NVT = (CT / 8) * (D / 4) / T;
+    constexpr int NBT = (CT + T - 1) / T;
+    static_assert(NKT * T == CT * (D / 8) && NVT * T == (CT / 8) * (D / 4), "staging split");
+    // (without registers to spare, a tile is loaded just before it is staged)
+    constexpr bool kPrefetch = NKT * 2 + NVT * 8 <= 16;
+    float4 kv[NKT][2], vv[NVT][8];
+    int cv[NBT];
+    __syncthreads();  // selmask complete
+    // Tiles holding at least one unselected centroid, in order.
+    auto tile_live = [&](int b0) {
+      int any = 0;
+      for (int e = b0 >> 5; e < ((b0 + CT) >> 5) && e < nwords; ++e) {
+        const uint32_t wmask = e == nwords - 1 && (nkc & 31) ? (1u << (nkc & 31)) - 1u : ~0u;
+        any |= (~selmask[e] & wmask) != 0u;
       }
-      int live = 0;
-      for (int e = tid; e < CT; e += T) {
-        const int b = b0 + e;
-        float bi = -INFINITY;
-        if (b < nkc && !((selmask[b >> 5] >> (b & 31)) & 1u)) {
-          const int c = cnth[b];
-          bi = c > 0 ? __builtin_amdgcn_logf((float)c) : -INFINITY;  // log2 of the size
-        }
-        live |= bi != -INFINITY;
-        bias[e] = bi;
+      return any;
+    };
+    auto next_live = [&](int b0) {
+      while (b0 < nkc && !tile_live(b0)) b0 += CT;
+      return b0;
+    };
+    auto load_k = [&](int b0) {
+#pragma unroll
+      for (int u = 0; u < NKT; ++u) {
+        const int i = tid + T * u, row = i / (D / 8), c8 = i % (D / 8), b = b0 + row;
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+          kv[u][hh] = b < nkc ? *(const float4*)(ckh + (size_t)b * D + 8 * c8 + 4 * hh)
+                              : make_float4(0.f, 0.f, 0.f, 0.f);
       }
-      // Uniform skip of tiles whose centroids are all selected (or past nkc).
-      if (!__syncthreads_or(live)) continue;
+#pragma unroll
+      for (int u = 0; u < NBT; ++u) {
+        const int e = tid + T * u, b = b0 + e;
+        cv[u] = e < CT && b < nkc ? cnth[b] : 0;
+      }
+    };
+    auto load_v = [&](int b0) {
+#pragma unroll
+      for (int u = 0; u < NVT; ++u) {
+        const int i = tid + T * u, g = i % (CT / 8), cc = i / (CT / 8);
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+          const int b = b0 + 8 * g + r;
+          vv[u][r] = b < nkc ? *(const float4*)(cvh + (size_t)b * D + 4 * cc)
+                             : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      }
+    };
+    auto store_k = [&](int b0) {
+#pragma unroll
+      for (int u = 0; u < NKT; ++u) {
+        const int i = tid + T * u, row = i / (D / 8), c8 = i % (D / 8);
+        const float f[8] = {kv[u][0].x, kv[u][0].y, kv[u][0].z, kv[u][0].w,
+                            kv[u][1].x, kv[u][1].y, kv[u][1].z, kv[u][1].w};
+        *(bf16x8*)&Ks[row * KP + 8 * c8] = pack8(f);
+      }
+#pragma unroll
+      for (int u = 0; u < NBT; ++u) {
+        const int e = tid + T * u, b = b0 + e;
+        if (e < CT) {
+          float bi = -INFINITY;
+          if (b < nkc && !((selmask[b >> 5] >> (b & 31)) & 1u) && cv[u] > 0)
+            bi = __builtin_amdgcn_logf((float)cv[u]);  // log2 of the size
+          bias[e] = bi;
+        }
+      }
+    };
+    auto store_v = [&]() {
+#pragma unroll
+      for (int u = 0; u < NVT; ++u) {
+        const int i = tid + T * u, g = i % (CT / 8), cc = i / (CT / 8);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          float f[8];
+#pragma unroll
+          for (int r = 0; r < 8; ++r)
+            f[r] = j == 0 ? vv[u][r].x : (j == 1 ? vv[u][r].y : (j == 2 ? vv[u][r].z : vv[u][r].w));
+          *(bf16x8*)&Vs[(4 * cc + j) * VP + 8 * g] = pack8(f);
+        }
+      }
+    };
+    int b0 = next_live(0);
+    if (kPrefetch && b0 < nkc) {
+      load_k(b0);
+      load_v(b0);
+    }
+    while (b0 < nkc) {
+      __syncthreads();  // the previous tile is fully consumed
+      if (!kPrefetch) load_k(b0);
+      store_k(b0);
+      if (!kPrefetch) load_v(b0);
+      store_v();
+      __syncthreads();
+      const int b1 = next_live(b0 + CT);
+      if (kPrefetch && b1 < nkc) {
+        load_k(b1);
+        load_v(b1);
+      }
 
       f32x16 sacc[MT];
 #pragma unroll
@@ -126,16 +199,27 @@ __global__ __launch_bounds__(CQ * 2) void comp_bf16_kernel(
           sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qreg[ks], sacc[mt], 0, 0, 0);
         }
       }
-      // logits in log2 units: scale*log2e*q.kbar + log2|b|
+      // logits in log2 units: scale*log2e*q.kbar + log2|b|. The bias of
+      // accumulator r of row tile mt is bias[32 mt + (r & 7) + 16 (r >> 3) + 8 h]:
+      // two runs of 8 consecutive entries, read as four 16-byte loads.
       float mx = -INFINITY;
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+      for (int mt = 0; mt < MT; ++mt) {
+        float bv[16];
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const float4 b0v = *(const float4*)&bias[32 * mt + 16 * hh + 8 * h];
+          const float4 b1v = *(const float4*)&bias[32 * mt + 16 * hh + 8 * h + 4];
+          bv[8 * hh + 0] = b0v.x, bv[8 * hh + 1] = b0v.y, bv[8 * hh + 2] = b0v.z, bv[8 * hh + 3] = b0v.w;
+          bv[8 * hh + 4] = b1v.x, bv[8 * hh + 5] = b1v.y, bv[8 * hh + 6] = b1v.z, bv[8 * hh + 7] = b1v.w;
+        }
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float t = __builtin_fmaf(sacc[mt][r], sl2, bias[acc_key(mt, r, h)]);
+          const float t = __builtin_fmaf(sacc[mt][r], sl2, bv[r]);
           sacc[mt][r] = t;
           mx = fmaxf(mx, t);
         }
+      }
       mx = fmaxf(mx, wave_xor32(mx));
       const float m_new = fmaxf(m_run, mx);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
@@ -147,11 +231,9 @@ __global__ __launch_bounds__(CQ * 2) void comp_bf16_kernel(
         for (int s = 0; s < 2; ++s) {
           float pv[8];
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            pv[j] = __builtin_amdgcn_exp2f(sacc[mt][8 * s + j] - m_new);
-            lsum += pv[j];
-          }
+          for (int j = 0; j < 8; ++j) pv[j] = __builtin_amdgcn_exp2f(sacc[mt][8 * s + j] - m_new);
           pb[mt][s] = pack8(pv);
+          lsum = sum8(pb[mt][s], lsum);
         }
       l_run = l_run * alpha + lsum;
       m_run = m_new;
@@ -168,6 +250,7 @@ __global__ __launch_bounds__(CQ * 2) void comp_bf16_kernel(
             oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[mt][s], oacc[dt], 0, 0, 0);
           }
       }
+      b0 = b1;
     }
   }
 
