@@ -31,6 +31,20 @@ WORKLOAD = dict(cfg=2, name="tabular-8h-n65536-d64-bf16-c128-keep1/8", heads=8, 
                 c=128, keep=1 / 8)
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
+# HBM bytes per launch of the attention kernel from rocprofv3 FETCH_SIZE and
+# WRITE_SIZE, scaled by a plain-copy calibration (see the traffic summary under
+# profiles/), valid for the kernel source with this fingerprint only.
+ATTN_TRAFFIC = {"fingerprint": "1c44fc85fedb5fcc", "bytes": 1.556e9}
+
+
+def attn_fingerprint():
+    """sha256 over k_attn.hip then attn_tile.h (first 16 hex digits)."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("k_attn.hip", "attn_tile.h"):
+        with open(os.path.join(ROOT, "paper_2608_26965_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def cpu_model():
@@ -145,7 +159,8 @@ def main():
         "roofline": {"kernel": "attn_bf16_kernel<64,128,128>", "bound": "mfma",
                      "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None},
+                     "traffic": (ATTN_TRAFFIC["bytes"]
+                                 if attn_fingerprint() == ATTN_TRAFFIC["fingerprint"] else None)},
         "compensate_tflops": round(f_comp / (call_ms[3] * 1e-3) / 1e12, 2),
     }
     if not args.no_cpu_baseline:
