@@ -234,7 +234,14 @@ struct EighJobs {
   EighJob j[2];
 };
 
-constexpr int kEighThreads = 512;
+// Threads of the eigensolver workgroup: a Jacobi step is a chain of LDS
+// round trips, so the most wavefronts a workgroup can have (16) issue each
+// step's traffic with the most parallelism (measured: 8 -> 16 wavefronts
+// takes d = 64 from 577 to 519 us for 16 problems; 4 wavefronts is slower).
+template <int DM>
+constexpr int eigh_threads() {
+  return 1024;
+}
 
 __host__ __device__ constexpr size_t eigh_lds_bytes(int dm) {
   return 2 * (size_t)dm * (dm + 1) * sizeof(float);
@@ -275,13 +282,14 @@ __device__ __forceinline__ void jacobi_rotation(float app, float aqq, float apq,
   *s = t * cc;
 }
 
-// 4x4 register blocks of a d x d product (d <= 128, kEighThreads threads: at
-// most two blocks per thread): acc = op(X) op(Y), op(Z) = Z or Z^T, with X, Y
+// 4x4 register blocks of a d x d product (d <= 128, NT threads: at most two
+// blocks per thread): acc = op(X) op(Y), op(Z) = Z or Z^T, with X, Y
 // in LDS at row stride ld and zero padding up to a multiple of 4.
 struct MMAcc {
   float v[2][16];
 };
 
+template <int NT>
 __device__ __forceinline__ void lds_mm(const float* X, bool tX, const float* Y, bool tY, int ld,
                                        int d, MMAcc& acc) {
   const int d4 = (d + 3) >> 2, nb = d4 * d4;
@@ -289,7 +297,7 @@ __device__ __forceinline__ void lds_mm(const float* X, bool tX, const float* Y, 
   for (int u = 0; u < 2; ++u) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc.v[u][e] = 0.f;
-    const int blk = threadIdx.x + kEighThreads * u;
+    const int blk = threadIdx.x + NT * u;
     if (blk >= nb) continue;
     const int i0 = 4 * (blk / d4), j0 = 4 * (blk % d4);
     for (int t = 0; t < d; ++t) {
@@ -308,11 +316,12 @@ __device__ __forceinline__ void lds_mm(const float* X, bool tX, const float* Y, 
 }
 
 // Writes acc to an LDS matrix (stride ld); entries outside d x d stay zero.
+template <int NT>
 __device__ __forceinline__ void lds_mm_store(const MMAcc& acc, float* Z, int ld, int d) {
   const int d4 = (d + 3) >> 2, nb = d4 * d4;
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
-    const int blk = threadIdx.x + kEighThreads * u;
+    const int blk = threadIdx.x + NT * u;
     if (blk >= nb) continue;
     const int i0 = 4 * (blk / d4), j0 = 4 * (blk % d4);
 #pragma unroll
@@ -324,9 +333,11 @@ __device__ __forceinline__ void lds_mm_store(const MMAcc& acc, float* Z, int ld,
 }
 
 template <int DM>
-__global__ __launch_bounds__(kEighThreads) void eigh_kernel(Ctx C, EighJobs J) {
+__global__ __launch_bounds__(eigh_threads<DM>()) void eigh_kernel(Ctx C, EighJobs J) {
+  constexpr int NT = eigh_threads<DM>();
+  static_assert((DM / 4) * (DM / 4) <= 2 * NT, "two 4x4 product blocks per thread");
   constexpr int EP = DM + 1;               // odd row stride: column sweeps hit distinct banks
-  constexpr int NW = kEighThreads / 64;
+  constexpr int NW = NT / 64;
   constexpr int PPW = DM / 2 / NW;         // pairs per wavefront and step
   constexpr int CPL = DM / 64;             // columns (rows) per lane in a row (column) pass
   static_assert(PPW >= 1 && CPL >= 1, "matrix size");
@@ -375,13 +386,13 @@ __global__ __launch_bounds__(kEighThreads) void eigh_kernel(Ctx C, EighJobs J) {
     if (Sg) {
       // A = S^T (B S)
       MMAcc acc;
-      lds_mm(A, false, Vt, false, EP, d, acc);  // T1 = B S
+      lds_mm<NT>(A, false, Vt, false, EP, d, acc);  // T1 = B S
       __syncthreads();
-      lds_mm_store(acc, A, EP, d);
+      lds_mm_store<NT>(acc, A, EP, d);
       __syncthreads();
-      lds_mm(Vt, true, A, false, EP, d, acc);   // S^T T1
+      lds_mm<NT>(Vt, true, A, false, EP, d, acc);   // S^T T1
       __syncthreads();
-      lds_mm_store(acc, A, EP, d);
+      lds_mm_store<NT>(acc, A, EP, d);
     }
     __syncthreads();
     if (jb.rank1)
@@ -551,11 +562,11 @@ __global__ __launch_bounds__(kEighThreads) void eigh_kernel(Ctx C, EighJobs J) {
       }
     __syncthreads();
     MMAcc acc;
-    lds_mm(A, false, Vt, true, EP, d, acc);
+    lds_mm<NT>(A, false, Vt, true, EP, d, acc);
     const int d4 = (d + 3) >> 2, nb = d4 * d4;
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      const int blk = tid + kEighThreads * u;
+      const int blk = tid + NT * u;
       if (blk >= nb) continue;
       const int i0 = 4 * (blk / d4), j0 = 4 * (blk % d4);
 #pragma unroll
@@ -2133,9 +2144,9 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
         J.j[1] = {M_C3, -1, V_MUR, 1, -1, -1, M_C3, V_L3, M_EK, M_TQ, wq};
     }
     if (d <= 64)
-      hipLaunchKernelGGL(eigh_kernel<64>, dim3(BH, 2), dim3(kEighThreads), eigh_lds_bytes(64), st, C, J);
+      hipLaunchKernelGGL(eigh_kernel<64>, dim3(BH, 2), dim3(eigh_threads<64>()), eigh_lds_bytes(64), st, C, J);
     else
-      hipLaunchKernelGGL(eigh_kernel<128>, dim3(BH, 2), dim3(kEighThreads), kEighLds, st, C, J);
+      hipLaunchKernelGGL(eigh_kernel<128>, dim3(BH, 2), dim3(eigh_threads<128>()), kEighLds, st, C, J);
     CA_CHECK();
   }
   {
