@@ -1590,10 +1590,10 @@ __global__ __launch_bounds__(256) void split_scatter_kernel(Ctx C, LevelArgs L) 
 // workgroup: per level every active sub-node picks its coordinate (one
 // wavefront each), keys are gathered, a four-pass 8-bit radix select runs on
 // per-sub-node LDS histograms, and a block-wide scan partitions stably.
-constexpr int kTailThreads = 512;
+constexpr int kTailThreads = 1024;
 constexpr int kMaxSub = 32;
 
-__device__ __forceinline__ int scan512(int x, int* wsum) {
+__device__ __forceinline__ int scan_tail(int x, int* wsum) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   int v = x;
 #pragma unroll
@@ -1639,11 +1639,12 @@ __global__ __launch_bounds__(kTailThreads) void split_tail_kernel(Ctx C, int par
   for (int r = 0; r < nsub_levels; ++r) {
     const int nslots = 1 << r;
     __syncthreads();
-    if (threadIdx.x == 0) {
-      // Sub-node ranges at this level (relative to the node) and the active list.
-      int nact = 0;
-      for (int sl = 0; sl < nslots; ++sl) {
-        int st = 0, s = size;
+    if (threadIdx.x < 64) {
+      // Sub-node ranges at this level (relative to the node), one lane per
+      // slot (at most tail / c <= 64 slots), and the active list.
+      const int sl = threadIdx.x;
+      int st = 0, s = size;
+      if (sl < nslots) {
         for (int b = r - 1; b >= 0; --b) {
           const int bit = (sl >> b) & 1;
           const int mL = s > c ? left_size(s, c) : s;
@@ -1654,16 +1655,20 @@ __global__ __launch_bounds__(kTailThreads) void split_tail_kernel(Ctx C, int par
             s = mL;
           }
         }
+      }
+      const bool act = sl < nslots && s > c;
+      const uint64_t am = __ballot(act);
+      if (sl < nslots) {
+        const int rank = (int)__popcll(am & ((1ull << sl) - 1ull));
         sub_start[sl] = st;
         sub_size[sl] = s;
-        act_of[sl] = -1;
-        if (s > c) {
-          act_of[sl] = nact;
-          act_list[nact++] = sl;
-        }
+        act_of[sl] = act ? rank : -1;
+        if (act) act_list[rank] = sl;
       }
-      sub_start[nslots] = size;
-      sh_nact = nact;
+      if (sl == 0) {
+        sub_start[nslots] = size;
+        sh_nact = (int)__popcll(am);
+      }
     }
     __syncthreads();
     const int nact = sh_nact;
@@ -1769,7 +1774,7 @@ __global__ __launch_bounds__(kTailThreads) void split_tail_kernel(Ctx C, int par
       less += keys[o] < thr;
       eq += keys[o] == thr;
     }
-    const int packed0 = scan512((less << 16) | eq, wsum);
+    const int packed0 = scan_tail((less << 16) | eq, wsum);
     // exclusive prefix at every position (packed), then per-sub-node offsets
     int run = packed0;
     int slots_local[per];
