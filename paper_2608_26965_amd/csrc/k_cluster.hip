@@ -1096,13 +1096,14 @@ __global__ __launch_bounds__(256) void project_mfma_kernel(Ctx C) {
 // wavefront: lane t owns coordinates t and t + 64. fp64, two passes over the
 // rows in order, mean = sum/m, variance = sum((y - mean)^2)/m, no contraction;
 // ties go to the lowest coordinate. The sample rows are located first (lane j
-// holds the row of sample j and j + 64), then read in batches of independent
-// loads, so a pass costs m/32 memory round trips rather than m.
+// holds the row of sample j and j + 64), then read in batches of B
+// independent loads; with at most B samples both passes use the one batch, so
+// the whole choice costs two memory round trips (B = 64 where registers allow).
+template <int B>
 __device__ int choose_coordinate(const float* __restrict__ Y, int d, const int32_t* idx,
                                  bool identity, int start, int size, int lane,
                                  double* mean_out = nullptr, double* var_out = nullptr) {
 #pragma clang fp contract(off)
-  constexpr int B = 32;
   const int m = size < d ? size : d;
   int row[2];
 #pragma unroll
@@ -1122,14 +1123,17 @@ __device__ int choose_coordinate(const float* __restrict__ Y, int d, const int32
     const bool tv = t < d;
     const float* Yt = Y + (tv ? t : 0);
     double acc = 0.0;
-    for (int j0 = 0; j0 < m; j0 += B) {
-      float v[B];
+    float v[B];
+    auto load = [&](int j0) {
 #pragma unroll
       for (int u = 0; u < B; ++u) {
         const int j = j0 + u;
         const int r = __builtin_amdgcn_readlane(j < 64 ? row[0] : row[1], j & 63);
         v[u] = Yt[(size_t)r * d];
       }
+    };
+    for (int j0 = 0; j0 < m; j0 += B) {
+      load(j0);
 #pragma unroll
       for (int u = 0; u < B; ++u)
         if (j0 + u < m) acc = acc + (double)v[u];
@@ -1137,13 +1141,7 @@ __device__ int choose_coordinate(const float* __restrict__ Y, int d, const int32
     const double mean = acc / (double)m;
     double acc2 = 0.0;
     for (int j0 = 0; j0 < m; j0 += B) {
-      float v[B];
-#pragma unroll
-      for (int u = 0; u < B; ++u) {
-        const int j = j0 + u;
-        const int r = __builtin_amdgcn_readlane(j < 64 ? row[0] : row[1], j & 63);
-        v[u] = Yt[(size_t)r * d];
-      }
+      if (B < 64 || m > B) load(j0);  // (a single batch of 64 is still in registers)
 #pragma unroll
       for (int u = 0; u < B; ++u)
         if (j0 + u < m) {
@@ -1233,7 +1231,7 @@ __global__ __launch_bounds__(64) void split_choose_kernel(Ctx C, LevelArgs L) {
   }
   const int32_t* idx = L.idx_in + (size_t)pid * C.nmax;
   double mean, var;
-  const int js = choose_coordinate(S.y + (size_t)bh * S.n * C.d, C.d, idx, L.first, start, size,
+  const int js = choose_coordinate<64>(S.y + (size_t)bh * S.n * C.d, C.d, idx, L.first, start, size,
                                    lane, &mean, &var);
   if (lane == 0) {
     const double sd = sqrt(var);
@@ -1676,7 +1674,7 @@ __global__ __launch_bounds__(kTailThreads) void split_tail_kernel(Ctx C, int par
     // coordinate choice: one wavefront per active sub-node
     for (int a = w; a < nact; a += kTailThreads / 64) {
       const int sl = act_list[a];
-      const int js = choose_coordinate(Y, d, cur, false, sub_start[sl], sub_size[sl], lane);
+      const int js = choose_coordinate<32>(Y, d, cur, false, sub_start[sl], sub_size[sl], lane);
       if (lane == 0) {
         sub_js[sl] = js;
         sub_thr[sl] = 0;
