@@ -113,7 +113,7 @@ def main():
         if ev:
             ev[3].record()
         ca.compensate(p, r["qp"], r["cent_k"], r["cent_v"], r["count_k"], lists, keep_k, op, lse,
-                      r["perm_q"], out=out)
+                      r["perm_q"], out=out, ws=ws)
         if ev:
             ev[4].record()
 

@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define CA_ABI_VERSION 1
+#define CA_ABI_VERSION 2
 
 #if defined(__GNUC__) || defined(__clang__)
 #define CA_API __attribute__((visibility("default")))
@@ -128,9 +128,10 @@ CA_API const char* ca_status_str(int status);
 /* Detail of the last non-OK status returned on the calling thread ("" if none). */
 CA_API const char* ca_last_error(void);
 
-/* Bytes of workspace ca_cluster and ca_select need for this problem with k
- * kept key clusters (k is only used for validation; the size does not depend
- * on it). Host-only; enqueues nothing. Workspace must be 256-byte aligned. */
+/* Bytes of workspace ca_cluster, ca_select and ca_compensate need for this
+ * problem with k kept key clusters (k is only used for validation; the size
+ * does not depend on it). Host-only; enqueues nothing. Workspace must be
+ * 256-byte aligned. */
 CA_API int ca_workspace_size(const ca_problem* p, int32_t k, size_t* bytes);
 
 /* Step 1: clustering (Method: Clustering, Recursive splitting - diagonalized
@@ -199,11 +200,14 @@ CA_API int ca_block_sparse_attn(const ca_problem* p, const void* qp, const void*
  * qp, op: [BH][nq_pad][d] dtype; cent_k, cent_v: [BH][nkc][d] fp32; count_k:
  * [BH][nkc]; lists: [BH][nqc][k]; lse: [BH][nq_pad] fp32; perm_q: [BH][nq];
  * out: [B,H,nq,d] in the problem layout and dtype; lse_out: optional
- * [BH][nq] fp32 in original order. */
+ * [BH][nq] fp32 in original order. ws: device workspace of ws_bytes >=
+ * ca_workspace_size(), where the bf16 path stages the centroids as bf16
+ * tiles; required only for bf16 with enable != 0 and k < nkc (otherwise it
+ * may be NULL with ws_bytes 0). */
 CA_API int ca_compensate(const ca_problem* p, const void* qp, const float* cent_k, const float* cent_v,
                   const int32_t* count_k, const int32_t* lists, int32_t k, float scale,
                   int32_t enable, const void* op, const float* lse, const int32_t* perm_q,
-                  void* out, float* lse_out, void* stream);
+                  void* out, float* lse_out, void* ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

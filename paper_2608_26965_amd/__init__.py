@@ -157,16 +157,19 @@ def block_sparse_attn(p: Problem, qp, kp, vp, count_k, lists, keep_k: int, scale
 
 
 def compensate(p: Problem, qp, cent_k, cent_v, count_k, lists, keep_k: int, op, lse, perm_q,
-               scale: float = 0.0, enable: bool = True, want_lse: bool = False, out=None):
+               scale: float = 0.0, enable: bool = True, want_lse: bool = False, out=None,
+               ws=None):
     """Step 4. Returns (out in the problem layout, lse [BH,nq] or None)."""
     dev = op.device
     if out is None:
         out = torch.empty(p.shape(p.nq), dtype=p.dtype, device=dev)
     lse_out = torch.empty(p.bh, p.nq, dtype=torch.float32, device=dev) if want_lse else None
+    if ws is None and enable and p.dtype == torch.bfloat16 and keep_k < p.nkc:
+        ws = workspace(p, dev, keep_k)
     st = _lib.load().ca_compensate(p.c(), _ptr(qp), _ptr(cent_k), _ptr(cent_v), _ptr(count_k),
                                    _ptr(lists), keep_k, float(scale), int(bool(enable)), _ptr(op),
-                                   _ptr(lse), _ptr(perm_q), _ptr(out), _ptr(lse_out),
-                                   _stream(dev))
+                                   _ptr(lse), _ptr(perm_q), _ptr(out), _ptr(lse_out), _ptr(ws),
+                                   0 if ws is None else ws.numel(), _stream(dev))
     _lib.check(st, "ca_compensate")
     return out, lse_out
 
@@ -192,11 +195,12 @@ def forward(q, k, v, cq=128, ck=None, keep=None, keep_k=None, transform="metric"
     if keep_k is None:
         keep_k = keep_to_k(1.0 / 8 if keep is None else keep, p.nkc)
     sc = 0.0 if scale is None else float(scale)
-    c = cluster(p, q, k, v)
-    lists, _ = select(p, c["cent_q"], c["cent_k"], keep_k)
+    ws = workspace(p, q.device, keep_k)
+    c = cluster(p, q, k, v, ws=ws)
+    lists, _ = select(p, c["cent_q"], c["cent_k"], keep_k, ws=ws)
     op, lse = block_sparse_attn(p, c["qp"], c["kp"], c["vp"], c["count_k"], lists, keep_k, sc)
     out, lse_out = compensate(p, c["qp"], c["cent_k"], c["cent_v"], c["count_k"], lists, keep_k,
-                              op, lse, c["perm_q"], sc, compensation, want_lse=return_parts)
+                              op, lse, c["perm_q"], sc, compensation, want_lse=return_parts, ws=ws)
     if return_parts:
         return out, dict(c, lists=lists, op=op, lse_s=lse, lse=lse_out, problem=p)
     return out

@@ -76,7 +76,7 @@ def load() -> ctypes.CDLL:
                                          _vp, _vp]
     lib.ca_compensate.restype = ctypes.c_int
     lib.ca_compensate.argtypes = [P, _vp, _vp, _vp, _vp, _vp, _i32, ctypes.c_float, _i32, _vp,
-                                  _vp, _vp, _vp, _vp, _vp]
+                                  _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
     _lib = lib
     return lib
 

@@ -131,6 +131,8 @@ void plan_workspace(const Prob& P, Workspace* W) {
   W->hist = take(2 * BH * W->hist_slots * kBins * 4);
   W->chunk_cnt = take(2 * BH * W->hist_slots * 2 * 4);
   W->scores = take(BH * P.nqc * P.nkc * 4);
+  const size_t ntile = (P.nkc + kCompTile - 1) / kCompTile;
+  W->comp_tiles = take(P.dtype == CA_BF16 ? BH * ntile * comp_tile_bytes(P.d) : 0);
   W->total = off;
 }
 
@@ -226,7 +228,7 @@ int ca_block_sparse_attn(const ca_problem* p, const void* qp, const void* kp, co
 int ca_compensate(const ca_problem* p, const void* qp, const float* cent_k, const float* cent_v,
                   const int32_t* count_k, const int32_t* lists, int32_t k, float scale,
                   int32_t enable, const void* op, const float* lse, const int32_t* perm_q,
-                  void* out, float* lse_out, void* stream) {
+                  void* out, float* lse_out, void* ws, size_t ws_bytes, void* stream) {
   ca::Prob P;
   int s = check_problem(p, &P);
   if (s) return s;
@@ -236,9 +238,16 @@ int ca_compensate(const ca_problem* p, const void* qp, const float* cent_k, cons
   if (enable && (!qp || !cent_k || !cent_v || !count_k || !lists))
     return fail(CA_E_INVALID, "compensation needs qp, cent_k, cent_v, count_k and lists");
   if ((s = check_attn_shape(P))) return s;
+  char* tiles = nullptr;
+  if (P.dtype == CA_BF16 && enable && k < P.nkc) {
+    ca::Workspace W;
+    ca::plan_workspace(P, &W);
+    if ((s = check_ws(W, ws, ws_bytes))) return s;
+    tiles = (char*)ws + W.comp_tiles;
+  }
   if (!(scale > 0.0f)) scale = 1.0f / sqrtf((float)P.d);
   return device_status(ca::launch_comp(P, qp, cent_k, cent_v, count_k, lists, k, scale, enable,
-                                       op, lse, perm_q, out, lse_out, (hipStream_t)stream),
+                                       op, lse, perm_q, out, lse_out, tiles, (hipStream_t)stream),
                        "ca_compensate");
 }
 

@@ -107,6 +107,8 @@ struct Workspace {
   size_t chunk_cnt;         // int32 [2][BH][hist_slots][2] chunk prefixes (less, equal)
   // selection
   size_t scores;            // fp32 [BH][nqc][nkc]
+  // compensation
+  size_t comp_tiles;        // bf16 centroid tiles [BH][ceil(nkc/kCompTile)][comp_tile_bytes]
   size_t total;
   // derived split parameters
   int nblk_mom;             // row blocks per tensor for moment partials
@@ -123,6 +125,12 @@ constexpr int kBins = 4096;       // linear bins of the multi-block split select
 constexpr int kChunk = 4096;      // tokens per block in the multi-block split passes
 constexpr int kTail = 4096;       // nodes of at most this size finish in one workgroup
 constexpr int kMomRows = 2048;    // rows per moment-partial block
+constexpr int kCompTile = 128;    // centroids per tile of the bf16 compensation kernel
+
+// Bytes of one bf16 compensation tile: kCompTile centroid key rows [kCompTile][d]
+// bf16, the centroid values transposed [d][kCompTile] bf16, and kCompTile fp32
+// biases (log2 of the cluster size).
+inline size_t comp_tile_bytes(int d) { return (size_t)kCompTile * (4 * d + 4); }
 
 void plan_workspace(const Prob& P, Workspace* W);
 // Number of split levels done by the multi-block kernels (nodes above the tail size).
@@ -143,9 +151,11 @@ hipError_t launch_select(const Prob& P, const float* cq, const float* ck, const 
 hipError_t launch_attn(const Prob& P, const void* qp, const void* kp, const void* vp,
                        const int32_t* count_k, const int32_t* lists, int k, float scale, void* op,
                        float* lse, hipStream_t st);
+// tiles: workspace region of the bf16 centroid tiles (bf16 with compensation
+// only; ignored otherwise).
 hipError_t launch_comp(const Prob& P, const void* qp, const float* cent_k, const float* cent_v,
                        const int32_t* count_k, const int32_t* lists, int k, float scale,
                        int enable, const void* op, const float* lse, const int32_t* perm_q,
-                       void* out, float* lse_out, hipStream_t st);
+                       void* out, float* lse_out, char* tiles, hipStream_t st);
 
 }  // namespace ca

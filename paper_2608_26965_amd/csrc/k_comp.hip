@@ -6,9 +6,14 @@
 // query of a through its centroid key and value with the logit
 // scale*q.kbar_b + ln|b|. These centroid logits form a second softmax whose
 // (lse_c, o_c) is merged with the sparse part (lse_s, o_s) in log-sum-exp form.
-// bf16: centroids are rounded to bf16 in LDS and contracted on MFMA exactly like
-// key tiles, 128 centroids per tile. fp32: one thread per query.
+// bf16: the centroids of a head are first rounded once into bf16 tiles of 128
+// (keys row-major, values transposed, plus the log2 cluster sizes) in the
+// workspace; every query cluster then streams those tiles into LDS with
+// direct-to-LDS copies and contracts them on MFMA exactly like key tiles.
+// fp32: one thread per query.
 #include <math.h>
+
+#include <type_traits>
 
 #include "attn_tile.h"
 
@@ -19,6 +24,8 @@ namespace {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kMaskWords = 2048;  // up to 65536 key clusters
+// s_waitcnt immediate (gfx9 encoding) waiting for vmcnt = 0 only.
+constexpr int kVmcnt0 = 0x0F70;
 
 __device__ __forceinline__ int xcd_remap(int wg, int total) {
   int per = total >> 3, rem = total & 7;
@@ -30,25 +37,104 @@ __device__ __forceinline__ size_t out_row(int bh, int i, int nq, int H, int d, i
   return row_off(bh, i, nq, H, d, layout);
 }
 
+// bf16 centroid tiles (written once per call, read by every query cluster of
+// the head): tile t of head bh covers centroids [128 t, 128 t + 128) and holds
+//   K   [128][D] bf16   centroid keys, row-major (zero rows past nkc),
+//   V^T [D][128] bf16   centroid values transposed (zero columns past nkc),
+//   bias[128]    fp32   log2 of the cluster size (-inf: empty or past nkc).
+// blockIdx.z = 0 writes K and bias, 1 writes V^T (through an LDS transpose).
+template <int D>
+__global__ __launch_bounds__(256) void comp_stage_kernel(const float* __restrict__ cent_k,
+                                                         const float* __restrict__ cent_v,
+                                                         const int32_t* __restrict__ count_k,
+                                                         int nkc, int ntile,
+                                                         char* __restrict__ tiles) {
+  constexpr int CT = kCompTile;
+  constexpr int KBYTES = CT * D * 2, VBYTES = D * CT * 2;
+  constexpr int TB = KBYTES + VBYTES + CT * 4;
+  __shared__ float vs[CT][D + 1];
+  const int t = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  const int b0 = t * CT;
+  char* tile = tiles + ((size_t)bh * ntile + t) * TB;
+  if (blockIdx.z == 0) {
+    const float* src = cent_k + (size_t)bh * nkc * D;
+    bf16* kt = (bf16*)tile;
+    for (int i = tid; i < CT * (D / 8); i += 256) {
+      const int row = i / (D / 8), c8 = i % (D / 8), b = b0 + row;
+      float4 x = make_float4(0.f, 0.f, 0.f, 0.f), y = x;
+      if (b < nkc) {
+        x = *(const float4*)(src + (size_t)b * D + 8 * c8);
+        y = *(const float4*)(src + (size_t)b * D + 8 * c8 + 4);
+      }
+      const float f[8] = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
+      *(bf16x8*)(kt + row * D + 8 * c8) = pack8(f);
+    }
+    if (tid < CT) {
+      const int b = b0 + tid;
+      const int c = b < nkc ? count_k[(size_t)bh * nkc + b] : 0;
+      ((float*)(tile + KBYTES + VBYTES))[tid] =
+          c > 0 ? __builtin_amdgcn_logf((float)c) : -INFINITY;  // log2 of the size
+    }
+    return;
+  }
+  const float* src = cent_v + (size_t)bh * nkc * D;
+  for (int i = tid; i < CT * (D / 4); i += 256) {
+    const int row = i / (D / 4), c4 = i % (D / 4), b = b0 + row;
+    float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (b < nkc) x = *(const float4*)(src + (size_t)b * D + 4 * c4);
+    vs[row][4 * c4] = x.x;
+    vs[row][4 * c4 + 1] = x.y;
+    vs[row][4 * c4 + 2] = x.z;
+    vs[row][4 * c4 + 3] = x.w;
+  }
+  __syncthreads();
+  bf16* vt = (bf16*)(tile + KBYTES);
+  for (int i = tid; i < D * (CT / 8); i += 256) {
+    const int dim = i / (CT / 8), g = i % (CT / 8);
+    float f[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) f[r] = vs[8 * g + r][dim];
+    *(bf16x8*)(vt + dim * CT + 8 * g) = pack8(f);
+  }
+}
+
+// Workgroups per CU: as many as the LDS (two tile stages and the selection
+// mask) allows, capped at two waves per SIMD.
 template <int D, int CQ>
-__global__ __launch_bounds__(CQ * 2, (D == 64 ? 2 : 1)) void comp_bf16_kernel(
-    const bf16* __restrict__ qp, const float* __restrict__ cent_k,
-    const float* __restrict__ cent_v, const int32_t* __restrict__ count_k,
-    const int32_t* __restrict__ lists, int nq, int H, int nqc, int nkc, int k, float sl2,
-    int enable, const bf16* __restrict__ op, const float* __restrict__ lse_s,
+constexpr int comp_blocks_per_cu() {
+  constexpr int lds = 2 * (kCompTile * (4 * D + 4)) + kMaskWords * 4;
+  constexpr int by_lds = (160 * 1024) / lds;
+  constexpr int by_waves = 8 / (CQ / 32);
+  return by_lds < by_waves ? (by_lds < 1 ? 1 : by_lds) : by_waves;
+}
+
+template <int D, int CQ>
+__global__ __launch_bounds__(CQ * 2, (comp_blocks_per_cu<D, CQ>())) void comp_bf16_kernel(
+    const bf16* __restrict__ qp, const char* __restrict__ tiles,
+    const int32_t* __restrict__ lists, int nq, int H, int nqc, int nkc, int ntile, int k,
+    float sl2, int enable, const bf16* __restrict__ op, const float* __restrict__ lse_s,
     const int32_t* __restrict__ perm_q, bf16* __restrict__ out, float* __restrict__ lse_out,
     int layout, int total) {
   constexpr int NW = CQ / 32;
   constexpr int T = NW * 64;
-  constexpr int CT = 128;  // centroids per tile
+  constexpr int CT = kCompTile;  // centroids per tile
   constexpr int MT = CT / 32;
   constexpr int KS = D / 16;
   constexpr int DT = D / 32;
-  constexpr int KP = D + 8;
-  constexpr int VP = CT + 8;
-  __shared__ __attribute__((aligned(16))) bf16 Ks[CT * KP];
-  __shared__ __attribute__((aligned(16))) bf16 Vs[D * VP];
-  __shared__ __attribute__((aligned(16))) float bias[CT];
+  constexpr int KROW = 2 * D;   // bytes per centroid key row
+  constexpr int VROW = 2 * CT;  // bytes per transposed value row
+  constexpr int KBYTES = CT * KROW, VBYTES = D * VROW, BBYTES = CT * 4;
+  constexpr int STAGE = KBYTES + VBYTES + BBYTES;
+  constexpr int KLD = KBYTES / 1024 / NW;  // direct-to-LDS instructions per wave
+  constexpr int VLD = VBYTES / 1024 / NW;
+  constexpr int BLANES = BBYTES / 16 / NW;  // lanes of each wave copying the bias row
+  constexpr int NL = KLD + VLD + 1;
+  static_assert(KLD * 1024 * NW == KBYTES && VLD * 1024 * NW == VBYTES, "tile split");
+  static_assert(BLANES * 16 * NW == BBYTES, "bias split");
+  // Rescale the running output only when a query's maximum logit grows by more
+  // than 2^8 (log2 units): exponentials then stay below 256, exact in fp32.
+  constexpr float kLazy = 8.0f;
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
   __shared__ uint32_t selmask[kMaskWords];
 
   const int item = xcd_remap(blockIdx.x, total);
@@ -66,198 +152,185 @@ __global__ __launch_bounds__(CQ * 2, (D == 64 ? 2 : 1)) void comp_bf16_kernel(
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[dt][r] = 0.f;
 
+  // Operands of the final merge, loaded up front so that their latency
+  // overlaps the set-up instead of ending the kernel.
+  const bool row_ok = prow < nq;
+  float ls = 0.f;
+  int orig = 0;
+  bf16x4 s4[DT][4];
   const bool do_comp = enable && k < nkc;
+  const char* th = tiles + (size_t)bh * ntile * STAGE;
+  const TileCopy<KROW, KLD, NW> kcopy(w, lane);
+  const TileCopy<VROW, VLD, NW> vcopy(w, lane);
+  const uint32_t lds0 = lds_addr(smem);
+  auto issue = [&](int t, int stage) {
+    const char* src = th + (size_t)t * STAGE;
+    const uint32_t dst = lds0 + stage * STAGE;
+    kcopy.issue(src, dst, w);
+    vcopy.issue(src + KBYTES, dst + KBYTES, w);
+    const uint32_t boff = (uint32_t)(w * BLANES * 16);
+    const uint32_t bdst = __builtin_amdgcn_readfirstlane(dst + KBYTES + VBYTES + boff);
+    if (lane < BLANES) lds_dma16(src + KBYTES + VBYTES, boff + 16 * lane, bdst);
+  };
+  bf16x8 qreg[KS];
   if (do_comp) {
     for (int i = tid; i < nwords; i += T) selmask[i] = 0u;
-    __syncthreads();
+    // The first two tiles are copied before the selection is known (a tile
+    // whose centroids are all selected is then skipped, not un-copied).
+    issue(0, 0);
+    if (ntile > 1) issue(1, 1);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      qreg[ks] = *(const bf16x8*)(qp + qrow * D + 16 * ks + 8 * h);
+  }
+  if (row_ok) {
+    ls = lse_s[qrow];
+    orig = perm_q[(size_t)bh * nq + prow];
+    const bf16* srow = op + qrow * D;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) s4[dt][g] = *(const bf16x4*)(srow + 32 * dt + 8 * g + 4 * h);
+  }
+  if (do_comp) {
+    wait_lgkm();
+    raw_barrier();  // selmask cleared
     const int32_t* lst = lists + ((size_t)bh * nqc + a) * k;
     for (int i = tid; i < k; i += T) {
       int b = lst[i];
       if (b >= 0 && b < nkc) atomicOr(&selmask[b >> 5], 1u << (b & 31));
     }
-    bf16x8 qreg[KS];
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      qreg[ks] = *(const bf16x8*)(qp + qrow * D + 16 * ks + 8 * h);
+    // Retire every load issued so far, including the first two tile copies
+    // (a wait the compiler sees), so that no compiler-inserted vmcnt wait
+    // lands inside the loop, where it would also wait for the copy in flight.
+    __builtin_amdgcn_s_waitcnt(kVmcnt0);
+    wait_lgkm();
+    raw_barrier();  // selmask complete
 
-    const float* ckh = cent_k + (size_t)bh * nkc * D;
-    const float* cvh = cent_v + (size_t)bh * nkc * D;
-    const int32_t* cnth = count_k + (size_t)bh * nkc;
-    // Staging tasks: K rows as 8-column chunks (one 16-byte LDS store each);
-    // V as 8-centroid x 4-column blocks, transposed in registers into four
-    // 16-byte stores. The global loads of tile t+1 are issued before the
-    // products of tile t, so their latency hides behind the matrix work.
-    constexpr int NKT = CT * (D / 8) / T;
-    constexpr int NVT = (CT / 8) * (D / 4) / T;
-    constexpr int NBT = (CT + T - 1) / T;
-    static_assert(NKT * T == CT * (D / 8) && NVT * T == (CT / 8) * (D / 4), "staging split");
-    // (without registers to spare, a tile is loaded just before it is staged)
-    constexpr bool kPrefetch = NKT * 2 + NVT * 8 <= 16;
-    float4 kv[NKT][2], vv[NVT][8];
-    int cv[NBT];
-    __syncthreads();  // selmask complete
-    // Tiles holding at least one unselected centroid, in order.
-    auto tile_live = [&](int b0) {
+    // A tile is live if it holds at least one unselected centroid.
+    auto tile_live = [&](int t) {
       int any = 0;
-      for (int e = b0 >> 5; e < ((b0 + CT) >> 5) && e < nwords; ++e) {
+      const int e0 = t * (CT / 32);
+      for (int e = e0; e < e0 + CT / 32 && e < nwords; ++e) {
         const uint32_t wmask = e == nwords - 1 && (nkc & 31) ? (1u << (nkc & 31)) - 1u : ~0u;
         any |= (~selmask[e] & wmask) != 0u;
       }
-      return any;
+      return __builtin_amdgcn_readfirstlane(any) != 0;
     };
-    auto next_live = [&](int b0) {
-      while (b0 < nkc && !tile_live(b0)) b0 += CT;
-      return b0;
-    };
-    auto load_k = [&](int b0) {
+    int koff[KS];
+    {
+      const int row = kswz(l32);
 #pragma unroll
-      for (int u = 0; u < NKT; ++u) {
-        const int i = tid + T * u, row = i / (D / 8), c8 = i % (D / 8), b = b0 + row;
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh)
-          kv[u][hh] = b < nkc ? *(const float4*)(ckh + (size_t)b * D + 8 * c8 + 4 * hh)
-                              : make_float4(0.f, 0.f, 0.f, 0.f);
-      }
-#pragma unroll
-      for (int u = 0; u < NBT; ++u) {
-        const int e = tid + T * u, b = b0 + e;
-        cv[u] = e < CT && b < nkc ? cnth[b] : 0;
-      }
-    };
-    auto load_v = [&](int b0) {
-#pragma unroll
-      for (int u = 0; u < NVT; ++u) {
-        const int i = tid + T * u, g = i % (CT / 8), cc = i / (CT / 8);
-#pragma unroll
-        for (int r = 0; r < 8; ++r) {
-          const int b = b0 + 8 * g + r;
-          vv[u][r] = b < nkc ? *(const float4*)(cvh + (size_t)b * D + 4 * cc)
-                             : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-      }
-    };
-    auto store_k = [&](int b0) {
-#pragma unroll
-      for (int u = 0; u < NKT; ++u) {
-        const int i = tid + T * u, row = i / (D / 8), c8 = i % (D / 8);
-        const float f[8] = {kv[u][0].x, kv[u][0].y, kv[u][0].z, kv[u][0].w,
-                            kv[u][1].x, kv[u][1].y, kv[u][1].z, kv[u][1].w};
-        *(bf16x8*)&Ks[row * KP + 8 * c8] = pack8(f);
-      }
-#pragma unroll
-      for (int u = 0; u < NBT; ++u) {
-        const int e = tid + T * u, b = b0 + e;
-        if (e < CT) {
-          float bi = -INFINITY;
-          if (b < nkc && !((selmask[b >> 5] >> (b & 31)) & 1u) && cv[u] > 0)
-            bi = __builtin_amdgcn_logf((float)cv[u]);  // log2 of the size
-          bias[e] = bi;
-        }
-      }
-    };
-    auto store_v = [&]() {
-#pragma unroll
-      for (int u = 0; u < NVT; ++u) {
-        const int i = tid + T * u, g = i % (CT / 8), cc = i / (CT / 8);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          float f[8];
-#pragma unroll
-          for (int r = 0; r < 8; ++r)
-            f[r] = j == 0 ? vv[u][r].x : (j == 1 ? vv[u][r].y : (j == 2 ? vv[u][r].z : vv[u][r].w));
-          *(bf16x8*)&Vs[(4 * cc + j) * VP + 8 * g] = pack8(f);
-        }
-      }
-    };
-    int b0 = next_live(0);
-    if (kPrefetch && b0 < nkc) {
-      load_k(b0);
-      load_v(b0);
+      for (int kk = 0; kk < KS; ++kk) koff[kk] = swz_off<KROW>(row, 2 * kk + h);
     }
-    while (b0 < nkc) {
-      __syncthreads();  // the previous tile is fully consumed
-      if (!kPrefetch) load_k(b0);
-      store_k(b0);
-      if (!kPrefetch) load_v(b0);
-      store_v();
-      __syncthreads();
-      const int b1 = next_live(b0 + CT);
-      if (kPrefetch && b1 < nkc) {
-        load_k(b1);
-        load_v(b1);
-      }
+    int voff[MT][2];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) voff[mt][s2] = swz_off<VROW>(l32, 4 * mt + 2 * s2 + h);
 
-      f32x16 sacc[MT];
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[mt][r] = 0.f;
-        const bf16* krow = &Ks[(32 * mt + kswz(l32)) * KP + 8 * h];
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          bf16x8 av = *(const bf16x8*)(krow + 16 * ks);
-          sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qreg[ks], sacc[mt], 0, 0, 0);
+    auto body = [&](auto stage_tag, int t) {
+      constexpr int S = decltype(stage_tag)::value;
+      if (t + 1 < ntile)
+        wait_vmcnt<NL>();
+      else
+        wait_vmcnt<0>();
+      raw_barrier();
+      if (tile_live(t)) {
+        const char* ks = smem + S * STAGE;
+        const char* vs = ks + KBYTES;
+        float* bias = (float*)(smem + S * STAGE + KBYTES + VBYTES);
+        // Selected clusters are covered by the sparse part: drop them here.
+        if (tid < CT) {
+          const int b = t * CT + tid;
+          if (b < nkc && ((selmask[b >> 5] >> (b & 31)) & 1u)) bias[tid] = -INFINITY;
         }
-      }
-      // logits in log2 units: scale*log2e*q.kbar + log2|b|. The bias of
-      // accumulator r of row tile mt is bias[32 mt + (r & 7) + 16 (r >> 3) + 8 h]:
-      // two runs of 8 consecutive entries, read as four 16-byte loads.
-      float mx = -INFINITY;
+        f32x16 sacc[MT];
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        float bv[16];
+        for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const float4 b0v = *(const float4*)&bias[32 * mt + 16 * hh + 8 * h];
-          const float4 b1v = *(const float4*)&bias[32 * mt + 16 * hh + 8 * h + 4];
-          bv[8 * hh + 0] = b0v.x, bv[8 * hh + 1] = b0v.y, bv[8 * hh + 2] = b0v.z, bv[8 * hh + 3] = b0v.w;
-          bv[8 * hh + 4] = b1v.x, bv[8 * hh + 5] = b1v.y, bv[8 * hh + 6] = b1v.z, bv[8 * hh + 7] = b1v.w;
+          for (int r = 0; r < 16; ++r) sacc[mt][r] = 0.f;
+#pragma unroll
+          for (int kk = 0; kk < KS; ++kk) {
+            const bf16x8 av = *(const bf16x8*)(ks + 32 * mt * KROW + koff[kk]);
+            sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qreg[kk], sacc[mt], 0, 0, 0);
+          }
         }
+        wait_lgkm();
+        raw_barrier();  // bias row final
+        // logits in log2 units: scale*log2e*q.kbar + log2|b|. The bias of
+        // accumulator r of row tile mt is bias[32 mt + (r & 7) + 16 (r >> 3) + 8 h]:
+        // two runs of 8 consecutive entries, read as four 16-byte loads.
+        float mx = -INFINITY;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float t = __builtin_fmaf(sacc[mt][r], sl2, bv[r]);
-          sacc[mt][r] = t;
-          mx = fmaxf(mx, t);
+        for (int mt = 0; mt < MT; ++mt) {
+          float bv[16];
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const float4 b0v = *(const float4*)&bias[32 * mt + 16 * hh + 8 * h];
+            const float4 b1v = *(const float4*)&bias[32 * mt + 16 * hh + 8 * h + 4];
+            bv[8 * hh + 0] = b0v.x, bv[8 * hh + 1] = b0v.y, bv[8 * hh + 2] = b0v.z, bv[8 * hh + 3] = b0v.w;
+            bv[8 * hh + 4] = b1v.x, bv[8 * hh + 5] = b1v.y, bv[8 * hh + 6] = b1v.z, bv[8 * hh + 7] = b1v.w;
+          }
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float x = __builtin_fmaf(sacc[mt][r], sl2, bv[r]);
+            sacc[mt][r] = x;
+            mx = fmaxf(mx, x);
+          }
         }
-      }
-      mx = fmaxf(mx, wave_xor32(mx));
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      float lsum = 0.f;
-      bf16x8 pb[MT][2];
+        mx = fmaxf(mx, wave_xor32(mx));
+        if (__builtin_amdgcn_ballot_w64(mx > m_run + kLazy)) {
+          const float m_new = fmaxf(m_run, mx);
+          const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+          l_run *= alpha;
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+          for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          float pv[8];
-#pragma unroll
-          for (int j = 0; j < 8; ++j) pv[j] = __builtin_amdgcn_exp2f(sacc[mt][8 * s + j] - m_new);
-          pb[mt][s] = pack8(pv);
-          lsum = sum8(pb[mt][s], lsum);
+            for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
+          m_run = m_new;
         }
-      l_run = l_run * alpha + lsum;
-      m_run = m_new;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
-        const bf16* vrow = &Vs[(32 * dt + l32) * VP + 8 * h];
+        // A query that has seen no live centroid yet has m_run = -inf and only
+        // -inf logits: offset by 0 so that they give 0, not NaN.
+        const float m_use = m_run == -INFINITY ? 0.f : m_run;
+        float lsum = 0.f;
+        bf16x8 pb[MT][2];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int s = 0; s < 2; ++s) {
-            bf16x8 av = *(const bf16x8*)(vrow + 32 * mt + 16 * s);
-            oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[mt][s], oacc[dt], 0, 0, 0);
+          for (int s2 = 0; s2 < 2; ++s2) {
+            float pv[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+              pv[j] = __builtin_amdgcn_exp2f(sacc[mt][8 * s2 + j] - m_use);
+            pb[mt][s2] = pack8(pv);
+            lsum = sum8(pb[mt][s2], lsum);
           }
+        l_run += lsum;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int s2 = 0; s2 < 2; ++s2) {
+              const bf16x8 av = *(const bf16x8*)(vs + 32 * dt * VROW + voff[mt][s2]);
+              oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[mt][s2], oacc[dt], 0, 0, 0);
+            }
       }
-      b0 = b1;
+      wait_lgkm();
+      raw_barrier();  // every wave is done with this stage
+      if (t + 2 < ntile) issue(t + 2, S);
+    };
+
+    for (int t = 0; t < ntile; t += 2) {
+      body(std::integral_constant<int, 0>{}, t);
+      if (t + 1 < ntile) body(std::integral_constant<int, 1>{}, t + 1);
     }
   }
 
   // Merge with the sparse part and write to the original position.
   const float l_tot = l_run + wave_xor32(l_run);
-  if (prow >= nq) return;
-  const float ls = lse_s[qrow];
+  if (!row_ok) return;
   float ws = 1.f, wc = 0.f, lse = ls, inv_c = 0.f;
   if (l_tot > 0.f) {
     const float lc = (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2;
@@ -267,21 +340,17 @@ __global__ __launch_bounds__(CQ * 2, (D == 64 ? 2 : 1)) void comp_bf16_kernel(
     wc = expf(lc - lse);
     inv_c = 1.f / l_tot;
   }
-  int orig = perm_q[(size_t)bh * nq + prow];
   orig = orig < 0 ? 0 : (orig >= nq ? nq - 1 : orig);  // memory safety for a bad permutation
   bf16* orow = out + out_row(bh, orig, nq, H, D, layout);
-  const bf16* srow = op + qrow * D;
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const int col = 32 * dt + 8 * g + 4 * h;
-      bf16x4 s4 = *(const bf16x4*)(srow + col);
       bf16x4 v4;
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        v4[j] = f2bf(ws * bf2f(s4[j]) + wc * (oacc[dt][4 * g + j] * inv_c));
-      *(bf16x4*)(orow + col) = v4;
+        v4[j] = f2bf(ws * bf2f(s4[dt][g][j]) + wc * (oacc[dt][4 * g + j] * inv_c));
+      *(bf16x4*)(orow + 32 * dt + 8 * g + 4 * h) = v4;
     }
   if (lse_out && h == 0) lse_out[(size_t)bh * nq + orig] = lse;
 }
@@ -379,10 +448,17 @@ template <int D, int CQ>
 hipError_t run_bf16(const Prob& P, const void* qp, const float* cent_k, const float* cent_v,
                     const int32_t* count_k, const int32_t* lists, int k, float scale, int enable,
                     const void* op, const float* lse, const int32_t* perm_q, void* out,
-                    float* lse_out, hipStream_t st) {
+                    float* lse_out, char* tiles, hipStream_t st) {
   const int total = P.BH * P.nqc;
+  const int ntile = (P.nkc + kCompTile - 1) / kCompTile;
+  const bool do_comp = enable && k < P.nkc;
+  if (do_comp) {
+    if (!tiles) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(comp_stage_kernel<D>, dim3(ntile, P.BH, 2), dim3(256), 0, st, cent_k,
+                       cent_v, count_k, P.nkc, ntile, tiles);
+  }
   hipLaunchKernelGGL((comp_bf16_kernel<D, CQ>), dim3(total), dim3(CQ * 2), 0, st,
-                     (const bf16*)qp, cent_k, cent_v, count_k, lists, P.nq, P.H, P.nqc, P.nkc, k,
+                     (const bf16*)qp, (const char*)tiles, lists, P.nq, P.H, P.nqc, P.nkc, ntile, k,
                      scale * kLog2e, enable, (const bf16*)op, lse, perm_q, (bf16*)out, lse_out,
                      P.layout, total);
   return hipGetLastError();
@@ -393,13 +469,13 @@ hipError_t run_bf16(const Prob& P, const void* qp, const float* cent_k, const fl
 hipError_t launch_comp(const Prob& P, const void* qp, const float* cent_k, const float* cent_v,
                        const int32_t* count_k, const int32_t* lists, int k, float scale,
                        int enable, const void* op, const float* lse, const int32_t* perm_q,
-                       void* out, float* lse_out, hipStream_t st) {
+                       void* out, float* lse_out, char* tiles, hipStream_t st) {
   if (P.nkc > kMaskWords * 32) return hipErrorInvalidValue;
   if (P.dtype == CA_BF16) {
 #define CA_COMP_CASE(D, CQ) \
   if (P.d == D && P.cq == CQ) \
     return run_bf16<D, CQ>(P, qp, cent_k, cent_v, count_k, lists, k, scale, enable, op, lse, \
-                           perm_q, out, lse_out, st);
+                           perm_q, out, lse_out, tiles, st);
     CA_COMP_CASE(64, 64)
     CA_COMP_CASE(64, 128)
     CA_COMP_CASE(128, 64)

@@ -25,7 +25,7 @@ def test_header_symbols_exported():
     assert declared == set(L.EXPORTS)
     for name in declared:
         assert hasattr(lib, name)
-    assert lib.ca_abi_version() == 1
+    assert lib.ca_abi_version() == 2
 
 
 def _prob(**kw):
@@ -75,9 +75,12 @@ def test_calls_reject_before_enqueue():
     assert lib.ca_block_sparse_attn(_prob(cq=32), *args, 2, 0.0, fake, fake, None) == \
         L.CA_E_UNSUPPORTED
     assert lib.ca_compensate(p, fake, fake, fake, fake, fake, 2, 0.0, 1, None, fake, fake, fake,
-                             None, None) == L.CA_E_INVALID
+                             None, None, 0, None) == L.CA_E_INVALID
     assert lib.ca_compensate(p, None, None, None, None, None, 2, 0.0, 1, fake, fake, fake, fake,
-                             None, None) == L.CA_E_INVALID
+                             None, None, 0, None) == L.CA_E_INVALID
+    # bf16 with compensation stages the centroids in the workspace
+    assert lib.ca_compensate(p, fake, fake, fake, fake, fake, 2, 0.0, 1, fake, fake, fake, fake,
+                             None, fake, 16, None) == L.CA_E_WORKSPACE
     ws_misaligned = ctypes.c_void_p(0x1001)
     need = ctypes.c_size_t(0)
     lib.ca_workspace_size(p, 1, need)

@@ -118,6 +118,74 @@ def test_compensation_parity(dt, d, cq, ck, n, k, enable):
         assert np.abs(lse_out[h] - l_w).max() <= 1e-4 * max(1.0, np.abs(l_w).max())
 
 
+MULTI = [
+    # dtype, d, cq, ck, n, k, whole_tile: every other query cluster selects all
+    # of centroids [128, 256), a 128-centroid tile the bf16 kernel must skip
+    ("bf16", 64, 128, 64, 20000, 140, True),
+    ("bf16", 128, 64, 64, 9000, 10, False),
+    ("bf16", 64, 64, 128, 40000, 20, False),
+    ("f32", 64, 64, 64, 20000, 140, True),
+]
+
+
+@pytest.mark.parametrize("dt,d,cq,ck,n,k,whole_tile", MULTI)
+def test_compensation_multi_tile(dt, d, cq, ck, n, k, whole_tile):
+    """Compensation over several 128-centroid tiles with a ragged last tile.
+    The sparse part is synthetic (it only enters through the merge)."""
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    from synth import bf16_round
+    G.flush(f"comp multi-tile dt={dt} d={d} cq={cq} ck={ck} n={n} k={k} whole={whole_tile}")
+    H = 2
+    Q, K, V = mixture_inputs(21, H, n, d, dt, centres=8, sigma=0.4)
+    rng = np.random.default_rng(22)
+    p = ca.Problem(1, H, n, n, d, cq, ck, G.tdtype(dt))
+    perm_q = np.stack([rng.permutation(n) for _ in range(H)]).astype(np.int32)
+    perm_k = np.stack([rng.permutation(n) for _ in range(H)]).astype(np.int32)
+    lists = G.random_lists(rng, H, p.nqc, p.nkc, k)
+    if whole_tile:
+        assert p.nkc > 256 and k >= 128
+        for b in range(H):
+            for a in range(0, p.nqc, 2):
+                rest = np.setdiff1d(np.arange(p.nkc), np.arange(128, 256))
+                extra = rng.choice(rest, size=k - 128, replace=False)
+                lists[b, a] = np.sort(np.concatenate([np.arange(128, 256), extra]))
+    cq_n, ck_n = G.counts(n, cq), G.counts(n, ck)
+    tau = 1 / math.sqrt(d)
+    op = np.zeros((H, p.nq_pad, d), np.float32)
+    lse = np.zeros((H, p.nq_pad), np.float32)
+    kbar = np.zeros((H, p.nkc, d), np.float32)
+    vbar = np.zeros((H, p.nkc, d), np.float32)
+    want = []
+    for h in range(H):
+        o = rng.standard_normal((n, d)) * 0.5
+        if dt == "bf16":
+            o = bf16_round(o.astype(np.float32)).astype(np.float64)
+        ls = rng.uniform(8.0, 12.0, n).astype(np.float32).astype(np.float64)
+        op[h, :n] = o[perm_q[h]]
+        lse[h, :n] = ls[perm_q[h]]
+        kbar[h] = ref.centroids(K[h], perm_k[h], ck_n).astype(np.float32)
+        vbar[h] = ref.centroids(V[h], perm_k[h], ck_n).astype(np.float32)
+        want.append(ref.compensate(Q[h], kbar[h], vbar[h], ck_n, perm_q[h], cq_n, lists[h], o,
+                                   ls, tau))
+    tq = G.permuted_rows(Q, perm_q, cq, G.tdtype(dt))
+    out, lse_out = ca.compensate(p, tq, G.dev(kbar), G.dev(vbar),
+                                 G.dev(np.stack([ck_n] * H), torch.int32),
+                                 G.dev(lists, torch.int32), k, G.dev(op, G.tdtype(dt)),
+                                 G.dev(lse), G.dev(perm_q, torch.int32), want_lse=True)
+    torch.cuda.synchronize()
+    out, lse_out = G.host(out)[0], G.host(lse_out)
+    worst = 0.0
+    for h in range(H):
+        o_w, l_w = want[h]
+        err = np.abs(out[h] - o_w).max()
+        worst = max(worst, err)
+        assert err <= G.TOL[dt], (h, err)
+        assert np.abs(lse_out[h] - l_w).max() <= 1e-4 * max(1.0, np.abs(l_w).max())
+    G.flush(f"  max abs err {worst:.3g}")
+
+
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
 def test_all_kept_equals_dense(dt):
     """Every key cluster selected: the two calls give dense attention."""
