@@ -18,6 +18,8 @@
 // order and no contraction, so it is reproducible bit for bit.
 #include <math.h>
 
+#include <type_traits>
+
 #include "attn_tile.h"
 #include "common.h"
 
@@ -207,13 +209,18 @@ __global__ __launch_bounds__(256) void moments_finish_kernel(Ctx C) {
 // The DM players of a round-robin tournament (rows beyond d are zero padding,
 // so any pair that touches one is an identity rotation) give DM/2 disjoint
 // pairs per step; every pair of indices meets once per sweep of DM-1 steps
-// (Golub & Van Loan, parallel Jacobi). A step is applied as J^T A J in two
-// passes over LDS: first the rows p, q of A and of V^T (one column per lane),
-// then the columns p, q of A (one row per lane). Each wavefront owns the same
-// DM/16 pairs in both passes and computes their rotations itself, so a step
-// costs two barriers and every LDS access is a conflict-free row or column
-// sweep. Output: eigenvalues in descending order and the matching eigenvectors
-// as columns.
+// (Golub & Van Loan, parallel Jacobi). A is stored by tournament position, so
+// a step's pairs are always (k, DM/2 + k). A step applies J^T A J block-wise:
+// the pairs cut A into (DM/2)^2 blocks of 2x2, and each thread owns the blocks
+// of one row pair and some column pairs. It derives the rotations of its row
+// and column pairs itself from the diagonal blocks, rotates its blocks from
+// the left and then from the right in registers (the arithmetic of a row pass
+// followed by a column pass), and writes them where the players move for the
+// next step; every read and write is then a contiguous row segment. The rows
+// of V^T travel with their players in the same way. Every entry has one
+// owner, so with A and V^T double-buffered a step costs a single barrier (two
+// when they are rotated in place). Output: eigenvalues in descending order and
+// the matching eigenvectors as columns.
 // ---------------------------------------------------------------------------
 
 // One eigenproblem: A = B, A = B - m m^T, or A = S^T B S (- u u^T with
@@ -234,52 +241,59 @@ struct EighJobs {
   EighJob j[2];
 };
 
-// Threads of the eigensolver workgroup: a Jacobi step is a chain of LDS
-// round trips, so the most wavefronts a workgroup can have (16) issue each
-// step's traffic with the most parallelism (measured: 8 -> 16 wavefronts
-// takes d = 64 from 577 to 519 us for 16 problems; 4 wavefronts is slower).
+// Threads of the eigensolver workgroup: the most a workgroup can have. A
+// step is a short dependency chain (LDS reads, the rotation, the 2x2 block
+// products, LDS writes, a barrier), and more wavefronts overlap more of it
+// (measured at d = 64 for 16 problems: 1024 threads beat 512 by 31 us and
+// 256 by 139 us).
+__host__ __device__ constexpr int eigh_nt(int dm) { return 1024; }
 template <int DM>
 constexpr int eigh_threads() {
-  return 1024;
+  return eigh_nt(DM);
 }
 
+// Row stride of the LDS matrices: DM plus the number of threads that share a
+// row pair, so that the row segments the threads of one wavefront touch in a
+// step fall on disjoint LDS banks.
+__host__ __device__ constexpr int eigh_stride(int dm) { return dm + eigh_nt(dm) / (dm / 2); }
+// A and V^T are double-buffered (a step reads one copy and writes the other,
+// so it needs a single barrier) when four matrices fit comfortably in LDS.
+__host__ __device__ constexpr bool eigh_double_buffer(int dm) {
+  return 4 * (size_t)dm * eigh_stride(dm) * sizeof(float) <= 100 * 1024;
+}
 __host__ __device__ constexpr size_t eigh_lds_bytes(int dm) {
-  return 2 * (size_t)dm * (dm + 1) * sizeof(float);
+  return (eigh_double_buffer(dm) ? 4 : 2) * (size_t)dm * eigh_stride(dm) * sizeof(float);
 }
 
-// Round-robin pairing of m players at a step: pair k joins positions k and
-// m-1-k; position 0 is fixed and the others rotate by one place per step, so
-// every pair meets once per m-1 steps. Returns p < q.
-__device__ __forceinline__ void rr_pair(int k, int step, int m, int* p, int* q) {
-  int x = k - 1 + step;
-  x -= x >= m - 1 ? m - 1 : 0;
-  const int a = k == 0 ? 0 : 1 + x;
-  int y = m - 2 - k + step;
-  y -= y >= m - 1 ? m - 1 : 0;
-  const int b = 1 + y;
-  *p = a < b ? a : b;
-  *q = a < b ? b : a;
+// Tournament positions: slot k of a step pairs position k ("top") with
+// position NP + k ("bottom"). Between steps position 0 stays, tops move right,
+// bottoms move left, top NP-1 drops to bottom NP-1 and bottom 0 climbs to
+// top 1: the circle method, so every two players meet once per 2 NP - 1 steps
+// and after a whole sweep every player is back at its first position.
+__device__ __forceinline__ int eigh_next(int pos, int np) {
+  if (pos < np) return pos == 0 ? 0 : (pos == np - 1 ? 2 * np - 1 : pos + 1);
+  return pos == np ? 1 : pos - 1;
 }
 
 // Rotation (c, s) that zeroes entry (p, q) of J^T A J, J = [[c, s], [-s, c]]
 // on rows/columns (p, q): t = tan(theta) is the smaller root of
-// t^2 + 2 tau t - 1 = 0, tau = (a_qq - a_pp) / (2 a_pq). Hardware reciprocal
-// and square-root approximations are enough: any (c, s) with c^2 + s^2 = 1 to
+// t^2 + 2 tau t - 1 = 0, tau = (a_qq - a_pp) / (2 a_pq), taken in the form
+// t = sign(delta) 2 a_pq / (|delta| + sqrt(delta^2 + 4 a_pq^2)), delta =
+// a_qq - a_pp (one square root and one reciprocal). Hardware reciprocal and
+// square-root approximations are enough: any (c, s) with c^2 + s^2 = 1 to
 // rounding keeps the transform orthogonal, and a slightly inexact angle only
-// leaves a tiny off-diagonal that later sweeps remove.
+// leaves a tiny off-diagonal that later sweeps remove. Branch-free (selects,
+// not a branch), so that a step's LDS reads issue together.
 __device__ __forceinline__ void jacobi_rotation(float app, float aqq, float apq, float* c,
                                                 float* s) {
-  if (!(fabsf(apq) > 1e-30f)) {
-    *c = 1.f;
-    *s = 0.f;
-    return;
-  }
-  const float tau = 0.5f * (aqq - app) * __builtin_amdgcn_rcpf(apq);
-  const float den = fabsf(tau) + __builtin_amdgcn_sqrtf(1.f + tau * tau);
-  const float t = copysignf(__builtin_amdgcn_rcpf(den), tau);
-  const float cc = __builtin_amdgcn_rsqf(1.f + t * t);
-  *c = cc;
-  *s = t * cc;
+  const bool live = fabsf(apq) > 1e-30f;
+  const float dl = aqq - app, a2 = 2.f * apq;
+  const float r = __builtin_amdgcn_sqrtf(__builtin_fmaf(dl, dl, a2 * a2));
+  float t = a2 * __builtin_amdgcn_rcpf(fabsf(dl) + r);
+  t = __int_as_float(__float_as_int(t) ^ (__float_as_int(dl) & (int)0x80000000));
+  const float cc = __builtin_amdgcn_rsqf(__builtin_fmaf(t, t, 1.f));
+  *c = live ? cc : 1.f;
+  *s = live ? t * cc : 0.f;
 }
 
 // 4x4 register blocks of a d x d product (d <= 128, NT threads: at most two
@@ -336,14 +350,20 @@ template <int DM>
 __global__ __launch_bounds__(eigh_threads<DM>()) void eigh_kernel(Ctx C, EighJobs J) {
   constexpr int NT = eigh_threads<DM>();
   static_assert((DM / 4) * (DM / 4) <= 2 * NT, "two 4x4 product blocks per thread");
-  constexpr int EP = DM + 1;               // odd row stride: column sweeps hit distinct banks
+  constexpr int EP = eigh_stride(DM);
   constexpr int NW = NT / 64;
-  constexpr int PPW = DM / 2 / NW;         // pairs per wavefront and step
-  constexpr int CPL = DM / 64;             // columns (rows) per lane in a row (column) pass
-  static_assert(PPW >= 1 && CPL >= 1, "matrix size");
+  constexpr int CPL = DM / 64;             // columns per lane in a row sweep
+  constexpr int NP = DM / 2;               // pairs per step
+  constexpr int TPI = NT / NP;             // threads per row pair
+  constexpr int BPT = NP / TPI;            // 2x2 blocks per thread
+  constexpr int RG = 64 / TPI;             // row pairs per wavefront
+  static_assert(CPL >= 1 && TPI * NP == NT && BPT * TPI == NP && RG * TPI == 64, "matrix size");
+  constexpr bool kDB = eigh_double_buffer(DM);
   extern __shared__ float esh[];
   float* A = esh;             // [DM][EP]
   float* Vt = esh + DM * EP;  // [DM][EP], Vt[i][j] = V[j][i]
+  float* A2 = kDB ? esh + 2 * DM * EP : esh;  // second copies (double-buffered)
+  float* Vt2 = kDB ? esh + 3 * DM * EP : Vt;
   __shared__ float red[2][NW];
   __shared__ float uvec[DM], ovec[DM], lam[DM], sgn[DM];
   __shared__ int rnk[DM];
@@ -411,7 +431,83 @@ __global__ __launch_bounds__(eigh_threads<DM>()) void eigh_kernel(Ctx C, EighJob
       }
   }
   if (tid == 0) sh_stop = 0;
+  int cur = 0;  // which copy holds the current A and V^T (double-buffered)
+  const int rp = tid / TPI, cp0 = tid % TPI;  // this thread's row pair, first column pair
+  // One step of a sweep, with the copy it reads (S) fixed at compile time so
+  // that every LDS address is loop-invariant.
+  auto step_body = [&](auto copy_tag) {
+    constexpr int S = decltype(copy_tag)::value;
+    const float* Ac = S ? A2 : A;
+    const float* Vc = S ? Vt2 : Vt;
+    float* An = S ? A : A2;
+    float* Vn = S ? Vt : Vt2;
+    const int ti = rp, bi = NP + rp;  // positions of the row pair
+    // Rotations of this thread's column pairs.
+    float cj[BPT], sj[BPT];
+#pragma unroll
+    for (int b = 0; b < BPT; ++b) {
+      const int tj = cp0 + TPI * b, bj = NP + tj;
+      jacobi_rotation(Ac[tj * EP + tj], Ac[bj * EP + bj], Ac[tj * EP + bj], &cj[b], &sj[b]);
+    }
+    // The row pair's rotation was derived by the lane of group 0 whose column
+    // pair it is (the same block index for every group of the wavefront).
+    float ci = 1.f, si = 0.f;
+    {
+      const int bsel = (RG * wv) / TPI;
+      float cs = cj[0], ss = sj[0];
+#pragma unroll
+      for (int b = 1; b < BPT; ++b)
+        if (b == bsel) cs = cj[b], ss = sj[b];
+#pragma unroll
+      for (int g = 0; g < RG; ++g) {
+        const int rg = (RG * wv + g) % TPI;
+        const float cg = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cs), rg));
+        const float sg = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ss), rg));
+        const bool mine = lane / TPI == g;
+        ci = mine ? cg : ci;
+        si = mine ? sg : si;
+      }
+    }
+    float blk[BPT][4], vb[BPT][4];
+#pragma unroll
+    for (int b = 0; b < BPT; ++b) {
+      const int cp = cp0 + TPI * b, tj = cp, bj = NP + cp;
+      const float a00 = Ac[ti * EP + tj], a01 = Ac[ti * EP + bj];
+      const float a10 = Ac[bi * EP + tj], a11 = Ac[bi * EP + bj];
+      // rows (p, q) from the left, then columns from the right
+      const float x00 = ci * a00 - si * a10, x01 = ci * a01 - si * a11;
+      const float x10 = si * a00 + ci * a10, x11 = si * a01 + ci * a11;
+      blk[b][0] = cj[b] * x00 - sj[b] * x01;
+      blk[b][1] = sj[b] * x00 + cj[b] * x01;
+      blk[b][2] = cj[b] * x10 - sj[b] * x11;
+      blk[b][3] = sj[b] * x10 + cj[b] * x11;
+      if (cp == rp) blk[b][1] = blk[b][2] = 0.f;  // the pair's own entry is zeroed
+      const float v00 = Vc[ti * EP + tj], v01 = Vc[ti * EP + bj];
+      const float v10 = Vc[bi * EP + tj], v11 = Vc[bi * EP + bj];
+      vb[b][0] = ci * v00 - si * v10;
+      vb[b][1] = ci * v01 - si * v11;
+      vb[b][2] = si * v00 + ci * v10;
+      vb[b][3] = si * v01 + ci * v11;
+    }
+    if (!kDB) __syncthreads();  // every read done before A and V^T are overwritten
+    const int nti = eigh_next(ti, NP), nbi = eigh_next(bi, NP);
+#pragma unroll
+    for (int b = 0; b < BPT; ++b) {
+      const int cp = cp0 + TPI * b, tj = cp, bj = NP + cp;
+      const int ntj = eigh_next(tj, NP), nbj = eigh_next(bj, NP);
+      An[nti * EP + ntj] = blk[b][0];
+      An[nti * EP + nbj] = blk[b][1];
+      An[nbi * EP + ntj] = blk[b][2];
+      An[nbi * EP + nbj] = blk[b][3];
+      Vn[nti * EP + tj] = vb[b][0];
+      Vn[nti * EP + bj] = vb[b][1];
+      Vn[nbi * EP + tj] = vb[b][2];
+      Vn[nbi * EP + bj] = vb[b][3];
+    }
+    __syncthreads();
+  };
   for (int sweep = 0; sweep < 40; ++sweep) {
+    const float* Ac = cur ? A2 : A;
     __syncthreads();
     // Convergence: off-diagonal mass relative to the total.
     float off = 0.f, tot = 0.f;
@@ -419,7 +515,7 @@ __global__ __launch_bounds__(eigh_threads<DM>()) void eigh_kernel(Ctx C, EighJob
 #pragma unroll
       for (int cc = 0; cc < CPL; ++cc) {
         const int j = lane + 64 * cc;
-        const float a = A[i * EP + j];
+        const float a = Ac[i * EP + j];
         tot += a * a;
         off += i != j ? a * a : 0.f;
       }
@@ -449,75 +545,21 @@ __global__ __launch_bounds__(eigh_threads<DM>()) void eigh_kernel(Ctx C, EighJob
     __syncthreads();
     if (sh_stop >= 2) break;
     for (int step = 0; step < DM - 1; ++step) {
-      // This wavefront's pairs k = wv + NW t; lane t (mod PPW) derives pair t's
-      // rotation, then every lane reads it back as a wave-uniform value.
-      int pl, ql;
-      rr_pair(wv + NW * (lane % PPW), step, DM, &pl, &ql);
-      float cl, sl;
-      jacobi_rotation(A[pl * EP + pl], A[ql * EP + ql], A[pl * EP + ql], &cl, &sl);
-      int P[PPW], Q[PPW];
-      float Cs[PPW], Ss[PPW];
-#pragma unroll
-      for (int t = 0; t < PPW; ++t) {
-        P[t] = __builtin_amdgcn_readlane(pl, t);
-        Q[t] = __builtin_amdgcn_readlane(ql, t);
-        Cs[t] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cl), t));
-        Ss[t] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sl), t));
-      }
-      // Row pass: rows p, q of A and of V^T.
-      float ra[PPW][CPL][4];
-#pragma unroll
-      for (int t = 0; t < PPW; ++t)
-#pragma unroll
-        for (int cc = 0; cc < CPL; ++cc) {
-          const int j = lane + 64 * cc;
-          ra[t][cc][0] = A[P[t] * EP + j];
-          ra[t][cc][1] = A[Q[t] * EP + j];
-          ra[t][cc][2] = Vt[P[t] * EP + j];
-          ra[t][cc][3] = Vt[Q[t] * EP + j];
-        }
-#pragma unroll
-      for (int t = 0; t < PPW; ++t)
-#pragma unroll
-        for (int cc = 0; cc < CPL; ++cc) {
-          const int j = lane + 64 * cc;
-          const float c = Cs[t], s = Ss[t];
-          A[P[t] * EP + j] = c * ra[t][cc][0] - s * ra[t][cc][1];
-          A[Q[t] * EP + j] = s * ra[t][cc][0] + c * ra[t][cc][1];
-          Vt[P[t] * EP + j] = c * ra[t][cc][2] - s * ra[t][cc][3];
-          Vt[Q[t] * EP + j] = s * ra[t][cc][2] + c * ra[t][cc][3];
-        }
-      __syncthreads();
-      // Column pass: columns p, q of A; the (p, q) entries become exact zeros.
-      float ca[PPW][CPL][2];
-#pragma unroll
-      for (int t = 0; t < PPW; ++t)
-#pragma unroll
-        for (int cc = 0; cc < CPL; ++cc) {
-          const int i = lane + 64 * cc;
-          ca[t][cc][0] = A[i * EP + P[t]];
-          ca[t][cc][1] = A[i * EP + Q[t]];
-        }
-#pragma unroll
-      for (int t = 0; t < PPW; ++t)
-#pragma unroll
-        for (int cc = 0; cc < CPL; ++cc) {
-          const int i = lane + 64 * cc;
-          const float c = Cs[t], s = Ss[t];
-          const float np_ = c * ca[t][cc][0] - s * ca[t][cc][1];
-          const float nq_ = s * ca[t][cc][0] + c * ca[t][cc][1];
-          A[i * EP + P[t]] = i == Q[t] ? 0.f : np_;
-          A[i * EP + Q[t]] = i == P[t] ? 0.f : nq_;
-        }
-      __syncthreads();
+      if (cur == 0)
+        step_body(std::integral_constant<int, 0>{});
+      else
+        step_body(std::integral_constant<int, 1>{});
+      if (kDB) cur ^= 1;
     }
   }
   __syncthreads();
+  float* Ac = cur ? A2 : A;
+  const float* Vc = cur ? Vt2 : Vt;
   // ---- epilogue: eigenvalues, ranks (descending, ties by index), orientation
   if (tid < d) {
-    lam[tid] = A[tid * EP + tid];
+    lam[tid] = Ac[tid * EP + tid];
     float o = 0.f;
-    for (int t = 0; t < d; ++t) o = __builtin_fmaf(ovec[t], Vt[tid * EP + t], o);
+    for (int t = 0; t < d; ++t) o = __builtin_fmaf(ovec[t], Vc[tid * EP + t], o);
     sgn[tid] = o < 0.f ? -1.f : 1.f;
   }
   __syncthreads();
@@ -535,12 +577,12 @@ __global__ __launch_bounds__(eigh_threads<DM>()) void eigh_kernel(Ctx C, EighJob
   float* U = mat(C, bh, jb.vecs);
   float* T = mat(C, bh, jb.t_out);
   bf16* W = jb.wop_out >= 0 ? wop(C, bh, jb.wop_out) : nullptr;
-  // Eigenvector i becomes column rnk[i]: U[r][rnk[i]] = sgn[i] Vt[i][r].
+  // Eigenvector i becomes column rnk[i]: U[r][rnk[i]] = sgn[i] Vc[i][r].
   for (int i = wv; i < d; i += NW)
 #pragma unroll
     for (int cc = 0; cc < CPL; ++cc) {
       const int r = lane + 64 * cc;
-      if (r < d) U[r * d + rnk[i]] = sgn[i] * Vt[i * EP + r];
+      if (r < d) U[r * d + rnk[i]] = sgn[i] * Vc[i * EP + r];
     }
   auto put_t = [&](int r, int i, float v) {  // T[r][rnk[i]] = v
     const int j = rnk[i];
@@ -552,17 +594,17 @@ __global__ __launch_bounds__(eigh_threads<DM>()) void eigh_kernel(Ctx C, EighJob
     }
   };
   if (jb.t_f >= 0) {
-    // T'[r][i] = sum_t F[r][t] Vt[i][t]; F goes into the A region.
+    // T'[r][i] = sum_t F[r][t] Vc[i][t]; F goes into the A region.
     const float* Sg = mat(C, bh, jb.t_f);
     for (int i = wv; i < DM; i += NW)
 #pragma unroll
       for (int cc = 0; cc < CPL; ++cc) {
         const int j = lane + 64 * cc;
-        A[i * EP + j] = i < d && j < d ? Sg[i * d + j] : 0.f;
+        Ac[i * EP + j] = i < d && j < d ? Sg[i * d + j] : 0.f;
       }
     __syncthreads();
     MMAcc acc;
-    lds_mm<NT>(A, false, Vt, true, EP, d, acc);
+    lds_mm<NT>(Ac, false, Vc, true, EP, d, acc);
     const int d4 = (d + 3) >> 2, nb = d4 * d4;
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
@@ -582,7 +624,7 @@ __global__ __launch_bounds__(eigh_threads<DM>()) void eigh_kernel(Ctx C, EighJob
 #pragma unroll
       for (int cc = 0; cc < CPL; ++cc) {
         const int r = lane + 64 * cc;
-        if (r < d) put_t(r, i, sgn[i] * Vt[i * EP + r]);
+        if (r < d) put_t(r, i, sgn[i] * Vc[i * EP + r]);
       }
   }
 }
@@ -2013,6 +2055,9 @@ hipError_t set_lds_limits() {
   static bool done = [] {
     (void)hipFuncSetAttribute((const void*)eigh_kernel<128>,
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)kEighLds);
+    (void)hipFuncSetAttribute((const void*)eigh_kernel<64>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)eigh_lds_bytes(64));
     (void)hipFuncSetAttribute((const void*)cholesky_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
                         (int)kCholLds);
     (void)hipFuncSetAttribute((const void*)qnorm_partial_kernel,
