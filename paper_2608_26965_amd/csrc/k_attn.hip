@@ -60,9 +60,6 @@ __global__ __launch_bounds__(CQ * 2, (attn_blocks_per_cu<D, CQ, CK>())) void att
   constexpr int VLD = VBYTES / 1024 / NW;
   constexpr int NL = KLD + VLD;
   static_assert(KLD * 1024 * NW == KBYTES && VLD * 1024 * NW == VBYTES, "tile split");
-  // Rescale the running output only when a query's maximum logit grows by more
-  // than 2^8 (log2 units): exponentials then stay below 256, exact in fp32.
-  constexpr float kLazy = 8.0f;
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
   const int item = xcd_remap(blockIdx.x, total);
@@ -144,13 +141,37 @@ __global__ __launch_bounds__(CQ * 2, (attn_blocks_per_cu<D, CQ, CK>())) void att
         for (int r = 0; r < 16; ++r)
           if (acc_key(mt, r, h) >= cnt) sacc[mt][r] = -INFINITY;
     }
-    float mx = -INFINITY;
+    // Exponentials are taken against the running maximum without first
+    // forming this tile's maximum. Only a tile whose logits pass the running
+    // maximum by so much that a lane's row sum exceeds 2^40 is redone against
+    // its own maximum: always the first tile (m_run = -inf, so the sums are
+    // infinite), later ones only on a jump of about 2^33 in a probability.
+    // Below that, large exponentials cost no accuracy (fp32 and bf16 keep
+    // their relative precision at any scale).
+    float lsum;
+    bf16x8 pb[MT][2];
+    auto exps = [&]() {
+      lsum = 0.f;
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[mt][r]);
-    mx = fmaxf(mx, wave_xor32(mx)) * sl2;
-    if (__builtin_amdgcn_ballot_w64(mx > m_run + kLazy)) {
+        for (int s2 = 0; s2 < 2; ++s2) {
+          float pv[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            pv[j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[mt][8 * s2 + j], sl2, -m_run));
+          pb[mt][s2] = pack8(pv);
+          lsum = sum8(pb[mt][s2], lsum);
+        }
+    };
+    exps();
+    if (__builtin_amdgcn_ballot_w64(!(lsum <= 0x1p40f))) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[mt][r]);
+      mx = fmaxf(mx, wave_xor32(mx)) * sl2;
       const float m_new = fmaxf(m_run, mx);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
       l_run *= alpha;
@@ -159,20 +180,8 @@ __global__ __launch_bounds__(CQ * 2, (attn_blocks_per_cu<D, CQ, CK>())) void att
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
       m_run = m_new;
+      exps();
     }
-    float lsum = 0.f;
-    bf16x8 pb[MT][2];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) {
-        float pv[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-          pv[j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[mt][8 * s2 + j], sl2, -m_run));
-        pb[mt][s2] = pack8(pv);
-        lsum = sum8(pb[mt][s2], lsum);
-      }
     l_run += lsum;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
