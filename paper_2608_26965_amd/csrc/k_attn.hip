@@ -58,7 +58,6 @@ __global__ __launch_bounds__(CQ * 2, (attn_blocks_per_cu<D, CQ, CK>())) void att
   constexpr int STAGE = KBYTES + VBYTES;
   constexpr int KLD = KBYTES / 1024 / NW;  // direct-to-LDS instructions per wave
   constexpr int VLD = VBYTES / 1024 / NW;
-  constexpr int NL = KLD + VLD;
   static_assert(KLD * 1024 * NW == KBYTES && VLD * 1024 * NW == VBYTES, "tile split");
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
@@ -112,13 +111,16 @@ __global__ __launch_bounds__(CQ * 2, (attn_blocks_per_cu<D, CQ, CK>())) void att
     for (int r = 0; r < 16; ++r) oacc[dt][r] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
+  // Tile t sits in stage t % 2. Its copy was issued at the start of tile t-1,
+  // right after the barrier that every wavefront passes only once done with
+  // tile t-2 (which used the same stage), so one barrier per tile suffices
+  // and each copy has a whole tile of compute to land.
   auto body = [&](auto stage_tag, int t) {
     constexpr int S = decltype(stage_tag)::value;
-    if (t + 1 < k)
-      wait_vmcnt<NL>();
-    else
-      wait_vmcnt<0>();
+    wait_vmcnt<0>();
+    wait_lgkm();
     raw_barrier();
+    if (t + 1 < k) issue(tile_id(t + 1), S ^ 1);
     const char* ks = smem + S * STAGE;
     const char* vs = ks + KBYTES;
     const int cnt = cnth[tile_id(t)];
@@ -192,13 +194,9 @@ __global__ __launch_bounds__(CQ * 2, (attn_blocks_per_cu<D, CQ, CK>())) void att
           const bf16x8 av = *(const bf16x8*)(vs + 32 * dt * VROW + voff[mt][s2]);
           oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[mt][s2], oacc[dt], 0, 0, 0);
         }
-    wait_lgkm();
-    raw_barrier();  // every wave is done with this stage
-    if (t + 2 < k) issue(tile_id(t + 2), S);
   };
 
   issue(tile_id(0), 0);
-  if (k > 1) issue(tile_id(1), 1);
   for (int t = 0; t < k; t += 2) {
     body(std::integral_constant<int, 0>{}, t);
     if (t + 1 < k) body(std::integral_constant<int, 1>{}, t + 1);
