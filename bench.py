@@ -34,7 +34,7 @@ PEAK_HBM_GBS = 8000.0
 # HBM bytes per launch of the attention kernel from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE, scaled by a plain-copy calibration (see the traffic summary under
 # profiles/), valid for the kernel source with this fingerprint only.
-ATTN_TRAFFIC = {"fingerprint": "1c44fc85fedb5fcc", "bytes": 1.556e9}
+ATTN_TRAFFIC = {"fingerprint": "98c8f1be6fd61f4d", "bytes": 1.562e9}
 
 
 def attn_fingerprint():
@@ -71,13 +71,31 @@ def time_oracle(Q, K, V, c, k):
     return dt, threads
 
 
+def copy_calibration():
+    """A plain device copy of 256 MiB (fp32), three launches."""
+    import torch
+    n = 256 * 1024 * 1024 // 4
+    src = torch.randn(n, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(f"copied {n * 4 // 1024} KiB per launch")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 256 MiB device copy three times: the known-size "
+                         "reference that scales the FETCH_SIZE / WRITE_SIZE counters")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration()
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: ClusterAttention's heads are independent, so a "
               "multi-GPU layer shards heads with no communication; run with --gpus 1.",
