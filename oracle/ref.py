@@ -94,19 +94,20 @@ def pca_basis(X):
 def key_split_space(Q, K, mode):
     """Split coordinates Y_K of the keys.
 
-    none:   Y_K = K.
-    pca:    Y_K = K U, U the principal axes of K.
-    metric: keys are mapped into the query-aware metric M = Q^T Q / n (Method,
-            key clustering): K -> K S_q with S_q S_q^T = M, then projected on
-            the principal axes of K S_q (diagonalized splitting). The principal
-            axes of K S_q are the eigenvectors of S_q^T C_K S_q.
+    none:     Y_K = K.
+    pca:      Y_K = K U, U the principal axes of K.
+    metric:   keys are mapped into the query-aware metric M = Q^T Q / n (Method,
+              key clustering): K -> K S_q with S_q S_q^T = M, then projected on
+              the principal axes of K S_q (diagonalized splitting). The
+              principal axes of K S_q are the eigenvectors of S_q^T C_K S_q.
+    adaptive: as metric (the key side does not depend on the selection mode).
     """
     Q, K = np.asarray(Q, F64), np.asarray(K, F64)
     if mode == "none":
         return K.copy()
     if mode == "pca":
         return K @ pca_basis(K)
-    if mode == "metric":
+    if mode in ("metric", "adaptive"):
         S_q = psd_root(second_moment(Q))
         Z = K @ S_q
         return Z @ pca_basis(Z)
@@ -125,9 +126,22 @@ def query_representation(Q, K):
     return np.where(nrm[:, None] > 0.0, rho / safe[:, None], 0.0)
 
 
+def query_representation_adaptive(Q, K):
+    """r(q) = q S_k with S_k S_k^T = K_c^T K_c / n, not normalised (Method,
+    query clustering, the adaptive-assignment case; App. B.1: the
+    representation K_c q / sqrt(n), whose distances are those of the metric
+    K_c^T K_c / n; the root factor gives the same distances in d coordinates).
+    Queries with the same attention distribution over the keys map to the
+    same point: K_c removes the shift invariance of the softmax."""
+    Q, K = np.asarray(Q, F64), np.asarray(K, F64)
+    return Q @ psd_root(centred_cov(K))
+
+
 def query_split_space(Q, K, mode):
     """Split coordinates Y_Q of the queries: none -> Q; pca -> Q on its principal
-    axes; metric -> r(q) (top-k representation) on its principal axes."""
+    axes; metric -> r(q) (top-k representation) on its principal axes;
+    adaptive -> the unnormalised centred-key representation on its principal
+    axes."""
     Q = np.asarray(Q, F64)
     if mode == "none":
         return Q.copy()
@@ -135,6 +149,9 @@ def query_split_space(Q, K, mode):
         return Q @ pca_basis(Q)
     if mode == "metric":
         R = query_representation(Q, K)
+        return R @ pca_basis(R)
+    if mode == "adaptive":
+        R = query_representation_adaptive(Q, K)
         return R @ pca_basis(R)
     raise ValueError(mode)
 
@@ -268,6 +285,93 @@ def topk(S, k):
     return out
 
 
+HIST_BINS = 128            # bins of each of the two histogram passes
+HIST_GRID = HIST_BINS * HIST_BINS
+MASS_ONE = float(2 ** 32)  # fixed-point unit of the estimated attention mass
+
+
+def hist_grid_index(S_row):
+    """Grid position of every score of one query cluster's row (Method:
+    selection, the 128-bin histogram from the lowest to the highest
+    cluster-interaction score, refined by 128 bins inside one bin).
+
+    Reading: the refinement splits a bin into 128 equal parts, so the two
+    passes work on one grid of 128 x 128 steps over [lo, hi]; g =
+    floor((S - lo) * (16384 / (hi - lo))) in float32 arithmetic (the kernel's
+    precision, so that both sides bin identically), clamped to 16383; the
+    coarse bin is g // 128 and the fine bin g % 128. Returns None when every
+    score is equal (no range to bin: everything is selected)."""
+    S32 = np.asarray(S_row, dtype=np.float32)
+    lo, hi = S32.min(), S32.max()
+    if not hi > lo:
+        return None
+    inv = np.float32(HIST_GRID) / np.float32(hi - lo)
+    g = np.floor((S32 - lo) * inv).astype(np.int64)
+    return np.clip(g, 0, HIST_GRID - 1)
+
+
+def hist_mass_units(S_row, counts_k, tau):
+    """Estimated attention mass of each key cluster for the query cluster,
+    count_b * exp(tau * (S_b - max S)), in integer units of 2^-32 (Method:
+    scoring and selection: the unnormalised attention score of the centroid
+    pair, weighted by the cluster size, is the estimate of the mass the
+    cluster receives; by Jensen's inequality it underestimates the true mass).
+    Reading: the fixed point makes the running sums exact and independent of
+    summation order; the common factor exp(tau * max S) cancels in the
+    recall fraction."""
+    S = np.asarray(S_row, F64)
+    m = np.asarray(counts_k, F64) * np.exp(tau * (S - S.max()))
+    return np.floor(m * MASS_ONE + 0.5).astype(np.int64)
+
+
+def hist_select(S_row, counts_k, tau, min_count, mass_recall):
+    """Key clusters selected for one query cluster by the two-pass histogram
+    (Method: selection): thresholds on the number of selected clusters
+    (min_count) and on the fraction of the estimated attention mass
+    (mass_recall); the coarse bin in which the first of them to need it is
+    passed (scanning from the highest scores down) is refined by a second
+    histogram, and every cluster at or above the lower edge of the refinement
+    bin where both thresholds hold is selected. Top-k assignment is
+    mass_recall = 0 (returns at least k clusters, the ties inside the edge's
+    bin included); adaptive assignment uses min_count = 16.
+
+    Reading: the count threshold counts clusters (so that top-k's k is the
+    same k as in exact top-k); the mass threshold is ceil(mass_recall *
+    total) in the fixed-point units of hist_mass_units. Returns the selected
+    indices in ascending order."""
+    S_row = np.asarray(S_row)
+    n = S_row.shape[0]
+    g = hist_grid_index(S_row)
+    if g is None or min_count >= n:
+        return np.arange(n)
+    mass = hist_mass_units(S_row, counts_k, tau)
+    need_mass = int(np.ceil(float(mass_recall) * float(mass.sum())))
+    coarse, fine = g // HIST_BINS, g % HIST_BINS
+
+    def crossing(cnt, ms, cnt_above, mass_above):
+        # highest bin whose lower edge already holds both thresholds
+        c, m = cnt_above, mass_above
+        for b in range(HIST_BINS - 1, -1, -1):
+            c += cnt[b]
+            m += ms[b]
+            if c >= min_count and m >= need_mass:
+                return b
+        return 0
+
+    # pass 1: coarse histogram of counts and masses
+    cnt1 = np.bincount(coarse, minlength=HIST_BINS)
+    ms1 = np.bincount(coarse, weights=mass, minlength=HIST_BINS).astype(np.int64)
+    B = crossing(cnt1, ms1, 0, 0)
+    # pass 2: the refinement inside coarse bin B
+    inside = coarse == B
+    above = coarse > B
+    cnt2 = np.bincount(fine[inside], minlength=HIST_BINS)
+    ms2 = np.zeros(HIST_BINS, dtype=np.int64)
+    np.add.at(ms2, fine[inside], mass[inside])
+    j = crossing(cnt2, ms2, int(above.sum()), int(mass[above].sum()))
+    return np.nonzero(g >= B * HIST_BINS + j)[0]
+
+
 # ---------------------------------------------------------------------------
 # Block-sparse attention and striped mean-compensation (Method: overview;
 # Preliminaries: error in sparse attention; App. A)
@@ -331,10 +435,13 @@ def compensate(Q, kbar, vbar, counts_k, perm_q, counts_q, lists, o_s, lse_s, tau
 
 
 def forward(Q, K, V, cq, ck, k, mode="metric", enable_comp=True, tau=None,
-            perm_q=None, perm_k=None, lists=None, scores=None):
+            perm_q=None, perm_k=None, lists=None, scores=None, select="topk",
+            mass_recall=0.0):
     """ClusterAttention for one head: clustering -> centroids -> scores ->
-    top-k -> block-sparse attention -> compensation (Method: overview).
+    selection -> block-sparse attention -> compensation (Method: overview).
 
+    select="topk": exact top-k; select="hist": the two-pass histogram with
+    min_count = k and the given mass_recall (lists then have varying length).
     perm_q / perm_k / scores / lists may be supplied from outside (parity hooks:
     the checker then follows the given permutation or ranking instead of its
     own). Returns a dict with every intermediate; ``out`` and ``lse`` are in
@@ -359,7 +466,14 @@ def forward(Q, K, V, cq, ck, k, mode="metric", enable_comp=True, tau=None,
     r["kbar"] = centroids(K, perm_k, counts_k)
     r["vbar"] = centroids(V, perm_k, counts_k)
     r["scores"] = centroid_scores(r["qbar"], r["kbar"]) if scores is None else np.asarray(scores, F64)
-    r["lists"] = topk(r["scores"], k) if lists is None else np.asarray(lists)
+    if lists is not None:
+        r["lists"] = lists
+    elif select == "topk":
+        r["lists"] = topk(r["scores"], k)
+    elif select == "hist":
+        r["lists"] = [hist_select(row, counts_k, tau, k, mass_recall) for row in r["scores"]]
+    else:
+        raise ValueError(select)
     o_s, lse_s = sparse_attention(Q, K, V, perm_q, counts_q, perm_k, counts_k, r["lists"], tau)
     r["o_s"], r["lse_s"] = o_s, lse_s
     r["out"], r["lse"] = compensate(Q, r["kbar"], r["vbar"], counts_k, perm_q, counts_q,

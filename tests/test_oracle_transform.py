@@ -59,7 +59,7 @@ def test_pairwise_difference_gram_is_2n_covariance():
     assert np.abs(D.T @ D - 2 * n * n * ref.centred_cov(K)).max() < 1e-10
 
 
-@pytest.mark.parametrize("mode", ["pca", "metric"])
+@pytest.mark.parametrize("mode", ["pca", "metric", "adaptive"])
 def test_split_space_is_decorrelated_sorted_and_oriented(mode):
     """Diagonalized splitting works on principal coordinates: the covariance of
     Y is diagonal with non-increasing variances, and (orientation reading) every
@@ -80,6 +80,43 @@ def test_query_space_is_invariant_to_key_shift():
     a = ref.query_split_space(Q, K, "metric")
     b = ref.query_split_space(Q, K + np.array([3.0, -1, 2, 0.5, 0, 1]), "metric")
     assert np.abs(a - b).max() < 1e-9
+
+
+def test_adaptive_representation_distances():
+    """App. B.1: for adaptive assignment the queries live in the metric
+    K_c^T K_c / n, i.e. |r(q1) - r(q2)|^2 = |K_c (q1 - q2)|^2 / n, written out
+    here with the centred key matrix itself."""
+    Q, K = _mix(7)
+    R = ref.query_representation_adaptive(Q, K)
+    Kc = K - K.mean(axis=0)
+    rng = np.random.default_rng(7)
+    for a, b in rng.integers(0, len(Q), size=(40, 2)):
+        want = ((Kc @ (Q[a] - Q[b])) ** 2).sum() / len(K)
+        got = ((R[a] - R[b]) ** 2).sum()
+        assert abs(got - want) <= 1e-10 * max(1.0, want)
+
+
+def test_adaptive_representation_quotients_softmax_shift():
+    """App. B.1: queries whose logits differ by a constant over all keys (the
+    softmax's invariance) get the same representation, and so do queries that
+    differ along a direction in which the keys do not vary; the top-k
+    representation normalises, the adaptive one does not (scaling q scales r)."""
+    rng = np.random.default_rng(8)
+    K = rng.standard_normal((50, 5))
+    K[:, 4] = 2.5  # every key has the same last coordinate
+    Q = rng.standard_normal((20, 5))
+    delta = np.array([0, 0, 0, 0, 3.0])
+    a = ref.query_representation_adaptive(Q, K)
+    b = ref.query_representation_adaptive(Q + delta, K)
+    assert np.abs(a - b).max() < 1e-12
+    assert np.allclose(ref.query_representation_adaptive(2 * Q, K), 2 * a, atol=1e-12)
+    # same attention distribution => same point: logits K q1 and K q2 differ by a constant
+    assert np.allclose(np.diff(K @ (Q[0] + delta) - K @ Q[0]), 0.0)
+
+
+def test_adaptive_key_space_equals_metric():
+    Q, K = _mix(9)
+    assert np.array_equal(ref.key_split_space(Q, K, "adaptive"), ref.key_split_space(Q, K, "metric"))
 
 
 def test_metric_key_space_independent_of_root_choice():
