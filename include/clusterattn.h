@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define CA_ABI_VERSION 2
+#define CA_ABI_VERSION 3
 
 #if defined(__GNUC__) || defined(__clang__)
 #define CA_API __attribute__((visibility("default")))
@@ -80,8 +80,18 @@ typedef enum { CA_F32 = 0, CA_BF16 = 1 } ca_dtype;
  *   CA_XF_METRIC: keys in the query-induced metric Q^T Q / n, queries through
  *                 r(q) = q S_k / |q S_k| with S_k S_k^T = the key covariance
  *                 (top-k representation, App. B.2), each side then on its own
- *                 principal coordinates. This is the evaluated method. */
-typedef enum { CA_XF_NONE = 0, CA_XF_PCA = 1, CA_XF_METRIC = 2 } ca_transform;
+ *                 principal coordinates. This is the evaluated method.
+ *   CA_XF_ADAPTIVE: keys as CA_XF_METRIC; queries through the unnormalised
+ *                 r(q) = q S_k (the metric K_c^T K_c / n of the centred keys,
+ *                 Method: query clustering for adaptive assignment; App. B.1),
+ *                 on its principal coordinates. For use with the adaptive
+ *                 (attention-mass) selection of ca_select_hist. */
+typedef enum {
+  CA_XF_NONE = 0,
+  CA_XF_PCA = 1,
+  CA_XF_METRIC = 2,
+  CA_XF_ADAPTIVE = 3
+} ca_transform;
 
 /* Layout of Q, K, V and the final output: BHND = [B][H][N][d],
  * BNHD = [B][N][H][d] (the usual activation layout of a transformer). */
@@ -166,6 +176,32 @@ CA_API int ca_select(const ca_problem* p, const float* cent_q, const float* cent
               const float* scores_in, float* scores_out, int32_t k, int32_t* lists,
               void* ws, size_t ws_bytes, void* stream);
 
+/* Step 2, histogram variant (Method: Cluster assignment - selection, the
+ * two-pass histogram). For query cluster a, with S = the centroid scores of
+ * its row: a 16384-step grid over [min S, max S] (coarse bins of 128 steps,
+ * each refined into 128), g_b = min(16383, floor((S_b - min S) * (16384 /
+ * (max S - min S)))) in fp32; the estimated attention mass of key cluster b,
+ * count_k[b] * exp(scale * (S_b - max S)), in fixed point (2^-32 units, fp64
+ * arithmetic, exact integer sums); need = ceil(mass_recall * total mass).
+ * The coarse histogram finds the highest coarse bin whose lower edge keeps
+ * at least min_count clusters and at least `need` mass; its 128 fine bins
+ * find the highest such edge G inside it; every b with g_b >= G is selected.
+ * If all scores are equal, or min_count >= nkc, every cluster is selected.
+ *   top-k through the histogram: min_count = k, mass_recall = 0 (at least k
+ *   clusters: the ties inside the edge's fine bin are kept);
+ *   adaptive assignment: min_count = 16, mass_recall in (0, 1].
+ *
+ * cent_q, cent_k, scores_in, scores_out: as ca_select. count_k: [BH][nkc].
+ * min_count >= 1; mass_recall in [0, 1]; scale <= 0 selects 1/sqrt(d).
+ * lists: [BH][nqc][nkc] int32 output, lens[a] ascending cluster indices in
+ * row a (the rest of the row is not written); lens: [BH][nqc] int32 output,
+ * each in [1, nkc]. Pass lists with list stride k = nkc and lens to the
+ * attention and compensation calls. ws: as ca_select. */
+CA_API int ca_select_hist(const ca_problem* p, const float* cent_q, const float* cent_k,
+                   const int32_t* count_k, const float* scores_in, float* scores_out,
+                   int32_t min_count, float mass_recall, float scale, int32_t* lists,
+                   int32_t* lens, void* ws, size_t ws_bytes, void* stream);
+
 /* Step 3: block-sparse attention (Method: Overview - attention over the
  * selected clusters, returning the softmax denominator).
  *
@@ -178,13 +214,15 @@ CA_API int ca_select(const ca_problem* p, const float* cent_q, const float* cent
  * qp: [BH][nq_pad][d], kp: [BH][nk_pad][d], vp: [BH][nkc][d][ck] value tiles
  * as written by ca_cluster (all dtype), count_k: [BH][nkc],
  * lists: [BH][nqc][k] with entries in [0, nkc) (not checked on the device;
- * out-of-range entries are clamped), op: [BH][nq_pad][d] dtype, lse:
+ * out-of-range entries are clamped), lens: optional [BH][nqc] list lengths
+ * (NULL: every list has k entries; otherwise row a uses its first lens[a]
+ * entries, clamped to [1, k] on the device), op: [BH][nq_pad][d] dtype, lse:
  * [BH][nq_pad] fp32. scale <= 0 selects 1/sqrt(d). Padding query rows get
  * defined values that callers ignore. bf16: d in {64, 128}, cq and ck in
  * {64, 128}; fp32: d % 4 == 0, any cq, ck. */
 CA_API int ca_block_sparse_attn(const ca_problem* p, const void* qp, const void* kp, const void* vp,
-                         const int32_t* count_k, const int32_t* lists, int32_t k, float scale,
-                         void* op, float* lse, void* stream);
+                         const int32_t* count_k, const int32_t* lists, const int32_t* lens,
+                         int32_t k, float scale, void* op, float* lse, void* stream);
 
 /* Step 4: striped mean-compensation and un-permutation (Preliminaries: error
  * in sparse attention; App. A).
@@ -198,14 +236,16 @@ CA_API int ca_block_sparse_attn(const ca_problem* p, const void* qp, const void*
  * enable == 0, or when every cluster is selected, out = op[p], lse = lse[p].
  *
  * qp, op: [BH][nq_pad][d] dtype; cent_k, cent_v: [BH][nkc][d] fp32; count_k:
- * [BH][nkc]; lists: [BH][nqc][k]; lse: [BH][nq_pad] fp32; perm_q: [BH][nq];
+ * [BH][nkc]; lists: [BH][nqc][k], lens: optional list lengths as in
+ * ca_block_sparse_attn; lse: [BH][nq_pad] fp32; perm_q: [BH][nq];
  * out: [B,H,nq,d] in the problem layout and dtype; lse_out: optional
  * [BH][nq] fp32 in original order. ws: device workspace of ws_bytes >=
  * ca_workspace_size(), where the bf16 path stages the centroids as bf16
- * tiles; required only for bf16 with enable != 0 and k < nkc (otherwise it
- * may be NULL with ws_bytes 0). */
+ * tiles; required only for bf16 with enable != 0 and either k < nkc or lens
+ * given (otherwise it may be NULL with ws_bytes 0). */
 CA_API int ca_compensate(const ca_problem* p, const void* qp, const float* cent_k, const float* cent_v,
-                  const int32_t* count_k, const int32_t* lists, int32_t k, float scale,
+                  const int32_t* count_k, const int32_t* lists, const int32_t* lens, int32_t k,
+                  float scale,
                   int32_t enable, const void* op, const float* lse, const int32_t* perm_q,
                   void* out, float* lse_out, void* ws, size_t ws_bytes, void* stream);
 

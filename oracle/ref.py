@@ -337,15 +337,17 @@ def hist_select(S_row, counts_k, tau, min_count, mass_recall):
 
     Reading: the count threshold counts clusters (so that top-k's k is the
     same k as in exact top-k); the mass threshold is ceil(mass_recall *
-    total) in the fixed-point units of hist_mass_units. Returns the selected
-    indices in ascending order."""
+    total) in the fixed-point units of hist_mass_units, at most the total.
+    Returns the selected indices in ascending order."""
     S_row = np.asarray(S_row)
     n = S_row.shape[0]
     g = hist_grid_index(S_row)
     if g is None or min_count >= n:
         return np.arange(n)
     mass = hist_mass_units(S_row, counts_k, tau)
-    need_mass = int(np.ceil(float(mass_recall) * float(mass.sum())))
+    total = int(mass.sum())
+    # never above the total (the product is rounded in fp64 for large totals)
+    need_mass = min(int(np.ceil(float(mass_recall) * float(total))), total)
     coarse, fine = g // HIST_BINS, g % HIST_BINS
 
     def crossing(cnt, ms, cnt_above, mass_above):

@@ -17,13 +17,13 @@ from dataclasses import dataclass
 import torch
 
 from . import _lib
-from ._lib import (CA_BF16, CA_F32, CA_LAYOUT_BHND, CA_LAYOUT_BNHD, CA_XF_METRIC, CA_XF_NONE,
-                   CA_XF_PCA, CAError)
+from ._lib import (CA_BF16, CA_F32, CA_LAYOUT_BHND, CA_LAYOUT_BNHD, CA_XF_ADAPTIVE, CA_XF_METRIC,
+                   CA_XF_NONE, CA_XF_PCA, CAError)
 
-__all__ = ["Problem", "workspace_size", "cluster", "select", "block_sparse_attn", "compensate",
-           "forward", "CAError", "abi_version"]
+__all__ = ["Problem", "workspace_size", "cluster", "select", "select_hist", "block_sparse_attn",
+           "compensate", "forward", "CAError", "abi_version"]
 
-_XF = {"none": CA_XF_NONE, "pca": CA_XF_PCA, "metric": CA_XF_METRIC}
+_XF = {"none": CA_XF_NONE, "pca": CA_XF_PCA, "metric": CA_XF_METRIC, "adaptive": CA_XF_ADAPTIVE}
 _LAYOUT = {"bhnd": CA_LAYOUT_BHND, "bnhd": CA_LAYOUT_BNHD}
 _DT = {torch.float32: CA_F32, torch.bfloat16: CA_BF16}
 
@@ -144,30 +144,61 @@ def select(p: Problem, cent_q, cent_k, keep_k: int, *, scores_in=None, export_sc
     return lists, scores
 
 
-def block_sparse_attn(p: Problem, qp, kp, vp, count_k, lists, keep_k: int, scale: float = 0.0):
-    """Step 3. Returns (op [BH,nq_pad,d] dtype, lse [BH,nq_pad] fp32)."""
+# `forward` takes a `select=` mode argument; this name reaches the top-k call from there.
+select_topk = select
+
+
+def select_hist(p: Problem, cent_q, cent_k, count_k, min_count: int, mass_recall: float = 0.0,
+                scale: float = 0.0, *, scores_in=None, export_scores=False, ws=None):
+    """Step 2, the two-pass histogram selection. min_count = k with
+    mass_recall = 0 is top-k through the histogram (at least k clusters);
+    min_count = 16 with mass_recall in (0, 1] is adaptive assignment.
+    Returns (lists [BH,nqc,nkc] int32, lens [BH,nqc] int32, scores or None);
+    row a of lists holds lens[a] ascending cluster indices."""
+    dev = (cent_q if cent_q is not None else scores_in).device
+    lists = torch.empty(p.bh, p.nqc, p.nkc, dtype=torch.int32, device=dev)
+    lens = torch.empty(p.bh, p.nqc, dtype=torch.int32, device=dev)
+    scores = None
+    if export_scores:
+        scores = torch.empty(p.bh, p.nqc, p.nkc, dtype=torch.float32, device=dev)
+    if ws is None and scores_in is None and scores is None:
+        ws = workspace(p, dev)
+    st = _lib.load().ca_select_hist(p.c(), _ptr(cent_q), _ptr(cent_k), _ptr(count_k),
+                                    _ptr(scores_in), _ptr(scores), int(min_count),
+                                    float(mass_recall), float(scale), _ptr(lists), _ptr(lens),
+                                    _ptr(ws), 0 if ws is None else ws.numel(), _stream(dev))
+    _lib.check(st, "ca_select_hist")
+    return lists, lens, scores
+
+
+def block_sparse_attn(p: Problem, qp, kp, vp, count_k, lists, keep_k: int, scale: float = 0.0,
+                      lens=None):
+    """Step 3. Returns (op [BH,nq_pad,d] dtype, lse [BH,nq_pad] fp32). keep_k is
+    the list stride; lens (optional) the per-cluster list lengths."""
     dev = qp.device
     op = torch.empty(p.bh, p.nq_pad, p.d, dtype=p.dtype, device=dev)
     lse = torch.empty(p.bh, p.nq_pad, dtype=torch.float32, device=dev)
     st = _lib.load().ca_block_sparse_attn(p.c(), _ptr(qp), _ptr(kp), _ptr(vp), _ptr(count_k),
-                                          _ptr(lists), keep_k, float(scale), _ptr(op), _ptr(lse),
-                                          _stream(dev))
+                                          _ptr(lists), _ptr(lens), keep_k, float(scale), _ptr(op),
+                                          _ptr(lse), _stream(dev))
     _lib.check(st, "ca_block_sparse_attn")
     return op, lse
 
 
 def compensate(p: Problem, qp, cent_k, cent_v, count_k, lists, keep_k: int, op, lse, perm_q,
                scale: float = 0.0, enable: bool = True, want_lse: bool = False, out=None,
-               ws=None):
+               ws=None, lens=None):
     """Step 4. Returns (out in the problem layout, lse [BH,nq] or None)."""
     dev = op.device
     if out is None:
         out = torch.empty(p.shape(p.nq), dtype=p.dtype, device=dev)
     lse_out = torch.empty(p.bh, p.nq, dtype=torch.float32, device=dev) if want_lse else None
-    if ws is None and enable and p.dtype == torch.bfloat16 and keep_k < p.nkc:
+    if (ws is None and enable and p.dtype == torch.bfloat16
+            and (keep_k < p.nkc or lens is not None)):
         ws = workspace(p, dev, keep_k)
     st = _lib.load().ca_compensate(p.c(), _ptr(qp), _ptr(cent_k), _ptr(cent_v), _ptr(count_k),
-                                   _ptr(lists), keep_k, float(scale), int(bool(enable)), _ptr(op),
+                                   _ptr(lists), _ptr(lens), keep_k, float(scale),
+                                   int(bool(enable)), _ptr(op),
                                    _ptr(lse), _ptr(perm_q), _ptr(out), _ptr(lse_out), _ptr(ws),
                                    0 if ws is None else ws.numel(), _stream(dev))
     _lib.check(st, "ca_compensate")
@@ -180,10 +211,16 @@ def keep_to_k(keep: float, n_kc: int) -> int:
 
 
 def forward(q, k, v, cq=128, ck=None, keep=None, keep_k=None, transform="metric",
-            compensation=True, scale=None, layout="bhnd", return_parts=False):
+            compensation=True, scale=None, layout="bhnd", return_parts=False, select="topk",
+            mass_recall=0.9, min_count=16):
     """ClusterAttention for one layer. q, k, v: [B,H,N,d] ("bhnd") or [B,N,H,d]
-    ("bnhd"), bf16 or fp32, on one GPU. Keep either a fraction (``keep``) or a
-    count (``keep_k``) of key clusters per query cluster."""
+    ("bnhd"), bf16 or fp32, on one GPU.
+
+    select="topk": exact top-k of either a fraction (``keep``) or a count
+    (``keep_k``) of key clusters per query cluster; select="hist": the
+    two-pass histogram top-k (at least that many clusters); select="adaptive":
+    attention-mass recall ``mass_recall`` with at least ``min_count`` clusters
+    (use it with transform="adaptive")."""
     ck = cq if ck is None else ck
     if layout == "bhnd":
         B, H, nq, d = q.shape
@@ -197,10 +234,23 @@ def forward(q, k, v, cq=128, ck=None, keep=None, keep_k=None, transform="metric"
     sc = 0.0 if scale is None else float(scale)
     ws = workspace(p, q.device, keep_k)
     c = cluster(p, q, k, v, ws=ws)
-    lists, _ = select(p, c["cent_q"], c["cent_k"], keep_k, ws=ws)
-    op, lse = block_sparse_attn(p, c["qp"], c["kp"], c["vp"], c["count_k"], lists, keep_k, sc)
-    out, lse_out = compensate(p, c["qp"], c["cent_k"], c["cent_v"], c["count_k"], lists, keep_k,
-                              op, lse, c["perm_q"], sc, compensation, want_lse=return_parts, ws=ws)
+    lens = None
+    stride = keep_k
+    if select == "topk":
+        lists, _ = select_topk(p, c["cent_q"], c["cent_k"], keep_k, ws=ws)
+    elif select in ("hist", "adaptive"):
+        floor, recall = (keep_k, 0.0) if select == "hist" else (min_count, mass_recall)
+        lists, lens, _ = select_hist(p, c["cent_q"], c["cent_k"], c["count_k"], floor, recall,
+                                     sc, ws=ws)
+        stride = p.nkc
+    else:
+        raise ValueError(select)
+    op, lse = block_sparse_attn(p, c["qp"], c["kp"], c["vp"], c["count_k"], lists, stride, sc,
+                                lens=lens)
+    out, lse_out = compensate(p, c["qp"], c["cent_k"], c["cent_v"], c["count_k"], lists, stride,
+                              op, lse, c["perm_q"], sc, compensation, want_lse=return_parts, ws=ws,
+                              lens=lens)
     if return_parts:
-        return out, dict(c, lists=lists, op=op, lse_s=lse, lse=lse_out, problem=p)
+        return out, dict(c, lists=lists, lens=lens, op=op, lse_s=lse, lse=lse_out, problem=p)
     return out
+

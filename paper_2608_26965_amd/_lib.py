@@ -9,7 +9,7 @@ LIB_PATH = os.path.join(_HERE, "libclusterattn.so")
 
 CA_OK, CA_E_INVALID, CA_E_UNSUPPORTED, CA_E_WORKSPACE, CA_E_DEVICE = range(5)
 CA_F32, CA_BF16 = 0, 1
-CA_XF_NONE, CA_XF_PCA, CA_XF_METRIC = 0, 1, 2
+CA_XF_NONE, CA_XF_PCA, CA_XF_METRIC, CA_XF_ADAPTIVE = 0, 1, 2, 3
 CA_LAYOUT_BHND, CA_LAYOUT_BNHD = 0, 1
 
 EXPORTS = (
@@ -19,6 +19,7 @@ EXPORTS = (
     "ca_workspace_size",
     "ca_cluster",
     "ca_select",
+    "ca_select_hist",
     "ca_block_sparse_attn",
     "ca_compensate",
 )
@@ -72,11 +73,14 @@ def load() -> ctypes.CDLL:
     lib.ca_select.restype = ctypes.c_int
     lib.ca_select.argtypes = [P, _vp, _vp, _vp, _vp, _i32, _vp, _vp, ctypes.c_size_t, _vp]
     lib.ca_block_sparse_attn.restype = ctypes.c_int
-    lib.ca_block_sparse_attn.argtypes = [P, _vp, _vp, _vp, _vp, _vp, _i32, ctypes.c_float, _vp,
-                                         _vp, _vp]
+    lib.ca_block_sparse_attn.argtypes = [P, _vp, _vp, _vp, _vp, _vp, _vp, _i32, ctypes.c_float,
+                                         _vp, _vp, _vp]
+    lib.ca_select_hist.restype = ctypes.c_int
+    lib.ca_select_hist.argtypes = [P, _vp, _vp, _vp, _vp, _vp, _i32, ctypes.c_float,
+                                   ctypes.c_float, _vp, _vp, _vp, ctypes.c_size_t, _vp]
     lib.ca_compensate.restype = ctypes.c_int
-    lib.ca_compensate.argtypes = [P, _vp, _vp, _vp, _vp, _vp, _i32, ctypes.c_float, _i32, _vp,
-                                  _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
+    lib.ca_compensate.argtypes = [P, _vp, _vp, _vp, _vp, _vp, _vp, _i32, ctypes.c_float, _i32,
+                                  _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
     _lib = lib
     return lib
 

@@ -44,7 +44,7 @@ int check_problem(const ca_problem* p, ca::Prob* P) {
   if (!pow2(p->cq) || !pow2(p->ck) || p->cq > ca::kMaxC || p->ck > ca::kMaxC)
     return fail(CA_E_INVALID, "cluster sizes must be powers of two in [1, %d]", ca::kMaxC);
   if (p->dtype != CA_F32 && p->dtype != CA_BF16) return fail(CA_E_INVALID, "unknown dtype");
-  if (p->transform < CA_XF_NONE || p->transform > CA_XF_METRIC)
+  if (p->transform < CA_XF_NONE || p->transform > CA_XF_ADAPTIVE)
     return fail(CA_E_INVALID, "unknown transform");
   if (p->layout != CA_LAYOUT_BHND && p->layout != CA_LAYOUT_BNHD)
     return fail(CA_E_INVALID, "unknown layout");
@@ -209,9 +209,36 @@ int ca_select(const ca_problem* p, const float* cent_q, const float* cent_k,
                        "ca_select");
 }
 
+int ca_select_hist(const ca_problem* p, const float* cent_q, const float* cent_k,
+                   const int32_t* count_k, const float* scores_in, float* scores_out,
+                   int32_t min_count, float mass_recall, float scale, int32_t* lists,
+                   int32_t* lens, void* ws, size_t ws_bytes, void* stream) {
+  ca::Prob P;
+  int s = check_problem(p, &P);
+  if (s) return s;
+  if (!lists || !lens || !count_k) return fail(CA_E_INVALID, "lists, lens and count_k are required");
+  if (!scores_in && (!cent_q || !cent_k))
+    return fail(CA_E_INVALID, "cent_q and cent_k are required when scores_in is NULL");
+  if (min_count < 1) return fail(CA_E_INVALID, "min_count=%d must be >= 1", min_count);
+  if (!(mass_recall >= 0.0f && mass_recall <= 1.0f))
+    return fail(CA_E_INVALID, "mass_recall must be in [0, 1]");
+  float* scores = scores_out;
+  if (!scores_in && !scores) {
+    ca::Workspace W;
+    ca::plan_workspace(P, &W);
+    if ((s = check_ws(W, ws, ws_bytes))) return s;
+    scores = (float*)((char*)ws + W.scores);
+  }
+  if (!(scale > 0.0f)) scale = 1.0f / sqrtf((float)P.d);
+  return device_status(ca::launch_select_hist(P, cent_q, cent_k, count_k, scores_in, scores,
+                                              min_count, mass_recall, scale, lists, lens,
+                                              (hipStream_t)stream),
+                       "ca_select_hist");
+}
+
 int ca_block_sparse_attn(const ca_problem* p, const void* qp, const void* kp, const void* vp,
-                         const int32_t* count_k, const int32_t* lists, int32_t k, float scale,
-                         void* op, float* lse, void* stream) {
+                         const int32_t* count_k, const int32_t* lists, const int32_t* lens,
+                         int32_t k, float scale, void* op, float* lse, void* stream) {
   ca::Prob P;
   int s = check_problem(p, &P);
   if (s) return s;
@@ -221,12 +248,13 @@ int ca_block_sparse_attn(const ca_problem* p, const void* qp, const void* kp, co
   if ((s = check_attn_shape(P))) return s;
   if (!(scale > 0.0f)) scale = 1.0f / sqrtf((float)P.d);
   return device_status(
-      ca::launch_attn(P, qp, kp, vp, count_k, lists, k, scale, op, lse, (hipStream_t)stream),
+      ca::launch_attn(P, qp, kp, vp, count_k, lists, lens, k, scale, op, lse, (hipStream_t)stream),
       "ca_block_sparse_attn");
 }
 
 int ca_compensate(const ca_problem* p, const void* qp, const float* cent_k, const float* cent_v,
-                  const int32_t* count_k, const int32_t* lists, int32_t k, float scale,
+                  const int32_t* count_k, const int32_t* lists, const int32_t* lens, int32_t k,
+                  float scale,
                   int32_t enable, const void* op, const float* lse, const int32_t* perm_q,
                   void* out, float* lse_out, void* ws, size_t ws_bytes, void* stream) {
   ca::Prob P;
@@ -239,15 +267,16 @@ int ca_compensate(const ca_problem* p, const void* qp, const float* cent_k, cons
     return fail(CA_E_INVALID, "compensation needs qp, cent_k, cent_v, count_k and lists");
   if ((s = check_attn_shape(P))) return s;
   char* tiles = nullptr;
-  if (P.dtype == CA_BF16 && enable && k < P.nkc) {
+  if (P.dtype == CA_BF16 && enable && (k < P.nkc || lens)) {
     ca::Workspace W;
     ca::plan_workspace(P, &W);
     if ((s = check_ws(W, ws, ws_bytes))) return s;
     tiles = (char*)ws + W.comp_tiles;
   }
   if (!(scale > 0.0f)) scale = 1.0f / sqrtf((float)P.d);
-  return device_status(ca::launch_comp(P, qp, cent_k, cent_v, count_k, lists, k, scale, enable,
-                                       op, lse, perm_q, out, lse_out, tiles, (hipStream_t)stream),
+  return device_status(ca::launch_comp(P, qp, cent_k, cent_v, count_k, lists, lens, k, scale,
+                                       enable, op, lse, perm_q, out, lse_out, tiles,
+                                       (hipStream_t)stream),
                        "ca_compensate");
 }
 

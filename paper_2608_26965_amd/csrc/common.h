@@ -148,13 +148,19 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
                           hipStream_t st);
 hipError_t launch_select(const Prob& P, const float* cq, const float* ck, const float* scores_in,
                          float* scores, int k, int32_t* lists, hipStream_t st);
+hipError_t launch_select_hist(const Prob& P, const float* cq, const float* ck,
+                              const int32_t* count_k, const float* scores_in, float* scores,
+                              int min_count, float recall, float scale, int32_t* lists,
+                              int32_t* lens, hipStream_t st);
+// lens (optional): per query cluster list lengths, clamped to [1, k] on the device.
 hipError_t launch_attn(const Prob& P, const void* qp, const void* kp, const void* vp,
-                       const int32_t* count_k, const int32_t* lists, int k, float scale, void* op,
-                       float* lse, hipStream_t st);
+                       const int32_t* count_k, const int32_t* lists, const int32_t* lens, int k,
+                       float scale, void* op, float* lse, hipStream_t st);
 // tiles: workspace region of the bf16 centroid tiles (bf16 with compensation
 // only; ignored otherwise).
 hipError_t launch_comp(const Prob& P, const void* qp, const float* cent_k, const float* cent_v,
-                       const int32_t* count_k, const int32_t* lists, int k, float scale,
+                       const int32_t* count_k, const int32_t* lists, const int32_t* lens, int k,
+                       float scale,
                        int enable, const void* op, const float* lse, const int32_t* perm_q,
                        void* out, float* lse_out, char* tiles, hipStream_t st);
 

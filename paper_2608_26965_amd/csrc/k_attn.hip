@@ -46,8 +46,9 @@ constexpr int attn_blocks_per_cu() {
 template <int D, int CQ, int CK>
 __global__ __launch_bounds__(CQ * 2, (attn_blocks_per_cu<D, CQ, CK>())) void attn_bf16_kernel(
     const bf16* __restrict__ qp, const bf16* __restrict__ kp, const bf16* __restrict__ vp,
-    const int32_t* __restrict__ count_k, const int32_t* __restrict__ lists, int nqc, int nkc,
-    int k, float sl2, bf16* __restrict__ op, float* __restrict__ lse, int total) {
+    const int32_t* __restrict__ count_k, const int32_t* __restrict__ lists,
+    const int32_t* __restrict__ lens, int nqc, int nkc, int k, float sl2, bf16* __restrict__ op,
+    float* __restrict__ lse, int total) {
   constexpr int NW = CQ / 32;
   constexpr int MT = CK / 32;
   constexpr int KS = D / 16;
@@ -78,6 +79,8 @@ __global__ __launch_bounds__(CQ * 2, (attn_blocks_per_cu<D, CQ, CK>())) void att
 
   const int32_t* lst = lists + ((size_t)bh * nqc + a) * k;
   const int32_t* cnth = count_k + (size_t)bh * nkc;
+  // this query cluster's list length (uniform; clamped for memory safety)
+  const int nt = lens ? min(max(lens[(size_t)bh * nqc + a], 1), k) : k;
   auto tile_id = [&](int t) {
     int b = lst[t];
     return b < 0 ? 0 : (b >= nkc ? nkc - 1 : b);
@@ -120,7 +123,7 @@ __global__ __launch_bounds__(CQ * 2, (attn_blocks_per_cu<D, CQ, CK>())) void att
     wait_vmcnt<0>();
     wait_lgkm();
     raw_barrier();
-    if (t + 1 < k) issue(tile_id(t + 1), S ^ 1);
+    if (t + 1 < nt) issue(tile_id(t + 1), S ^ 1);
     const char* ks = smem + S * STAGE;
     const char* vs = ks + KBYTES;
     const int cnt = cnth[tile_id(t)];
@@ -197,9 +200,9 @@ __global__ __launch_bounds__(CQ * 2, (attn_blocks_per_cu<D, CQ, CK>())) void att
   };
 
   issue(tile_id(0), 0);
-  for (int t = 0; t < k; t += 2) {
+  for (int t = 0; t < nt; t += 2) {
     body(std::integral_constant<int, 0>{}, t);
-    if (t + 1 < k) body(std::integral_constant<int, 1>{}, t + 1);
+    if (t + 1 < nt) body(std::integral_constant<int, 1>{}, t + 1);
   }
 
   const float l_tot = l_run + wave_xor32(l_run);
@@ -221,8 +224,9 @@ __global__ __launch_bounds__(CQ * 2, (attn_blocks_per_cu<D, CQ, CK>())) void att
 template <int DP>
 __global__ __launch_bounds__(256) void attn_f32_kernel(
     const float* __restrict__ qp, const float* __restrict__ kp, const float* __restrict__ vp,
-    const int32_t* __restrict__ count_k, const int32_t* __restrict__ lists, int nqc, int nkc,
-    int cq, int ck, int d, int k, float scale, float* __restrict__ op, float* __restrict__ lse) {
+    const int32_t* __restrict__ count_k, const int32_t* __restrict__ lists,
+    const int32_t* __restrict__ lens, int nqc, int nkc, int cq, int ck, int d, int k, float scale,
+    float* __restrict__ op, float* __restrict__ lse) {
   constexpr int KC = 32;
   __shared__ float Ksh[KC][DP + 1];
   __shared__ float Vsh[KC][DP + 1];
@@ -238,7 +242,8 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
   }
   float m = -INFINITY, l = 0.f;
   const int32_t* lst = lists + ((size_t)bh * nqc + a) * k;
-  for (int tt = 0; tt < k; ++tt) {
+  const int nt = lens ? min(max(lens[(size_t)bh * nqc + a], 1), k) : k;
+  for (int tt = 0; tt < nt; ++tt) {
     int b = lst[tt];
     b = b < 0 ? 0 : (b >= nkc ? nkc - 1 : b);
     const int cnt = count_k[(size_t)bh * nkc + b];
@@ -283,24 +288,24 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
 
 template <int D, int CQ, int CK>
 hipError_t run_bf16(const Prob& P, const void* qp, const void* kp, const void* vp,
-                    const int32_t* count_k, const int32_t* lists, int k, float scale, void* op,
-                    float* lse, hipStream_t st) {
+                    const int32_t* count_k, const int32_t* lists, const int32_t* lens, int k,
+                    float scale, void* op, float* lse, hipStream_t st) {
   int total = P.BH * P.nqc;
   hipLaunchKernelGGL((attn_bf16_kernel<D, CQ, CK>), dim3(total), dim3(CQ * 2), 0, st,
-                     (const bf16*)qp, (const bf16*)kp, (const bf16*)vp, count_k, lists, P.nqc,
-                     P.nkc, k, scale * kLog2e, (bf16*)op, lse, total);
+                     (const bf16*)qp, (const bf16*)kp, (const bf16*)vp, count_k, lists, lens,
+                     P.nqc, P.nkc, k, scale * kLog2e, (bf16*)op, lse, total);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_attn(const Prob& P, const void* qp, const void* kp, const void* vp,
-                       const int32_t* count_k, const int32_t* lists, int k, float scale, void* op,
-                       float* lse, hipStream_t st) {
+                       const int32_t* count_k, const int32_t* lists, const int32_t* lens, int k,
+                       float scale, void* op, float* lse, hipStream_t st) {
   if (P.dtype == CA_BF16) {
 #define CA_ATTN_CASE(D, CQ, CK) \
   if (P.d == D && P.cq == CQ && P.ck == CK) \
-    return run_bf16<D, CQ, CK>(P, qp, kp, vp, count_k, lists, k, scale, op, lse, st);
+    return run_bf16<D, CQ, CK>(P, qp, kp, vp, count_k, lists, lens, k, scale, op, lse, st);
     CA_ATTN_CASE(64, 64, 64)
     CA_ATTN_CASE(64, 64, 128)
     CA_ATTN_CASE(64, 128, 64)
@@ -316,16 +321,16 @@ hipError_t launch_attn(const Prob& P, const void* qp, const void* kp, const void
   int threads = ((P.cq + 63) / 64) * 64;
   if (P.d <= 32) {
     hipLaunchKernelGGL(attn_f32_kernel<32>, grid, dim3(threads), 0, st, (const float*)qp,
-                       (const float*)kp, (const float*)vp, count_k, lists, P.nqc, P.nkc, P.cq,
-                       P.ck, P.d, k, scale, (float*)op, lse);
+                       (const float*)kp, (const float*)vp, count_k, lists, lens, P.nqc, P.nkc,
+                       P.cq, P.ck, P.d, k, scale, (float*)op, lse);
   } else if (P.d <= 64) {
     hipLaunchKernelGGL(attn_f32_kernel<64>, grid, dim3(threads), 0, st, (const float*)qp,
-                       (const float*)kp, (const float*)vp, count_k, lists, P.nqc, P.nkc, P.cq,
-                       P.ck, P.d, k, scale, (float*)op, lse);
+                       (const float*)kp, (const float*)vp, count_k, lists, lens, P.nqc, P.nkc,
+                       P.cq, P.ck, P.d, k, scale, (float*)op, lse);
   } else {
     hipLaunchKernelGGL(attn_f32_kernel<128>, grid, dim3(threads), 0, st, (const float*)qp,
-                       (const float*)kp, (const float*)vp, count_k, lists, P.nqc, P.nkc, P.cq,
-                       P.ck, P.d, k, scale, (float*)op, lse);
+                       (const float*)kp, (const float*)vp, count_k, lists, lens, P.nqc, P.nkc,
+                       P.cq, P.ck, P.d, k, scale, (float*)op, lse);
   }
   return hipGetLastError();
 }

@@ -2173,20 +2173,27 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
                          (int)M_A0, (int)M_E0, (int)M_CK, (int)M_EK,
                          P.dtype == CA_BF16 ? (int)O_FK : -1);
       CA_CHECK();
-      const size_t qlds = kQnormLds;
-      if (mfma && d == 64)
-        hipLaunchKernelGGL(qnorm_mfma_kernel<64>, dim3(C.nblk, BH), dim3(256), 0, st, C);
-      else if (mfma)
-        hipLaunchKernelGGL(qnorm_mfma_kernel<128>, dim3(C.nblk, BH), dim3(256), 0, st, C);
-      else
-        hipLaunchKernelGGL(qnorm_partial_kernel, dim3(C.nblk, BH), dim3(256), qlds, st, C);
-      CA_CHECK();
-      hipLaunchKernelGGL(qnorm_finish_kernel, dim3((d * d + d + 255) / 256, BH), dim3(256), 0, st, C);
-      CA_CHECK();
+      if (P.xf == CA_XF_METRIC) {
+        const size_t qlds = kQnormLds;
+        if (mfma && d == 64)
+          hipLaunchKernelGGL(qnorm_mfma_kernel<64>, dim3(C.nblk, BH), dim3(256), 0, st, C);
+        else if (mfma)
+          hipLaunchKernelGGL(qnorm_mfma_kernel<128>, dim3(C.nblk, BH), dim3(256), 0, st, C);
+        else
+          hipLaunchKernelGGL(qnorm_partial_kernel, dim3(C.nblk, BH), dim3(256), qlds, st, C);
+        CA_CHECK();
+        hipLaunchKernelGGL(qnorm_finish_kernel, dim3((d * d + d + 255) / 256, BH), dim3(256), 0,
+                           st, C);
+        CA_CHECK();
+      }
       // keys: C2 = S_q^T C_K S_q, oriented by S_q^T mu_K, T_K = S_q U2
       J.j[0] = {M_CK, M_E0, V_MUK, 0, V_KQ, -1, M_C2, V_L2, M_E0, M_TK, wk};
-      // queries: cov(r(q)), oriented by mu_r, W_Q = S_k U3
-      if (mfma)
+      if (P.xf == CA_XF_ADAPTIVE)
+        // queries: cov(q S_k) = S_k^T (Q^T Q / n - mu_Q mu_Q^T) S_k, oriented by
+        // S_k^T mu_Q (the mean of q S_k), W_Q = S_k U3; no normalisation
+        J.j[1] = {M_A0, M_EK, V_MUQ, 1, -1, -1, M_C3, V_L3, M_EK, M_TQ, wq};
+      else if (mfma)
+        // queries: cov(r(q)), oriented by mu_r, W_Q = S_k U3
         J.j[1] = {M_C3, M_EK, V_MUR, 1, V_MUR, -1, M_C3, V_L3, M_EK, M_TQ, wq};
       else
         J.j[1] = {M_C3, -1, V_MUR, 1, -1, -1, M_C3, V_L3, M_EK, M_TQ, wq};

@@ -111,8 +111,9 @@ constexpr int comp_blocks_per_cu() {
 template <int D, int CQ>
 __global__ __launch_bounds__(CQ * 2, (comp_blocks_per_cu<D, CQ>())) void comp_bf16_kernel(
     const bf16* __restrict__ qp, const char* __restrict__ tiles,
-    const int32_t* __restrict__ lists, int nq, int H, int nqc, int nkc, int ntile, int k,
-    float sl2, int enable, const bf16* __restrict__ op, const float* __restrict__ lse_s,
+    const int32_t* __restrict__ lists, const int32_t* __restrict__ lens, int nq, int H, int nqc,
+    int nkc, int ntile, int k, float sl2, int enable, const bf16* __restrict__ op,
+    const float* __restrict__ lse_s,
     const int32_t* __restrict__ perm_q, bf16* __restrict__ out, float* __restrict__ lse_out,
     int layout, int total) {
   constexpr int NW = CQ / 32;
@@ -158,7 +159,9 @@ __global__ __launch_bounds__(CQ * 2, (comp_blocks_per_cu<D, CQ>())) void comp_bf
   float ls = 0.f;
   int orig = 0;
   bf16x4 s4[DT][4];
-  const bool do_comp = enable && k < nkc;
+  // this query cluster's list length (uniform; clamped for memory safety)
+  const int nsel = lens ? min(max(lens[(size_t)bh * nqc + a], 1), k) : k;
+  const bool do_comp = enable && nsel < nkc;
   const char* th = tiles + (size_t)bh * ntile * STAGE;
   const TileCopy<KROW, KLD, NW> kcopy(w, lane);
   const TileCopy<VROW, VLD, NW> vcopy(w, lane);
@@ -196,7 +199,7 @@ __global__ __launch_bounds__(CQ * 2, (comp_blocks_per_cu<D, CQ>())) void comp_bf
     wait_lgkm();
     raw_barrier();  // selmask cleared
     const int32_t* lst = lists + ((size_t)bh * nqc + a) * k;
-    for (int i = tid; i < k; i += T) {
+    for (int i = tid; i < nsel; i += T) {
       int b = lst[i];
       if (b >= 0 && b < nkc) atomicOr(&selmask[b >> 5], 1u << (b & 31));
     }
@@ -360,8 +363,9 @@ template <int DP>
 __global__ __launch_bounds__(256) void comp_f32_kernel(
     const float* __restrict__ qp, const float* __restrict__ cent_k,
     const float* __restrict__ cent_v, const int32_t* __restrict__ count_k,
-    const int32_t* __restrict__ lists, int nq, int H, int nqc, int nkc, int cq, int d, int k,
-    float scale, int enable, const float* __restrict__ op, const float* __restrict__ lse_s,
+    const int32_t* __restrict__ lists, const int32_t* __restrict__ lens, int nq, int H, int nqc,
+    int nkc, int cq, int d, int k, float scale, int enable, const float* __restrict__ op,
+    const float* __restrict__ lse_s,
     const int32_t* __restrict__ perm_q, float* __restrict__ out, float* __restrict__ lse_out,
     int layout) {
   constexpr int KC = 32;
@@ -373,7 +377,8 @@ __global__ __launch_bounds__(256) void comp_f32_kernel(
   const int prow = a * cq + i;
   const bool active = i < cq && prow < nq;
   const size_t qrow = ((size_t)bh * nqc + a) * cq + (i < cq ? i : 0);
-  const bool do_comp = enable && k < nkc;
+  const int nsel = lens ? min(max(lens[(size_t)bh * nqc + a], 1), k) : k;
+  const bool do_comp = enable && nsel < nkc;
   float q[DP], o[DP];
 #pragma unroll
   for (int t = 0; t < DP; ++t) {
@@ -386,7 +391,7 @@ __global__ __launch_bounds__(256) void comp_f32_kernel(
     for (int e = i; e < nwords; e += blockDim.x) selmask[e] = 0u;
     __syncthreads();
     const int32_t* lst = lists + ((size_t)bh * nqc + a) * k;
-    for (int e = i; e < k; e += blockDim.x) {
+    for (int e = i; e < nsel; e += blockDim.x) {
       int b = lst[e];
       if (b >= 0 && b < nkc) atomicOr(&selmask[b >> 5], 1u << (b & 31));
     }
@@ -446,19 +451,20 @@ __global__ __launch_bounds__(256) void comp_f32_kernel(
 
 template <int D, int CQ>
 hipError_t run_bf16(const Prob& P, const void* qp, const float* cent_k, const float* cent_v,
-                    const int32_t* count_k, const int32_t* lists, int k, float scale, int enable,
-                    const void* op, const float* lse, const int32_t* perm_q, void* out,
-                    float* lse_out, char* tiles, hipStream_t st) {
+                    const int32_t* count_k, const int32_t* lists, const int32_t* lens, int k,
+                    float scale, int enable, const void* op, const float* lse,
+                    const int32_t* perm_q, void* out, float* lse_out, char* tiles,
+                    hipStream_t st) {
   const int total = P.BH * P.nqc;
   const int ntile = (P.nkc + kCompTile - 1) / kCompTile;
-  const bool do_comp = enable && k < P.nkc;
+  const bool do_comp = enable && (k < P.nkc || lens);
   if (do_comp) {
     if (!tiles) return hipErrorInvalidValue;
     hipLaunchKernelGGL(comp_stage_kernel<D>, dim3(ntile, P.BH, 2), dim3(256), 0, st, cent_k,
                        cent_v, count_k, P.nkc, ntile, tiles);
   }
   hipLaunchKernelGGL((comp_bf16_kernel<D, CQ>), dim3(total), dim3(CQ * 2), 0, st,
-                     (const bf16*)qp, (const char*)tiles, lists, P.nq, P.H, P.nqc, P.nkc, ntile, k,
+                     (const bf16*)qp, (const char*)tiles, lists, lens, P.nq, P.H, P.nqc, P.nkc, ntile, k,
                      scale * kLog2e, enable, (const bf16*)op, lse, perm_q, (bf16*)out, lse_out,
                      P.layout, total);
   return hipGetLastError();
@@ -467,14 +473,15 @@ hipError_t run_bf16(const Prob& P, const void* qp, const float* cent_k, const fl
 }  // namespace
 
 hipError_t launch_comp(const Prob& P, const void* qp, const float* cent_k, const float* cent_v,
-                       const int32_t* count_k, const int32_t* lists, int k, float scale,
+                       const int32_t* count_k, const int32_t* lists, const int32_t* lens, int k,
+                       float scale,
                        int enable, const void* op, const float* lse, const int32_t* perm_q,
                        void* out, float* lse_out, char* tiles, hipStream_t st) {
   if (P.nkc > kMaskWords * 32) return hipErrorInvalidValue;
   if (P.dtype == CA_BF16) {
 #define CA_COMP_CASE(D, CQ) \
   if (P.d == D && P.cq == CQ) \
-    return run_bf16<D, CQ>(P, qp, cent_k, cent_v, count_k, lists, k, scale, enable, op, lse, \
+    return run_bf16<D, CQ>(P, qp, cent_k, cent_v, count_k, lists, lens, k, scale, enable, op, lse, \
                            perm_q, out, lse_out, tiles, st);
     CA_COMP_CASE(64, 64)
     CA_COMP_CASE(64, 128)
@@ -487,7 +494,8 @@ hipError_t launch_comp(const Prob& P, const void* qp, const float* cent_k, const
   const int threads = ((P.cq + 63) / 64) * 64;
 #define CA_COMP_F32(DP)                                                                       \
   hipLaunchKernelGGL(comp_f32_kernel<DP>, grid, dim3(threads), 0, st, (const float*)qp,       \
-                     cent_k, cent_v, count_k, lists, P.nq, P.H, P.nqc, P.nkc, P.cq, P.d, k,   \
+                     cent_k, cent_v, count_k, lists, lens, P.nq, P.H, P.nqc, P.nkc, P.cq, P.d, \
+                     k,                                                                       \
                      scale, enable, (const float*)op, lse, perm_q, (float*)out, lse_out,      \
                      P.layout)
   if (P.d <= 32)

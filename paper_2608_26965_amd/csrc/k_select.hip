@@ -1,5 +1,5 @@
-// Cluster assignment (paper: Method, Cluster assignment - scoring and top-k
-// selection).
+// Cluster assignment (paper: Method, Cluster assignment - scoring, top-k
+// selection and the two-pass histogram selection).
 //
 // scores[a][b] = qbar_a . kbar_b in fp32 (fixed summation order, so scores are
 // reproducible); lists[a] = the k key clusters of largest score, ties to the
@@ -172,6 +172,194 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ S, 
   }
 }
 
+// ---------------------------------------------------------------------------
+// Two-pass histogram selection (paper: Method, Cluster assignment -
+// selection). One block per row: the grid position g of every score on a
+// 128 x 128 grid over [min, max] of the row (fp32), coarse counts and masses
+// (the estimated attention mass count_b * exp(tau (S_b - max)) in 2^-32
+// fixed point, so the sums are exact), the highest coarse bin whose lower
+// edge keeps both thresholds, the same on the 128 fine bins inside it, then
+// every b with g_b at or above that edge, in ascending order.
+// ---------------------------------------------------------------------------
+
+constexpr int kHistBins = 128;
+constexpr int kHistGrid = kHistBins * kHistBins;
+
+__device__ __forceinline__ float block_min_max(float v, bool want_max, float* sh) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float y = __shfl_xor(v, o, 64);
+    v = want_max ? fmaxf(v, y) : fminf(v, y);
+  }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (lane == 0) sh[w] = v;
+  __syncthreads();
+  float r = sh[0];
+#pragma unroll
+  for (int i = 1; i < 4; ++i) r = want_max ? fmaxf(r, sh[i]) : fminf(r, sh[i]);
+  __syncthreads();
+  return r;
+}
+
+__device__ __forceinline__ unsigned long long block_sum_u64(unsigned long long v,
+                                                            unsigned long long* sh) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (lane == 0) sh[w] = v;
+  __syncthreads();
+  const unsigned long long r = sh[0] + sh[1] + sh[2] + sh[3];
+  __syncthreads();
+  return r;
+}
+
+// Estimated mass of one key cluster in 2^-32 units (fp64 arithmetic).
+__device__ __forceinline__ unsigned long long mass_units(float s, float hi, int count, float tau) {
+  const double m = (double)count * exp((double)tau * ((double)s - (double)hi));
+  return (unsigned long long)floor(m * 4294967296.0 + 0.5);
+}
+
+// Wavefront 0: the highest bin b whose suffix (bins >= b, plus the given
+// count and mass above them) holds both thresholds; also the suffix just
+// above b. The condition only grows as b decreases, so b = (number of bins
+// that hold it) - 1. Bin 0 always holds it for the thresholds this kernel is
+// given.
+__device__ __forceinline__ void hist_crossing(const int* cnt, const unsigned long long* ms,
+                                              int above_c, unsigned long long above_m,
+                                              int min_count, unsigned long long need, int* bin,
+                                              int* next_c, unsigned long long* next_m) {
+  const int l = threadIdx.x;  // 0..63, bins 2l and 2l + 1
+  const int c0 = cnt[2 * l], c1 = cnt[2 * l + 1];
+  const unsigned long long m0 = ms[2 * l], m1 = ms[2 * l + 1];
+  int vc = c0 + c1;
+  unsigned long long vm = m0 + m1;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {  // suffix sums over lanes >= l
+    const int yc = __shfl_down(vc, o, 64);
+    const unsigned long long ym = __shfl_down(vm, o, 64);
+    if (l + o < 64) {
+      vc += yc;
+      vm += ym;
+    }
+  }
+  const int suf0c = above_c + vc, suf1c = suf0c - c0;  // from bin 2l, from bin 2l + 1
+  const unsigned long long suf0m = above_m + vm, suf1m = suf0m - m0;
+  const bool ok0 = suf0c >= min_count && suf0m >= need;
+  const bool ok1 = suf1c >= min_count && suf1m >= need;
+  const int nok = __popcll(__ballot(ok0)) + __popcll(__ballot(ok1));
+  const int b = nok > 0 ? nok - 1 : 0;
+  // the suffix strictly above b, held by the lane of bin b + 1
+  if (b + 1 < kHistBins && ((b + 1) >> 1) == l) {
+    const bool odd = (b + 1) & 1;
+    *next_c = odd ? suf1c : suf0c;
+    *next_m = odd ? suf1m : suf0m;
+  }
+  if (b + 1 == kHistBins && l == 0) {
+    *next_c = above_c;
+    *next_m = above_m;
+  }
+  if (l == 0) *bin = b;
+}
+
+__global__ __launch_bounds__(256) void hist_select_kernel(const float* __restrict__ S,
+                                                          const int32_t* __restrict__ count_k,
+                                                          int nqc, int nkc, int min_count,
+                                                          float recall, float tau,
+                                                          int32_t* __restrict__ lists,
+                                                          int32_t* __restrict__ lens) {
+  __shared__ int cnt[kHistBins];
+  __shared__ unsigned long long ms[kHistBins];
+  __shared__ float sh_f[4];
+  __shared__ unsigned long long sh_u[4];
+  __shared__ int sh_warp[4];
+  __shared__ int sh_bin, sh_above_c;
+  __shared__ unsigned long long sh_above_m;
+  const size_t row = blockIdx.x;
+  const int bh = (int)(row / nqc);
+  const float* s = S + row * nkc;
+  const int32_t* cntk = count_k + (size_t)bh * nkc;
+  int32_t* out = lists + row * nkc;
+  const int tid = threadIdx.x;
+
+  float lo = INFINITY, hi = -INFINITY;
+  for (int b = tid; b < nkc; b += 256) {
+    lo = fminf(lo, s[b]);
+    hi = fmaxf(hi, s[b]);
+  }
+  lo = block_min_max(lo, false, sh_f);
+  hi = block_min_max(hi, true, sh_f);
+  if (!(hi > lo) || min_count >= nkc) {  // nothing to bin, or the floor takes all
+    for (int b = tid; b < nkc; b += 256) out[b] = b;
+    if (tid == 0) lens[row] = nkc;
+    return;
+  }
+  const float inv = (float)kHistGrid / (hi - lo);
+  auto grid = [&](float v) {
+    const int g = (int)floorf((v - lo) * inv);
+    return g < 0 ? 0 : (g >= kHistGrid ? kHistGrid - 1 : g);
+  };
+  const bool use_mass = recall > 0.f;
+
+  // pass 1: coarse counts and masses
+  for (int i = tid; i < kHistBins; i += 256) {
+    cnt[i] = 0;
+    ms[i] = 0ull;
+  }
+  __syncthreads();
+  unsigned long long tot = 0ull;
+  for (int b = tid; b < nkc; b += 256) {
+    const int g = grid(s[b]);
+    atomicAdd(&cnt[g / kHistBins], 1);
+    if (use_mass) {
+      const unsigned long long u = mass_units(s[b], hi, cntk[b], tau);
+      atomicAdd(&ms[g / kHistBins], u);
+      tot += u;
+    }
+  }
+  unsigned long long need = 0ull;
+  if (use_mass) {
+    tot = block_sum_u64(tot, sh_u);
+    need = (unsigned long long)ceil((double)tot * (double)recall);
+    need = need < tot ? need : tot;
+  } else {
+    __syncthreads();
+  }
+  if (tid < 64)
+    hist_crossing(cnt, ms, 0, 0ull, min_count, need, &sh_bin, &sh_above_c, &sh_above_m);
+  __syncthreads();
+  const int B = sh_bin;
+  const int above_c = sh_above_c;
+  const unsigned long long above_m = sh_above_m;
+  // pass 2: fine counts and masses inside coarse bin B
+  for (int i = tid; i < kHistBins; i += 256) {
+    cnt[i] = 0;
+    ms[i] = 0ull;
+  }
+  __syncthreads();
+  for (int b = tid; b < nkc; b += 256) {
+    const int g = grid(s[b]);
+    if (g / kHistBins != B) continue;
+    atomicAdd(&cnt[g % kHistBins], 1);
+    if (use_mass) atomicAdd(&ms[g % kHistBins], mass_units(s[b], hi, cntk[b], tau));
+  }
+  __syncthreads();
+  if (tid < 64)
+    hist_crossing(cnt, ms, above_c, above_m, min_count, need, &sh_bin, &sh_above_c, &sh_above_m);
+  __syncthreads();
+  const int G = B * kHistBins + sh_bin;
+
+  // ascending compaction of {b : g_b >= G}
+  const int per = (nkc + 255) / 256;
+  const int b0 = min(nkc, tid * per), b1 = min(nkc, b0 + per);
+  int n = 0;
+  for (int b = b0; b < b1; ++b) n += grid(s[b]) >= G;
+  int total;
+  int pos = block_scan_256(n, sh_warp, &total);
+  for (int b = b0; b < b1; ++b)
+    if (grid(s[b]) >= G) out[pos++] = b;
+  if (tid == 0) lens[row] = total;
+}
+
 }  // namespace
 
 hipError_t launch_select(const Prob& P, const float* cq, const float* ck, const float* scores_in,
@@ -190,6 +378,31 @@ hipError_t launch_select(const Prob& P, const float* cq, const float* ck, const 
   }
   hipLaunchKernelGGL(topk_kernel, dim3((unsigned)((size_t)P.BH * P.nqc)), dim3(256), 0, st, S,
                      P.nkc, k, lists);
+  return hipGetLastError();
+}
+
+}  // namespace ca
+
+namespace ca {
+
+hipError_t launch_select_hist(const Prob& P, const float* cq, const float* ck,
+                              const int32_t* count_k, const float* scores_in, float* scores,
+                              int min_count, float recall, float scale, int32_t* lists,
+                              int32_t* lens, hipStream_t st) {
+  const float* S = scores_in;
+  if (!S) {
+    dim3 grid((P.nkc + kTileS - 1) / kTileS, (P.nqc + kTileS - 1) / kTileS, P.BH);
+    hipLaunchKernelGGL(scores_kernel, grid, dim3(256), 0, st, cq, ck, P.nqc, P.nkc, P.d, scores);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    S = scores;
+  } else if (scores && scores != scores_in) {
+    hipError_t e = hipMemcpyAsync(scores, scores_in, (size_t)P.BH * P.nqc * P.nkc * 4,
+                                  hipMemcpyDeviceToDevice, st);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(hist_select_kernel, dim3((unsigned)((size_t)P.BH * P.nqc)), dim3(256), 0, st,
+                     S, count_k, P.nqc, P.nkc, min_count, recall, scale, lists, lens);
   return hipGetLastError();
 }
 

@@ -25,7 +25,7 @@ def test_header_symbols_exported():
     assert declared == set(L.EXPORTS)
     for name in declared:
         assert hasattr(lib, name)
-    assert lib.ca_abi_version() == 2
+    assert lib.ca_abi_version() == 3
 
 
 def _prob(**kw):
@@ -38,7 +38,7 @@ def _prob(**kw):
 
 @pytest.mark.parametrize("kw,status", [
     (dict(cq=48), 1), (dict(ck=512), 1), (dict(d=0), 1), (dict(d=129), 1), (dict(nq=0), 1),
-    (dict(dtype=7), 1), (dict(transform=3), 1), (dict(layout=2), 1), (dict(heads=0), 1),
+    (dict(dtype=7), 1), (dict(transform=4), 1), (dict(layout=2), 1), (dict(heads=0), 1),
 ])
 def test_invalid_problem(kw, status):
     L, lib = _lib()
@@ -67,20 +67,31 @@ def test_calls_reject_before_enqueue():
     assert lib.ca_cluster(p, fake, fake, None, full, fake, 16, None) == L.CA_E_WORKSPACE
     assert lib.ca_select(p, None, None, None, None, 4, fake, None, 0, None) == L.CA_E_INVALID
     assert lib.ca_select(p, fake, fake, None, None, 4, fake, None, 0, None) == L.CA_E_WORKSPACE
-    args = [fake] * 5
+    args = [fake] * 5 + [None]  # qp, kp, vp, count_k, lists; lens omitted
     assert lib.ca_block_sparse_attn(p, *args, 0, 0.0, fake, fake, None) == L.CA_E_INVALID
     assert lib.ca_block_sparse_attn(p, *args, 99, 0.0, fake, fake, None) == L.CA_E_INVALID
     assert lib.ca_block_sparse_attn(_prob(d=48), *args, 2, 0.0, fake, fake, None) == \
         L.CA_E_UNSUPPORTED
     assert lib.ca_block_sparse_attn(_prob(cq=32), *args, 2, 0.0, fake, fake, None) == \
         L.CA_E_UNSUPPORTED
-    assert lib.ca_compensate(p, fake, fake, fake, fake, fake, 2, 0.0, 1, None, fake, fake, fake,
-                             None, None, 0, None) == L.CA_E_INVALID
-    assert lib.ca_compensate(p, None, None, None, None, None, 2, 0.0, 1, fake, fake, fake, fake,
-                             None, None, 0, None) == L.CA_E_INVALID
+    assert lib.ca_compensate(p, fake, fake, fake, fake, fake, None, 2, 0.0, 1, None, fake, fake,
+                             fake, None, None, 0, None) == L.CA_E_INVALID
+    assert lib.ca_compensate(p, None, None, None, None, None, None, 2, 0.0, 1, fake, fake, fake,
+                             fake, None, None, 0, None) == L.CA_E_INVALID
     # bf16 with compensation stages the centroids in the workspace
-    assert lib.ca_compensate(p, fake, fake, fake, fake, fake, 2, 0.0, 1, fake, fake, fake, fake,
-                             None, fake, 16, None) == L.CA_E_WORKSPACE
+    assert lib.ca_compensate(p, fake, fake, fake, fake, fake, None, 2, 0.0, 1, fake, fake, fake,
+                             fake, None, fake, 16, None) == L.CA_E_WORKSPACE
+    # ... also when every list may be full length but lengths are given
+    assert lib.ca_compensate(p, fake, fake, fake, fake, fake, fake, 16, 0.0, 1, fake, fake, fake,
+                             fake, None, fake, 16, None) == L.CA_E_WORKSPACE
+    # histogram selection: lists, lens and count_k are required; thresholds in range
+    sh = [fake, fake, fake, None, None]  # cent_q, cent_k, count_k, scores_in, scores_out
+    assert lib.ca_select_hist(p, *sh, 16, 0.5, 0.0, fake, None, None, 0, None) == L.CA_E_INVALID
+    assert lib.ca_select_hist(p, *sh, 0, 0.5, 0.0, fake, fake, None, 0, None) == L.CA_E_INVALID
+    assert lib.ca_select_hist(p, *sh, 4, 1.5, 0.0, fake, fake, None, 0, None) == L.CA_E_INVALID
+    assert lib.ca_select_hist(p, *sh, 4, float("nan"), 0.0, fake, fake, None, 0, None) == \
+        L.CA_E_INVALID
+    assert lib.ca_select_hist(p, *sh, 4, 0.5, 0.0, fake, fake, fake, 16, None) == L.CA_E_WORKSPACE
     ws_misaligned = ctypes.c_void_p(0x1001)
     need = ctypes.c_size_t(0)
     lib.ca_workspace_size(p, 1, need)

@@ -186,6 +186,72 @@ def test_compensation_multi_tile(dt, d, cq, ck, n, k, whole_tile):
     G.flush(f"  max abs err {worst:.3g}")
 
 
+LENS_CASES = [
+    # dtype, d, cq, ck, n
+    ("bf16", 64, 128, 128, 20000),
+    ("bf16", 128, 64, 64, 5000),
+    ("bf16", 64, 64, 128, 9000),
+    ("f32", 64, 64, 64, 3000),
+]
+
+
+@pytest.mark.parametrize("dt,d,cq,ck,n", LENS_CASES)
+def test_attention_and_compensation_with_lengths(dt, d, cq, ck, n):
+    """Lists of varying length (histogram selection): row a uses its first
+    lens[a] entries (list stride nkc; the rest of the row holds garbage that
+    must not be read), from a single cluster to all of them."""
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    G.flush(f"lens case dt={dt} d={d} cq={cq} ck={ck} n={n}")
+    H = 2
+    Q, K, V = mixture_inputs(31, H, n, d, dt, centres=8, sigma=0.4)
+    rng = np.random.default_rng(32)
+    p = ca.Problem(1, H, n, n, d, cq, ck, G.tdtype(dt))
+    perm_q = np.stack([rng.permutation(n) for _ in range(H)]).astype(np.int32)
+    perm_k = np.stack([rng.permutation(n) for _ in range(H)]).astype(np.int32)
+    nkc = p.nkc
+    lens = rng.integers(1, nkc + 1, size=(H, p.nqc)).astype(np.int32)
+    lens[0, 0], lens[-1, -1] = 1, nkc
+    L = np.full((H, p.nqc, nkc), 10 ** 6, np.int32)  # garbage past each length
+    ragged = []
+    for h in range(H):
+        rows = []
+        for a in range(p.nqc):
+            sel = np.sort(rng.choice(nkc, size=lens[h, a], replace=False)).astype(np.int32)
+            L[h, a, :lens[h, a]] = sel
+            rows.append(sel)
+        ragged.append(rows)
+    tau = 1 / math.sqrt(d)
+    cq_n, ck_n = G.counts(n, cq), G.counts(n, ck)
+    tq = G.permuted_rows(Q, perm_q, cq, G.tdtype(dt))
+    cnt = G.dev(np.stack([ck_n] * H), torch.int32)
+    dL, dN = G.dev(L, torch.int32), G.dev(lens, torch.int32)
+    op, lse = ca.block_sparse_attn(p, tq, G.permuted_rows(K, perm_k, ck, G.tdtype(dt)),
+                                   G.value_tiles(V, perm_k, ck, G.tdtype(dt)), cnt, dL, nkc,
+                                   lens=dN)
+    kbar = np.stack([ref.centroids(K[h], perm_k[h], ck_n) for h in range(H)]).astype(np.float32)
+    vbar = np.stack([ref.centroids(V[h], perm_k[h], ck_n) for h in range(H)]).astype(np.float32)
+    out, lse_out = ca.compensate(p, tq, G.dev(kbar), G.dev(vbar), cnt, dL, nkc, op, lse,
+                                 G.dev(perm_q, torch.int32), want_lse=True, lens=dN)
+    torch.cuda.synchronize()
+    op_h, lse_h = G.host(op), G.host(lse)
+    out_h, lse_out_h = G.host(out)[0], G.host(lse_out)
+    for h in range(H):
+        o, l = ref.sparse_attention(Q[h], K[h], V[h], perm_q[h], cq_n, perm_k[h], ck_n, ragged[h],
+                                    tau)
+        assert np.abs(op_h[h, :n] - o[perm_q[h]]).max() <= G.TOL[dt]
+        assert np.abs(lse_h[h, :n] - l[perm_q[h]]).max() <= (1e-5 if dt == "f32" else 1e-3) * max(
+            1.0, np.abs(l).max())
+        # compensation from the GPU's own sparse part (in its storage precision)
+        o_s = op_h[h, :n][np.argsort(perm_q[h])]
+        l_s = lse_h[h, :n][np.argsort(perm_q[h])]
+        o_w, l_w = ref.compensate(Q[h], kbar[h], vbar[h], ck_n, perm_q[h], cq_n, ragged[h], o_s,
+                                  l_s, tau)
+        assert np.abs(out_h[h] - o_w).max() <= G.TOL[dt]
+        assert np.abs(lse_out_h[h] - l_w).max() <= 1e-4 * max(1.0, np.abs(l_w).max())
+
+
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
 def test_all_kept_equals_dense(dt):
     """Every key cluster selected: the two calls give dense attention."""

@@ -35,6 +35,10 @@ SPLIT_CASES = [
     # d below the eigensolver's padded size (zero rows in the tournament)
     ("f32", 2000, 40, 32, "metric"),
     ("bf16", 4000, 100, 64, "pca"),
+    # queries in the centred-key metric (adaptive assignment)
+    ("bf16", 20000, 64, 128, "adaptive"),
+    ("bf16", 6000, 128, 64, "adaptive"),
+    ("f32", 1500, 48, 32, "adaptive"),
 ]
 
 
@@ -108,7 +112,20 @@ def _check_split_space(Q, K, yq, yk, xf):
         assert (Y.mean(axis=0) >= -1e-4 * np.sqrt(scale)).all(), "oriented"
     rng = np.random.default_rng(0)
     pairs = rng.integers(0, len(K), size=(200, 2))
-    if xf == "metric":
+    if xf == "adaptive":
+        for a, b in pairs:
+            want = ((Q @ (K[a] - K[b])) ** 2).mean()
+            got = ((yk[a] - yk[b]) ** 2).sum()
+            assert abs(got - want) <= rtol * ((yk[a] ** 2).sum() + (yk[b] ** 2).sum()) + 1e-9
+        # queries: |y_a - y_b|^2 = (q_a - q_b)^T C_K (q_a - q_b), C_K the key covariance
+        C = ref.centred_cov(K)
+        qpairs = rng.integers(0, len(Q), size=(200, 2))
+        for a, b in qpairs:
+            dq = Q[a] - Q[b]
+            want = dq @ C @ dq
+            got = ((yq[a] - yq[b]) ** 2).sum()
+            assert abs(got - want) <= rtol * ((yq[a] ** 2).sum() + (yq[b] ** 2).sum()) + 1e-9
+    elif xf == "metric":
         for a, b in pairs:
             want = ((Q @ (K[a] - K[b])) ** 2).mean()
             got = ((yk[a] - yk[b]) ** 2).sum()

@@ -141,3 +141,69 @@ def test_pipeline_deterministic():
         assert torch.equal(x, y)
     for key in a[0]:
         assert torch.equal(a[0][key], b[0][key]), key
+
+
+@pytest.mark.parametrize("mode", ["hist", "adaptive"])
+def test_tabular_histogram_selection_pipeline(mode):
+    """The benchmarked workload (all 8 heads) through the two-pass histogram
+    selection: top-k through the histogram (k = 64, metric transform), and
+    adaptive assignment (90% of the estimated attention mass, at least 16
+    clusters, adaptive query transform). Per checked head: permutations
+    bit-exact against the oracle's split of the exported coordinates; every
+    row's list and length equal to the oracle's histogram selection of the
+    exported scores; sampled query clusters' outputs within the tolerance of
+    the oracle's compensated sparse attention given the GPU's permutations
+    and lists."""
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    G.flush(f"e2e histogram selection, mode={mode}")
+    Q, K, V = make_config(2)
+    H, n, d = Q.shape
+    c = 128
+    p = ca.Problem(1, H, n, n, d, c, c, torch.bfloat16, "metric" if mode == "hist" else "adaptive")
+    floor, recall = (64, 0.0) if mode == "hist" else (16, 0.9)
+    scale = np.float32(1.0 / math.sqrt(d))
+    tq, tk, tv = (G.dev(x[None], torch.bfloat16) for x in (Q, K, V))
+    r = ca.cluster(p, tq, tk, tv, export_y=True)
+    lists, lens, scores = ca.select_hist(p, r["cent_q"], r["cent_k"], r["count_k"], floor, recall,
+                                         float(scale), export_scores=True)
+    op, lse = ca.block_sparse_attn(p, r["qp"], r["kp"], r["vp"], r["count_k"], lists, p.nkc,
+                                   lens=lens)
+    out, _ = ca.compensate(p, r["qp"], r["cent_k"], r["cent_v"], r["count_k"], lists, p.nkc, op,
+                           lse, r["perm_q"], lens=lens)
+    torch.cuda.synchronize()
+    outh = G.host(out)[0]
+    N = lens.cpu().numpy()
+    G.flush(f"  list length: mean {N.mean():.1f}, min {N.min()}, max {N.max()} of {p.nkc}")
+    cn = G.counts(n, c)
+    for h in (0, 4, 7):
+        yq = r["yq"][h].double().cpu().numpy()
+        yk = r["yk"][h].double().cpu().numpy()
+        perm_q = r["perm_q"][h].cpu().numpy()
+        perm_k = r["perm_k"][h].cpu().numpy()
+        assert np.array_equal(perm_q, ref.split(yq, c)[0]), "query permutation"
+        assert np.array_equal(perm_k, ref.split(yk, c)[0]), "key permutation"
+        S = scores[h].double().cpu().numpy()
+        L = lists[h].cpu().numpy()
+        rows_sel = []
+        for a in range(p.nqc):
+            want = ref.hist_select(S[a], cn, float(scale), floor, float(np.float32(recall)))
+            assert N[h, a] == len(want) and np.array_equal(L[a, :N[h, a]], want), (h, a)
+            rows_sel.append(want)
+        kbar = ref.centroids(K[h], perm_k, cn)
+        vbar = ref.centroids(V[h], perm_k, cn)
+        rng = np.random.default_rng(h)
+        sample = np.unique(np.concatenate([[p.nqc - 1], rng.choice(p.nqc, 8, replace=False)]))
+        mem = ref.cluster_members(perm_q, cn)
+        rows = np.concatenate([mem[a] for a in sample])
+        sub_counts = cn[sample]
+        sub_perm = np.arange(len(rows))
+        sub_lists = [rows_sel[a] for a in sample]
+        tau = float(scale)
+        o_s, l_s = ref.sparse_attention(Q[h][rows], K[h], V[h], sub_perm, sub_counts, perm_k, cn,
+                                        sub_lists, tau)
+        o, _ = ref.compensate(Q[h][rows], kbar, vbar, cn, sub_perm, sub_counts, sub_lists, o_s,
+                              l_s, tau)
+        err = np.abs(outh[h][rows] - o).max()
+        assert err <= G.TOL["bf16"], f"head {h}: output error {err}"

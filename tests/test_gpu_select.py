@@ -47,3 +47,78 @@ def test_topk_with_ties_given_scores(k):
     L = lists.cpu().numpy()
     for h in range(H):
         assert np.array_equal(L[h], ref.topk(S[h].astype(np.float64), k))
+
+
+HIST_CASES = [
+    # nqc, nkc, d, min_count, mass_recall
+    (16, 16, 64, 4, 0.0),
+    (50, 130, 64, 13, 0.0),
+    (50, 130, 64, 16, 0.9),
+    (33, 300, 128, 16, 0.5),
+    (7, 1000, 32, 1, 0.99),
+    (200, 77, 64, 76, 0.0),
+    (64, 512, 64, 64, 0.0),   # one head of the tabular workload: top-k through the histogram
+    (64, 512, 64, 16, 0.9),   # ... and adaptive assignment
+    (5, 3000, 64, 16, 1.0),
+]
+
+
+@pytest.mark.parametrize("nqc,nkc,d,min_count,recall", HIST_CASES)
+def test_hist_select(nqc, nkc, d, min_count, recall):
+    """Two-pass histogram selection: lists and lengths equal the oracle's on
+    the GPU's own scores (count-only mode is integer work on fp32 grid
+    positions; the mass mode sums fp64 estimates in fixed point)."""
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    G.flush(f"hist select nqc={nqc} nkc={nkc} d={d} min_count={min_count} recall={recall}")
+    rng = np.random.default_rng(nqc * 7 + nkc)
+    H = 2
+    cq = (rng.standard_normal((H, nqc, d)) * 0.7).astype(np.float32)
+    ck = (rng.standard_normal((H, nkc, d)) * 0.7).astype(np.float32)
+    cnt = rng.integers(1, 129, size=(H, nkc)).astype(np.int32)
+    p = ca.Problem(1, H, nqc * 64, nkc * 64, d, 64, 64, torch.bfloat16)
+    scale = np.float32(1.0 / np.sqrt(d))
+    lists, lens, scores = ca.select_hist(p, G.dev(cq), G.dev(ck), G.dev(cnt, torch.int32),
+                                         min_count, recall, float(scale), export_scores=True)
+    torch.cuda.synchronize()
+    S = scores.cpu().numpy().astype(np.float64)
+    L, N = lists.cpu().numpy(), lens.cpu().numpy()
+    worst = 0
+    for h in range(H):
+        for a in range(nqc):
+            want = ref.hist_select(S[h, a], cnt[h], float(scale), min_count,
+                                   float(np.float32(recall)))
+            assert N[h, a] == len(want), (h, a, N[h, a], len(want))
+            assert np.array_equal(L[h, a, :N[h, a]], want), (h, a)
+            worst = max(worst, len(want))
+    G.flush(f"  longest list {worst} of {nkc}")
+
+
+@pytest.mark.parametrize("min_count,recall", [(5, 0.0), (1, 0.7), (16, 0.95)])
+def test_hist_select_ties_and_degenerate_rows(min_count, recall):
+    """Integer scores with many exact ties (-0.0 and +0.0 among them), rows
+    whose scores are all equal, and a row of one distinct value plus one
+    outlier, given through scores_in."""
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    rng = np.random.default_rng(min_count)
+    H, nqc, nkc = 2, 12, 40
+    S = rng.integers(-3, 4, size=(H, nqc, nkc)).astype(np.float32)
+    S[S == 0] = np.where(rng.random((S == 0).sum()) < 0.5, -0.0, 0.0)
+    S[0, 3] = 1.5                      # all equal
+    S[1, 5] = 2.0
+    S[1, 5, 17] = 9.0                  # one outlier
+    cnt = rng.integers(1, 65, size=(H, nkc)).astype(np.int32)
+    p = ca.Problem(1, H, nqc * 16, nkc * 16, 8, 16, 16, torch.float32)
+    lists, lens, _ = ca.select_hist(p, None, None, G.dev(cnt, torch.int32), min_count, recall,
+                                    0.25, scores_in=G.dev(S))
+    torch.cuda.synchronize()
+    L, N = lists.cpu().numpy(), lens.cpu().numpy()
+    for h in range(H):
+        for a in range(nqc):
+            want = ref.hist_select(S[h, a].astype(np.float64), cnt[h], 0.25, min_count,
+                                   float(np.float32(recall)))
+            assert N[h, a] == len(want) and np.array_equal(L[h, a, :N[h, a]], want), (h, a)
+    assert N[0, 3] == nkc

@@ -71,7 +71,7 @@ def _hist_bruteforce(S, counts, tau, min_count, mass_recall):
     if g is None or min_count >= n:
         return np.arange(n)
     mass = ref.hist_mass_units(S, counts, tau)
-    need = int(np.ceil(float(mass_recall) * float(mass.sum())))
+    need = min(int(np.ceil(float(mass_recall) * float(mass.sum()))), int(mass.sum()))
     for G in range(ref.HIST_GRID - 1, -1, -1):
         up = g >= G
         if up.sum() >= min_count and mass[up].sum() >= need:
