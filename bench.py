@@ -71,6 +71,60 @@ def time_oracle(Q, K, V, c, k):
     return dt, threads
 
 
+def time_selection_modes(ca, torch, p, q, k, v, keep_k, out, args):
+    """The same layer with the two-pass histogram selection, timed after (and
+    apart from) the headline run: top-k through the histogram (at least
+    keep_k clusters, metric transform) and adaptive assignment (90% of the
+    estimated attention mass, at least 16 clusters, adaptive transform).
+    Per call ms (HIP events, mean over the timed steps), ms per layer and the
+    mean number of selected key clusters per query cluster."""
+    res = {}
+    for name, xf, floor, recall in (("hist_topk", "metric", keep_k, 0.0),
+                                    ("adaptive_mass0.9_min16", "adaptive", 16, 0.9)):
+        pm = ca.Problem(p.batch, p.heads, p.nq, p.nk, p.d, p.cq, p.ck, p.dtype, xf, p.layout)
+        ws = ca.workspace(pm, q.device, keep_k)
+        lens_seen = []
+
+        def step(ev=None):
+            if ev:
+                ev[0].record()
+            r = ca.cluster(pm, q, k, v, ws=ws)
+            if ev:
+                ev[1].record()
+            lists, lens, _ = ca.select_hist(pm, r["cent_q"], r["cent_k"], r["count_k"], floor,
+                                            recall, ws=ws)
+            if ev:
+                ev[2].record()
+            op, lse = ca.block_sparse_attn(pm, r["qp"], r["kp"], r["vp"], r["count_k"], lists,
+                                           pm.nkc, lens=lens)
+            if ev:
+                ev[3].record()
+            ca.compensate(pm, r["qp"], r["cent_k"], r["cent_v"], r["count_k"], lists, pm.nkc, op,
+                          lse, r["perm_q"], out=out, ws=ws, lens=lens)
+            if ev:
+                ev[4].record()
+            return lens
+
+        for _ in range(args.warmup):
+            step()
+        steps = max(3, args.steps // 2)
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for s in range(steps):
+            lens = step(evs[s])
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / steps
+        calls = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(4)] for e in evs]).mean(0)
+        res[name] = {"transform": xf, "min_count": floor, "mass_recall": recall,
+                     "ms_per_step": round(ms, 4),
+                     "breakdown_ms": {"cluster": round(calls[0], 4), "select": round(calls[1], 4),
+                                      "block_sparse_attn": round(calls[2], 4),
+                                      "compensate": round(calls[3], 4)},
+                     "mean_clusters": round(float(lens.float().mean()), 2)}
+    return res
+
+
 def copy_calibration():
     """A plain device copy of 256 MiB (fp32), three launches."""
     import torch
@@ -89,6 +143,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-modes", action="store_true",
+                    help="skip the histogram-selection modes timed after the headline run")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy three times: the known-size "
                          "reference that scales the FETCH_SIZE / WRITE_SIZE counters")
@@ -181,6 +237,8 @@ def main():
                                  if attn_fingerprint() == ATTN_TRAFFIC["fingerprint"] else None)},
         "compensate_tflops": round(f_comp / (call_ms[3] * 1e-3) / 1e12, 2),
     }
+    if not args.no_modes:
+        rec["modes"] = time_selection_modes(ca, torch, p, q, k, v, keep_k, out, args)
     if not args.no_cpu_baseline:
         t_head, threads = time_oracle(Qh[0], Kh[0], Vh[0], c, keep_k)
         rec["cpu_baseline"] = {
