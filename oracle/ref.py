@@ -91,7 +91,35 @@ def pca_basis(X):
     return orient(U, X.mean(axis=0))
 
 
-def key_split_space(Q, K, mode):
+SPLITMIX_GAMMA = 0x9E3779B97F4A7C15
+
+
+def splitmix64(c):
+    """Output number c (counting from 0) of splitmix64 started at state 0, the
+    generator published by S. Vigna: the state after c + 1 increments by the
+    golden-ratio constant, passed through the published mixing function.
+    Vectorised over uint64 arrays (arithmetic modulo 2^64)."""
+    z = (np.asarray(c, dtype=np.uint64) + np.uint64(1)) * np.uint64(SPLITMIX_GAMMA)
+    z = (z ^ (z >> np.uint64(30))) * np.uint64(0xBF58476D1CE4E5B9)
+    z = (z ^ (z >> np.uint64(27))) * np.uint64(0x94D049BB133111EB)
+    return z ^ (z >> np.uint64(31))
+
+
+def random_split_space(n, d, head, side):
+    """Split coordinates of the random-cluster control (Experiments:
+    baselines, random clusters with top-k routing through centroid scores):
+    y[i][j] = (top 24 bits of splitmix64 output c) / 2^24, c = (((2 head +
+    side) << 22 | i) << 7) | j, side 0 for queries and 1 for keys. Splitting
+    on these coordinates partitions the tokens into clusters at random.
+    Reading: the paper does not say how its random assignment is drawn; a
+    counter-based generator makes it reproducible on both sides."""
+    i = np.arange(n, dtype=np.uint64)[:, None]
+    j = np.arange(d, dtype=np.uint64)[None, :]
+    c = (((np.uint64(2 * head + side) << np.uint64(22)) | i) << np.uint64(7)) | j
+    return (splitmix64(c) >> np.uint64(40)).astype(F64) * 2.0 ** -24
+
+
+def key_split_space(Q, K, mode, head=0):
     """Split coordinates Y_K of the keys.
 
     none:     Y_K = K.
@@ -101,10 +129,13 @@ def key_split_space(Q, K, mode):
               the principal axes of K S_q (diagonalized splitting). The
               principal axes of K S_q are the eigenvectors of S_q^T C_K S_q.
     adaptive: as metric (the key side does not depend on the selection mode).
+    random:   pseudo-random coordinates (random_split_space, side 1).
     """
     Q, K = np.asarray(Q, F64), np.asarray(K, F64)
     if mode == "none":
         return K.copy()
+    if mode == "random":
+        return random_split_space(K.shape[0], K.shape[1], head, 1)
     if mode == "pca":
         return K @ pca_basis(K)
     if mode in ("metric", "adaptive"):
@@ -137,14 +168,16 @@ def query_representation_adaptive(Q, K):
     return Q @ psd_root(centred_cov(K))
 
 
-def query_split_space(Q, K, mode):
+def query_split_space(Q, K, mode, head=0):
     """Split coordinates Y_Q of the queries: none -> Q; pca -> Q on its principal
     axes; metric -> r(q) (top-k representation) on its principal axes;
     adaptive -> the unnormalised centred-key representation on its principal
-    axes."""
+    axes; random -> pseudo-random coordinates (side 0)."""
     Q = np.asarray(Q, F64)
     if mode == "none":
         return Q.copy()
+    if mode == "random":
+        return random_split_space(Q.shape[0], Q.shape[1], head, 0)
     if mode == "pca":
         return Q @ pca_basis(Q)
     if mode == "metric":
@@ -438,7 +471,7 @@ def compensate(Q, kbar, vbar, counts_k, perm_q, counts_q, lists, o_s, lse_s, tau
 
 def forward(Q, K, V, cq, ck, k, mode="metric", enable_comp=True, tau=None,
             perm_q=None, perm_k=None, lists=None, scores=None, select="topk",
-            mass_recall=0.0):
+            mass_recall=0.0, head=0):
     """ClusterAttention for one head: clustering -> centroids -> scores ->
     selection -> block-sparse attention -> compensation (Method: overview).
 
@@ -454,10 +487,10 @@ def forward(Q, K, V, cq, ck, k, mode="metric", enable_comp=True, tau=None,
     tau = 1.0 / np.sqrt(d) if tau is None else tau
     r = {}
     if perm_q is None:
-        r["yq"] = query_split_space(Q, K, mode)
+        r["yq"] = query_split_space(Q, K, mode, head)
         perm_q, _, _ = split(r["yq"], cq)
     if perm_k is None:
-        r["yk"] = key_split_space(Q, K, mode)
+        r["yk"] = key_split_space(Q, K, mode, head)
         perm_k, _, _ = split(r["yk"], ck)
     nq, nk = Q.shape[0], K.shape[0]
     counts_q = np.array([min(cq, nq - a * cq) for a in range(-(-nq // cq))])

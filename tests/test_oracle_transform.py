@@ -145,3 +145,33 @@ def test_clamped_root_of_indefinite_matrix():
     S = ref.psd_root(A)
     want = E @ np.diag([4.0, 1.0, 0.0]) @ E.T
     assert np.abs(S @ S.T - want).max() < 1e-13
+
+
+def test_splitmix64_published_outputs():
+    """The generator behind the random-cluster control: its first outputs from
+    state 0 as published with splitmix64."""
+    out = ref.splitmix64(np.arange(3))
+    assert [int(x) for x in out] == [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F]
+
+
+def test_random_split_space():
+    """Coordinates are 24-bit fractions in [0, 1), differ between heads and
+    sides, look uniform, and splitting on them gives valid clusters whose
+    membership does not follow the data."""
+    Y = ref.random_split_space(5000, 16, head=3, side=1)
+    assert Y.shape == (5000, 16) and Y.min() >= 0.0 and Y.max() < 1.0
+    assert np.array_equal(Y * 2 ** 24, np.floor(Y * 2 ** 24))
+    assert abs(Y.mean() - 0.5) < 0.01 and abs(Y.var() - 1 / 12) < 0.005
+    assert not np.array_equal(Y, ref.random_split_space(5000, 16, head=3, side=0))
+    assert not np.array_equal(Y, ref.random_split_space(5000, 16, head=4, side=1))
+    c = ref.random_split_space(1, 4, head=0, side=0)[0]
+    want = (ref.splitmix64(np.arange(4)) >> np.uint64(40)).astype(float) * 2.0 ** -24
+    assert np.array_equal(c, want)  # head 0, queries, token 0: outputs 0..3
+    Q, K = _mix(10)
+    yq = ref.query_split_space(Q, K, "random", head=2)
+    perm, cid, counts = ref.split(yq, 16)
+    assert sorted(perm) == list(range(len(Q)))
+    # clusters of random coordinates ignore the data: cluster means of Q stay
+    # near the global mean (a data-driven split would separate them)
+    means = ref.centroids(Q, perm, counts)
+    assert np.abs(means - Q.mean(axis=0)).max() < 6 * Q.std(axis=0).max() / np.sqrt(16)
