@@ -72,15 +72,17 @@ def time_oracle(Q, K, V, c, k):
 
 
 def time_selection_modes(ca, torch, p, q, k, v, keep_k, out, args):
-    """The same layer with the two-pass histogram selection, timed after (and
-    apart from) the headline run: top-k through the histogram (at least
-    keep_k clusters, metric transform) and adaptive assignment (90% of the
-    estimated attention mass, at least 16 clusters, adaptive transform).
-    Per call ms (HIP events, mean over the timed steps), ms per layer and the
-    mean number of selected key clusters per query cluster."""
+    """The same layer in the other modes, timed after (and apart from) the
+    headline run: top-k through the two-pass histogram (at least keep_k
+    clusters, metric transform), adaptive assignment (90% of the estimated
+    attention mass, at least 16 clusters, adaptive transform) and the
+    random-cluster control (random clusters, exact top-k of keep_k). Per call
+    ms (HIP events, mean over the timed steps), ms per layer and the mean
+    number of selected key clusters per query cluster."""
     res = {}
     for name, xf, floor, recall in (("hist_topk", "metric", keep_k, 0.0),
-                                    ("adaptive_mass0.9_min16", "adaptive", 16, 0.9)):
+                                    ("adaptive_mass0.9_min16", "adaptive", 16, 0.9),
+                                    ("random_clusters_topk", "random", keep_k, None)):
         pm = ca.Problem(p.batch, p.heads, p.nq, p.nk, p.d, p.cq, p.ck, p.dtype, xf, p.layout)
         ws = ca.workspace(pm, q.device, keep_k)
         lens_seen = []
@@ -91,15 +93,20 @@ def time_selection_modes(ca, torch, p, q, k, v, keep_k, out, args):
             r = ca.cluster(pm, q, k, v, ws=ws)
             if ev:
                 ev[1].record()
-            lists, lens, _ = ca.select_hist(pm, r["cent_q"], r["cent_k"], r["count_k"], floor,
-                                            recall, ws=ws)
+            if recall is None:  # exact top-k
+                lists, _ = ca.select(pm, r["cent_q"], r["cent_k"], floor, ws=ws)
+                lens, stride = None, floor
+            else:
+                lists, lens, _ = ca.select_hist(pm, r["cent_q"], r["cent_k"], r["count_k"], floor,
+                                                recall, ws=ws)
+                stride = pm.nkc
             if ev:
                 ev[2].record()
             op, lse = ca.block_sparse_attn(pm, r["qp"], r["kp"], r["vp"], r["count_k"], lists,
-                                           pm.nkc, lens=lens)
+                                           stride, lens=lens)
             if ev:
                 ev[3].record()
-            ca.compensate(pm, r["qp"], r["cent_k"], r["cent_v"], r["count_k"], lists, pm.nkc, op,
+            ca.compensate(pm, r["qp"], r["cent_k"], r["cent_v"], r["count_k"], lists, stride, op,
                           lse, r["perm_q"], out=out, ws=ws, lens=lens)
             if ev:
                 ev[4].record()
@@ -116,12 +123,14 @@ def time_selection_modes(ca, torch, p, q, k, v, keep_k, out, args):
         torch.cuda.synchronize()
         ms = (time.perf_counter() - t0) * 1e3 / steps
         calls = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(4)] for e in evs]).mean(0)
-        res[name] = {"transform": xf, "min_count": floor, "mass_recall": recall,
+        res[name] = {"transform": xf, "min_count": floor,
+                     "mass_recall": recall if recall is not None else "exact top-k",
                      "ms_per_step": round(ms, 4),
                      "breakdown_ms": {"cluster": round(calls[0], 4), "select": round(calls[1], 4),
                                       "block_sparse_attn": round(calls[2], 4),
                                       "compensate": round(calls[3], 4)},
-                     "mean_clusters": round(float(lens.float().mean()), 2)}
+                     "mean_clusters": (round(float(lens.float().mean()), 2) if lens is not None
+                                       else float(floor))}
     return res
 
 

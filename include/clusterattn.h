@@ -85,12 +85,20 @@ typedef enum { CA_F32 = 0, CA_BF16 = 1 } ca_dtype;
  *                 r(q) = q S_k (the metric K_c^T K_c / n of the centred keys,
  *                 Method: query clustering for adaptive assignment; App. B.1),
  *                 on its principal coordinates. For use with the adaptive
- *                 (attention-mass) selection of ca_select_hist. */
+ *                 (attention-mass) selection of ca_select_hist.
+ *   CA_XF_RANDOM: the random-cluster control (Experiments: baselines, random
+ *                 clusters routed by centroid scores): tokens are split on
+ *                 pseudo-random coordinates y[i][j] = (splitmix64 output
+ *                 number c, top 24 bits) / 2^24 with c = (((2 bh + side) <<
+ *                 22 | i) << 7) | j (bh = b * heads + h, side 0 queries / 1
+ *                 keys; splitmix64 as published by S. Vigna, started at state
+ *                 0), which partitions them into clusters at random. */
 typedef enum {
   CA_XF_NONE = 0,
   CA_XF_PCA = 1,
   CA_XF_METRIC = 2,
-  CA_XF_ADAPTIVE = 3
+  CA_XF_ADAPTIVE = 3,
+  CA_XF_RANDOM = 4
 } ca_transform;
 
 /* Layout of Q, K, V and the final output: BHND = [B][H][N][d],

@@ -18,12 +18,13 @@ import torch
 
 from . import _lib
 from ._lib import (CA_BF16, CA_F32, CA_LAYOUT_BHND, CA_LAYOUT_BNHD, CA_XF_ADAPTIVE, CA_XF_METRIC,
-                   CA_XF_NONE, CA_XF_PCA, CAError)
+                   CA_XF_NONE, CA_XF_PCA, CA_XF_RANDOM, CAError)
 
 __all__ = ["Problem", "workspace_size", "cluster", "select", "select_hist", "block_sparse_attn",
            "compensate", "forward", "CAError", "abi_version"]
 
-_XF = {"none": CA_XF_NONE, "pca": CA_XF_PCA, "metric": CA_XF_METRIC, "adaptive": CA_XF_ADAPTIVE}
+_XF = {"none": CA_XF_NONE, "pca": CA_XF_PCA, "metric": CA_XF_METRIC, "adaptive": CA_XF_ADAPTIVE,
+       "random": CA_XF_RANDOM}
 _LAYOUT = {"bhnd": CA_LAYOUT_BHND, "bnhd": CA_LAYOUT_BNHD}
 _DT = {torch.float32: CA_F32, torch.bfloat16: CA_BF16}
 

@@ -9,7 +9,7 @@ LIB_PATH = os.path.join(_HERE, "libclusterattn.so")
 
 CA_OK, CA_E_INVALID, CA_E_UNSUPPORTED, CA_E_WORKSPACE, CA_E_DEVICE = range(5)
 CA_F32, CA_BF16 = 0, 1
-CA_XF_NONE, CA_XF_PCA, CA_XF_METRIC, CA_XF_ADAPTIVE = 0, 1, 2, 3
+CA_XF_NONE, CA_XF_PCA, CA_XF_METRIC, CA_XF_ADAPTIVE, CA_XF_RANDOM = 0, 1, 2, 3, 4
 CA_LAYOUT_BHND, CA_LAYOUT_BNHD = 0, 1
 
 EXPORTS = (

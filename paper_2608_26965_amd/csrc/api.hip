@@ -44,7 +44,7 @@ int check_problem(const ca_problem* p, ca::Prob* P) {
   if (!pow2(p->cq) || !pow2(p->ck) || p->cq > ca::kMaxC || p->ck > ca::kMaxC)
     return fail(CA_E_INVALID, "cluster sizes must be powers of two in [1, %d]", ca::kMaxC);
   if (p->dtype != CA_F32 && p->dtype != CA_BF16) return fail(CA_E_INVALID, "unknown dtype");
-  if (p->transform < CA_XF_NONE || p->transform > CA_XF_ADAPTIVE)
+  if (p->transform < CA_XF_NONE || p->transform > CA_XF_RANDOM)
     return fail(CA_E_INVALID, "unknown transform");
   if (p->layout != CA_LAYOUT_BHND && p->layout != CA_LAYOUT_BNHD)
     return fail(CA_E_INVALID, "unknown layout");

@@ -792,6 +792,18 @@ __global__ __launch_bounds__(256) void qnorm_finish_kernel(Ctx C) {
 
 constexpr int kProjRows = 256;
 
+// Pseudo-random split coordinate in [0, 1) of the random-cluster control:
+// output number c (counting from 0) of splitmix64 (S. Vigna's generator,
+// started at state 0), top 24 bits, so the value is exact in fp32.
+__device__ __forceinline__ float random_coord(int bh, int side, int i, int j) {
+  const uint64_t c = ((((uint64_t)bh * 2 + (uint64_t)side) << 22 | (uint64_t)i) << 7) | (uint64_t)j;
+  uint64_t z = (c + 1ull) * 0x9e3779b97f4a7c15ull;
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+  z ^= z >> 31;
+  return (float)(uint32_t)(z >> 40) * 0x1p-24f;
+}
+
 __global__ __launch_bounds__(256) void project_kernel(Ctx C) {
   extern __shared__ float psh[];
   float* T = psh;                                        // [d][kDP]
@@ -806,6 +818,13 @@ __global__ __launch_bounds__(256) void project_kernel(Ctx C) {
     for (int e = threadIdx.x; e < (r1 - r0) * d; e += 256) {
       const int r = r0 + e / d, t = e % d;
       Y[(size_t)r * d + t] = load_x(S.x, bh, r, S.n, C.H, d, t, C.dtype, C.layout);
+    }
+    return;
+  }
+  if (C.xf == CA_XF_RANDOM) {
+    for (int e = threadIdx.x; e < (r1 - r0) * d; e += 256) {
+      const int r = r0 + e / d, t = e % d;
+      Y[(size_t)r * d + t] = random_coord(bh, side, r, t);
     }
     return;
   }
@@ -2151,7 +2170,8 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
   } while (0)
 
   const bool mfma = P.dtype == CA_BF16 && (d == 64 || d == 128);
-  if (P.xf != CA_XF_NONE) {
+  const bool transformed = P.xf != CA_XF_NONE && P.xf != CA_XF_RANDOM;
+  if (transformed) {
     if (mfma && d == 64)
       hipLaunchKernelGGL(moments_mfma_kernel<64>, dim3(C.nblk, 2 * BH), dim3(256), 0, st, C);
     else if (mfma)
@@ -2208,9 +2228,9 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
     const int nmax = C.nmax;
     const size_t plds = kProjLds;
     const dim3 pgrid((nmax + kProjRows - 1) / kProjRows, 2 * BH);
-    if (mfma && P.xf != CA_XF_NONE && d == 64)
+    if (mfma && transformed && d == 64)
       hipLaunchKernelGGL(project_mfma_kernel<64>, pgrid, dim3(256), 0, st, C);
-    else if (mfma && P.xf != CA_XF_NONE)
+    else if (mfma && transformed)
       hipLaunchKernelGGL(project_mfma_kernel<128>, pgrid, dim3(256), 0, st, C);
     else
       hipLaunchKernelGGL(project_kernel, pgrid, dim3(256), plds, st, C);

@@ -38,7 +38,7 @@ def _prob(**kw):
 
 @pytest.mark.parametrize("kw,status", [
     (dict(cq=48), 1), (dict(ck=512), 1), (dict(d=0), 1), (dict(d=129), 1), (dict(nq=0), 1),
-    (dict(dtype=7), 1), (dict(transform=4), 1), (dict(layout=2), 1), (dict(heads=0), 1),
+    (dict(dtype=7), 1), (dict(transform=5), 1), (dict(layout=2), 1), (dict(heads=0), 1),
 ])
 def test_invalid_problem(kw, status):
     L, lib = _lib()

@@ -39,6 +39,9 @@ SPLIT_CASES = [
     ("bf16", 20000, 64, 128, "adaptive"),
     ("bf16", 6000, 128, 64, "adaptive"),
     ("f32", 1500, 48, 32, "adaptive"),
+    # the random-cluster control
+    ("bf16", 20000, 64, 128, "random"),
+    ("f32", 3000, 32, 64, "random"),
 ]
 
 
@@ -78,6 +81,9 @@ def test_cluster_parity(dt, n, d, c, xf):
         yk = r["yk"][h].numpy().astype(np.float64)
         if xf == "none":
             assert np.array_equal(yq, Q[h]) and np.array_equal(yk, K[h])
+        if xf == "random":  # the generator is exact on both sides
+            assert np.array_equal(yq, ref.random_split_space(n, d, h, 0))
+            assert np.array_equal(yk, ref.random_split_space(n, d, h, 1))
         pq, cidq, cntq = ref.split(yq, c)
         pk, cidk, cntk = ref.split(yk, c)
         assert np.array_equal(r["perm_q"][h].numpy(), pq), "query permutation"
@@ -94,7 +100,7 @@ def test_cluster_parity(dt, n, d, c, xf):
         assert np.array_equal(r["vp"][h].float().numpy(), tiles.astype(np.float32))
         wantv = ref.centroids(V[h], pk, cntk)
         assert np.abs(r["cent_v"][h].numpy() - wantv).max() <= 1e-5 * max(1, np.abs(wantv).max())
-        if xf != "none":
+        if xf not in ("none", "random"):
             _check_split_space(Q[h], K[h], yq, yk, xf)
 
 
