@@ -134,6 +134,90 @@ def time_selection_modes(ca, torch, p, q, k, v, keep_k, out, args):
     return res
 
 
+SWEEP_N = (8192, 16384, 32768, 65536, 131072, 262144, 524288, 1048576)
+
+
+def latency_sweep(args):
+    """Latency scaling with the number of tokens (the paper's latency-scaling
+    experiment): 8 heads, d = 64, bf16, c = 128, metric transform, exact top-k,
+    compensation on; k fixed to 64 clusters (8192 keys) or set to 10% of the
+    key clusters. Inputs: the tabular recipe (per head 64 mixture centres
+    N(0, I), Dirichlet(1) weights, queries and keys drawn from the mixture
+    with sigma 0.5 and independent labels, values N(0, 1)), drawn on the GPU
+    with torch's generator seeded by N (the host generator would take minutes
+    at a million tokens), rounded to bf16. Per call ms: HIP events, mean over
+    the timed steps after the warm-up."""
+    import torch
+    import paper_2608_26965_amd as ca
+    H, d, c = 8, 64, 128
+    dev = torch.device("cuda:0")
+    steps, warmup = max(2, min(args.steps, 5)), max(1, min(args.warmup, 2))
+
+    def mixture(n, g):
+        mu = torch.randn(H, 64, d, device=dev, generator=g)
+        w = -torch.log(torch.rand(H, 64, device=dev, generator=g))  # Dirichlet(1) via Exp(1)
+        w = w / w.sum(dim=1, keepdim=True)
+        xs = []
+        for _ in range(2):  # queries, keys: independent labels, shared centres
+            lab = torch.multinomial(w, n, replacement=True, generator=g)
+            x = torch.gather(mu, 1, lab[..., None].expand(H, n, d))
+            xs.append((x + 0.5 * torch.randn(H, n, d, device=dev, generator=g))
+                      .to(torch.bfloat16)[None].contiguous())
+        v = torch.randn(H, n, d, device=dev, generator=g).to(torch.bfloat16)[None].contiguous()
+        return xs[0], xs[1], v
+
+    for n in SWEEP_N:
+        g = torch.Generator(device=dev)
+        g.manual_seed(n)
+        q, k, v = mixture(n, g)
+        p = ca.Problem(1, H, n, n, d, c, c, torch.bfloat16, "metric", "bhnd")
+        out = torch.empty(p.shape(n), dtype=torch.bfloat16, device=dev)
+        for rule in ("k64", "keep10pct"):
+            keep_k = min(64, p.nkc) if rule == "k64" else ca.keep_to_k(0.1, p.nkc)
+            ws = ca.workspace(p, dev, keep_k)
+
+            def step(ev=None):
+                if ev:
+                    ev[0].record()
+                r = ca.cluster(p, q, k, v, ws=ws)
+                if ev:
+                    ev[1].record()
+                lists, _ = ca.select(p, r["cent_q"], r["cent_k"], keep_k, ws=ws)
+                if ev:
+                    ev[2].record()
+                op, lse = ca.block_sparse_attn(p, r["qp"], r["kp"], r["vp"], r["count_k"], lists,
+                                               keep_k)
+                if ev:
+                    ev[3].record()
+                ca.compensate(p, r["qp"], r["cent_k"], r["cent_v"], r["count_k"], lists, keep_k,
+                              op, lse, r["perm_q"], out=out, ws=ws)
+                if ev:
+                    ev[4].record()
+
+            for _ in range(warmup):
+                step()
+            evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for i in range(steps):
+                step(evs[i])
+            torch.cuda.synchronize()
+            ms = (time.perf_counter() - t0) * 1e3 / steps
+            calls = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(4)]
+                              for e in evs]).mean(0)
+            f_dense = 4.0 * H * n * n * d
+            print(json.dumps({"sweep": "latency_scaling", "n": n, "rule": rule, "kept_clusters":
+                              keep_k, "key_clusters": p.nkc, "ms_per_layer": round(ms, 4),
+                              "cluster_ms": round(calls[0], 4), "select_ms": round(calls[1], 4),
+                              "attention_ms": round(calls[2], 4),
+                              "compensation_ms": round(calls[3], 4),
+                              "dense_equiv_tflops": round(f_dense / (ms * 1e-3) / 1e12, 1)}),
+                  flush=True)
+            del ws
+        del q, k, v, out
+        torch.cuda.empty_cache()
+
+
 def copy_calibration():
     """A plain device copy of 256 MiB (fp32), three launches."""
     import torch
@@ -152,6 +236,9 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep", action="store_true",
+                    help="latency scaling with the token count instead of the headline run: one "
+                         "JSON line per (N, rule), k = 64 clusters or 10%% of the key clusters")
     ap.add_argument("--no-modes", action="store_true",
                     help="skip the histogram-selection modes timed after the headline run")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -160,6 +247,9 @@ def main():
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.sweep:
+        latency_sweep(args)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: ClusterAttention's heads are independent, so a "
