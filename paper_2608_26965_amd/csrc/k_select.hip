@@ -80,27 +80,104 @@ __device__ __forceinline__ int block_scan_256(int x, int* sh_warp, int* total) {
   return base + v - x;
 }
 
-// One row (head, query cluster) per block: exact top-k of S[row][0..nkc).
-__global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ S, int nkc, int k,
-                                                   int32_t* __restrict__ lists) {
-  __shared__ int hist[256];
-  __shared__ int sh_warp[4];
-  __shared__ uint32_t sh_prefix;
-  __shared__ int sh_rank;
-  const size_t row = blockIdx.x;
-  const float* s = S + row * nkc;
-  const int tid = threadIdx.x;
+__device__ __forceinline__ float block_min_max(float v, bool want_max, float* sh) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float y = __shfl_xor(v, o, 64);
+    v = want_max ? fmaxf(v, y) : fminf(v, y);
+  }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (lane == 0) sh[w] = v;
+  __syncthreads();
+  float r = sh[0];
+#pragma unroll
+  for (int i = 1; i < 4; ++i) r = want_max ? fmaxf(r, sh[i]) : fminf(r, sh[i]);
+  __syncthreads();
+  return r;
+}
 
-  // Radix select of the k-th smallest key (rank k-1), most significant digit first.
+constexpr int kTopBins = 2048;   // linear bins of the top-k pre-pass
+constexpr int kTopStage = 8192;  // rows up to this length are staged in LDS
+
+// One row (head, query cluster) per block: exact top-k of S[row][0..nkc).
+// A pre-pass counts the row into linear bins over [min, max] (descending
+// score; the map is monotone, so the k-th largest lies in one bin and every
+// key of a lower bin precedes it); the radix select then only counts that
+// bin's keys, which keeps the LDS atomics of long rows from piling onto the
+// few digits a narrow score range has in common.
+// Rows of at most kTopStage scores are first copied to LDS (dynamic shared
+// memory of nkc floats), so the passes below read the row once from memory.
+__global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ S, int nkc, int k,
+                                                   int32_t* __restrict__ lists, int staged) {
+  __shared__ int hist[256];
+  __shared__ int bins[kTopBins];
+  __shared__ int sh_warp[4];
+  __shared__ float sh_f[4];
+  __shared__ uint32_t sh_prefix;
+  __shared__ int sh_rank, sh_bin;
+  extern __shared__ float srow[];
+  const size_t row = blockIdx.x;
+  const int tid = threadIdx.x;
+  const float* s = S + row * nkc;
+  if (staged) {
+    for (int b = tid; b < nkc; b += 256) srow[b] = s[b];
+    __syncthreads();
+    s = srow;
+  }
+
+  float lo = INFINITY, hi = -INFINITY;
+  for (int b = tid; b < nkc; b += 256) {
+    lo = fminf(lo, s[b]);
+    hi = fmaxf(hi, s[b]);
+  }
+  lo = block_min_max(lo, false, sh_f);
+  hi = block_min_max(hi, true, sh_f);
+  const float inv = hi > lo ? (float)kTopBins / (hi - lo) : 0.f;
+  auto bin_of = [&](float v) {
+    const float t = (hi - v) * inv;  // 0 for the largest score
+    return t < (float)kTopBins ? (t > 0.f ? (int)t : 0) : kTopBins - 1;
+  };
+  for (int i = tid; i < kTopBins; i += 256) bins[i] = 0;
+  __syncthreads();
+  for (int b = tid; b < nkc; b += 256) atomicAdd(&bins[bin_of(s[b])], 1);
+  __syncthreads();
+  {
+    constexpr int PB = kTopBins / 256;
+    int c[PB], sum = 0;
+#pragma unroll
+    for (int i = 0; i < PB; ++i) {
+      c[i] = bins[PB * tid + i];
+      sum += c[i];
+    }
+    int tot;
+    int before = block_scan_256(sum, sh_warp, &tot);
+    if (k - 1 >= before && k - 1 < before + sum) {
+#pragma unroll
+      for (int i = 0; i < PB; ++i) {
+        if (k - 1 < before + c[i]) {
+          sh_bin = PB * tid + i;
+          sh_rank = k - 1 - before;
+          break;
+        }
+        before += c[i];
+      }
+    }
+    __syncthreads();
+  }
+  const int B = sh_bin;
+
+  // Radix select of the wanted key inside bin B, most significant digit first.
   uint32_t prefix = 0;
-  int rank = k - 1;
+  int rank = sh_rank;
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
     const uint32_t hmask = pass == 0 ? 0u : (0xFFFFFFFFu << (shift + 8));
     hist[tid] = 0;
     __syncthreads();
     for (int b = tid; b < nkc; b += 256) {
-      const uint32_t u = desc_key(s[b]);
+      const float v = s[b];
+      if (bin_of(v) != B) continue;
+      const uint32_t u = desc_key(v);
       if ((u & hmask) == prefix) atomicAdd(&hist[(u >> shift) & 255], 1);
     }
     __syncthreads();
@@ -140,13 +217,13 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ S, 
   const uint32_t thr = prefix;
   const int need_eq = rank + 1;
   const int per = (nkc + 255) / 256;
-  const int lo = min(nkc, tid * per), hi = min(nkc, lo + per);
+  const int b_lo = min(nkc, tid * per), b_hi = min(nkc, b_lo + per);
   int eq = 0;
-  for (int b = lo; b < hi; ++b) eq += desc_key(s[b]) == thr;
+  for (int b = b_lo; b < b_hi; ++b) eq += desc_key(s[b]) == thr;
   int tot;
   const int eq_before = block_scan_256(eq, sh_warp, &tot);
   int sel = 0, er = eq_before;
-  for (int b = lo; b < hi; ++b) {
+  for (int b = b_lo; b < b_hi; ++b) {
     const uint32_t u = desc_key(s[b]);
     if (u < thr) {
       ++sel;
@@ -159,7 +236,7 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ S, 
   int32_t* out = lists + row * k;
   int pos = sel_before;
   er = eq_before;
-  for (int b = lo; b < hi; ++b) {
+  for (int b = b_lo; b < b_hi; ++b) {
     const uint32_t u = desc_key(s[b]);
     bool take = false;
     if (u < thr) {
@@ -184,22 +261,6 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ S, 
 
 constexpr int kHistBins = 128;
 constexpr int kHistGrid = kHistBins * kHistBins;
-
-__device__ __forceinline__ float block_min_max(float v, bool want_max, float* sh) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float y = __shfl_xor(v, o, 64);
-    v = want_max ? fmaxf(v, y) : fminf(v, y);
-  }
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  if (lane == 0) sh[w] = v;
-  __syncthreads();
-  float r = sh[0];
-#pragma unroll
-  for (int i = 1; i < 4; ++i) r = want_max ? fmaxf(r, sh[i]) : fminf(r, sh[i]);
-  __syncthreads();
-  return r;
-}
 
 __device__ __forceinline__ unsigned long long block_sum_u64(unsigned long long v,
                                                             unsigned long long* sh) {
@@ -376,8 +437,9 @@ hipError_t launch_select(const Prob& P, const float* cq, const float* ck, const 
                                   hipMemcpyDeviceToDevice, st);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(topk_kernel, dim3((unsigned)((size_t)P.BH * P.nqc)), dim3(256), 0, st, S,
-                     P.nkc, k, lists);
+  const int staged = P.nkc <= kTopStage;
+  hipLaunchKernelGGL(topk_kernel, dim3((unsigned)((size_t)P.BH * P.nqc)), dim3(256),
+                     staged ? (size_t)P.nkc * sizeof(float) : 0, st, S, P.nkc, k, lists, staged);
   return hipGetLastError();
 }
 

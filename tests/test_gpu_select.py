@@ -9,7 +9,8 @@ pytestmark = pytest.mark.gpu
 
 
 @pytest.mark.parametrize("nqc,nkc,d,k", [(16, 16, 64, 4), (50, 130, 64, 13), (33, 300, 128, 300),
-                                         (7, 1000, 32, 1), (200, 77, 64, 76)])
+                                         (7, 1000, 32, 1), (200, 77, 64, 76), (4, 8192, 64, 64),
+                                         (3, 5000, 64, 820)])
 def test_scores_and_topk(nqc, nkc, d, k):
     import torch
     import paper_2608_26965_amd as ca
@@ -41,6 +42,8 @@ def test_topk_with_ties_given_scores(k):
     H, nqc, nkc = 3, 20, 40
     S = rng.integers(-3, 4, size=(H, nqc, nkc)).astype(np.float32)
     S[S == 0] = np.where(rng.random((S == 0).sum()) < 0.5, -0.0, 0.0)
+    S[1, 2] = 0.5  # a row of equal scores
+    S[2, 3] = np.linspace(1.0, 1.0 + 1e-5, nkc, dtype=np.float32)  # a very narrow range
     p = ca.Problem(1, H, nqc * 16, nkc * 16, 8, 16, 16, torch.float32)
     lists, _ = ca.select(p, None, None, k, scores_in=G.dev(S))
     torch.cuda.synchronize()
