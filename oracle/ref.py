@@ -130,6 +130,8 @@ def key_split_space(Q, K, mode, head=0):
               principal axes of K S_q are the eigenvectors of S_q^T C_K S_q.
     adaptive: as metric (the key side does not depend on the selection mode).
     random:   pseudo-random coordinates (random_split_space, side 1).
+    metric_root: K S_q without the principal axes (basic splitting finds its
+              own directions: "the metric injected", no eigendecomposition).
     """
     Q, K = np.asarray(Q, F64), np.asarray(K, F64)
     if mode == "none":
@@ -138,6 +140,8 @@ def key_split_space(Q, K, mode, head=0):
         return random_split_space(K.shape[0], K.shape[1], head, 1)
     if mode == "pca":
         return K @ pca_basis(K)
+    if mode == "metric_root":
+        return K @ psd_root(second_moment(Q))
     if mode in ("metric", "adaptive"):
         S_q = psd_root(second_moment(Q))
         Z = K @ S_q
@@ -183,6 +187,8 @@ def query_split_space(Q, K, mode, head=0):
     if mode == "metric":
         R = query_representation(Q, K)
         return R @ pca_basis(R)
+    if mode == "metric_root":
+        return query_representation(Q, K)
     if mode == "adaptive":
         R = query_representation_adaptive(Q, K)
         return R @ pca_basis(R)
@@ -274,6 +280,145 @@ def split(Y, c, trace=None):
         rec(right)
 
     rec(np.arange(n, dtype=np.int64))
+    perm = np.concatenate(leaves)
+    counts = np.array([len(x) for x in leaves], dtype=np.int64)
+    cid = np.empty(n, dtype=np.int64)
+    for a, x in enumerate(leaves):
+        cid[x] = a
+    return perm, cid, counts
+
+
+# ---------------------------------------------------------------------------
+# Basic recursive splitting (Method: recursive splitting, basic: a PDDP
+# variant with power iteration)
+# ---------------------------------------------------------------------------
+
+BASIC_POWER_ITERS = 8
+
+
+def irwin_hall_normal(counters):
+    """Approximately standard normal values, one per counter: the sum of 12
+    uniforms on [0, 1) minus 6 (the Irwin-Hall approximation of N(0, 1)),
+    uniform u of counter c being the top 24 bits of splitmix64 output
+    16 c + u. The 24-bit integers are summed exactly, scaled in fp64 and
+    rounded once to fp32, so the values are reproducible bit for bit."""
+    c = np.asarray(counters, dtype=np.uint64)[..., None] * np.uint64(16) + \
+        np.arange(12, dtype=np.uint64)
+    u = (splitmix64(c) >> np.uint64(40)).astype(np.int64).sum(axis=-1)
+    return (u.astype(F64) * 2.0 ** -24 - 6.0).astype(np.float32)
+
+
+def basic_noise(d, head, side, level, node):
+    """Warm-start noise of the split at slot `node` of tree level `level`
+    (the slot numbering of the split tree: a node's children are 2 node and
+    2 node + 1 one level down): irwin_hall_normal at counters
+    ((((2 head + side) << 5 | level) << 20 | node) << 7) | k, k < d."""
+    base = ((((np.uint64(2 * head + side) << np.uint64(5)) | np.uint64(level))
+             << np.uint64(20) | np.uint64(node)) << np.uint64(7))
+    return irwin_hall_normal(base | np.arange(d, dtype=np.uint64))
+
+
+def f32_dot_rows(X, v):
+    """X v row by row in fp32, summed over the coordinates in order (a
+    rounded product and a rounded sum per step, no fused multiply-add)."""
+    X = np.asarray(X, np.float32)
+    v = np.asarray(v, np.float32)
+    acc = np.zeros(X.shape[0], np.float32)
+    for k in range(X.shape[1]):
+        acc = (acc + X[:, k] * v[k]).astype(np.float32)
+    return acc
+
+
+def power_direction(sub, v0, iters=BASIC_POWER_ITERS):
+    """First principal direction of the subsample rows (m x d) by power
+    iteration on their centred covariance, started at v0 (Method: basic
+    recursive splitting: the first principal component of the subset is
+    estimated with power iteration). fp32 in a fixed order: the mean (rows
+    summed in order, divided by m), centred rows, then per iteration
+    t_j = (x_j - mu) . v (f32_dot_rows), w = sum_j t_j (x_j - mu) (rows in
+    order), v = w / sqrt(|w|^2) (|w|^2 summed in order; a zero w keeps v).
+    The 1/m of the covariance cancels in the normalisation. Reading: the
+    paper does not give the number of iterations; BASIC_POWER_ITERS."""
+    sub = np.asarray(sub, np.float32)
+    m, d = sub.shape
+    mu = np.zeros(d, np.float32)
+    for j in range(m):
+        mu = (mu + sub[j]).astype(np.float32)
+    mu = (mu / np.float32(m)).astype(np.float32)
+    D = (sub - mu).astype(np.float32)
+    v = np.asarray(v0, np.float32).copy()
+    for _ in range(iters):
+        t = f32_dot_rows(D, v)
+        w = np.zeros(d, np.float32)
+        for j in range(m):
+            w = (w + t[j] * D[j]).astype(np.float32)
+        nn = np.float32(0.0)
+        for k in range(d):
+            nn = np.float32(nn + np.float32(w[k] * w[k]))
+        if nn > 0:
+            v = (w / np.sqrt(nn)).astype(np.float32)
+    return v
+
+
+def warm_start(v_parent, noise):
+    """Start of a node's power iteration (Method: basic recursive splitting):
+    the mean of the parent's estimate and a random normal vector rescaled to
+    the parent estimate's norm, in fp32: v0 = (v_p + r * (|v_p| / |r|)) / 2
+    (squared norms summed in order). The root starts from the noise alone."""
+    if v_parent is None:
+        return np.asarray(noise, np.float32)
+    vp = np.asarray(v_parent, np.float32)
+    r = np.asarray(noise, np.float32)
+    nv = np.float32(0.0)
+    nr = np.float32(0.0)
+    for k in range(len(vp)):
+        nv = np.float32(nv + np.float32(vp[k] * vp[k]))
+        nr = np.float32(nr + np.float32(r[k] * r[k]))
+    sc = np.float32(np.sqrt(nv) / np.sqrt(nr))
+    return ((vp + (r * sc).astype(np.float32)).astype(np.float32) * np.float32(0.5)).astype(
+        np.float32)
+
+
+def basic_split(Y, c, head=0, side=0, iters=BASIC_POWER_ITERS, trace=None):
+    """Basic recursive splitting of the rows of Y into clusters of size c
+    (Method: recursive splitting, basic; a variation of principal direction
+    divisive partitioning). A node of s <= c points is a leaf. Otherwise:
+
+      1. subsample m = min(d, s) members at ``subsample_positions``;
+      2. v = ``power_direction`` of the subsample from ``warm_start`` (the
+         parent's direction and ``basic_noise`` of this node);
+      3. project every member on v (``f32_dot_rows``) and send the
+         ``left_size(s, c)`` smallest (projection, original index) pairs left
+         (-0.0 counts as +0.0), the rest right, both in ascending index order;
+      4. recurse on the children, passing v down.
+
+    Y is used in fp32 (the split coordinates the GPU works on). Returns
+    (perm, cid, counts) as ``split``; ``trace`` collects (members, v, left,
+    right) per split."""
+    Y32 = np.asarray(Y, np.float32)
+    n, d = Y32.shape
+    leaves = []
+
+    def rec(members, level, node, v_parent):
+        s = len(members)
+        if s <= c:
+            leaves.append(members)
+            return
+        m = min(d, s)
+        sub = Y32[members[subsample_positions(s, m)]]
+        v0 = warm_start(v_parent, basic_noise(d, head, side, level, node))
+        v = power_direction(sub, v0, iters)
+        keys = f32_dot_rows(Y32[members], v).astype(F64) + 0.0
+        mL = left_size(s, c)
+        order = np.argsort(keys, kind="stable")
+        left = np.sort(members[order[:mL]])
+        right = np.sort(members[order[mL:]])
+        if trace is not None:
+            trace.append((members, v, left, right))
+        rec(left, level + 1, 2 * node, v)
+        rec(right, level + 1, 2 * node + 1, v)
+
+    rec(np.arange(n, dtype=np.int64), 0, 0, None)
     perm = np.concatenate(leaves)
     counts = np.array([len(x) for x in leaves], dtype=np.int64)
     cid = np.empty(n, dtype=np.int64)
