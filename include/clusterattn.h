@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define CA_ABI_VERSION 3
+#define CA_ABI_VERSION 4
 
 #if defined(__GNUC__) || defined(__clang__)
 #define CA_API __attribute__((visibility("default")))
@@ -101,6 +101,33 @@ typedef enum {
   CA_XF_RANDOM = 4
 } ca_transform;
 
+/* Recursive split algorithm (Method: Recursive splitting).
+ *   CA_SPLIT_DIAG:  diagonalized splitting (the evaluated method): at each node
+ *                   the global principal coordinate of highest variance on a
+ *                   subsample (see ca_cluster).
+ *   CA_SPLIT_BASIC: basic splitting, a variation of principal direction
+ *                   divisive partitioning: at each node the first principal
+ *                   direction of the subsample's centred covariance by 8
+ *                   power iterations, warm-started from the mean of the
+ *                   parent's direction and random normal noise rescaled to its
+ *                   norm; every member is projected on it and the split is
+ *                   made on the projections. Supported with CA_XF_NONE and
+ *                   CA_XF_METRIC (the metric root space without principal
+ *                   axes: keys k S_q, queries q S_k / |q S_k|, no
+ *                   eigendecomposition). Arithmetic (fp32, fixed order, no
+ *                   fused multiply-add): mean mu = (sum of the m subsample
+ *                   rows in order) / m; rows centred; per iteration t_j =
+ *                   sum_k (x_jk - mu_k) v_k, w_k = sum_j t_j (x_jk - mu_k),
+ *                   v = w / sqrt(sum_k w_k^2) (a zero w keeps v); start v0 =
+ *                   noise at the root, else (v_p + r sqrt(|v_p|^2) /
+ *                   sqrt(|r|^2)) / 2; projections sum_k y_ik v_k. Noise of
+ *                   the node at slot s of level l of head bh, side (0 queries,
+ *                   1 keys), coordinate k: (sum over u < 12 of the top 24 bits
+ *                   of splitmix64 output 16 c + u) / 2^24 - 6 (fp64, rounded
+ *                   once to fp32), c = ((((2 bh + side) << 5 | l) << 20 | s)
+ *                   << 7) | k. */
+typedef enum { CA_SPLIT_DIAG = 0, CA_SPLIT_BASIC = 1 } ca_split;
+
 /* Layout of Q, K, V and the final output: BHND = [B][H][N][d],
  * BNHD = [B][N][H][d] (the usual activation layout of a transformer). */
 typedef enum { CA_LAYOUT_BHND = 0, CA_LAYOUT_BNHD = 1 } ca_layout;
@@ -113,6 +140,7 @@ typedef struct {
   int32_t dtype;         /* ca_dtype of Q/K/V, permuted copies and output */
   int32_t transform;     /* ca_transform (ca_cluster only) */
   int32_t layout;        /* ca_layout of Q/K/V/out */
+  int32_t split;         /* ca_split (ca_cluster only) */
 } ca_problem;
 
 /* Outputs of ca_cluster. Required unless marked optional. */

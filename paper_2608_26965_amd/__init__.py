@@ -17,8 +17,8 @@ from dataclasses import dataclass
 import torch
 
 from . import _lib
-from ._lib import (CA_BF16, CA_F32, CA_LAYOUT_BHND, CA_LAYOUT_BNHD, CA_XF_ADAPTIVE, CA_XF_METRIC,
-                   CA_XF_NONE, CA_XF_PCA, CA_XF_RANDOM, CAError)
+from ._lib import (CA_BF16, CA_F32, CA_LAYOUT_BHND, CA_LAYOUT_BNHD, CA_SPLIT_BASIC, CA_SPLIT_DIAG,
+                   CA_XF_ADAPTIVE, CA_XF_METRIC, CA_XF_NONE, CA_XF_PCA, CA_XF_RANDOM, CAError)
 
 __all__ = ["Problem", "workspace_size", "cluster", "select", "select_hist", "block_sparse_attn",
            "compensate", "forward", "CAError", "abi_version"]
@@ -26,6 +26,7 @@ __all__ = ["Problem", "workspace_size", "cluster", "select", "select_hist", "blo
 _XF = {"none": CA_XF_NONE, "pca": CA_XF_PCA, "metric": CA_XF_METRIC, "adaptive": CA_XF_ADAPTIVE,
        "random": CA_XF_RANDOM}
 _LAYOUT = {"bhnd": CA_LAYOUT_BHND, "bnhd": CA_LAYOUT_BNHD}
+_SPLIT = {"diag": CA_SPLIT_DIAG, "basic": CA_SPLIT_BASIC}
 _DT = {torch.float32: CA_F32, torch.bfloat16: CA_BF16}
 
 
@@ -45,6 +46,7 @@ class Problem:
     dtype: torch.dtype = torch.bfloat16
     transform: str = "metric"
     layout: str = "bhnd"
+    split: str = "diag"
 
     @property
     def bh(self):
@@ -68,7 +70,8 @@ class Problem:
 
     def c(self) -> _lib.CaProblem:
         return _lib.CaProblem(self.batch, self.heads, self.nq, self.nk, self.d, self.cq, self.ck,
-                              _DT[self.dtype], _XF[self.transform], _LAYOUT[self.layout])
+                              _DT[self.dtype], _XF[self.transform], _LAYOUT[self.layout],
+                              _SPLIT[self.split])
 
     def shape(self, n):
         if self.layout == "bhnd":

@@ -11,6 +11,7 @@ CA_OK, CA_E_INVALID, CA_E_UNSUPPORTED, CA_E_WORKSPACE, CA_E_DEVICE = range(5)
 CA_F32, CA_BF16 = 0, 1
 CA_XF_NONE, CA_XF_PCA, CA_XF_METRIC, CA_XF_ADAPTIVE, CA_XF_RANDOM = 0, 1, 2, 3, 4
 CA_LAYOUT_BHND, CA_LAYOUT_BNHD = 0, 1
+CA_SPLIT_DIAG, CA_SPLIT_BASIC = 0, 1
 
 EXPORTS = (
     "ca_abi_version",
@@ -30,7 +31,7 @@ _vp = ctypes.c_void_p
 
 class CaProblem(ctypes.Structure):
     _fields_ = [(n, _i32) for n in ("batch", "heads", "nq", "nk", "d", "cq", "ck", "dtype",
-                                    "transform", "layout")]
+                                    "transform", "layout", "split")]
 
 
 class CaClusterOut(ctypes.Structure):

@@ -48,6 +48,10 @@ int check_problem(const ca_problem* p, ca::Prob* P) {
     return fail(CA_E_INVALID, "unknown transform");
   if (p->layout != CA_LAYOUT_BHND && p->layout != CA_LAYOUT_BNHD)
     return fail(CA_E_INVALID, "unknown layout");
+  if (p->split != CA_SPLIT_DIAG && p->split != CA_SPLIT_BASIC)
+    return fail(CA_E_INVALID, "unknown split");
+  if (p->split == CA_SPLIT_BASIC && p->transform != CA_XF_NONE && p->transform != CA_XF_METRIC)
+    return fail(CA_E_UNSUPPORTED, "basic splitting runs with CA_XF_NONE or CA_XF_METRIC");
   P->B = p->batch;
   P->H = p->heads;
   P->BH = p->batch * p->heads;
@@ -59,6 +63,7 @@ int check_problem(const ca_problem* p, ca::Prob* P) {
   P->dtype = p->dtype;
   P->xf = p->transform;
   P->layout = p->layout;
+  P->split = p->split;
   P->nqc = (p->nq + p->cq - 1) / p->cq;
   P->nkc = (p->nk + p->ck - 1) / p->ck;
   P->nq_pad = P->nqc * p->cq;
@@ -110,8 +115,10 @@ void plan_workspace(const Prob& P, Workspace* W) {
   W->nblk_mom = (nmax + kMomRows - 1) / kMomRows;
   W->levels_q = num_levels(P.nq, P.cq);
   W->levels_k = num_levels(P.nk, P.ck);
-  W->big_q = split_big_levels(P.nq, P.cq, W->levels_q);
-  W->big_k = split_big_levels(P.nk, P.ck, W->levels_k);
+  // Basic splitting runs every level with the multi-block kernels.
+  const bool basic = P.split == CA_SPLIT_BASIC;
+  W->big_q = basic ? W->levels_q : split_big_levels(P.nq, P.cq, W->levels_q);
+  W->big_k = basic ? W->levels_k : split_big_levels(P.nk, P.ck, W->levels_k);
   int bigmax = W->big_q > W->big_k ? W->big_q : W->big_k;
   W->max_big_nodes = bigmax > 0 ? (1 << (bigmax - 1)) : 1;
   W->hist_slots = split_hist_slots(P, W->big_q, W->big_k);
@@ -130,6 +137,7 @@ void plan_workspace(const Prob& P, Workspace* W) {
   W->node_state = take(2 * BH * W->max_big_nodes * kNodeInts * 4);
   W->hist = take(2 * BH * W->hist_slots * kBins * 4);
   W->chunk_cnt = take(2 * BH * W->hist_slots * 2 * 4);
+  W->dirs = take(basic ? 2 * 2 * BH * W->max_big_nodes * d * 4 : 0);
   W->scores = take(BH * P.nqc * P.nkc * 4);
   const size_t ntile = (P.nkc + kCompTile - 1) / kCompTile;
   W->comp_tiles = take(P.dtype == CA_BF16 ? BH * ntile * comp_tile_bytes(P.d) : 0);

@@ -46,7 +46,7 @@ __device__ __forceinline__ uint32_t ordered_bits(float f) {
 // ---- problem description ---------------------------------------------------
 
 struct Prob {
-  int B, H, BH, nq, nk, d, cq, ck, dtype, xf, layout;
+  int B, H, BH, nq, nk, d, cq, ck, dtype, xf, layout, split;
   int nqc, nkc, nq_pad, nk_pad;
   size_t esize;
 };
@@ -105,6 +105,7 @@ struct Workspace {
   size_t node_state;        // int32 [2][BH][max_big_nodes][kNodeInts]
   size_t hist;              // uint32 [2][BH][hist_slots][kBins] chunk histograms
   size_t chunk_cnt;         // int32 [2][BH][hist_slots][2] chunk prefixes (less, equal)
+  size_t dirs;              // fp32 [2 levels][2][BH][max_big_nodes][d] split directions (basic)
   // selection
   size_t scores;            // fp32 [BH][nqc][nkc]
   // compensation

@@ -61,6 +61,8 @@ struct Ctx {
   uint32_t* hist;
   int32_t* chunk_cnt;
   int max_nodes, hist_slots;
+  int split;        // ca_split
+  float* dirs;      // [2 levels][2][BH][max_nodes][d] split directions (basic splitting)
 };
 
 // Matrix slots
@@ -1315,6 +1317,179 @@ __global__ __launch_bounds__(64) void split_choose_kernel(Ctx C, LevelArgs L) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Basic splitting (Method: recursive splitting, basic; a variation of
+// principal direction divisive partitioning): the direction of each node at
+// one level, by power iteration on its strided subsample. Every reduction
+// runs in a fixed order with separately rounded products and sums (no fused
+// multiply-add), so the directions, and the splits made on them, are
+// reproducible bit for bit.
+// ---------------------------------------------------------------------------
+
+// Separately rounded fp32 operations: a product is never fused into the sum
+// that follows it, and the quotient and square root are the correctly rounded
+// ones (the default contraction would otherwise turn a + x * y into an FMA,
+// and the HIP __f*_rn intrinsics are plain operators here).
+__device__ __forceinline__ float add_rn(float a, float b) {
+#pragma clang fp contract(off)
+  return a + b;
+}
+__device__ __forceinline__ float sub_rn(float a, float b) {
+#pragma clang fp contract(off)
+  return a - b;
+}
+__device__ __forceinline__ float mul_rn(float a, float b) {
+#pragma clang fp contract(off)
+  return a * b;
+}
+__device__ __forceinline__ float div_rn(float a, float b) { return a / b; }
+__device__ __forceinline__ float sqrt_rn(float a) { return __builtin_sqrtf(a); }
+
+constexpr int kBasicThreads = 128;
+constexpr int kBasicIters = 8;
+
+__device__ __forceinline__ float* dir_ptr(const Ctx& C, int level, int pid, int node) {
+  return C.dirs + ((((size_t)(level & 1) * 2 * C.BH) + pid) * C.max_nodes + node) * C.d;
+}
+
+// Output number c (counting from 0) of splitmix64 started at state 0
+// (S. Vigna's generator).
+__device__ __forceinline__ uint64_t splitmix64_at(uint64_t c) {
+  uint64_t z = (c + 1ull) * 0x9e3779b97f4a7c15ull;
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+  return z ^ (z >> 31);
+}
+
+// Approximately standard normal: the sum of 12 uniforms minus 6 (Irwin-Hall),
+// uniform u the top 24 bits of output 16 c + u, summed as integers.
+__device__ __forceinline__ float irwin_hall(uint64_t c) {
+  long long sum = 0;
+#pragma unroll
+  for (int u = 0; u < 12; ++u) sum += (long long)(splitmix64_at(c * 16ull + (uint64_t)u) >> 40);
+  return (float)((double)sum * 0x1p-24 - 6.0);
+}
+
+// One block per node of the level. Dynamic LDS: the subsample, m x (d + 1).
+__global__ __launch_bounds__(kBasicThreads) void basic_choose_kernel(Ctx C, LevelArgs L) {
+  extern __shared__ float bsub[];
+  __shared__ float mu[kMaxD], v[kMaxD], t[kMaxD], w[kMaxD];
+  __shared__ float sh_nn, sh_sc, sh_mean, sh_var;
+  const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH, node = blockIdx.x;
+  const Side& S = C.s[side];
+  if (L.level >= S.big) return;
+  int start, size;
+  node_range(S.n, S.c, L.level, node, &start, &size);
+  int32_t* ns = node_ptr(C, pid, node);
+  const int tid = threadIdx.x, d = C.d, DP = d + 1;
+  if (size <= S.c) {
+    if (tid == 0) ns[0] = -1;
+    return;
+  }
+  const int m = d < size ? d : size;
+  const int32_t* idx = L.idx_in + (size_t)pid * C.nmax;
+  const float* Y = S.y + (size_t)bh * S.n * d;
+  for (int e = tid; e < m * d; e += kBasicThreads) {
+    const int j = e / d, k = e % d;
+    const int p = (int)(((long long)(2 * j + 1) * size) / (2 * m));
+    const int row = L.first ? start + p : idx[start + p];
+    bsub[j * DP + k] = Y[(size_t)row * d + k];
+  }
+  __syncthreads();
+  if (tid < d) {
+    float a = 0.f;
+    for (int j = 0; j < m; ++j) a = add_rn(a, bsub[j * DP + tid]);
+    mu[tid] = div_rn(a, (float)m);
+  }
+  __syncthreads();
+  for (int e = tid; e < m * d; e += kBasicThreads) {
+    const int j = e / d, k = e % d;
+    bsub[j * DP + k] = sub_rn(bsub[j * DP + k], mu[k]);
+  }
+  // warm start: noise of this node, the parent's direction one level up
+  if (tid < d) {
+    const uint64_t base = ((((uint64_t)(2 * bh + side) << 5 | (uint64_t)L.level) << 20 |
+                            (uint64_t)node) << 7);
+    t[tid] = irwin_hall(base | (uint64_t)tid);
+  }
+  __syncthreads();
+  const float* vp = L.level > 0 ? dir_ptr(C, L.level - 1, pid, node >> 1) : nullptr;
+  if (tid == 0 && vp) {
+    float nv = 0.f, nr = 0.f;
+    for (int k = 0; k < d; ++k) {
+      nv = add_rn(nv, mul_rn(vp[k], vp[k]));
+      nr = add_rn(nr, mul_rn(t[k], t[k]));
+    }
+    sh_sc = div_rn(sqrt_rn(nv), sqrt_rn(nr));
+  }
+  __syncthreads();
+  if (tid < d)
+    v[tid] = vp ? mul_rn(add_rn(vp[tid], mul_rn(t[tid], sh_sc)), 0.5f) : t[tid];
+  for (int it = 0; it < kBasicIters; ++it) {
+    __syncthreads();
+    if (tid < m) {
+      float a = 0.f;
+      for (int k = 0; k < d; ++k) a = add_rn(a, mul_rn(bsub[tid * DP + k], v[k]));
+      t[tid] = a;
+    }
+    __syncthreads();
+    if (tid < d) {
+      float a = 0.f;
+      for (int j = 0; j < m; ++j) a = add_rn(a, mul_rn(t[j], bsub[j * DP + tid]));
+      w[tid] = a;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      float nn = 0.f;
+      for (int k = 0; k < d; ++k) nn = add_rn(nn, mul_rn(w[k], w[k]));
+      sh_nn = nn;
+    }
+    __syncthreads();
+    if (tid < d && sh_nn > 0.f) v[tid] = div_rn(w[tid], sqrt_rn(sh_nn));
+  }
+  __syncthreads();
+  float* vo = dir_ptr(C, L.level, pid, node);
+  if (tid < d) vo[tid] = v[tid];
+  // spread of the subsample's projections, for the linear bins of the select
+  if (tid < m) {
+    float a = 0.f;
+    for (int k = 0; k < d; ++k) a = add_rn(a, mul_rn(bsub[tid * DP + k], v[k]));
+    t[tid] = a;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double mp = 0.0, vv = 0.0;
+    for (int k = 0; k < d; ++k) mp += (double)mu[k] * (double)v[k];
+    for (int j = 0; j < m; ++j) vv += (double)t[j] * (double)t[j];
+    const double sd = sqrt(vv / m);
+    float lo = (float)(mp - 4.0 * sd), scale = (float)((double)kBins / (8.0 * sd));
+    if (!(sd > 0.0) || !isfinite(lo) || !isfinite(scale)) {
+      lo = 0.f;
+      scale = 0.f;  // one bin: the select step falls back to streaming
+    }
+    const int mL = left_size(size, S.c);
+    ns[0] = 0;
+    ns[1] = 0;
+    ns[2] = 0;
+    ns[3] = mL;
+    ns[4] = start;
+    ns[5] = size;
+    ns[6] = __float_as_int(lo);
+    ns[7] = (size + kChunk - 1) / kChunk;
+    ns[8] = __float_as_int(scale);
+    ns[9] = mL - 1;
+  }
+}
+
+// T_K = F_q and T_Q = F_k (basic splitting in the metric root space).
+__global__ __launch_bounds__(256) void copy_roots_kernel(Ctx C) {
+  const int bh = blockIdx.x, dd = C.d * C.d;
+  for (int e = threadIdx.x; e < dd; e += 256) {
+    mat(C, bh, M_TK)[e] = mat(C, bh, M_E0)[e];
+    mat(C, bh, M_TQ)[e] = mat(C, bh, M_EK)[e];
+  }
+}
+
 // Block-wide exclusive scan (NT threads).
 template <int NT>
 __device__ __forceinline__ int block_scan(int x, int* wsum, int* total) {
@@ -1369,8 +1544,23 @@ __global__ __launch_bounds__(256) void split_keys_kernel(Ctx C, LevelArgs L) {
     rows[u] = o < c1 ? (L.first ? start + o : idx[start + o]) : 0;
   }
   uint32_t kv[kPer];
+  if (C.split == CA_SPLIT_BASIC) {
+    // projection on the node's direction, coordinates summed in order
+    __shared__ float dv[kMaxD];
+    const float* dir = dir_ptr(C, L.level, pid, node);
+    for (int k = threadIdx.x; k < C.d; k += 256) dv[k] = dir[k];
+    __syncthreads();
 #pragma unroll
-  for (int u = 0; u < kPer; ++u) kv[u] = ordered_bits(Y[(size_t)rows[u] * C.d + js]);
+    for (int u = 0; u < kPer; ++u) {
+      const float* yr = Y + (size_t)rows[u] * C.d;
+      float a = 0.f;
+      for (int k = 0; k < C.d; ++k) a = add_rn(a, mul_rn(yr[k], dv[k]));
+      kv[u] = ordered_bits(a);
+    }
+  } else {
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) kv[u] = ordered_bits(Y[(size_t)rows[u] * C.d + js]);
+  }
   __syncthreads();
 #pragma unroll
   for (int u = 0; u < kPer; ++u) {
@@ -2085,6 +2275,9 @@ hipError_t set_lds_limits() {
                         (int)kProjLds);
     (void)hipFuncSetAttribute((const void*)gather_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
                         (int)kGatherLds);
+    (void)hipFuncSetAttribute((const void*)basic_choose_kernel,
+                              hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)((size_t)kMaxD * (kMaxD + 1) * sizeof(float)));
     (void)hipFuncSetAttribute((const void*)gather_fast_kernel<bf16>,
                               hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     (void)hipFuncSetAttribute((const void*)gather_fast_kernel<float>,
@@ -2131,6 +2324,9 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
   C.chunk_cnt = (int32_t*)(ws + W.chunk_cnt);
   C.max_nodes = W.max_big_nodes;
   C.hist_slots = W.hist_slots;
+  C.split = P.split;
+  C.dirs = (float*)(ws + W.dirs);
+  const bool basic = P.split == CA_SPLIT_BASIC;
   Side& Sq = C.s[0];
   Side& Sk = C.s[1];
   Sq.x = q;
@@ -2218,7 +2414,9 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
       else
         J.j[1] = {M_C3, -1, V_MUR, 1, -1, -1, M_C3, V_L3, M_EK, M_TQ, wq};
     }
-    if (d <= 64)
+    if (basic)  // the metric root space: the Cholesky factors are the projections
+      hipLaunchKernelGGL(copy_roots_kernel, dim3(BH), dim3(256), 0, st, C);
+    else if (d <= 64)
       hipLaunchKernelGGL(eigh_kernel<64>, dim3(BH, 2), dim3(eigh_threads<64>()), eigh_lds_bytes(64), st, C, J);
     else
       hipLaunchKernelGGL(eigh_kernel<128>, dim3(BH, 2), dim3(eigh_threads<128>()), kEighLds, st, C, J);
@@ -2228,9 +2426,9 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
     const int nmax = C.nmax;
     const size_t plds = kProjLds;
     const dim3 pgrid((nmax + kProjRows - 1) / kProjRows, 2 * BH);
-    if (mfma && transformed && d == 64)
+    if (mfma && transformed && !basic && d == 64)
       hipLaunchKernelGGL(project_mfma_kernel<64>, pgrid, dim3(256), 0, st, C);
-    else if (mfma && transformed)
+    else if (mfma && transformed && !basic)
       hipLaunchKernelGGL(project_mfma_kernel<128>, pgrid, dim3(256), 0, st, C);
     else
       hipLaunchKernelGGL(project_kernel, pgrid, dim3(256), plds, st, C);
@@ -2245,7 +2443,11 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
     L.idx_out = (l & 1) ? C.idx0 : C.idx1;
     const int cpn = split_level_cpn(P, W.big_q, W.big_k, l);
     L.cpn = cpn;
-    hipLaunchKernelGGL(split_choose_kernel, dim3(1 << l, 2 * BH), dim3(64), 0, st, C, L);
+    if (basic)
+      hipLaunchKernelGGL(basic_choose_kernel, dim3(1 << l, 2 * BH), dim3(kBasicThreads),
+                         (size_t)d * (d + 1) * sizeof(float), st, C, L);
+    else
+      hipLaunchKernelGGL(split_choose_kernel, dim3(1 << l, 2 * BH), dim3(64), 0, st, C, L);
     CA_CHECK();
     hipLaunchKernelGGL(split_keys_kernel, dim3(cpn, 1 << l, 2 * BH), dim3(256), 0, st, C, L);
     CA_CHECK();

@@ -25,20 +25,21 @@ def test_header_symbols_exported():
     assert declared == set(L.EXPORTS)
     for name in declared:
         assert hasattr(lib, name)
-    assert lib.ca_abi_version() == 3
+    assert lib.ca_abi_version() == 4
 
 
 def _prob(**kw):
     from paper_2608_26965_amd import _lib as L
     base = dict(batch=1, heads=2, nq=1000, nk=1000, d=64, cq=64, ck=64, dtype=L.CA_BF16,
-                transform=L.CA_XF_METRIC, layout=L.CA_LAYOUT_BHND)
+                transform=L.CA_XF_METRIC, layout=L.CA_LAYOUT_BHND, split=L.CA_SPLIT_DIAG)
     base.update(kw)
     return L.CaProblem(**base)
 
 
 @pytest.mark.parametrize("kw,status", [
     (dict(cq=48), 1), (dict(ck=512), 1), (dict(d=0), 1), (dict(d=129), 1), (dict(nq=0), 1),
-    (dict(dtype=7), 1), (dict(transform=5), 1), (dict(layout=2), 1), (dict(heads=0), 1),
+    (dict(dtype=7), 1), (dict(transform=5), 1), (dict(split=2), 1),
+    (dict(split=1, transform=1), 2), (dict(split=1, transform=3), 2), (dict(layout=2), 1), (dict(heads=0), 1),
 ])
 def test_invalid_problem(kw, status):
     L, lib = _lib()

@@ -171,3 +171,56 @@ def test_single_cluster_and_tiny():
         for h in range(2):
             assert r["perm_q"][h].tolist() == list(range(n))
             assert r["count_k"][h].tolist() == [n]
+
+
+BASIC_CASES = [
+    # dtype, n, d, c, transform
+    ("f32", 3000, 16, 64, "none"),
+    ("bf16", 20000, 64, 128, "none"),
+    ("bf16", 20000, 64, 128, "metric"),
+    ("f32", 5000, 128, 64, "metric"),
+    ("bf16", 9000, 32, 16, "none"),
+    ("bf16", 700, 64, 64, "metric"),
+]
+
+
+@pytest.mark.parametrize("dt,n,d,c,xf", BASIC_CASES)
+def test_basic_split_parity(dt, n, d, c, xf):
+    """Basic recursive splitting (power iteration per node): permutations
+    bit-exact against the oracle's basic split of the exported split
+    coordinates (the directions, projections and noise are reproduced bit for
+    bit); permuted copies and centroids as for the diagonalized split; in the
+    metric root space the key distances are the query-induced metric's and
+    the query representations have unit norm."""
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    G.flush(f"basic split case dt={dt} n={n} d={d} c={c} xf={xf}")
+    heads = 2
+    Q, K, V = mixture_inputs(41, heads, n, d, dt, centres=12, sigma=0.5)
+    p = ca.Problem(1, heads, n, n, d, c, c, G.tdtype(dt), xf, "bhnd", split="basic")
+    tq, tk, tv = (G.dev(x[None], G.tdtype(dt)) for x in (Q, K, V))
+    r = ca.cluster(p, tq, tk, tv, export_y=True)
+    torch.cuda.synchronize()
+    r = {k: v.cpu() for k, v in r.items()}
+    for h in range(heads):
+        yq = r["yq"][h].numpy()
+        yk = r["yk"][h].numpy()
+        if xf == "none":
+            assert np.array_equal(yq, Q[h].astype(np.float32))
+        pq, cidq, _ = ref.basic_split(yq, c, head=h, side=0)
+        pk, cidk, _ = ref.basic_split(yk, c, head=h, side=1)
+        assert np.array_equal(r["perm_q"][h].numpy(), pq), "query permutation"
+        assert np.array_equal(r["perm_k"][h].numpy(), pk), "key permutation"
+        assert np.array_equal(r["cid_q"][h].numpy(), cidq)
+        _check_copies(Q[h], pq, r["count_q"][h], r["cent_q"][h], r["qp"][h], c, dt)
+        _check_copies(K[h], pk, r["count_k"][h], r["cent_k"][h], r["kp"][h], c, dt)
+        if xf == "metric":
+            yk64, yq64 = yk.astype(np.float64), yq.astype(np.float64)
+            rng = np.random.default_rng(h)
+            for a, b in rng.integers(0, n, size=(100, 2)):
+                want = ((Q[h] @ (K[h][a] - K[h][b])) ** 2).mean()
+                got = ((yk64[a] - yk64[b]) ** 2).sum()
+                assert abs(got - want) <= 2e-4 * ((yk64[a] ** 2).sum() + (yk64[b] ** 2).sum()) + 1e-9
+            nrm = np.sqrt((yq64 ** 2).sum(axis=1))
+            assert np.abs(nrm[nrm > 0] - 1.0).max() < 1e-4
