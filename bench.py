@@ -76,14 +76,19 @@ def time_selection_modes(ca, torch, p, q, k, v, keep_k, out, args):
     headline run: top-k through the two-pass histogram (at least keep_k
     clusters, metric transform), adaptive assignment (90% of the estimated
     attention mass, at least 16 clusters, adaptive transform) and the
-    random-cluster control (random clusters, exact top-k of keep_k). Per call
-    ms (HIP events, mean over the timed steps), ms per layer and the mean
-    number of selected key clusters per query cluster."""
+    random-cluster control (random clusters, exact top-k of keep_k) and basic
+    recursive splitting (power-iteration directions in the metric root space,
+    exact top-k of keep_k). Per call ms (HIP events, mean over the timed
+    steps), ms per layer and the mean number of selected key clusters per
+    query cluster."""
     res = {}
-    for name, xf, floor, recall in (("hist_topk", "metric", keep_k, 0.0),
-                                    ("adaptive_mass0.9_min16", "adaptive", 16, 0.9),
-                                    ("random_clusters_topk", "random", keep_k, None)):
-        pm = ca.Problem(p.batch, p.heads, p.nq, p.nk, p.d, p.cq, p.ck, p.dtype, xf, p.layout)
+    for name, xf, floor, recall, split in (
+            ("hist_topk", "metric", keep_k, 0.0, "diag"),
+            ("adaptive_mass0.9_min16", "adaptive", 16, 0.9, "diag"),
+            ("random_clusters_topk", "random", keep_k, None, "diag"),
+            ("basic_split_topk", "metric", keep_k, None, "basic")):
+        pm = ca.Problem(p.batch, p.heads, p.nq, p.nk, p.d, p.cq, p.ck, p.dtype, xf, p.layout,
+                        split=split)
         ws = ca.workspace(pm, q.device, keep_k)
         lens_seen = []
 
@@ -123,7 +128,7 @@ def time_selection_modes(ca, torch, p, q, k, v, keep_k, out, args):
         torch.cuda.synchronize()
         ms = (time.perf_counter() - t0) * 1e3 / steps
         calls = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(4)] for e in evs]).mean(0)
-        res[name] = {"transform": xf, "min_count": floor,
+        res[name] = {"transform": xf, "split": split, "min_count": floor,
                      "mass_recall": recall if recall is not None else "exact top-k",
                      "ms_per_step": round(ms, 4),
                      "breakdown_ms": {"cluster": round(calls[0], 4), "select": round(calls[1], 4),

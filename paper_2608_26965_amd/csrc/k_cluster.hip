@@ -1305,6 +1305,7 @@ __global__ __launch_bounds__(64) void split_choose_kernel(Ctx C, LevelArgs L) {
     }
     const int mL = left_size(size, S.c);
     ns[0] = js;
+    ns[10] = 0;
     ns[1] = 0;
     ns[2] = 0;
     ns[3] = mL;
@@ -1371,17 +1372,21 @@ __device__ __forceinline__ float irwin_hall(uint64_t c) {
 }
 
 // One block per node of the level. Dynamic LDS: the subsample, m x (d + 1).
+// D is the feature count when it is a compile-time constant (64, 128), so the
+// in-order chains unroll and their LDS reads are issued ahead; D = 0 reads d
+// from the problem. Norms are computed by every thread from the same LDS
+// values (identical results), which saves a barrier per iteration.
+template <int D>
 __global__ __launch_bounds__(kBasicThreads) void basic_choose_kernel(Ctx C, LevelArgs L) {
   extern __shared__ float bsub[];
   __shared__ float mu[kMaxD], v[kMaxD], t[kMaxD], w[kMaxD];
-  __shared__ float sh_nn, sh_sc, sh_mean, sh_var;
   const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH, node = blockIdx.x;
   const Side& S = C.s[side];
   if (L.level >= S.big) return;
   int start, size;
   node_range(S.n, S.c, L.level, node, &start, &size);
   int32_t* ns = node_ptr(C, pid, node);
-  const int tid = threadIdx.x, d = C.d, DP = d + 1;
+  const int tid = threadIdx.x, d = D ? D : C.d, DP = d + 1;
   if (size <= S.c) {
     if (tid == 0) ns[0] = -1;
     return;
@@ -1389,11 +1394,33 @@ __global__ __launch_bounds__(kBasicThreads) void basic_choose_kernel(Ctx C, Leve
   const int m = d < size ? d : size;
   const int32_t* idx = L.idx_in + (size_t)pid * C.nmax;
   const float* Y = S.y + (size_t)bh * S.n * d;
-  for (int e = tid; e < m * d; e += kBasicThreads) {
-    const int j = e / d, k = e % d;
-    const int p = (int)(((long long)(2 * j + 1) * size) / (2 * m));
-    const int row = L.first ? start + p : idx[start + p];
-    bsub[j * DP + k] = Y[(size_t)row * d + k];
+  if (D != 0 && D % 4 == 0) {
+    // float4 reads of the sample rows
+    const int d4 = d / 4;
+    for (int e = tid; e < m * d4; e += kBasicThreads) {
+      const int j = e / d4, k4 = e % d4;
+      const int p = (int)(((long long)(2 * j + 1) * size) / (2 * m));
+      const int row = L.first ? start + p : idx[start + p];
+      const float4 x = *(const float4*)(Y + (size_t)row * d + 4 * k4);
+      float* dst = bsub + j * DP + 4 * k4;
+      dst[0] = x.x;
+      dst[1] = x.y;
+      dst[2] = x.z;
+      dst[3] = x.w;
+    }
+  } else {
+    for (int e = tid; e < m * d; e += kBasicThreads) {
+      const int j = e / d, k = e % d;
+      const int p = (int)(((long long)(2 * j + 1) * size) / (2 * m));
+      const int row = L.first ? start + p : idx[start + p];
+      bsub[j * DP + k] = Y[(size_t)row * d + k];
+    }
+  }
+  // warm start noise of this node
+  if (tid < d) {
+    const uint64_t base = ((((uint64_t)(2 * bh + side) << 5 | (uint64_t)L.level) << 20 |
+                            (uint64_t)node) << 7);
+    t[tid] = irwin_hall(base | (uint64_t)tid);
   }
   __syncthreads();
   if (tid < d) {
@@ -1406,46 +1433,45 @@ __global__ __launch_bounds__(kBasicThreads) void basic_choose_kernel(Ctx C, Leve
     const int j = e / d, k = e % d;
     bsub[j * DP + k] = sub_rn(bsub[j * DP + k], mu[k]);
   }
-  // warm start: noise of this node, the parent's direction one level up
-  if (tid < d) {
-    const uint64_t base = ((((uint64_t)(2 * bh + side) << 5 | (uint64_t)L.level) << 20 |
-                            (uint64_t)node) << 7);
-    t[tid] = irwin_hall(base | (uint64_t)tid);
-  }
-  __syncthreads();
+  // the parent's direction one level up, mixed with the noise
   const float* vp = L.level > 0 ? dir_ptr(C, L.level - 1, pid, node >> 1) : nullptr;
-  if (tid == 0 && vp) {
-    float nv = 0.f, nr = 0.f;
-    for (int k = 0; k < d; ++k) {
-      nv = add_rn(nv, mul_rn(vp[k], vp[k]));
-      nr = add_rn(nr, mul_rn(t[k], t[k]));
+  if (tid < d) {
+    float vk = t[tid];
+    if (vp) {
+      float nv = 0.f, nr = 0.f;
+#pragma unroll 16
+      for (int k = 0; k < d; ++k) {
+        const float pk = vp[k];
+        nv = add_rn(nv, mul_rn(pk, pk));
+        nr = add_rn(nr, mul_rn(t[k], t[k]));
+      }
+      const float sc = div_rn(sqrt_rn(nv), sqrt_rn(nr));
+      vk = mul_rn(add_rn(vp[tid], mul_rn(vk, sc)), 0.5f);
     }
-    sh_sc = div_rn(sqrt_rn(nv), sqrt_rn(nr));
+    v[tid] = vk;
   }
-  __syncthreads();
-  if (tid < d)
-    v[tid] = vp ? mul_rn(add_rn(vp[tid], mul_rn(t[tid], sh_sc)), 0.5f) : t[tid];
   for (int it = 0; it < kBasicIters; ++it) {
     __syncthreads();
     if (tid < m) {
       float a = 0.f;
+#pragma unroll 16
       for (int k = 0; k < d; ++k) a = add_rn(a, mul_rn(bsub[tid * DP + k], v[k]));
       t[tid] = a;
     }
     __syncthreads();
     if (tid < d) {
       float a = 0.f;
+#pragma unroll 16
       for (int j = 0; j < m; ++j) a = add_rn(a, mul_rn(t[j], bsub[j * DP + tid]));
       w[tid] = a;
     }
     __syncthreads();
-    if (tid == 0) {
+    if (tid < d) {
       float nn = 0.f;
+#pragma unroll 16
       for (int k = 0; k < d; ++k) nn = add_rn(nn, mul_rn(w[k], w[k]));
-      sh_nn = nn;
+      if (nn > 0.f) v[tid] = div_rn(w[tid], sqrt_rn(nn));
     }
-    __syncthreads();
-    if (tid < d && sh_nn > 0.f) v[tid] = div_rn(w[tid], sqrt_rn(sh_nn));
   }
   __syncthreads();
   float* vo = dir_ptr(C, L.level, pid, node);
@@ -1453,6 +1479,7 @@ __global__ __launch_bounds__(kBasicThreads) void basic_choose_kernel(Ctx C, Leve
   // spread of the subsample's projections, for the linear bins of the select
   if (tid < m) {
     float a = 0.f;
+#pragma unroll 16
     for (int k = 0; k < d; ++k) a = add_rn(a, mul_rn(bsub[tid * DP + k], v[k]));
     t[tid] = a;
   }
@@ -1472,6 +1499,7 @@ __global__ __launch_bounds__(kBasicThreads) void basic_choose_kernel(Ctx C, Leve
     ns[1] = 0;
     ns[2] = 0;
     ns[3] = mL;
+    ns[10] = 0;
     ns[4] = start;
     ns[5] = size;
     ns[6] = __float_as_int(lo);
@@ -1481,12 +1509,211 @@ __global__ __launch_bounds__(kBasicThreads) void basic_choose_kernel(Ctx C, Leve
   }
 }
 
-// T_K = F_q and T_Q = F_k (basic splitting in the metric root space).
-__global__ __launch_bounds__(256) void copy_roots_kernel(Ctx C) {
-  const int bh = blockIdx.x, dd = C.d * C.d;
+// d = 64: one wavefront per node. Lane j holds sample row j and lane k holds
+// coordinate k of every sample row (the sample column), both read straight
+// from HBM, so each in-order chain runs on registers and 16-byte broadcast
+// reads of one LDS vector (v, t or w). Same operations, in the same order, as
+// basic_choose_kernel.
+__global__ __launch_bounds__(64) void basic_choose64_kernel(Ctx C, LevelArgs L) {
+  constexpr int D = 64;
+  __shared__ __attribute__((aligned(16))) float mu[D], v[D], t[D], w[D];
+  const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH, node = blockIdx.x;
+  const Side& S = C.s[side];
+  if (L.level >= S.big) return;
+  int start, size;
+  node_range(S.n, S.c, L.level, node, &start, &size);
+  int32_t* ns = node_ptr(C, pid, node);
+  const int lane = threadIdx.x;
+  if (size <= S.c) {
+    if (lane == 0) ns[0] = -1;
+    return;
+  }
+  const int m = D < size ? D : size;
+  const int32_t* idx = L.idx_in + (size_t)pid * C.nmax;
+  const float* Y = S.y + (size_t)bh * S.n * D;
+  int myrow = L.first ? start : idx[start];
+  if (lane < m) {
+    const int p = (int)(((long long)(2 * lane + 1) * size) / (2 * m));
+    myrow = L.first ? start + p : idx[start + p];
+  }
+  float row[D], col[D];
+  {
+    const float4* src = (const float4*)(Y + (size_t)myrow * D);
+#pragma unroll
+    for (int k4 = 0; k4 < D / 4; ++k4) {
+      const float4 x = src[k4];
+      row[4 * k4] = x.x;
+      row[4 * k4 + 1] = x.y;
+      row[4 * k4 + 2] = x.z;
+      row[4 * k4 + 3] = x.w;
+    }
+  }
+  // Entries past the m sample rows are held at exactly zero, so every chain
+  // can run over all D terms without branches: a sum that starts at +0 never
+  // becomes -0 in round-to-nearest, so adding a zero product leaves it as is.
+  uint32_t keep[D / 32];
+#pragma unroll
+  for (int h = 0; h < D / 32; ++h)
+    keep[h] = m >= 32 * (h + 1) ? 0xFFFFFFFFu : (m <= 32 * h ? 0u : (1u << (m - 32 * h)) - 1u);
+  auto kept = [&](float x, int j) {
+    return __uint_as_float(__float_as_uint(x) & (0u - ((keep[j >> 5] >> (j & 31)) & 1u)));
+  };
+#pragma unroll
+  for (int j = 0; j < D; ++j) {
+    const int rj = __builtin_amdgcn_readlane(myrow, j);
+    col[j] = kept(Y[(size_t)rj * D + lane], j);
+  }
+  float a = 0.f;
+#pragma unroll
+  for (int j = 0; j < D; ++j) a = add_rn(a, col[j]);
+  const float muk = div_rn(a, (float)m);
+  mu[lane] = muk;
+#pragma unroll
+  for (int j = 0; j < D; ++j) col[j] = kept(sub_rn(col[j], muk), j);
+  const uint64_t base = ((((uint64_t)(2 * bh + side) << 5 | (uint64_t)L.level) << 20 |
+                          (uint64_t)node) << 7);
+  const float noise = irwin_hall(base | (uint64_t)lane);
+  t[lane] = noise;
+  __syncthreads();
+#pragma unroll
+  for (int k4 = 0; k4 < D / 4; ++k4) {
+    const float4 u = *(const float4*)(mu + 4 * k4);
+    row[4 * k4] = sub_rn(row[4 * k4], u.x);
+    row[4 * k4 + 1] = sub_rn(row[4 * k4 + 1], u.y);
+    row[4 * k4 + 2] = sub_rn(row[4 * k4 + 2], u.z);
+    row[4 * k4 + 3] = sub_rn(row[4 * k4 + 3], u.w);
+  }
+  // warm start: the parent's direction one level up, mixed with the noise
+  float vk = noise;
+  if (L.level > 0) {
+    const float* vp = dir_ptr(C, L.level - 1, pid, node >> 1);
+    float nv = 0.f, nr = 0.f;
+#pragma unroll
+    for (int k4 = 0; k4 < D / 4; ++k4) {
+      const float4 pv = *(const float4*)(vp + 4 * k4);
+      const float4 r4 = *(const float4*)(t + 4 * k4);
+      nv = add_rn(nv, mul_rn(pv.x, pv.x));
+      nr = add_rn(nr, mul_rn(r4.x, r4.x));
+      nv = add_rn(nv, mul_rn(pv.y, pv.y));
+      nr = add_rn(nr, mul_rn(r4.y, r4.y));
+      nv = add_rn(nv, mul_rn(pv.z, pv.z));
+      nr = add_rn(nr, mul_rn(r4.z, r4.z));
+      nv = add_rn(nv, mul_rn(pv.w, pv.w));
+      nr = add_rn(nr, mul_rn(r4.w, r4.w));
+    }
+    const float sc = div_rn(sqrt_rn(nv), sqrt_rn(nr));
+    vk = mul_rn(add_rn(vp[lane], mul_rn(noise, sc)), 0.5f);
+  }
+  __syncthreads();
+  v[lane] = vk;
+  for (int it = 0; it < kBasicIters; ++it) {
+    __syncthreads();
+    float ta = 0.f;
+#pragma unroll
+    for (int k4 = 0; k4 < D / 4; ++k4) {
+      const float4 q = *(const float4*)(v + 4 * k4);
+      ta = add_rn(ta, mul_rn(row[4 * k4], q.x));
+      ta = add_rn(ta, mul_rn(row[4 * k4 + 1], q.y));
+      ta = add_rn(ta, mul_rn(row[4 * k4 + 2], q.z));
+      ta = add_rn(ta, mul_rn(row[4 * k4 + 3], q.w));
+    }
+    t[lane] = lane < m ? ta : 0.f;
+    __syncthreads();
+    float wa = 0.f;
+#pragma unroll
+    for (int j4 = 0; j4 < D / 4; ++j4) {
+      const float4 q = *(const float4*)(t + 4 * j4);
+      wa = add_rn(wa, mul_rn(q.x, col[4 * j4]));
+      wa = add_rn(wa, mul_rn(q.y, col[4 * j4 + 1]));
+      wa = add_rn(wa, mul_rn(q.z, col[4 * j4 + 2]));
+      wa = add_rn(wa, mul_rn(q.w, col[4 * j4 + 3]));
+    }
+    w[lane] = wa;
+    __syncthreads();
+    float nn = 0.f;
+#pragma unroll
+    for (int k4 = 0; k4 < D / 4; ++k4) {
+      const float4 q = *(const float4*)(w + 4 * k4);
+      nn = add_rn(nn, mul_rn(q.x, q.x));
+      nn = add_rn(nn, mul_rn(q.y, q.y));
+      nn = add_rn(nn, mul_rn(q.z, q.z));
+      nn = add_rn(nn, mul_rn(q.w, q.w));
+    }
+    if (nn > 0.f) v[lane] = div_rn(wa, sqrt_rn(nn));
+  }
+  __syncthreads();
+  dir_ptr(C, L.level, pid, node)[lane] = v[lane];
+  // spread of the subsample's projections, for the linear bins of the select
+  float ta = 0.f;
+#pragma unroll
+  for (int k4 = 0; k4 < D / 4; ++k4) {
+    const float4 q = *(const float4*)(v + 4 * k4);
+    ta = add_rn(ta, mul_rn(row[4 * k4], q.x));
+    ta = add_rn(ta, mul_rn(row[4 * k4 + 1], q.y));
+    ta = add_rn(ta, mul_rn(row[4 * k4 + 2], q.z));
+    ta = add_rn(ta, mul_rn(row[4 * k4 + 3], q.w));
+  }
+  t[lane] = ta;
+  __syncthreads();
+  if (lane == 0) {
+    double mp = 0.0, vv = 0.0;
+    for (int k = 0; k < D; ++k) mp += (double)mu[k] * (double)v[k];
+    for (int j = 0; j < m; ++j) vv += (double)t[j] * (double)t[j];
+    const double sd = sqrt(vv / m);
+    float lo = (float)(mp - 4.0 * sd), scale = (float)((double)kBins / (8.0 * sd));
+    if (!(sd > 0.0) || !isfinite(lo) || !isfinite(scale)) {
+      lo = 0.f;
+      scale = 0.f;  // one bin: the select step falls back to streaming
+    }
+    const int mL = left_size(size, S.c);
+    ns[0] = 0;
+    ns[1] = 0;
+    ns[2] = 0;
+    ns[3] = mL;
+    ns[4] = start;
+    ns[5] = size;
+    ns[6] = __float_as_int(lo);
+    ns[7] = (size + kChunk - 1) / kChunk;
+    ns[8] = __float_as_int(scale);
+    ns[9] = mL - 1;
+    ns[10] = 0;
+  }
+}
+
+// The order after the last split level, copied to perm (basic splitting runs
+// every level with the multi-block kernels, so no tail pass is needed).
+__global__ __launch_bounds__(256) void copy_order_kernel(Ctx C, int parity0, int parity1) {
+  const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH;
+  const Side& S = C.s[side];
+  const int32_t* src = ((side == 0 ? parity0 : parity1) ? C.idx1 : C.idx0) + (size_t)pid * C.nmax;
+  int32_t* perm = S.perm + (size_t)bh * S.n;
+  const bool identity = S.big == 0;
+  for (int o = blockIdx.x * 256 + threadIdx.x; o < S.n; o += gridDim.x * 256)
+    perm[o] = identity ? o : src[o];
+}
+
+// T_K = F_q and T_Q = F_k (basic splitting in the metric root space), and
+// for the MFMA projection their transposed hi/lo bf16 operands: W_Q^T is the
+// operand the Cholesky pass already packed for F_k, W_K^T is packed here.
+__global__ __launch_bounds__(256) void copy_roots_kernel(Ctx C, int pack) {
+  const int bh = blockIdx.x, d = C.d, dd = d * d;
+  const float* Fq = mat(C, bh, M_E0);
   for (int e = threadIdx.x; e < dd; e += 256) {
-    mat(C, bh, M_TK)[e] = mat(C, bh, M_E0)[e];
+    mat(C, bh, M_TK)[e] = Fq[e];
     mat(C, bh, M_TQ)[e] = mat(C, bh, M_EK)[e];
+  }
+  if (!pack) return;
+  bf16* tk = wop(C, bh, O_TK);
+  bf16* tq = wop(C, bh, O_TQ);
+  const bf16* fk = wop(C, bh, O_FK);
+  for (int e = threadIdx.x; e < dd; e += 256) {
+    const int i = e / d, k = e % d;  // row i = output dim, column k = input dim
+    const float w = Fq[k * d + i];
+    const bf16 hi = (bf16)w;
+    tk[e] = hi;
+    tk[dd + e] = (bf16)(w - (float)hi);
+    tq[e] = fk[e];
+    tq[dd + e] = fk[dd + e];
   }
 }
 
@@ -1519,12 +1746,53 @@ __device__ __forceinline__ int scan256(int x, int* wsum, int* total) {
 }
 
 // Keys of one chunk and its linear-bin histogram.
+// Projection keys of a thread's kPer rows on the direction dv (LDS): each row
+// is read whole with 16-byte loads, R rows at a time (two at d = 64, one at
+// d = 128 to bound registers), and its coordinates are summed in order with
+// separately rounded products.
+template <int D>
+__device__ __forceinline__ void basic_keys(const float* __restrict__ Y, const int (&rows)[kPer],
+                                           const float* dv, int nu, uint32_t (&kv)[kPer]) {
+  constexpr int D4 = D / 4, R = D <= 64 ? 2 : 1;
+#pragma unroll
+  for (int u = 0; u < kPer; u += R) {
+    if (u >= nu) break;  // block-uniform: no position of the chunk is left
+    float4 x[R][D4];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const float4* src = (const float4*)(Y + (size_t)rows[u + r] * D);
+#pragma unroll
+      for (int k = 0; k < D4; ++k) x[r][k] = src[k];
+    }
+    float a[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) a[r] = 0.f;
+#pragma unroll
+    for (int k = 0; k < D4; ++k) {
+      const float4 w = *(const float4*)(dv + 4 * k);
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        a[r] = add_rn(a[r], mul_rn(x[r][k].x, w.x));
+        a[r] = add_rn(a[r], mul_rn(x[r][k].y, w.y));
+        a[r] = add_rn(a[r], mul_rn(x[r][k].z, w.z));
+        a[r] = add_rn(a[r], mul_rn(x[r][k].w, w.w));
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) kv[u + r] = ordered_bits(a[r]);
+  }
+}
+
+// BD < 0: keys are the chosen coordinate (diagonalized splitting); BD >= 0:
+// projections on the node's direction (basic splitting), BD = d when it is
+// 64 or 128, else 0.
+template <int BD>
 __global__ __launch_bounds__(256) void split_keys_kernel(Ctx C, LevelArgs L) {
   __shared__ int lh[kBins];
   const int pid = blockIdx.z, side = pid / C.BH, bh = pid % C.BH, node = blockIdx.y;
   const Side& S = C.s[side];
   if (L.level >= S.big) return;
-  const int32_t* ns = node_ptr(C, pid, node);
+  int32_t* ns = node_ptr(C, pid, node);
   const int js = ns[0];
   if (js < 0) return;
   const int start = ns[4], size = ns[5];
@@ -1544,22 +1812,90 @@ __global__ __launch_bounds__(256) void split_keys_kernel(Ctx C, LevelArgs L) {
     rows[u] = o < c1 ? (L.first ? start + o : idx[start + o]) : 0;
   }
   uint32_t kv[kPer];
-  if (C.split == CA_SPLIT_BASIC) {
+  if constexpr (BD >= 0) {
     // projection on the node's direction, coordinates summed in order
-    __shared__ float dv[kMaxD];
+    __shared__ __attribute__((aligned(16))) float dv[kMaxD];
     const float* dir = dir_ptr(C, L.level, pid, node);
     for (int k = threadIdx.x; k < C.d; k += 256) dv[k] = dir[k];
     __syncthreads();
+    if constexpr (BD > 0)
+      basic_keys<BD>(Y, rows, dv, (c1 - c0 + 255) / 256, kv);
+    else
 #pragma unroll
-    for (int u = 0; u < kPer; ++u) {
-      const float* yr = Y + (size_t)rows[u] * C.d;
-      float a = 0.f;
-      for (int k = 0; k < C.d; ++k) a = add_rn(a, mul_rn(yr[k], dv[k]));
-      kv[u] = ordered_bits(a);
-    }
+      for (int u = 0; u < kPer; ++u) {
+        const float* yr = Y + (size_t)rows[u] * C.d;
+        float a = 0.f;
+        for (int k = 0; k < C.d; ++k) a = add_rn(a, mul_rn(yr[k], dv[k]));
+        kv[u] = ordered_bits(a);
+      }
   } else {
 #pragma unroll
     for (int u = 0; u < kPer; ++u) kv[u] = ordered_bits(Y[(size_t)rows[u] * C.d + js]);
+  }
+  if constexpr (BD >= 0) {
+    if (size <= kChunk) {
+      // The whole node is in this block: exact select of the rank-th key here
+      // (four 8-bit digits, high first), and no histogram for the select pass.
+      __shared__ int rh[256];
+      __shared__ int sh_digit, sh_rank;
+      const int tid = threadIdx.x, lane = tid & 63;
+      uint32_t thr = 0u;
+      int r = ns[9];
+      for (int pass = 0; pass < 4; ++pass) {
+        const int shift = 24 - 8 * pass;
+        rh[tid] = 0;
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+          const int o = tid + 256 * u;
+          if (o < c1 && (pass == 0 || (kv[u] >> (shift + 8)) == (thr >> (shift + 8))))
+            atomicAdd(&rh[(kv[u] >> shift) & 255u], 1);
+        }
+        __syncthreads();
+        if (tid < 64) {
+          int cnt[4], sum = 0;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            cnt[i] = rh[4 * tid + i];
+            sum += cnt[i];
+          }
+          int incl = sum;
+#pragma unroll
+          for (int o = 1; o < 64; o <<= 1) {
+            const int y = __shfl_up(incl, o, 64);
+            if (lane >= o) incl += y;
+          }
+          int acc = incl - sum;
+          if (r >= acc && r < incl) {
+            for (int i = 0; i < 4; ++i) {
+              if (r < acc + cnt[i]) {
+                sh_digit = 4 * tid + i;
+                sh_rank = r - acc;
+                break;
+              }
+              acc += cnt[i];
+            }
+          }
+        }
+        __syncthreads();
+        thr |= (uint32_t)sh_digit << shift;
+        r = sh_rank;
+      }
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int o = tid + 256 * u;
+        if (o < c1) keys[start + o] = kv[u];
+      }
+      if (tid == 0) {
+        int32_t* cc = C.chunk_cnt + ((size_t)pid * C.hist_slots + (size_t)node * L.cpn) * 2;
+        cc[0] = 0;
+        cc[1] = 0;
+        ns[1] = (int)thr;
+        ns[2] = r;
+        ns[10] = 1;  // selected
+      }
+      return;
+    }
   }
   __syncthreads();
 #pragma unroll
@@ -1594,7 +1930,7 @@ __global__ __launch_bounds__(kSelThreads) void split_select_kernel(Ctx C, LevelA
   const Side& S = C.s[side];
   if (L.level >= S.big) return;
   int32_t* ns = node_ptr(C, pid, node);
-  if (ns[0] < 0) return;
+  if (ns[0] < 0 || ns[10]) return;  // a leaf, or selected with its keys
   const int start = ns[4], size = ns[5], nch = ns[7];
   const float lo = __int_as_float(ns[6]), scale = __int_as_float(ns[8]);
   const int tid = threadIdx.x, lane = tid & 63;
@@ -2275,9 +2611,9 @@ hipError_t set_lds_limits() {
                         (int)kProjLds);
     (void)hipFuncSetAttribute((const void*)gather_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
                         (int)kGatherLds);
-    (void)hipFuncSetAttribute((const void*)basic_choose_kernel,
-                              hipFuncAttributeMaxDynamicSharedMemorySize,
-                              (int)((size_t)kMaxD * (kMaxD + 1) * sizeof(float)));
+    for (const void* f : {(const void*)basic_choose_kernel<0>, (const void*)basic_choose_kernel<128>})
+      (void)hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)((size_t)kMaxD * (kMaxD + 1) * sizeof(float)));
     (void)hipFuncSetAttribute((const void*)gather_fast_kernel<bf16>,
                               hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     (void)hipFuncSetAttribute((const void*)gather_fast_kernel<float>,
@@ -2415,7 +2751,7 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
         J.j[1] = {M_C3, -1, V_MUR, 1, -1, -1, M_C3, V_L3, M_EK, M_TQ, wq};
     }
     if (basic)  // the metric root space: the Cholesky factors are the projections
-      hipLaunchKernelGGL(copy_roots_kernel, dim3(BH), dim3(256), 0, st, C);
+      hipLaunchKernelGGL(copy_roots_kernel, dim3(BH), dim3(256), 0, st, C, (int)mfma);
     else if (d <= 64)
       hipLaunchKernelGGL(eigh_kernel<64>, dim3(BH, 2), dim3(eigh_threads<64>()), eigh_lds_bytes(64), st, C, J);
     else
@@ -2426,9 +2762,9 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
     const int nmax = C.nmax;
     const size_t plds = kProjLds;
     const dim3 pgrid((nmax + kProjRows - 1) / kProjRows, 2 * BH);
-    if (mfma && transformed && !basic && d == 64)
+    if (mfma && transformed && d == 64)
       hipLaunchKernelGGL(project_mfma_kernel<64>, pgrid, dim3(256), 0, st, C);
-    else if (mfma && transformed && !basic)
+    else if (mfma && transformed)
       hipLaunchKernelGGL(project_mfma_kernel<128>, pgrid, dim3(256), 0, st, C);
     else
       hipLaunchKernelGGL(project_kernel, pgrid, dim3(256), plds, st, C);
@@ -2443,13 +2779,29 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
     L.idx_out = (l & 1) ? C.idx0 : C.idx1;
     const int cpn = split_level_cpn(P, W.big_q, W.big_k, l);
     L.cpn = cpn;
-    if (basic)
-      hipLaunchKernelGGL(basic_choose_kernel, dim3(1 << l, 2 * BH), dim3(kBasicThreads),
-                         (size_t)d * (d + 1) * sizeof(float), st, C, L);
+    if (basic) {
+      const size_t blds = (size_t)d * (d + 1) * sizeof(float);
+      if (d == 64)
+        hipLaunchKernelGGL(basic_choose64_kernel, dim3(1 << l, 2 * BH), dim3(64), 0, st, C, L);
+      else if (d == 128)
+        hipLaunchKernelGGL(basic_choose_kernel<128>, dim3(1 << l, 2 * BH), dim3(kBasicThreads),
+                           blds, st, C, L);
+      else
+        hipLaunchKernelGGL(basic_choose_kernel<0>, dim3(1 << l, 2 * BH), dim3(kBasicThreads),
+                           blds, st, C, L);
+    }
     else
       hipLaunchKernelGGL(split_choose_kernel, dim3(1 << l, 2 * BH), dim3(64), 0, st, C, L);
     CA_CHECK();
-    hipLaunchKernelGGL(split_keys_kernel, dim3(cpn, 1 << l, 2 * BH), dim3(256), 0, st, C, L);
+    const dim3 kgrid(cpn, 1 << l, 2 * BH);
+    if (!basic)
+      hipLaunchKernelGGL(split_keys_kernel<-1>, kgrid, dim3(256), 0, st, C, L);
+    else if (d == 64)
+      hipLaunchKernelGGL(split_keys_kernel<64>, kgrid, dim3(256), 0, st, C, L);
+    else if (d == 128)
+      hipLaunchKernelGGL(split_keys_kernel<128>, kgrid, dim3(256), 0, st, C, L);
+    else
+      hipLaunchKernelGGL(split_keys_kernel<0>, kgrid, dim3(256), 0, st, C, L);
     CA_CHECK();
     hipLaunchKernelGGL(split_select_kernel, dim3(1 << l, 2 * BH), dim3(kSelThreads), 0, st, C, L);
     CA_CHECK();
@@ -2459,8 +2811,12 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
   {
     // After its last multi-block level, side s holds its order in idx[(big_s) & 1].
     const int nodes = 1 << big;
-    hipLaunchKernelGGL(split_tail_kernel, dim3(nodes, 2 * BH), dim3(kTailThreads), 0, st, C,
-                       W.big_q & 1, W.big_k & 1);
+    if (basic)
+      hipLaunchKernelGGL(copy_order_kernel, dim3((C.nmax + 255) / 256 < 1024 ? (C.nmax + 255) / 256 : 1024, 2 * BH),
+                         dim3(256), 0, st, C, W.big_q & 1, W.big_k & 1);
+    else
+      hipLaunchKernelGGL(split_tail_kernel, dim3(nodes, 2 * BH), dim3(kTailThreads), 0, st, C,
+                         W.big_q & 1, W.big_k & 1);
     CA_CHECK();
   }
   {

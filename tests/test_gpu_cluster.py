@@ -181,6 +181,9 @@ BASIC_CASES = [
     ("f32", 5000, 128, 64, "metric"),
     ("bf16", 9000, 32, 16, "none"),
     ("bf16", 700, 64, 64, "metric"),
+    # nodes smaller than d (samples of m < d rows) at d = 64 and d = 128
+    ("bf16", 3000, 64, 16, "metric"),
+    ("bf16", 4000, 128, 32, "none"),
 ]
 
 
