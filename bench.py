@@ -146,7 +146,8 @@ def latency_sweep(args):
     """Latency scaling with the number of tokens (the paper's latency-scaling
     experiment): 8 heads, d = 64, bf16, c = 128, metric transform, exact top-k,
     compensation on; k fixed to 64 clusters (8192 keys) or set to 10% of the
-    key clusters. Inputs: the tabular recipe (per head 64 mixture centres
+    key clusters; and, with k fixed, basic recursive splitting in the metric
+    root space (power iteration per node, no eigendecomposition). Inputs: the tabular recipe (per head 64 mixture centres
     N(0, I), Dirichlet(1) weights, queries and keys drawn from the mixture
     with sigma 0.5 and independent labels, values N(0, 1)), drawn on the GPU
     with torch's generator seeded by N (the host generator would take minutes
@@ -175,9 +176,11 @@ def latency_sweep(args):
         g = torch.Generator(device=dev)
         g.manual_seed(n)
         q, k, v = mixture(n, g)
-        p = ca.Problem(1, H, n, n, d, c, c, torch.bfloat16, "metric", "bhnd")
-        out = torch.empty(p.shape(n), dtype=torch.bfloat16, device=dev)
-        for rule in ("k64", "keep10pct"):
+        out = None
+        for rule, split in (("k64", "diag"), ("keep10pct", "diag"), ("k64", "basic")):
+            p = ca.Problem(1, H, n, n, d, c, c, torch.bfloat16, "metric", "bhnd", split=split)
+            if out is None:
+                out = torch.empty(p.shape(n), dtype=torch.bfloat16, device=dev)
             keep_k = min(64, p.nkc) if rule == "k64" else ca.keep_to_k(0.1, p.nkc)
             ws = ca.workspace(p, dev, keep_k)
 
@@ -211,7 +214,8 @@ def latency_sweep(args):
             calls = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(4)]
                               for e in evs]).mean(0)
             f_dense = 4.0 * H * n * n * d
-            print(json.dumps({"sweep": "latency_scaling", "n": n, "rule": rule, "kept_clusters":
+            print(json.dumps({"sweep": "latency_scaling", "n": n, "rule": rule, "split": split,
+                              "kept_clusters":
                               keep_k, "key_clusters": p.nkc, "ms_per_layer": round(ms, 4),
                               "cluster_ms": round(calls[0], 4), "select_ms": round(calls[1], 4),
                               "attention_ms": round(calls[2], 4),
