@@ -28,7 +28,7 @@ def _pipeline(p, q, k, v, keep_k, comp=True):
     return r, lists, scores, out, lse_out
 
 
-def _check_head(Q, K, V, r, lists, scores, out, h, c, k, dt, nsample, comp, seed):
+def _check_head(Q, K, V, r, lists, scores, out, h, c, k, dt, nsample, comp, seed, split="diag"):
     from tests import gpu_util as G
     n, d = Q.shape
     tau = 1 / math.sqrt(d)
@@ -36,8 +36,13 @@ def _check_head(Q, K, V, r, lists, scores, out, h, c, k, dt, nsample, comp, seed
     yk = r["yk"][h].double().cpu().numpy()
     perm_q = r["perm_q"][h].cpu().numpy()
     perm_k = r["perm_k"][h].cpu().numpy()
-    assert np.array_equal(perm_q, ref.split(yq, c)[0]), "query permutation"
-    assert np.array_equal(perm_k, ref.split(yk, c)[0]), "key permutation"
+    if split == "basic":
+        want_q = ref.basic_split(yq, c, head=h, side=0)[0]
+        want_k = ref.basic_split(yk, c, head=h, side=1)[0]
+    else:
+        want_q, want_k = ref.split(yq, c)[0], ref.split(yk, c)[0]
+    assert np.array_equal(perm_q, want_q), "query permutation"
+    assert np.array_equal(perm_k, want_k), "key permutation"
     cq_n, ck_n = G.counts(n, c), G.counts(n, c)
     S = scores[h].double().cpu().numpy()
     L = lists[h].cpu().numpy()
@@ -64,16 +69,16 @@ def _check_head(Q, K, V, r, lists, scores, out, h, c, k, dt, nsample, comp, seed
     return err
 
 
-def _run_config(cid, heads, c, keep, comp=True, check_heads=None, nsample=12):
+def _run_config(cid, heads, c, keep, comp=True, check_heads=None, nsample=12, split="diag"):
     import torch
     import paper_2608_26965_amd as ca
     from tests import gpu_util as G
     cfg = CONFIGS[cid]
-    G.flush(f"e2e config {cid} heads={len(heads)} c={c} keep={keep} comp={comp}")
+    G.flush(f"e2e config {cid} heads={len(heads)} c={c} keep={keep} comp={comp} split={split}")
     Q, K, V = make_config(cid, heads=heads)
     H, n, d = Q.shape
     dt = cfg.dtype
-    p = ca.Problem(1, H, n, n, d, c, c, G.tdtype(dt), "metric")
+    p = ca.Problem(1, H, n, n, d, c, c, G.tdtype(dt), "metric", split=split)
     k = keep_to_k(keep, p.nkc)
     tq, tk, tv = (G.dev(x[None], G.tdtype(dt)) for x in (Q, K, V))
     r, lists, scores, out, lse = _pipeline(p, tq, tk, tv, k, comp)
@@ -82,7 +87,7 @@ def _run_config(cid, heads, c, keep, comp=True, check_heads=None, nsample=12):
     worst = 0.0
     for h in (check_heads if check_heads is not None else range(H)):
         worst = max(worst, _check_head(Q[h], K[h], V[h], r, lists, scores, outh, h, c, k, dt,
-                                       nsample, comp, seed=cid * 100 + h))
+                                       nsample, comp, seed=cid * 100 + h, split=split))
     G.flush(f"  worst sampled error {worst:.3g}")
     return r, lists, out
 
@@ -109,6 +114,13 @@ def test_small_fp32_all_kept_is_dense():
 def test_tabular_bench_workload_all_heads():
     """The benchmarked workload at full size, all 8 heads."""
     _run_config(2, list(range(8)), 128, 1 / 8, check_heads=[0, 3, 7])
+
+
+def test_tabular_bench_workload_basic_split():
+    """The benchmarked workload at full size with basic recursive splitting in
+    the metric root space: the power-iteration directions, projections and
+    partitions reproduced bit for bit on the checked heads of both sides."""
+    _run_config(2, list(range(8)), 128, 1 / 8, check_heads=[0, 5], split="basic", nsample=8)
 
 
 @pytest.mark.parametrize("keep", [1 / 16, 1 / 4])
