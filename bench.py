@@ -108,7 +108,7 @@ def time_selection_modes(ca, torch, p, q, k, v, keep_k, out, args):
             if ev:
                 ev[2].record()
             op, lse = ca.block_sparse_attn(pm, r["qp"], r["kp"], r["vp"], r["count_k"], lists,
-                                           stride, lens=lens)
+                                           stride, lens=lens, ws=ws)
             if ev:
                 ev[3].record()
             ca.compensate(pm, r["qp"], r["cent_k"], r["cent_v"], r["count_k"], lists, stride, op,

@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define CA_ABI_VERSION 4
+#define CA_ABI_VERSION 5
 
 #if defined(__GNUC__) || defined(__clang__)
 #define CA_API __attribute__((visibility("default")))
@@ -255,10 +255,18 @@ CA_API int ca_select_hist(const ca_problem* p, const float* cent_q, const float*
  * entries, clamped to [1, k] on the device), op: [BH][nq_pad][d] dtype, lse:
  * [BH][nq_pad] fp32. scale <= 0 selects 1/sqrt(d). Padding query rows get
  * defined values that callers ignore. bf16: d in {64, 128}, cq and ck in
- * {64, 128}; fp32: d % 4 == 0, any cq, ck. */
+ * {64, 128}; fp32: d % 4 == 0, any cq, ck.
+ *
+ * ws: optional device workspace of ws_bytes >= ca_workspace_size(). With
+ * lens given (lists of different lengths) the bf16 path uses it to schedule
+ * the query clusters: they are cut into eight contiguous ranges of about
+ * equal work, one per XCD, and each range runs longest list first. With ws
+ * NULL (ws_bytes 0) the query clusters run in index order. The results are
+ * the same either way: only the order in which workgroups start changes. */
 CA_API int ca_block_sparse_attn(const ca_problem* p, const void* qp, const void* kp, const void* vp,
                          const int32_t* count_k, const int32_t* lists, const int32_t* lens,
-                         int32_t k, float scale, void* op, float* lse, void* stream);
+                         int32_t k, float scale, void* op, float* lse, void* ws,
+                         size_t ws_bytes, void* stream);
 
 /* Step 4: striped mean-compensation and un-permutation (Preliminaries: error
  * in sparse attention; App. A).

@@ -176,15 +176,18 @@ def select_hist(p: Problem, cent_q, cent_k, count_k, min_count: int, mass_recall
 
 
 def block_sparse_attn(p: Problem, qp, kp, vp, count_k, lists, keep_k: int, scale: float = 0.0,
-                      lens=None):
+                      lens=None, ws=None):
     """Step 3. Returns (op [BH,nq_pad,d] dtype, lse [BH,nq_pad] fp32). keep_k is
-    the list stride; lens (optional) the per-cluster list lengths."""
+    the list stride; lens (optional) the per-cluster list lengths; ws
+    (optional) the workspace, with which lists of different lengths are
+    scheduled longest first per XCD."""
     dev = qp.device
     op = torch.empty(p.bh, p.nq_pad, p.d, dtype=p.dtype, device=dev)
     lse = torch.empty(p.bh, p.nq_pad, dtype=torch.float32, device=dev)
     st = _lib.load().ca_block_sparse_attn(p.c(), _ptr(qp), _ptr(kp), _ptr(vp), _ptr(count_k),
                                           _ptr(lists), _ptr(lens), keep_k, float(scale), _ptr(op),
-                                          _ptr(lse), _stream(dev))
+                                          _ptr(lse), _ptr(ws), ws.numel() if ws is not None else 0,
+                                          _stream(dev))
     _lib.check(st, "ca_block_sparse_attn")
     return op, lse
 
@@ -250,7 +253,7 @@ def forward(q, k, v, cq=128, ck=None, keep=None, keep_k=None, transform="metric"
     else:
         raise ValueError(select)
     op, lse = block_sparse_attn(p, c["qp"], c["kp"], c["vp"], c["count_k"], lists, stride, sc,
-                                lens=lens)
+                                lens=lens, ws=ws)
     out, lse_out = compensate(p, c["qp"], c["cent_k"], c["cent_v"], c["count_k"], lists, stride,
                               op, lse, c["perm_q"], sc, compensation, want_lse=return_parts, ws=ws,
                               lens=lens)

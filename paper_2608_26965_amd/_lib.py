@@ -75,7 +75,7 @@ def load() -> ctypes.CDLL:
     lib.ca_select.argtypes = [P, _vp, _vp, _vp, _vp, _i32, _vp, _vp, ctypes.c_size_t, _vp]
     lib.ca_block_sparse_attn.restype = ctypes.c_int
     lib.ca_block_sparse_attn.argtypes = [P, _vp, _vp, _vp, _vp, _vp, _vp, _i32, ctypes.c_float,
-                                         _vp, _vp, _vp]
+                                         _vp, _vp, _vp, ctypes.c_size_t, _vp]
     lib.ca_select_hist.restype = ctypes.c_int
     lib.ca_select_hist.argtypes = [P, _vp, _vp, _vp, _vp, _vp, _i32, ctypes.c_float,
                                    ctypes.c_float, _vp, _vp, _vp, ctypes.c_size_t, _vp]

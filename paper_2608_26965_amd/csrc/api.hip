@@ -139,6 +139,7 @@ void plan_workspace(const Prob& P, Workspace* W) {
   W->chunk_cnt = take(2 * BH * W->hist_slots * 2 * 4);
   W->dirs = take(basic ? 2 * 2 * BH * W->max_big_nodes * d * 4 : 0);
   W->scores = take(BH * P.nqc * P.nkc * 4);
+  W->sched = take(((size_t)8 + 8 * (size_t)attn_sched_cap((int)(BH * P.nqc))) * 4);
   const size_t ntile = (P.nkc + kCompTile - 1) / kCompTile;
   W->comp_tiles = take(P.dtype == CA_BF16 ? BH * ntile * comp_tile_bytes(P.d) : 0);
   W->total = off;
@@ -246,7 +247,8 @@ int ca_select_hist(const ca_problem* p, const float* cent_q, const float* cent_k
 
 int ca_block_sparse_attn(const ca_problem* p, const void* qp, const void* kp, const void* vp,
                          const int32_t* count_k, const int32_t* lists, const int32_t* lens,
-                         int32_t k, float scale, void* op, float* lse, void* stream) {
+                         int32_t k, float scale, void* op, float* lse, void* ws, size_t ws_bytes,
+                         void* stream) {
   ca::Prob P;
   int s = check_problem(p, &P);
   if (s) return s;
@@ -254,10 +256,17 @@ int ca_block_sparse_attn(const ca_problem* p, const void* qp, const void* kp, co
   if (!qp || !kp || !vp || !count_k || !lists || !op || !lse)
     return fail(CA_E_INVALID, "a required pointer of ca_block_sparse_attn is NULL");
   if ((s = check_attn_shape(P))) return s;
+  int32_t* sched = nullptr;
+  if (ws && lens && P.dtype == CA_BF16) {
+    ca::Workspace W;
+    ca::plan_workspace(P, &W);
+    if ((s = check_ws(W, ws, ws_bytes))) return s;
+    sched = (int32_t*)((char*)ws + W.sched);
+  }
   if (!(scale > 0.0f)) scale = 1.0f / sqrtf((float)P.d);
-  return device_status(
-      ca::launch_attn(P, qp, kp, vp, count_k, lists, lens, k, scale, op, lse, (hipStream_t)stream),
-      "ca_block_sparse_attn");
+  return device_status(ca::launch_attn(P, qp, kp, vp, count_k, lists, lens, k, scale, op, lse,
+                                       sched, (hipStream_t)stream),
+                       "ca_block_sparse_attn");
 }
 
 int ca_compensate(const ca_problem* p, const void* qp, const float* cent_k, const float* cent_v,

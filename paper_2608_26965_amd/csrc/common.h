@@ -108,6 +108,8 @@ struct Workspace {
   size_t dirs;              // fp32 [2 levels][2][BH][max_big_nodes][d] split directions (basic)
   // selection
   size_t scores;            // fp32 [BH][nqc][nkc]
+  // attention schedule of lists with lengths
+  size_t sched;             // int32 [8 + 8 * attn_sched_cap(BH * nqc)]
   // compensation
   size_t comp_tiles;        // bf16 centroid tiles [BH][ceil(nkc/kCompTile)][comp_tile_bytes]
   size_t total;
@@ -154,9 +156,13 @@ hipError_t launch_select_hist(const Prob& P, const float* cq, const float* ck,
                               int min_count, float recall, float scale, int32_t* lists,
                               int32_t* lens, hipStream_t st);
 // lens (optional): per query cluster list lengths, clamped to [1, k] on the device.
+// Items per XCD of the attention schedule: about 1.25 times the mean, so a
+// range of short lists can take more items than one of long lists.
+inline int attn_sched_cap(int items) { return (5 * items + 31) / 32 + 1; }
+// sched: workspace region of the schedule (bf16 with lens; else may be NULL).
 hipError_t launch_attn(const Prob& P, const void* qp, const void* kp, const void* vp,
                        const int32_t* count_k, const int32_t* lists, const int32_t* lens, int k,
-                       float scale, void* op, float* lse, hipStream_t st);
+                       float scale, void* op, float* lse, int32_t* sched, hipStream_t st);
 // tiles: workspace region of the bf16 centroid tiles (bf16 with compensation
 // only; ignored otherwise).
 hipError_t launch_comp(const Prob& P, const void* qp, const float* cent_k, const float* cent_v,

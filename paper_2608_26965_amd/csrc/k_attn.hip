@@ -48,7 +48,7 @@ __global__ __launch_bounds__(CQ * 2, (attn_blocks_per_cu<D, CQ, CK>())) void att
     const bf16* __restrict__ qp, const bf16* __restrict__ kp, const bf16* __restrict__ vp,
     const int32_t* __restrict__ count_k, const int32_t* __restrict__ lists,
     const int32_t* __restrict__ lens, int nqc, int nkc, int k, float sl2, bf16* __restrict__ op,
-    float* __restrict__ lse, int total) {
+    float* __restrict__ lse, int total, const int32_t* __restrict__ sched, int cap) {
   constexpr int NW = CQ / 32;
   constexpr int MT = CK / 32;
   constexpr int KS = D / 16;
@@ -62,7 +62,15 @@ __global__ __launch_bounds__(CQ * 2, (attn_blocks_per_cu<D, CQ, CK>())) void att
   static_assert(KLD * 1024 * NW == KBYTES && VLD * 1024 * NW == VBYTES, "tile split");
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
-  const int item = xcd_remap(blockIdx.x, total);
+  int item;
+  if (sched) {
+    // scheduled launch: slot loc of XCD x (workgroups run on XCD blockIdx % 8)
+    const int x = blockIdx.x & 7, loc = blockIdx.x >> 3;
+    if (loc >= sched[x]) return;
+    item = sched[8 + x * cap + loc];
+  } else {
+    item = xcd_remap(blockIdx.x, total);
+  }
   const int bh = item / nqc, a = item - bh * nqc;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
   const size_t nq_pad = (size_t)nqc * CQ, nk_pad = (size_t)nkc * CK;
@@ -286,14 +294,122 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
   }
 }
 
+// Launch order for lists of different lengths. Work of an item (head, query
+// cluster) = its list length + 2 (the per-workgroup fixed cost in tiles). The
+// items are cut into eight contiguous ranges of about equal work (an item
+// goes to XCD floor(8 * work before it / total work)), each range holding at
+// most cap items, so neighbouring query clusters (which share key tiles)
+// still meet in one L2; block x then lists its range longest first (counting
+// sort on the length; the order among equal lengths is not fixed, and does not
+// change any result). sched[x] = items of XCD x, sched[8 + x * cap + i] = its
+// i-th item.
+constexpr int kSchedThreads = 1024;
+constexpr int kSchedBins = 4096;
+
+__global__ __launch_bounds__(kSchedThreads) void attn_sched_kernel(const int32_t* __restrict__ lens,
+                                                                   int total, int k, int cap,
+                                                                   int32_t* __restrict__ sched) {
+  __shared__ long long wsum[kSchedThreads / 64];
+  __shared__ int bound[9];
+  __shared__ int hist[kSchedBins];
+  const int x = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  auto work = [&](int i) { return (long long)min(max(lens[i], 1), k) + 2; };
+  // 1. exclusive prefix of the work at each thread's contiguous chunk
+  const int per = (total + kSchedThreads - 1) / kSchedThreads;
+  const int i0 = min(tid * per, total), i1 = min(i0 + per, total);
+  long long mine = 0;
+  for (int i = i0; i < i1; ++i) mine += work(i);
+  long long incl = mine;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const long long y = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += y;
+  }
+  if (lane == 63) wsum[wv] = incl;
+  if (tid < 9) bound[tid] = tid == 0 ? 0 : total;
+  __syncthreads();
+  long long before = incl - mine, W = 0;
+  for (int i = 0; i < kSchedThreads / 64; ++i) {
+    before += i < wv ? wsum[i] : 0;
+    W += wsum[i];
+  }
+  // 2. range boundaries: the first item whose prefix reaches y * W / 8
+  {
+    long long pre = before;
+    for (int i = i0; i < i1; ++i) {
+      const long long nxt = pre + work(i);
+#pragma unroll
+      for (int y = 1; y < 8; ++y) {
+        const long long t = (long long)y * W;
+        if (8 * pre < t && 8 * nxt >= t) bound[y] = i + 1;
+      }
+      pre = nxt;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    // at most cap items per range, and room for the rest in the ranges after
+    int b = 0;
+    for (int y = 1; y < 8; ++y) {
+      int v = min(bound[y], b + cap);
+      v = max(v, total - (8 - y) * cap);
+      v = max(v, b);
+      bound[y] = v;
+      b = v;
+    }
+  }
+  for (int e = tid; e < kSchedBins; e += kSchedThreads) hist[e] = 0;
+  __syncthreads();
+  const int r0 = bound[x], r1 = bound[x + 1];
+  auto key = [&](int i) {
+    const int len = min(max(lens[i], 1), k);
+    const int bin = k <= kSchedBins ? len - 1 : (int)((long long)(len - 1) * kSchedBins / k);
+    return kSchedBins - 1 - bin;  // longest first
+  };
+  // 3. counting sort of the range
+  for (int i = r0 + tid; i < r1; i += kSchedThreads) atomicAdd(&hist[key(i)], 1);
+  __syncthreads();
+  if (tid < 64) {
+    // exclusive scan of the bins, 64 per lane
+    int s = 0;
+    for (int j = 0; j < kSchedBins / 64; ++j) s += hist[64 * tid + j];
+    int inc = s;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(inc, o, 64);
+      if (lane >= o) inc += y;
+    }
+    int run = inc - s;
+    for (int j = 0; j < kSchedBins / 64; ++j) {
+      const int c = hist[64 * tid + j];
+      hist[64 * tid + j] = run;
+      run += c;
+    }
+  }
+  __syncthreads();
+  int32_t* out = sched + 8 + (size_t)x * cap;
+  for (int i = r0 + tid; i < r1; i += kSchedThreads) out[atomicAdd(&hist[key(i)], 1)] = i;
+  if (tid == 0) sched[x] = r1 - r0;
+}
+
 template <int D, int CQ, int CK>
 hipError_t run_bf16(const Prob& P, const void* qp, const void* kp, const void* vp,
                     const int32_t* count_k, const int32_t* lists, const int32_t* lens, int k,
-                    float scale, void* op, float* lse, hipStream_t st) {
-  int total = P.BH * P.nqc;
-  hipLaunchKernelGGL((attn_bf16_kernel<D, CQ, CK>), dim3(total), dim3(CQ * 2), 0, st,
-                     (const bf16*)qp, (const bf16*)kp, (const bf16*)vp, count_k, lists, lens,
-                     P.nqc, P.nkc, k, scale * kLog2e, (bf16*)op, lse, total);
+                    float scale, void* op, float* lse, int32_t* sched, hipStream_t st) {
+  const int total = P.BH * P.nqc;
+  const int cap = attn_sched_cap(total);
+  if (sched && lens) {
+    hipLaunchKernelGGL(attn_sched_kernel, dim3(8), dim3(kSchedThreads), 0, st, lens, total, k, cap,
+                       sched);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  } else {
+    sched = nullptr;
+  }
+  hipLaunchKernelGGL((attn_bf16_kernel<D, CQ, CK>), dim3(sched ? 8 * cap : total), dim3(CQ * 2),
+                     0, st, (const bf16*)qp, (const bf16*)kp, (const bf16*)vp, count_k, lists,
+                     lens, P.nqc, P.nkc, k, scale * kLog2e, (bf16*)op, lse, total,
+                     (const int32_t*)sched, cap);
   return hipGetLastError();
 }
 
@@ -301,11 +417,11 @@ hipError_t run_bf16(const Prob& P, const void* qp, const void* kp, const void* v
 
 hipError_t launch_attn(const Prob& P, const void* qp, const void* kp, const void* vp,
                        const int32_t* count_k, const int32_t* lists, const int32_t* lens, int k,
-                       float scale, void* op, float* lse, hipStream_t st) {
+                       float scale, void* op, float* lse, int32_t* sched, hipStream_t st) {
   if (P.dtype == CA_BF16) {
 #define CA_ATTN_CASE(D, CQ, CK) \
   if (P.d == D && P.cq == CQ && P.ck == CK) \
-    return run_bf16<D, CQ, CK>(P, qp, kp, vp, count_k, lists, lens, k, scale, op, lse, st);
+    return run_bf16<D, CQ, CK>(P, qp, kp, vp, count_k, lists, lens, k, scale, op, lse, sched, st);
     CA_ATTN_CASE(64, 64, 64)
     CA_ATTN_CASE(64, 64, 128)
     CA_ATTN_CASE(64, 128, 64)

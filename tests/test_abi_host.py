@@ -25,7 +25,7 @@ def test_header_symbols_exported():
     assert declared == set(L.EXPORTS)
     for name in declared:
         assert hasattr(lib, name)
-    assert lib.ca_abi_version() == 4
+    assert lib.ca_abi_version() == 5
 
 
 def _prob(**kw):
@@ -69,12 +69,16 @@ def test_calls_reject_before_enqueue():
     assert lib.ca_select(p, None, None, None, None, 4, fake, None, 0, None) == L.CA_E_INVALID
     assert lib.ca_select(p, fake, fake, None, None, 4, fake, None, 0, None) == L.CA_E_WORKSPACE
     args = [fake] * 5 + [None]  # qp, kp, vp, count_k, lists; lens omitted
-    assert lib.ca_block_sparse_attn(p, *args, 0, 0.0, fake, fake, None) == L.CA_E_INVALID
-    assert lib.ca_block_sparse_attn(p, *args, 99, 0.0, fake, fake, None) == L.CA_E_INVALID
-    assert lib.ca_block_sparse_attn(_prob(d=48), *args, 2, 0.0, fake, fake, None) == \
+    assert lib.ca_block_sparse_attn(p, *args, 0, 0.0, fake, fake, None, 0, None) == L.CA_E_INVALID
+    assert lib.ca_block_sparse_attn(p, *args, 99, 0.0, fake, fake, None, 0, None) == L.CA_E_INVALID
+    assert lib.ca_block_sparse_attn(_prob(d=48), *args, 2, 0.0, fake, fake, None, 0, None) == \
         L.CA_E_UNSUPPORTED
-    assert lib.ca_block_sparse_attn(_prob(cq=32), *args, 2, 0.0, fake, fake, None) == \
+    assert lib.ca_block_sparse_attn(_prob(cq=32), *args, 2, 0.0, fake, fake, None, 0, None) == \
         L.CA_E_UNSUPPORTED
+    # with list lengths, a workspace (for the schedule) is checked for its size
+    largs = [fake] * 6  # ... and lens given
+    assert lib.ca_block_sparse_attn(p, *largs, 2, 0.0, fake, fake, fake, 16, None) == \
+        L.CA_E_WORKSPACE
     assert lib.ca_compensate(p, fake, fake, fake, fake, fake, None, 2, 0.0, 1, None, fake, fake,
                              fake, None, None, 0, None) == L.CA_E_INVALID
     assert lib.ca_compensate(p, None, None, None, None, None, None, 2, 0.0, 1, fake, fake, fake,

@@ -180,8 +180,13 @@ def test_tabular_histogram_selection_pipeline(mode):
     r = ca.cluster(p, tq, tk, tv, export_y=True)
     lists, lens, scores = ca.select_hist(p, r["cent_q"], r["cent_k"], r["count_k"], floor, recall,
                                          float(scale), export_scores=True)
+    ws = ca.workspace(p, tq.device, p.nkc)
     op, lse = ca.block_sparse_attn(p, r["qp"], r["kp"], r["vp"], r["count_k"], lists, p.nkc,
-                                   lens=lens)
+                                   lens=lens, ws=ws)
+    # the longest-first schedule changes only the launch order
+    op0, lse0 = ca.block_sparse_attn(p, r["qp"], r["kp"], r["vp"], r["count_k"], lists, p.nkc,
+                                     lens=lens)
+    assert torch.equal(op, op0) and torch.equal(lse, lse0), "scheduled launch"
     out, _ = ca.compensate(p, r["qp"], r["cent_k"], r["cent_v"], r["count_k"], lists, p.nkc, op,
                            lse, r["perm_q"], lens=lens)
     torch.cuda.synchronize()
