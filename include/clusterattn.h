@@ -201,8 +201,11 @@ CA_API int ca_cluster(const ca_problem* p, const void* q, const void* k, const v
 
 /* Step 2: assignment (Method: Cluster assignment - scoring and top-k
  * selection). scores[a][b] = cent_q[a] . cent_k[b] (fp32, the mean pairwise
- * logit up to the 1/sqrt(d) factor); lists[a] = the k key clusters with the
- * largest scores, ties to the lower index, in ascending order.
+ * logit up to the 1/sqrt(d) factor; for bf16 problems with d = 64 or 128 and
+ * 16-byte aligned centroids they are formed on the matrix cores from a
+ * three-term bf16 split of the fp32 centroids, about 2^-16 relative per
+ * product); lists[a] = the k key clusters with the largest scores, ties to
+ * the lower index, in ascending order.
  *
  * cent_q: [BH][nqc][d], cent_k: [BH][nkc][d] fp32. scores_in: optional
  * [BH][nqc][nkc] fp32 scores to rank instead of computing them (NULL:

@@ -2,7 +2,8 @@
 // selection and the two-pass histogram selection).
 //
 // scores[a][b] = qbar_a . kbar_b in fp32 (fixed summation order, so scores are
-// reproducible); lists[a] = the k key clusters of largest score, ties to the
+// reproducible; bf16 problems with d = 64 or 128 form them on the matrix
+// cores from a three-term bf16 split of the fp32 centroids); lists[a] = the k key clusters of largest score, ties to the
 // lower index, in ascending order. The selection is an exact radix select on
 // order-preserving integer images of the scores (four 8-bit digit passes),
 // followed by an order-keeping compaction; it makes no floating-point
@@ -52,6 +53,103 @@ __global__ __launch_bounds__(256) void scores_kernel(const float* __restrict__ c
       const int a = a0 + tr + i, b = b0 + tc + j;
       if (a < nqc && b < nkc) Sh[(size_t)a * nkc + b] = acc[i][j];
     }
+}
+
+// Centroid scores on the matrix cores (bf16 problems, d = 64 or 128). Each
+// fp32 operand x is split into hi = bf16(x) and lo = bf16(x - hi), and
+// S = lo_q hi_k + hi_q lo_k + hi_q hi_k is accumulated in fp32 (the dropped
+// lo_q lo_k term is about 2^-16 of each product), so the scores keep close to
+// fp32 accuracy at the bf16 MFMA rate. One workgroup per 128 x 128 tile of
+// one head: wave w owns query rows 32 w .. 32 w + 31 and takes the four
+// 32-column key blocks in turn. v_mfma_f32_32x32x16_bf16 with the query rows
+// as the A operand and the key rows as B: lane l holds key column l % 32 of
+// the output block and query rows 8 (r / 4) + 4 (l / 32) + r % 4, so each
+// store instruction writes two 128-byte row segments.
+__device__ __forceinline__ void split_hilo(const float4 x0, const float4 x1, bf16x8& hi,
+                                           bf16x8& lo) {
+  const float v[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const bf16 h = (bf16)v[i];
+    hi[i] = h;
+    lo[i] = (bf16)(v[i] - (float)h);
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void scores_mfma_kernel(const float* __restrict__ cq,
+                                                          const float* __restrict__ ck, int nqc,
+                                                          int nkc, float* __restrict__ S) {
+  constexpr int KS = D / 16;
+  const int bh = blockIdx.z, a0 = blockIdx.y * 128, b0 = blockIdx.x * 128;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, h = lane >> 5, l32 = lane & 31;
+  const float* qh = cq + (size_t)bh * nqc * D;
+  const float* kh = ck + (size_t)bh * nkc * D;
+  const int arow = a0 + 32 * w + l32;
+  bf16x8 qhi[KS], qlo[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
+    if (arow < nqc) {
+      const float4* src = (const float4*)(qh + (size_t)arow * D + 16 * ks + 8 * h);
+      x0 = src[0];
+      x1 = src[1];
+    }
+    split_hilo(x0, x1, qhi[ks], qlo[ks]);
+  }
+  float* Sh = S + (size_t)bh * nqc * nkc;
+  for (int j = 0; j < 4; ++j) {
+    if (b0 + 32 * j >= nkc) break;  // uniform
+    const int bcol = b0 + 32 * j + l32;
+    bf16x8 khi[KS], klo[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
+      if (bcol < nkc) {
+        const float4* src = (const float4*)(kh + (size_t)bcol * D + 16 * ks + 8 * h);
+        x0 = src[0];
+        x1 = src[1];
+      }
+      split_hilo(x0, x1, khi[ks], klo[ks]);
+    }
+    f32x16 acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qlo[ks], khi[ks], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qhi[ks], klo[ks], acc, 0, 0, 0);
+    }
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qhi[ks], khi[ks], acc, 0, 0, 0);
+    if (bcol < nkc) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int a = a0 + 32 * w + 8 * (r >> 2) + 4 * h + (r & 3);
+        if (a < nqc) Sh[(size_t)a * nkc + bcol] = acc[r];
+      }
+    }
+  }
+}
+
+// Scores of every (query cluster, key cluster) pair of every head.
+hipError_t launch_scores(const Prob& P, const float* cq, const float* ck, float* scores,
+                         hipStream_t st) {
+  const bool aligned = (((uintptr_t)cq | (uintptr_t)ck) & 15) == 0;
+  if (P.dtype == CA_BF16 && (P.d == 64 || P.d == 128) && aligned) {
+    const dim3 grid((P.nkc + 127) / 128, (P.nqc + 127) / 128, P.BH);
+    if (P.d == 64)
+      hipLaunchKernelGGL(scores_mfma_kernel<64>, grid, dim3(256), 0, st, cq, ck, P.nqc, P.nkc,
+                         scores);
+    else
+      hipLaunchKernelGGL(scores_mfma_kernel<128>, grid, dim3(256), 0, st, cq, ck, P.nqc, P.nkc,
+                         scores);
+  } else {
+    const dim3 grid((P.nkc + kTileS - 1) / kTileS, (P.nqc + kTileS - 1) / kTileS, P.BH);
+    hipLaunchKernelGGL(scores_kernel, grid, dim3(256), 0, st, cq, ck, P.nqc, P.nkc, P.d, scores);
+  }
+  return hipGetLastError();
 }
 
 // Key that orders scores descending: the largest score gets the smallest key.
@@ -132,7 +230,9 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ S, 
   }
   lo = block_min_max(lo, false, sh_f);
   hi = block_min_max(hi, true, sh_f);
-  const float inv = hi > lo ? (float)kTopBins / (hi - lo) : 0.f;
+  // (a range too narrow for a finite bin scale puts every score in bin 0)
+  const float inv0 = (float)kTopBins / (hi - lo);
+  const float inv = hi > lo && inv0 < INFINITY ? inv0 : 0.f;
   auto bin_of = [&](float v) {
     const float t = (hi - v) * inv;  // 0 for the largest score
     return t < (float)kTopBins ? (t > 0.f ? (int)t : 0) : kTopBins - 1;
@@ -246,6 +346,204 @@ __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ S, 
       ++er;
     }
     if (take && pos < k) out[pos++] = b;
+  }
+}
+
+// Exact top-k of rows of at most 64 * VPL scores, one row per wavefront, the
+// row held in registers (lane l owns the VPL consecutive scores from VPL * l),
+// so no block barrier is needed. The same selection as topk_kernel: linear
+// bins over [min, max] locate the bin holding the k-th largest score; that
+// bin's scores are compacted into a per-wave LDS list (ballot positions) and
+// an 8-bit radix select finds the k-th key among them (or among the bin's
+// scores in registers when more than kWaveCand fall in it); the first rank+1
+// keys equal to it in index order are kept.
+constexpr int kWaveBins = 1024;
+constexpr int kWaveCand = 512;
+
+__device__ __forceinline__ void wave_lds_sync() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+}
+
+__device__ __forceinline__ int wave_incl_scan(int x, int lane) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
+template <int VPL>
+__global__ __launch_bounds__(256) void topk_wave_kernel(const float* __restrict__ S, int nkc, int k,
+                                                        int nrows, int vec4,
+                                                        int32_t* __restrict__ lists) {
+  __shared__ int bins_all[4][kWaveBins];
+  __shared__ int hist_all[4][256];
+  __shared__ uint32_t ckey_all[4][kWaveCand];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const size_t row = (size_t)blockIdx.x * 4 + w;
+  if (row >= (size_t)nrows) return;  // whole wavefront; no block barrier follows
+  int* bins = bins_all[w];
+  int* hist = hist_all[w];
+  uint32_t* ckey = ckey_all[w];
+  const float* s = S + row * nkc;
+  const int b0 = VPL * lane;
+  float v[VPL];
+  if (vec4 && VPL >= 4) {
+#pragma unroll
+    for (int j = 0; j < VPL; j += 4) {
+      float4 x = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+      if (b0 + j < nkc) x = *(const float4*)(s + b0 + j);  // nkc % 4 == 0: whole float4
+      v[j] = x.x;
+      v[j + 1] = x.y;
+      v[j + 2] = x.z;
+      v[j + 3] = x.w;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) v[j] = b0 + j < nkc ? s[b0 + j] : -INFINITY;
+  }
+  // Positions past the row hold -inf: they sort after every score (last bin,
+  // largest key, and indices after the row's), so with k <= nkc they are never
+  // taken; only the range below has to leave them out.
+  float lo = INFINITY, hi = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < VPL; ++j)
+    if (b0 + j < nkc) {
+      lo = fminf(lo, v[j]);
+      hi = fmaxf(hi, v[j]);
+    }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    lo = fminf(lo, __shfl_xor(lo, o, 64));
+    hi = fmaxf(hi, __shfl_xor(hi, o, 64));
+  }
+  const float inv0 = (float)kWaveBins / (hi - lo);
+  const float inv = hi > lo && inv0 < INFINITY ? inv0 : 0.f;  // too narrow: one bin
+  auto bin_of = [&](float x) {
+    const float t = (hi - x) * inv;  // 0 for the largest score
+    return t < (float)kWaveBins ? (t > 0.f ? (int)t : 0) : kWaveBins - 1;
+  };
+  for (int i = lane; i < kWaveBins; i += 64) bins[i] = 0;
+  wave_lds_sync();
+#pragma unroll
+  for (int j = 0; j < VPL; ++j) atomicAdd(&bins[bin_of(v[j])], 1);
+  wave_lds_sync();
+  // Each pass recomputes bins and keys from the scores: keeping them from an
+  // earlier pass would hold two more registers per score.
+  auto fence_row = [&]() {
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) asm volatile("" : "+v"(v[j]));
+  };
+  fence_row();
+  // the bin holding rank k - 1 (bins in descending score order)
+  int B, rank;
+  {
+    constexpr int PB = kWaveBins / 64;
+    int sum = 0;
+#pragma unroll
+    for (int i = 0; i < PB; ++i) sum += bins[PB * lane + i];
+    const int incl = wave_incl_scan(sum, lane);
+    const bool mine = k - 1 >= incl - sum && k - 1 < incl;
+    const int owner = __ffsll((long long)__ballot(mine)) - 1;
+    int fb = 0, fr = 0;
+    if (mine) {
+      int acc = incl - sum;
+      for (int i = 0; i < PB; ++i) {
+        const int c = bins[PB * lane + i];
+        if (k - 1 < acc + c) {
+          fb = PB * lane + i;
+          fr = k - 1 - acc;
+          break;
+        }
+        acc += c;
+      }
+    }
+    B = __builtin_amdgcn_readlane(fb, owner);
+    rank = __builtin_amdgcn_readlane(fr, owner);
+  }
+  // candidates: the keys of bin B
+  int ncand = 0;
+#pragma unroll
+  for (int j = 0; j < VPL; ++j) {
+    const bool hit = bin_of(v[j]) == B;
+    const uint64_t m = __ballot(hit);
+    const int pos = ncand + (int)__popcll(m & ((1ull << lane) - 1ull));
+    if (hit && pos < kWaveCand) ckey[pos] = desc_key(v[j]);
+    ncand += (int)__popcll(m);
+  }
+  wave_lds_sync();
+  fence_row();
+  const bool in_lds = ncand <= kWaveCand;
+  uint32_t prefix = 0;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    const uint32_t hmask = pass == 0 ? 0u : (0xFFFFFFFFu << (shift + 8));
+    for (int i = lane; i < 256; i += 64) hist[i] = 0;
+    wave_lds_sync();
+    if (in_lds) {
+      for (int i = lane; i < ncand; i += 64) {
+        const uint32_t u = ckey[i];
+        if ((u & hmask) == prefix) atomicAdd(&hist[(u >> shift) & 255], 1);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < VPL; ++j)
+        if (bin_of(v[j]) == B) {
+          const uint32_t u = desc_key(v[j]);
+          if ((u & hmask) == prefix) atomicAdd(&hist[(u >> shift) & 255], 1);
+        }
+    }
+    wave_lds_sync();
+    int c[4], sum = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      c[i] = hist[4 * lane + i];
+      sum += c[i];
+    }
+    const int incl = wave_incl_scan(sum, lane);
+    const bool mine = rank >= incl - sum && rank < incl;
+    const int owner = __ffsll((long long)__ballot(mine)) - 1;
+    int fd = 0, fr = 0;
+    if (mine) {
+      int acc = incl - sum;
+      for (int i = 0; i < 4; ++i) {
+        if (rank < acc + c[i]) {
+          fd = 4 * lane + i;
+          fr = rank - acc;
+          break;
+        }
+        acc += c[i];
+      }
+    }
+    prefix |= (uint32_t)__builtin_amdgcn_readlane(fd, owner) << shift;
+    rank = __builtin_amdgcn_readlane(fr, owner);
+    wave_lds_sync();  // hist is cleared again by the next pass
+    fence_row();
+  }
+  // keys below the threshold, and the first rank + 1 equal ones in index order
+  fence_row();
+  const uint32_t thr = prefix;
+  const int need_eq = rank + 1;
+  int less = 0, eq = 0;
+#pragma unroll
+  for (int j = 0; j < VPL; ++j) {
+    const uint32_t u = desc_key(v[j]);
+    less += u < thr;
+    eq += u == thr;
+  }
+  fence_row();
+  const int eq_before = wave_incl_scan(eq, lane) - eq;
+  const int sel = less + min(max(need_eq - eq_before, 0), eq);
+  int pos = wave_incl_scan(sel, lane) - sel;
+  int er = eq_before;
+  int32_t* out = lists + row * k;
+#pragma unroll
+  for (int j = 0; j < VPL; ++j) {
+    const uint32_t u = desc_key(v[j]);
+    bool take = u < thr;
+    if (u == thr) take = er++ < need_eq;
+    if (take && pos < k) out[pos++] = b0 + j;
   }
 }
 
@@ -427,9 +725,7 @@ hipError_t launch_select(const Prob& P, const float* cq, const float* ck, const 
                          float* scores, int k, int32_t* lists, hipStream_t st) {
   const float* S = scores_in;
   if (!S) {
-    dim3 grid((P.nkc + kTileS - 1) / kTileS, (P.nqc + kTileS - 1) / kTileS, P.BH);
-    hipLaunchKernelGGL(scores_kernel, grid, dim3(256), 0, st, cq, ck, P.nqc, P.nkc, P.d, scores);
-    hipError_t e = hipGetLastError();
+    hipError_t e = launch_scores(P, cq, ck, scores, st);
     if (e != hipSuccess) return e;
     S = scores;
   } else if (scores && scores != scores_in) {
@@ -437,8 +733,26 @@ hipError_t launch_select(const Prob& P, const float* cq, const float* ck, const 
                                   hipMemcpyDeviceToDevice, st);
     if (e != hipSuccess) return e;
   }
+  const size_t nrows = (size_t)P.BH * P.nqc;
+  if (P.nkc <= 64 * 128) {
+    const int vec4 = (P.nkc % 4 == 0) && (((uintptr_t)S & 15) == 0);
+    const dim3 grid((unsigned)((nrows + 3) / 4));
+#define CA_TOPK_WAVE(V)                                                                        \
+  if (P.nkc <= 64 * V) {                                                                       \
+    hipLaunchKernelGGL(topk_wave_kernel<V>, grid, dim3(256), 0, st, S, P.nkc, k, (int)nrows, \
+                       vec4, lists);                                                           \
+    return hipGetLastError();                                                                  \
+  }
+    CA_TOPK_WAVE(4)
+    CA_TOPK_WAVE(8)
+    CA_TOPK_WAVE(16)
+    CA_TOPK_WAVE(32)
+    CA_TOPK_WAVE(64)
+    CA_TOPK_WAVE(128)
+#undef CA_TOPK_WAVE
+  }
   const int staged = P.nkc <= kTopStage;
-  hipLaunchKernelGGL(topk_kernel, dim3((unsigned)((size_t)P.BH * P.nqc)), dim3(256),
+  hipLaunchKernelGGL(topk_kernel, dim3((unsigned)nrows), dim3(256),
                      staged ? (size_t)P.nkc * sizeof(float) : 0, st, S, P.nkc, k, lists, staged);
   return hipGetLastError();
 }
@@ -453,9 +767,7 @@ hipError_t launch_select_hist(const Prob& P, const float* cq, const float* ck,
                               int32_t* lens, hipStream_t st) {
   const float* S = scores_in;
   if (!S) {
-    dim3 grid((P.nkc + kTileS - 1) / kTileS, (P.nqc + kTileS - 1) / kTileS, P.BH);
-    hipLaunchKernelGGL(scores_kernel, grid, dim3(256), 0, st, cq, ck, P.nqc, P.nkc, P.d, scores);
-    hipError_t e = hipGetLastError();
+    hipError_t e = launch_scores(P, cq, ck, scores, st);
     if (e != hipSuccess) return e;
     S = scores;
   } else if (scores && scores != scores_in) {

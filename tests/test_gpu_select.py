@@ -1,5 +1,7 @@
-"""GPU parity of ca_select: centroid scores within fp32 rounding of the oracle,
-and lists bit-exact against the oracle's top-k of the very same scores."""
+"""GPU parity of ca_select: centroid scores within 1e-5 of the oracle's (fp32
+rounding, or the three-term bf16 split on the matrix cores for bf16 problems
+with d = 64 or 128), and lists bit-exact against the oracle's top-k of the
+very same scores."""
 import numpy as np
 import pytest
 
@@ -50,6 +52,34 @@ def test_topk_with_ties_given_scores(k):
     L = lists.cpu().numpy()
     for h in range(H):
         assert np.array_equal(L[h], ref.topk(S[h].astype(np.float64), k))
+
+
+@pytest.mark.parametrize("nkc,k", [(5000, 64), (8192, 820), (8192, 64), (1001, 500), (1000, 1),
+                                   (9000, 64), (257, 257)])
+def test_topk_long_rows_with_ties(nkc, k):
+    """Rows of up to 8192 scores (one row per wavefront) and beyond (one per
+    workgroup), with heavy ties (so the threshold's bin overflows the
+    candidate list), a constant row, a range a few subnormals wide, and row
+    lengths that are not multiples of four: lists equal the oracle's."""
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    G.flush(f"long-row top-k nkc={nkc} k={k}")
+    rng = np.random.default_rng(nkc + k)
+    H, nqc = 2, 6
+    S = rng.integers(-3, 4, size=(H, nqc, nkc)).astype(np.float32)
+    S[0, 1] = rng.standard_normal(nkc).astype(np.float32)
+    S[0, 2] = 2.5
+    S[1, 0] = (np.arange(nkc) % 7).astype(np.float32) * np.float32(1e-44)
+    S[1, 1] = rng.standard_normal(nkc).astype(np.float32) * 1e3
+    S[1, 1, ::97] = -1e30  # far outliers stretch the linear bins
+    p = ca.Problem(1, H, nqc * 16, nkc * 16, 8, 16, 16, torch.float32)
+    lists, _ = ca.select(p, None, None, k, scores_in=G.dev(S))
+    torch.cuda.synchronize()
+    L = lists.cpu().numpy()
+    for h in range(H):
+        for a in range(nqc):
+            assert np.array_equal(L[h, a], ref.topk(S[h, a:a + 1].astype(np.float64), k)[0]), (h, a)
 
 
 HIST_CASES = [
