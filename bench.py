@@ -227,6 +227,92 @@ def latency_sweep(args):
         torch.cuda.empty_cache()
 
 
+# Rows of the per-configuration table: (config, cluster size, keep fraction,
+# compensation, distinct heads generated). The generated heads are repeated up
+# to the configuration's head count (heads are independent units of the
+# method, so the work and its shape are those of the full layer; generating
+# every head on the host would take minutes).
+CONFIG_ROWS = (
+    [(1, 64, 0.25, True, 1), (1, 64, 1.0, True, 1), (2, 128, 0.125, True, 8),
+     (3, 128, 0.0625, True, 2), (3, 128, 0.25, True, 2), (4, 64, 0.25, True, 4)]
+    + [(5, c, keep, comp, 4) for c in (64, 128) for keep in (0.25, 0.125, 0.0625)
+       for comp in (True, False)])
+
+
+def config_table(args):
+    """One JSON line per row of CONFIG_ROWS: the whole layer (metric
+    transform, exact top-k) timed with HIP events, mean over the timed steps
+    after the warm-ups; dense-equivalent TFLOP/s; the attention kernel's
+    TFLOP/s on the computed interactions (4 d c_q c_k per query-cluster /
+    selected-key-cluster pair) against the bf16 MFMA peak."""
+    import torch
+    import paper_2608_26965_amd as ca
+    from synth import CONFIGS, make_config
+    dev = torch.device("cuda:0")
+    steps, warmup = max(3, min(args.steps, 10)), max(1, min(args.warmup, 3))
+    cache = {}
+    for cid, c, keep, comp, gen in CONFIG_ROWS:
+        cfg = CONFIGS[cid]
+        if cid not in cache:
+            cache.clear()
+            torch.cuda.empty_cache()
+            Qh, Kh, Vh = make_config(cid, heads=list(range(gen)))
+            rep = -(-cfg.heads // gen)
+            dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+            cache[cid] = tuple(torch.from_numpy(x).to(dev).to(dt).repeat(rep, 1, 1)[:cfg.heads][None]
+                               .contiguous() for x in (Qh, Kh, Vh))
+        q, k, v = cache[cid]
+        H, n, d = q.shape[1:]
+        p = ca.Problem(1, H, n, n, d, c, c, q.dtype, "metric", "bhnd")
+        keep_k = ca.keep_to_k(keep, p.nkc)
+        ws = ca.workspace(p, dev, keep_k)
+        out = torch.empty(p.shape(n), dtype=q.dtype, device=dev)
+
+        def step(ev=None):
+            if ev:
+                ev[0].record()
+            r = ca.cluster(p, q, k, v, ws=ws)
+            if ev:
+                ev[1].record()
+            lists, _ = ca.select(p, r["cent_q"], r["cent_k"], keep_k, ws=ws)
+            if ev:
+                ev[2].record()
+            op, lse = ca.block_sparse_attn(p, r["qp"], r["kp"], r["vp"], r["count_k"], lists,
+                                           keep_k)
+            if ev:
+                ev[3].record()
+            ca.compensate(p, r["qp"], r["cent_k"], r["cent_v"], r["count_k"], lists, keep_k, op,
+                          lse, r["perm_q"], enable=comp, out=out, ws=ws)
+            if ev:
+                ev[4].record()
+
+        for _ in range(warmup):
+            step()
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            step(evs[i])
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / steps
+        calls = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(4)] for e in evs]).mean(0)
+        f_dense = 4.0 * H * n * n * d
+        f_attn = 4.0 * d * c * c * keep_k * p.nqc * H
+        attn_tf = f_attn / (calls[2] * 1e-3) / 1e12
+        print(json.dumps({"table": "configs", "config": cfg.name, "heads": H, "n": n, "d": d,
+                          "dtype": cfg.dtype, "c": c, "keep": keep, "kept_clusters": keep_k,
+                          "key_clusters": p.nkc, "compensation": comp,
+                          "distinct_heads_generated": gen, "ms_per_layer": round(ms, 4),
+                          "cluster_ms": round(calls[0], 4), "select_ms": round(calls[1], 4),
+                          "attention_ms": round(calls[2], 4), "compensation_ms": round(calls[3], 4),
+                          "dense_equiv_tflops": round(f_dense / (ms * 1e-3) / 1e12, 1),
+                          "attention_tflops": round(attn_tf, 1),
+                          "attention_mfma_frac": (round(attn_tf / PEAK_BF16_TFLOPS, 4)
+                                                  if cfg.dtype == "bf16" else None)}),
+              flush=True)
+        del ws, out
+
+
 def copy_calibration():
     """A plain device copy of 256 MiB (fp32), three launches."""
     import torch
@@ -248,6 +334,9 @@ def main():
     ap.add_argument("--sweep", action="store_true",
                     help="latency scaling with the token count instead of the headline run: one "
                          "JSON line per (N, rule), k = 64 clusters or 10%% of the key clusters")
+    ap.add_argument("--configs", action="store_true",
+                    help="every workload configuration (cluster sizes, keep fractions, "
+                         "compensation on/off) instead of the headline run: one JSON line each")
     ap.add_argument("--no-modes", action="store_true",
                     help="skip the histogram-selection modes timed after the headline run")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -259,6 +348,9 @@ def main():
         return
     if args.sweep:
         latency_sweep(args)
+        return
+    if args.configs:
+        config_table(args)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: ClusterAttention's heads are independent, so a "
