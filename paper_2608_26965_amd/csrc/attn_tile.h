@@ -119,8 +119,9 @@ __device__ __forceinline__ int swz_off(int r, int lc) {
 // Per-lane global byte offsets of a tile copy: wavefront w's instruction i
 // fills LDS bytes [(i*NW + w)*1024, +1024); lane l writes 16 of them, which
 // belong to row r, LDS chunk pc, i.e. to the row's logical chunk
-// pc ^ swz_key(r) in global memory.
-template <int ROWBYTES, int NINSTR, int NW>
+// pc ^ swz_key(r) in global memory, where rows are GROWBYTES apart (a tile
+// may be a column range of wider rows).
+template <int ROWBYTES, int NINSTR, int NW, int GROWBYTES = ROWBYTES>
 struct TileCopy {
   uint32_t off[NINSTR];
   __device__ __forceinline__ TileCopy(int w, int lane) {
@@ -129,7 +130,7 @@ struct TileCopy {
     for (int i = 0; i < NINSTR; ++i) {
       const int g = (i * NW + w) * 64 + lane;
       const int r = g / NCH, pc = g % NCH;
-      off[i] = (uint32_t)(r * ROWBYTES + ((pc ^ swz_key<ROWBYTES>(r)) << 4));
+      off[i] = (uint32_t)(r * GROWBYTES + ((pc ^ swz_key<ROWBYTES>(r)) << 4));
     }
   }
   __device__ __forceinline__ void issue(const void* src, uint32_t lds, int w) const {

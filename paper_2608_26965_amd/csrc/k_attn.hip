@@ -30,32 +30,40 @@ __device__ __forceinline__ int xcd_remap(int wg, int total) {
   return xcd < rem ? xcd * (per + 1) + loc : rem * (per + 1) + (xcd - rem) * per + loc;
 }
 
-// Waves per SIMD the bf16 kernel is compiled for: two when the double-buffered
-// tiles of two workgroups fit in LDS (so MFMA of one wave overlaps the softmax
-// of another), else one.
-// Workgroups per CU the bf16 kernel is compiled for: as many double-buffered
-// tile pairs as fit in LDS (so the MFMA of one wave overlaps the softmax of
-// another), capped at two waves per SIMD.
+// Keys per LDS stage: a whole key cluster, except at d = 128 with query and
+// key clusters of 128, where a stage holds half a key cluster (64 KB for the
+// two stages instead of 128 KB), so that two workgroups share a CU.
 template <int D, int CQ, int CK>
-constexpr int attn_blocks_per_cu() {
-  constexpr int by_lds = (160 * 1024) / (8 * D * CK);
+constexpr int attn_stage_keys() {
+  return D == 128 && CQ == 128 && CK == 128 ? 64 : CK;
+}
+
+// Waves per SIMD the bf16 kernel is compiled for (the second launch bound):
+// as many workgroups as their double-buffered stages fit in LDS, capped at two
+// waves per SIMD, so that the MFMA of one wave overlaps the softmax of another.
+template <int D, int CQ, int CK>
+constexpr int attn_waves_per_simd() {
+  constexpr int by_lds = (160 * 1024) / (8 * D * attn_stage_keys<D, CQ, CK>());
   constexpr int by_waves = 8 / (CQ / 32);
-  return by_lds < by_waves ? (by_lds < 1 ? 1 : by_lds) : by_waves;
+  constexpr int blocks = by_lds < by_waves ? (by_lds < 1 ? 1 : by_lds) : by_waves;
+  return blocks * (CQ / 32) / 4 < 1 ? 1 : blocks * (CQ / 32) / 4;
 }
 
 template <int D, int CQ, int CK>
-__global__ __launch_bounds__(CQ * 2, (attn_blocks_per_cu<D, CQ, CK>())) void attn_bf16_kernel(
+__global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void attn_bf16_kernel(
     const bf16* __restrict__ qp, const bf16* __restrict__ kp, const bf16* __restrict__ vp,
     const int32_t* __restrict__ count_k, const int32_t* __restrict__ lists,
     const int32_t* __restrict__ lens, int nqc, int nkc, int k, float sl2, bf16* __restrict__ op,
     float* __restrict__ lse, int total, const int32_t* __restrict__ sched, int cap) {
   constexpr int NW = CQ / 32;
-  constexpr int MT = CK / 32;
+  constexpr int HK = attn_stage_keys<D, CQ, CK>();  // keys per stage
+  constexpr int SUB = CK / HK;                      // stages per key cluster
+  constexpr int MT = HK / 32;
   constexpr int KS = D / 16;
   constexpr int DT = D / 32;
   constexpr int KROW = 2 * D;   // bytes per K row
-  constexpr int VROW = 2 * CK;  // bytes per V^T row
-  constexpr int KBYTES = CK * KROW, VBYTES = D * VROW;
+  constexpr int VROW = 2 * HK;  // bytes per V^T row in LDS (2 * CK in HBM)
+  constexpr int KBYTES = HK * KROW, VBYTES = D * VROW;
   constexpr int STAGE = KBYTES + VBYTES;
   constexpr int KLD = KBYTES / 1024 / NW;  // direct-to-LDS instructions per wave
   constexpr int VLD = VBYTES / 1024 / NW;
@@ -94,11 +102,13 @@ __global__ __launch_bounds__(CQ * 2, (attn_blocks_per_cu<D, CQ, CK>())) void att
     return b < 0 ? 0 : (b >= nkc ? nkc - 1 : b);
   };
   const TileCopy<KROW, KLD, NW> kcopy(w, lane);
-  const TileCopy<VROW, VLD, NW> vcopy(w, lane);
+  const TileCopy<VROW, VLD, NW, 2 * CK> vcopy(w, lane);
   const uint32_t lds0 = lds_addr(smem);
-  auto issue = [&](int b, int stage) {
-    const bf16* kt = kp + ((size_t)bh * nk_pad + (size_t)b * CK) * D;
-    const bf16* vt = vp + ((size_t)bh * nkc + b) * (size_t)D * CK;
+  // stage g holds keys [HK (g % SUB), HK (g % SUB) + HK) of list entry g / SUB
+  auto issue = [&](int g, int stage) {
+    const int b = tile_id(g / SUB), s = g % SUB;
+    const bf16* kt = kp + ((size_t)bh * nk_pad + (size_t)b * CK + (size_t)s * HK) * D;
+    const bf16* vt = vp + ((size_t)bh * nkc + b) * (size_t)D * CK + (size_t)s * HK;
     kcopy.issue(kt, lds0 + stage * STAGE, w);
     vcopy.issue(vt, lds0 + stage * STAGE + KBYTES, w);
   };
@@ -122,19 +132,22 @@ __global__ __launch_bounds__(CQ * 2, (attn_blocks_per_cu<D, CQ, CK>())) void att
     for (int r = 0; r < 16; ++r) oacc[dt][r] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
-  // Tile t sits in stage t % 2. Its copy was issued at the start of tile t-1,
-  // right after the barrier that every wavefront passes only once done with
-  // tile t-2 (which used the same stage), so one barrier per tile suffices
-  // and each copy has a whole tile of compute to land.
-  auto body = [&](auto stage_tag, int t) {
+  // Stage g (of ng = nt * SUB) sits in LDS stage g % 2. Its copy was issued
+  // at the start of stage g-1, right after the barrier that every wavefront
+  // passes only once done with stage g-2 (which used the same buffer), so one
+  // barrier per stage suffices and each copy has a whole stage of compute to
+  // land.
+  const int ng = nt * SUB;
+  auto body = [&](auto stage_tag, int g) {
     constexpr int S = decltype(stage_tag)::value;
     wait_vmcnt<0>();
     wait_lgkm();
     raw_barrier();
-    if (t + 1 < nt) issue(tile_id(t + 1), S ^ 1);
+    if (g + 1 < ng) issue(g + 1, S ^ 1);
     const char* ks = smem + S * STAGE;
     const char* vs = ks + KBYTES;
-    const int cnt = cnth[tile_id(t)];
+    // keys of this stage past the cluster's count are padding
+    const int cnt = cnth[tile_id(g / SUB)] - (g % SUB) * HK;
 
     f32x16 sacc[MT];
 #pragma unroll
@@ -147,7 +160,7 @@ __global__ __launch_bounds__(CQ * 2, (attn_blocks_per_cu<D, CQ, CK>())) void att
         sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qreg[kk], sacc[mt], 0, 0, 0);
       }
     }
-    if (cnt < CK) {
+    if (cnt < HK) {
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -207,10 +220,10 @@ __global__ __launch_bounds__(CQ * 2, (attn_blocks_per_cu<D, CQ, CK>())) void att
         }
   };
 
-  issue(tile_id(0), 0);
-  for (int t = 0; t < nt; t += 2) {
-    body(std::integral_constant<int, 0>{}, t);
-    if (t + 1 < nt) body(std::integral_constant<int, 1>{}, t + 1);
+  issue(0, 0);
+  for (int g = 0; g < ng; g += 2) {
+    body(std::integral_constant<int, 0>{}, g);
+    if (g + 1 < ng) body(std::integral_constant<int, 1>{}, g + 1);
   }
 
   const float l_tot = l_run + wave_xor32(l_run);

@@ -98,18 +98,20 @@ __global__ __launch_bounds__(256) void comp_stage_kernel(const float* __restrict
   }
 }
 
-// Workgroups per CU: as many as the LDS (two tile stages and the selection
-// mask) allows, capped at two waves per SIMD.
+// Waves per SIMD (the second launch bound): as many workgroups as the LDS
+// (two tile stages and the selection mask) allows, capped at two waves per
+// SIMD.
 template <int D, int CQ>
-constexpr int comp_blocks_per_cu() {
+constexpr int comp_waves_per_simd() {
   constexpr int lds = 2 * (kCompTile * (4 * D + 4)) + kMaskWords * 4;
   constexpr int by_lds = (160 * 1024) / lds;
   constexpr int by_waves = 8 / (CQ / 32);
-  return by_lds < by_waves ? (by_lds < 1 ? 1 : by_lds) : by_waves;
+  constexpr int blocks = by_lds < by_waves ? (by_lds < 1 ? 1 : by_lds) : by_waves;
+  return blocks * (CQ / 32) / 4 < 1 ? 1 : blocks * (CQ / 32) / 4;
 }
 
 template <int D, int CQ>
-__global__ __launch_bounds__(CQ * 2, (comp_blocks_per_cu<D, CQ>())) void comp_bf16_kernel(
+__global__ __launch_bounds__(CQ * 2, (comp_waves_per_simd<D, CQ>())) void comp_bf16_kernel(
     const bf16* __restrict__ qp, const char* __restrict__ tiles,
     const int32_t* __restrict__ lists, const int32_t* __restrict__ lens, int nq, int H, int nqc,
     int nkc, int ntile, int k, float sl2, int enable, const bf16* __restrict__ op,
