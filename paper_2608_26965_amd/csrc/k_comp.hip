@@ -98,12 +98,19 @@ __global__ __launch_bounds__(256) void comp_stage_kernel(const float* __restrict
   }
 }
 
+// Centroids per LDS stage: a whole tile of 128 at d = 64; half a tile at
+// d = 128, so that two stages and the mask take 74 KB instead of 140 KB and
+// two workgroups share a CU.
+template <int D>
+constexpr int comp_stage_cents() {
+  return D == 128 ? kCompTile / 2 : kCompTile;
+}
+
 // Waves per SIMD (the second launch bound): as many workgroups as the LDS
-// (two tile stages and the selection mask) allows, capped at two waves per
-// SIMD.
+// (two stages and the selection mask) allows, capped at two waves per SIMD.
 template <int D, int CQ>
 constexpr int comp_waves_per_simd() {
-  constexpr int lds = 2 * (kCompTile * (4 * D + 4)) + kMaskWords * 4;
+  constexpr int lds = 2 * (comp_stage_cents<D>() * (4 * D + 4)) + kMaskWords * 4;
   constexpr int by_lds = (160 * 1024) / lds;
   constexpr int by_waves = 8 / (CQ / 32);
   constexpr int blocks = by_lds < by_waves ? (by_lds < 1 ? 1 : by_lds) : by_waves;
@@ -120,14 +127,18 @@ __global__ __launch_bounds__(CQ * 2, (comp_waves_per_simd<D, CQ>())) void comp_b
     int layout, int total) {
   constexpr int NW = CQ / 32;
   constexpr int T = NW * 64;
-  constexpr int CT = kCompTile;  // centroids per tile
-  constexpr int MT = CT / 32;
+  constexpr int CT = kCompTile;               // centroids per staged tile
+  constexpr int HC = comp_stage_cents<D>();   // centroids per LDS stage
+  constexpr int SUB = CT / HC;                // stages per tile
+  constexpr int MT = HC / 32;
   constexpr int KS = D / 16;
   constexpr int DT = D / 32;
   constexpr int KROW = 2 * D;   // bytes per centroid key row
-  constexpr int VROW = 2 * CT;  // bytes per transposed value row
-  constexpr int KBYTES = CT * KROW, VBYTES = D * VROW, BBYTES = CT * 4;
+  constexpr int VROW = 2 * HC;  // bytes per transposed value row in LDS (2 * CT in the tile)
+  constexpr int KBYTES = HC * KROW, VBYTES = D * VROW, BBYTES = HC * 4;
   constexpr int STAGE = KBYTES + VBYTES + BBYTES;
+  constexpr int TKB = CT * KROW, TVB = D * 2 * CT;  // a staged tile: K, V^T, bias
+  constexpr int TILE = TKB + TVB + CT * 4;
   constexpr int KLD = KBYTES / 1024 / NW;  // direct-to-LDS instructions per wave
   constexpr int VLD = VBYTES / 1024 / NW;
   constexpr int BLANES = BBYTES / 16 / NW;  // lanes of each wave copying the bias row
@@ -164,18 +175,21 @@ __global__ __launch_bounds__(CQ * 2, (comp_waves_per_simd<D, CQ>())) void comp_b
   // this query cluster's list length (uniform; clamped for memory safety)
   const int nsel = lens ? min(max(lens[(size_t)bh * nqc + a], 1), k) : k;
   const bool do_comp = enable && nsel < nkc;
-  const char* th = tiles + (size_t)bh * ntile * STAGE;
+  const char* th = tiles + (size_t)bh * ntile * TILE;
   const TileCopy<KROW, KLD, NW> kcopy(w, lane);
-  const TileCopy<VROW, VLD, NW> vcopy(w, lane);
+  const TileCopy<VROW, VLD, NW, 2 * CT> vcopy(w, lane);
   const uint32_t lds0 = lds_addr(smem);
-  auto issue = [&](int t, int stage) {
-    const char* src = th + (size_t)t * STAGE;
+  const int ng = ntile * SUB;  // stages
+  // stage g holds centroids [HC (g % SUB), + HC) of tile g / SUB
+  auto issue = [&](int g, int stage) {
+    const int s = g % SUB;
+    const char* src = th + (size_t)(g / SUB) * TILE;
     const uint32_t dst = lds0 + stage * STAGE;
-    kcopy.issue(src, dst, w);
-    vcopy.issue(src + KBYTES, dst + KBYTES, w);
+    kcopy.issue(src + s * KBYTES, dst, w);
+    vcopy.issue(src + TKB + s * VROW, dst + KBYTES, w);
     const uint32_t boff = (uint32_t)(w * BLANES * 16);
     const uint32_t bdst = __builtin_amdgcn_readfirstlane(dst + KBYTES + VBYTES + boff);
-    if (lane < BLANES) lds_dma16(src + KBYTES + VBYTES, boff + 16 * lane, bdst);
+    if (lane < BLANES) lds_dma16(src + TKB + TVB + s * BBYTES, boff + 16 * lane, bdst);
   };
   bf16x8 qreg[KS];
   if (do_comp) {
@@ -183,7 +197,7 @@ __global__ __launch_bounds__(CQ * 2, (comp_waves_per_simd<D, CQ>())) void comp_b
     // The first two tiles are copied before the selection is known (a tile
     // whose centroids are all selected is then skipped, not un-copied).
     issue(0, 0);
-    if (ntile > 1) issue(1, 1);
+    if (ng > 1) issue(1, 1);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
       qreg[ks] = *(const bf16x8*)(qp + qrow * D + 16 * ks + 8 * h);
@@ -212,11 +226,11 @@ __global__ __launch_bounds__(CQ * 2, (comp_waves_per_simd<D, CQ>())) void comp_b
     wait_lgkm();
     raw_barrier();  // selmask complete
 
-    // A tile is live if it holds at least one unselected centroid.
-    auto tile_live = [&](int t) {
+    // A stage is live if it holds at least one unselected centroid.
+    auto tile_live = [&](int g) {
       int any = 0;
-      const int e0 = t * (CT / 32);
-      for (int e = e0; e < e0 + CT / 32 && e < nwords; ++e) {
+      const int e0 = g * (HC / 32);
+      for (int e = e0; e < e0 + HC / 32 && e < nwords; ++e) {
         const uint32_t wmask = e == nwords - 1 && (nkc & 31) ? (1u << (nkc & 31)) - 1u : ~0u;
         any |= (~selmask[e] & wmask) != 0u;
       }
@@ -234,20 +248,20 @@ __global__ __launch_bounds__(CQ * 2, (comp_waves_per_simd<D, CQ>())) void comp_b
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2) voff[mt][s2] = swz_off<VROW>(l32, 4 * mt + 2 * s2 + h);
 
-    auto body = [&](auto stage_tag, int t) {
+    auto body = [&](auto stage_tag, int g) {
       constexpr int S = decltype(stage_tag)::value;
-      if (t + 1 < ntile)
+      if (g + 1 < ng)
         wait_vmcnt<NL>();
       else
         wait_vmcnt<0>();
       raw_barrier();
-      if (tile_live(t)) {
+      if (tile_live(g)) {
         const char* ks = smem + S * STAGE;
         const char* vs = ks + KBYTES;
         float* bias = (float*)(smem + S * STAGE + KBYTES + VBYTES);
         // Selected clusters are covered by the sparse part: drop them here.
-        if (tid < CT) {
-          const int b = t * CT + tid;
+        if (tid < HC) {
+          const int b = g * HC + tid;
           if (b < nkc && ((selmask[b >> 5] >> (b & 31)) & 1u)) bias[tid] = -INFINITY;
         }
         f32x16 sacc[MT];
@@ -324,12 +338,12 @@ __global__ __launch_bounds__(CQ * 2, (comp_waves_per_simd<D, CQ>())) void comp_b
       }
       wait_lgkm();
       raw_barrier();  // every wave is done with this stage
-      if (t + 2 < ntile) issue(t + 2, S);
+      if (g + 2 < ng) issue(g + 2, S);
     };
 
-    for (int t = 0; t < ntile; t += 2) {
-      body(std::integral_constant<int, 0>{}, t);
-      if (t + 1 < ntile) body(std::integral_constant<int, 1>{}, t + 1);
+    for (int g = 0; g < ng; g += 2) {
+      body(std::integral_constant<int, 0>{}, g);
+      if (g + 1 < ng) body(std::integral_constant<int, 1>{}, g + 1);
     }
   }
 
