@@ -955,6 +955,23 @@ __device__ __forceinline__ void project_tile(const char* wl, const bf16x8 (&xop)
   }
 }
 
+// Output tile ot of (X W)^T alone (dims 32 ot.., tokens = lanes).
+template <int D>
+__device__ __forceinline__ void project_tile1(const char* wl, const bf16x8 (&xop)[D / 16], int l32,
+                                              int h, int ot, f32x16& acc) {
+  constexpr int ROWB = 2 * D;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) {
+    const int off = swz_off<ROWB>(32 * ot + l32, 2 * ks + h);
+    const bf16x8 ahi = *(const bf16x8*)(wl + off);
+    const bf16x8 alo = *(const bf16x8*)(wl + D * ROWB + off);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ahi, xop[ks], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(alo, xop[ks], acc, 0, 0, 0);
+  }
+}
+
 // Adds the symmetric Gram tiles (it <= jt) of one wave into red[d][d] (and
 // the mirror), waves in a fixed order.
 template <int D>
@@ -1118,7 +1135,7 @@ __global__ __launch_bounds__(256) void qnorm_mfma_kernel(Ctx C) {
 
 // Y = X T (keys) or inv * (X W_Q) (metric queries), lane = token, fp32 rows.
 template <int D>
-__global__ __launch_bounds__(256) void project_mfma_kernel(Ctx C) {
+__global__ __launch_bounds__(256, 2) void project_mfma_kernel(Ctx C) {
   constexpr int FT = D / 32, KS = D / 16;
   __shared__ __attribute__((aligned(16))) char wl[2 * D * 2 * D];
   const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH;
@@ -1133,19 +1150,21 @@ __global__ __launch_bounds__(256) void project_mfma_kernel(Ctx C) {
   for (int tok0 = r0 + 32 * w; tok0 < r1; tok0 += 128) {
     bf16x8 xop[KS];
     load_xtile<D>((const bf16*)S.x, bh, tok0, r1, S.n, C.H, C.layout, l32, h, xop);
-    f32x16 acc[FT];
-    project_tile<D>(wl, xop, l32, h, acc);
     const int tok = tok0 + l32;
-    if (tok < r1) {
-      const float sc = scale ? C.inv_q[(size_t)bh * S.n + tok] : 1.f;
-      float* yrow = Y + (size_t)tok * D;
-#pragma unroll
-      for (int ot = 0; ot < FT; ++ot)
+    const float sc = scale && tok < r1 ? C.inv_q[(size_t)bh * S.n + tok] : 1.f;
+    float* yrow = Y + (size_t)tok * D;
+    // one 32-column output tile at a time: a single accumulator stays live
+    // (not unrolled, so the operand reads of later tiles are not hoisted)
+#pragma unroll 1
+    for (int ot = 0; ot < FT; ++ot) {
+      f32x16 acc;
+      project_tile1<D>(wl, xop, l32, h, ot, acc);
+      if (tok < r1)
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
           const int col = 32 * ot + 8 * g4 + 4 * h;
-          *(float4*)(yrow + col) = make_float4(acc[ot][4 * g4] * sc, acc[ot][4 * g4 + 1] * sc,
-                                               acc[ot][4 * g4 + 2] * sc, acc[ot][4 * g4 + 3] * sc);
+          *(float4*)(yrow + col) = make_float4(acc[4 * g4] * sc, acc[4 * g4 + 1] * sc,
+                                               acc[4 * g4 + 2] * sc, acc[4 * g4 + 3] * sc);
         }
     }
   }
