@@ -2508,27 +2508,41 @@ __global__ __launch_bounds__(256) void gather_fast_kernel(Ctx C) {
 #pragma unroll
   for (int u = 0; u < EPC; ++u) acc[u] = accv[u] = 0.f;
   T* dst = (T*)S.xp + ((size_t)bh * S.npad + (size_t)a * c) * d;
-  for (int r = r0; r < c; r += rstep) {
-    uint4 chunk = make_uint4(0u, 0u, 0u, 0u), vchunk = chunk;
-    if (r < cnt) {
-      const int i = perm[r];
-      chunk = *(const uint4*)((const T*)S.x + row_off(bh, i, S.n, C.H, d, C.layout) + col * EPC);
-      if (vals)
-        vchunk = *(const uint4*)((const T*)C.v + row_off(bh, i, S.n, C.H, d, C.layout) + col * EPC);
+  // A thread's rows r0, r0 + rstep, ... (at most kGatherRows of them): all
+  // loads are issued before the first is used.
+  constexpr int kGatherRows = 8;
+  for (int rb = r0; rb < c; rb += kGatherRows * rstep) {
+    uint4 chunk[kGatherRows], vchunk[kGatherRows];
+#pragma unroll
+    for (int u = 0; u < kGatherRows; ++u) {
+      const int r = rb + u * rstep;
+      chunk[u] = vchunk[u] = make_uint4(0u, 0u, 0u, 0u);
+      if (r < cnt) {
+        const int i = perm[r];
+        chunk[u] = *(const uint4*)((const T*)S.x + row_off(bh, i, S.n, C.H, d, C.layout) + col * EPC);
+        if (vals)
+          vchunk[u] =
+              *(const uint4*)((const T*)C.v + row_off(bh, i, S.n, C.H, d, C.layout) + col * EPC);
+      }
     }
-    *(uint4*)(dst + (size_t)r * d + col * EPC) = chunk;
-    union {
-      uint4 v;
-      T e[EPC];
-    } cx, cv;
-    cx.v = chunk;
 #pragma unroll
-    for (int u = 0; u < EPC; ++u) acc[u] += (float)cx.e[u];
-    if (vals) {
-      *(uint4*)(vstage + r * d + col * EPC) = vchunk;
-      cv.v = vchunk;
+    for (int u = 0; u < kGatherRows; ++u) {
+      const int r = rb + u * rstep;
+      if (r >= c) break;
+      *(uint4*)(dst + (size_t)r * d + col * EPC) = chunk[u];
+      union {
+        uint4 v;
+        T e[EPC];
+      } cx, cv;
+      cx.v = chunk[u];
 #pragma unroll
-      for (int u = 0; u < EPC; ++u) accv[u] += (float)cv.e[u];
+      for (int e = 0; e < EPC; ++e) acc[e] += (float)cx.e[e];
+      if (vals) {
+        *(uint4*)(vstage + r * d + col * EPC) = vchunk[u];
+        cv.v = vchunk[u];
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) accv[e] += (float)cv.e[e];
+      }
     }
   }
 #pragma unroll
