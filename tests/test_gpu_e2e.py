@@ -224,3 +224,25 @@ def test_tabular_histogram_selection_pipeline(mode):
                               l_s, tau)
         err = np.abs(outh[h][rows] - o).max()
         assert err <= G.TOL["bf16"], f"head {h}: output error {err}"
+
+
+def test_one_million_tokens_one_head():
+    """The largest size of the latency sweep (2^20 tokens, d = 64, bf16,
+    clusters of 128, k = 64 of 8192 key clusters, metric transform,
+    compensation on) on one head: permutations and lists bit-exact, scores
+    and sampled outputs (including the last, ragged query cluster) within the
+    tolerances."""
+    import torch
+    import paper_2608_26965_amd as ca
+    from synth import mixture_inputs
+    from tests import gpu_util as G
+    n, d, c, k = 1 << 20, 64, 128, 64
+    G.flush(f"e2e one head n={n} d={d} c={c} k={k}")
+    Q, K, V = mixture_inputs(77, 1, n, d, "bf16", centres=64, sigma=0.5)
+    p = ca.Problem(1, 1, n, n, d, c, c, torch.bfloat16, "metric")
+    tq, tk, tv = (G.dev(x[None], torch.bfloat16) for x in (Q, K, V))
+    r, lists, scores, out, _ = _pipeline(p, tq, tk, tv, k)
+    torch.cuda.synchronize()
+    err = _check_head(Q[0], K[0], V[0], r, lists, scores, G.host(out)[0], 0, c, k, "bf16", 6,
+                      True, seed=77)
+    G.flush(f"  worst sampled error {err:.3g}")
