@@ -20,14 +20,16 @@ constexpr float kLn2 = 0.6931471805599453f;
 // s_waitcnt immediate (gfx9 encoding) waiting for vmcnt = 0 only.
 constexpr int kVmcnt0 = 0x0F70;
 
-// Workgroup w of a 1-D grid runs on XCD w % 8. Renumber so that each XCD gets
-// one contiguous range of (head, query cluster) items: neighbouring query
-// clusters of one head share most selected key tiles, which then stay in that
-// XCD's L2.
-__device__ __forceinline__ int xcd_remap(int wg, int total) {
-  int per = total >> 3, rem = total & 7;
-  int xcd = wg & 7, loc = wg >> 3;
-  return xcd < rem ? xcd * (per + 1) + loc : rem * (per + 1) + (xcd - rem) * per + loc;
+// Workgroup w of a 1-D grid runs on XCD w % 8. The items (head, query
+// cluster) are numbered so that each XCD takes a contiguous eighth of a head's
+// query clusters (neighbouring query clusters share most selected key tiles,
+// which then stay in that XCD's L2), and all eight XCDs work on the same head
+// at a time. Slot loc of XCD x holds query cluster x * chunk + loc % chunk of
+// head loc / chunk, chunk = ceil(nqc / 8); slots past nqc hold nothing.
+__device__ __forceinline__ int head_sync_item(int wg, int nqc, int total) {
+  const int x = wg & 7, loc = wg >> 3, chunk = (nqc + 7) >> 3;
+  const int bh = loc / chunk, a = x * chunk + loc % chunk;
+  return a < nqc && bh * nqc < total ? bh * nqc + a : -1;
 }
 
 // Keys per LDS stage: a whole key cluster, except at d = 128 with query and
@@ -77,7 +79,8 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
     if (loc >= sched[x]) return;
     item = sched[8 + x * cap + loc];
   } else {
-    item = xcd_remap(blockIdx.x, total);
+    item = head_sync_item(blockIdx.x, nqc, total);
+    if (item < 0) return;
   }
   const int bh = item / nqc, a = item - bh * nqc;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
@@ -419,7 +422,8 @@ hipError_t run_bf16(const Prob& P, const void* qp, const void* kp, const void* v
   } else {
     sched = nullptr;
   }
-  hipLaunchKernelGGL((attn_bf16_kernel<D, CQ, CK>), dim3(sched ? 8 * cap : total), dim3(CQ * 2),
+  hipLaunchKernelGGL((attn_bf16_kernel<D, CQ, CK>),
+                     dim3(sched ? 8 * cap : 8 * ((P.nqc + 7) / 8) * P.BH), dim3(CQ * 2),
                      0, st, (const bf16*)qp, (const bf16*)kp, (const bf16*)vp, count_k, lists,
                      lens, P.nqc, P.nkc, k, scale * kLog2e, (bf16*)op, lse, total,
                      (const int32_t*)sched, cap);
