@@ -34,7 +34,7 @@ PEAK_HBM_GBS = 8000.0
 # HBM bytes per launch of the attention kernel from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE, scaled by a plain-copy calibration (see the traffic summary under
 # profiles/), valid for the kernel source with this fingerprint only.
-ATTN_TRAFFIC = {"fingerprint": "af9ab9a7e45340ed", "bytes": 1.562e9}
+ATTN_TRAFFIC = {"fingerprint": "ded28d6c8123f3b6", "bytes": 1.611e+09}
 
 
 def attn_fingerprint():
