@@ -665,22 +665,32 @@ __global__ __launch_bounds__(kCholThreads) void cholesky_kernel(Ctx C, int in0, 
   }
   __syncthreads();
   const double tol = sh_tol;
+  // Elimination on unscaled columns (the order of an L D L^T factorisation):
+  // step j subtracts a_ij a_kj / a_jj from the trailing lower triangle (rows
+  // i > j, columns j < k <= i) and leaves column j as it is, so a step reads
+  // only column j and needs one barrier. A pivot at or below tol contributes
+  // nothing and gives a zero column.
   for (int j = 0; j < d; ++j) {
-    // every thread derives the pivot from the same LDS value
-    const double dj = A[j * kCP + j];
-    const double piv = dj > tol ? sqrt(dj) : 0.0;
-    const double ip = piv > 0.0 ? 1.0 / piv : 0.0;
-    __syncthreads();
-    for (int i = j + 1 + tid; i < d; i += kCholThreads) A[i * kCP + j] *= ip;
-    if (tid == 0) A[j * kCP + j] = piv;
-    __syncthreads();
-    // trailing update of the lower triangle, rows i > j, columns j < k <= i
+    const double dj = A[j * kCP + j];  // the same LDS value in every thread
+    const double inv = dj > tol ? 1.0 / dj : 0.0;
     for (int i = j + 1 + tr; i < d; i += 16) {
-      const double lij = A[i * kCP + j];
+      const double lij = A[i * kCP + j] * inv;
       for (int k = j + 1 + tc; k <= i; k += 16) A[i * kCP + k] -= lij * A[k * kCP + j];
     }
     __syncthreads();
   }
+  // Scale: l_jj = sqrt(a_jj), l_ij = a_ij / l_jj.
+  __shared__ double piv[kMaxD], ipiv[kMaxD];
+  if (tid < d) {
+    const double dj = A[tid * kCP + tid];
+    const double p = dj > tol ? sqrt(dj) : 0.0;
+    piv[tid] = p;
+    ipiv[tid] = p > 0.0 ? 1.0 / p : 0.0;
+  }
+  __syncthreads();
+  for (int i = tr; i < d; i += 16)
+    for (int k = tc; k <= i; k += 16) A[i * kCP + k] = k == i ? piv[k] : A[i * kCP + k] * ipiv[k];
+  __syncthreads();
   for (int i = tr; i < d; i += 16)
     for (int k = tc; k < d; k += 16) F[i * d + k] = k <= i ? (float)A[i * kCP + k] : 0.f;
   if (pack >= 0) {
