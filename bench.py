@@ -1,15 +1,19 @@
 #!/usr/bin/env python3
 """Throughput of the ClusterAttention hot path on one MI355X.
 
-One step = one whole layer: ca_cluster -> ca_select -> ca_block_sparse_attn ->
-ca_compensate over all heads of the tabular-attention workload (batch 1, 8
-heads, 65,536 tokens, d = 64, bf16, clusters of 128, top 1/8 of key
-clusters, compensation on), inputs resident in HBM.
+One step = one whole layer: ca_cluster -> ca_select -> ca_attn_compensated
+(block-sparse attention and the striped mean compensation in one pass) over
+all heads of the tabular-attention workload (batch 1, 8 heads, 65,536 tokens,
+d = 64, bf16, clusters of 128, top 1/8 of key clusters, compensation on),
+inputs resident in HBM.
 
 Reported value: dense-equivalent attention TFLOP/s = 4 * heads * N^2 * d /
 (end-to-end time per layer). Alongside: ms per layer, per-call ms from HIP
-events, the roofline position of the dominant kernel (block-sparse attention,
-bf16 MFMA) and the CPU oracle timed on one head.
+events, the roofline position of the dominant kernel (the attention kernel
+with its centroid stages, bf16 MFMA), the same layer with the two calls
+ca_block_sparse_attn and ca_compensate, and the CPU oracle timed on one head.
+The selection modes and the --configs and --sweep tables time the two separate
+calls.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
 """
@@ -34,7 +38,7 @@ PEAK_HBM_GBS = 8000.0
 # HBM bytes per launch of the attention kernel from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE, scaled by a plain-copy calibration (see the traffic summary under
 # profiles/), valid for the kernel source with this fingerprint only.
-ATTN_TRAFFIC = {"fingerprint": "ded28d6c8123f3b6", "bytes": 1.611e+09}
+ATTN_TRAFFIC = {"fingerprint": "b30eb1a42825b6c0", "bytes": 1.607e+09}
 
 
 def attn_fingerprint():
@@ -339,6 +343,9 @@ def main():
                          "compensation on/off) instead of the headline run: one JSON line each")
     ap.add_argument("--no-modes", action="store_true",
                     help="skip the histogram-selection modes timed after the headline run")
+    ap.add_argument("--no-separate", action="store_true",
+                    help="skip the two-call layer (ca_block_sparse_attn + ca_compensate) timed "
+                         "after the headline run")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy three times: the known-size "
                          "reference that scales the FETCH_SIZE / WRITE_SIZE counters")
@@ -383,19 +390,29 @@ def main():
         lists, _ = ca.select(p, r["cent_q"], r["cent_k"], keep_k, ws=ws)
         if ev:
             ev[2].record()
-        op, lse = ca.block_sparse_attn(p, r["qp"], r["kp"], r["vp"], r["count_k"], lists, keep_k)
+        ca.attn_compensated(p, r["qp"], r["kp"], r["vp"], r["cent_k"], r["cent_v"], r["count_k"],
+                            lists, keep_k, r["perm_q"], out=out, ws=ws)
         if ev:
             ev[3].record()
+
+    def step_separate(ev=None):
+        r = ca.cluster(p, q, k, v, ws=ws)
+        lists, _ = ca.select(p, r["cent_q"], r["cent_k"], keep_k, ws=ws)
+        if ev:
+            ev[0].record()
+        op, lse = ca.block_sparse_attn(p, r["qp"], r["kp"], r["vp"], r["count_k"], lists, keep_k)
+        if ev:
+            ev[1].record()
         ca.compensate(p, r["qp"], r["cent_k"], r["cent_v"], r["count_k"], lists, keep_k, op, lse,
                       r["perm_q"], out=out, ws=ws)
         if ev:
-            ev[4].record()
+            ev[2].record()
 
     for _ in range(args.warmup):
         step()
     # HIP events on the stream the calls are enqueued on (torch's current
     # stream), one set per step, read back after the timed region.
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
@@ -403,14 +420,27 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / args.steps
-    calls = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(4)] for e in evs])
+    calls = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(3)] for e in evs])
     call_ms = calls.mean(axis=0)
+    # the same layer with steps 3 and 4 as two calls (after the timed region)
+    sep_ms = None
+    if not args.no_separate:
+        sep_steps = min(args.steps, 10)
+        for _ in range(2):
+            step_separate()
+        sevs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(sep_steps)]
+        for s in range(sep_steps):
+            step_separate(sevs[s])
+        torch.cuda.synchronize()
+        sep_ms = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(2)] for e in sevs]).mean(0)
 
     f_dense = 4.0 * H * n * n * d
     value = f_dense / (ms_step * 1e-3) / 1e12
+    # algorithmic flops of the attention launch: the selected keys, then the
+    # unselected clusters' centroids (4 d per query and key either way)
     f_attn = 4.0 * d * c * c * keep_k * p.nqc * H
-    attn_tflops = f_attn / (call_ms[2] * 1e-3) / 1e12
-    f_comp = 4.0 * d * p.nq_pad * p.nkc * H
+    f_cent = 4.0 * d * c * (p.nkc - keep_k) * p.nqc * H
+    attn_tflops = (f_attn + f_cent) / (call_ms[2] * 1e-3) / 1e12
     rec = {
         "metric": "dense-equivalent attention TFLOP/s + end-to-end ms/layer (clustering incl.)",
         "value": round(value, 2),
@@ -428,15 +458,17 @@ def main():
                    "cluster_size": c, "keep": W["keep"], "kept_clusters": keep_k,
                    "transform": "metric", "compensation": True},
         "breakdown_ms": {"cluster": round(call_ms[0], 4), "select": round(call_ms[1], 4),
-                         "block_sparse_attn": round(call_ms[2], 4),
-                         "compensate": round(call_ms[3], 4)},
-        "roofline": {"kernel": "attn_bf16_kernel<64,128,128>", "bound": "mfma",
+                         "attn_compensated": round(call_ms[2], 4)},
+        "roofline": {"kernel": "attn_bf16_kernel<64,128,128,fused>", "bound": "mfma",
                      "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
                      "traffic": (ATTN_TRAFFIC["bytes"]
                                  if attn_fingerprint() == ATTN_TRAFFIC["fingerprint"] else None)},
-        "compensate_tflops": round(f_comp / (call_ms[3] * 1e-3) / 1e12, 2),
     }
+    if sep_ms is not None:
+        rec["separate_calls_ms"] = {"block_sparse_attn": round(sep_ms[0], 4),
+                                    "compensate": round(sep_ms[1], 4),
+                                    "sum": round(sep_ms[0] + sep_ms[1], 4)}
     if not args.no_modes:
         rec["modes"] = time_selection_modes(ca, torch, p, q, k, v, keep_k, out, args)
     if not args.no_cpu_baseline:

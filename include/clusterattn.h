@@ -18,6 +18,8 @@
  *                            weighted by its size, merged with step 3, and the
  *                            rows restored to the original token order
  *                            (Preliminaries: error in sparse attention; App. A).
+ * ca_attn_compensated computes steps 3 and 4 in one pass (bf16): the same
+ * result without the intermediate op/lse arrays.
  *
  * Conventions shared by every call
  * --------------------------------
@@ -55,7 +57,7 @@
 extern "C" {
 #endif
 
-#define CA_ABI_VERSION 5
+#define CA_ABI_VERSION 6
 
 #if defined(__GNUC__) || defined(__clang__)
 #define CA_API __attribute__((visibility("default")))
@@ -295,6 +297,31 @@ CA_API int ca_compensate(const ca_problem* p, const void* qp, const float* cent_
                   float scale,
                   int32_t enable, const void* op, const float* lse, const int32_t* perm_q,
                   void* out, float* lse_out, void* ws, size_t ws_bytes, void* stream);
+
+/* Steps 3 and 4 in one pass (bf16 problems; Method: Overview; Preliminaries:
+ * error in sparse attention; App. A).
+ *
+ * The result of ca_block_sparse_attn followed by ca_compensate on the same
+ * arguments, up to rounding: each query cluster runs one online softmax over
+ * the keys of its selected clusters and then over the centroid keys of the
+ * unselected clusters, the logit of centroid b being
+ * scale * qp[p] . cent_k[b] + ln count_k[b]. Combining the two parts inside
+ * one softmax gives the merged output and lse directly (ln of the sum of both
+ * parts' exponentials), so op and lse are never formed or rounded, and the
+ * rows go straight to out[perm_q[p]].
+ *
+ * Arguments as in ca_block_sparse_attn (qp, kp, vp, count_k, lists, lens, k,
+ * scale) and ca_compensate (cent_k, cent_v, enable, perm_q, out, lse_out).
+ * ws: device workspace of ws_bytes >= ca_workspace_size(); required when
+ * enable != 0 and either k < nkc or lens is given (the centroids are staged
+ * there as bf16 tiles) and used for the launch schedule when lens is given;
+ * otherwise it may be NULL with ws_bytes 0. Returns CA_E_UNSUPPORTED for fp32
+ * problems and for more than 65536 key clusters. */
+CA_API int ca_attn_compensated(const ca_problem* p, const void* qp, const void* kp, const void* vp,
+                               const float* cent_k, const float* cent_v, const int32_t* count_k,
+                               const int32_t* lists, const int32_t* lens, int32_t k, float scale,
+                               int32_t enable, const int32_t* perm_q, void* out, float* lse_out,
+                               void* ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

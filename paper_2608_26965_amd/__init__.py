@@ -21,7 +21,7 @@ from ._lib import (CA_BF16, CA_F32, CA_LAYOUT_BHND, CA_LAYOUT_BNHD, CA_SPLIT_BAS
                    CA_XF_ADAPTIVE, CA_XF_METRIC, CA_XF_NONE, CA_XF_PCA, CA_XF_RANDOM, CAError)
 
 __all__ = ["Problem", "workspace_size", "cluster", "select", "select_hist", "block_sparse_attn",
-           "compensate", "forward", "CAError", "abi_version"]
+           "compensate", "attn_compensated", "forward", "CAError", "abi_version"]
 
 _XF = {"none": CA_XF_NONE, "pca": CA_XF_PCA, "metric": CA_XF_METRIC, "adaptive": CA_XF_ADAPTIVE,
        "random": CA_XF_RANDOM}
@@ -209,6 +209,26 @@ def compensate(p: Problem, qp, cent_k, cent_v, count_k, lists, keep_k: int, op, 
                                    _ptr(lse), _ptr(perm_q), _ptr(out), _ptr(lse_out), _ptr(ws),
                                    0 if ws is None else ws.numel(), _stream(dev))
     _lib.check(st, "ca_compensate")
+    return out, lse_out
+
+
+def attn_compensated(p: Problem, qp, kp, vp, cent_k, cent_v, count_k, lists, keep_k: int,
+                     perm_q, scale: float = 0.0, enable: bool = True, want_lse: bool = False,
+                     out=None, ws=None, lens=None):
+    """Steps 3 and 4 in one pass (bf16). Returns (out in the problem layout,
+    lse [BH,nq] or None), as block_sparse_attn followed by compensate."""
+    dev = qp.device
+    if out is None:
+        out = torch.empty(p.shape(p.nq), dtype=p.dtype, device=dev)
+    lse_out = torch.empty(p.bh, p.nq, dtype=torch.float32, device=dev) if want_lse else None
+    if ws is None and ((enable and keep_k < p.nkc) or lens is not None):
+        ws = workspace(p, dev, keep_k)
+    st = _lib.load().ca_attn_compensated(p.c(), _ptr(qp), _ptr(kp), _ptr(vp), _ptr(cent_k),
+                                         _ptr(cent_v), _ptr(count_k), _ptr(lists), _ptr(lens),
+                                         keep_k, float(scale), int(bool(enable)), _ptr(perm_q),
+                                         _ptr(out), _ptr(lse_out), _ptr(ws),
+                                         0 if ws is None else ws.numel(), _stream(dev))
+    _lib.check(st, "ca_attn_compensated")
     return out, lse_out
 
 

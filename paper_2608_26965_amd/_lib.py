@@ -23,6 +23,7 @@ EXPORTS = (
     "ca_select_hist",
     "ca_block_sparse_attn",
     "ca_compensate",
+    "ca_attn_compensated",
 )
 
 _i32 = ctypes.c_int32
@@ -82,6 +83,10 @@ def load() -> ctypes.CDLL:
     lib.ca_compensate.restype = ctypes.c_int
     lib.ca_compensate.argtypes = [P, _vp, _vp, _vp, _vp, _vp, _vp, _i32, ctypes.c_float, _i32,
                                   _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp]
+    lib.ca_attn_compensated.restype = ctypes.c_int
+    lib.ca_attn_compensated.argtypes = [P, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32,
+                                        ctypes.c_float, _i32, _vp, _vp, _vp, _vp, ctypes.c_size_t,
+                                        _vp]
     _lib = lib
     return lib
 

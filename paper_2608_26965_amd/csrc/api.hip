@@ -297,4 +297,43 @@ int ca_compensate(const ca_problem* p, const void* qp, const float* cent_k, cons
                        "ca_compensate");
 }
 
+int ca_attn_compensated(const ca_problem* p, const void* qp, const void* kp, const void* vp,
+                        const float* cent_k, const float* cent_v, const int32_t* count_k,
+                        const int32_t* lists, const int32_t* lens, int32_t k, float scale,
+                        int32_t enable, const int32_t* perm_q, void* out, float* lse_out,
+                        void* ws, size_t ws_bytes, void* stream) {
+  ca::Prob P;
+  int s = check_problem(p, &P);
+  if (s) return s;
+  if ((s = check_k(P, k))) return s;
+  if (P.dtype != CA_BF16) return fail(CA_E_UNSUPPORTED, "ca_attn_compensated needs bf16 inputs");
+  if (!qp || !kp || !vp || !count_k || !lists || !perm_q || !out)
+    return fail(CA_E_INVALID, "a required pointer of ca_attn_compensated is NULL");
+  if (enable && (!cent_k || !cent_v))
+    return fail(CA_E_INVALID, "compensation needs cent_k and cent_v");
+  if ((s = check_attn_shape(P))) return s;
+  if (P.nkc > ca::kMaskWords * 32)
+    return fail(CA_E_UNSUPPORTED, "ca_attn_compensated supports at most 65536 key clusters");
+  const bool comp = enable && (k < P.nkc || lens);
+  char* tiles = nullptr;
+  int32_t* sched = nullptr;
+  if (comp || (ws && lens)) {
+    ca::Workspace W;
+    ca::plan_workspace(P, &W);
+    if ((s = check_ws(W, ws, ws_bytes))) return s;
+    if (comp) tiles = (char*)ws + W.comp_tiles;
+    if (lens) sched = (int32_t*)((char*)ws + W.sched);
+  }
+  if (!(scale > 0.0f)) scale = 1.0f / sqrtf((float)P.d);
+  hipStream_t st = (hipStream_t)stream;
+  if (tiles) {
+    s = device_status(ca::launch_comp_stage(P, cent_k, cent_v, count_k, tiles, st),
+                      "ca_attn_compensated");
+    if (s) return s;
+  }
+  return device_status(ca::launch_attn_fused(P, qp, kp, vp, count_k, lists, lens, k, scale, tiles,
+                                             perm_q, out, lse_out, sched, st),
+                       "ca_attn_compensated");
+}
+
 }  // extern "C"

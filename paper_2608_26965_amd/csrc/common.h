@@ -129,6 +129,7 @@ constexpr int kChunk = 4096;      // tokens per block in the multi-block split p
 constexpr int kTail = 4096;       // nodes of at most this size finish in one workgroup
 constexpr int kMomRows = 2048;    // rows per moment-partial block
 constexpr int kCompTile = 128;    // centroids per tile of the bf16 compensation kernel
+constexpr int kMaskWords = 2048;  // selection bitmap words in LDS: up to 65536 key clusters
 
 // Bytes of one bf16 compensation tile: kCompTile centroid key rows [kCompTile][d]
 // bf16, the centroid values transposed [d][kCompTile] bf16, and kCompTile fp32
@@ -170,5 +171,19 @@ hipError_t launch_comp(const Prob& P, const void* qp, const float* cent_k, const
                        float scale,
                        int enable, const void* op, const float* lse, const int32_t* perm_q,
                        void* out, float* lse_out, char* tiles, hipStream_t st);
+
+// Writes the bf16 centroid tiles (keys, transposed values, log2 sizes) of
+// every head into tiles (bf16 problems).
+hipError_t launch_comp_stage(const Prob& P, const float* cent_k, const float* cent_v,
+                             const int32_t* count_k, char* tiles, hipStream_t st);
+// Block-sparse attention with the striped mean compensation folded in (bf16):
+// after its selected key clusters each query cluster continues the same
+// online softmax over the unselected centroids (tiles: staged centroid tiles,
+// or NULL for no compensation) and writes the merged rows to their original
+// positions (out, problem layout) and lse_out (optional).
+hipError_t launch_attn_fused(const Prob& P, const void* qp, const void* kp, const void* vp,
+                             const int32_t* count_k, const int32_t* lists, const int32_t* lens,
+                             int k, float scale, const char* tiles, const int32_t* perm_q,
+                             void* out, float* lse_out, int32_t* sched, hipStream_t st);
 
 }  // namespace ca

@@ -51,12 +51,27 @@ constexpr int attn_waves_per_simd() {
   return blocks * (CQ / 32) / 4 < 1 ? 1 : blocks * (CQ / 32) / 4;
 }
 
-template <int D, int CQ, int CK>
+// Compensation folded into the attention kernel: the staged centroid tiles of
+// the unselected clusters are extra stages of the same online softmax, with
+// log2 of the cluster size added to their logits (the merged output of the
+// paper's two partial results, formed without writing either of them), and
+// the rows go to their original positions.
+struct FusedArgs {
+  const char* tiles;      // staged centroid tiles [BH][ntile] (NULL: no compensation)
+  int ntile;
+  const int32_t* perm_q;  // [BH][nq]
+  bf16* out;              // problem layout
+  float* lse_out;         // [BH][nq] or NULL
+  int nq, H, layout;
+};
+
+template <int D, int CQ, int CK, bool FUSED = false>
 __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void attn_bf16_kernel(
     const bf16* __restrict__ qp, const bf16* __restrict__ kp, const bf16* __restrict__ vp,
     const int32_t* __restrict__ count_k, const int32_t* __restrict__ lists,
     const int32_t* __restrict__ lens, int nqc, int nkc, int k, float sl2, bf16* __restrict__ op,
-    float* __restrict__ lse, int total, const int32_t* __restrict__ sched, int cap) {
+    float* __restrict__ lse, int total, const int32_t* __restrict__ sched, int cap,
+    FusedArgs fa = FusedArgs{}) {
   constexpr int NW = CQ / 32;
   constexpr int HK = attn_stage_keys<D, CQ, CK>();  // keys per stage
   constexpr int SUB = CK / HK;                      // stages per key cluster
@@ -71,6 +86,14 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   constexpr int VLD = VBYTES / 1024 / NW;
   static_assert(KLD * 1024 * NW == KBYTES && VLD * 1024 * NW == VBYTES, "tile split");
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+  // fused: the query cluster's selection bitmap and the two stages' bias rows
+  __shared__ uint32_t selmask[FUSED ? kMaskWords : 1];
+  __shared__ __attribute__((aligned(16))) float cbias[2][FUSED ? HK : 4];
+  constexpr int SUBC = kCompTile / HK;                     // stages per centroid tile
+  constexpr int CTK = kCompTile * KROW, CTV = D * 2 * kCompTile;
+  constexpr int CTILE = CTK + CTV + kCompTile * 4;        // bytes of a staged centroid tile
+  constexpr int BLANES = FUSED ? HK / 4 / NW : 1;          // lanes per wave copying a bias row
+  static_assert(!FUSED || (BLANES >= 1 && BLANES * 16 * NW == HK * 4), "bias split");
 
   int item;
   if (sched) {
@@ -100,6 +123,18 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   const int32_t* cnth = count_k + (size_t)bh * nkc;
   // this query cluster's list length (uniform; clamped for memory safety)
   const int nt = lens ? min(max(lens[(size_t)bh * nqc + a], 1), k) : k;
+  // centroid stages (fused, when some cluster is unselected)
+  const int nc = FUSED && fa.tiles && nt < nkc ? fa.ntile * SUBC : 0;
+  if (FUSED && nc) {
+    const int nwords = (nkc + 31) >> 5;
+    for (int i = tid; i < nwords; i += CQ * 2) selmask[i] = 0u;
+    __syncthreads();
+    for (int i = tid; i < nt; i += CQ * 2) {
+      const int b = lst[i];
+      if (b >= 0 && b < nkc) atomicOr(&selmask[b >> 5], 1u << (b & 31));
+    }
+    // ordered before any read by the first stage's barrier
+  }
   auto tile_id = [&](int t) {
     int b = lst[t];
     return b < 0 ? 0 : (b >= nkc ? nkc - 1 : b);
@@ -114,6 +149,23 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
     const bf16* vt = vp + ((size_t)bh * nkc + b) * (size_t)D * CK + (size_t)s * HK;
     kcopy.issue(kt, lds0 + stage * STAGE, w);
     vcopy.issue(vt, lds0 + stage * STAGE + KBYTES, w);
+  };
+  // fused: stage ng + c holds centroids [HK (c % SUBC), + HK) of centroid tile
+  // c / SUBC, with their bias row in cbias
+  const TileCopy<VROW, VLD, NW, 2 * kCompTile> ccopy(w, lane);
+  const char* ctl = FUSED && nc ? fa.tiles + (size_t)bh * fa.ntile * CTILE : nullptr;
+  auto issue_any = [&](int g, int stage) {
+    if (!FUSED || g < nt * SUB) {
+      issue(g, stage);
+      return;
+    }
+    const int c = g - nt * SUB, s = c % SUBC;
+    const char* src = ctl + (size_t)(c / SUBC) * CTILE;
+    kcopy.issue(src + s * KBYTES, lds0 + stage * STAGE, w);
+    ccopy.issue(src + CTK + s * VROW, lds0 + stage * STAGE + KBYTES, w);
+    const uint32_t boff = (uint32_t)(w * BLANES * 16);
+    const uint32_t bdst = __builtin_amdgcn_readfirstlane(lds_addr(&cbias[stage][0]) + boff);
+    if (lane < BLANES) lds_dma16(src + CTK + CTV + s * HK * 4, boff + 16 * lane, bdst);
   };
   // Loop-invariant LDS read offsets (rows r and r + 32 share the swizzle key).
   int koff[KS];
@@ -140,17 +192,28 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   // passes only once done with stage g-2 (which used the same buffer), so one
   // barrier per stage suffices and each copy has a whole stage of compute to
   // land.
-  const int ng = nt * SUB;
-  auto body = [&](auto stage_tag, int g) {
+  const int ng = nt * SUB, ngt = ng + nc;
+  const float isl2 = 1.f / sl2;
+  auto body = [&](auto stage_tag, auto cen_tag, int g) {
     constexpr int S = decltype(stage_tag)::value;
     wait_vmcnt<0>();
     wait_lgkm();
     raw_barrier();
-    if (g + 1 < ng) issue(g + 1, S ^ 1);
+    if (g + 1 < ngt) issue_any(g + 1, S ^ 1);
     const char* ks = smem + S * STAGE;
     const char* vs = ks + KBYTES;
+    constexpr bool cstage = decltype(cen_tag)::value;  // a centroid stage
+    if constexpr (cstage) {
+      // Selected clusters are covered by the sparse part: drop them here.
+      if (tid < HK) {
+        const int c = g - ng, b = (c / SUBC) * kCompTile + (c % SUBC) * HK + tid;
+        if (b < nkc && ((selmask[b >> 5] >> (b & 31)) & 1u)) cbias[S][tid] = -INFINITY;
+      }
+      wait_lgkm();
+      raw_barrier();  // bias row final
+    }
     // keys of this stage past the cluster's count are padding
-    const int cnt = cnth[tile_id(g / SUB)] - (g % SUB) * HK;
+    const int cnt = cstage ? HK : cnth[tile_id(g / SUB)] - (g % SUB) * HK;
 
     f32x16 sacc[MT];
 #pragma unroll
@@ -169,6 +232,22 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
 #pragma unroll
         for (int r = 0; r < 16; ++r)
           if (acc_key(mt, r, h) >= cnt) sacc[mt][r] = -INFINITY;
+    }
+    if constexpr (cstage) {
+      // logit + log2|b| / sl2, so that the exponent below is sl2 q.kbar + log2|b| - m.
+      // The bias of accumulator r of row tile mt is that of key acc_key(mt, r, h):
+      // two runs of eight consecutive entries.
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const float4 b0 = *(const float4*)&cbias[S][32 * mt + 16 * hh + 8 * h];
+          const float4 b1 = *(const float4*)&cbias[S][32 * mt + 16 * hh + 8 * h + 4];
+          const float bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            sacc[mt][8 * hh + j] = __builtin_fmaf(bv[j], isl2, sacc[mt][8 * hh + j]);
+        }
     }
     // Exponentials are taken against the running maximum without first
     // forming this tile's maximum. Only a tile whose logits pass the running
@@ -224,13 +303,44 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   };
 
   issue(0, 0);
+  using key_stage = std::false_type;
   for (int g = 0; g < ng; g += 2) {
-    body(std::integral_constant<int, 0>{}, g);
-    if (g + 1 < ng) body(std::integral_constant<int, 1>{}, g + 1);
+    body(std::integral_constant<int, 0>{}, key_stage{}, g);
+    if (g + 1 < ng) body(std::integral_constant<int, 1>{}, key_stage{}, g + 1);
+  }
+  if constexpr (FUSED) {
+    // the centroid stages, in their own loop so that the key stages' code is
+    // that of the plain kernel
+    for (int g = ng; g < ngt; ++g) {
+      if (g & 1)
+        body(std::integral_constant<int, 1>{}, std::true_type{}, g);
+      else
+        body(std::integral_constant<int, 0>{}, std::true_type{}, g);
+    }
   }
 
   const float l_tot = l_run + wave_xor32(l_run);
   const float inv = 1.f / l_tot;
+  if constexpr (FUSED) {
+    // merged rows to their original positions
+    const int prow = a * CQ + 32 * w + l32;
+    if (prow >= fa.nq) return;
+    int orig = fa.perm_q[(size_t)bh * fa.nq + prow];
+    orig = orig < 0 ? 0 : (orig >= fa.nq ? fa.nq - 1 : orig);  // memory safety for a bad permutation
+    bf16* orow = fa.out + row_off(bh, orig, fa.nq, fa.H, D, fa.layout);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        bf16x4 v4;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v4[j] = f2bf(oacc[dt][4 * g + j] * inv);
+        *(bf16x4*)(orow + 32 * dt + 8 * g + 4 * h) = v4;
+      }
+    if (fa.lse_out && h == 0)
+      fa.lse_out[(size_t)bh * fa.nq + orig] = (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2;
+    return;
+  }
   bf16* orow = op + qrow * D;
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt)
@@ -408,10 +518,11 @@ __global__ __launch_bounds__(kSchedThreads) void attn_sched_kernel(const int32_t
   if (tid == 0) sched[x] = r1 - r0;
 }
 
-template <int D, int CQ, int CK>
+template <int D, int CQ, int CK, bool FUSED = false>
 hipError_t run_bf16(const Prob& P, const void* qp, const void* kp, const void* vp,
                     const int32_t* count_k, const int32_t* lists, const int32_t* lens, int k,
-                    float scale, void* op, float* lse, int32_t* sched, hipStream_t st) {
+                    float scale, void* op, float* lse, int32_t* sched, hipStream_t st,
+                    FusedArgs fa = FusedArgs{}) {
   const int total = P.BH * P.nqc;
   const int cap = attn_sched_cap(total);
   if (sched && lens) {
@@ -422,11 +533,11 @@ hipError_t run_bf16(const Prob& P, const void* qp, const void* kp, const void* v
   } else {
     sched = nullptr;
   }
-  hipLaunchKernelGGL((attn_bf16_kernel<D, CQ, CK>),
+  hipLaunchKernelGGL((attn_bf16_kernel<D, CQ, CK, FUSED>),
                      dim3(sched ? 8 * cap : 8 * ((P.nqc + 7) / 8) * P.BH), dim3(CQ * 2),
                      0, st, (const bf16*)qp, (const bf16*)kp, (const bf16*)vp, count_k, lists,
                      lens, P.nqc, P.nkc, k, scale * kLog2e, (bf16*)op, lse, total,
-                     (const int32_t*)sched, cap);
+                     (const int32_t*)sched, cap, fa);
   return hipGetLastError();
 }
 
@@ -466,6 +577,29 @@ hipError_t launch_attn(const Prob& P, const void* qp, const void* kp, const void
                        P.cq, P.ck, P.d, k, scale, (float*)op, lse);
   }
   return hipGetLastError();
+}
+
+hipError_t launch_attn_fused(const Prob& P, const void* qp, const void* kp, const void* vp,
+                             const int32_t* count_k, const int32_t* lists, const int32_t* lens,
+                             int k, float scale, const char* tiles, const int32_t* perm_q,
+                             void* out, float* lse_out, int32_t* sched, hipStream_t st) {
+  if (P.dtype != CA_BF16 || P.nkc > kMaskWords * 32) return hipErrorInvalidValue;
+  const FusedArgs fa{tiles, (P.nkc + kCompTile - 1) / kCompTile, perm_q, (bf16*)out, lse_out,
+                     P.nq, P.H, P.layout};
+#define CA_ATTN_CASE(D, CQ, CK) \
+  if (P.d == D && P.cq == CQ && P.ck == CK) \
+    return run_bf16<D, CQ, CK, true>(P, qp, kp, vp, count_k, lists, lens, k, scale, nullptr, \
+                                     nullptr, sched, st, fa);
+  CA_ATTN_CASE(64, 64, 64)
+  CA_ATTN_CASE(64, 64, 128)
+  CA_ATTN_CASE(64, 128, 64)
+  CA_ATTN_CASE(64, 128, 128)
+  CA_ATTN_CASE(128, 64, 64)
+  CA_ATTN_CASE(128, 64, 128)
+  CA_ATTN_CASE(128, 128, 64)
+  CA_ATTN_CASE(128, 128, 128)
+#undef CA_ATTN_CASE
+  return hipErrorInvalidValue;
 }
 
 }  // namespace ca

@@ -23,7 +23,6 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
-constexpr int kMaskWords = 2048;  // up to 65536 key clusters
 // s_waitcnt immediate (gfx9 encoding) waiting for vmcnt = 0 only.
 constexpr int kVmcnt0 = 0x0F70;
 
@@ -487,6 +486,20 @@ hipError_t run_bf16(const Prob& P, const void* qp, const float* cent_k, const fl
 }
 
 }  // namespace
+
+hipError_t launch_comp_stage(const Prob& P, const float* cent_k, const float* cent_v,
+                             const int32_t* count_k, char* tiles, hipStream_t st) {
+  const int ntile = (P.nkc + kCompTile - 1) / kCompTile;
+  if (P.d == 64)
+    hipLaunchKernelGGL(comp_stage_kernel<64>, dim3(ntile, P.BH, 2), dim3(256), 0, st, cent_k,
+                       cent_v, count_k, P.nkc, ntile, tiles);
+  else if (P.d == 128)
+    hipLaunchKernelGGL(comp_stage_kernel<128>, dim3(ntile, P.BH, 2), dim3(256), 0, st, cent_k,
+                       cent_v, count_k, P.nkc, ntile, tiles);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
 
 hipError_t launch_comp(const Prob& P, const void* qp, const float* cent_k, const float* cent_v,
                        const int32_t* count_k, const int32_t* lists, const int32_t* lens, int k,

@@ -25,7 +25,7 @@ def test_header_symbols_exported():
     assert declared == set(L.EXPORTS)
     for name in declared:
         assert hasattr(lib, name)
-    assert lib.ca_abi_version() == 5
+    assert lib.ca_abi_version() == 6
 
 
 def _prob(**kw):
@@ -89,6 +89,23 @@ def test_calls_reject_before_enqueue():
     # ... also when every list may be full length but lengths are given
     assert lib.ca_compensate(p, fake, fake, fake, fake, fake, fake, 16, 0.0, 1, fake, fake, fake,
                              fake, None, fake, 16, None) == L.CA_E_WORKSPACE
+    # steps 3 and 4 in one pass: (qp, kp, vp, cent_k, cent_v, count_k, lists, lens), k, scale,
+    # enable, perm_q, out, lse_out, ws, ws_bytes, stream
+    fa = [fake] * 7 + [None]
+    assert lib.ca_attn_compensated(p, *fa, 2, 0.0, 1, None, fake, None, None, 0, None) == \
+        L.CA_E_INVALID
+    fb = [fake] * 3 + [None, None] + [fake] * 2 + [None]  # centroids missing
+    assert lib.ca_attn_compensated(p, *fb, 2, 0.0, 1, fake, fake, None, None, 0, None) == \
+        L.CA_E_INVALID
+    assert lib.ca_attn_compensated(_prob(dtype=L.CA_F32), *fa, 2, 0.0, 1, fake, fake, None, None,
+                                   0, None) == L.CA_E_UNSUPPORTED
+    assert lib.ca_attn_compensated(p, *fa, 99, 0.0, 1, fake, fake, None, None, 0, None) == \
+        L.CA_E_INVALID
+    # compensation needs the workspace for the centroid tiles
+    assert lib.ca_attn_compensated(p, *fa, 2, 0.0, 1, fake, fake, None, fake, 16, None) == \
+        L.CA_E_WORKSPACE
+    assert lib.ca_attn_compensated(p, *fa, 2, 0.0, 1, fake, fake, None, None, 0, None) == \
+        L.CA_E_WORKSPACE
     # histogram selection: lists, lens and count_k are required; thresholds in range
     sh = [fake, fake, fake, None, None]  # cent_q, cent_k, count_k, scores_in, scores_out
     assert lib.ca_select_hist(p, *sh, 16, 0.5, 0.0, fake, None, None, 0, None) == L.CA_E_INVALID

@@ -18,10 +18,15 @@ from synth import CONFIGS, keep_to_k, make_config
 pytestmark = pytest.mark.gpu
 
 
-def _pipeline(p, q, k, v, keep_k, comp=True):
+def _pipeline(p, q, k, v, keep_k, comp=True, fused=False):
     import paper_2608_26965_amd as ca
     r = ca.cluster(p, q, k, v, export_y=True)
     lists, scores = ca.select(p, r["cent_q"], r["cent_k"], keep_k, export_scores=True)
+    if fused:
+        out, lse_out = ca.attn_compensated(p, r["qp"], r["kp"], r["vp"], r["cent_k"], r["cent_v"],
+                                           r["count_k"], lists, keep_k, r["perm_q"], enable=comp,
+                                           want_lse=True)
+        return r, lists, scores, out, lse_out
     op, lse = ca.block_sparse_attn(p, r["qp"], r["kp"], r["vp"], r["count_k"], lists, keep_k)
     out, lse_out = ca.compensate(p, r["qp"], r["cent_k"], r["cent_v"], r["count_k"], lists, keep_k,
                                  op, lse, r["perm_q"], enable=comp, want_lse=True)
@@ -69,19 +74,21 @@ def _check_head(Q, K, V, r, lists, scores, out, h, c, k, dt, nsample, comp, seed
     return err
 
 
-def _run_config(cid, heads, c, keep, comp=True, check_heads=None, nsample=12, split="diag"):
+def _run_config(cid, heads, c, keep, comp=True, check_heads=None, nsample=12, split="diag",
+                fused=False):
     import torch
     import paper_2608_26965_amd as ca
     from tests import gpu_util as G
     cfg = CONFIGS[cid]
-    G.flush(f"e2e config {cid} heads={len(heads)} c={c} keep={keep} comp={comp} split={split}")
+    G.flush(f"e2e config {cid} heads={len(heads)} c={c} keep={keep} comp={comp} split={split} "
+            f"fused={fused}")
     Q, K, V = make_config(cid, heads=heads)
     H, n, d = Q.shape
     dt = cfg.dtype
     p = ca.Problem(1, H, n, n, d, c, c, G.tdtype(dt), "metric", split=split)
     k = keep_to_k(keep, p.nkc)
     tq, tk, tv = (G.dev(x[None], G.tdtype(dt)) for x in (Q, K, V))
-    r, lists, scores, out, lse = _pipeline(p, tq, tk, tv, k, comp)
+    r, lists, scores, out, lse = _pipeline(p, tq, tk, tv, k, comp, fused)
     torch.cuda.synchronize()
     outh = G.host(out)[0]
     worst = 0.0
@@ -121,6 +128,17 @@ def test_tabular_bench_workload_basic_split():
     the metric root space: the power-iteration directions, projections and
     partitions reproduced bit for bit on the checked heads of both sides."""
     _run_config(2, list(range(8)), 128, 1 / 8, check_heads=[0, 5], split="basic", nsample=8)
+
+
+def test_tabular_bench_workload_fused():
+    """The benchmarked workload, all 8 heads, with steps 3 and 4 in one pass
+    (ca_attn_compensated), against the oracle like the four separate calls."""
+    _run_config(2, list(range(8)), 128, 1 / 8, check_heads=[0, 3, 7], fused=True)
+
+
+@pytest.mark.parametrize("c,keep", [(64, 1 / 16), (128, 1 / 8)])
+def test_video_720p_one_head_fused(c, keep):
+    _run_config(5, [0], c, keep, nsample=8, fused=True)
 
 
 @pytest.mark.parametrize("keep", [1 / 16, 1 / 4])
