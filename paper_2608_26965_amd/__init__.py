@@ -239,7 +239,7 @@ def keep_to_k(keep: float, n_kc: int) -> int:
 
 def forward(q, k, v, cq=128, ck=None, keep=None, keep_k=None, transform="metric",
             compensation=True, scale=None, layout="bhnd", return_parts=False, select="topk",
-            mass_recall=0.9, min_count=16):
+            mass_recall=0.9, min_count=16, one_pass=True):
     """ClusterAttention for one layer. q, k, v: [B,H,N,d] ("bhnd") or [B,N,H,d]
     ("bnhd"), bf16 or fp32, on one GPU.
 
@@ -247,7 +247,9 @@ def forward(q, k, v, cq=128, ck=None, keep=None, keep_k=None, transform="metric"
     (``keep_k``) of key clusters per query cluster; select="hist": the
     two-pass histogram top-k (at least that many clusters); select="adaptive":
     attention-mass recall ``mass_recall`` with at least ``min_count`` clusters
-    (use it with transform="adaptive")."""
+    (use it with transform="adaptive"). bf16 layers run steps 3 and 4 in one
+    pass (attn_compensated) unless one_pass is False or return_parts asks for
+    the sparse part's output and lse."""
     ck = cq if ck is None else ck
     if layout == "bhnd":
         B, H, nq, d = q.shape
@@ -272,6 +274,11 @@ def forward(q, k, v, cq=128, ck=None, keep=None, keep_k=None, transform="metric"
         stride = p.nkc
     else:
         raise ValueError(select)
+    if one_pass and not return_parts and p.dtype == torch.bfloat16:
+        out, _ = attn_compensated(p, c["qp"], c["kp"], c["vp"], c["cent_k"], c["cent_v"],
+                                  c["count_k"], lists, stride, c["perm_q"], sc, compensation,
+                                  ws=ws, lens=lens)
+        return out
     op, lse = block_sparse_attn(p, c["qp"], c["kp"], c["vp"], c["count_k"], lists, stride, sc,
                                 lens=lens, ws=ws)
     out, lse_out = compensate(p, c["qp"], c["cent_k"], c["cent_v"], c["count_k"], lists, stride,

@@ -96,3 +96,24 @@ def test_fused_adaptive_lists(scheduled):
     assert n.min() < n.max() or n.min() < p.nkc
     _compare(_fused(p, r, lists, p.nkc, True, lens=lens, ws=ws),
              _separate(p, r, lists, p.nkc, True, lens=lens, ws=ws), "adaptive")
+
+
+@pytest.mark.parametrize("select,transform", [("topk", "metric"), ("adaptive", "adaptive")])
+def test_forward_one_pass_matches_two_calls(select, transform):
+    """The layer API: bf16 layers take the one-pass call by default."""
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    G.flush(f"forward: one pass vs two calls, select={select}")
+    g = torch.Generator(device="cpu").manual_seed(3)
+    q, k, v = (torch.randn(1, 2, 3500, 64, generator=g).to("cuda").to(torch.bfloat16)
+               for _ in range(3))
+    kw = dict(cq=128, keep=0.2, transform=transform, select=select, min_count=4)
+    a = ca.forward(q, k, v, **kw)
+    b, parts = ca.forward(q, k, v, return_parts=True, **kw)
+    c = ca.forward(q, k, v, one_pass=False, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(b, c)
+    d = (a.float() - c.float()).abs()
+    assert (d / c.float().abs().clamp_min(1.0)).max().item() <= 2e-2
+    assert d.mean().item() <= 2e-3
