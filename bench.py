@@ -303,6 +303,31 @@ def config_table(args):
         f_dense = 4.0 * H * n * n * d
         f_attn = 4.0 * d * c * c * keep_k * p.nqc * H
         attn_tf = f_attn / (calls[2] * 1e-3) / 1e12
+        # bf16: the same layer with steps 3 and 4 in one pass (ca_attn_compensated)
+        one_pass = None
+        if cfg.dtype == "bf16":
+            def step1(ev=None):
+                r = ca.cluster(p, q, k, v, ws=ws)
+                lists, _ = ca.select(p, r["cent_q"], r["cent_k"], keep_k, ws=ws)
+                if ev:
+                    ev[0].record()
+                ca.attn_compensated(p, r["qp"], r["kp"], r["vp"], r["cent_k"], r["cent_v"],
+                                    r["count_k"], lists, keep_k, r["perm_q"], enable=comp,
+                                    out=out, ws=ws)
+                if ev:
+                    ev[1].record()
+
+            for _ in range(warmup):
+                step1()
+            ev1 = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            for i in range(steps):
+                step1(ev1[i])
+            torch.cuda.synchronize()
+            one_pass = {"ms_per_layer": round((time.perf_counter() - t1) * 1e3 / steps, 4),
+                        "attn_compensated_ms": round(float(np.mean(
+                            [e[0].elapsed_time(e[1]) for e in ev1])), 4)}
         print(json.dumps({"table": "configs", "config": cfg.name, "heads": H, "n": n, "d": d,
                           "dtype": cfg.dtype, "c": c, "keep": keep, "kept_clusters": keep_k,
                           "key_clusters": p.nkc, "compensation": comp,
@@ -312,7 +337,8 @@ def config_table(args):
                           "dense_equiv_tflops": round(f_dense / (ms * 1e-3) / 1e12, 1),
                           "attention_tflops": round(attn_tf, 1),
                           "attention_mfma_frac": (round(attn_tf / PEAK_BF16_TFLOPS, 4)
-                                                  if cfg.dtype == "bf16" else None)}),
+                                                  if cfg.dtype == "bf16" else None),
+                          "one_pass": one_pass}),
               flush=True)
         del ws, out
 
