@@ -218,7 +218,31 @@ def latency_sweep(args):
             calls = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(4)]
                               for e in evs]).mean(0)
             f_dense = 4.0 * H * n * n * d
+
+            # the same layer with steps 3 and 4 in one pass (ca_attn_compensated)
+            def step1(ev=None):
+                r = ca.cluster(p, q, k, v, ws=ws)
+                lists, _ = ca.select(p, r["cent_q"], r["cent_k"], keep_k, ws=ws)
+                if ev:
+                    ev[0].record()
+                ca.attn_compensated(p, r["qp"], r["kp"], r["vp"], r["cent_k"], r["cent_v"],
+                                    r["count_k"], lists, keep_k, r["perm_q"], out=out, ws=ws)
+                if ev:
+                    ev[1].record()
+
+            for _ in range(warmup):
+                step1()
+            ev1 = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            for i in range(steps):
+                step1(ev1[i])
+            torch.cuda.synchronize()
+            one_pass = {"ms_per_layer": round((time.perf_counter() - t1) * 1e3 / steps, 4),
+                        "attn_compensated_ms": round(float(np.mean(
+                            [e[0].elapsed_time(e[1]) for e in ev1])), 4)}
             print(json.dumps({"sweep": "latency_scaling", "n": n, "rule": rule, "split": split,
+                              "one_pass": one_pass,
                               "kept_clusters":
                               keep_k, "key_clusters": p.nkc, "ms_per_layer": round(ms, 4),
                               "cluster_ms": round(calls[0], 4), "select_ms": round(calls[1], 4),
