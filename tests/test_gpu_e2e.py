@@ -1,4 +1,5 @@
-"""End-to-end GPU parity of the four calls chained, at the workloads' full
+"""End-to-end GPU parity of the calls chained (the four calls, or with steps 3
+and 4 as the one call ca_attn_compensated where a test says fused), at the workloads' full
 per-head sizes (the tabular workload at all 8 heads, in the launch
 configuration the bench times).
 
