@@ -265,3 +265,14 @@ def test_one_million_tokens_one_head():
     err = _check_head(Q[0], K[0], V[0], r, lists, scores, G.host(out)[0], 0, c, k, "bf16", 6,
                       True, seed=77)
     G.flush(f"  worst sampled error {err:.3g}")
+    # steps 3 and 4 in one pass on the same clusters and lists (a selection
+    # bitmap of 8192 clusters): within one bf16 unit of the two calls, and the
+    # sampled rows within the tolerance of the oracle
+    out1, _ = ca.attn_compensated(p, r["qp"], r["kp"], r["vp"], r["cent_k"], r["cent_v"],
+                                  r["count_k"], lists, k, r["perm_q"])
+    torch.cuda.synchronize()
+    dd = (out1.float() - out.float()).abs()
+    assert (dd / out.float().abs().clamp_min(1.0)).max().item() <= 2e-2
+    err1 = _check_head(Q[0], K[0], V[0], r, lists, scores, G.host(out1)[0], 0, c, k, "bf16", 6,
+                       True, seed=78)
+    G.flush(f"  one pass: worst sampled error {err1:.3g}")
