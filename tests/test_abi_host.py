@@ -101,6 +101,14 @@ def test_calls_reject_before_enqueue():
                                    0, None) == L.CA_E_UNSUPPORTED
     assert lib.ca_attn_compensated(p, *fa, 99, 0.0, 1, fake, fake, None, None, 0, None) == \
         L.CA_E_INVALID
+    # the largest problem (2^22 keys in clusters of 64) has 65536 key clusters, what
+    # the selection bitmap holds: accepted up to the workspace check; one key more
+    # is not a valid problem
+    big = _prob(nq=64, nk=1 << 22)
+    assert lib.ca_attn_compensated(big, *fa, 2, 0.0, 1, fake, fake, None, fake, 16, None) == \
+        L.CA_E_WORKSPACE
+    assert lib.ca_attn_compensated(_prob(nq=64, nk=(1 << 22) + 1), *fa, 2, 0.0, 1, fake, fake,
+                                   None, fake, 16, None) == L.CA_E_INVALID
     # compensation needs the workspace for the centroid tiles
     assert lib.ca_attn_compensated(p, *fa, 2, 0.0, 1, fake, fake, None, fake, 16, None) == \
         L.CA_E_WORKSPACE
