@@ -227,3 +227,91 @@ def test_basic_split_parity(dt, n, d, c, xf):
                 assert abs(got - want) <= 2e-4 * ((yk64[a] ** 2).sum() + (yk64[b] ** 2).sum()) + 1e-9
             nrm = np.sqrt((yq64 ** 2).sum(axis=1))
             assert np.abs(nrm[nrm > 0] - 1.0).max() < 1e-4
+
+
+# Inputs whose multi-block split levels take the select pass's fallback
+# paths. "duplicates": 60% of the queries and 70% of the keys are one repeated
+# row, so at the root the wanted rank falls inside a run of more than 8192
+# equal keys (a run of D equal values covers rank r whatever its position when
+# D > max(r, s - r)); that linear bin overflows the select pass's candidate
+# buffer and the threshold is found by streaming the node's keys from memory.
+# "flat_root_sample": the root's subsample rows are all equal, so its spread
+# is zero and every key lands in one bin (and streams). "all_identical": every
+# node of every level is in that case, and the order is decided by the
+# original index alone.
+DEGENERATE = [
+    # kind, n, transform, split
+    ("duplicates", 40000, "none", "diag"),
+    ("duplicates", 40000, "metric", "diag"),
+    ("flat_root_sample", 40000, "none", "diag"),
+    ("flat_root_sample", 40000, "metric", "diag"),
+    ("all_identical", 33000, "none", "diag"),
+    ("all_identical", 33000, "metric", "diag"),
+    ("duplicates", 40000, "none", "basic"),
+    ("flat_root_sample", 40000, "metric", "basic"),
+    ("all_identical", 33000, "metric", "basic"),
+]
+
+
+def _degenerate_inputs(kind, n, d, seed):
+    Q, K, V = mixture_inputs(seed, 1, n, d, "bf16", centres=12, sigma=0.5)
+    rng = np.random.default_rng([seed, 1])
+    for X, frac in ((Q[0], 0.6), (K[0], 0.7)):
+        row = X[rng.integers(n)].copy()
+        if kind == "duplicates":
+            X[rng.choice(n, int(frac * n), replace=False)] = row
+        elif kind == "flat_root_sample":
+            X[ref.subsample_positions(n, min(d, n))] = row
+        else:
+            X[:] = row
+    return Q, K, V
+
+
+def _reaches_fallback(kind, Y, c):
+    """The exported split coordinates really put the root on the fallback
+    path: a long enough run of equal rows, or a subsample without spread."""
+    n, d = Y.shape
+    if kind == "flat_root_sample":
+        sub = Y[ref.subsample_positions(n, min(d, n))]
+        return bool((sub == sub[0]).all())
+    _, dup = np.unique(Y, axis=0, return_counts=True)
+    mL = ref.left_size(n, c)
+    return dup.max() > max(8192, mL - 1, n - mL + 1)
+
+
+@pytest.mark.parametrize("kind,n,xf,split", DEGENERATE)
+def test_split_select_fallbacks(kind, n, xf, split):
+    """Permutations bit-exact against the oracle's split of the exported
+    coordinates on inputs with long runs of equal split keys and subsamples
+    without spread (padding rows, repeated tokens), which take the select
+    pass's streaming and one-bin paths; permuted copies, counts and centroids
+    as in the other cluster tests."""
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    d, c = 64, 128
+    G.flush(f"split fallback case kind={kind} n={n} xf={xf} split={split}")
+    Q, K, V = _degenerate_inputs(kind, n, d, seed=n)
+    p = ca.Problem(1, 1, n, n, d, c, c, torch.bfloat16, xf, "bhnd", split=split)
+    tq, tk, tv = (G.dev(x[None], torch.bfloat16) for x in (Q, K, V))
+    r = ca.cluster(p, tq, tk, tv, export_y=True)
+    torch.cuda.synchronize()
+    r = {key: val.cpu() for key, val in r.items()}
+    yq = r["yq"][0].numpy().astype(np.float64)
+    yk = r["yk"][0].numpy().astype(np.float64)
+    for side, Y in (("query", yq), ("key", yk)):
+        assert _reaches_fallback(kind, Y, c), f"{side} input does not reach the fallback path"
+    if split == "basic":
+        pq, cidq, _ = ref.basic_split(yq, c, head=0, side=0)
+        pk, cidk, _ = ref.basic_split(yk, c, head=0, side=1)
+    else:
+        pq, cidq, _ = ref.split(yq, c)
+        pk, cidk, _ = ref.split(yk, c)
+    if kind == "all_identical" and split == "diag":
+        assert np.array_equal(pq, np.arange(n)) and np.array_equal(pk, np.arange(n))
+    assert np.array_equal(r["perm_q"][0].numpy(), pq), "query permutation"
+    assert np.array_equal(r["perm_k"][0].numpy(), pk), "key permutation"
+    assert np.array_equal(r["cid_q"][0].numpy(), cidq)
+    assert np.array_equal(r["cid_k"][0].numpy(), cidk)
+    _check_copies(Q[0], pq, r["count_q"][0], r["cent_q"][0], r["qp"][0], c, "bf16")
+    _check_copies(K[0], pk, r["count_k"][0], r["cent_k"][0], r["kp"][0], c, "bf16")

@@ -15,6 +15,7 @@ import pytest
 
 from oracle import ref
 from synth import CONFIGS, keep_to_k, make_config
+from tests.oracle_check import check_head, oracle_rows, sample_clusters
 
 pytestmark = pytest.mark.gpu
 
@@ -34,47 +35,6 @@ def _pipeline(p, q, k, v, keep_k, comp=True, fused=False):
     return r, lists, scores, out, lse_out
 
 
-def _check_head(Q, K, V, r, lists, scores, out, h, c, k, dt, nsample, comp, seed, split="diag"):
-    from tests import gpu_util as G
-    n, d = Q.shape
-    tau = 1 / math.sqrt(d)
-    yq = r["yq"][h].double().cpu().numpy()
-    yk = r["yk"][h].double().cpu().numpy()
-    perm_q = r["perm_q"][h].cpu().numpy()
-    perm_k = r["perm_k"][h].cpu().numpy()
-    if split == "basic":
-        want_q = ref.basic_split(yq, c, head=h, side=0)[0]
-        want_k = ref.basic_split(yk, c, head=h, side=1)[0]
-    else:
-        want_q, want_k = ref.split(yq, c)[0], ref.split(yk, c)[0]
-    assert np.array_equal(perm_q, want_q), "query permutation"
-    assert np.array_equal(perm_k, want_k), "key permutation"
-    cq_n, ck_n = G.counts(n, c), G.counts(n, c)
-    S = scores[h].double().cpu().numpy()
-    L = lists[h].cpu().numpy()
-    assert np.array_equal(L, ref.topk(S, k)), "lists"
-    qbar = ref.centroids(Q, perm_q, cq_n)
-    kbar = ref.centroids(K, perm_k, ck_n)
-    vbar = ref.centroids(V, perm_k, ck_n)
-    S_or = ref.centroid_scores(qbar, kbar)
-    assert np.abs(S - S_or).max() <= 1e-4 * max(1.0, np.abs(S_or).max()), "scores"
-    rng = np.random.default_rng(seed)
-    nqc = len(cq_n)
-    sample = np.unique(np.concatenate([[nqc - 1], rng.choice(nqc, min(nsample, nqc), replace=False)]))
-    mem = ref.cluster_members(perm_q, cq_n)
-    rows = np.concatenate([mem[a] for a in sample])
-    sub_counts = cq_n[sample]
-    sub_perm = np.arange(len(rows))
-    o_s, l_s = ref.sparse_attention(Q[rows], K, V, sub_perm, sub_counts, perm_k, ck_n, L[sample],
-                                    tau)
-    o, l = ref.compensate(Q[rows], kbar, vbar, ck_n, sub_perm, sub_counts, L[sample], o_s, l_s,
-                          tau, comp)
-    got = out[h][rows]
-    err = np.abs(got - o).max()
-    assert err <= G.TOL[dt], f"head {h}: output error {err}"
-    return err
-
-
 def _run_config(cid, heads, c, keep, comp=True, check_heads=None, nsample=12, split="diag",
                 fused=False):
     import torch
@@ -92,10 +52,11 @@ def _run_config(cid, heads, c, keep, comp=True, check_heads=None, nsample=12, sp
     r, lists, scores, out, lse = _pipeline(p, tq, tk, tv, k, comp, fused)
     torch.cuda.synchronize()
     outh = G.host(out)[0]
+    lseh = G.host(lse)
     worst = 0.0
     for h in (check_heads if check_heads is not None else range(H)):
-        worst = max(worst, _check_head(Q[h], K[h], V[h], r, lists, scores, outh, h, c, k, dt,
-                                       nsample, comp, seed=cid * 100 + h, split=split))
+        worst = max(worst, check_head(Q[h], K[h], V[h], r, lists, scores, outh, h, c, k, dt,
+                                      nsample, comp, seed=cid * 100 + h, split=split, lse=lseh))
     G.flush(f"  worst sampled error {worst:.3g}")
     return r, lists, out
 
@@ -182,9 +143,11 @@ def test_tabular_histogram_selection_pipeline(mode):
     clusters, adaptive query transform). Per checked head: permutations
     bit-exact against the oracle's split of the exported coordinates; every
     row's list and length equal to the oracle's histogram selection of the
-    exported scores; sampled query clusters' outputs within the tolerance of
-    the oracle's compensated sparse attention given the GPU's permutations
-    and lists."""
+    exported scores; sampled query clusters' outputs and merged lse (the
+    shortest and the longest list among them) within the tolerance of the
+    oracle's compensated sparse attention given the GPU's permutations and
+    lists, for the two calls and for the one-pass call over the same ragged
+    lists."""
     import torch
     import paper_2608_26965_amd as ca
     from tests import gpu_util as G
@@ -206,10 +169,15 @@ def test_tabular_histogram_selection_pipeline(mode):
     op0, lse0 = ca.block_sparse_attn(p, r["qp"], r["kp"], r["vp"], r["count_k"], lists, p.nkc,
                                      lens=lens)
     assert torch.equal(op, op0) and torch.equal(lse, lse0), "scheduled launch"
-    out, _ = ca.compensate(p, r["qp"], r["cent_k"], r["cent_v"], r["count_k"], lists, p.nkc, op,
-                           lse, r["perm_q"], lens=lens)
+    out, lse_out = ca.compensate(p, r["qp"], r["cent_k"], r["cent_v"], r["count_k"], lists, p.nkc,
+                                 op, lse, r["perm_q"], lens=lens, want_lse=True)
+    # steps 3 and 4 in one pass over the same ragged lists (scheduled launch)
+    out1, lse1 = ca.attn_compensated(p, r["qp"], r["kp"], r["vp"], r["cent_k"], r["cent_v"],
+                                     r["count_k"], lists, p.nkc, r["perm_q"], lens=lens, ws=ws,
+                                     want_lse=True)
     torch.cuda.synchronize()
-    outh = G.host(out)[0]
+    outh, lseh = G.host(out)[0], G.host(lse_out)
+    outh1, lseh1 = G.host(out1)[0], G.host(lse1)
     N = lens.cpu().numpy()
     G.flush(f"  list length: mean {N.mean():.1f}, min {N.min()}, max {N.max()} of {p.nkc}")
     cn = G.counts(n, c)
@@ -227,22 +195,17 @@ def test_tabular_histogram_selection_pipeline(mode):
             want = ref.hist_select(S[a], cn, float(scale), floor, float(np.float32(recall)))
             assert N[h, a] == len(want) and np.array_equal(L[a, :N[h, a]], want), (h, a)
             rows_sel.append(want)
-        kbar = ref.centroids(K[h], perm_k, cn)
-        vbar = ref.centroids(V[h], perm_k, cn)
-        rng = np.random.default_rng(h)
-        sample = np.unique(np.concatenate([[p.nqc - 1], rng.choice(p.nqc, 8, replace=False)]))
-        mem = ref.cluster_members(perm_q, cn)
-        rows = np.concatenate([mem[a] for a in sample])
-        sub_counts = cn[sample]
-        sub_perm = np.arange(len(rows))
-        sub_lists = [rows_sel[a] for a in sample]
-        tau = float(scale)
-        o_s, l_s = ref.sparse_attention(Q[h][rows], K[h], V[h], sub_perm, sub_counts, perm_k, cn,
-                                        sub_lists, tau)
-        o, _ = ref.compensate(Q[h][rows], kbar, vbar, cn, sub_perm, sub_counts, sub_lists, o_s,
-                              l_s, tau)
-        err = np.abs(outh[h][rows] - o).max()
-        assert err <= G.TOL["bf16"], f"head {h}: output error {err}"
+        # sampled clusters: the shortest and the longest list, the last cluster
+        # and random ones
+        sample = np.unique(np.concatenate([sample_clusters(p.nqc, 8, h),
+                                           [np.argmin(N[h]), np.argmax(N[h])]]))
+        rows, o, l = oracle_rows(Q[h], K[h], V[h], perm_q, perm_k, c, c, rows_sel, sample,
+                                 float(scale), True)
+        for what, oh, lh in (("two calls", outh, lseh), ("one pass", outh1, lseh1)):
+            err = np.abs(oh[h][rows] - o).max()
+            assert err <= G.TOL["bf16"], f"{what}, head {h}: output error {err}"
+            lerr = np.abs(lh[h][rows] - l).max()
+            assert lerr <= G.TOL["bf16"], f"{what}, head {h}: lse error {lerr}"
 
 
 def test_one_million_tokens_one_head():
@@ -262,17 +225,17 @@ def test_one_million_tokens_one_head():
     tq, tk, tv = (G.dev(x[None], torch.bfloat16) for x in (Q, K, V))
     r, lists, scores, out, _ = _pipeline(p, tq, tk, tv, k)
     torch.cuda.synchronize()
-    err = _check_head(Q[0], K[0], V[0], r, lists, scores, G.host(out)[0], 0, c, k, "bf16", 6,
-                      True, seed=77)
+    err = check_head(Q[0], K[0], V[0], r, lists, scores, G.host(out)[0], 0, c, k, "bf16", 6,
+                     True, seed=77)
     G.flush(f"  worst sampled error {err:.3g}")
     # steps 3 and 4 in one pass on the same clusters and lists (a selection
     # bitmap of 8192 clusters): within one bf16 unit of the two calls, and the
     # sampled rows within the tolerance of the oracle
-    out1, _ = ca.attn_compensated(p, r["qp"], r["kp"], r["vp"], r["cent_k"], r["cent_v"],
-                                  r["count_k"], lists, k, r["perm_q"])
+    out1, lse1 = ca.attn_compensated(p, r["qp"], r["kp"], r["vp"], r["cent_k"], r["cent_v"],
+                                     r["count_k"], lists, k, r["perm_q"], want_lse=True)
     torch.cuda.synchronize()
     dd = (out1.float() - out.float()).abs()
     assert (dd / out.float().abs().clamp_min(1.0)).max().item() <= 2e-2
-    err1 = _check_head(Q[0], K[0], V[0], r, lists, scores, G.host(out1)[0], 0, c, k, "bf16", 6,
-                       True, seed=78)
+    err1 = check_head(Q[0], K[0], V[0], r, lists, scores, G.host(out1)[0], 0, c, k, "bf16", 6,
+                      True, seed=78, lse=G.host(lse1))
     G.flush(f"  one pass: worst sampled error {err1:.3g}")
