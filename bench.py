@@ -3,24 +3,27 @@
 
 One step = one whole layer: ca_cluster -> ca_select -> ca_attn_compensated
 (block-sparse attention and the striped mean compensation in one pass) over
-all heads of the tabular-attention workload (batch 1, 8 heads, 65,536 tokens,
-d = 64, bf16, clusters of 128, top 1/8 of key clusters, compensation on),
-inputs resident in HBM.
+all heads of the large tabular-attention workload (batch 1, 16 heads, 262,144
+tokens, d = 64, bf16, clusters of 128, top 1/16 of key clusters, compensation
+on, metric transform, exact top-k), inputs resident in HBM.
 
 Reported value: dense-equivalent attention TFLOP/s = 4 * heads * N^2 * d /
 (end-to-end time per layer). Alongside: ms per layer, per-call ms from HIP
-events, the roofline position of the dominant kernel (the attention kernel
-with its centroid stages, bf16 MFMA), the same layer with the two calls
-ca_block_sparse_attn and ca_compensate, and the CPU oracle timed on one head.
-The selection modes and the --configs and --sweep tables time the two separate
-calls.
+events, the same layer keeping 1/4 of the key clusters, the dense baseline
+(this library's attention with every key cluster kept) and the layer's
+speedup over it, the roofline position of the dominant kernel (the attention
+kernel with its centroid stages, bf16 MFMA) and of the clustering call (HBM),
+the same layer with the two calls ca_block_sparse_attn and ca_compensate, the
+selection modes, and the CPU oracle timed on a bounded sample of one head.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+       [--no-modes] [--headline-only] [--configs] [--sweep] [--copy-calibration]
 """
 from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import platform
 import sys
@@ -31,24 +34,34 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-WORKLOAD = dict(cfg=2, name="tabular-8h-n65536-d64-bf16-c128-keep1/8", heads=8, n=65536, d=64,
-                c=128, keep=1 / 8)
+WORKLOAD = dict(cfg=3, name="tabular-16h-n262144-d64-bf16-c128-keep1/16", heads=16, n=262144,
+                d=64, c=128, keep=1 / 16, keep2=1 / 4)
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
-# HBM bytes per launch of the attention kernel from rocprofv3 FETCH_SIZE and
-# WRITE_SIZE, scaled by a plain-copy calibration (see the traffic summary under
-# profiles/), valid for the kernel source with this fingerprint only.
-ATTN_TRAFFIC = {"fingerprint": "b30eb1a42825b6c0", "bytes": 1.607e+09}
+# HBM bytes per launch from rocprofv3 FETCH_SIZE and WRITE_SIZE, scaled by a
+# plain-copy calibration (FETCH_SIZE x 2, WRITE_SIZE x 1; the traffic summaries
+# under profiles/ give the commands), valid for the kernel sources with the
+# given fingerprint only (else reported as null).
+ATTN_TRAFFIC = {"fingerprint": None, "bytes": None}
+CLUSTER_TRAFFIC = {"fingerprint": None, "bytes": None}
 
 
-def attn_fingerprint():
-    """sha256 over k_attn.hip then attn_tile.h (first 16 hex digits)."""
+def _fingerprint(files):
+    """sha256 over the given csrc files in order (first 16 hex digits)."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("k_attn.hip", "attn_tile.h"):
+    for f in files:
         with open(os.path.join(ROOT, "paper_2608_26965_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
+
+
+def attn_fingerprint():
+    return _fingerprint(("k_attn.hip", "attn_tile.h"))
+
+
+def cluster_fingerprint():
+    return _fingerprint(("k_cluster.hip",))
 
 
 def cpu_model():
@@ -61,30 +74,82 @@ def cpu_model():
     return platform.processor() or "unknown"
 
 
-def time_oracle(Q, K, V, c, k):
-    """The oracle, as it stands, on one head of the workload (full pipeline)."""
+def cluster_bytes(heads, n, d, e, c):
+    """Algorithmic HBM bytes of one ca_cluster call (both sides, all heads):
+    per head and token, moments 2de (q, k read), query representation de,
+    projection 2de read + 8d (fp32 split coordinates written, both sides),
+    4 + 4 + 4 bytes per split level and side (key and index read, index
+    written), permute/gather 6de (q, k, v read and written), permutation and
+    cluster ids 16."""
+    levels = max(0, math.ceil(math.log2(-(-n // c))))
+    return float(heads) * n * (11 * d * e + 8 * d + 24 * levels + 16)
+
+
+def time_oracle_sample(Q, K, V, c, k, every=2):
+    """The oracle, as it stands, on a bounded sample of one head: the whole
+    clustering (split spaces and recursive splits of both sides), centroids,
+    scores and top-k, then the block-sparse attention and the compensation of
+    every ``every``-th query cluster. Returns (measured seconds, estimated
+    seconds for the whole head = clustering and selection + every x the
+    sampled attention and compensation, threads, sampled clusters)."""
     from oracle import ref
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
         threads = os.cpu_count() or 1
+    Q, K, V = (np.asarray(x, np.float64) for x in (Q, K, V))
+    n, d = Q.shape
+    tau = 1.0 / math.sqrt(d)
     t0 = time.perf_counter()
-    ref.forward(Q, K, V, c, c, k, "metric", True)
-    dt = time.perf_counter() - t0
-    return dt, threads
+    yq = ref.query_split_space(Q, K, "metric")
+    yk = ref.key_split_space(Q, K, "metric")
+    perm_q, _, cnt_q = ref.split(yq, c)
+    perm_k, _, cnt_k = ref.split(yk, c)
+    kbar = ref.centroids(K, perm_k, cnt_k)
+    vbar = ref.centroids(V, perm_k, cnt_k)
+    lists = ref.topk(ref.centroid_scores(ref.centroids(Q, perm_q, cnt_q), kbar), k)
+    t1 = time.perf_counter()
+    sample = np.arange(0, len(cnt_q), every)
+    mem = ref.cluster_members(perm_q, cnt_q)
+    rows = np.concatenate([mem[a] for a in sample])
+    sub = np.arange(len(rows))
+    o_s, l_s = ref.sparse_attention(Q[rows], K, V, sub, cnt_q[sample], perm_k, cnt_k,
+                                    lists[sample], tau)
+    ref.compensate(Q[rows], kbar, vbar, cnt_k, sub, cnt_q[sample], lists[sample], o_s, l_s, tau)
+    t2 = time.perf_counter()
+    est = (t1 - t0) + (t2 - t1) * len(cnt_q) / len(sample)
+    return t2 - t0, est, threads, len(sample)
+
+
+def _timed(torch, step, n_ev, steps, warmup):
+    """Run step() warmup times, then steps times with n_ev HIP events each
+    (recorded by step on the stream the calls are enqueued on); returns (ms
+    per step by the host clock between two synchronisations, mean ms between
+    consecutive events)."""
+    for _ in range(warmup):
+        step()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(steps):
+        step(evs[s])
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    calls = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(n_ev - 1)] for e in evs])
+    return ms, calls.mean(axis=0)
 
 
 def time_selection_modes(ca, torch, p, q, k, v, keep_k, out, args):
     """The same layer in the other modes, timed after (and apart from) the
     headline run: top-k through the two-pass histogram (at least keep_k
     clusters, metric transform), adaptive assignment (90% of the estimated
-    attention mass, at least 16 clusters, adaptive transform) and the
+    attention mass, at least 16 clusters, adaptive transform), the
     random-cluster control (random clusters, exact top-k of keep_k) and basic
     recursive splitting (power-iteration directions in the metric root space,
-    exact top-k of keep_k). Per call ms (HIP events, mean over the timed
-    steps), ms per layer and the mean number of selected key clusters per
-    query cluster."""
+    exact top-k of keep_k); steps 3 and 4 in one pass. Per call ms (HIP
+    events, mean over the timed steps), ms per layer and the mean number of
+    selected key clusters per query cluster."""
     res = {}
     for name, xf, floor, recall, split in (
             ("hist_topk", "metric", keep_k, 0.0, "diag"),
@@ -94,7 +159,7 @@ def time_selection_modes(ca, torch, p, q, k, v, keep_k, out, args):
         pm = ca.Problem(p.batch, p.heads, p.nq, p.nk, p.d, p.cq, p.ck, p.dtype, xf, p.layout,
                         split=split)
         ws = ca.workspace(pm, q.device, keep_k)
-        lens_seen = []
+        seen = {}
 
         def step(ev=None):
             if ev:
@@ -111,35 +176,23 @@ def time_selection_modes(ca, torch, p, q, k, v, keep_k, out, args):
                 stride = pm.nkc
             if ev:
                 ev[2].record()
-            op, lse = ca.block_sparse_attn(pm, r["qp"], r["kp"], r["vp"], r["count_k"], lists,
-                                           stride, lens=lens, ws=ws)
+            ca.attn_compensated(pm, r["qp"], r["kp"], r["vp"], r["cent_k"], r["cent_v"],
+                                r["count_k"], lists, stride, r["perm_q"], out=out, ws=ws,
+                                lens=lens)
             if ev:
                 ev[3].record()
-            ca.compensate(pm, r["qp"], r["cent_k"], r["cent_v"], r["count_k"], lists, stride, op,
-                          lse, r["perm_q"], out=out, ws=ws, lens=lens)
-            if ev:
-                ev[4].record()
-            return lens
+            seen["lens"] = lens
 
-        for _ in range(args.warmup):
-            step()
-        steps = max(3, args.steps // 2)
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for s in range(steps):
-            lens = step(evs[s])
-        torch.cuda.synchronize()
-        ms = (time.perf_counter() - t0) * 1e3 / steps
-        calls = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(4)] for e in evs]).mean(0)
+        ms, calls = _timed(torch, step, 4, max(3, args.steps // 2), args.warmup)
+        lens = seen["lens"]
         res[name] = {"transform": xf, "split": split, "min_count": floor,
                      "mass_recall": recall if recall is not None else "exact top-k",
                      "ms_per_step": round(ms, 4),
                      "breakdown_ms": {"cluster": round(calls[0], 4), "select": round(calls[1], 4),
-                                      "block_sparse_attn": round(calls[2], 4),
-                                      "compensate": round(calls[3], 4)},
+                                      "attn_compensated": round(calls[2], 4)},
                      "mean_clusters": (round(float(lens.float().mean()), 2) if lens is not None
                                        else float(floor))}
+        del ws
     return res
 
 
@@ -255,43 +308,45 @@ def latency_sweep(args):
         torch.cuda.empty_cache()
 
 
-# Rows of the per-configuration table: (config, cluster size, keep fraction,
-# compensation, distinct heads generated). The generated heads are repeated up
-# to the configuration's head count (heads are independent units of the
-# method, so the work and its shape are those of the full layer; generating
-# every head on the host would take minutes).
+# Rows of the per-configuration table: (config, query cluster size, key
+# cluster size, keep fraction, compensation). Every head of a configuration
+# is generated (in parallel processes, before the GPU is used).
 CONFIG_ROWS = (
-    [(1, 64, 0.25, True, 1), (1, 64, 1.0, True, 1), (2, 128, 0.125, True, 8),
-     (3, 128, 0.0625, True, 2), (3, 128, 0.25, True, 2), (4, 64, 0.25, True, 4)]
-    + [(5, c, keep, comp, 4) for c in (64, 128) for keep in (0.25, 0.125, 0.0625)
-       for comp in (True, False)])
+    [(1, 64, 64, 0.25, True), (1, 64, 64, 1.0, True), (2, 128, 128, 0.125, True),
+     (3, 128, 128, 0.0625, True), (3, 128, 128, 0.25, True), (4, 64, 64, 0.25, True)]
+    + [(5, c, c, keep, comp) for c in (64, 128) for keep in (0.25, 0.125, 0.0625)
+       for comp in (True, False)]
+    # the paper's evaluated tile shape: query clusters of 64, key clusters of 128
+    + [(2, 64, 128, 0.125, True), (5, 64, 128, 0.125, True)])
 
 
 def config_table(args):
     """One JSON line per row of CONFIG_ROWS: the whole layer (metric
     transform, exact top-k) timed with HIP events, mean over the timed steps
-    after the warm-ups; dense-equivalent TFLOP/s; the attention kernel's
-    TFLOP/s on the computed interactions (4 d c_q c_k per query-cluster /
-    selected-key-cluster pair) against the bf16 MFMA peak."""
+    after the warm-ups, with steps 3 and 4 as two calls and (bf16) as the one
+    pass; dense-equivalent TFLOP/s; the attention kernel's TFLOP/s on the
+    computed interactions (4 d c_q c_k per query-cluster / selected
+    key-cluster pair) against the bf16 MFMA peak."""
+    from synth import CONFIGS, make_config
+    workers = min(16, os.cpu_count() or 1)
+    host = {}
+    for cid in sorted({row[0] for row in CONFIG_ROWS}):
+        host[cid] = make_config(cid, workers=workers)
     import torch
     import paper_2608_26965_amd as ca
-    from synth import CONFIGS, make_config
     dev = torch.device("cuda:0")
     steps, warmup = max(3, min(args.steps, 10)), max(1, min(args.warmup, 3))
     cache = {}
-    for cid, c, keep, comp, gen in CONFIG_ROWS:
+    for cid, cq, ck, keep, comp in CONFIG_ROWS:
         cfg = CONFIGS[cid]
         if cid not in cache:
             cache.clear()
             torch.cuda.empty_cache()
-            Qh, Kh, Vh = make_config(cid, heads=list(range(gen)))
-            rep = -(-cfg.heads // gen)
             dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
-            cache[cid] = tuple(torch.from_numpy(x).to(dev).to(dt).repeat(rep, 1, 1)[:cfg.heads][None]
-                               .contiguous() for x in (Qh, Kh, Vh))
+            cache[cid] = tuple(torch.from_numpy(x[None]).to(dev).to(dt) for x in host[cid])
         q, k, v = cache[cid]
         H, n, d = q.shape[1:]
-        p = ca.Problem(1, H, n, n, d, c, c, q.dtype, "metric", "bhnd")
+        p = ca.Problem(1, H, n, n, d, cq, ck, q.dtype, "metric", "bhnd")
         keep_k = ca.keep_to_k(keep, p.nkc)
         ws = ca.workspace(p, dev, keep_k)
         out = torch.empty(p.shape(n), dtype=q.dtype, device=dev)
@@ -314,20 +369,10 @@ def config_table(args):
             if ev:
                 ev[4].record()
 
-        for _ in range(warmup):
-            step()
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for i in range(steps):
-            step(evs[i])
-        torch.cuda.synchronize()
-        ms = (time.perf_counter() - t0) * 1e3 / steps
-        calls = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(4)] for e in evs]).mean(0)
+        ms, calls = _timed(torch, step, 5, steps, warmup)
         f_dense = 4.0 * H * n * n * d
-        f_attn = 4.0 * d * c * c * keep_k * p.nqc * H
+        f_attn = 4.0 * d * cq * ck * keep_k * p.nqc * H
         attn_tf = f_attn / (calls[2] * 1e-3) / 1e12
-        # bf16: the same layer with steps 3 and 4 in one pass (ca_attn_compensated)
         one_pass = None
         if cfg.dtype == "bf16":
             def step1(ev=None):
@@ -341,21 +386,12 @@ def config_table(args):
                 if ev:
                     ev[1].record()
 
-            for _ in range(warmup):
-                step1()
-            ev1 = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
-            torch.cuda.synchronize()
-            t1 = time.perf_counter()
-            for i in range(steps):
-                step1(ev1[i])
-            torch.cuda.synchronize()
-            one_pass = {"ms_per_layer": round((time.perf_counter() - t1) * 1e3 / steps, 4),
-                        "attn_compensated_ms": round(float(np.mean(
-                            [e[0].elapsed_time(e[1]) for e in ev1])), 4)}
+            ms1, c1 = _timed(torch, step1, 2, steps, warmup)
+            one_pass = {"ms_per_layer": round(ms1, 4), "attn_compensated_ms": round(c1[0], 4)}
         print(json.dumps({"table": "configs", "config": cfg.name, "heads": H, "n": n, "d": d,
-                          "dtype": cfg.dtype, "c": c, "keep": keep, "kept_clusters": keep_k,
-                          "key_clusters": p.nkc, "compensation": comp,
-                          "distinct_heads_generated": gen, "ms_per_layer": round(ms, 4),
+                          "dtype": cfg.dtype, "cq": cq, "ck": ck, "keep": keep,
+                          "kept_clusters": keep_k, "key_clusters": p.nkc, "compensation": comp,
+                          "distinct_heads_generated": H, "ms_per_layer": round(ms, 4),
                           "cluster_ms": round(calls[0], 4), "select_ms": round(calls[1], 4),
                           "attention_ms": round(calls[2], 4), "compensation_ms": round(calls[3], 4),
                           "dense_equiv_tflops": round(f_dense / (ms * 1e-3) / 1e12, 1),
@@ -392,10 +428,11 @@ def main():
                     help="every workload configuration (cluster sizes, keep fractions, "
                          "compensation on/off) instead of the headline run: one JSON line each")
     ap.add_argument("--no-modes", action="store_true",
-                    help="skip the histogram-selection modes timed after the headline run")
-    ap.add_argument("--no-separate", action="store_true",
-                    help="skip the two-call layer (ca_block_sparse_attn + ca_compensate) timed "
-                         "after the headline run")
+                    help="skip the selection modes timed after the headline run")
+    ap.add_argument("--headline-only", action="store_true",
+                    help="time only the headline layer (no keep-1/4 layer, dense baseline, "
+                         "two-call layer, modes or CPU baseline): the profiling runs use it, so "
+                         "that the attention kernel's launches are all the headline's")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy three times: the known-size "
                          "reference that scales the FETCH_SIZE / WRITE_SIZE counters")
@@ -415,82 +452,57 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
-    import torch
-    import paper_2608_26965_amd as ca
     from synth import make_config
-
     W = WORKLOAD
     H, n, d, c = W["heads"], W["n"], W["d"], W["c"]
-    Qh, Kh, Vh = make_config(W["cfg"])
+    # Every head drawn on the host (forked workers, before anything touches the GPU).
+    t_gen = time.perf_counter()
+    Qh, Kh, Vh = make_config(W["cfg"], workers=min(16, os.cpu_count() or 1))
+    t_gen = time.perf_counter() - t_gen
+    print(f"inputs: {H} heads drawn in {t_gen:.1f} s", file=sys.stderr, flush=True)
+
+    import torch
+    import paper_2608_26965_amd as ca
+
     dev = torch.device("cuda:0")
-    q = torch.from_numpy(Qh[None]).to(dev).to(torch.bfloat16)
-    k = torch.from_numpy(Kh[None]).to(dev).to(torch.bfloat16)
-    v = torch.from_numpy(Vh[None]).to(dev).to(torch.bfloat16)
+    q, k, v = (torch.from_numpy(x[None]).to(dev).to(torch.bfloat16) for x in (Qh, Kh, Vh))
+    head0 = (Qh[0].copy(), Kh[0].copy(), Vh[0].copy())
+    del Qh, Kh, Vh
     p = ca.Problem(1, H, n, n, d, c, c, torch.bfloat16, "metric", "bhnd")
-    keep_k = ca.keep_to_k(W["keep"], p.nkc)
-    ws = ca.workspace(p, dev, keep_k)
+    ws = ca.workspace(p, dev, p.nkc)
     out = torch.empty(p.shape(n), dtype=torch.bfloat16, device=dev)
-
-    def step(ev=None):
-        if ev:
-            ev[0].record()
-        r = ca.cluster(p, q, k, v, ws=ws)
-        if ev:
-            ev[1].record()
-        lists, _ = ca.select(p, r["cent_q"], r["cent_k"], keep_k, ws=ws)
-        if ev:
-            ev[2].record()
-        ca.attn_compensated(p, r["qp"], r["kp"], r["vp"], r["cent_k"], r["cent_v"], r["count_k"],
-                            lists, keep_k, r["perm_q"], out=out, ws=ws)
-        if ev:
-            ev[3].record()
-
-    def step_separate(ev=None):
-        r = ca.cluster(p, q, k, v, ws=ws)
-        lists, _ = ca.select(p, r["cent_q"], r["cent_k"], keep_k, ws=ws)
-        if ev:
-            ev[0].record()
-        op, lse = ca.block_sparse_attn(p, r["qp"], r["kp"], r["vp"], r["count_k"], lists, keep_k)
-        if ev:
-            ev[1].record()
-        ca.compensate(p, r["qp"], r["cent_k"], r["cent_v"], r["count_k"], lists, keep_k, op, lse,
-                      r["perm_q"], out=out, ws=ws)
-        if ev:
-            ev[2].record()
-
-    for _ in range(args.warmup):
-        step()
-    # HIP events on the stream the calls are enqueued on (torch's current
-    # stream), one set per step, read back after the timed region.
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for s in range(args.steps):
-        step(evs[s])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_step = wall * 1e3 / args.steps
-    calls = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(3)] for e in evs])
-    call_ms = calls.mean(axis=0)
-    # the same layer with steps 3 and 4 as two calls (after the timed region)
-    sep_ms = None
-    if not args.no_separate:
-        sep_steps = min(args.steps, 10)
-        for _ in range(2):
-            step_separate()
-        sevs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(sep_steps)]
-        for s in range(sep_steps):
-            step_separate(sevs[s])
-        torch.cuda.synchronize()
-        sep_ms = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(2)] for e in sevs]).mean(0)
-
     f_dense = 4.0 * H * n * n * d
+
+    def layer(keep_k):
+        def step(ev=None):
+            if ev:
+                ev[0].record()
+            r = ca.cluster(p, q, k, v, ws=ws)
+            if ev:
+                ev[1].record()
+            lists, _ = ca.select(p, r["cent_q"], r["cent_k"], keep_k, ws=ws)
+            if ev:
+                ev[2].record()
+            ca.attn_compensated(p, r["qp"], r["kp"], r["vp"], r["cent_k"], r["cent_v"],
+                                r["count_k"], lists, keep_k, r["perm_q"], out=out, ws=ws)
+            if ev:
+                ev[3].record()
+        return step
+
+    def attn_flops(keep_k):
+        # algorithmic flops of the attention launch: the selected keys, then
+        # the unselected clusters' centroids (4 d per query and key either way)
+        return (4.0 * d * c * c * keep_k * p.nqc * H
+                + 4.0 * d * c * (p.nkc - keep_k) * p.nqc * H)
+
+    keep_k = ca.keep_to_k(W["keep"], p.nkc)
+    # headline: warm-up, then exactly K timed steps between two synchronisations
+    ms_step, call_ms = _timed(torch, layer(keep_k), 4, args.steps, args.warmup)
+    print(f"headline: {ms_step:.3f} ms per layer", file=sys.stderr, flush=True)
     value = f_dense / (ms_step * 1e-3) / 1e12
-    # algorithmic flops of the attention launch: the selected keys, then the
-    # unselected clusters' centroids (4 d per query and key either way)
-    f_attn = 4.0 * d * c * c * keep_k * p.nqc * H
-    f_cent = 4.0 * d * c * (p.nkc - keep_k) * p.nqc * H
-    attn_tflops = (f_attn + f_cent) / (call_ms[2] * 1e-3) / 1e12
+    attn_tflops = attn_flops(keep_k) / (call_ms[2] * 1e-3) / 1e12
+    cl_bytes = cluster_bytes(H, n, d, 2, c)
+    cl_gbs = cl_bytes / (call_ms[0] * 1e-3) / 1e9
     rec = {
         "metric": "dense-equivalent attention TFLOP/s + end-to-end ms/layer (clustering incl.)",
         "value": round(value, 2),
@@ -506,7 +518,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": W["name"], "batch": 1, "heads": H, "seq_len": n, "head_dim": d,
                    "cluster_size": c, "keep": W["keep"], "kept_clusters": keep_k,
-                   "transform": "metric", "compensation": True},
+                   "key_clusters": p.nkc, "transform": "metric", "selection": "exact top-k",
+                   "compensation": True},
         "breakdown_ms": {"cluster": round(call_ms[0], 4), "select": round(call_ms[1], 4),
                          "attn_compensated": round(call_ms[2], 4)},
         "roofline": {"kernel": "attn_bf16_kernel<64,128,128,fused>", "bound": "mfma",
@@ -514,20 +527,81 @@ def main():
                      "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
                      "traffic": (ATTN_TRAFFIC["bytes"]
                                  if attn_fingerprint() == ATTN_TRAFFIC["fingerprint"] else None)},
+        "cluster_roofline": {"call": "ca_cluster", "bound": "hbm", "algorithmic_bytes": cl_bytes,
+                             "achieved": round(cl_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                             "frac": round(cl_gbs / PEAK_HBM_GBS, 4),
+                             "traffic": (CLUSTER_TRAFFIC["bytes"]
+                                         if cluster_fingerprint() == CLUSTER_TRAFFIC["fingerprint"]
+                                         else None)},
     }
-    if sep_ms is not None:
-        rec["separate_calls_ms"] = {"block_sparse_attn": round(sep_ms[0], 4),
-                                    "compensate": round(sep_ms[1], 4),
-                                    "sum": round(sep_ms[0] + sep_ms[1], 4)}
-    if not args.no_modes:
-        rec["modes"] = time_selection_modes(ca, torch, p, q, k, v, keep_k, out, args)
-    if not args.no_cpu_baseline:
-        t_head, threads = time_oracle(Qh[0], Kh[0], Vh[0], c, keep_k)
-        rec["cpu_baseline"] = {
-            "value": round(4.0 * n * n * d / t_head / 1e12, 5), "unit": "TFLOP/s",
-            "cores": threads, "kind": "oracle",
-            "sample": f"head 0 of {H}, full pipeline (clustering, selection, sparse attention, "
-                      f"compensation), fp64 NumPy, {t_head:.1f} s; {cpu_model()}"}
+    if not args.headline_only:
+        # the same layer keeping 1/4 of the key clusters
+        keep2 = ca.keep_to_k(W["keep2"], p.nkc)
+        ms2, c2 = _timed(torch, layer(keep2), 4, max(3, args.steps // 2), 1)
+        a2 = attn_flops(keep2) / (c2[2] * 1e-3) / 1e12
+        rec["keep_1/4"] = {"kept_clusters": keep2, "ms_per_layer": round(ms2, 4),
+                           "dense_equiv_tflops": round(f_dense / (ms2 * 1e-3) / 1e12, 2),
+                           "breakdown_ms": {"cluster": round(c2[0], 4), "select": round(c2[1], 4),
+                                            "attn_compensated": round(c2[2], 4)},
+                           "attention_tflops": round(a2, 2),
+                           "attention_mfma_frac": round(a2 / PEAK_BF16_TFLOPS, 4)}
+        # dense baseline: this library's attention with every key cluster kept
+        # (the exact dense softmax; compensation has nothing to add), on the
+        # clustered layout, no clustering or selection
+        r = ca.cluster(p, q, k, v, ws=ws)
+        all_lists = torch.arange(p.nkc, dtype=torch.int32, device=dev).expand(
+            H, p.nqc, p.nkc).contiguous()
+
+        def dense_step(ev=None):
+            if ev:
+                ev[0].record()
+            ca.attn_compensated(p, r["qp"], r["kp"], r["vp"], r["cent_k"], r["cent_v"],
+                                r["count_k"], all_lists, p.nkc, r["perm_q"], out=out, ws=ws)
+            if ev:
+                ev[1].record()
+
+        ms_d, c_d = _timed(torch, dense_step, 2, 3, 1)
+        f_all = 4.0 * d * c * c * p.nkc * p.nqc * H
+        rec["dense_baseline"] = {
+            "what": "ca_attn_compensated with all key clusters kept (exact dense attention)",
+            "ms_per_layer": round(c_d[0], 4),
+            "dense_tflops": round(f_dense / (c_d[0] * 1e-3) / 1e12, 2),
+            "attention_mfma_frac": round(f_all / (c_d[0] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "speedup_keep_1/16": round(c_d[0] / ms_step, 3),
+            "speedup_keep_1/4": round(c_d[0] / ms2, 3)}
+        del all_lists, r
+        # steps 3 and 4 as the two calls ca_block_sparse_attn + ca_compensate
+        def step_separate(ev=None):
+            r = ca.cluster(p, q, k, v, ws=ws)
+            lists, _ = ca.select(p, r["cent_q"], r["cent_k"], keep_k, ws=ws)
+            if ev:
+                ev[0].record()
+            op, lse = ca.block_sparse_attn(p, r["qp"], r["kp"], r["vp"], r["count_k"], lists,
+                                           keep_k)
+            if ev:
+                ev[1].record()
+            ca.compensate(p, r["qp"], r["cent_k"], r["cent_v"], r["count_k"], lists, keep_k, op,
+                          lse, r["perm_q"], out=out, ws=ws)
+            if ev:
+                ev[2].record()
+
+        _, sep = _timed(torch, step_separate, 3, min(args.steps, 10), 2)
+        rec["separate_calls_ms"] = {"block_sparse_attn": round(sep[0], 4),
+                                    "compensate": round(sep[1], 4),
+                                    "sum": round(sep[0] + sep[1], 4)}
+        if not args.no_modes:
+            rec["modes"] = time_selection_modes(ca, torch, p, q, k, v, keep_k, out, args)
+        if not args.no_cpu_baseline:
+            measured, est, threads, ns = time_oracle_sample(*head0, c, keep_k)
+            rec["cpu_baseline"] = {
+                "value": round(4.0 * n * n * d / est / 1e12, 5), "unit": "TFLOP/s",
+                "cores": threads, "kind": "oracle",
+                "sample": (f"head 0 of {H}: whole clustering (split spaces and splits of both "
+                           f"sides), centroids, scores and top-k, then block-sparse attention and "
+                           f"compensation of every 2nd query cluster ({ns} of {p.nqc}), fp64 "
+                           f"NumPy; {measured:.1f} s measured, {est:.1f} s estimated for the "
+                           f"whole head (attention and compensation scaled x{p.nqc / ns:g}); "
+                           f"value = 4 n^2 d of one head / that estimate; {cpu_model()}")}
     print(json.dumps(rec))
 
 

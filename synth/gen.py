@@ -25,11 +25,13 @@ import numpy as np
 
 
 def bf16_round(x: np.ndarray) -> np.ndarray:
-    """Round float32 values to the nearest bfloat16 (ties to even); return float32."""
-    b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    lsb = (b >> np.uint64(16)) & np.uint64(1)
-    b = (b + np.uint64(0x7FFF) + lsb) & np.uint64(0xFFFF0000)
-    return b.astype(np.uint32).view(np.float32)
+    """Round float32 values to the nearest bfloat16 (ties to even); return float32.
+    Finite inputs only (the largest finite pattern plus the rounding increment
+    still fits in 32 bits)."""
+    b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    lsb = (b >> np.uint32(16)) & np.uint32(1)
+    b = (b + (np.uint32(0x7FFF) + lsb)) & np.uint32(0xFFFF0000)
+    return b.view(np.float32)
 
 
 def keep_to_k(keep: float, n_kc: int) -> int:
@@ -145,22 +147,34 @@ def field_inputs(seed, heads, grid, d, dtype="bf16", corr_len=4.0, noise=0.2):
     return np.stack(qs), np.stack(ks), np.stack(vs)
 
 
-def make_config(cid, heads=None):
-    """Inputs of a named workload. ``heads`` selects a subset of head indices
-    (default: all); each head's draw depends only on (config id, head index)."""
+def _config_head(cid, h):
     cfg = CONFIGS[cid]
-    hs = range(cfg.heads) if heads is None else list(heads)
-    qs, ks, vs = [], [], []
-    for h in hs:
-        rng = np.random.default_rng([cid, int(h)])
-        if cfg.recipe == "mixture":
-            p = cfg.params
-            q, k, v = _mixture_head(rng, cfg.n, cfg.d, p["centres"], p.get("sigma"),
-                                    p.get("weights", "uniform"), p.get("aniso"),
-                                    p.get("outliers", 0.0))
-        else:
-            p = cfg.params
-            q, k, v = _field_head(rng, p["grid"], cfg.d, p["corr_len"], p["noise"])
-        q, k, v = _finish((q, k, v), cfg.dtype)
-        qs.append(q), ks.append(k), vs.append(v)
-    return np.stack(qs), np.stack(ks), np.stack(vs)
+    rng = np.random.default_rng([cid, int(h)])
+    p = cfg.params
+    if cfg.recipe == "mixture":
+        q, k, v = _mixture_head(rng, cfg.n, cfg.d, p["centres"], p.get("sigma"),
+                                p.get("weights", "uniform"), p.get("aniso"),
+                                p.get("outliers", 0.0))
+    else:
+        q, k, v = _field_head(rng, p["grid"], cfg.d, p["corr_len"], p["noise"])
+    return _finish((q, k, v), cfg.dtype)
+
+
+def _config_head_star(args):
+    return _config_head(*args)
+
+
+def make_config(cid, heads=None, workers=1):
+    """Inputs of a named workload. ``heads`` selects a subset of head indices
+    (default: all); each head's draw depends only on (config id, head index),
+    so ``workers`` > 1 draws heads in that many forked processes with the same
+    result. Fork before anything initialises a GPU in the calling process."""
+    cfg = CONFIGS[cid]
+    hs = list(range(cfg.heads) if heads is None else heads)
+    if workers > 1 and len(hs) > 1:
+        import multiprocessing as mp
+        with mp.get_context("fork").Pool(min(workers, len(hs))) as pool:
+            parts = pool.map(_config_head_star, [(cid, h) for h in hs])
+    else:
+        parts = [_config_head(cid, h) for h in hs]
+    return tuple(np.stack([pt[i] for pt in parts]) for i in range(3))
