@@ -32,17 +32,20 @@ __device__ __forceinline__ int head_sync_item(int wg, int nqc, int total) {
   return a < nqc && bh * nqc < total ? bh * nqc + a : -1;
 }
 
-// Keys per LDS stage: a whole key cluster, except at d = 128 with query and
-// key clusters of 128, where a stage holds half a key cluster (64 KB for the
-// two stages instead of 128 KB), so that two workgroups share a CU.
+// Keys per LDS stage: 64, so a key cluster of 128 is two stages. The two
+// stages then take 16 KB (d = 64) or 32 KB (d = 128) per buffer pair instead
+// of twice that, and the logits of a stage need half the registers: at d = 64
+// with query clusters of 128 three workgroups share a CU (three waves per
+// SIMD) instead of two, and at d = 128 two instead of one.
 template <int D, int CQ, int CK>
 constexpr int attn_stage_keys() {
-  return D == 128 && CQ == 128 && CK == 128 ? 64 : CK;
+  return CK == 128 ? 64 : CK;
 }
 
-// Waves per SIMD the bf16 kernel is compiled for (the second launch bound):
-// as many workgroups as their double-buffered stages fit in LDS, capped at two
-// waves per SIMD, so that the MFMA of one wave overlaps the softmax of another.
+// Waves per SIMD the bf16 kernel is compiled for (the second launch bound, a
+// minimum): as many workgroups as their double-buffered stages fit in LDS,
+// capped at two waves per SIMD, so that the MFMA of one wave overlaps the
+// softmax of another. Where registers and LDS allow, more workgroups run.
 template <int D, int CQ, int CK>
 constexpr int attn_waves_per_simd() {
   constexpr int by_lds = (160 * 1024) / (8 * D * attn_stage_keys<D, CQ, CK>());
@@ -141,30 +144,31 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   };
   const TileCopy<KROW, KLD, NW> kcopy(w, lane);
   const TileCopy<VROW, VLD, NW, 2 * CK> vcopy(w, lane);
+  // LDS: two key buffers, then two value buffers
   const uint32_t lds0 = lds_addr(smem);
+  const uint32_t ldsk = lds0, ldsv = lds0 + 2 * KBYTES;
   // stage g holds keys [HK (g % SUB), HK (g % SUB) + HK) of list entry g / SUB
-  auto issue = [&](int g, int stage) {
+  auto issue_k = [&](int g, int kb) __attribute__((always_inline)) {
     const int b = tile_id(g / SUB), s = g % SUB;
-    const bf16* kt = kp + ((size_t)bh * nk_pad + (size_t)b * CK + (size_t)s * HK) * D;
-    const bf16* vt = vp + ((size_t)bh * nkc + b) * (size_t)D * CK + (size_t)s * HK;
-    kcopy.issue(kt, lds0 + stage * STAGE, w);
-    vcopy.issue(vt, lds0 + stage * STAGE + KBYTES, w);
+    kcopy.issue(kp + ((size_t)bh * nk_pad + (size_t)b * CK + (size_t)s * HK) * D,
+                ldsk + kb * KBYTES, w);
   };
-  // fused: stage ng + c holds centroids [HK (c % SUBC), + HK) of centroid tile
-  // c / SUBC, with their bias row in cbias
+  auto issue_v = [&](int g, int vb) __attribute__((always_inline)) {
+    const int b = tile_id(g / SUB), s = g % SUB;
+    vcopy.issue(vp + ((size_t)bh * nkc + b) * (size_t)D * CK + (size_t)s * HK, ldsv + vb * VBYTES,
+                w);
+  };
+  // fused: centroid stage c holds centroids [HK (c % SUBC), + HK) of centroid
+  // tile c / SUBC, with their bias row in cbias
   const TileCopy<VROW, VLD, NW, 2 * kCompTile> ccopy(w, lane);
   const char* ctl = FUSED && nc ? fa.tiles + (size_t)bh * fa.ntile * CTILE : nullptr;
-  auto issue_any = [&](int g, int stage) {
-    if (!FUSED || g < nt * SUB) {
-      issue(g, stage);
-      return;
-    }
-    const int c = g - nt * SUB, s = c % SUBC;
+  auto issue_c = [&](int c, int kb, int vb, int sb) __attribute__((always_inline)) {
+    const int s = c % SUBC;
     const char* src = ctl + (size_t)(c / SUBC) * CTILE;
-    kcopy.issue(src + s * KBYTES, lds0 + stage * STAGE, w);
-    ccopy.issue(src + CTK + s * VROW, lds0 + stage * STAGE + KBYTES, w);
+    kcopy.issue(src + s * KBYTES, ldsk + kb * KBYTES, w);
+    ccopy.issue(src + CTK + s * VROW, ldsv + vb * VBYTES, w);
     const uint32_t boff = (uint32_t)(w * BLANES * 16);
-    const uint32_t bdst = __builtin_amdgcn_readfirstlane(lds_addr(&cbias[stage][0]) + boff);
+    const uint32_t bdst = __builtin_amdgcn_readfirstlane(lds_addr(&cbias[sb][0]) + boff);
     if (lane < BLANES) lds_dma16(src + CTK + CTV + s * HK * 4, boff + 16 * lane, bdst);
   };
   // Loop-invariant LDS read offsets (rows r and r + 32 share the swizzle key).
@@ -186,36 +190,12 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[dt][r] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
-
-  // Stage g (of ng = nt * SUB) sits in LDS stage g % 2. Its copy was issued
-  // at the start of stage g-1, right after the barrier that every wavefront
-  // passes only once done with stage g-2 (which used the same buffer), so one
-  // barrier per stage suffices and each copy has a whole stage of compute to
-  // land.
-  const int ng = nt * SUB, ngt = ng + nc;
   const float isl2 = 1.f / sl2;
-  auto body = [&](auto stage_tag, auto cen_tag, int g) {
-    constexpr int S = decltype(stage_tag)::value;
-    wait_vmcnt<0>();
-    wait_lgkm();
-    raw_barrier();
-    if (g + 1 < ngt) issue_any(g + 1, S ^ 1);
-    const char* ks = smem + S * STAGE;
-    const char* vs = ks + KBYTES;
-    constexpr bool cstage = decltype(cen_tag)::value;  // a centroid stage
-    if constexpr (cstage) {
-      // Selected clusters are covered by the sparse part: drop them here.
-      if (tid < HK) {
-        const int c = g - ng, b = (c / SUBC) * kCompTile + (c % SUBC) * HK + tid;
-        if (b < nkc && ((selmask[b >> 5] >> (b & 31)) & 1u)) cbias[S][tid] = -INFINITY;
-      }
-      wait_lgkm();
-      raw_barrier();  // bias row final
-    }
-    // keys of this stage past the cluster's count are padding
-    const int cnt = cstage ? HK : cnth[tile_id(g / SUB)] - (g % SUB) * HK;
+  f32x16 sacc[MT];   // logits of the current stage
+  bf16x8 pb[MT][2];  // its probabilities (bf16), the value product's operand
 
-    f32x16 sacc[MT];
+  // S^T = K Q^T for the stage in key buffer ks
+  auto logits = [&](const char* ks) __attribute__((always_inline)) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
@@ -226,54 +206,79 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
         sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qreg[kk], sacc[mt], 0, 0, 0);
       }
     }
+  };
+  // keys of a stage past its cluster's count are padding
+  auto mask_pad = [&](int cnt) __attribute__((always_inline)) {
     if (cnt < HK) {
+      // only the remainder cluster of a head. Accumulator r of row tile mt
+      // holds key 32 mt + 16 (r / 8) + 8 h + r % 8 (acc_key), so the test
+      // compares cnt - 8 h with constants and keeps no per-key registers.
+      const int ch = cnt - 8 * h;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-          if (acc_key(mt, r, h) >= cnt) sacc[mt][r] = -INFINITY;
+          if (32 * mt + 16 * (r >> 3) + (r & 7) >= ch) sacc[mt][r] = -INFINITY;
     }
-    if constexpr (cstage) {
-      // logit + log2|b| / sl2, so that the exponent below is sl2 q.kbar + log2|b| - m.
-      // The bias of accumulator r of row tile mt is that of key acc_key(mt, r, h):
-      // two runs of eight consecutive entries.
+  };
+  // probabilities of accumulator group (mt, s2) against the running maximum,
+  // added to the lane's row sum
+  auto exp_group = [&](int mt, int s2, float& ls) __attribute__((always_inline)) {
+    float pv[8];
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+    for (int j = 0; j < 8; ++j)
+      pv[j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[mt][8 * s2 + j], sl2, -m_run));
+    pb[mt][s2] = pack8(pv);
+    ls = sum8(pb[mt][s2], ls);
+  };
+  auto exps = [&]() __attribute__((always_inline)) {
+    float ls = 0.f;
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const float4 b0 = *(const float4*)&cbias[S][32 * mt + 16 * hh + 8 * h];
-          const float4 b1 = *(const float4*)&cbias[S][32 * mt + 16 * hh + 8 * h + 4];
-          const float bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int j = 0; j < 8; ++j)
-            sacc[mt][8 * hh + j] = __builtin_fmaf(bv[j], isl2, sacc[mt][8 * hh + j]);
+      for (int s2 = 0; s2 < 2; ++s2) exp_group(mt, s2, ls);
+    return ls;
+  };
+  // O^T += V^T P^T for the previous stage's probabilities, each group's two
+  // (DT) products issued right before that group's probabilities of this
+  // stage overwrite them, so the matrix cores run while the exponentials of
+  // the next group are formed
+  auto pv_exps = [&](const char* vs) __attribute__((always_inline)) {
+    float ls = 0.f;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          const bf16x8 av = *(const bf16x8*)(vs + 32 * dt * VROW + voff[mt][s2]);
+          oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[mt][s2], oacc[dt], 0, 0, 0);
         }
-    }
-    // Exponentials are taken against the running maximum without first
-    // forming this tile's maximum. Only a tile whose logits pass the running
-    // maximum by so much that a lane's row sum exceeds 2^40 is redone against
-    // its own maximum: always the first tile (m_run = -inf, so the sums are
-    // infinite), later ones only on a jump of about 2^33 in a probability.
-    // Below that, large exponentials cost no accuracy (fp32 and bf16 keep
-    // their relative precision at any scale).
-    float lsum;
-    bf16x8 pb[MT][2];
-    auto exps = [&]() {
-      lsum = 0.f;
+        exp_group(mt, s2, ls);
+      }
+    return ls;
+  };
+  auto pv = [&](const char* vs) __attribute__((always_inline)) {
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2) {
-          float pv[8];
-#pragma unroll
-          for (int j = 0; j < 8; ++j)
-            pv[j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[mt][8 * s2 + j], sl2, -m_run));
-          pb[mt][s2] = pack8(pv);
-          lsum = sum8(pb[mt][s2], lsum);
+          const bf16x8 av = *(const bf16x8*)(vs + 32 * dt * VROW + voff[mt][s2]);
+          oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[mt][s2], oacc[dt], 0, 0, 0);
         }
-    };
-    exps();
-    if (__builtin_amdgcn_ballot_w64(!(lsum <= 0x1p40f))) {
+  };
+  // Exponentials are taken against the running maximum without first
+  // forming the stage's maximum. Only a stage whose logits pass the running
+  // maximum by so much that a lane's row sum exceeds 2^40 is redone against
+  // its own maximum: always the first stage (m_run = -inf, so the sums are
+  // infinite), later ones only on a jump of about 2^33 in a probability.
+  // Below that, large exponentials cost no accuracy (fp32 and bf16 keep
+  // their relative precision at any scale). The output accumulated so far
+  // (all earlier stages) is rescaled to the new maximum.
+  auto settle = [&](float ls) __attribute__((always_inline)) {
+    if (__builtin_amdgcn_ballot_w64(!(ls <= 0x1p40f))) {
       float mx = -INFINITY;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
@@ -288,34 +293,88 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
       m_run = m_new;
-      exps();
+      ls = exps();
     }
-    l_run += lsum;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
+    l_run += ls;
+  };
+  auto sync_stage = [&]() __attribute__((always_inline)) {
+    wait_vmcnt<0>();
+    wait_lgkm();
+    raw_barrier();
+  };
+
+  // Key stages, software-pipelined one stage deep. Stage g's keys sit in key
+  // buffer g % 2 and its values in value buffer g % 2. At iteration g, after
+  // the one barrier (every wavefront is past iteration g-1, so key buffer
+  // (g+1) % 2 and value buffer g % 2 are free, and the copies issued at
+  // iteration g-1 have landed), the keys of stage g+1 and the values of stage
+  // g are copied; the logits of stage g are formed, then the value product of
+  // stage g-1 runs interleaved with the exponentials of stage g. The last
+  // value product follows the loop.
+  const int ng = nt * SUB;
+  const char* kbuf0 = smem;
+  const char* kbuf1 = smem + KBYTES;
+  const char* vbuf0 = smem + 2 * KBYTES;
+  const char* vbuf1 = smem + 2 * KBYTES + VBYTES;
+  issue_k(0, 0);
+  {
+    sync_stage();
+    if (1 < ng) issue_k(1, 1);
+    issue_v(0, 0);
+    logits(kbuf0);
+    mask_pad(cnth[tile_id(0)]);
+    settle(exps());
+  }
+  auto step = [&](auto par_tag, int g) __attribute__((always_inline)) {
+    constexpr int P = decltype(par_tag)::value;  // g % 2
+    sync_stage();
+    if (g + 1 < ng) issue_k(g + 1, P ^ 1);
+    issue_v(g, P);
+    logits(P ? kbuf1 : kbuf0);
+    mask_pad(cnth[tile_id(g / SUB)] - (g % SUB) * HK);
+    settle(pv_exps(P ? vbuf0 : vbuf1));
+  };
+  for (int g = 1; g < ng; g += 2) {
+    step(std::integral_constant<int, 1>{}, g);
+    if (g + 1 < ng) step(std::integral_constant<int, 0>{}, g + 1);
+  }
+  // the last key stage's value product; the first centroid stage's copies go
+  // to the free buffers (both key buffers, value buffer ng % 2) meanwhile
+  sync_stage();
+  if (FUSED && nc) issue_c(0, 0, ng & 1, 0);
+  pv((ng & 1) ? vbuf0 : vbuf1);
+  if constexpr (FUSED) {
+    // Centroid stages (compensation), after the keys and not pipelined:
+    // centroid stage c sits in key buffer c % 2, value buffer (ng + c) % 2
+    // and bias row c % 2. The selected clusters are covered by the sparse
+    // part: their bias is set to -inf once the row has landed.
+    for (int c = 0; c < nc; ++c) {
+      const int sb = c & 1, vb = (ng + c) & 1;
+      sync_stage();
+      if (c + 1 < nc) issue_c(c + 1, sb ^ 1, vb ^ 1, sb ^ 1);
+      if (tid < HK) {
+        const int b = (c / SUBC) * kCompTile + (c % SUBC) * HK + tid;
+        if (b < nkc && ((selmask[b >> 5] >> (b & 31)) & 1u)) cbias[sb][tid] = -INFINITY;
+      }
+      wait_lgkm();
+      raw_barrier();  // bias row final
+      logits(sb ? kbuf1 : kbuf0);
+      // logit + log2|b| / sl2, so that the exponent is sl2 q.kbar + log2|b| - m.
+      // The bias of accumulator r of row tile mt is that of key acc_key(mt, r, h):
+      // two runs of eight consecutive entries.
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) {
-          const bf16x8 av = *(const bf16x8*)(vs + 32 * dt * VROW + voff[mt][s2]);
-          oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[mt][s2], oacc[dt], 0, 0, 0);
+        for (int hh = 0; hh < 2; ++hh) {
+          const float4 b0 = *(const float4*)&cbias[sb][32 * mt + 16 * hh + 8 * h];
+          const float4 b1 = *(const float4*)&cbias[sb][32 * mt + 16 * hh + 8 * h + 4];
+          const float bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            sacc[mt][8 * hh + j] = __builtin_fmaf(bv[j], isl2, sacc[mt][8 * hh + j]);
         }
-  };
-
-  issue(0, 0);
-  using key_stage = std::false_type;
-  for (int g = 0; g < ng; g += 2) {
-    body(std::integral_constant<int, 0>{}, key_stage{}, g);
-    if (g + 1 < ng) body(std::integral_constant<int, 1>{}, key_stage{}, g + 1);
-  }
-  if constexpr (FUSED) {
-    // the centroid stages, in their own loop so that the key stages' code is
-    // that of the plain kernel
-    for (int g = ng; g < ngt; ++g) {
-      if (g & 1)
-        body(std::integral_constant<int, 1>{}, std::true_type{}, g);
-      else
-        body(std::integral_constant<int, 0>{}, std::true_type{}, g);
+      settle(exps());
+      pv(vb ? vbuf1 : vbuf0);
     }
   }
 
