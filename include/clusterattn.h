@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define CA_ABI_VERSION 6
+#define CA_ABI_VERSION 7
 
 #if defined(__GNUC__) || defined(__clang__)
 #define CA_API __attribute__((visibility("default")))
@@ -322,6 +322,33 @@ CA_API int ca_attn_compensated(const ca_problem* p, const void* qp, const void* 
                                const int32_t* lists, const int32_t* lens, int32_t k, float scale,
                                int32_t enable, const int32_t* perm_q, void* out, float* lse_out,
                                void* ws, size_t ws_bytes, void* stream);
+
+/* ca_attn_compensated without a workspace, for callers that cannot allocate
+ * device memory: code under HIP graph capture, serving loops and harnesses
+ * that forbid allocation. Same arguments and result as ca_attn_compensated
+ * (bit for bit; the same kernels run), minus ws and ws_bytes.
+ *
+ * The centroid tiles (compensation with unselected clusters:
+ * BH * ceil(nkc/128) * 128 * (4 d + 4) bytes, rounded up to 256) and the
+ * launch schedule (lens given: (16 + 8 * floor((5 * BH * nqc + 31) / 32)) * 4
+ * bytes) go to a scratch array that the library holds on every device it
+ * runs on: 32 MiB (33554432 bytes), part of the library's code object, kept
+ * until the process ends. Returns CA_E_WORKSPACE, with nothing enqueued,
+ * when a problem needs more; ca_attn_compensated with a workspace has no
+ * such limit. This call allocates nothing: no hipMalloc and no allocating
+ * library routine (the array's device address is looked up once per device,
+ * on the first call with that device current).
+ *
+ * All calls on one device share that device's array, which keeps the last
+ * call's contents. Calls that overlap in time on one device (on different
+ * streams, or from host threads without ordering between them) race and give
+ * wrong results; calls ordered on one stream are safe. */
+CA_API int ca_attn_compensated_noalloc(const ca_problem* p, const void* qp, const void* kp,
+                                       const void* vp, const float* cent_k, const float* cent_v,
+                                       const int32_t* count_k, const int32_t* lists,
+                                       const int32_t* lens, int32_t k, float scale,
+                                       int32_t enable, const int32_t* perm_q, void* out,
+                                       float* lse_out, void* stream);
 
 #ifdef __cplusplus
 }

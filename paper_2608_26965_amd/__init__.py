@@ -21,7 +21,8 @@ from ._lib import (CA_BF16, CA_F32, CA_LAYOUT_BHND, CA_LAYOUT_BNHD, CA_SPLIT_BAS
                    CA_XF_ADAPTIVE, CA_XF_METRIC, CA_XF_NONE, CA_XF_PCA, CA_XF_RANDOM, CAError)
 
 __all__ = ["Problem", "workspace_size", "cluster", "select", "select_hist", "block_sparse_attn",
-           "compensate", "attn_compensated", "forward", "CAError", "abi_version"]
+           "compensate", "attn_compensated", "attn_compensated_noalloc", "forward", "CAError",
+           "abi_version"]
 
 _XF = {"none": CA_XF_NONE, "pca": CA_XF_PCA, "metric": CA_XF_METRIC, "adaptive": CA_XF_ADAPTIVE,
        "random": CA_XF_RANDOM}
@@ -229,6 +230,27 @@ def attn_compensated(p: Problem, qp, kp, vp, cent_k, cent_v, count_k, lists, kee
                                          _ptr(out), _ptr(lse_out), _ptr(ws),
                                          0 if ws is None else ws.numel(), _stream(dev))
     _lib.check(st, "ca_attn_compensated")
+    return out, lse_out
+
+
+def attn_compensated_noalloc(p: Problem, qp, kp, vp, cent_k, cent_v, count_k, lists,
+                             keep_k: int, perm_q, scale: float = 0.0, enable: bool = True,
+                             want_lse: bool = False, out=None, lens=None):
+    """attn_compensated without a workspace: the library's per-device scratch
+    holds the centroid tiles and the schedule (see the header for its size
+    and for calls that overlap on one device). Allocates nothing when out
+    (and lse, with want_lse) are supplied by the caller: pass out= and, for
+    the lse, call the C function directly."""
+    dev = qp.device
+    if out is None:
+        out = torch.empty(p.shape(p.nq), dtype=p.dtype, device=dev)
+    lse_out = torch.empty(p.bh, p.nq, dtype=torch.float32, device=dev) if want_lse else None
+    st = _lib.load().ca_attn_compensated_noalloc(p.c(), _ptr(qp), _ptr(kp), _ptr(vp),
+                                                 _ptr(cent_k), _ptr(cent_v), _ptr(count_k),
+                                                 _ptr(lists), _ptr(lens), keep_k, float(scale),
+                                                 int(bool(enable)), _ptr(perm_q), _ptr(out),
+                                                 _ptr(lse_out), _stream(dev))
+    _lib.check(st, "ca_attn_compensated_noalloc")
     return out, lse_out
 
 

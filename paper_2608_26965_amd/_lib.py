@@ -24,6 +24,7 @@ EXPORTS = (
     "ca_block_sparse_attn",
     "ca_compensate",
     "ca_attn_compensated",
+    "ca_attn_compensated_noalloc",
 )
 
 _i32 = ctypes.c_int32
@@ -87,6 +88,9 @@ def load() -> ctypes.CDLL:
     lib.ca_attn_compensated.argtypes = [P, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32,
                                         ctypes.c_float, _i32, _vp, _vp, _vp, _vp, ctypes.c_size_t,
                                         _vp]
+    lib.ca_attn_compensated_noalloc.restype = ctypes.c_int
+    lib.ca_attn_compensated_noalloc.argtypes = [P, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32,
+                                                ctypes.c_float, _i32, _vp, _vp, _vp, _vp]
     _lib = lib
     return lib
 

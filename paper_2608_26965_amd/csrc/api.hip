@@ -6,7 +6,17 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "common.h"
+
+// Device memory of ca_attn_compensated_noalloc: the staged centroid tiles and
+// the launch schedule. Every device the library runs on holds its own copy,
+// from the code object's load until the process ends. Host code never uses
+// this name as an address: each device's address comes from
+// hipGetSymbolAddress (scratch_on_current_device below).
+static constexpr size_t kScratchBytes = (size_t)32 << 20;
+static __device__ __align__(256) char scratch[kScratchBytes];
 
 namespace {
 
@@ -82,6 +92,31 @@ int check_ws(const ca::Workspace& W, const void* ws, size_t ws_bytes) {
     return fail(CA_E_WORKSPACE, "workspace of %zu bytes, need %zu", ws_bytes, W.total);
   if (W.total > 0 && !ws) return fail(CA_E_INVALID, "workspace is NULL");
   if (((uintptr_t)ws & 255u) != 0) return fail(CA_E_INVALID, "workspace must be 256-byte aligned");
+  return CA_OK;
+}
+
+// The scratch array's address on the current device, looked up once per
+// device with that device current and kept.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_on_current_device(char** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return device_status(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(CA_E_UNSUPPORTED, "device %d: scratch is kept for devices 0..%d", dev,
+                kMaxDevices - 1);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return device_status(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(CA_E_DEVICE, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = (char*)p;
+  }
+  *out = g_scratch_ptr[dev];
   return CA_OK;
 }
 
@@ -334,6 +369,55 @@ int ca_attn_compensated(const ca_problem* p, const void* qp, const void* kp, con
   return device_status(ca::launch_attn_fused(P, qp, kp, vp, count_k, lists, lens, k, scale, tiles,
                                              perm_q, out, lse_out, sched, st),
                        "ca_attn_compensated");
+}
+
+int ca_attn_compensated_noalloc(const ca_problem* p, const void* qp, const void* kp,
+                                const void* vp, const float* cent_k, const float* cent_v,
+                                const int32_t* count_k, const int32_t* lists,
+                                const int32_t* lens, int32_t k, float scale, int32_t enable,
+                                const int32_t* perm_q, void* out, float* lse_out,
+                                void* stream) {
+  ca::Prob P;
+  int s = check_problem(p, &P);
+  if (s) return s;
+  if ((s = check_k(P, k))) return s;
+  if (P.dtype != CA_BF16)
+    return fail(CA_E_UNSUPPORTED, "ca_attn_compensated_noalloc needs bf16 inputs");
+  if (!qp || !kp || !vp || !count_k || !lists || !perm_q || !out)
+    return fail(CA_E_INVALID, "a required pointer of ca_attn_compensated_noalloc is NULL");
+  if (enable && (!cent_k || !cent_v))
+    return fail(CA_E_INVALID, "compensation needs cent_k and cent_v");
+  if ((s = check_attn_shape(P))) return s;
+  if (P.nkc > ca::kMaskWords * 32)
+    return fail(CA_E_UNSUPPORTED,
+                "ca_attn_compensated_noalloc supports at most 65536 key clusters");
+  // the same regions as the workspace of ca_attn_compensated: centroid
+  // tiles (compensation with unselected clusters), then the schedule (lens)
+  const bool comp = enable && (k < P.nkc || lens);
+  const size_t ntile = (size_t)(P.nkc + ca::kCompTile - 1) / ca::kCompTile;
+  const size_t tile_bytes =
+      comp ? ca::align256((size_t)P.BH * ntile * ca::comp_tile_bytes(P.d)) : 0;
+  const size_t sched_bytes =
+      lens ? ((size_t)8 + 8 * (size_t)ca::attn_sched_cap((int)((size_t)P.BH * P.nqc))) * 4 : 0;
+  if (tile_bytes + sched_bytes > kScratchBytes)
+    return fail(CA_E_WORKSPACE,
+                "ca_attn_compensated_noalloc: this problem needs %zu bytes of scratch, the "
+                "library holds %zu per device (use ca_attn_compensated with a workspace)",
+                tile_bytes + sched_bytes, kScratchBytes);
+  char* base = nullptr;
+  if (tile_bytes + sched_bytes > 0 && (s = scratch_on_current_device(&base))) return s;
+  char* tiles = comp ? base : nullptr;
+  int32_t* sched = lens ? (int32_t*)(base + tile_bytes) : nullptr;
+  if (!(scale > 0.0f)) scale = 1.0f / sqrtf((float)P.d);
+  hipStream_t st = (hipStream_t)stream;
+  if (tiles) {
+    s = device_status(ca::launch_comp_stage(P, cent_k, cent_v, count_k, tiles, st),
+                      "ca_attn_compensated_noalloc");
+    if (s) return s;
+  }
+  return device_status(ca::launch_attn_fused(P, qp, kp, vp, count_k, lists, lens, k, scale, tiles,
+                                             perm_q, out, lse_out, sched, st),
+                       "ca_attn_compensated_noalloc");
 }
 
 }  // extern "C"
