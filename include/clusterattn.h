@@ -291,7 +291,10 @@ CA_API int ca_block_sparse_attn(const ca_problem* p, const void* qp, const void*
  * [BH][nq] fp32 in original order. ws: device workspace of ws_bytes >=
  * ca_workspace_size(), where the bf16 path stages the centroids as bf16
  * tiles; required only for bf16 with enable != 0 and either k < nkc or lens
- * given (otherwise it may be NULL with ws_bytes 0). */
+ * given (otherwise it may be NULL with ws_bytes 0). Compensation keeps a
+ * selection bitmap of the key clusters per query cluster: with enable != 0
+ * and either k < nkc or lens given, more than 65536 key clusters return
+ * CA_E_UNSUPPORTED (enable == 0, or every cluster kept, has no such limit). */
 CA_API int ca_compensate(const ca_problem* p, const void* qp, const float* cent_k, const float* cent_v,
                   const int32_t* count_k, const int32_t* lists, const int32_t* lens, int32_t k,
                   float scale,

@@ -318,6 +318,12 @@ int ca_compensate(const ca_problem* p, const void* qp, const float* cent_k, cons
   if (enable && (!qp || !cent_k || !cent_v || !count_k || !lists))
     return fail(CA_E_INVALID, "compensation needs qp, cent_k, cent_v, count_k and lists");
   if ((s = check_attn_shape(P))) return s;
+  // the selection bitmap of a query cluster (in LDS) exists only when some
+  // cluster can be unselected and compensation runs
+  if (enable && (k < P.nkc || lens) && P.nkc > ca::kMaskWords * 32)
+    return fail(CA_E_UNSUPPORTED,
+                "ca_compensate: compensation supports at most %d key clusters (got %d; "
+                "enable = 0 has no such limit)", ca::kMaskWords * 32, P.nkc);
   char* tiles = nullptr;
   if (P.dtype == CA_BF16 && enable && (k < P.nkc || lens)) {
     ca::Workspace W;

@@ -506,7 +506,7 @@ hipError_t launch_comp(const Prob& P, const void* qp, const float* cent_k, const
                        float scale,
                        int enable, const void* op, const float* lse, const int32_t* perm_q,
                        void* out, float* lse_out, char* tiles, hipStream_t st) {
-  if (P.nkc > kMaskWords * 32) return hipErrorInvalidValue;
+  if (enable && (k < P.nkc || lens) && P.nkc > kMaskWords * 32) return hipErrorInvalidValue;
   if (P.dtype == CA_BF16) {
 #define CA_COMP_CASE(D, CQ) \
   if (P.d == D && P.cq == CQ) \

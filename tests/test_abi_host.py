@@ -154,3 +154,16 @@ def test_noalloc_rejects_oversize_before_enqueue():
     assert lib.ca_attn_compensated_noalloc(_prob(dtype=L.CA_F32), fake, fake, fake, fake, fake,
                                            fake, fake, None, 2, 0.0, 1, fake, fake, None,
                                            None) == L.CA_E_UNSUPPORTED
+
+
+def test_compensate_cluster_limit_only_when_compensating():
+    """The compensation's per-query-cluster selection bitmap holds 65536 key
+    clusters: more are refused (CA_E_UNSUPPORTED, with the count) when
+    compensation runs, before anything is enqueued."""
+    L, lib = _lib()
+    fake = 256
+    p = _prob(dtype=L.CA_F32, nq=64, nk=(1 << 21), cq=16, ck=16)  # 131072 key clusters
+    st = lib.ca_compensate(p, fake, fake, fake, fake, fake, None, 2, 0.0, 1, fake, fake, fake,
+                           fake, None, None, 0, None)
+    assert st == L.CA_E_UNSUPPORTED
+    assert "131072" in L.last_error()
