@@ -17,7 +17,8 @@ the same layer with the two calls ca_block_sparse_attn and ca_compensate, the
 selection modes, and the CPU oracle timed on a bounded sample of one head.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
-       [--no-modes] [--headline-only] [--configs] [--sweep] [--copy-calibration]
+       [--no-modes] [--headline-only] [--configs] [--sweep] [--quality]
+       [--copy-calibration]
 """
 from __future__ import annotations
 
@@ -403,6 +404,72 @@ def config_table(args):
         del ws, out
 
 
+# Rows of the quality table: (config, cluster size, keep fraction, transform).
+QUALITY_ROWS = (
+    [(2, 128, 1 / 8, "metric"), (2, 128, 1 / 8, "random"),
+     (3, 128, 1 / 16, "metric"), (3, 128, 1 / 4, "metric"), (3, 128, 1 / 16, "random"),
+     (4, 64, 1 / 4, "metric"), (4, 64, 1 / 4, "random")]
+    + [(5, c, keep, "metric") for c in (64, 128) for keep in (1 / 4, 1 / 8, 1 / 16)]
+    + [(5, 128, 1 / 8, "random")])
+
+
+def quality_table(args):
+    """How close the layer's output is to dense attention (the paper's
+    measure of the approximation: output similarity to the exact softmax
+    attention). Per row of QUALITY_ROWS, two generated heads run through the
+    layer (exact top-k, steps 3 and 4 in one pass) with compensation on and
+    off; for 512 sampled queries per head the exact dense attention output is
+    formed in fp32 on the GPU (scores against every key, softmax, values),
+    and the JSON line gives the relative L2 error ||o - o_dense|| /
+    ||o_dense|| over the sampled rows, the mean per-row relative error and
+    the mean cosine similarity of the rows."""
+    from synth import CONFIGS, make_config
+    import torch
+    import paper_2608_26965_amd as ca
+    dev = torch.device("cuda:0")
+    cache = {}
+    for cid, c, keep, xf in QUALITY_ROWS:
+        if cid not in cache:
+            cache.clear()
+            torch.cuda.empty_cache()
+            cache[cid] = tuple(torch.from_numpy(x[None]).to(dev).to(torch.bfloat16)
+                               for x in make_config(cid, heads=[0, 1]))
+        q, k, v = cache[cid]
+        H, n, d = q.shape[1:]
+        p = ca.Problem(1, H, n, n, d, c, c, torch.bfloat16, xf, "bhnd")
+        keep_k = ca.keep_to_k(keep, p.nkc)
+        ws = ca.workspace(p, dev, keep_k)
+        r = ca.cluster(p, q, k, v, ws=ws)
+        lists, _ = ca.select(p, r["cent_q"], r["cent_k"], keep_k, ws=ws)
+        g = torch.Generator(device="cpu").manual_seed(cid * 1000 + c)
+        rows = torch.randint(0, n, (H, 512), generator=g).to(dev)
+        dense = []
+        for h in range(H):
+            qs = q[0, h, rows[h]].float()
+            s = (qs @ k[0, h].float().T) / math.sqrt(d)
+            dense.append(torch.softmax(s, dim=1) @ v[0, h].float())
+        dense = torch.stack(dense)
+        res = {}
+        for comp in (True, False):
+            out, _ = ca.attn_compensated(p, r["qp"], r["kp"], r["vp"], r["cent_k"], r["cent_v"],
+                                         r["count_k"], lists, keep_k, r["perm_q"], enable=comp,
+                                         ws=ws)
+            got = torch.stack([out[0, h, rows[h]].float() for h in range(H)])
+            err = (got - dense).flatten(0, 1)
+            ref_rows = dense.flatten(0, 1)
+            got_rows = got.flatten(0, 1)
+            res["compensated" if comp else "uncompensated"] = {
+                "rel_l2": round(float(err.norm() / ref_rows.norm()), 5),
+                "mean_row_rel_l2": round(float((err.norm(dim=1) / ref_rows.norm(dim=1)).mean()), 5),
+                "mean_cosine": round(float(torch.nn.functional.cosine_similarity(
+                    got_rows, ref_rows, dim=1).mean()), 5)}
+        print(json.dumps({"table": "quality_vs_dense", "config": CONFIGS[cid].name, "n": n,
+                          "d": d, "c": c, "keep": keep, "kept_clusters": keep_k,
+                          "key_clusters": p.nkc, "transform": xf, "heads_sampled": H,
+                          "rows_per_head": 512, **res}), flush=True)
+        del ws, r, lists
+
+
 def copy_calibration():
     """A plain device copy of 256 MiB (fp32), three launches."""
     import torch
@@ -433,6 +500,9 @@ def main():
                     help="time only the headline layer (no keep-1/4 layer, dense baseline, "
                          "two-call layer, modes or CPU baseline): the profiling runs use it, so "
                          "that the attention kernel's launches are all the headline's")
+    ap.add_argument("--quality", action="store_true",
+                    help="output quality against dense attention per configuration instead of "
+                         "the headline run: one JSON line each")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy three times: the known-size "
                          "reference that scales the FETCH_SIZE / WRITE_SIZE counters")
@@ -445,6 +515,9 @@ def main():
         return
     if args.configs:
         config_table(args)
+        return
+    if args.quality:
+        quality_table(args)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: ClusterAttention's heads are independent, so a "

@@ -36,17 +36,18 @@ def _pipeline(p, q, k, v, keep_k, comp=True, fused=False):
 
 
 def _run_config(cid, heads, c, keep, comp=True, check_heads=None, nsample=12, split="diag",
-                fused=False):
+                fused=False, ck=None):
     import torch
     import paper_2608_26965_amd as ca
     from tests import gpu_util as G
     cfg = CONFIGS[cid]
-    G.flush(f"e2e config {cid} heads={len(heads)} c={c} keep={keep} comp={comp} split={split} "
-            f"fused={fused}")
+    ck = c if ck is None else ck
+    G.flush(f"e2e config {cid} heads={len(heads)} cq={c} ck={ck} keep={keep} comp={comp} "
+            f"split={split} fused={fused}")
     Q, K, V = make_config(cid, heads=heads)
     H, n, d = Q.shape
     dt = cfg.dtype
-    p = ca.Problem(1, H, n, n, d, c, c, G.tdtype(dt), "metric", split=split)
+    p = ca.Problem(1, H, n, n, d, c, ck, G.tdtype(dt), "metric", split=split)
     k = keep_to_k(keep, p.nkc)
     tq, tk, tv = (G.dev(x[None], G.tdtype(dt)) for x in (Q, K, V))
     r, lists, scores, out, lse = _pipeline(p, tq, tk, tv, k, comp, fused)
@@ -56,7 +57,8 @@ def _run_config(cid, heads, c, keep, comp=True, check_heads=None, nsample=12, sp
     worst = 0.0
     for h in (check_heads if check_heads is not None else range(H)):
         worst = max(worst, check_head(Q[h], K[h], V[h], r, lists, scores, outh, h, c, k, dt,
-                                      nsample, comp, seed=cid * 100 + h, split=split, lse=lseh))
+                                      nsample, comp, seed=cid * 100 + h, split=split, lse=lseh,
+                                      ck=ck))
     G.flush(f"  worst sampled error {worst:.3g}")
     return r, lists, out
 
@@ -96,6 +98,22 @@ def test_tabular_bench_workload_fused():
     """The benchmarked workload, all 8 heads, with steps 3 and 4 in one pass
     (ca_attn_compensated), against the oracle like the four separate calls."""
     _run_config(2, list(range(8)), 128, 1 / 8, check_heads=[0, 3, 7], fused=True)
+
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_tabular_query64_key128_all_heads(fused):
+    """The paper's evaluated tile shape, query clusters of 64 and key
+    clusters of 128, on the tabular workload (all 8 heads, keep 1/8 of the
+    key clusters): each side split with its own cluster size, selection, and
+    steps 3 and 4 in one pass or as two calls, against the oracle."""
+    _run_config(2, list(range(8)), 64, 1 / 8, check_heads=[0, 7], nsample=12, fused=fused, ck=128)
+
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_video_720p_query64_key128(fused):
+    """Query clusters of 64 and key clusters of 128 at d = 128 (one 720p head,
+    keep 1/8, remainder clusters of 16 queries and 80 keys)."""
+    _run_config(5, [0], 64, 1 / 8, nsample=8, fused=fused, ck=128)
 
 
 @pytest.mark.parametrize("c,keep", [(64, 1 / 16), (128, 1 / 8)])
