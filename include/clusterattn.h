@@ -42,8 +42,9 @@
  * - Every output element is written (including padding rows). Outputs must not
  *   alias inputs. Results are deterministic: two identical calls give
  *   bit-identical outputs.
- * - Non-finite inputs (NaN/Inf) are not checked: the calls stay memory-safe
- *   but the results are unspecified.
+ * - Non-finite inputs (NaN/Inf) are not checked by the steps: the calls stay
+ *   memory-safe but the results are unspecified. Checked mode is the separate
+ *   call ca_check_finite, which flags them on the device.
  * - Calls on different streams may run concurrently if their outputs and
  *   workspaces do not overlap.
  */
@@ -57,7 +58,7 @@
 extern "C" {
 #endif
 
-#define CA_ABI_VERSION 7
+#define CA_ABI_VERSION 8
 
 #if defined(__GNUC__) || defined(__clang__)
 #define CA_API __attribute__((visibility("default")))
@@ -70,7 +71,10 @@ typedef enum {
   CA_E_INVALID = 1,     /* bad argument: null pointer, size out of range, c not a power of two, k not in [1, nkc] */
   CA_E_UNSUPPORTED = 2, /* valid but not built: e.g. bf16 attention with d not in {64, 128} */
   CA_E_WORKSPACE = 3,   /* workspace smaller than ca_workspace_size() */
-  CA_E_DEVICE = 4       /* HIP reported an error while enqueueing */
+  CA_E_DEVICE = 4,      /* HIP reported an error while enqueueing */
+  CA_E_NONFINITE = 5    /* checked mode: an input holds NaN or Inf (reported by the caller's
+                           read of ca_check_finite's flags; no call returns it itself, since
+                           the library never synchronises) */
 } ca_status;
 
 typedef enum { CA_F32 = 0, CA_BF16 = 1 } ca_dtype;
@@ -131,8 +135,11 @@ typedef enum {
 typedef enum { CA_SPLIT_DIAG = 0, CA_SPLIT_BASIC = 1 } ca_split;
 
 /* Layout of Q, K, V and the final output: BHND = [B][H][N][d],
- * BNHD = [B][N][H][d] (the usual activation layout of a transformer). */
-typedef enum { CA_LAYOUT_BHND = 0, CA_LAYOUT_BNHD = 1 } ca_layout;
+ * BNHD = [B][N][H][d] (the usual activation layout of a transformer), both
+ * dense; STRIDED = any element strides given in the problem (for instance
+ * views of a fused QKV projection, [B][N][3][H][d], with the output in a
+ * tensor of its own). In every layout the last dimension is contiguous. */
+typedef enum { CA_LAYOUT_BHND = 0, CA_LAYOUT_BNHD = 1, CA_LAYOUT_STRIDED = 2 } ca_layout;
 
 typedef struct {
   int32_t batch, heads;  /* >= 1 */
@@ -143,6 +150,14 @@ typedef struct {
   int32_t transform;     /* ca_transform (ca_cluster only) */
   int32_t layout;        /* ca_layout of Q/K/V/out */
   int32_t split;         /* ca_split (ca_cluster only) */
+  /* CA_LAYOUT_STRIDED only (ignored by the dense layouts): element strides
+   * {batch, head, token} of q, k, v and the output; element (b, h, i, t) of
+   * q sits at q + b q_stride[0] + h q_stride[1] + i q_stride[2] + t. Each
+   * stride is >= 0 and a multiple of 16 bytes' worth of elements (8 for
+   * bf16, 4 for fp32), and the tensors' base pointers are 16-byte aligned,
+   * so that rows can be read and written in 16-byte pieces. The output's
+   * rows must not overlap one another or any input (not checked). */
+  int64_t q_stride[3], k_stride[3], v_stride[3], out_stride[3];
 } ca_problem;
 
 /* Outputs of ca_cluster. Required unless marked optional. */
@@ -325,6 +340,17 @@ CA_API int ca_attn_compensated(const ca_problem* p, const void* qp, const void* 
                                const int32_t* lists, const int32_t* lens, int32_t k, float scale,
                                int32_t enable, const int32_t* perm_q, void* out, float* lse_out,
                                void* ws, size_t ws_bytes, void* stream);
+
+/* Checked mode (the method is defined for finite query, key and value
+ * vectors; Method: Overview). Scans q, k and v (v may be NULL) in the
+ * problem's layout and writes flags[0] on the stream: bit 0 if q holds a NaN
+ * or an infinity, bit 1 for k, bit 2 for v; 0 when all are finite. flags: one
+ * device int32, cleared by this call before the scan (no memset is
+ * recorded); read it once the stream has passed the call, and treat a
+ * non-zero value as CA_E_NONFINITE. Reads each input once (an HBM pass over
+ * q, k and v). */
+CA_API int ca_check_finite(const ca_problem* p, const void* q, const void* k, const void* v,
+                           int32_t* flags, void* stream);
 
 /* ca_attn_compensated without a workspace, for callers that cannot allocate
  * device memory: code under HIP graph capture, serving loops and harnesses

@@ -17,16 +17,17 @@ from dataclasses import dataclass
 import torch
 
 from . import _lib
-from ._lib import (CA_BF16, CA_F32, CA_LAYOUT_BHND, CA_LAYOUT_BNHD, CA_SPLIT_BASIC, CA_SPLIT_DIAG,
-                   CA_XF_ADAPTIVE, CA_XF_METRIC, CA_XF_NONE, CA_XF_PCA, CA_XF_RANDOM, CAError)
+from ._lib import (CA_BF16, CA_F32, CA_LAYOUT_BHND, CA_LAYOUT_BNHD, CA_LAYOUT_STRIDED,
+                   CA_SPLIT_BASIC, CA_SPLIT_DIAG, CA_XF_ADAPTIVE, CA_XF_METRIC, CA_XF_NONE,
+                   CA_XF_PCA, CA_XF_RANDOM, CAError)
 
-__all__ = ["Problem", "workspace_size", "cluster", "select", "select_hist", "block_sparse_attn",
-           "compensate", "attn_compensated", "attn_compensated_noalloc", "forward", "CAError",
-           "abi_version"]
+__all__ = ["Problem", "bhnd_strides", "workspace_size", "cluster", "select", "select_hist", "block_sparse_attn",
+           "compensate", "attn_compensated", "attn_compensated_noalloc", "check_finite",
+           "forward", "CAError", "abi_version"]
 
 _XF = {"none": CA_XF_NONE, "pca": CA_XF_PCA, "metric": CA_XF_METRIC, "adaptive": CA_XF_ADAPTIVE,
        "random": CA_XF_RANDOM}
-_LAYOUT = {"bhnd": CA_LAYOUT_BHND, "bnhd": CA_LAYOUT_BNHD}
+_LAYOUT = {"bhnd": CA_LAYOUT_BHND, "bnhd": CA_LAYOUT_BNHD, "strided": CA_LAYOUT_STRIDED}
 _SPLIT = {"diag": CA_SPLIT_DIAG, "basic": CA_SPLIT_BASIC}
 _DT = {torch.float32: CA_F32, torch.bfloat16: CA_BF16}
 
@@ -48,6 +49,11 @@ class Problem:
     transform: str = "metric"
     layout: str = "bhnd"
     split: str = "diag"
+    # layout "strided": element strides (batch, head, token) of q, k, v, out
+    q_stride: tuple = (0, 0, 0)
+    k_stride: tuple = (0, 0, 0)
+    v_stride: tuple = (0, 0, 0)
+    out_stride: tuple = (0, 0, 0)
 
     @property
     def bh(self):
@@ -70,14 +76,28 @@ class Problem:
         return self.nkc * self.ck
 
     def c(self) -> _lib.CaProblem:
+        st = [(__import__("ctypes").c_int64 * 3)(*t) for t in
+              (self.q_stride, self.k_stride, self.v_stride, self.out_stride)]
         return _lib.CaProblem(self.batch, self.heads, self.nq, self.nk, self.d, self.cq, self.ck,
                               _DT[self.dtype], _XF[self.transform], _LAYOUT[self.layout],
-                              _SPLIT[self.split])
+                              _SPLIT[self.split], *st)
 
     def shape(self, n):
-        if self.layout == "bhnd":
+        """Shape of a dense output tensor: [B,H,n,d] for "bhnd" and "strided"
+        (whose out_stride must then describe it; see bhnd_strides), else
+        [B,n,H,d]."""
+        if self.layout in ("bhnd", "strided"):
             return (self.batch, self.heads, n, self.d)
         return (self.batch, n, self.heads, self.d)
+
+
+def bhnd_strides(t) -> tuple:
+    """(batch, head, token) element strides of a tensor viewed as [B,H,N,d]
+    with its last dimension contiguous (any permutation or slice of a larger
+    tensor, e.g. one third of a fused [B,N,3,H,d] projection)."""
+    if t.dim() != 4 or t.stride(3) != 1:
+        raise ValueError("expected a [B,H,N,d] view whose last dimension is contiguous")
+    return (t.stride(0), t.stride(1), t.stride(2))
 
 
 def _ptr(t):
@@ -254,6 +274,22 @@ def attn_compensated_noalloc(p: Problem, qp, kp, vp, cent_k, cent_v, count_k, li
     return out, lse_out
 
 
+def check_finite(p: Problem, q, k, v=None, *, raise_error=True) -> int:
+    """Checked mode: ca_check_finite on the current stream, then a
+    synchronisation to read its flags (bit 0 q, 1 k, 2 v hold a NaN or an
+    infinity). Raises CAError with CA_E_NONFINITE when raise_error and any bit
+    is set; returns the flags."""
+    flags = torch.empty(1, dtype=torch.int32, device=q.device)
+    st = _lib.load().ca_check_finite(p.c(), _ptr(q), _ptr(k), _ptr(v), _ptr(flags),
+                                     _stream(q.device))
+    _lib.check(st, "ca_check_finite")
+    f = int(flags.item())
+    if f and raise_error:
+        which = ", ".join(n for b, n in ((1, "q"), (2, "k"), (4, "v")) if f & b)
+        raise CAError(_lib.CA_E_NONFINITE, "ca_check_finite", f"non-finite values in {which}")
+    return f
+
+
 def keep_to_k(keep: float, n_kc: int) -> int:
     """Kept key clusters for a keep fraction: ceil(keep * n_kc), in [1, n_kc]."""
     return max(1, min(n_kc, int(math.ceil(keep * n_kc - 1e-9))))
@@ -261,9 +297,12 @@ def keep_to_k(keep: float, n_kc: int) -> int:
 
 def forward(q, k, v, cq=128, ck=None, keep=None, keep_k=None, transform="metric",
             compensation=True, scale=None, layout="bhnd", return_parts=False, select="topk",
-            mass_recall=0.9, min_count=16, one_pass=True):
+            mass_recall=0.9, min_count=16, one_pass=True, checked=False):
     """ClusterAttention for one layer. q, k, v: [B,H,N,d] ("bhnd") or [B,N,H,d]
-    ("bnhd"), bf16 or fp32, on one GPU.
+    ("bnhd"), bf16 or fp32, on one GPU; with layout="strided", any [B,H,N,d]
+    views whose last dimension is contiguous (for instance slices of a fused
+    [B,N,3,H,d] projection), read in place; the output is then a new dense
+    [B,H,N,d] tensor.
 
     select="topk": exact top-k of either a fraction (``keep``) or a count
     (``keep_k``) of key clusters per query cluster; select="hist": the
@@ -271,15 +310,25 @@ def forward(q, k, v, cq=128, ck=None, keep=None, keep_k=None, transform="metric"
     attention-mass recall ``mass_recall`` with at least ``min_count`` clusters
     (use it with transform="adaptive"). bf16 layers run steps 3 and 4 in one
     pass (attn_compensated) unless one_pass is False or return_parts asks for
-    the sparse part's output and lse."""
+    the sparse part's output and lse. checked=True first runs the checked
+    mode (check_finite), which synchronises and raises CAError with
+    CA_E_NONFINITE on NaN or Inf inputs."""
     ck = cq if ck is None else ck
-    if layout == "bhnd":
+    if layout in ("bhnd", "strided"):
         B, H, nq, d = q.shape
         nk = k.shape[2]
     else:
         B, nq, H, d = q.shape
         nk = k.shape[1]
-    p = Problem(B, H, nq, nk, d, cq, ck, q.dtype, transform, layout)
+    if layout == "strided":
+        dense_out = (H * nq * d, nq * d, d)
+        p = Problem(B, H, nq, nk, d, cq, ck, q.dtype, transform, layout,
+                    q_stride=bhnd_strides(q), k_stride=bhnd_strides(k), v_stride=bhnd_strides(v),
+                    out_stride=dense_out)
+    else:
+        p = Problem(B, H, nq, nk, d, cq, ck, q.dtype, transform, layout)
+    if checked:
+        check_finite(p, q, k, v)
     if keep_k is None:
         keep_k = keep_to_k(1.0 / 8 if keep is None else keep, p.nkc)
     sc = 0.0 if scale is None else float(scale)

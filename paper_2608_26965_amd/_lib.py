@@ -7,10 +7,10 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libclusterattn.so")
 
-CA_OK, CA_E_INVALID, CA_E_UNSUPPORTED, CA_E_WORKSPACE, CA_E_DEVICE = range(5)
+CA_OK, CA_E_INVALID, CA_E_UNSUPPORTED, CA_E_WORKSPACE, CA_E_DEVICE, CA_E_NONFINITE = range(6)
 CA_F32, CA_BF16 = 0, 1
 CA_XF_NONE, CA_XF_PCA, CA_XF_METRIC, CA_XF_ADAPTIVE, CA_XF_RANDOM = 0, 1, 2, 3, 4
-CA_LAYOUT_BHND, CA_LAYOUT_BNHD = 0, 1
+CA_LAYOUT_BHND, CA_LAYOUT_BNHD, CA_LAYOUT_STRIDED = 0, 1, 2
 CA_SPLIT_DIAG, CA_SPLIT_BASIC = 0, 1
 
 EXPORTS = (
@@ -25,6 +25,7 @@ EXPORTS = (
     "ca_compensate",
     "ca_attn_compensated",
     "ca_attn_compensated_noalloc",
+    "ca_check_finite",
 )
 
 _i32 = ctypes.c_int32
@@ -32,8 +33,10 @@ _vp = ctypes.c_void_p
 
 
 class CaProblem(ctypes.Structure):
-    _fields_ = [(n, _i32) for n in ("batch", "heads", "nq", "nk", "d", "cq", "ck", "dtype",
-                                    "transform", "layout", "split")]
+    _fields_ = ([(n, _i32) for n in ("batch", "heads", "nq", "nk", "d", "cq", "ck", "dtype",
+                                     "transform", "layout", "split")]
+                + [(n, ctypes.c_int64 * 3) for n in ("q_stride", "k_stride", "v_stride",
+                                                     "out_stride")])
 
 
 class CaClusterOut(ctypes.Structure):
@@ -91,6 +94,8 @@ def load() -> ctypes.CDLL:
     lib.ca_attn_compensated_noalloc.restype = ctypes.c_int
     lib.ca_attn_compensated_noalloc.argtypes = [P, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32,
                                                 ctypes.c_float, _i32, _vp, _vp, _vp, _vp]
+    lib.ca_check_finite.restype = ctypes.c_int
+    lib.ca_check_finite.argtypes = [P, _vp, _vp, _vp, _vp, _vp]
     _lib = lib
     return lib
 

@@ -56,7 +56,8 @@ int check_problem(const ca_problem* p, ca::Prob* P) {
   if (p->dtype != CA_F32 && p->dtype != CA_BF16) return fail(CA_E_INVALID, "unknown dtype");
   if (p->transform < CA_XF_NONE || p->transform > CA_XF_RANDOM)
     return fail(CA_E_INVALID, "unknown transform");
-  if (p->layout != CA_LAYOUT_BHND && p->layout != CA_LAYOUT_BNHD)
+  if (p->layout != CA_LAYOUT_BHND && p->layout != CA_LAYOUT_BNHD &&
+      p->layout != CA_LAYOUT_STRIDED)
     return fail(CA_E_INVALID, "unknown layout");
   if (p->split != CA_SPLIT_DIAG && p->split != CA_SPLIT_BASIC)
     return fail(CA_E_INVALID, "unknown split");
@@ -79,6 +80,49 @@ int check_problem(const ca_problem* p, ca::Prob* P) {
   P->nq_pad = P->nqc * p->cq;
   P->nk_pad = P->nkc * p->ck;
   P->esize = p->dtype == CA_BF16 ? 2 : 4;
+  // element strides of q, k, v and the output
+  auto dense = [&](int n) {
+    ca::Lay L;
+    L.H = p->heads;
+    if (p->layout == CA_LAYOUT_BHND) {
+      L.sn = p->d;
+      L.sh = (int64_t)n * p->d;
+      L.sb = (int64_t)p->heads * n * p->d;
+    } else {
+      L.sh = p->d;
+      L.sn = (int64_t)p->heads * p->d;
+      L.sb = (int64_t)n * p->heads * p->d;
+    }
+    return L;
+  };
+  if (p->layout == CA_LAYOUT_STRIDED) {
+    const int64_t unit = 16 / (int64_t)P->esize;
+    const int64_t* st[4] = {p->q_stride, p->k_stride, p->v_stride, p->out_stride};
+    const char* nm[4] = {"q", "k", "v", "out"};
+    ca::Lay* dst[4] = {&P->lq, &P->lk, &P->lv, &P->lo};
+    for (int t = 0; t < 4; ++t) {
+      for (int j = 0; j < 3; ++j)
+        if (st[t][j] < 0 || st[t][j] % unit != 0)
+          return fail(CA_E_INVALID,
+                      "%s_stride[%d] = %lld: strides must be >= 0 and multiples of %lld elements",
+                      nm[t], j, (long long)st[t][j], (long long)unit);
+      dst[t]->sb = st[t][0];
+      dst[t]->sh = st[t][1];
+      dst[t]->sn = st[t][2];
+      dst[t]->H = p->heads;
+    }
+  } else {
+    P->lq = P->lo = dense(p->nq);
+    P->lk = P->lv = dense(p->nk);
+  }
+  return CA_OK;
+}
+
+// The 16-byte alignment strided tensors need (the dense layouts keep their
+// own row alignment).
+int check_aligned(const ca::Prob& P, const void* x, const char* what) {
+  if (P.layout == CA_LAYOUT_STRIDED && ((uintptr_t)x & 15u) != 0)
+    return fail(CA_E_INVALID, "%s must be 16-byte aligned with CA_LAYOUT_STRIDED", what);
   return CA_OK;
 }
 
@@ -193,6 +237,7 @@ const char* ca_status_str(int status) {
     case CA_E_UNSUPPORTED: return "CA_E_UNSUPPORTED: combination not built";
     case CA_E_WORKSPACE: return "CA_E_WORKSPACE: workspace too small";
     case CA_E_DEVICE: return "CA_E_DEVICE: HIP error";
+    case CA_E_NONFINITE: return "CA_E_NONFINITE: an input holds NaN or Inf";
     default: return "unknown status";
   }
 }
@@ -224,6 +269,9 @@ int ca_cluster(const ca_problem* p, const void* q, const void* k, const void* v,
   bool want_v = v != nullptr;
   if (want_v && (!out->cent_v || !out->vp))
     return fail(CA_E_INVALID, "v given but cent_v or vp is NULL");
+  if ((s = check_aligned(P, q, "q")) || (s = check_aligned(P, k, "k")) ||
+      (want_v && (s = check_aligned(P, v, "v"))))
+    return s;
   ca::Workspace W;
   ca::plan_workspace(P, &W);
   if ((s = check_ws(W, ws, ws_bytes))) return s;
@@ -315,6 +363,7 @@ int ca_compensate(const ca_problem* p, const void* qp, const float* cent_k, cons
   if ((s = check_k(P, k))) return s;
   if (!op || !lse || !perm_q || !out)
     return fail(CA_E_INVALID, "a required pointer of ca_compensate is NULL");
+  if ((s = check_aligned(P, out, "out"))) return s;
   if (enable && (!qp || !cent_k || !cent_v || !count_k || !lists))
     return fail(CA_E_INVALID, "compensation needs qp, cent_k, cent_v, count_k and lists");
   if ((s = check_attn_shape(P))) return s;
@@ -350,6 +399,7 @@ int ca_attn_compensated(const ca_problem* p, const void* qp, const void* kp, con
   if (P.dtype != CA_BF16) return fail(CA_E_UNSUPPORTED, "ca_attn_compensated needs bf16 inputs");
   if (!qp || !kp || !vp || !count_k || !lists || !perm_q || !out)
     return fail(CA_E_INVALID, "a required pointer of ca_attn_compensated is NULL");
+  if ((s = check_aligned(P, out, "out"))) return s;
   if (enable && (!cent_k || !cent_v))
     return fail(CA_E_INVALID, "compensation needs cent_k and cent_v");
   if ((s = check_attn_shape(P))) return s;
@@ -391,6 +441,7 @@ int ca_attn_compensated_noalloc(const ca_problem* p, const void* qp, const void*
     return fail(CA_E_UNSUPPORTED, "ca_attn_compensated_noalloc needs bf16 inputs");
   if (!qp || !kp || !vp || !count_k || !lists || !perm_q || !out)
     return fail(CA_E_INVALID, "a required pointer of ca_attn_compensated_noalloc is NULL");
+  if ((s = check_aligned(P, out, "out"))) return s;
   if (enable && (!cent_k || !cent_v))
     return fail(CA_E_INVALID, "compensation needs cent_k and cent_v");
   if ((s = check_attn_shape(P))) return s;
@@ -424,6 +475,19 @@ int ca_attn_compensated_noalloc(const ca_problem* p, const void* qp, const void*
   return device_status(ca::launch_attn_fused(P, qp, kp, vp, count_k, lists, lens, k, scale, tiles,
                                              perm_q, out, lse_out, sched, st),
                        "ca_attn_compensated_noalloc");
+}
+
+int ca_check_finite(const ca_problem* p, const void* q, const void* k, const void* v,
+                    int32_t* flags, void* stream) {
+  ca::Prob P;
+  int s = check_problem(p, &P);
+  if (s) return s;
+  if (!q || !k || !flags) return fail(CA_E_INVALID, "q, k and flags are required");
+  if ((s = check_aligned(P, q, "q")) || (s = check_aligned(P, k, "k")) ||
+      (v && (s = check_aligned(P, v, "v"))))
+    return s;
+  return device_status(ca::launch_check_finite(P, q, k, v, flags, (hipStream_t)stream),
+                       "ca_check_finite");
 }
 
 }  // extern "C"

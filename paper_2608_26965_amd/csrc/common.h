@@ -45,18 +45,25 @@ __device__ __forceinline__ uint32_t ordered_bits(float f) {
 
 // ---- problem description ---------------------------------------------------
 
+// Element strides of a [B][H][N][d] tensor whose last dimension is
+// contiguous: (batch b, head h, token i, dim 0) sits at b sb + h sh + i sn.
+struct Lay {
+  int64_t sb, sh, sn;
+  int H;
+};
+
+// Element offset of (bh = b H + h, token i, dim 0).
+__host__ __device__ __forceinline__ size_t row_off(int bh, int i, const Lay& L) {
+  const int b = bh / L.H, h = bh - b * L.H;
+  return (size_t)((int64_t)b * L.sb + (int64_t)h * L.sh + (int64_t)i * L.sn);
+}
+
 struct Prob {
   int B, H, BH, nq, nk, d, cq, ck, dtype, xf, layout, split;
   int nqc, nkc, nq_pad, nk_pad;
   size_t esize;
+  Lay lq, lk, lv, lo;  // q, k, v and the output
 };
-
-// Element offset of (bh, token i, dim 0) in a [B,H,N,d] tensor of the given layout.
-__host__ __device__ __forceinline__ size_t row_off(int bh, int i, int N, int H, int d, int layout) {
-  if (layout == CA_LAYOUT_BHND) return ((size_t)bh * N + i) * d;
-  int b = bh / H, h = bh - b * H;
-  return (((size_t)b * N + i) * H + h) * d;
-}
 
 // ---- the split tree -----------------------------------------------------------
 // Node sizes depend only on (n, c): a node of s > c tokens sends
@@ -147,6 +154,10 @@ int split_hist_slots(const Prob& P, int big_q, int big_k);
 
 // ---- launchers (return hipError_t of the last launch) ----------------------
 
+// Checked mode: flags[0] = bit 0 (q), 1 (k), 2 (v, if given) for a tensor
+// holding a NaN or an infinity; cleared first on the stream.
+hipError_t launch_check_finite(const Prob& P, const void* q, const void* k, const void* v,
+                               int32_t* flags, hipStream_t st);
 hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const void* v,
                           const ca_cluster_out* out, char* ws, const Workspace& W,
                           hipStream_t st);

@@ -63,9 +63,10 @@ struct FusedArgs {
   const char* tiles;      // staged centroid tiles [BH][ntile] (NULL: no compensation)
   int ntile;
   const int32_t* perm_q;  // [BH][nq]
-  bf16* out;              // problem layout
+  bf16* out;              // strides lo
   float* lse_out;         // [BH][nq] or NULL
-  int nq, H, layout;
+  int nq;
+  Lay lo;
 };
 
 template <int D, int CQ, int CK, bool FUSED = false>
@@ -386,7 +387,7 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
     if (prow >= fa.nq) return;
     int orig = fa.perm_q[(size_t)bh * fa.nq + prow];
     orig = orig < 0 ? 0 : (orig >= fa.nq ? fa.nq - 1 : orig);  // memory safety for a bad permutation
-    bf16* orow = fa.out + row_off(bh, orig, fa.nq, fa.H, D, fa.layout);
+    bf16* orow = fa.out + row_off(bh, orig, fa.lo);
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -644,7 +645,7 @@ hipError_t launch_attn_fused(const Prob& P, const void* qp, const void* kp, cons
                              void* out, float* lse_out, int32_t* sched, hipStream_t st) {
   if (P.dtype != CA_BF16 || P.nkc > kMaskWords * 32) return hipErrorInvalidValue;
   const FusedArgs fa{tiles, (P.nkc + kCompTile - 1) / kCompTile, perm_q, (bf16*)out, lse_out,
-                     P.nq, P.H, P.layout};
+                     P.nq, P.lo};
 #define CA_ATTN_CASE(D, CQ, CK) \
   if (P.d == D && P.cq == CQ && P.ck == CK) \
     return run_bf16<D, CQ, CK, true>(P, qp, kp, vp, count_k, lists, lens, k, scale, nullptr, \

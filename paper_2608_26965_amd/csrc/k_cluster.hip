@@ -32,7 +32,8 @@ namespace {
 // ---------------------------------------------------------------------------
 
 struct Side {
-  const void* x;    // input tensor, problem layout
+  const void* x;    // input tensor (strides lx)
+  Lay lx;
   float* y;         // split coordinates [BH][n][d]
   int32_t* perm;    // [BH][n]
   int32_t* cid;     // [BH][n] (may be null)
@@ -47,7 +48,8 @@ struct Ctx {
   const void* v;    // values (may be null)
   float* cent_v;
   void* vp;         // value tiles [BH][nkc][d][ck]
-  int BH, H, d, dtype, layout, xf, nmax, nblk;
+  Lay lv;           // strides of the values
+  int BH, H, d, dtype, xf, nmax, nblk;
   float* mats;      // [BH][kMats][d][d]
   float* vecs;      // [BH][kVecs][d]
   float* inv_q;     // [BH][nq]
@@ -82,9 +84,9 @@ __device__ __forceinline__ float* vec(const Ctx& C, int bh, int slot) {
   return C.vecs + ((size_t)bh * kVecs + slot) * C.d;
 }
 
-__device__ __forceinline__ float load_x(const void* x, int bh, int i, int n, int H, int d, int t,
-                                        int dtype, int layout) {
-  return load_elem(x, row_off(bh, i, n, H, d, layout) + t, dtype);
+__device__ __forceinline__ float load_x(const void* x, int bh, int i, const Lay& L, int t,
+                                        int dtype) {
+  return load_elem(x, row_off(bh, i, L) + t, dtype);
 }
 
 // ---------------------------------------------------------------------------
@@ -151,7 +153,7 @@ __global__ __launch_bounds__(256) void moments_partial_kernel(Ctx C) {
     for (int e = threadIdx.x; e < kStage * 4 * d4; e += 256) {
       const int r = e / (4 * d4), t = e % (4 * d4);
       X[r][t] = (r < rows && t < d)
-                    ? load_x(S.x, bh, rs + r, S.n, C.H, d, t, C.dtype, C.layout)
+                    ? load_x(S.x, bh, rs + r, S.lx, t, C.dtype)
                     : 0.f;
     }
     __syncthreads();
@@ -734,7 +736,7 @@ __global__ __launch_bounds__(256) void qnorm_partial_kernel(Ctx C) {
     __syncthreads();
     for (int e = threadIdx.x; e < kStage * 4 * d4; e += 256) {
       const int r = e / (4 * d4), t = e % (4 * d4);
-      X[r][t] = (r < rows && t < d) ? load_x(S.x, bh, rs + r, S.n, C.H, d, t, C.dtype, C.layout)
+      X[r][t] = (r < rows && t < d) ? load_x(S.x, bh, rs + r, S.lx, t, C.dtype)
                                     : 0.f;
     }
     __syncthreads();
@@ -829,7 +831,7 @@ __global__ __launch_bounds__(256) void project_kernel(Ctx C) {
   if (C.xf == CA_XF_NONE) {
     for (int e = threadIdx.x; e < (r1 - r0) * d; e += 256) {
       const int r = r0 + e / d, t = e % d;
-      Y[(size_t)r * d + t] = load_x(S.x, bh, r, S.n, C.H, d, t, C.dtype, C.layout);
+      Y[(size_t)r * d + t] = load_x(S.x, bh, r, S.lx, t, C.dtype);
     }
     return;
   }
@@ -851,7 +853,7 @@ __global__ __launch_bounds__(256) void project_kernel(Ctx C) {
     __syncthreads();
     for (int e = threadIdx.x; e < kStage * 4 * d4; e += 256) {
       const int r = e / (4 * d4), t = e % (4 * d4);
-      X[r][t] = (r < rows && t < d) ? load_x(S.x, bh, rs + r, S.n, C.H, d, t, C.dtype, C.layout)
+      X[r][t] = (r < rows && t < d) ? load_x(S.x, bh, rs + r, S.lx, t, C.dtype)
                                     : 0.f;
     }
     __syncthreads();
@@ -888,11 +890,11 @@ __global__ __launch_bounds__(256) void project_kernel(Ctx C) {
 
 template <int D>
 __device__ __forceinline__ void load_xtile(const bf16* __restrict__ x, int bh, int tok0, int lim,
-                                           int n, int H, int layout, int l32, int h,
+                                           const Lay& L, int l32, int h,
                                            bf16x8 (&xop)[D / 16]) {
   const int tok = tok0 + l32;
   if (tok < lim) {
-    const bf16* row = x + row_off(bh, tok, n, H, D, layout);
+    const bf16* row = x + row_off(bh, tok, L);
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) xop[ks] = *(const bf16x8*)(row + 16 * ks + 8 * h);
   } else {
@@ -1027,7 +1029,7 @@ __global__ __launch_bounds__(256) void moments_mfma_kernel(Ctx C) {
   for (int ft = 0; ft < FT; ++ft) cs[ft] = 0.f;
   for (int tok0 = r0 + 32 * w; tok0 < r1; tok0 += 128) {
     bf16x8 xop[KS];
-    load_xtile<D>((const bf16*)S.x, bh, tok0, r1, S.n, C.H, C.layout, l32, h, xop);
+    load_xtile<D>((const bf16*)S.x, bh, tok0, r1, S.lx, l32, h, xop);
     f32x16 xT[FT];
     transpose_tile<D>(xop, id, xT);
 #pragma unroll
@@ -1085,7 +1087,7 @@ __global__ __launch_bounds__(256) void qnorm_mfma_kernel(Ctx C) {
   for (int ft = 0; ft < FT; ++ft) cs[ft] = 0.f;
   for (int tok0 = r0 + 32 * w; tok0 < r1; tok0 += 128) {
     bf16x8 xop[KS];
-    load_xtile<D>((const bf16*)S.x, bh, tok0, r1, S.n, C.H, C.layout, l32, h, xop);
+    load_xtile<D>((const bf16*)S.x, bh, tok0, r1, S.lx, l32, h, xop);
     f32x16 acc[FT];
     project_tile<D>(wl, xop, l32, h, acc);
     float nrm = 0.f;
@@ -1159,7 +1161,7 @@ __global__ __launch_bounds__(256, 2) void project_mfma_kernel(Ctx C) {
   float* Y = S.y + (size_t)bh * S.n * D;
   for (int tok0 = r0 + 32 * w; tok0 < r1; tok0 += 128) {
     bf16x8 xop[KS];
-    load_xtile<D>((const bf16*)S.x, bh, tok0, r1, S.n, C.H, C.layout, l32, h, xop);
+    load_xtile<D>((const bf16*)S.x, bh, tok0, r1, S.lx, l32, h, xop);
     const int tok = tok0 + l32;
     const float sc = scale && tok < r1 ? C.inv_q[(size_t)bh * S.n + tok] : 1.f;
     float* yrow = Y + (size_t)tok * D;
@@ -2466,10 +2468,10 @@ __global__ __launch_bounds__(128) void gather_kernel(Ctx C) {
       float x = 0.f, xv = 0.f;
       if (r < cnt) {
         const int i = perm[r];
-        x = load_x(S.x, bh, i, S.n, C.H, d, tt, C.dtype, C.layout);
+        x = load_x(S.x, bh, i, S.lx, tt, C.dtype);
         s += x;
         if (vals) {
-          xv = load_x(C.v, bh, i, S.n, C.H, d, tt, C.dtype, C.layout);
+          xv = load_x(C.v, bh, i, C.lv, tt, C.dtype);
           sv += xv;
         }
       }
@@ -2529,10 +2531,10 @@ __global__ __launch_bounds__(256) void gather_fast_kernel(Ctx C) {
       chunk[u] = vchunk[u] = make_uint4(0u, 0u, 0u, 0u);
       if (r < cnt) {
         const int i = perm[r];
-        chunk[u] = *(const uint4*)((const T*)S.x + row_off(bh, i, S.n, C.H, d, C.layout) + col * EPC);
+        chunk[u] = *(const uint4*)((const T*)S.x + row_off(bh, i, S.lx) + col * EPC);
         if (vals)
           vchunk[u] =
-              *(const uint4*)((const T*)C.v + row_off(bh, i, S.n, C.H, d, C.layout) + col * EPC);
+              *(const uint4*)((const T*)C.v + row_off(bh, i, C.lv) + col * EPC);
       }
     }
 #pragma unroll
@@ -2682,7 +2684,7 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
   C.H = P.H;
   C.d = d;
   C.dtype = P.dtype;
-  C.layout = P.layout;
+  C.lv = P.lv;
   C.xf = P.xf;
   C.nmax = P.nq > P.nk ? P.nq : P.nk;
   C.nblk = W.nblk_mom;
@@ -2710,6 +2712,9 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
   Side& Sk = C.s[1];
   Sq.x = q;
   Sk.x = k;
+  Sq.lx = P.lq;
+  Sk.lx = P.lk;
+  if (P.lq.H < 1 || P.lk.H < 1 || P.lv.H < 1) return hipErrorInvalidValue;
   Sq.y = out->yq_dbg ? out->yq_dbg : (float*)(ws + W.y_q);
   Sk.y = out->yk_dbg ? out->yk_dbg : (float*)(ws + W.y_k);
   Sq.perm = out->perm_q;
@@ -2881,6 +2886,59 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
   }
 #undef CA_CHECK
   return hipSuccess;
+}
+
+// ---------------------------------------------------------------------------
+// Checked mode: flag bits of the tensors holding a NaN or an infinity
+// ---------------------------------------------------------------------------
+
+namespace {
+
+__global__ void flags_clear_kernel(int32_t* flags) { flags[0] = 0; }
+
+// One block of 256 threads per 64 rows of one tensor (blockIdx.y: 0 q, 1 k,
+// 2 v); a value is non-finite when its exponent bits are all ones.
+__global__ __launch_bounds__(256) void check_finite_kernel(const void* q, const void* k,
+                                                           const void* v, Lay lq, Lay lk, Lay lv,
+                                                           int nq, int nk, int BH, int d,
+                                                           int dtype, int32_t* flags) {
+  const int t = blockIdx.y;
+  const void* x = t == 0 ? q : (t == 1 ? k : v);
+  const Lay& L = t == 0 ? lq : (t == 1 ? lk : lv);
+  const int n = t == 0 ? nq : nk;
+  const long long rows = (long long)BH * n;
+  const long long r0 = (long long)blockIdx.x * 64;
+  int bad = 0;
+  if (x != nullptr) {
+    for (int e = threadIdx.x; e < 64 * d; e += 256) {
+      const long long r = r0 + e / d;
+      if (r >= rows) break;
+      const int bh = (int)(r / n), i = (int)(r % n), c = e % d;
+      const size_t off = row_off(bh, i, L) + c;
+      if (dtype == CA_BF16) {
+        const uint16_t u = ((const uint16_t*)x)[off];
+        bad |= (u & 0x7F80u) == 0x7F80u;
+      } else {
+        const uint32_t u = ((const uint32_t*)x)[off];
+        bad |= (u & 0x7F800000u) == 0x7F800000u;
+      }
+    }
+  }
+  if (__syncthreads_or(bad) && threadIdx.x == 0) atomicOr(flags, 1 << t);
+}
+
+}  // namespace
+
+hipError_t launch_check_finite(const Prob& P, const void* q, const void* k, const void* v,
+                               int32_t* flags, hipStream_t st) {
+  hipLaunchKernelGGL(flags_clear_kernel, dim3(1), dim3(1), 0, st, flags);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const long long rows = (long long)P.BH * (P.nq > P.nk ? P.nq : P.nk);
+  const unsigned blocks = (unsigned)((rows + 63) / 64);
+  hipLaunchKernelGGL(check_finite_kernel, dim3(blocks, v ? 3 : 2), dim3(256), 0, st, q, k, v,
+                     P.lq, P.lk, P.lv, P.nq, P.nk, P.BH, P.d, P.dtype, flags);
+  return hipGetLastError();
 }
 
 }  // namespace ca

@@ -32,9 +32,7 @@ __device__ __forceinline__ int xcd_remap(int wg, int total) {
   return xcd < rem ? xcd * (per + 1) + loc : rem * (per + 1) + (xcd - rem) * per + loc;
 }
 
-__device__ __forceinline__ size_t out_row(int bh, int i, int nq, int H, int d, int layout) {
-  return row_off(bh, i, nq, H, d, layout);
-}
+
 
 // bf16 centroid tiles (written once per call, read by every query cluster of
 // the head): tile t of head bh covers centroids [128 t, 128 t + 128) and holds
@@ -123,7 +121,7 @@ __global__ __launch_bounds__(CQ * 2, (comp_waves_per_simd<D, CQ>())) void comp_b
     int nkc, int ntile, int k, float sl2, int enable, const bf16* __restrict__ op,
     const float* __restrict__ lse_s,
     const int32_t* __restrict__ perm_q, bf16* __restrict__ out, float* __restrict__ lse_out,
-    int layout, int total) {
+    Lay lo, int total) {
   constexpr int NW = CQ / 32;
   constexpr int T = NW * 64;
   constexpr int CT = kCompTile;               // centroids per staged tile
@@ -359,7 +357,7 @@ __global__ __launch_bounds__(CQ * 2, (comp_waves_per_simd<D, CQ>())) void comp_b
     inv_c = 1.f / l_tot;
   }
   orig = orig < 0 ? 0 : (orig >= nq ? nq - 1 : orig);  // memory safety for a bad permutation
-  bf16* orow = out + out_row(bh, orig, nq, H, D, layout);
+  bf16* orow = out + row_off(bh, orig, lo);
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -382,7 +380,7 @@ __global__ __launch_bounds__(256) void comp_f32_kernel(
     int nkc, int cq, int d, int k, float scale, int enable, const float* __restrict__ op,
     const float* __restrict__ lse_s,
     const int32_t* __restrict__ perm_q, float* __restrict__ out, float* __restrict__ lse_out,
-    int layout) {
+    Lay lo) {
   constexpr int KC = 32;
   __shared__ float Ksh[KC][DP + 1];
   __shared__ float Vsh[KC][DP + 1];
@@ -459,7 +457,7 @@ __global__ __launch_bounds__(256) void comp_f32_kernel(
   }
   int orig = perm_q[(size_t)bh * nq + prow];
   orig = orig < 0 ? 0 : (orig >= nq ? nq - 1 : orig);
-  float* orow = out + row_off(bh, orig, nq, H, d, layout);
+  float* orow = out + row_off(bh, orig, lo);
   for (int t = 0; t < d; ++t) orow[t] = ws * op[qrow * d + t] + wc * (o[t] * inv_c);
   if (lse_out) lse_out[(size_t)bh * nq + orig] = lse;
 }
@@ -481,7 +479,7 @@ hipError_t run_bf16(const Prob& P, const void* qp, const float* cent_k, const fl
   hipLaunchKernelGGL((comp_bf16_kernel<D, CQ>), dim3(total), dim3(CQ * 2), 0, st,
                      (const bf16*)qp, (const char*)tiles, lists, lens, P.nq, P.H, P.nqc, P.nkc, ntile, k,
                      scale * kLog2e, enable, (const bf16*)op, lse, perm_q, (bf16*)out, lse_out,
-                     P.layout, total);
+                     P.lo, total);
   return hipGetLastError();
 }
 
@@ -526,7 +524,7 @@ hipError_t launch_comp(const Prob& P, const void* qp, const float* cent_k, const
                      cent_k, cent_v, count_k, lists, lens, P.nq, P.H, P.nqc, P.nkc, P.cq, P.d, \
                      k,                                                                       \
                      scale, enable, (const float*)op, lse, perm_q, (float*)out, lse_out,      \
-                     P.layout)
+                     P.lo)
   if (P.d <= 32)
     CA_COMP_F32(32);
   else if (P.d <= 64)

@@ -25,7 +25,7 @@ def test_header_symbols_exported():
     assert declared == set(L.EXPORTS)
     for name in declared:
         assert hasattr(lib, name)
-    assert lib.ca_abi_version() == 7
+    assert lib.ca_abi_version() == 8
 
 
 def _prob(**kw):
@@ -39,7 +39,7 @@ def _prob(**kw):
 @pytest.mark.parametrize("kw,status", [
     (dict(cq=48), 1), (dict(ck=512), 1), (dict(d=0), 1), (dict(d=129), 1), (dict(nq=0), 1),
     (dict(dtype=7), 1), (dict(transform=5), 1), (dict(split=2), 1),
-    (dict(split=1, transform=1), 2), (dict(split=1, transform=3), 2), (dict(layout=2), 1), (dict(heads=0), 1),
+    (dict(split=1, transform=1), 2), (dict(split=1, transform=3), 2), (dict(layout=3), 1), (dict(heads=0), 1),
 ])
 def test_invalid_problem(kw, status):
     L, lib = _lib()
@@ -167,3 +167,41 @@ def test_compensate_cluster_limit_only_when_compensating():
                            fake, None, None, 0, None)
     assert st == L.CA_E_UNSUPPORTED
     assert "131072" in L.last_error()
+
+
+def test_strided_layout_validation():
+    """CA_LAYOUT_STRIDED: strides must be non-negative multiples of 16 bytes'
+    worth of elements; strided tensors must be 16-byte aligned."""
+    L, lib = _lib()
+    fake = 256
+    ok = dict(layout=L.CA_LAYOUT_STRIDED)
+    P = L.CaProblem
+    good = _prob(**ok)
+    for name in ("q_stride", "k_stride", "v_stride", "out_stride"):
+        getattr(good, name)[:] = [2 * 1000 * 64 * 3, 64, 3 * 2 * 64]
+    n = ctypes.c_size_t(0)
+    assert lib.ca_workspace_size(good, 2, n) == L.CA_OK
+    bad = _prob(**ok)
+    for name in ("q_stride", "k_stride", "v_stride", "out_stride"):
+        getattr(bad, name)[:] = [2 * 1000 * 64 * 3, 64, 3 * 2 * 64]
+    bad.k_stride[2] = 100  # not a multiple of 8 bf16 elements
+    assert lib.ca_workspace_size(bad, 2, n) == L.CA_E_INVALID
+    assert "k_stride[2]" in L.last_error()
+    bad.k_stride[2] = -8
+    assert lib.ca_workspace_size(bad, 2, n) == L.CA_E_INVALID
+    # misaligned q is refused before anything is enqueued
+    out = L.CaClusterOut(*([fake] * 12 + [None, None]))
+    assert lib.ca_cluster(good, fake + 2, fake, fake, out, fake, 1 << 40, None) == L.CA_E_INVALID
+    assert "16-byte aligned" in L.last_error()
+    assert lib.ca_abi_version() == 8
+
+
+def test_check_finite_validation():
+    """ca_check_finite validates before enqueueing: q, k and flags required."""
+    L, lib = _lib()
+    fake = 256
+    p = _prob()
+    assert lib.ca_check_finite(p, fake, None, None, fake, None) == L.CA_E_INVALID
+    assert lib.ca_check_finite(p, fake, fake, None, None, None) == L.CA_E_INVALID
+    assert lib.ca_check_finite(_prob(d=0), fake, fake, None, fake, None) == L.CA_E_INVALID
+    assert "NaN" in lib.ca_status_str(L.CA_E_NONFINITE).decode()
