@@ -204,6 +204,9 @@ void plan_workspace(const Prob& P, Workspace* W) {
 
   W->y_q = take(BH * P.nq * d * 4);
   W->y_k = take(BH * P.nk * d * 4);
+  const bool cols = col_copy_used(P);
+  W->ycol_q = take(cols ? BH * kColCopy * P.nq * 4 : 0);
+  W->ycol_k = take(cols ? BH * kColCopy * P.nk * 4 : 0);
   W->idx0 = take(2 * BH * nmax * 4);
   W->idx1 = take(2 * BH * nmax * 4);
   W->keys = take(2 * BH * nmax * 4);

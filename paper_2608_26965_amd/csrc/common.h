@@ -102,6 +102,7 @@ inline int num_levels(int n, int c) {
 struct Workspace {
   // clustering
   size_t y_q, y_k;          // fp32 [BH][n][d] split coordinates (unless exported)
+  size_t ycol_q, ycol_k;    // fp32 [BH][kColCopy][n] their first coordinates, coordinate-major
   size_t idx0, idx1, keys;  // int32 / uint32 [2][BH][nmax]
   size_t mom_part;          // fp32 [2][BH][nblk][d*d + d]
   size_t mats;              // fp32 [BH][kMats][d][d]
@@ -128,6 +129,16 @@ struct Workspace {
   int hist_slots;           // chunk slots of the busiest multi-block level
 };
 
+// Leading split coordinates also kept coordinate-major (one contiguous column
+// per coordinate), from which the multi-block keys pass reads a node's chosen
+// coordinate: the upper levels choose among the leading principal coordinates.
+constexpr int kColCopy = 16;
+// The column copy exists for bf16 problems with d = 64 or 128 in a transformed
+// space (the MFMA projection writes it) and diagonalized splitting.
+inline bool col_copy_used(const Prob& P) {
+  return P.dtype == CA_BF16 && (P.d == 64 || P.d == 128) && P.xf != CA_XF_NONE &&
+         P.xf != CA_XF_RANDOM && P.split == CA_SPLIT_DIAG;
+}
 constexpr int kMats = 8;
 constexpr int kVecs = 8;
 constexpr int kNodeInts = 16;

@@ -35,6 +35,7 @@ struct Side {
   const void* x;    // input tensor (strides lx)
   Lay lx;
   float* y;         // split coordinates [BH][n][d]
+  float* ycol;      // the first kColCopy of them, [BH][kColCopy][n] (or NULL)
   int32_t* perm;    // [BH][n]
   int32_t* cid;     // [BH][n] (may be null)
   int32_t* count;   // [BH][nc]
@@ -1171,13 +1172,25 @@ __global__ __launch_bounds__(256, 2) void project_mfma_kernel(Ctx C) {
     for (int ot = 0; ot < FT; ++ot) {
       f32x16 acc;
       project_tile1<D>(wl, xop, l32, h, ot, acc);
-      if (tok < r1)
+      if (tok < r1) {
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
           const int col = 32 * ot + 8 * g4 + 4 * h;
           *(float4*)(yrow + col) = make_float4(acc[4 * g4] * sc, acc[4 * g4 + 1] * sc,
                                                acc[4 * g4 + 2] * sc, acc[4 * g4 + 3] * sc);
         }
+        // the same values of coordinates 0 .. 15, coordinate-major: each
+        // store is 32 consecutive tokens of one coordinate per half-wave
+        if (ot == 0 && S.ycol) {
+          static_assert(kColCopy == 16, "coordinates of g4 = 0, 1 of the first tile");
+#pragma unroll
+          for (int g4 = 0; g4 < 2; ++g4)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              S.ycol[((size_t)bh * kColCopy + 8 * g4 + 4 * h + e) * S.n + tok] =
+                  acc[4 * g4 + e] * sc;
+        }
+      }
     }
   }
 }
@@ -1859,6 +1872,12 @@ __global__ __launch_bounds__(256) void split_keys_kernel(Ctx C, LevelArgs L) {
         for (int k = 0; k < C.d; ++k) a = add_rn(a, mul_rn(yr[k], dv[k]));
         kv[u] = ordered_bits(a);
       }
+  } else if (S.ycol && js < kColCopy) {
+    // the node's coordinate from its contiguous column: the nodes of a level
+    // share few columns, so the lines they read are mostly used in full
+    const float* col = S.ycol + ((size_t)bh * kColCopy + js) * S.n;
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) kv[u] = ordered_bits(col[rows[u]]);
   } else {
 #pragma unroll
     for (int u = 0; u < kPer; ++u) kv[u] = ordered_bits(Y[(size_t)rows[u] * C.d + js]);
@@ -2717,6 +2736,10 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
   if (P.lq.H < 1 || P.lk.H < 1 || P.lv.H < 1) return hipErrorInvalidValue;
   Sq.y = out->yq_dbg ? out->yq_dbg : (float*)(ws + W.y_q);
   Sk.y = out->yk_dbg ? out->yk_dbg : (float*)(ws + W.y_k);
+  // coordinate-major leading coordinates, where a multi-block level reads them
+  const bool cols = col_copy_used(P);
+  Sq.ycol = cols && W.big_q > 0 ? (float*)(ws + W.ycol_q) : nullptr;
+  Sk.ycol = cols && W.big_k > 0 ? (float*)(ws + W.ycol_k) : nullptr;
   Sq.perm = out->perm_q;
   Sk.perm = out->perm_k;
   Sq.cid = out->cid_q;

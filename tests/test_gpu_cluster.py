@@ -315,3 +315,31 @@ def test_split_select_fallbacks(kind, n, xf, split):
     assert np.array_equal(r["cid_k"][0].numpy(), cidk)
     _check_copies(Q[0], pq, r["count_q"][0], r["cent_q"][0], r["qp"][0], c, "bf16")
     _check_copies(K[0], pk, r["count_k"][0], r["cent_k"][0], r["kp"][0], c, "bf16")
+
+
+@pytest.mark.parametrize("seed", [0, 3])
+def test_split_column_copy_and_fallback(seed):
+    """The multi-block keys pass reads a node's coordinate from the
+    coordinate-major copy of the first 16 split coordinates, and from the
+    row-major coordinates for any later one. Input chosen so that, on the
+    exported coordinates, nodes above the tail size choose both kinds (checked
+    on the oracle's trace of those coordinates); permutations bit-exact."""
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    n, d, c = 20000, 64, 128
+    G.flush(f"column copy and fallback, seed={seed}")
+    Q, K, V = mixture_inputs(seed, 1, n, d, "bf16", centres=2, sigma=1.0)
+    p = ca.Problem(1, 1, n, n, d, c, c, torch.bfloat16, "metric")
+    tq, tk, tv = (G.dev(x[None], torch.bfloat16) for x in (Q, K, V))
+    r = ca.cluster(p, tq, tk, tv, export_y=True)
+    torch.cuda.synchronize()
+    chosen = []
+    for side, key in ((0, "yq"), (1, "yk")):
+        Y = r[key][0].double().cpu().numpy()
+        trace = []
+        perm, cid, _ = ref.split(Y, c, trace=trace)
+        chosen += [j for (mem, j, _, _, _) in trace if len(mem) > 4096]
+        got = r["perm_q" if side == 0 else "perm_k"][0].cpu().numpy()
+        assert np.array_equal(got, perm), f"side {side} permutation"
+    assert min(chosen) < 16 <= max(chosen), f"multi-block choices {chosen}"
