@@ -2160,8 +2160,15 @@ __global__ __launch_bounds__(kSelThreads) void split_select_kernel(Ctx C, LevelA
 // Stable partition of every node: the m_L smallest (key, position) pairs go
 // left in node order, the rest right in node order. Nodes that are already
 // leaves are copied.
+// LDS slot of position i of a chunk: one pad word per 16, so that the
+// 16-position runs of consecutive threads start on different banks.
+__device__ __forceinline__ int scat_slot(int i) { return i + (i >> 4); }
+
 __global__ __launch_bounds__(256) void split_scatter_kernel(Ctx C, LevelArgs L) {
   __shared__ int wsum[4];
+  __shared__ uint32_t skey[kChunk + kChunk / 16];
+  __shared__ int32_t srow[kChunk + kChunk / 16];
+  __shared__ int32_t sout[kChunk];
   const int pid = blockIdx.z, side = pid / C.BH, node = blockIdx.y;
   const Side& S = C.s[side];
   if (L.level >= S.big) return;
@@ -2169,14 +2176,15 @@ __global__ __launch_bounds__(256) void split_scatter_kernel(Ctx C, LevelArgs L) 
   node_range(S.n, S.c, L.level, node, &start, &size);
   const int c0 = blockIdx.x * kChunk;
   if (c0 >= size) return;
-  const int c1 = min(size, c0 + kChunk);
+  const int c1 = min(size, c0 + kChunk), nc = c1 - c0;
   const int32_t* idx_in = L.idx_in + (size_t)pid * C.nmax;
   int32_t* idx_out = L.idx_out + (size_t)pid * C.nmax;
   const int32_t* ns = node_ptr(C, pid, node);
+  const int t = threadIdx.x;
   if (size <= S.c) {
 #pragma unroll
     for (int u = 0; u < kPer; ++u) {
-      const int o = c0 + threadIdx.x + 256 * u;
+      const int o = c0 + t + 256 * u;
       if (o < c1) idx_out[start + o] = L.first ? start + o : idx_in[start + o];
     }
     return;
@@ -2187,37 +2195,57 @@ __global__ __launch_bounds__(256) void split_scatter_kernel(Ctx C, LevelArgs L) 
       C.chunk_cnt + ((size_t)pid * C.hist_slots + (size_t)node * L.cpn + blockIdx.x) * 2;
   const int less0 = cc[0], eq0 = cc[1];
   const uint32_t* keys = C.keys + (size_t)pid * C.nmax;
-  // Each thread owns kPer consecutive positions; keys and rows are loaded
-  // together before the scan.
-  const int o0 = c0 + threadIdx.x * kPer;
-  uint32_t kv[kPer];
-  int rows[kPer];
+  // coalesced loads of the chunk's keys and rows into LDS
 #pragma unroll
   for (int u = 0; u < kPer; ++u) {
-    const int o = o0 + u;
-    kv[u] = o < c1 ? keys[start + o] : 0xFFFFFFFFu;
-    rows[u] = o < c1 ? (L.first ? start + o : idx_in[start + o]) : 0;
+    const int i = t + 256 * u;
+    if (i < nc) {
+      skey[scat_slot(i)] = keys[start + c0 + i];
+      srow[scat_slot(i)] = L.first ? start + c0 + i : idx_in[start + c0 + i];
+    }
   }
+  __syncthreads();
+  // Each thread owns kPer consecutive positions (the scan order).
+  const int i0 = t * kPer;
+  uint32_t kv[kPer];
   int less = 0, eq = 0;
 #pragma unroll
   for (int u = 0; u < kPer; ++u) {
-    less += o0 + u < c1 && kv[u] < thr;
-    eq += o0 + u < c1 && kv[u] == thr;
+    const int i = i0 + u;
+    kv[u] = i < nc ? skey[scat_slot(i)] : 0xFFFFFFFFu;
+    less += i < nc && kv[u] < thr;
+    eq += i < nc && kv[u] == thr;
   }
   int tot;
   const int packed = scan256((less << 16) | eq, wsum, &tot);
+  // The chunk's left-goers land in one contiguous range of the node starting
+  // at lmin, its right-goers in one starting at rmin: stage both in order,
+  // left part first, then write them out coalesced.
+  const int lmin = less0 + min(eq0, need_eq);
+  const int rmin = mL + (c0 - lmin);
+  const int tot_less = tot >> 16, tot_eq = tot & 0xFFFF;
+  const int nleft = tot_less + min(eq0 + tot_eq, need_eq) - min(eq0, need_eq);
   int lb = less0 + (packed >> 16), eb = eq0 + (packed & 0xFFFF);
 #pragma unroll
   for (int u = 0; u < kPer; ++u) {
-    const int o = o0 + u;
-    if (o >= c1) break;
+    const int i = i0 + u;
+    if (i >= nc) break;
     const uint32_t key = kv[u];
     const int Lo = lb + min(eb, need_eq);
     const bool left = key < thr || (key == thr && eb < need_eq);
-    const int dst = left ? Lo : mL + (o - Lo);
-    if (dst >= 0 && dst < size) idx_out[start + dst] = rows[u];
+    const int loc = left ? Lo - lmin : nleft + (c0 + i - Lo) - (c0 - lmin);
+    if (loc >= 0 && loc < nc) sout[loc] = srow[scat_slot(i)];
     lb += key < thr;
     eb += key == thr;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int i = t + 256 * u;
+    if (i < nc) {
+      const int dst = i < nleft ? lmin + i : rmin + (i - nleft);
+      if (dst >= 0 && dst < size) idx_out[start + dst] = sout[i];
+    }
   }
 }
 
