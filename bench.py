@@ -230,7 +230,7 @@ def latency_sweep(args):
         v = torch.randn(H, n, d, device=dev, generator=g).to(torch.bfloat16)[None].contiguous()
         return xs[0], xs[1], v
 
-    for n in SWEEP_N:
+    for n in (args.sweep_sizes or SWEEP_N):
         g = torch.Generator(device=dev)
         g.manual_seed(n)
         q, k, v = mixture(n, g)
@@ -491,6 +491,8 @@ def main():
     ap.add_argument("--sweep", action="store_true",
                     help="latency scaling with the token count instead of the headline run: one "
                          "JSON line per (N, rule), k = 64 clusters or 10%% of the key clusters")
+    ap.add_argument("--sweep-sizes", type=lambda x: [int(t) for t in x.split(",")], default=None,
+                    help="token counts of the sweep (comma-separated; default: 8192 to 1048576)")
     ap.add_argument("--configs", action="store_true",
                     help="every workload configuration (cluster sizes, keep fractions, "
                          "compensation on/off) instead of the headline run: one JSON line each")

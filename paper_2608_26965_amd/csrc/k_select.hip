@@ -194,34 +194,26 @@ __device__ __forceinline__ float block_min_max(float v, bool want_max, float* sh
   return r;
 }
 
-constexpr int kTopBins = 2048;   // linear bins of the top-k pre-pass
-constexpr int kTopStage = 8192;  // rows up to this length are staged in LDS
+constexpr int kTopBins = 2048;  // linear bins of the top-k pre-pass
 
 // One row (head, query cluster) per block: exact top-k of S[row][0..nkc).
 // A pre-pass counts the row into linear bins over [min, max] (descending
 // score; the map is monotone, so the k-th largest lies in one bin and every
 // key of a lower bin precedes it); the radix select then only counts that
 // bin's keys, which keeps the LDS atomics of long rows from piling onto the
-// few digits a narrow score range has in common.
-// Rows of at most kTopStage scores are first copied to LDS (dynamic shared
-// memory of nkc floats), so the passes below read the row once from memory.
+// few digits a narrow score range has in common. Rows longer than 8192
+// scores take this kernel; shorter ones the wave and block kernels below.
 __global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ S, int nkc, int k,
-                                                   int32_t* __restrict__ lists, int staged) {
+                                                   int32_t* __restrict__ lists) {
   __shared__ int hist[256];
   __shared__ int bins[kTopBins];
   __shared__ int sh_warp[4];
   __shared__ float sh_f[4];
   __shared__ uint32_t sh_prefix;
   __shared__ int sh_rank, sh_bin;
-  extern __shared__ float srow[];
   const size_t row = blockIdx.x;
   const int tid = threadIdx.x;
   const float* s = S + row * nkc;
-  if (staged) {
-    for (int b = tid; b < nkc; b += 256) srow[b] = s[b];
-    __syncthreads();
-    s = srow;
-  }
 
   float lo = INFINITY, hi = -INFINITY;
   for (int b = tid; b < nkc; b += 256) {
@@ -547,6 +539,228 @@ __global__ __launch_bounds__(256) void topk_wave_kernel(const float* __restrict_
   }
 }
 
+// Exact top-k of rows of up to 64 * VPL * NWV scores, one row per block of NWV
+// wavefronts (for rows too wide for one wavefront's registers). Wave w owns
+// the contiguous range [64 VPL w, 64 VPL (w + 1)) of the row, read as
+// float4s interleaved over the lanes (lane l holds positions
+// 64 VPL w + 256 g + 4 l + e, g < VPL / 4, e < 4), so every load instruction
+// reads 1 KB of consecutive scores. The selection is that of topk_wave_kernel
+// (linear bins over [min, max], candidates of the k-th's bin, 8-bit radix
+// select on order-preserving keys, ties to the lower index) with the
+// histograms shared by the block; the output is written in index order.
+template <int VPL, int NWV>
+__global__ __launch_bounds__(64 * NWV, 4) void topk_block_kernel(const float* __restrict__ S, int nkc,
+                                                              int k, int vec4,
+                                                              int32_t* __restrict__ lists) {
+  constexpr int NT = 64 * NWV, G = VPL / 4;
+  static_assert(VPL % 4 == 0, "float4 groups");
+  __shared__ int bins[kWaveBins];
+  __shared__ int hist[256];
+  __shared__ uint32_t ckey[NWV][kWaveCand];
+  __shared__ float red_lo[NWV], red_hi[NWV];
+  __shared__ int wcnt[2][NWV];
+  __shared__ int sh_over;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, tid = threadIdx.x;
+  const size_t row = blockIdx.x;
+  const float* s = S + row * nkc;
+  const int wbase = 64 * VPL * w;
+  auto pos_of = [&](int g, int e) { return wbase + 256 * g + 4 * lane + e; };
+  float v[VPL];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const int p0 = pos_of(g, 0);
+    if (vec4) {
+      float4 x = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+      if (p0 < nkc) x = *(const float4*)(s + p0);  // nkc % 4 == 0: whole float4
+      v[4 * g] = x.x;
+      v[4 * g + 1] = x.y;
+      v[4 * g + 2] = x.z;
+      v[4 * g + 3] = x.w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[4 * g + e] = p0 + e < nkc ? s[p0 + e] : -INFINITY;
+    }
+  }
+  // Positions past the row hold -inf (sorted after every score); only the
+  // range below leaves them out.
+  float lo = INFINITY, hi = -INFINITY;
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (pos_of(g, e) < nkc) {
+        lo = fminf(lo, v[4 * g + e]);
+        hi = fmaxf(hi, v[4 * g + e]);
+      }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    lo = fminf(lo, __shfl_xor(lo, o, 64));
+    hi = fmaxf(hi, __shfl_xor(hi, o, 64));
+  }
+  if (lane == 0) {
+    red_lo[w] = lo;
+    red_hi[w] = hi;
+  }
+  for (int i = tid; i < kWaveBins; i += NT) bins[i] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < NWV; ++i) {
+    lo = fminf(lo, red_lo[i]);
+    hi = fmaxf(hi, red_hi[i]);
+  }
+  const float inv0 = (float)kWaveBins / (hi - lo);
+  const float inv = hi > lo && inv0 < INFINITY ? inv0 : 0.f;  // too narrow: one bin
+  auto bin_of = [&](float x) {
+    const float t = (hi - x) * inv;  // 0 for the largest score
+    return t < (float)kWaveBins ? (t > 0.f ? (int)t : 0) : kWaveBins - 1;
+  };
+#pragma unroll
+  for (int j = 0; j < VPL; ++j) atomicAdd(&bins[bin_of(v[j])], 1);
+  __syncthreads();
+  // the bin holding rank k - 1 (every wavefront finds the same)
+  int B, rank;
+  {
+    constexpr int PB = kWaveBins / 64;
+    int sum = 0;
+#pragma unroll
+    for (int i = 0; i < PB; ++i) sum += bins[PB * lane + i];
+    const int incl = wave_incl_scan(sum, lane);
+    const bool mine = k - 1 >= incl - sum && k - 1 < incl;
+    const int owner = __ffsll((long long)__ballot(mine)) - 1;
+    int fb = 0, fr = 0;
+    if (mine) {
+      int acc = incl - sum;
+      for (int i = 0; i < PB; ++i) {
+        const int c = bins[PB * lane + i];
+        if (k - 1 < acc + c) {
+          fb = PB * lane + i;
+          fr = k - 1 - acc;
+          break;
+        }
+        acc += c;
+      }
+    }
+    B = __builtin_amdgcn_readlane(fb, owner);
+    rank = __builtin_amdgcn_readlane(fr, owner);
+  }
+  // candidates of bin B: each wavefront compacts its own into its segment
+  int ncand = 0;
+#pragma unroll
+  for (int j = 0; j < VPL; ++j) {
+    const bool hit = bin_of(v[j]) == B;
+    const uint64_t m = __ballot(hit);
+    const int pos = ncand + (int)__popcll(m & ((1ull << lane) - 1ull));
+    if (hit && pos < kWaveCand) ckey[w][pos] = desc_key(v[j]);
+    ncand += (int)__popcll(m);
+  }
+  if (tid == 0) sh_over = 0;
+  __syncthreads();
+  if (lane == 0 && ncand > kWaveCand) sh_over = 1;
+  __syncthreads();
+  const bool in_lds = sh_over == 0;
+  uint32_t prefix = 0;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    const uint32_t hmask = pass == 0 ? 0u : (0xFFFFFFFFu << (shift + 8));
+    for (int i = tid; i < 256; i += NT) hist[i] = 0;
+    __syncthreads();
+    if (in_lds) {
+      for (int i = lane; i < ncand; i += 64) {
+        const uint32_t u = ckey[w][i];
+        if ((u & hmask) == prefix) atomicAdd(&hist[(u >> shift) & 255], 1);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < VPL; ++j)
+        if (bin_of(v[j]) == B) {
+          const uint32_t u = desc_key(v[j]);
+          if ((u & hmask) == prefix) atomicAdd(&hist[(u >> shift) & 255], 1);
+        }
+    }
+    __syncthreads();
+    int c[4], sum = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      c[i] = hist[4 * lane + i];
+      sum += c[i];
+    }
+    const int incl = wave_incl_scan(sum, lane);
+    const bool mine = rank >= incl - sum && rank < incl;
+    const int owner = __ffsll((long long)__ballot(mine)) - 1;
+    int fd = 0, fr = 0;
+    if (mine) {
+      int acc = incl - sum;
+      for (int i = 0; i < 4; ++i) {
+        if (rank < acc + c[i]) {
+          fd = 4 * lane + i;
+          fr = rank - acc;
+          break;
+        }
+        acc += c[i];
+      }
+    }
+    prefix |= (uint32_t)__builtin_amdgcn_readlane(fd, owner) << shift;
+    rank = __builtin_amdgcn_readlane(fr, owner);
+    __syncthreads();  // hist is cleared again by the next pass
+  }
+  // keys below the threshold, and the first rank + 1 equal ones in index
+  // order: counts per wavefront first, then per float4 group in lane order
+  const uint32_t thr = prefix;
+  const int need_eq = rank + 1;
+  int eq_w = 0;
+#pragma unroll
+  for (int j = 0; j < VPL; ++j) eq_w += desc_key(v[j]) == thr;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) eq_w += __shfl_xor(eq_w, o, 64);
+  if (lane == 0) wcnt[0][w] = eq_w;
+  __syncthreads();
+  int eq_run = 0;  // equal keys before this wavefront's range
+  for (int i = 0; i < w; ++i) eq_run += wcnt[0][i];
+  // selected per float4 group; the same walk twice: once to count, once to
+  // write (after the wavefronts' totals are known)
+  auto walk = [&](bool write, int sel_base, int32_t* out) {
+    int er = eq_run, pos_run = sel_base, sel_tot = 0;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      uint32_t u[4];
+      int eq = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        u[e] = desc_key(v[4 * g + e]);
+        eq += u[e] == thr;
+      }
+      const int eq_incl = wave_incl_scan(eq, lane);
+      int ebefore = er + eq_incl - eq;
+      bool take[4];
+      int sel = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        take[e] = u[e] < thr;
+        if (u[e] == thr) take[e] = ebefore++ < need_eq;
+        sel += take[e];
+      }
+      const int sel_incl = wave_incl_scan(sel, lane);
+      if (write) {
+        int p = pos_run + sel_incl - sel;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (take[e] && p < k) out[p++] = pos_of(g, e);
+      }
+      er += __builtin_amdgcn_readlane(eq_incl, 63);
+      const int gsel = __builtin_amdgcn_readlane(sel_incl, 63);
+      pos_run += gsel;
+      sel_tot += gsel;
+    }
+    return sel_tot;
+  };
+  const int sel_w = walk(false, 0, nullptr);
+  if (lane == 0) wcnt[1][w] = sel_w;
+  __syncthreads();
+  int sel_base = 0;
+  for (int i = 0; i < w; ++i) sel_base += wcnt[1][i];
+  walk(true, sel_base, lists + row * k);
+}
+
 // ---------------------------------------------------------------------------
 // Two-pass histogram selection (paper: Method, Cluster assignment -
 // selection). One block per row: the grid position g of every score on a
@@ -747,13 +961,20 @@ hipError_t launch_select(const Prob& P, const float* cq, const float* ck, const 
     CA_TOPK_WAVE(8)
     CA_TOPK_WAVE(16)
     CA_TOPK_WAVE(32)
-    CA_TOPK_WAVE(64)
-    CA_TOPK_WAVE(128)
 #undef CA_TOPK_WAVE
+    // wider rows: one row per block of four wavefronts (more rows in flight
+    // than with a whole row in one wavefront's registers)
+#define CA_TOPK_BLOCK(V)                                                                      \
+  if (P.nkc <= 256 * V) {                                                                     \
+    hipLaunchKernelGGL((topk_block_kernel<V, 4>), dim3((unsigned)nrows), dim3(256), 0, st, S, \
+                       P.nkc, k, vec4, lists);                                                \
+    return hipGetLastError();                                                                 \
   }
-  const int staged = P.nkc <= kTopStage;
-  hipLaunchKernelGGL(topk_kernel, dim3((unsigned)nrows), dim3(256),
-                     staged ? (size_t)P.nkc * sizeof(float) : 0, st, S, P.nkc, k, lists, staged);
+    CA_TOPK_BLOCK(16)
+    CA_TOPK_BLOCK(32)
+#undef CA_TOPK_BLOCK
+  }
+  hipLaunchKernelGGL(topk_kernel, dim3((unsigned)nrows), dim3(256), 0, st, S, P.nkc, k, lists);
   return hipGetLastError();
 }
 

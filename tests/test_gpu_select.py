@@ -54,11 +54,14 @@ def test_topk_with_ties_given_scores(k):
         assert np.array_equal(L[h], ref.topk(S[h].astype(np.float64), k))
 
 
-@pytest.mark.parametrize("nkc,k", [(5000, 64), (8192, 820), (8192, 64), (1001, 500), (1000, 1),
-                                   (9000, 64), (257, 257)])
+@pytest.mark.parametrize("nkc,k", [(2049, 2049), (3000, 64), (4096, 100), (5000, 64),
+                                   (8192, 820), (8192, 64), (4097, 4097), (6001, 3),
+                                   (7999, 2000), (1001, 500), (1000, 1), (9000, 64),
+                                   (257, 257)])
 def test_topk_long_rows_with_ties(nkc, k):
-    """Rows of up to 8192 scores (one row per wavefront) and beyond (one per
-    workgroup), with heavy ties (so the threshold's bin overflows the
+    """Rows of up to 2048 scores (one row per wavefront), up to 8192 (one row
+    per block of four wavefronts) and beyond (one per block of 256 threads),
+    with heavy ties (so the threshold's bin overflows the
     candidate list), a constant row, a range a few subnormals wide, and row
     lengths that are not multiples of four: lists equal the oracle's."""
     import torch
