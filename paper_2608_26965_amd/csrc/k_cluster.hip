@@ -246,64 +246,147 @@ struct EighJobs {
   EighJob j[2];
 };
 
-// Threads of the eigensolver workgroup: the most a workgroup can have. A
-// step is a short dependency chain (LDS reads, the rotation, the 2x2 block
-// products, LDS writes, a barrier), and more wavefronts overlap more of it
-// (measured at d = 64 for 16 problems: 1024 threads beat 512 by 31 us and
-// 256 by 139 us).
-__host__ __device__ constexpr int eigh_nt(int dm) { return 1024; }
+// Symmetric eigensolver, one workgroup of kEighM * DM threads per d x d
+// problem (d <= DM):
+//  1. Householder reduction to a tridiagonal matrix T = Q^T A Q (A fp32 in
+//     LDS; column norms and reflector scales in fp64). Every wavefront builds
+//     reflector k from column k itself, so the pass over the trailing block,
+//     which applies reflector k-1 (the symmetric rank-two update) and forms
+//     p = A v_k in the same sweep, needs one barrier a step.
+//  2. Off-diagonal entries below 2^-24 of the norm are set to zero, so T
+//     splits into unreduced blocks (distinct eigenvalues, eigenvectors with
+//     disjoint supports). Eigenvalues by bisection on Sturm counts in fp64:
+//     sign changes of the leading minors (division free, rescaled every
+//     eight steps), kEighM points per eigenvalue and round.
+//  3. Eigenvectors of T by two steps of inverse iteration (an LDL^T
+//     factorisation of T - lambda I in fp64) from pseudo-random starts;
+//     eigenvalues closer than 1e-8 of the norm form clusters whose vectors
+//     are re-orthogonalised (modified Gram-Schmidt) after each step.
+//  4. Back-transformation by the reflectors: V = Q Z.
+// (Golub and Van Loan, Matrix Computations: the Householder tridiagonal
+// reduction, Sturm sequence bisection and inverse iteration.)
+constexpr int kEighM = 4;
 template <int DM>
 constexpr int eigh_threads() {
-  return eigh_nt(DM);
+  return kEighM * DM;
 }
-
-// Row stride of the LDS matrices: DM plus the number of threads that share a
-// row pair, so that the row segments the threads of one wavefront touch in a
-// step fall on disjoint LDS banks.
-__host__ __device__ constexpr int eigh_stride(int dm) { return dm + eigh_nt(dm) / (dm / 2); }
-// A and V^T are double-buffered (a step reads one copy and writes the other,
-// so it needs a single barrier) when four matrices fit comfortably in LDS.
-__host__ __device__ constexpr bool eigh_double_buffer(int dm) {
-  return 4 * (size_t)dm * eigh_stride(dm) * sizeof(float) <= 100 * 1024;
-}
+// Row stride of the LDS matrices (float4-aligned rows)
+__host__ __device__ constexpr int eigh_stride(int dm) { return dm + 4; }
 __host__ __device__ constexpr size_t eigh_lds_bytes(int dm) {
-  return (eigh_double_buffer(dm) ? 4 : 2) * (size_t)dm * eigh_stride(dm) * sizeof(float);
+  return 2 * (size_t)dm * eigh_stride(dm) * sizeof(float);
+}
+// Bisection rounds: (kEighM + 1)^-17 of the width 2 is 1.5e-12 of the norm,
+// far inside the cluster tolerance, so two inverse-iteration steps converge.
+constexpr int kBisectRounds = 17;
+constexpr double kDeflate = 0x1p-24;  // relative size of a negligible off-diagonal
+constexpr double kClusterTol = 1e-8;  // relative gap below which vectors are re-orthogonalised
+constexpr double kPivMin = 0x1p-50;   // smallest pivot magnitude of the LDL^T factorisation
+constexpr double kStore = 0x1p-64;    // scale of the intermediate vectors kept in fp32
+
+__device__ __forceinline__ void wave_lds_order() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// Cross-lane sums through DPP (no LDS round trip). dpp_add: x + x of lane
+// (CTRL); lanes outside the row mask add 0.
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ float dpp_add(float x) {
+  return x + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, ROWS, 0xF, false));
+}
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ double dpp_add(double x) {
+  const long long b = __double_as_longlong(x);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)b, CTRL, ROWS, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(b >> 32), CTRL, ROWS, 0xF, false);
+  return x + __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+}
+// Sum over the 4 lanes of a quad (every lane of the quad gets it)
+template <typename F>
+__device__ __forceinline__ F quad_sum(F x) {
+  x = dpp_add<0xB1>(x);  // quad_perm [1, 0, 3, 2]
+  return dpp_add<0x4E>(x);  // quad_perm [2, 3, 0, 1]
+}
+// Sum over the wavefront, returned to every lane (a uniform value)
+__device__ __forceinline__ float wave_sum(float x) {
+  x = quad_sum(x);
+  x = dpp_add<0x141>(x);        // row_half_mirror: 8 lanes
+  x = dpp_add<0x140>(x);        // row_mirror: 16 lanes
+  x = dpp_add<0x142, 0xA>(x);   // row_bcast15 into rows 1, 3
+  x = dpp_add<0x143, 0xC>(x);   // row_bcast31 into rows 2, 3: lane 63 holds the sum
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
+}
+__device__ __forceinline__ double wave_sum(double x) {
+  x = quad_sum(x);
+  x = dpp_add<0x141>(x);
+  x = dpp_add<0x140>(x);
+  x = dpp_add<0x142, 0xA>(x);
+  x = dpp_add<0x143, 0xC>(x);
+  const long long b = __double_as_longlong(x);
+  const int lo = __builtin_amdgcn_readlane((int)b, 63), hi = __builtin_amdgcn_readlane((int)(b >> 32), 63);
+  return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+}
+__device__ __forceinline__ float read_lane(float x, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
+}
+// 1 / x in fp64: the hardware reciprocal and two Newton steps
+__device__ __forceinline__ double recip64(double x) {
+  double r = __builtin_amdgcn_rcp(x);
+  double e = fma(-x, r, 1.0);
+  r = fma(r, e, r);
+  e = fma(-x, r, 1.0);
+  return fma(r, e, r);
 }
 
-// Tournament positions: slot k of a step pairs position k ("top") with
-// position NP + k ("bottom"). Between steps position 0 stays, tops move right,
-// bottoms move left, top NP-1 drops to bottom NP-1 and bottom 0 climbs to
-// top 1: the circle method, so every two players meet once per 2 NP - 1 steps
-// and after a whole sweep every player is back at its first position.
-__device__ __forceinline__ int eigh_next(int pos, int np) {
-  if (pos < np) return pos == 0 ? 0 : (pos == np - 1 ? 2 * np - 1 : pos + 1);
-  return pos == np ? 1 : pos - 1;
+// Number of eigenvalues below x of the block [s, t) of the scaled
+// tridiagonal matrix, tq[i] = (diagonal i, squared off-diagonal i - 1): the
+// sign changes of the sequence 1, p_s, ..., p_{t-1} of leading minors of
+// T - x I (a zero minor counts as a change).
+__device__ __forceinline__ int sturm_below(const double2* tq, int s, int t, double x) {
+  // A minor that is exactly zero counts as positive: the next one then has
+  // the opposite sign of the one before, so the pair adds exactly one change.
+  double p2 = 1.0, p1 = tq[s].x - x;
+  int cnt = p1 < 0.0;
+  int i0 = s + 1;
+  for (; i0 + 8 <= t; i0 += 8) {
+    double2 q[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) q[u] = tq[i0 + u];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const double p = (q[u].x - x) * p1 - q[u].y * p2;
+      cnt += (p < 0.0) != (p1 < 0.0);
+      p2 = p1;
+      p1 = p;
+    }
+    int ex;
+    (void)frexp(fmax(fabs(p1), fabs(p2)), &ex);
+    p1 = ldexp(p1, -ex);
+    p2 = ldexp(p2, -ex);
+  }
+  for (; i0 < t; ++i0) {
+    const double2 q = tq[i0];
+    const double p = (q.x - x) * p1 - q.y * p2;
+    cnt += (p < 0.0) != (p1 < 0.0);
+    p2 = p1;
+    p1 = p;
+  }
+  return cnt;
 }
 
-// Rotation (c, s) that zeroes entry (p, q) of J^T A J, J = [[c, s], [-s, c]]
-// on rows/columns (p, q): t = tan(theta) is the smaller root of
-// t^2 + 2 tau t - 1 = 0, tau = (a_qq - a_pp) / (2 a_pq), taken in the form
-// t = sign(delta) 2 a_pq / (|delta| + sqrt(delta^2 + 4 a_pq^2)), delta =
-// a_qq - a_pp (one square root and one reciprocal). Hardware reciprocal and
-// square-root approximations are enough: any (c, s) with c^2 + s^2 = 1 to
-// rounding keeps the transform orthogonal, and a slightly inexact angle only
-// leaves a tiny off-diagonal that later sweeps remove. Branch-free (selects,
-// not a branch), so that a step's LDS reads issue together.
-__device__ __forceinline__ void jacobi_rotation(float app, float aqq, float apq, float* c,
-                                                float* s) {
-  const bool live = fabsf(apq) > 1e-30f;
-  const float dl = aqq - app, a2 = 2.f * apq;
-  const float r = __builtin_amdgcn_sqrtf(__builtin_fmaf(dl, dl, a2 * a2));
-  float t = a2 * __builtin_amdgcn_rcpf(fabsf(dl) + r);
-  t = __int_as_float(__float_as_int(t) ^ (__float_as_int(dl) & (int)0x80000000));
-  const float cc = __builtin_amdgcn_rsqf(__builtin_fmaf(t, t, 1.f));
-  *c = live ? cc : 1.f;
-  *s = live ? t * cc : 0.f;
+// Pseudo-random start of inverse iteration: +-[0.5, 1.5)
+__device__ __forceinline__ float start_value(int g, int i) {
+  uint32_t h = (uint32_t)(g * 0x9E3779B1u) ^ (uint32_t)(i * 0x85EBCA77u + 0x165667B1u);
+  h ^= h >> 15;
+  h *= 0x2C1B3C6Du;
+  h ^= h >> 12;
+  h *= 0x297A2D39u;
+  h ^= h >> 15;
+  const float u = 0.5f + (float)(h & 0xFFFFu) * (1.f / 65536.f);
+  return (h & 0x10000u) ? -u : u;
 }
 
 // 4x4 register blocks of a d x d product (d <= 128, NT threads: at most two
-// blocks per thread): acc = op(X) op(Y), op(Z) = Z or Z^T, with X, Y
-// in LDS at row stride ld and zero padding up to a multiple of 4.
+// blocks per thread): acc = op(X) op(Y), op(Z) = Z or Z^T, with X, Y in LDS
+// at row stride ld (a multiple of 4, 16-byte aligned rows) and zeros up to a
+// multiple of 4; the sum runs over 4 indices per float4 load.
 struct MMAcc {
   float v[2][16];
 };
@@ -319,17 +402,26 @@ __device__ __forceinline__ void lds_mm(const float* X, bool tX, const float* Y, 
     const int blk = threadIdx.x + NT * u;
     if (blk >= nb) continue;
     const int i0 = 4 * (blk / d4), j0 = 4 * (blk % d4);
-    for (int t = 0; t < d; ++t) {
-      float x[4], y[4];
+    for (int t = 0; t < d; t += 4) {
+      float x[4][4], y[4][4];  // x[a][s] = op(X)[i0 + a][t + s], y[s][b] = op(Y)[t + s][j0 + b]
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        x[k] = tX ? X[t * ld + i0 + k] : X[(i0 + k) * ld + t];
-        y[k] = tY ? Y[(j0 + k) * ld + t] : Y[t * ld + j0 + k];
+        const float4 xv = *reinterpret_cast<const float4*>(tX ? &X[(t + k) * ld + i0] : &X[(i0 + k) * ld + t]);
+        const float4 yv = *reinterpret_cast<const float4*>(tY ? &Y[(j0 + k) * ld + t] : &Y[(t + k) * ld + j0]);
+        const float xs[4] = {xv.x, xv.y, xv.z, xv.w}, ys[4] = {yv.x, yv.y, yv.z, yv.w};
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          if (tX) x[m][k] = xs[m]; else x[k][m] = xs[m];
+          if (tY) y[m][k] = ys[m]; else y[k][m] = ys[m];
+        }
       }
 #pragma unroll
-      for (int a = 0; a < 4; ++a)
+      for (int s = 0; s < 4; ++s)
 #pragma unroll
-        for (int b = 0; b < 4; ++b) acc.v[u][4 * a + b] = __builtin_fmaf(x[a], y[b], acc.v[u][4 * a + b]);
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+          for (int b = 0; b < 4; ++b)
+            acc.v[u][4 * a + b] = __builtin_fmaf(x[a][s], y[s][b], acc.v[u][4 * a + b]);
     }
   }
 }
@@ -357,22 +449,24 @@ __global__ __launch_bounds__(eigh_threads<DM>()) void eigh_kernel(Ctx C, EighJob
   static_assert((DM / 4) * (DM / 4) <= 2 * NT, "two 4x4 product blocks per thread");
   constexpr int EP = eigh_stride(DM);
   constexpr int NW = NT / 64;
-  constexpr int CPL = DM / 64;             // columns per lane in a row sweep
-  constexpr int NP = DM / 2;               // pairs per step
-  constexpr int TPI = NT / NP;             // threads per row pair
-  constexpr int BPT = NP / TPI;            // 2x2 blocks per thread
-  constexpr int RG = 64 / TPI;             // row pairs per wavefront
-  static_assert(CPL >= 1 && TPI * NP == NT && BPT * TPI == NP && RG * TPI == 64, "matrix size");
-  constexpr bool kDB = eigh_double_buffer(DM);
-  extern __shared__ float esh[];
-  float* A = esh;             // [DM][EP]
-  float* Vt = esh + DM * EP;  // [DM][EP], Vt[i][j] = V[j][i]
-  float* A2 = kDB ? esh + 2 * DM * EP : esh;  // second copies (double-buffered)
-  float* Vt2 = kDB ? esh + 3 * DM * EP : Vt;
-  __shared__ float red[2][NW];
-  __shared__ float uvec[DM], ovec[DM], lam[DM], sgn[DM];
+  constexpr int CPL = DM / 64;           // rows (or columns) per lane in a wavefront sweep
+  constexpr int NQ = DM / (4 * kEighM);  // float4 column groups per thread in a row pass
+  constexpr int RW = DM / kEighM;        // rows per thread in the back-transformation
+  static_assert(CPL >= 1 && NQ >= 1 && RW % 4 == 0, "matrix size");
+  extern __shared__ __attribute__((aligned(16))) float esh[];
+  float* A = esh;             // [DM][EP]; row k keeps reflector k once reduced
+  float* Vt = esh + DM * EP;  // [DM][EP]: S during the prologue, then Z[g][r] (vector g)
+  __shared__ __attribute__((aligned(16))) float vvs[2][NW][DM];  // reflectors, one copy per wave
+  __shared__ __attribute__((aligned(16))) float pbuf[2][DM];     // p = A v of the last two steps
+  __shared__ float kpart[2][NW];
+  __shared__ float trid[2][DM];  // diagonal, off-diagonal of T
+  __shared__ double2 tq[DM];     // scaled (diagonal i, squared off-diagonal i - 1)
+  __shared__ double es[DM], lam64[DM];
+  __shared__ int bs[DM], be[DM], inv[DM];
+  __shared__ double sh_tn;
+  __shared__ uint64_t sh_link[CPL];
+  __shared__ float uvec[DM], ovec[DM], mvec[DM], lam[DM], sgn[DM];
   __shared__ int rnk[DM];
-  __shared__ int sh_stop;
   const int bh = blockIdx.x, d = C.d, tid = threadIdx.x;
   const EighJob& jb = J.j[blockIdx.y];
   const int lane = tid & 63;
@@ -389,18 +483,24 @@ __global__ __launch_bounds__(eigh_threads<DM>()) void eigh_kernel(Ctx C, EighJob
         A[i * EP + j] = in ? Bg[i * d + j] : 0.f;
         Vt[i * EP + j] = Sg ? (in ? Sg[i * d + j] : 0.f) : 0.f;  // S while it is needed
       }
-    if (tid < DM) ovec[tid] = 0.f;
+    if (tid < DM) {
+      ovec[tid] = 0.f;
+      mvec[tid] = jb.m >= 0 && tid < d ? vec(C, bh, jb.m)[tid] : 0.f;
+    }
     __syncthreads();
     if (jb.m >= 0) {
       // u = S^T m (or m)
-      const float* mg = vec(C, bh, jb.m);
       if (tid < d) {
         float u;
         if (Sg) {
-          u = 0.f;
-          for (int t = 0; t < d; ++t) u = __builtin_fmaf(Vt[t * EP + tid], mg[t], u);
+          float u4[4] = {0.f, 0.f, 0.f, 0.f};
+          for (int t = 0; t < d; t += 4)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              u4[e] = __builtin_fmaf(Vt[(t + e) * EP + tid], mvec[t + e], u4[e]);
+          u = (u4[0] + u4[1]) + (u4[2] + u4[3]);
         } else {
-          u = mg[tid];
+          u = mvec[tid];
         }
         uvec[tid] = u;
         ovec[tid] = u;
@@ -428,143 +528,416 @@ __global__ __launch_bounds__(eigh_threads<DM>()) void eigh_kernel(Ctx C, EighJob
           if (j < d) A[i * EP + j] -= uvec[i] * uvec[j];
         }
     if (jb.u_out >= 0 && tid < d) vec(C, bh, jb.u_out)[tid] = uvec[tid];
-    for (int i = wv; i < DM; i += NW)
-#pragma unroll
-      for (int cc = 0; cc < CPL; ++cc) {
-        const int j = lane + 64 * cc;
-        Vt[i * EP + j] = i == j ? 1.f : 0.f;
-      }
+    __syncthreads();
   }
-  if (tid == 0) sh_stop = 0;
-  int cur = 0;  // which copy holds the current A and V^T (double-buffered)
-  const int rp = tid / TPI, cp0 = tid % TPI;  // this thread's row pair, first column pair
-  // One step of a sweep, with the copy it reads (S) fixed at compile time so
-  // that every LDS address is loop-invariant.
-  auto step_body = [&](auto copy_tag) {
-    constexpr int S = decltype(copy_tag)::value;
-    const float* Ac = S ? A2 : A;
-    const float* Vc = S ? Vt2 : Vt;
-    float* An = S ? A : A2;
-    float* Vn = S ? Vt : Vt2;
-    const int ti = rp, bi = NP + rp;  // positions of the row pair
-    // Rotations of this thread's column pairs.
-    float cj[BPT], sj[BPT];
+  // ---- 1. Householder reduction. Step k: reflector H_k = I - v v^T (|v|^2 = 2,
+  // support k+1..d-1) from column k after the update by H_{k-1}; the row pass
+  // applies H_{k-1} to the block [k+1, d)^2 and accumulates p = A v; with
+  // w = p - (v^T p / 2) v, H A H = A - v w^T - w v^T.
+  const int nref = d > 2 ? d - 2 : 0;
+  {
+    // Row pass layout: the 16 lanes of a DPP row share 4 rows (rs, rs + DM/4,
+    // rs + DM/2, rs + 3 DM/4; rs = 4 * wave + lane / 16, so the live rows of
+    // a step are spread over all wavefronts) and split their float4 column
+    // groups (c16, c16 + 16, ...): the vectors are read once per group and
+    // used for 4 rows, and the 16 lanes read an A row contiguously.
+    constexpr int RPT = 4;               // rows per lane
+    constexpr int NG = DM / 64;          // column groups per lane
+    const int c16 = lane & 15, rs = 4 * wv + (lane >> 4);
+    for (int k = 0; k < nref; ++k) {
+      const int cur = k & 1, prv = cur ^ 1;
+      float* vcur = vvs[cur][wv];
+      const float* vprv = vvs[prv][wv];
+      const float* pprv = pbuf[prv];
+      float Kp = 0.f, vk = 0.f, wk = 0.f;
+      if (k > 0) {
 #pragma unroll
-    for (int b = 0; b < BPT; ++b) {
-      const int tj = cp0 + TPI * b, bj = NP + tj;
-      jacobi_rotation(Ac[tj * EP + tj], Ac[bj * EP + bj], Ac[tj * EP + bj], &cj[b], &sj[b]);
-    }
-    // The row pair's rotation was derived by the lane of group 0 whose column
-    // pair it is (the same block index for every group of the wavefront).
-    float ci = 1.f, si = 0.f;
-    {
-      const int bsel = (RG * wv) / TPI;
-      float cs = cj[0], ss = sj[0];
-#pragma unroll
-      for (int b = 1; b < BPT; ++b)
-        if (b == bsel) cs = cj[b], ss = sj[b];
-#pragma unroll
-      for (int g = 0; g < RG; ++g) {
-        const int rg = (RG * wv + g) % TPI;
-        const float cg = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cs), rg));
-        const float sg = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ss), rg));
-        const bool mine = lane / TPI == g;
-        ci = mine ? cg : ci;
-        si = mine ? sg : si;
+        for (int w = 0; w < NW; ++w) Kp += kpart[prv][w];
+        Kp *= 0.5f;
+        vk = vprv[k];
+        wk = pprv[k] - Kp * vk;
       }
-    }
-    float blk[BPT][4], vb[BPT][4];
+      // column k below the diagonal (every wavefront, one or two rows a lane)
+      float x[CPL];
+      double s2 = 0.0;
 #pragma unroll
-    for (int b = 0; b < BPT; ++b) {
-      const int cp = cp0 + TPI * b, tj = cp, bj = NP + cp;
-      const float a00 = Ac[ti * EP + tj], a01 = Ac[ti * EP + bj];
-      const float a10 = Ac[bi * EP + tj], a11 = Ac[bi * EP + bj];
-      // rows (p, q) from the left, then columns from the right
-      const float x00 = ci * a00 - si * a10, x01 = ci * a01 - si * a11;
-      const float x10 = si * a00 + ci * a10, x11 = si * a01 + ci * a11;
-      blk[b][0] = cj[b] * x00 - sj[b] * x01;
-      blk[b][1] = sj[b] * x00 + cj[b] * x01;
-      blk[b][2] = cj[b] * x10 - sj[b] * x11;
-      blk[b][3] = sj[b] * x10 + cj[b] * x11;
-      if (cp == rp) blk[b][1] = blk[b][2] = 0.f;  // the pair's own entry is zeroed
-      const float v00 = Vc[ti * EP + tj], v01 = Vc[ti * EP + bj];
-      const float v10 = Vc[bi * EP + tj], v11 = Vc[bi * EP + bj];
-      vb[b][0] = ci * v00 - si * v10;
-      vb[b][1] = ci * v01 - si * v11;
-      vb[b][2] = si * v00 + ci * v10;
-      vb[b][3] = si * v01 + ci * v11;
-    }
-    if (!kDB) __syncthreads();  // every read done before A and V^T are overwritten
-    const int nti = eigh_next(ti, NP), nbi = eigh_next(bi, NP);
+      for (int h = 0; h < CPL; ++h) {
+        const int i = lane + 64 * h;
+        float xi = 0.f;
+        if (i > k && i < d) {
+          xi = A[i * EP + k];
+          if (k > 0) {
+            const float vi = vprv[i], wi = pprv[i] - Kp * vi;
+            xi -= vi * wk + wi * vk;
+          }
+        }
+        x[h] = xi;
+        s2 += (double)xi * (double)xi;
+      }
+      s2 = wave_sum(s2);
+      const int i0 = k + 1;
+      float x0 = x[0];
 #pragma unroll
-    for (int b = 0; b < BPT; ++b) {
-      const int cp = cp0 + TPI * b, tj = cp, bj = NP + cp;
-      const int ntj = eigh_next(tj, NP), nbj = eigh_next(bj, NP);
-      An[nti * EP + ntj] = blk[b][0];
-      An[nti * EP + nbj] = blk[b][1];
-      An[nbi * EP + ntj] = blk[b][2];
-      An[nbi * EP + nbj] = blk[b][3];
-      Vn[nti * EP + tj] = vb[b][0];
-      Vn[nti * EP + bj] = vb[b][1];
-      Vn[nbi * EP + tj] = vb[b][2];
-      Vn[nbi * EP + bj] = vb[b][3];
-    }
-    __syncthreads();
-  };
-  for (int sweep = 0; sweep < 40; ++sweep) {
-    const float* Ac = cur ? A2 : A;
-    __syncthreads();
-    // Convergence: off-diagonal mass relative to the total.
-    float off = 0.f, tot = 0.f;
-    for (int i = wv; i < d; i += NW)
+      for (int h = 1; h < CPL; ++h) x0 = (i0 >> 6) == h ? x[h] : x0;
+      x0 = read_lane(x0, i0 & 63);
+      // sigma = |x|, alpha = -sign(x0) sigma, scale 1 / sqrt(sigma (sigma + |x0|)):
+      // hardware reciprocal square roots with one Newton step each
+      double rs2 = __builtin_amdgcn_rsq(s2);
+      rs2 = rs2 * fma(-0.5 * s2 * rs2, rs2, 1.5);
+      const double sig = s2 > 0.0 ? s2 * rs2 : 0.0;
+      const double alpha = x0 >= 0.f ? -sig : sig;
+      const double hq = sig * (sig + fabs((double)x0));
+      double scl = __builtin_amdgcn_rsq(hq);
+      scl = s2 > 0.0 ? scl * fma(-0.5 * hq * scl, scl, 1.5) : 0.0;
 #pragma unroll
-      for (int cc = 0; cc < CPL; ++cc) {
-        const int j = lane + 64 * cc;
-        const float a = Ac[i * EP + j];
-        tot += a * a;
-        off += i != j ? a * a : 0.f;
+      for (int h = 0; h < CPL; ++h) {
+        const int i = lane + 64 * h;
+        float v = 0.f;
+        if (i > k && i < d) v = (float)(((double)x[h] - (i == i0 ? alpha : 0.0)) * scl);
+        vcur[i] = v;
+        if (wv == 0 && i > k && i < d) A[k * EP + i] = v;
+      }
+      if (wv == 0 && lane == 0) {
+        trid[0][k] = A[k * EP + k] - (k > 0 ? 2.f * vk * wk : 0.f);
+        trid[1][k] = (float)alpha;
+      }
+      wave_lds_order();
+      // row pass over [k+1, d)^2
+      float vr[RPT], wr[RPT], vc[RPT], acc[RPT];
+      bool rl[RPT];
+#pragma unroll
+      for (int r = 0; r < RPT; ++r) {
+        const int row = rs + r * (DM / RPT);
+        rl[r] = row > k && row < d;
+        vc[r] = vcur[row];
+        vr[r] = k > 0 ? vprv[row] : 0.f;
+        wr[r] = k > 0 ? pprv[row] - Kp * vr[r] : 0.f;
+        acc[r] = 0.f;
       }
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      off += __shfl_xor(off, o, 64);
-      tot += __shfl_xor(tot, o, 64);
+      for (int q = 0; q < NG; ++q) {
+        const int j0 = 4 * (c16 + 16 * q);
+        if (j0 + 3 <= k) continue;  // every column of the group is dead
+        const float4 vn = *reinterpret_cast<const float4*>(&vcur[j0]);
+        const float vnv[4] = {vn.x, vn.y, vn.z, vn.w};
+        float wpv[4] = {0.f, 0.f, 0.f, 0.f}, vpv[4] = {0.f, 0.f, 0.f, 0.f};
+        if (k > 0) {
+          const float4 vp = *reinterpret_cast<const float4*>(&vprv[j0]);
+          const float4 pp = *reinterpret_cast<const float4*>(&pprv[j0]);
+          vpv[0] = vp.x; vpv[1] = vp.y; vpv[2] = vp.z; vpv[3] = vp.w;
+          wpv[0] = pp.x - Kp * vp.x; wpv[1] = pp.y - Kp * vp.y;
+          wpv[2] = pp.z - Kp * vp.z; wpv[3] = pp.w - Kp * vp.w;
+        }
+        bool ok[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) ok[e] = j0 + e > k && j0 + e < d;
+#pragma unroll
+        for (int r = 0; r < RPT; ++r) {
+          if (!rl[r]) continue;
+          const int row = rs + r * (DM / RPT);
+          const float4 a = *reinterpret_cast<const float4*>(&A[row * EP + j0]);
+          float av[4] = {a.x, a.y, a.z, a.w};
+          if (k > 0) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float upd = av[e] - (vr[r] * wpv[e] + wr[r] * vpv[e]);
+              av[e] = ok[e] ? upd : av[e];
+            }
+            *reinterpret_cast<float4*>(&A[row * EP + j0]) = make_float4(av[0], av[1], av[2], av[3]);
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[r] += ok[e] ? av[e] * vnv[e] : 0.f;
+        }
+      }
+      // row sums over the 16 lanes of the DPP row
+      float vp_part = 0.f;
+#pragma unroll
+      for (int r = 0; r < RPT; ++r) {
+        float t = quad_sum(acc[r]);
+        t = dpp_add<0x141>(t);  // row_half_mirror
+        t = dpp_add<0x140>(t);  // row_mirror
+        const int row = rs + r * (DM / RPT);
+        if (c16 == 0) {
+          pbuf[cur][row] = rl[r] ? t : 0.f;
+          vp_part += rl[r] ? vc[r] * t : 0.f;
+        }
+      }
+      vp_part = wave_sum(vp_part);
+      if (lane == 0) kpart[cur][wv] = vp_part;
+      __syncthreads();
     }
-    if (lane == 0) {
-      red[0][wv] = off;
-      red[1][wv] = tot;
-    }
-    __syncthreads();
+    // the last 2 x 2 block after the last reflector
     if (tid == 0) {
-      float so = 0.f, st = 0.f;
-      for (int i = 0; i < NW; ++i) {
-        so += red[0][i];
-        st += red[1][i];
+      if (d == 1) {
+        trid[0][0] = A[0];
+      } else if (d >= 2) {
+        const int i = d - 2, j = d - 1;
+        float vi = 0.f, wi = 0.f, vj = 0.f, wj = 0.f;
+        if (nref > 0) {
+          const int l = (nref - 1) & 1;
+          float Kp = 0.f;
+          for (int w = 0; w < NW; ++w) Kp += kpart[l][w];
+          Kp *= 0.5f;
+          vi = vvs[l][0][i];
+          vj = vvs[l][0][j];
+          wi = pbuf[l][i] - Kp * vi;
+          wj = pbuf[l][j] - Kp * vj;
+        }
+        trid[0][i] = A[i * EP + i] - 2.f * vi * wi;
+        trid[0][j] = A[j * EP + j] - 2.f * vj * wj;
+        trid[1][i] = A[j * EP + i] - (vj * wi + wj * vi);
       }
-      // Stop one sweep after the off-diagonal mass falls below (d * 2e-6)^2 of
-      // the total: above the fp32 rounding floor (about (d * eps)^2), and
-      // quadratic convergence makes the extra sweep reach that floor.
-      const float thr = (float)d * 2e-6f;
-      sh_stop = (so <= thr * thr * st) ? sh_stop + 1 : 0;
-      if (so == 0.f) sh_stop = 2;
     }
     __syncthreads();
-    if (sh_stop >= 2) break;
-    for (int step = 0; step < DM - 1; ++step) {
-      if (cur == 0)
-        step_body(std::integral_constant<int, 0>{});
-      else
-        step_body(std::integral_constant<int, 1>{});
-      if (kDB) cur ^= 1;
+    // row k < nref holds reflector k in columns k+1..d-1; clear the rest
+    for (int idx = tid; idx < DM * DM; idx += NT) {
+      const int k = idx / DM, j = idx % DM;
+      if (k < nref && j <= k) A[k * EP + j] = 0.f;
     }
+    __syncthreads();
+  }
+  // ---- 2. scaling, deflation, blocks (wavefront 0), then bisection
+  if (wv == 0) {
+    double tn = 0.0;
+    double dv[CPL], ev[CPL];
+#pragma unroll
+    for (int h = 0; h < CPL; ++h) {
+      const int i = lane + 64 * h;
+      dv[h] = i < d ? (double)trid[0][i] : 0.0;
+      ev[h] = i + 1 < d ? (double)trid[1][i] : 0.0;
+      const double el = i >= 1 && i < d ? fabs((double)trid[1][i - 1]) : 0.0;
+      tn = fmax(tn, fabs(dv[h]) + fabs(ev[h]) + el);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) tn = fmax(tn, __shfl_xor(tn, o, 64));
+    const double inv_tn = tn > 0.0 ? 1.0 / tn : 0.0;
+    uint64_t brk[CPL];
+#pragma unroll
+    for (int h = 0; h < CPL; ++h) {
+      const int i = lane + 64 * h;
+      double e = ev[h] * inv_tn;
+      if (fabs(e) <= kDeflate) e = 0.0;
+      es[i] = e;
+      // a block ends after i when i is the last index or T decouples there
+      brk[h] = __ballot(i < d && (i == d - 1 || e == 0.0));
+    }
+    wave_lds_order();
+#pragma unroll
+    for (int h = 0; h < CPL; ++h) {
+      const int i = lane + 64 * h;
+      const double em = i >= 1 ? es[i - 1] : 0.0;
+      tq[i] = make_double2(dv[h] * inv_tn, em * em);
+      // start: one past the last break before i; end: one past the first break at or after i
+      int st = 0, en = d;
+#pragma unroll
+      for (int g = CPL - 1; g >= 0; --g) {
+        if (g > h) continue;
+        const uint64_t m = g == h ? (lane == 0 ? 0ull : (brk[g] & ((~0ull) >> (64 - lane)))) : brk[g];
+        if (m && st == 0) st = 64 * g + 63 - __builtin_clzll(m) + 1;
+      }
+#pragma unroll
+      for (int g = 0; g < CPL; ++g) {
+        if (g < h) continue;
+        const uint64_t m = g == h ? (brk[g] & ((~0ull) << lane)) : brk[g];
+        if (m && en == d) en = 64 * g + __builtin_ctzll(m) + 1;
+      }
+      bs[i] = i < d ? st : 0;
+      be[i] = i < d ? en : 1;
+    }
+    if (lane == 0) sh_tn = tn;
   }
   __syncthreads();
-  float* Ac = cur ? A2 : A;
-  const float* Vc = cur ? Vt2 : Vt;
+  const double tn = sh_tn;
+  {
+    const int g = tid / kEighM, q = tid % kEighM;
+    const bool live = g < d && tn > 0.0;
+    const int s = live ? bs[g] : 0, t = live ? be[g] : 1, j = g - s;
+    double lo = -1.0 - 0x1p-40, hi = 1.0 + 0x1p-40;
+    for (int round = 0; round < kBisectRounds; ++round) {
+      const double step = (hi - lo) / (double)(kEighM + 1);
+      const int c = live ? sturm_below(tq, s, t, lo + step * (double)(q + 1)) : 0;
+      // counts of the quad's four points (quad_perm broadcasts)
+      const int below = (__builtin_amdgcn_update_dpp(0, c, 0x00, 0xF, 0xF, false) <= j) +
+                        (__builtin_amdgcn_update_dpp(0, c, 0x55, 0xF, 0xF, false) <= j) +
+                        (__builtin_amdgcn_update_dpp(0, c, 0xAA, 0xF, 0xF, false) <= j) +
+                        (__builtin_amdgcn_update_dpp(0, c, 0xFF, 0xF, 0xF, false) <= j);
+      const double nlo = below > 0 ? lo + step * (double)below : lo;
+      const double nhi = below < kEighM ? lo + step * (double)(below + 1) : hi;
+      lo = nlo;
+      hi = nhi;
+    }
+    if (q == 0) lam64[g] = live ? 0.5 * (lo + hi) : 0.0;
+  }
+  __syncthreads();
+  // ---- 3. eigenvectors of T: clusters (wavefront 0), start vectors (all)
+  if (wv == 0) {
+#pragma unroll
+    for (int h = 0; h < CPL; ++h) {
+      const int g = lane + 64 * h;
+      const bool link = g >= 1 && g < d && bs[g] == bs[g - 1] &&
+                        lam64[g] - lam64[g - 1] < kClusterTol;
+      const uint64_t m = __ballot(link);
+      if (lane == 0) sh_link[h] = m;
+    }
+  }
+  for (int idx = tid; idx < DM * DM; idx += NT) {
+    const int g = idx / DM, i = idx % DM;
+    const bool in = g < d && i >= bs[g] && i < be[g];
+    Vt[g * EP + i] = in ? (tn > 0.0 ? start_value(g, i) : (i == g ? 1.f : 0.f)) : 0.f;
+  }
+  __syncthreads();
+  if (tn > 0.0) {
+    // vector g on the kEighM lanes of a quad, SEG consecutive entries each.
+    // No per-entry masks: the off-diagonal entry at each end of g's block is
+    // zero, so both recurrences restart there, and the start vector is zero
+    // outside the block, so those entries stay exactly zero.
+    constexpr int SEG = DM / kEighM;
+    const int g = tid / kEighM, part = tid % kEighM;
+    const bool live = g < d;
+    const double sigma = live ? lam64[g] : 0.0;
+    float* z = Vt + (size_t)(live ? g : 0) * EP + SEG * part;
+    const double2* tqs = tq + SEG * part;
+    const double* ess = es + SEG * part;
+    for (int it = 0; it < 2; ++it) {
+      double r[SEG];  // 1 / pivot of this lane's entries
+      // forward: T - sigma I = L D L^T, y = L^{-1} b (kept in z, scaled);
+      // the quad's lanes take their segments in turn, passing (l, y) on
+      double lprev = 0.0, yprev = 0.0;
+#pragma unroll
+      for (int h = 0; h < kEighM; ++h) {
+        if (h > 0) {
+          const int src = (lane & ~(kEighM - 1)) + h - 1;
+          lprev = __shfl(lprev, src, 64);
+          yprev = __shfl(yprev, src, 64);
+        }
+        if (live && part == h) {
+#pragma unroll
+          for (int u = 0; u < SEG; ++u) {
+            if ((u & 7) == 0) asm volatile("" ::: "memory");
+            const double a = tqs[u].x - sigma;
+            const double em = u > 0 ? ess[u - 1] : (h > 0 ? es[SEG * h - 1] : 0.0);
+            double dl = fma(-lprev, em, a);
+            const double y = fma(-lprev, yprev, (double)z[u]);
+            dl = fabs(dl) < kPivMin ? (dl < 0.0 ? -kPivMin : kPivMin) : dl;
+            r[u] = recip64(dl);
+            lprev = ess[u] * r[u];
+            yprev = y;
+            z[u] = (float)(y * kStore);
+          }
+        }
+      }
+      // backward: x = D^{-1} y - L^T x, kept in z (scaled); max |x|
+      double xn = 0.0, mx = 0.0;
+#pragma unroll
+      for (int h = kEighM - 1; h >= 0; --h) {
+        if (h < kEighM - 1) xn = __shfl(xn, (lane & ~(kEighM - 1)) + h + 1, 64);
+        if (live && part == h) {
+#pragma unroll
+          for (int u = SEG - 1; u >= 0; --u) {
+            if ((u & 7) == 7) asm volatile("" ::: "memory");
+            const double xv = r[u] * fma(-ess[u], xn, (double)z[u] * (1.0 / kStore));
+            xn = xv;
+            mx = fmax(mx, fabs(xv));
+            z[u] = (float)(xv * kStore);
+          }
+        }
+      }
+      mx = fmax(mx, __shfl_xor(mx, 1, 64));
+      mx = fmax(mx, __shfl_xor(mx, 2, 64));
+      // normalise
+      const double sc = mx > 0.0 ? 1.0 / (mx * kStore) : 0.0;
+      double ss = 0.0;
+      if (live)
+#pragma unroll
+        for (int u = 0; u < SEG; ++u) {
+          const double v = (double)z[u] * sc;
+          ss += v * v;
+        }
+      ss = quad_sum(ss);
+      const double nrm = ss > 0.0 ? sc / sqrt(ss) : 0.0;
+      if (live)
+#pragma unroll
+        for (int u = 0; u < SEG; ++u) z[u] = (float)((double)z[u] * nrm);
+      __syncthreads();
+      // clusters: modified Gram-Schmidt in slot order (wavefront 0)
+      if (wv == 0) {
+        for (int h = 0; h < CPL; ++h) {
+          uint64_t m = sh_link[h];
+          while (m) {
+            const int gj = 64 * h + __builtin_ctzll(m);
+            m &= m - 1;
+            int g0 = gj;
+            while (g0 > 0 && ((sh_link[g0 >> 6] >> (g0 & 63)) & 1)) --g0;
+            float zj[CPL];
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) zj[c] = Vt[gj * EP + lane + 64 * c];
+            for (int gi = g0; gi < gj; ++gi) {
+              float dot = 0.f;
+#pragma unroll
+              for (int c = 0; c < CPL; ++c) dot += Vt[gi * EP + lane + 64 * c] * zj[c];
+              dot = wave_sum(dot);
+#pragma unroll
+              for (int c = 0; c < CPL; ++c) zj[c] -= dot * Vt[gi * EP + lane + 64 * c];
+            }
+            float nn = 0.f;
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) nn += zj[c] * zj[c];
+            nn = wave_sum(nn);
+            const float rn = nn > 0.f ? 1.f / sqrtf(nn) : 0.f;
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) Vt[gj * EP + lane + 64 * c] = zj[c] * rn;
+            wave_lds_order();
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // ---- 4. back-transformation: vector g (rows split over kEighM threads)
+  {
+    const int g = tid / kEighM, c = tid % kEighM;
+    float zr[RW];
+#pragma unroll
+    for (int u = 0; u < RW; u += 4) {
+      const float4 v4 = *reinterpret_cast<const float4*>(&Vt[g * EP + c * RW + u]);
+      zr[u] = v4.x;
+      zr[u + 1] = v4.y;
+      zr[u + 2] = v4.z;
+      zr[u + 3] = v4.w;
+    }
+    for (int k = nref - 1; k >= 0; --k) {
+      float vr[RW];
+      float dp[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int u = 0; u < RW; u += 4) {
+        const float4 v4 = *reinterpret_cast<const float4*>(&A[k * EP + c * RW + u]);
+        vr[u] = v4.x;
+        vr[u + 1] = v4.y;
+        vr[u + 2] = v4.z;
+        vr[u + 3] = v4.w;
+      }
+#pragma unroll
+      for (int u = 0; u < RW; ++u) dp[u & 3] = __builtin_fmaf(vr[u], zr[u], dp[u & 3]);
+      const float dot = quad_sum((dp[0] + dp[1]) + (dp[2] + dp[3]));
+#pragma unroll
+      for (int u = 0; u < RW; ++u) zr[u] = __builtin_fmaf(-dot, vr[u], zr[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < RW; u += 4)
+      *reinterpret_cast<float4*>(&Vt[g * EP + c * RW + u]) =
+          make_float4(zr[u], zr[u + 1], zr[u + 2], zr[u + 3]);
+  }
+  __syncthreads();
+  float* Ac = A;
+  const float* Vc = Vt;
   // ---- epilogue: eigenvalues, ranks (descending, ties by index), orientation
   if (tid < d) {
-    lam[tid] = Ac[tid * EP + tid];
-    float o = 0.f;
-    for (int t = 0; t < d; ++t) o = __builtin_fmaf(ovec[t], Vc[tid * EP + t], o);
+    lam[tid] = (float)(lam64[tid] * tn);
+    float o4[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < d; t += 4)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o4[e] = __builtin_fmaf(ovec[t + e], Vc[tid * EP + t + e], o4[e]);
+    const float o = (o4[0] + o4[1]) + (o4[2] + o4[3]);
     sgn[tid] = o < 0.f ? -1.f : 1.f;
   }
   __syncthreads();
@@ -576,30 +949,30 @@ __global__ __launch_bounds__(eigh_threads<DM>()) void eigh_kernel(Ctx C, EighJob
       r += (lj > li) || (lj == li && j < tid);
     }
     rnk[tid] = r;
+    inv[r] = tid;
     vec(C, bh, jb.vals)[r] = li;
   }
   __syncthreads();
   float* U = mat(C, bh, jb.vecs);
   float* T = mat(C, bh, jb.t_out);
   bf16* W = jb.wop_out >= 0 ? wop(C, bh, jb.wop_out) : nullptr;
-  // Eigenvector i becomes column rnk[i]: U[r][rnk[i]] = sgn[i] Vc[i][r].
-  for (int i = wv; i < d; i += NW)
+  // Eigenvector g becomes column rnk[g]: U[r][c] = sgn[g] Vc[g][r], g = inv[c]
+  // (lanes over c: coalesced rows of U)
+  for (int r = wv; r < d; r += NW)
 #pragma unroll
     for (int cc = 0; cc < CPL; ++cc) {
-      const int r = lane + 64 * cc;
-      if (r < d) U[r * d + rnk[i]] = sgn[i] * Vc[i * EP + r];
+      const int c = lane + 64 * cc;
+      if (c < d) {
+        const int g = inv[c];
+        U[r * d + c] = sgn[g] * Vc[g * EP + r];
+      }
     }
-  auto put_t = [&](int r, int i, float v) {  // T[r][rnk[i]] = v
-    const int j = rnk[i];
-    T[r * d + j] = v;
-    if (W) {
-      const bf16 hi = (bf16)v;
-      W[j * d + r] = hi;
-      W[d * d + j * d + r] = (bf16)(v - (float)hi);
-    }
-  };
-  if (jb.t_f >= 0) {
-    // T'[r][i] = sum_t F[r][t] Vc[i][t]; F goes into the A region.
+  // The projection T[r][c] = sgn[g] P[r][g] with P = F V (t_f) or V, and its
+  // bf16 operand pair W[c][r] (hi) and W[d * d + c * d + r] (lo).
+  const float* P = Vc;  // P[r][g] at Vc[g * EP + r] (V), or at Ac[r * EP + g] (F V)
+  const bool fv = jb.t_f >= 0;
+  if (fv) {
+    // P = F V: F goes into the A region
     const float* Sg = mat(C, bh, jb.t_f);
     for (int i = wv; i < DM; i += NW)
 #pragma unroll
@@ -610,28 +983,34 @@ __global__ __launch_bounds__(eigh_threads<DM>()) void eigh_kernel(Ctx C, EighJob
     __syncthreads();
     MMAcc acc;
     lds_mm<NT>(Ac, false, Vc, true, EP, d, acc);
-    const int d4 = (d + 3) >> 2, nb = d4 * d4;
+    __syncthreads();
+    lds_mm_store<NT>(acc, Ac, EP, d);
+    __syncthreads();
+    P = Ac;
+  }
+  for (int r = wv; r < d; r += NW)
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int blk = tid + NT * u;
-      if (blk >= nb) continue;
-      const int i0 = 4 * (blk / d4), j0 = 4 * (blk % d4);
-#pragma unroll
-      for (int a2 = 0; a2 < 4; ++a2)
-#pragma unroll
-        for (int b2 = 0; b2 < 4; ++b2) {
-          const int r = i0 + a2, i = j0 + b2;
-          if (r < d && i < d) put_t(r, i, sgn[i] * acc.v[u][4 * a2 + b2]);
-        }
+    for (int cc = 0; cc < CPL; ++cc) {
+      const int c = lane + 64 * cc;
+      if (c < d) {
+        const int g = inv[c];
+        T[r * d + c] = sgn[g] * (fv ? P[r * EP + g] : P[g * EP + r]);
+      }
     }
-  } else {
-    for (int i = wv; i < d; i += NW)
+  if (W)
+    for (int c = wv; c < d; c += NW) {
+      const int g = inv[c];
 #pragma unroll
       for (int cc = 0; cc < CPL; ++cc) {
         const int r = lane + 64 * cc;
-        if (r < d) put_t(r, i, sgn[i] * Vc[i * EP + r]);
+        if (r < d) {
+          const float v = sgn[g] * (fv ? P[r * EP + g] : P[g * EP + r]);
+          const bf16 hi = (bf16)v;
+          W[c * d + r] = hi;
+          W[d * d + c * d + r] = (bf16)(v - (float)hi);
+        }
       }
-  }
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -648,7 +1027,7 @@ constexpr int kCP = kMaxD + 1;
 
 __global__ __launch_bounds__(kCholThreads) void cholesky_kernel(Ctx C, int in0, int out0, int in1,
                                                                  int out1, int pack1) {
-  extern __shared__ double csh[];  // [d][kCP]
+  extern __shared__ __attribute__((aligned(16))) double csh[];  // [d][kCP]
   __shared__ double sh_tol;
   const int bh = blockIdx.x, job = blockIdx.y, d = C.d, tid = threadIdx.x;
   const int tr = tid >> 4, tc = tid & 15;  // 16 x 16 thread grid
@@ -712,7 +1091,7 @@ __global__ __launch_bounds__(kCholThreads) void cholesky_kernel(Ctx C, int in0, 
 // Metric mode, queries: rho = q S_k, inv = 1/|rho| (0 if rho = 0), r = rho*inv;
 // partial sums of r r^T and r per row block; inv is kept for the projection.
 __global__ __launch_bounds__(256) void qnorm_partial_kernel(Ctx C) {
-  extern __shared__ float qsh[];
+  extern __shared__ __attribute__((aligned(16))) float qsh[];
   float* Sk = qsh;                                        // [d][kDP]
   float (*X)[kDP] = (float(*)[kDP])(qsh + kMaxD * kDP);   // [kStage][kDP]
   float (*R)[kDP] = (float(*)[kDP])(qsh + (kMaxD + kStage) * kDP);
@@ -820,7 +1199,7 @@ __device__ __forceinline__ float random_coord(int bh, int side, int i, int j) {
 }
 
 __global__ __launch_bounds__(256) void project_kernel(Ctx C) {
-  extern __shared__ float psh[];
+  extern __shared__ __attribute__((aligned(16))) float psh[];
   float* T = psh;                                        // [d][kDP]
   float (*X)[kDP] = (float(*)[kDP])(psh + kMaxD * kDP);  // [kStage][kDP]
   const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH;
@@ -1422,7 +1801,7 @@ __device__ __forceinline__ float irwin_hall(uint64_t c) {
 // values (identical results), which saves a barrier per iteration.
 template <int D>
 __global__ __launch_bounds__(kBasicThreads) void basic_choose_kernel(Ctx C, LevelArgs L) {
-  extern __shared__ float bsub[];
+  extern __shared__ __attribute__((aligned(16))) float bsub[];
   __shared__ float mu[kMaxD], v[kMaxD], t[kMaxD], w[kMaxD];
   const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH, node = blockIdx.x;
   const Side& S = C.s[side];
@@ -2497,7 +2876,7 @@ __global__ __launch_bounds__(kTailThreads) void split_tail_kernel(Ctx C, int par
 // ---------------------------------------------------------------------------
 
 __global__ __launch_bounds__(128) void gather_kernel(Ctx C) {
-  extern __shared__ float gsh[];  // value tile staging [c][d]
+  extern __shared__ __attribute__((aligned(16))) float gsh[];  // value tile staging [c][d]
   const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH, a = blockIdx.x;
   const Side& S = C.s[side];
   if (a >= S.nc) return;
@@ -2545,7 +2924,7 @@ __global__ __launch_bounds__(128) void gather_kernel(Ctx C) {
 // through LDS so that the value tiles are written 16 bytes at a time.
 template <typename T>
 __global__ __launch_bounds__(256) void gather_fast_kernel(Ctx C) {
-  extern __shared__ float gfs[];
+  extern __shared__ __attribute__((aligned(16))) float gfs[];
   constexpr int EPC = 16 / sizeof(T);  // elements per 16-byte chunk
   const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH, a = blockIdx.x;
   const Side& S = C.s[side];
