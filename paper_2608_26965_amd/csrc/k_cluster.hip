@@ -3,7 +3,8 @@
 //
 // Pipeline per head, both sides batched in every launch:
 //   moments      X^T X and column sums (fp32 partials, fp64 reduction)
-//   eigh         cyclic Jacobi on d x d matrices, one workgroup per matrix
+//   eigh         Householder tridiagonal reduction, Sturm bisection and
+//                inverse iteration on d x d matrices, one workgroup each
 //   transforms   metric roots, the key-side covariance in the query metric,
 //                the normalised query representation and its covariance
 //   project      Y = X T (queries additionally scaled by 1/|q S_k|)
@@ -210,22 +211,9 @@ __global__ __launch_bounds__(256) void moments_finish_kernel(Ctx C) {
 }
 
 // ---------------------------------------------------------------------------
-// Symmetric eigensolver: parallel cyclic Jacobi, one workgroup per matrix.
-// The DM players of a round-robin tournament (rows beyond d are zero padding,
-// so any pair that touches one is an identity rotation) give DM/2 disjoint
-// pairs per step; every pair of indices meets once per sweep of DM-1 steps
-// (Golub & Van Loan, parallel Jacobi). A is stored by tournament position, so
-// a step's pairs are always (k, DM/2 + k). A step applies J^T A J block-wise:
-// the pairs cut A into (DM/2)^2 blocks of 2x2, and each thread owns the blocks
-// of one row pair and some column pairs. It derives the rotations of its row
-// and column pairs itself from the diagonal blocks, rotates its blocks from
-// the left and then from the right in registers (the arithmetic of a row pass
-// followed by a column pass), and writes them where the players move for the
-// next step; every read and write is then a contiguous row segment. The rows
-// of V^T travel with their players in the same way. Every entry has one
-// owner, so with A and V^T double-buffered a step costs a single barrier (two
-// when they are rotated in place). Output: eigenvalues in descending order and
-// the matching eigenvectors as columns.
+// Symmetric eigenproblems of the transforms (the algorithm is described at
+// eigh_kernel). Output: eigenvalues in descending order and the matching
+// eigenvectors as columns.
 // ---------------------------------------------------------------------------
 
 // One eigenproblem: A = B, A = B - m m^T, or A = S^T B S (- u u^T with

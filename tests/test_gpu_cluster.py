@@ -32,7 +32,7 @@ SPLIT_CASES = [
     ("bf16", 20000, 64, 128, "metric"),
     ("bf16", 12345, 128, 64, "metric"),
     ("bf16", 100, 64, 128, "metric"),
-    # d below the eigensolver's padded size (zero rows in the tournament)
+    # d below the eigensolver's padded size (64 or 128)
     ("f32", 2000, 40, 32, "metric"),
     ("bf16", 4000, 100, 64, "pca"),
     # queries in the centred-key metric (adaptive assignment)
