@@ -116,10 +116,17 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   const size_t nq_pad = (size_t)nqc * CQ, nk_pad = (size_t)nkc * CK;
   const size_t qrow = (size_t)bh * nq_pad + (size_t)a * CQ + 32 * w + l32;
 
+  // Queries pre-scaled by sl2 = scale * log2(e) (rounded to bf16 once), so
+  // that the logits come out in the exponent's units.
   bf16x8 qreg[KS];
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks)
-    qreg[ks] = *(const bf16x8*)(qp + qrow * D + 16 * ks + 8 * h);
+  for (int ks = 0; ks < KS; ++ks) {
+    const bf16x8 q8 = *(const bf16x8*)(qp + qrow * D + 16 * ks + 8 * h);
+    float qf[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) qf[i] = (float)q8[i] * sl2;
+    qreg[ks] = pack8(qf);
+  }
   // Retire the query loads here (a wait the compiler sees), so that no
   // compiler-inserted vmcnt wait lands inside the loop, where it would also
   // wait for the in-flight copy of the next tile.
@@ -192,8 +199,10 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[dt][r] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
-  const float isl2 = 1.f / sl2;
+  // m_run: running maximum of the scaled logits (log2 units); m_ref: the value
+  // the current stage's accumulators start from (-m_ref), so that they hold
+  // logit - m_ref and the exponentials need no subtraction.
+  float m_run = -INFINITY, m_ref = 0.f, l_run = 0.f;
   f32x16 sacc[MT];   // logits of the current stage
   bf16x8 pb[MT][2];  // its probabilities (bf16), the value product's operand
 
@@ -202,7 +211,7 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[mt][r] = 0.f;
+      for (int r = 0; r < 16; ++r) sacc[mt][r] = -m_ref;
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) {
         const bf16x8 av = *(const bf16x8*)(ks + 32 * mt * KROW + koff[kk]);
@@ -224,15 +233,29 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
           if (32 * mt + 16 * (r >> 3) + (r & 7) >= ch) sacc[mt][r] = -INFINITY;
     }
   };
-  // probabilities of accumulator group (mt, s2) against the running maximum,
-  // added to the lane's row sum
+  // probabilities of accumulator group (mt, s2) against the running maximum
+  // (the accumulators already hold logit - m_ref), added to the lane's row sum
   auto exp_group = [&](int mt, int s2, float& ls) __attribute__((always_inline)) {
     float pv[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
-      pv[j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[mt][8 * s2 + j], sl2, -m_run));
+    for (int j = 0; j < 8; ++j) pv[j] = __builtin_amdgcn_exp2f(sacc[mt][8 * s2 + j]);
     pb[mt][s2] = pack8(pv);
     ls = sum8(pb[mt][s2], ls);
+  };
+  // the same against another reference: exp2(acc + off)
+  auto exps_off = [&](float off) __attribute__((always_inline)) {
+    float ls = 0.f;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        float pv[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) pv[j] = __builtin_amdgcn_exp2f(sacc[mt][8 * s2 + j] + off);
+        pb[mt][s2] = pack8(pv);
+        ls = sum8(pb[mt][s2], ls);
+      }
+    return ls;
   };
   auto exps = [&]() __attribute__((always_inline)) {
     float ls = 0.f;
@@ -275,30 +298,31 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   // Exponentials are taken against the running maximum without first
   // forming the stage's maximum. Only a stage whose logits pass the running
   // maximum by so much that a lane's row sum exceeds 2^40 is redone against
-  // its own maximum: always the first stage (m_run = -inf, so the sums are
-  // infinite), later ones only on a jump of about 2^33 in a probability.
-  // Below that, large exponentials cost no accuracy (fp32 and bf16 keep
-  // their relative precision at any scale). The output accumulated so far
-  // (all earlier stages) is rescaled to the new maximum.
+  // its own maximum: always the first stage (no maximum yet; its
+  // accumulators start from 0), later ones only on a jump of about 2^33 in a
+  // probability. Below that, large exponentials cost no accuracy (fp32 and
+  // bf16 keep their relative precision at any scale). The output accumulated
+  // so far (all earlier stages) is rescaled to the new maximum.
   auto settle = [&](float ls) __attribute__((always_inline)) {
-    if (__builtin_amdgcn_ballot_w64(!(ls <= 0x1p40f))) {
+    if (__builtin_amdgcn_ballot_w64(!(ls <= 0x1p40f) || m_run == -INFINITY)) {
       float mx = -INFINITY;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[mt][r]);
-      mx = fmaxf(mx, wave_xor32(mx)) * sl2;
-      const float m_new = fmaxf(m_run, mx);
+      mx = fmaxf(mx, wave_xor32(mx));
+      const float m_new = fmaxf(m_run, m_ref + mx);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
       l_run *= alpha;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
+      ls = exps_off(m_ref - m_new);
       m_run = m_new;
-      ls = exps();
     }
     l_run += ls;
+    m_ref = m_run;
   };
   auto sync_stage = [&]() __attribute__((always_inline)) {
     wait_vmcnt<0>();
@@ -362,7 +386,7 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
       wait_lgkm();
       raw_barrier();  // bias row final
       logits(sb ? kbuf1 : kbuf0);
-      // logit + log2|b| / sl2, so that the exponent is sl2 q.kbar + log2|b| - m.
+      // logit + log2|b|, so that the exponent is sl2 q.kbar + log2|b| - m.
       // The bias of accumulator r of row tile mt is that of key acc_key(mt, r, h):
       // two runs of eight consecutive entries.
 #pragma unroll
@@ -374,7 +398,7 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
           const float bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
 #pragma unroll
           for (int j = 0; j < 8; ++j)
-            sacc[mt][8 * hh + j] = __builtin_fmaf(bv[j], isl2, sacc[mt][8 * hh + j]);
+            sacc[mt][8 * hh + j] += bv[j];
         }
       settle(exps());
       pv(vb ? vbuf1 : vbuf0);
