@@ -2734,10 +2734,18 @@ __global__ __launch_bounds__(kTailThreads) void split_tail_kernel(Ctx C, int par
         gsl[u] = lo;
         grow[u] = o < size && act_of[lo] >= 0 ? cur[o] : -1;
       }
+      // the chosen coordinate, from the coordinate-major copy when it holds
+      // it (the nodes of a head run together, so they share its lines)
       float gv[PT];
 #pragma unroll
-      for (int u = 0; u < PT; ++u)
-        gv[u] = grow[u] >= 0 ? Y[(size_t)grow[u] * d + sub_js[gsl[u]]] : 0.f;
+      for (int u = 0; u < PT; ++u) {
+        gv[u] = 0.f;
+        if (grow[u] >= 0) {
+          const int js = sub_js[gsl[u]];
+          gv[u] = S.ycol && js < kColCopy ? S.ycol[((size_t)bh * kColCopy + js) * S.n + grow[u]]
+                                          : Y[(size_t)grow[u] * d + js];
+        }
+      }
 #pragma unroll
       for (int u = 0; u < PT; ++u) {
         const int o = threadIdx.x + kTailThreads * u;
