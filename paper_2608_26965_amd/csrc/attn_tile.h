@@ -102,13 +102,10 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 // operand reads of the MFMA kernels (32 rows in the K-row order of kswz, or 32
 // consecutive rows) hit distinct banks whether the hardware serves a
 // ds_read_b128 in groups of 8 lanes over 128 bytes or of 16 lanes over 256
-// bytes. Row r stores its logical chunk lc at chunk lc ^ swz_key(r). Rows of
-// 64 bytes (four chunks): rows r and r + 4 share banks, so the key is
-// (r / 4) % 4, which spreads 16 consecutive rows over all 64 banks.
+// bytes. Row r stores its logical chunk lc at chunk lc ^ swz_key(r).
 template <int ROWBYTES>
 __device__ __forceinline__ int swz_key(int r) {
-  static_assert(ROWBYTES == 64 || ROWBYTES == 128 || ROWBYTES == 256, "row width");
-  if constexpr (ROWBYTES == 64) return (r >> 2) & 3;
+  static_assert(ROWBYTES == 128 || ROWBYTES == 256, "row width");
   constexpr uint64_t tbl = ROWBYTES == 128 ? 0x1706352453427160ull : 0xba987654fedc3210ull;
   return (int)((tbl >> ((r & 15) * 4)) & 15);
 }

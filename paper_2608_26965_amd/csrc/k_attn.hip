@@ -36,12 +36,10 @@ __device__ __forceinline__ int head_sync_item(int wg, int nqc, int total) {
 // stages then take 16 KB (d = 64) or 32 KB (d = 128) per buffer pair instead
 // of twice that, and the logits of a stage need half the registers: at d = 64
 // with query clusters of 128 three workgroups share a CU (three waves per
-// SIMD) instead of two, and at d = 128 two instead of one. Query clusters of
-// 64 at d = 128 (two wavefronts per workgroup) stage 32 keys: 32 KB per
-// workgroup, so four share a CU (two waves per SIMD instead of one).
+// SIMD) instead of two, and at d = 128 two instead of one.
 template <int D, int CQ, int CK>
 constexpr int attn_stage_keys() {
-  return D == 128 && CQ == 64 ? 32 : (CK == 128 ? 64 : CK);
+  return CK == 128 ? 64 : CK;
 }
 
 // Waves per SIMD the bf16 kernel is compiled for (the second launch bound, a
