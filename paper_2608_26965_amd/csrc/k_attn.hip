@@ -78,6 +78,14 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
     FusedArgs fa = FusedArgs{}) {
   constexpr int NW = CQ / 32;
   constexpr int HK = attn_stage_keys<D, CQ, CK>();  // keys per stage
+  // Where two or more waves share a SIMD, VALU instructions are what the loop
+  // is short of: the logits' starting value -m_ref then sits in 16 registers
+  // of its own, refreshed only when the running maximum moves (no per-stage
+  // register fill), and every accumulator group of a stage keeps its own
+  // partial row sum (four short dependency chains instead of one long one).
+  // With one wave per SIMD (d = 128, query clusters of 64) the extra
+  // registers cost more than they save, and the stage-local forms are kept.
+  constexpr bool LEAN = attn_waves_per_simd<D, CQ, CK>() > 1;
   constexpr int SUB = CK / HK;                      // stages per key cluster
   constexpr int MT = HK / 32;
   constexpr int KS = D / 16;
@@ -201,6 +209,9 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   // the current stage's accumulators start from (-m_ref), so that they hold
   // logit - m_ref and the exponentials need no subtraction.
   float m_run = -INFINITY, m_ref = 0.f, l_run = 0.f;
+  f32x16 sinit;  // LEAN: -m_ref in every entry, the first logit product's addend
+#pragma unroll
+  for (int r = 0; r < 16; ++r) sinit[r] = -m_ref;
   f32x16 sacc[MT];   // logits of the current stage
   bf16x8 pb[MT][2];  // its probabilities (bf16), the value product's operand
 
@@ -208,12 +219,15 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   auto logits = [&](const char* ks) __attribute__((always_inline)) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
+      if constexpr (!LEAN) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[mt][r] = -m_ref;
+        for (int r = 0; r < 16; ++r) sacc[mt][r] = -m_ref;
+      }
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) {
         const bf16x8 av = *(const bf16x8*)(ks + 32 * mt * KROW + koff[kk]);
-        sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qreg[kk], sacc[mt], 0, 0, 0);
+        sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qreg[kk],
+                                                           LEAN && kk == 0 ? sinit : sacc[mt], 0, 0, 0);
       }
     }
   };
@@ -255,20 +269,29 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
       }
     return ls;
   };
+  // the stage's row sum from its partials (LEAN: one per accumulator group)
+  auto sum_parts = [&](const float* part) __attribute__((always_inline)) {
+    float ls = part[0];
+    if constexpr (LEAN) {
+#pragma unroll
+      for (int i = 1; i < 2 * MT; ++i) ls += part[i];
+    }
+    return ls;
+  };
   auto exps = [&]() __attribute__((always_inline)) {
-    float ls = 0.f;
+    float part[2 * MT] = {};
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) exp_group(mt, s2, ls);
-    return ls;
+      for (int s2 = 0; s2 < 2; ++s2) exp_group(mt, s2, part[LEAN ? 2 * mt + s2 : 0]);
+    return sum_parts(part);
   };
   // O^T += V^T P^T for the previous stage's probabilities, each group's two
   // (DT) products issued right before that group's probabilities of this
   // stage overwrite them, so the matrix cores run while the exponentials of
   // the next group are formed
   auto pv_exps = [&](const char* vs) __attribute__((always_inline)) {
-    float ls = 0.f;
+    float part[2 * MT] = {};
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -278,9 +301,9 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
           const bf16x8 av = *(const bf16x8*)(vs + 32 * dt * VROW + voff[mt][s2]);
           oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[mt][s2], oacc[dt], 0, 0, 0);
         }
-        exp_group(mt, s2, ls);
+        exp_group(mt, s2, part[LEAN ? 2 * mt + s2 : 0]);
       }
-    return ls;
+    return sum_parts(part);
   };
   auto pv = [&](const char* vs) __attribute__((always_inline)) {
 #pragma unroll
@@ -318,6 +341,10 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
         for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
       ls = exps_off(m_ref - m_new);
       m_run = m_new;
+      if constexpr (LEAN) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sinit[r] = -m_new;
+      }
     }
     l_run += ls;
     m_ref = m_run;
