@@ -100,6 +100,7 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
   // fused: the query cluster's selection bitmap and the two stages' bias rows
   __shared__ uint32_t selmask[FUSED ? kMaskWords : 1];
+  __shared__ int redo;  // some wavefront's fast pass overflowed
   __shared__ __attribute__((aligned(16))) float cbias[2][FUSED ? HK : 4];
   constexpr int SUBC = kCompTile / HK;                     // stages per centroid tile
   constexpr int CTK = kCompTile * KROW, CTV = D * 2 * kCompTile;
@@ -138,6 +139,7 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   // wait for the in-flight copy of the next tile.
   __builtin_amdgcn_s_waitcnt(kVmcnt0);
 
+  if (tid == 0) redo = 0;  // ordered before any write by the first stage's barrier
   const int32_t* lst = lists + ((size_t)bh * nqc + a) * k;
   const int32_t* cnth = count_k + (size_t)bh * nkc;
   // this query cluster's list length (uniform; clamped for memory safety)
@@ -201,19 +203,30 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
     for (int s2 = 0; s2 < 2; ++s2) voff[mt][s2] = swz_off<VROW>(l32, 4 * mt + 2 * s2 + h);
 
   f32x16 oacc[DT];
-#pragma unroll
-  for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) oacc[dt][r] = 0.f;
   // m_run: running maximum of the scaled logits (log2 units); m_ref: the value
   // the current stage's accumulators start from (-m_ref), so that they hold
   // logit - m_ref and the exponentials need no subtraction.
-  float m_run = -INFINITY, m_ref = 0.f, l_run = 0.f;
+  float m_run = -INFINITY, m_ref = 0.f;
   f32x16 sinit;  // LEAN: -m_ref in every entry, the first logit product's addend
 #pragma unroll
   for (int r = 0; r < 16; ++r) sinit[r] = -m_ref;
   f32x16 sacc[MT];   // logits of the current stage
   bf16x8 pb[MT][2];  // its probabilities (bf16), the value product's operand
+  // Row sums on the matrix cores instead of the VALU: a 16x16x32 product of
+  // a 0/1 selector R with a probability group (the group's B operand: lane l
+  // holds its 8 keys of query l % 32, in k block l / 16) gives in row 0,
+  // column n the group's sum for query n (k blocks 0 and 2: lanes n, n + 32)
+  // and in row 1 that for query n + 16 (blocks 1 and 3); the other rows are 0.
+  // Lane n < 16 thus holds the sums of queries n and n + 16 in entries 0 and 1
+  // of the product (lane l holds rows 4 (l / 16) .. + 3 of column l % 16).
+  bf16x8 rsel;  // lane l holds R[l % 16][k block l / 16]
+  {
+    const __bf16 one = (__bf16)((lane & 15) == ((lane >> 4) & 1) ? 1.f : 0.f);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) rsel[i] = one;
+  }
+  f32x4 lacc;  // running row sums in that layout
+  f32x4 ssum;  // the row sums of a stage that is still to be settled
 
   // S^T = K Q^T for the stage in key buffer ks
   auto logits = [&](const char* ks) __attribute__((always_inline)) {
@@ -245,53 +258,30 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
           if (32 * mt + 16 * (r >> 3) + (r & 7) >= ch) sacc[mt][r] = -INFINITY;
     }
   };
-  // probabilities of accumulator group (mt, s2) against the running maximum
-  // (the accumulators already hold logit - m_ref), added to the lane's row sum
-  auto exp_group = [&](int mt, int s2, float& ls) __attribute__((always_inline)) {
+  // probabilities of accumulator group (mt, s2) against m_ref (the
+  // accumulators already hold logit - m_ref), or with OFF against m_ref - off,
+  // with their row sums added to rs
+  auto exp_group = [&](auto off_tag, int mt, int s2, float off, f32x4& rs)
+                       __attribute__((always_inline)) {
     float pv[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) pv[j] = __builtin_amdgcn_exp2f(sacc[mt][8 * s2 + j]);
+    for (int j = 0; j < 8; ++j)
+      pv[j] = __builtin_amdgcn_exp2f(decltype(off_tag)::value ? sacc[mt][8 * s2 + j] + off
+                                                              : sacc[mt][8 * s2 + j]);
     pb[mt][s2] = pack8(pv);
-    ls = sum8(pb[mt][s2], ls);
+    rs = __builtin_amdgcn_mfma_f32_16x16x32_bf16(rsel, pb[mt][s2], rs, 0, 0, 0);
   };
-  // the same against another reference: exp2(acc + off)
-  auto exps_off = [&](float off) __attribute__((always_inline)) {
-    float ls = 0.f;
+  auto exps = [&](auto off_tag, float off, f32x4& rs) __attribute__((always_inline)) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) {
-        float pv[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) pv[j] = __builtin_amdgcn_exp2f(sacc[mt][8 * s2 + j] + off);
-        pb[mt][s2] = pack8(pv);
-        ls = sum8(pb[mt][s2], ls);
-      }
-    return ls;
-  };
-  // the stage's row sum from its partials (LEAN: one per accumulator group)
-  auto sum_parts = [&](const float* part) __attribute__((always_inline)) {
-    float ls = part[0];
-    if constexpr (LEAN) {
-#pragma unroll
-      for (int i = 1; i < 2 * MT; ++i) ls += part[i];
-    }
-    return ls;
-  };
-  auto exps = [&]() __attribute__((always_inline)) {
-    float part[2 * MT] = {};
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) exp_group(mt, s2, part[LEAN ? 2 * mt + s2 : 0]);
-    return sum_parts(part);
+      for (int s2 = 0; s2 < 2; ++s2) exp_group(off_tag, mt, s2, off, rs);
   };
   // O^T += V^T P^T for the previous stage's probabilities, each group's two
   // (DT) products issued right before that group's probabilities of this
   // stage overwrite them, so the matrix cores run while the exponentials of
   // the next group are formed
-  auto pv_exps = [&](const char* vs) __attribute__((always_inline)) {
-    float part[2 * MT] = {};
+  auto pv_exps = [&](const char* vs, f32x4& rs) __attribute__((always_inline)) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -301,9 +291,8 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
           const bf16x8 av = *(const bf16x8*)(vs + 32 * dt * VROW + voff[mt][s2]);
           oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[mt][s2], oacc[dt], 0, 0, 0);
         }
-        exp_group(mt, s2, part[LEAN ? 2 * mt + s2 : 0]);
+        exp_group(std::false_type{}, mt, s2, 0.f, rs);
       }
-    return sum_parts(part);
   };
   auto pv = [&](const char* vs) __attribute__((always_inline)) {
 #pragma unroll
@@ -316,16 +305,15 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
           oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[mt][s2], oacc[dt], 0, 0, 0);
         }
   };
-  // Exponentials are taken against the running maximum without first
-  // forming the stage's maximum. Only a stage whose logits pass the running
-  // maximum by so much that a lane's row sum exceeds 2^40 is redone against
-  // its own maximum: always the first stage (no maximum yet; its
-  // accumulators start from 0), later ones only on a jump of about 2^33 in a
-  // probability. Below that, large exponentials cost no accuracy (fp32 and
-  // bf16 keep their relative precision at any scale). The output accumulated
-  // so far (all earlier stages) is rescaled to the new maximum.
-  auto settle = [&](float ls) __attribute__((always_inline)) {
-    if (__builtin_amdgcn_ballot_w64(!(ls <= 0x1p40f) || m_run == -INFINITY)) {
+  // Settle a stage whose exponentials were taken against m_ref and whose row
+  // sums are in ssum: where this is the first stage (no maximum yet; its
+  // accumulators start from 0), or a row sum of the stage exceeds 2^40 (a jump
+  // of about 2^34 in a probability), the stage is redone against its own
+  // maximum and the output and row sums accumulated so far are rescaled to
+  // it. Large exponentials below that cost no accuracy (fp32 and bf16 keep
+  // their relative precision at any scale).
+  auto settle = [&]() __attribute__((always_inline)) {
+    if (__builtin_amdgcn_ballot_w64(!(fmaxf(ssum[0], ssum[1]) <= 0x1p40f) || m_run == -INFINITY)) {
       float mx = -INFINITY;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
@@ -334,19 +322,23 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
       mx = fmaxf(mx, wave_xor32(mx));
       const float m_new = fmaxf(m_run, m_ref + mx);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      l_run *= alpha;
+      // lane n < 16 holds the sums of queries n and n + 16
+      lacc[0] *= alpha;
+      lacc[1] *= __shfl_xor(alpha, 16, 64);
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
-      ls = exps_off(m_ref - m_new);
+      ssum = f32x4{0.f, 0.f, 0.f, 0.f};
+      exps(std::true_type{}, m_ref - m_new, ssum);
       m_run = m_new;
       if constexpr (LEAN) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) sinit[r] = -m_new;
       }
     }
-    l_run += ls;
+    lacc[0] += ssum[0];
+    lacc[1] += ssum[1];
     m_ref = m_run;
   };
   auto sync_stage = [&]() __attribute__((always_inline)) {
@@ -355,6 +347,15 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
     raw_barrier();
   };
 
+  // All stages of the query cluster: the key stages, then (fused) the
+  // centroid stages. The first stage sets the reference m_ref (its maximum).
+  // In the fast pass (SAFE false) every later stage is taken against that
+  // reference as it stands, with no check: probabilities may exceed 1, which
+  // costs no accuracy while nothing overflows, and whether anything did is
+  // checked once at the end. The safe pass settles every stage as above; it
+  // runs only for a query cluster whose fast pass overflowed (a logit jump of
+  // about 2^7 or more in log2 units over the first stage's maximum).
+  //
   // Key stages, software-pipelined one stage deep. Stage g's keys sit in key
   // buffer g % 2 and its values in value buffer g % 2. At iteration g, after
   // the one barrier (every wavefront is past iteration g-1, so key buffer
@@ -368,69 +369,114 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   const char* kbuf1 = smem + KBYTES;
   const char* vbuf0 = smem + 2 * KBYTES;
   const char* vbuf1 = smem + 2 * KBYTES + VBYTES;
-  issue_k(0, 0);
-  {
-    sync_stage();
-    if (1 < ng) issue_k(1, 1);
-    issue_v(0, 0);
-    logits(kbuf0);
-    mask_pad(cnth[tile_id(0)]);
-    settle(exps());
-  }
-  auto step = [&](auto par_tag, int g) __attribute__((always_inline)) {
-    constexpr int P = decltype(par_tag)::value;  // g % 2
-    sync_stage();
-    if (g + 1 < ng) issue_k(g + 1, P ^ 1);
-    issue_v(g, P);
-    logits(P ? kbuf1 : kbuf0);
-    mask_pad(cnth[tile_id(g / SUB)] - (g % SUB) * HK);
-    settle(pv_exps(P ? vbuf0 : vbuf1));
-  };
-  for (int g = 1; g < ng; g += 2) {
-    step(std::integral_constant<int, 1>{}, g);
-    if (g + 1 < ng) step(std::integral_constant<int, 0>{}, g + 1);
-  }
-  // the last key stage's value product; the first centroid stage's copies go
-  // to the free buffers (both key buffers, value buffer ng % 2) meanwhile
-  sync_stage();
-  if (FUSED && nc) issue_c(0, 0, ng & 1, 0);
-  pv((ng & 1) ? vbuf0 : vbuf1);
-  if constexpr (FUSED) {
-    // Centroid stages (compensation), after the keys and not pipelined:
-    // centroid stage c sits in key buffer c % 2, value buffer (ng + c) % 2
-    // and bias row c % 2. The selected clusters are covered by the sparse
-    // part: their bias is set to -inf once the row has landed.
-    for (int c = 0; c < nc; ++c) {
-      const int sb = c & 1, vb = (ng + c) & 1;
+  auto run = [&](auto safe_tag) __attribute__((always_inline)) {
+    constexpr bool SAFE = decltype(safe_tag)::value;
+    m_run = -INFINITY;
+    m_ref = 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sinit[r] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[dt][r] = 0.f;
+    lacc = f32x4{0.f, 0.f, 0.f, 0.f};
+    // a stage's exponentials and their row sums: settled (safe pass) or
+    // added to the running sums as they are (fast pass)
+    auto stage_exps = [&](auto with_pv, const char* vs) __attribute__((always_inline)) {
+      if constexpr (SAFE) ssum = f32x4{0.f, 0.f, 0.f, 0.f};
+      f32x4& rs = SAFE ? ssum : lacc;
+      if constexpr (decltype(with_pv)::value)
+        pv_exps(vs, rs);
+      else
+        exps(std::false_type{}, 0.f, rs);
+      if constexpr (SAFE) settle();
+    };
+    issue_k(0, 0);
+    {
       sync_stage();
-      if (c + 1 < nc) issue_c(c + 1, sb ^ 1, vb ^ 1, sb ^ 1);
-      if (tid < HK) {
-        const int b = (c / SUBC) * kCompTile + (c % SUBC) * HK + tid;
-        if (b < nkc && ((selmask[b >> 5] >> (b & 31)) & 1u)) cbias[sb][tid] = -INFINITY;
-      }
-      wait_lgkm();
-      raw_barrier();  // bias row final
-      logits(sb ? kbuf1 : kbuf0);
-      // logit + log2|b|, so that the exponent is sl2 q.kbar + log2|b| - m.
-      // The bias of accumulator r of row tile mt is that of key acc_key(mt, r, h):
-      // two runs of eight consecutive entries.
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const float4 b0 = *(const float4*)&cbias[sb][32 * mt + 16 * hh + 8 * h];
-          const float4 b1 = *(const float4*)&cbias[sb][32 * mt + 16 * hh + 8 * h + 4];
-          const float bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
-#pragma unroll
-          for (int j = 0; j < 8; ++j)
-            sacc[mt][8 * hh + j] += bv[j];
+      if (1 < ng) issue_k(1, 1);
+      issue_v(0, 0);
+      logits(kbuf0);
+      mask_pad(cnth[tile_id(0)]);
+      ssum = f32x4{0.f, 0.f, 0.f, 0.f};
+      exps(std::false_type{}, 0.f, ssum);
+      settle();
+    }
+    auto step = [&](auto par_tag, int g) __attribute__((always_inline)) {
+      constexpr int P = decltype(par_tag)::value;  // g % 2
+      sync_stage();
+      if (g + 1 < ng) issue_k(g + 1, P ^ 1);
+      issue_v(g, P);
+      logits(P ? kbuf1 : kbuf0);
+      mask_pad(cnth[tile_id(g / SUB)] - (g % SUB) * HK);
+      stage_exps(std::true_type{}, P ? vbuf0 : vbuf1);
+    };
+    for (int g = 1; g < ng; g += 2) {
+      step(std::integral_constant<int, 1>{}, g);
+      if (g + 1 < ng) step(std::integral_constant<int, 0>{}, g + 1);
+    }
+    // the last key stage's value product; the first centroid stage's copies go
+    // to the free buffers (both key buffers, value buffer ng % 2) meanwhile
+    sync_stage();
+    if (FUSED && nc) issue_c(0, 0, ng & 1, 0);
+    pv((ng & 1) ? vbuf0 : vbuf1);
+    if constexpr (FUSED) {
+      // Centroid stages (compensation), after the keys and not pipelined:
+      // centroid stage c sits in key buffer c % 2, value buffer (ng + c) % 2
+      // and bias row c % 2. The selected clusters are covered by the sparse
+      // part: their bias is set to -inf once the row has landed.
+      for (int c = 0; c < nc; ++c) {
+        const int sb = c & 1, vb = (ng + c) & 1;
+        sync_stage();
+        if (c + 1 < nc) issue_c(c + 1, sb ^ 1, vb ^ 1, sb ^ 1);
+        if (tid < HK) {
+          const int b = (c / SUBC) * kCompTile + (c % SUBC) * HK + tid;
+          if (b < nkc && ((selmask[b >> 5] >> (b & 31)) & 1u)) cbias[sb][tid] = -INFINITY;
         }
-      settle(exps());
-      pv(vb ? vbuf1 : vbuf0);
+        wait_lgkm();
+        raw_barrier();  // bias row final
+        logits(sb ? kbuf1 : kbuf0);
+        // logit + log2|b|, so that the exponent is sl2 q.kbar + log2|b| - m.
+        // The bias of accumulator r of row tile mt is that of key acc_key(mt, r, h):
+        // two runs of eight consecutive entries.
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const float4 b0 = *(const float4*)&cbias[sb][32 * mt + 16 * hh + 8 * h];
+            const float4 b1 = *(const float4*)&cbias[sb][32 * mt + 16 * hh + 8 * h + 4];
+            const float bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+              sacc[mt][8 * hh + j] += bv[j];
+          }
+        stage_exps(std::false_type{}, nullptr);
+        pv(vb ? vbuf1 : vbuf0);
+      }
+    }
+  };
+  // the row sum of this lane's query q = lane % 32: lane q % 16, entry q / 16
+  auto row_total = [&]() __attribute__((always_inline)) {
+    const float l_lo = __shfl(lacc[0], lane & 15, 64), l_hi = __shfl(lacc[1], lane & 15, 64);
+    return (lane & 16) ? l_hi : l_lo;
+  };
+  run(std::false_type{});
+  float l_tot = row_total();
+  {
+    // Did the fast pass overflow? Its row sums are at least 1 (the first
+    // stage's maximum) unless something became inf or NaN.
+    bool ok = l_tot <= 0x1p126f;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) ok = ok && fabsf(oacc[dt][r]) <= 0x1.fffffep127f;
+    if (__builtin_amdgcn_ballot_w64(!ok) && lane == 0) redo = 1;
+    __syncthreads();  // also: every wavefront is done with the stage buffers
+    if (redo) {
+      run(std::true_type{});
+      l_tot = row_total();
     }
   }
-
-  const float l_tot = l_run + wave_xor32(l_run);
   const float inv = 1.f / l_tot;
   if constexpr (FUSED) {
     // merged rows to their original positions

@@ -71,6 +71,64 @@ def test_block_sparse_attention_parity(dt, d, cq, ck, n, k):
     G.flush(f"  max abs err {worst:.3g}")
 
 
+JUMP = [
+    # d, cq, ck, n, k
+    (64, 128, 128, 1000, 3),
+    (128, 64, 64, 650, 4),
+    (64, 64, 128, 900, 3),
+    (128, 128, 128, 1111, 2),
+]
+
+
+@pytest.mark.parametrize("d,cq,ck,n,k", JUMP)
+def test_logit_jump_after_first_stage(d, cq, ck, n, k):
+    """bf16 attention where some logits exceed the first stage's maximum by
+    far more than the exponent range: every query has 3 on axis 0 and the
+    keys of the last key cluster 400 there, so that cluster's logits lie
+    about 2^7.2 to 2^7.6 (log2 units) above the others'. Every list holds that
+    cluster and never first (lists are in ascending order), so exponentials
+    taken against the first stage's maximum overflow and the kernel has to
+    settle stage by stage instead. The lse carries the rounding of the
+    pre-scaled queries (bf16, unit roundoff 2^-8), at most 2^-8 of
+    tau sum |q_i k_i| (a common shift of the large logits that the outputs do
+    not see)."""
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    from synth import bf16_round
+    G.flush(f"logit jump case d={d} cq={cq} ck={ck} n={n} k={k}")
+    Q, K, V, perm_q, perm_k, lists, k = _setup("bf16", d, cq, ck, n, k, seed=11)
+    H = Q.shape[0]
+    nkc = -(-n // ck)
+    Q[:, :, 0] = 3.0
+    for h in range(H):
+        K[h, perm_k[h][(nkc - 1) * ck:], 0] = 400.0
+        for a in range(lists.shape[1]):
+            if lists[h, a, -1] != nkc - 1:
+                lists[h, a, -1] = nkc - 1
+    Q, K = bf16_round(Q.astype(np.float32)).astype(np.float64), bf16_round(K.astype(np.float32)).astype(np.float64)
+    p = ca.Problem(1, H, n, n, d, cq, ck, torch.bfloat16)
+    tq = G.permuted_rows(Q, perm_q, cq, torch.bfloat16)
+    tk = G.permuted_rows(K, perm_k, ck, torch.bfloat16)
+    tv = G.value_tiles(V, perm_k, ck, torch.bfloat16)
+    cnt = G.dev(np.stack([G.counts(n, ck)] * H), torch.int32)
+    op, lse = ca.block_sparse_attn(p, tq, tk, tv, cnt, G.dev(lists, torch.int32), k)
+    torch.cuda.synchronize()
+    op, lse = G.host(op), G.host(lse)
+    tau = 1 / math.sqrt(d)
+    for h in range(H):
+        o, l = ref.sparse_attention(Q[h], K[h], V[h], perm_q[h], G.counts(n, cq), perm_k[h],
+                                    G.counts(n, ck), lists[h], tau)
+        got, want = op[h, :n], o[perm_q[h]]
+        assert np.isfinite(got).all() and np.isfinite(lse[h, :n]).all(), h
+        err = np.abs(got - want).max()
+        assert err <= G.TOL["bf16"], (h, err)
+        slack = 2.0 ** -8 * tau * (np.abs(Q[h]) @ np.abs(K[h]).T).max(axis=1)
+        lerr = np.abs(lse[h, :n] - l[perm_q[h]]) - slack[perm_q[h]]
+        assert lerr.max() <= 1e-3 * max(1.0, np.abs(l).max()), lerr.max()
+        G.flush(f"  head {h}: max abs err {err:.3g}")
+
+
 @pytest.mark.parametrize("dt,d,cq,ck,n,k", CASES)
 @pytest.mark.parametrize("enable", [True, False])
 def test_compensation_parity(dt, d, cq, ck, n, k, enable):

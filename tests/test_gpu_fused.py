@@ -69,6 +69,32 @@ def test_fused_matches_separate(d, cq, ck, n, keep):
     _compare(_fused(p, r, lists, k, False), _separate(p, r, lists, k, False), "no compensation")
 
 
+@pytest.mark.parametrize("d,cq,ck,n", [(64, 128, 128, 3000), (128, 64, 64, 2600),
+                                        (128, 128, 128, 4100)])
+def test_fused_logit_jump(d, cq, ck, n):
+    """Logits far above the first stage's maximum (queries with 3 on axis 0,
+    3% of the keys with 400 there): the one-pass call, whose exponentials
+    against the first stage's maximum overflow for many query clusters, must
+    still agree with the separate calls."""
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    G.flush(f"fused logit jump d={d} cq={cq} ck={ck} n={n}")
+    H = 2
+    g = torch.Generator(device="cpu").manual_seed(d + n)
+    q, k, v = (torch.randn((1, H, n, d), generator=g) for _ in range(3))
+    q[..., 0] = 3.0
+    out = torch.rand((1, H, n), generator=g) < 0.03
+    k[..., 0] = torch.where(out, torch.full_like(k[..., 0], 400.0), k[..., 0])
+    q, k, v = (t.to("cuda").to(torch.bfloat16) for t in (q, k, v))
+    p = ca.Problem(1, H, n, n, d, cq, ck, torch.bfloat16, "metric")
+    r = ca.cluster(p, q, k, v)
+    kk = ca.keep_to_k(0.2, p.nkc)
+    lists, _ = ca.select(p, r["cent_q"], r["cent_k"], kk)
+    _compare(_fused(p, r, lists, kk, True), _separate(p, r, lists, kk, True), "compensated")
+    _compare(_fused(p, r, lists, kk, False), _separate(p, r, lists, kk, False), "no compensation")
+
+
 def test_fused_bnhd_layout_and_all_kept():
     import paper_2608_26965_amd as ca
     from tests import gpu_util as G
