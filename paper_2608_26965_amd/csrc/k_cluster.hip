@@ -2620,7 +2620,7 @@ __global__ __launch_bounds__(256) void split_scatter_kernel(Ctx C, LevelArgs L) 
 // workgroup: per level every active sub-node picks its coordinate (one
 // wavefront each), keys are gathered, a four-pass 8-bit radix select runs on
 // per-sub-node LDS histograms, and a block-wide scan partitions stably.
-constexpr int kTailThreads = 1024;
+constexpr int kTailThreads = 512;
 constexpr int kMaxSub = 32;
 
 __device__ __forceinline__ int scan_tail(int x, int* wsum) {
@@ -2641,7 +2641,7 @@ __device__ __forceinline__ int scan_tail(int x, int* wsum) {
   return base + v - x;
 }
 
-__global__ __launch_bounds__(kTailThreads) void split_tail_kernel(Ctx C, int parity0, int parity1) {
+__global__ __launch_bounds__(kTailThreads, 4) void split_tail_kernel(Ctx C, int parity0, int parity1) {
   __shared__ int32_t ia[kTail], ib[kTail];
   __shared__ uint32_t keys[kTail];
   __shared__ int scan[kTail + 1];
@@ -2706,7 +2706,7 @@ __global__ __launch_bounds__(kTailThreads) void split_tail_kernel(Ctx C, int par
     // coordinate choice: one wavefront per active sub-node
     for (int a = w; a < nact; a += kTailThreads / 64) {
       const int sl = act_list[a];
-      const int js = choose_coordinate<32>(Y, d, cur, false, sub_start[sl], sub_size[sl], lane);
+      const int js = choose_coordinate<64>(Y, d, cur, false, sub_start[sl], sub_size[sl], lane);
       if (lane == 0) {
         sub_js[sl] = js;
         sub_thr[sl] = 0;
