@@ -2249,7 +2249,7 @@ __global__ __launch_bounds__(256) void split_keys_kernel(Ctx C, LevelArgs L) {
 #pragma unroll
     for (int u = 0; u < kPer; ++u) kv[u] = ordered_bits(Y[(size_t)rows[u] * C.d + js]);
   }
-  if constexpr (BD >= 0) {
+  {
     if (size <= kChunk) {
       // The whole node is in this block: exact select of the rank-th key here
       // (four 8-bit digits, high first), and no histogram for the select pass.
