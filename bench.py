@@ -43,7 +43,7 @@ PEAK_HBM_GBS = 8000.0
 # plain-copy calibration (FETCH_SIZE x 2, WRITE_SIZE x 1; the traffic summaries
 # under profiles/ give the commands), valid for the kernel sources with the
 # given fingerprint only (else reported as null).
-ATTN_TRAFFIC = {"fingerprint": "473412d70f8cc513", "bytes": 8.4807e10}
+ATTN_TRAFFIC = {"fingerprint": "6a85940ad400d117", "bytes": 8.4807e10}
 CLUSTER_TRAFFIC = {"fingerprint": "68b04a16e87bc068", "bytes": 1.8547e10}
 
 

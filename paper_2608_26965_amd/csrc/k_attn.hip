@@ -80,11 +80,9 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   constexpr int HK = attn_stage_keys<D, CQ, CK>();  // keys per stage
   // Where two or more waves share a SIMD, VALU instructions are what the loop
   // is short of: the logits' starting value -m_ref then sits in 16 registers
-  // of its own, refreshed only when the running maximum moves (no per-stage
-  // register fill), and every accumulator group of a stage keeps its own
-  // partial row sum (four short dependency chains instead of one long one).
-  // With one wave per SIMD (d = 128, query clusters of 64) the extra
-  // registers cost more than they save, and the stage-local forms are kept.
+  // of its own, refreshed only when the reference moves (no per-stage
+  // register fill). With one wave per SIMD (d = 128, query clusters of 64)
+  // the extra registers cost more than they save, and the fill is kept.
   constexpr bool LEAN = attn_waves_per_simd<D, CQ, CK>() > 1;
   constexpr int SUB = CK / HK;                      // stages per key cluster
   constexpr int MT = HK / 32;
