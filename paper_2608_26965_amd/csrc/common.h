@@ -145,7 +145,7 @@ constexpr int kNodeInts = 16;
 constexpr int kBins = 4096;       // linear bins of the multi-block split select
 constexpr int kChunk = 4096;      // tokens per block in the multi-block split passes
 constexpr int kTail = 2048;       // nodes of at most this size finish in one workgroup
-constexpr int kMomRows = 2048;    // rows per moment-partial block
+constexpr int kMomRows = 4096;    // rows per moment-partial block
 constexpr int kCompTile = 128;    // centroids per tile of the bf16 compensation kernel
 constexpr int kMaskWords = 2048;  // selection bitmap words in LDS: up to 65536 key clusters
 
