@@ -43,8 +43,8 @@ PEAK_HBM_GBS = 8000.0
 # plain-copy calibration (FETCH_SIZE x 2, WRITE_SIZE x 1; the traffic summaries
 # under profiles/ give the commands), valid for the kernel sources with the
 # given fingerprint only (else reported as null).
-ATTN_TRAFFIC = {"fingerprint": "6a85940ad400d117", "bytes": 8.4807e10}
-CLUSTER_TRAFFIC = {"fingerprint": "68b04a16e87bc068", "bytes": 1.8547e10}
+ATTN_TRAFFIC = {"fingerprint": "908dc7cb2b1f673f", "bytes": 8.4638e10}
+CLUSTER_TRAFFIC = {"fingerprint": "78f42e41dceae9d9", "bytes": 1.8441e10}
 
 
 def _fingerprint(files):
@@ -58,11 +58,11 @@ def _fingerprint(files):
 
 
 def attn_fingerprint():
-    return _fingerprint(("k_attn.hip", "attn_tile.h"))
+    return _fingerprint(("k_attn.hip", "attn_tile.h", "common.h"))
 
 
 def cluster_fingerprint():
-    return _fingerprint(("k_cluster.hip",))
+    return _fingerprint(("k_cluster.hip", "common.h"))
 
 
 def cpu_model():
