@@ -570,7 +570,11 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
   }
   if (active) {
     const float inv = 1.f / l;
-    for (int t = 0; t < d; ++t) op[qrow * d + t] = o[t] * inv;
+    // unrolled over DP with a guard: a loop to d would index o[] at run time
+    // and move it to scratch memory
+#pragma unroll
+    for (int t = 0; t < DP; ++t)
+      if (t < d) op[qrow * d + t] = o[t] * inv;
     lse[qrow] = m + logf(l);
   }
 }

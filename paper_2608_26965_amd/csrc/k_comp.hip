@@ -458,7 +458,10 @@ __global__ __launch_bounds__(256) void comp_f32_kernel(
   int orig = perm_q[(size_t)bh * nq + prow];
   orig = orig < 0 ? 0 : (orig >= nq ? nq - 1 : orig);
   float* orow = out + row_off(bh, orig, lo);
-  for (int t = 0; t < d; ++t) orow[t] = ws * op[qrow * d + t] + wc * (o[t] * inv_c);
+  // unrolled over DP with a guard, so that o[] stays in registers
+#pragma unroll
+  for (int t = 0; t < DP; ++t)
+    if (t < d) orow[t] = ws * op[qrow * d + t] + wc * (o[t] * inv_c);
   if (lse_out) lse_out[(size_t)bh * nq + orig] = lse;
 }
 
