@@ -42,16 +42,33 @@ constexpr int attn_stage_keys() {
   return CK == 128 ? 64 : CK;
 }
 
+// Key halves per stage. At d = 128 a query cluster of 64 is two wavefronts of
+// 32 queries, and its double-buffered stages (64 KB) let two workgroups share
+// a CU: one wavefront per SIMD, with nothing to overlap one wave's matrix
+// products with. Splitting every stage's keys in two gives four wavefronts per
+// workgroup in the same LDS: wavefront w takes queries 32 (w % 2) .. + 31
+// against the keys of row tile w / 2 of every stage, with a softmax state of
+// its own, and the two key halves of a query are merged at the end.
+template <int D, int CQ, int CK>
+constexpr int attn_key_split() {
+  return D == 128 && CQ == 64 ? 2 : 1;
+}
+template <int D, int CQ, int CK>
+constexpr int attn_waves() {
+  return CQ / 32 * attn_key_split<D, CQ, CK>();
+}
+
 // Waves per SIMD the bf16 kernel is compiled for (the second launch bound, a
 // minimum): as many workgroups as their double-buffered stages fit in LDS,
 // capped at two waves per SIMD, so that the MFMA of one wave overlaps the
 // softmax of another. Where registers and LDS allow, more workgroups run.
 template <int D, int CQ, int CK>
 constexpr int attn_waves_per_simd() {
+  constexpr int nw = attn_waves<D, CQ, CK>();
   constexpr int by_lds = (160 * 1024) / (8 * D * attn_stage_keys<D, CQ, CK>());
-  constexpr int by_waves = 8 / (CQ / 32);
+  constexpr int by_waves = 8 / nw;
   constexpr int blocks = by_lds < by_waves ? (by_lds < 1 ? 1 : by_lds) : by_waves;
-  return blocks * (CQ / 32) / 4 < 1 ? 1 : blocks * (CQ / 32) / 4;
+  return blocks * nw / 4 < 1 ? 1 : blocks * nw / 4;
 }
 
 // Compensation folded into the attention kernel: the staged centroid tiles of
@@ -70,22 +87,27 @@ struct FusedArgs {
 };
 
 template <int D, int CQ, int CK, bool FUSED = false>
-__global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void attn_bf16_kernel(
+__global__ __launch_bounds__((64 * attn_waves<D, CQ, CK>()), (attn_waves_per_simd<D, CQ, CK>())) void attn_bf16_kernel(
     const bf16* __restrict__ qp, const bf16* __restrict__ kp, const bf16* __restrict__ vp,
     const int32_t* __restrict__ count_k, const int32_t* __restrict__ lists,
     const int32_t* __restrict__ lens, int nqc, int nkc, int k, float sl2, bf16* __restrict__ op,
     float* __restrict__ lse, int total, const int32_t* __restrict__ sched, int cap,
     FusedArgs fa = FusedArgs{}) {
-  constexpr int NW = CQ / 32;
+  constexpr int QW = CQ / 32;                       // query tiles
+  constexpr int KSPL = attn_key_split<D, CQ, CK>();  // key halves
+  constexpr int NW = QW * KSPL;                      // wavefronts
+  constexpr int NT = 64 * NW;
   constexpr int HK = attn_stage_keys<D, CQ, CK>();  // keys per stage
   // Where two or more waves share a SIMD, VALU instructions are what the loop
   // is short of: the logits' starting value -m_ref then sits in 16 registers
   // of its own, refreshed only when the reference moves (no per-stage
-  // register fill). With one wave per SIMD (d = 128, query clusters of 64)
-  // the extra registers cost more than they save, and the fill is kept.
-  constexpr bool LEAN = attn_waves_per_simd<D, CQ, CK>() > 1;
+  // register fill). The key-split kernels (d = 128, query clusters of 64)
+  // keep the fill: their 256 registers have no room for the copy.
+  constexpr bool LEAN = attn_waves_per_simd<D, CQ, CK>() > 1 && attn_key_split<D, CQ, CK>() == 1;
   constexpr int SUB = CK / HK;                      // stages per key cluster
-  constexpr int MT = HK / 32;
+  constexpr int MT = HK / 32;   // row tiles of a stage
+  constexpr int MW = MT / KSPL;  // row tiles of a stage per wavefront
+  static_assert(MW * KSPL == MT, "key split");
   constexpr int KS = D / 16;
   constexpr int DT = D / 32;
   constexpr int KROW = 2 * D;   // bytes per K row
@@ -118,8 +140,10 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   }
   const int bh = item / nqc, a = item - bh * nqc;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
+  // query tile, key half (row tiles kh MW .. + MW - 1)
+  const int qw = KSPL > 1 ? w % QW : w, kh = KSPL > 1 ? w / QW : 0;
   const size_t nq_pad = (size_t)nqc * CQ, nk_pad = (size_t)nkc * CK;
-  const size_t qrow = (size_t)bh * nq_pad + (size_t)a * CQ + 32 * w + l32;
+  const size_t qrow = (size_t)bh * nq_pad + (size_t)a * CQ + 32 * qw + l32;
 
   // Queries pre-scaled by sl2 = scale * log2(e) (rounded to bf16 once), so
   // that the logits come out in the exponent's units.
@@ -146,9 +170,9 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   const int nc = FUSED && fa.tiles && nt < nkc ? fa.ntile * SUBC : 0;
   if (FUSED && nc) {
     const int nwords = (nkc + 31) >> 5;
-    for (int i = tid; i < nwords; i += CQ * 2) selmask[i] = 0u;
+    for (int i = tid; i < nwords; i += NT) selmask[i] = 0u;
     __syncthreads();
-    for (int i = tid; i < nt; i += CQ * 2) {
+    for (int i = tid; i < nt; i += NT) {
       const int b = lst[i];
       if (b >= 0 && b < nkc) atomicOr(&selmask[b >> 5], 1u << (b & 31));
     }
@@ -188,17 +212,18 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
     if (lane < BLANES) lds_dma16(src + CTK + CTV + s * HK * 4, boff + 16 * lane, bdst);
   };
   // Loop-invariant LDS read offsets (rows r and r + 32 share the swizzle key).
-  int koff[KS];
+  int koff[KS];  // with this wavefront's first row tile
   {
     const int row = kswz(l32);
 #pragma unroll
-    for (int kk = 0; kk < KS; ++kk) koff[kk] = swz_off<KROW>(row, 2 * kk + h);
+    for (int kk = 0; kk < KS; ++kk) koff[kk] = 32 * MW * kh * KROW + swz_off<KROW>(row, 2 * kk + h);
   }
-  int voff[MT][2];
+  int voff[MW][2];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
+  for (int mt = 0; mt < MW; ++mt)
 #pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) voff[mt][s2] = swz_off<VROW>(l32, 4 * mt + 2 * s2 + h);
+    for (int s2 = 0; s2 < 2; ++s2)
+      voff[mt][s2] = swz_off<VROW>(l32, 4 * (MW * kh + mt) + 2 * s2 + h);
 
   f32x16 oacc[DT];
   // m_run: running maximum of the scaled logits (log2 units); m_ref: the value
@@ -208,8 +233,8 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   f32x16 sinit;  // LEAN: -m_ref in every entry, the first logit product's addend
 #pragma unroll
   for (int r = 0; r < 16; ++r) sinit[r] = -m_ref;
-  f32x16 sacc[MT];   // logits of the current stage
-  bf16x8 pb[MT][2];  // its probabilities (bf16), the value product's operand
+  f32x16 sacc[MW];   // logits of this wavefront's keys of the current stage
+  bf16x8 pb[MW][2];  // their probabilities (bf16), the value product's operand
   // Row sums on the matrix cores instead of the VALU: a 16x16x32 product of
   // a 0/1 selector R with a probability group (the group's B operand: lane l
   // holds its 8 keys of query l % 32, in k block l / 16) gives in row 0,
@@ -229,7 +254,7 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   // S^T = K Q^T for the stage in key buffer ks
   auto logits = [&](const char* ks) __attribute__((always_inline)) {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
+    for (int mt = 0; mt < MW; ++mt) {
       if constexpr (!LEAN) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) sacc[mt][r] = -m_ref;
@@ -248,9 +273,9 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
       // only the remainder cluster of a head. Accumulator r of row tile mt
       // holds key 32 mt + 16 (r / 8) + 8 h + r % 8 (acc_key), so the test
       // compares cnt - 8 h with constants and keeps no per-key registers.
-      const int ch = cnt - 8 * h;
+      const int ch = cnt - 8 * h - 32 * MW * kh;
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+      for (int mt = 0; mt < MW; ++mt)
 #pragma unroll
         for (int r = 0; r < 16; ++r)
           if (32 * mt + 16 * (r >> 3) + (r & 7) >= ch) sacc[mt][r] = -INFINITY;
@@ -271,7 +296,7 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   };
   auto exps = [&](auto off_tag, float off, f32x4& rs) __attribute__((always_inline)) {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+    for (int mt = 0; mt < MW; ++mt)
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2) exp_group(off_tag, mt, s2, off, rs);
   };
@@ -281,7 +306,7 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   // the next group are formed
   auto pv_exps = [&](const char* vs, f32x4& rs) __attribute__((always_inline)) {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+    for (int mt = 0; mt < MW; ++mt)
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2) {
 #pragma unroll
@@ -296,7 +321,7 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+      for (int mt = 0; mt < MW; ++mt)
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2) {
           const bf16x8 av = *(const bf16x8*)(vs + 32 * dt * VROW + voff[mt][s2]);
@@ -314,12 +339,15 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
     if (__builtin_amdgcn_ballot_w64(!(fmaxf(ssum[0], ssum[1]) <= 0x1p40f) || m_run == -INFINITY)) {
       float mx = -INFINITY;
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
+      for (int mt = 0; mt < MW; ++mt)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[mt][r]);
       mx = fmaxf(mx, wave_xor32(mx));
       const float m_new = fmaxf(m_run, m_ref + mx);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      // split keys: no maximum yet where every key of the wavefront's half so
+      // far was padding (its sums stay 0)
+      const float m_use = KSPL > 1 && m_new == -INFINITY ? 0.f : m_new;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
       // lane n < 16 holds the sums of queries n and n + 16
       lacc[0] *= alpha;
       lacc[1] *= __shfl_xor(alpha, 16, 64);
@@ -328,16 +356,16 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[dt][r] *= alpha;
       ssum = f32x4{0.f, 0.f, 0.f, 0.f};
-      exps(std::true_type{}, m_ref - m_new, ssum);
+      exps(std::true_type{}, m_ref - m_use, ssum);
       m_run = m_new;
       if constexpr (LEAN) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) sinit[r] = -m_new;
+        for (int r = 0; r < 16; ++r) sinit[r] = -m_use;
       }
     }
     lacc[0] += ssum[0];
     lacc[1] += ssum[1];
-    m_ref = m_run;
+    m_ref = KSPL > 1 && m_run == -INFINITY ? 0.f : m_run;
   };
   auto sync_stage = [&]() __attribute__((always_inline)) {
     wait_vmcnt<0>();
@@ -438,11 +466,12 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
         // The bias of accumulator r of row tile mt is that of key acc_key(mt, r, h):
         // two runs of eight consecutive entries.
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+        for (int mt = 0; mt < MW; ++mt)
 #pragma unroll
           for (int hh = 0; hh < 2; ++hh) {
-            const float4 b0 = *(const float4*)&cbias[sb][32 * mt + 16 * hh + 8 * h];
-            const float4 b1 = *(const float4*)&cbias[sb][32 * mt + 16 * hh + 8 * h + 4];
+            const float* brow = &cbias[sb][32 * (MW * kh + mt) + 16 * hh + 8 * h];
+            const float4 b0 = *(const float4*)brow;
+            const float4 b1 = *(const float4*)(brow + 4);
             const float bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
 #pragma unroll
             for (int j = 0; j < 8; ++j)
@@ -463,7 +492,9 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
   {
     // Did the fast pass overflow? Its row sums are at least 1 (the first
     // stage's maximum) unless something became inf or NaN.
-    bool ok = l_tot <= 0x1p126f;
+    // A wavefront whose first stage was all padding (a key half past its
+    // cluster's count) has no reference yet: the safe pass sets one.
+    bool ok = l_tot <= 0x1p126f && (KSPL == 1 || m_run > -INFINITY);
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -475,10 +506,43 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
       l_tot = row_total();
     }
   }
+  // the state's reference: the row sums and outputs are taken against m_ref
+  float m_fin = KSPL > 1 ? m_ref : m_run;
+  if constexpr (KSPL > 1) {
+    // Key half 1 hands its state (reference, row sum, output accumulators) to
+    // key half 0 through the stage buffers; the merged state takes the larger
+    // reference of the halves that hold any key.
+    static_assert(KSPL == 2, "two key halves");
+    constexpr int NV = 2 + 16 * DT;  // floats per lane
+    static_assert(QW * NV * 64 * 4 <= 2 * STAGE, "merge buffer");
+    float* mb = (float*)smem + qw * NV * 64 + lane;  // entry i at mb[64 i]
+    __syncthreads();  // every wavefront is done with the stage buffers
+    if (kh == 1) {
+      mb[0] = m_ref;
+      mb[64] = l_tot;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mb[64 * (2 + 16 * dt + r)] = oacc[dt][r];
+    }
+    __syncthreads();
+    if (kh == 1) return;
+    const float lb = mb[64];
+    const float ma = l_tot > 0.f ? m_ref : -INFINITY, mbb = lb > 0.f ? mb[0] : -INFINITY;
+    const float m = fmaxf(ma, mbb);
+    const float mu = m == -INFINITY ? 0.f : m;
+    const float sa = __builtin_amdgcn_exp2f(ma - mu), sb = __builtin_amdgcn_exp2f(mbb - mu);
+    l_tot = l_tot * sa + lb * sb;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[dt][r] = oacc[dt][r] * sa + mb[64 * (2 + 16 * dt + r)] * sb;
+    m_fin = mu;
+  }
   const float inv = 1.f / l_tot;
   if constexpr (FUSED) {
     // merged rows to their original positions
-    const int prow = a * CQ + 32 * w + l32;
+    const int prow = a * CQ + 32 * qw + l32;
     if (prow >= fa.nq) return;
     int orig = fa.perm_q[(size_t)bh * fa.nq + prow];
     orig = orig < 0 ? 0 : (orig >= fa.nq ? fa.nq - 1 : orig);  // memory safety for a bad permutation
@@ -493,7 +557,7 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
         *(bf16x4*)(orow + 32 * dt + 8 * g + 4 * h) = v4;
       }
     if (fa.lse_out && h == 0)
-      fa.lse_out[(size_t)bh * fa.nq + orig] = (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2;
+      fa.lse_out[(size_t)bh * fa.nq + orig] = (m_fin + __builtin_amdgcn_logf(l_tot)) * kLn2;
     return;
   }
   bf16* orow = op + qrow * D;
@@ -506,7 +570,7 @@ __global__ __launch_bounds__(CQ * 2, (attn_waves_per_simd<D, CQ, CK>())) void at
       for (int j = 0; j < 4; ++j) v4[j] = f2bf(oacc[dt][4 * g + j] * inv);
       *(bf16x4*)(orow + 32 * dt + 8 * g + 4 * h) = v4;
     }
-  if (h == 0) lse[qrow] = (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2;
+  if (h == 0) lse[qrow] = (m_fin + __builtin_amdgcn_logf(l_tot)) * kLn2;
 }
 
 // fp32 path: one thread per query, keys streamed through LDS 32 at a time.
@@ -693,7 +757,8 @@ hipError_t run_bf16(const Prob& P, const void* qp, const void* kp, const void* v
     sched = nullptr;
   }
   hipLaunchKernelGGL((attn_bf16_kernel<D, CQ, CK, FUSED>),
-                     dim3(sched ? 8 * cap : 8 * ((P.nqc + 7) / 8) * P.BH), dim3(CQ * 2),
+                     dim3(sched ? 8 * cap : 8 * ((P.nqc + 7) / 8) * P.BH),
+                     dim3(64 * attn_waves<D, CQ, CK>()),
                      0, st, (const bf16*)qp, (const bf16*)kp, (const bf16*)vp, count_k, lists,
                      lens, P.nqc, P.nkc, k, scale * kLog2e, (bf16*)op, lse, total,
                      (const int32_t*)sched, cap, fa);

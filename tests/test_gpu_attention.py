@@ -129,6 +129,76 @@ def test_logit_jump_after_first_stage(d, cq, ck, n, k):
         G.flush(f"  head {h}: max abs err {err:.3g}")
 
 
+SHORT_FIRST = [
+    # d, cq, ck, n: the last key cluster holds n % ck <= 32 keys
+    (128, 64, 64, 650),
+    (128, 64, 128, 777),
+    (64, 128, 128, 918),
+    (64, 64, 64, 980),
+]
+
+
+@pytest.mark.parametrize("d,cq,ck,n", SHORT_FIRST)
+def test_short_cluster_first(d, cq, ck, n):
+    """The last key cluster (at most 32 real keys, so the second 32-key row
+    tile of its first stage is all padding) comes first in every list: every
+    third query cluster uses it alone (list length 1), the others follow it
+    with three more clusters, in both calls against the oracle. Where a
+    wavefront takes half of a stage's keys, one half then sees only padding in
+    its first stage, or in every stage."""
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    G.flush(f"short cluster first d={d} cq={cq} ck={ck} n={n}")
+    H, k = 2, 4
+    Q, K, V = mixture_inputs(41, H, n, d, "bf16", centres=8, sigma=0.4)
+    rng = np.random.default_rng(42)
+    p = ca.Problem(1, H, n, n, d, cq, ck, torch.bfloat16)
+    perm_q = np.stack([rng.permutation(n) for _ in range(H)]).astype(np.int32)
+    perm_k = np.stack([rng.permutation(n) for _ in range(H)]).astype(np.int32)
+    nkc, cq_n, ck_n = p.nkc, G.counts(n, cq), G.counts(n, ck)
+    assert ck_n[-1] <= 32 and nkc > k
+    L = np.zeros((H, p.nqc, k), np.int32)
+    lens = np.full((H, p.nqc), k, np.int32)
+    lens[:, ::3] = 1
+    ragged = []
+    for h in range(H):
+        rows = []
+        for a in range(p.nqc):
+            L[h, a, 0] = nkc - 1
+            L[h, a, 1:] = rng.choice(nkc - 1, size=k - 1, replace=False)
+            rows.append(L[h, a, :lens[h, a]].copy())
+        ragged.append(rows)
+    tau = 1 / math.sqrt(d)
+    tq = G.permuted_rows(Q, perm_q, cq, torch.bfloat16)
+    tk = G.permuted_rows(K, perm_k, ck, torch.bfloat16)
+    tv = G.value_tiles(V, perm_k, ck, torch.bfloat16)
+    cnt = G.dev(np.stack([ck_n] * H), torch.int32)
+    dL, dN = G.dev(L, torch.int32), G.dev(lens, torch.int32)
+    kbar = np.stack([ref.centroids(K[h], perm_k[h], ck_n) for h in range(H)]).astype(np.float32)
+    vbar = np.stack([ref.centroids(V[h], perm_k[h], ck_n) for h in range(H)]).astype(np.float32)
+    op, lse = ca.block_sparse_attn(p, tq, tk, tv, cnt, dL, k, lens=dN)
+    out, lse_out = ca.attn_compensated(p, tq, tk, tv, G.dev(kbar), G.dev(vbar), cnt, dL, k,
+                                       G.dev(perm_q, torch.int32), want_lse=True, lens=dN)
+    torch.cuda.synchronize()
+    op, lse = G.host(op), G.host(lse)
+    out, lse_out = G.host(out)[0], G.host(lse_out)
+    for h in range(H):
+        o, l = ref.sparse_attention(Q[h], K[h], V[h], perm_q[h], cq_n, perm_k[h], ck_n, ragged[h],
+                                    tau)
+        assert np.isfinite(op[h, :n]).all() and np.isfinite(lse[h, :n]).all(), h
+        err = np.abs(op[h, :n] - o[perm_q[h]]).max()
+        assert err <= G.TOL["bf16"], (h, err)
+        assert np.abs(lse[h, :n] - l[perm_q[h]]).max() <= 1e-3 * max(1.0, np.abs(l).max())
+        o_w, l_w = ref.compensate(Q[h], kbar[h], vbar[h], ck_n, perm_q[h], cq_n, ragged[h], o, l,
+                                  tau)
+        assert np.isfinite(out[h]).all() and np.isfinite(lse_out[h]).all(), h
+        ferr = np.abs(out[h] - o_w).max()
+        assert ferr <= G.TOL["bf16"], (h, ferr)
+        assert np.abs(lse_out[h] - l_w).max() <= 1e-3 * max(1.0, np.abs(l_w).max())
+        G.flush(f"  head {h}: max abs err {err:.3g} (two calls), {ferr:.3g} (one pass)")
+
+
 @pytest.mark.parametrize("dt,d,cq,ck,n,k", CASES)
 @pytest.mark.parametrize("enable", [True, False])
 def test_compensation_parity(dt, d, cq, ck, n, k, enable):
