@@ -268,7 +268,7 @@ CA_API int ca_select_hist(const ca_problem* p, const float* cent_q, const float*
  * Key rows past count_k[b] in a cluster are padding and are excluded.
  *
  * qp: [BH][nq_pad][d], kp: [BH][nk_pad][d], vp: [BH][nkc][d][ck] value tiles
- * as written by ca_cluster (all dtype), count_k: [BH][nkc],
+ * as written by ca_cluster (all dtype), count_k: [BH][nkc], each in [1, ck],
  * lists: [BH][nqc][k] with entries in [0, nkc) (not checked on the device;
  * out-of-range entries are clamped), lens: optional [BH][nqc] list lengths
  * (NULL: every list has k entries; otherwise row a uses its first lens[a]
