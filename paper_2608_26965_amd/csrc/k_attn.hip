@@ -42,16 +42,19 @@ constexpr int attn_stage_keys() {
   return CK == 128 ? 64 : CK;
 }
 
-// Key halves per stage. At d = 128 a query cluster of 64 is two wavefronts of
-// 32 queries, and its double-buffered stages (64 KB) let two workgroups share
-// a CU: one wavefront per SIMD, with nothing to overlap one wave's matrix
-// products with. Splitting every stage's keys in two gives four wavefronts per
-// workgroup in the same LDS: wavefront w takes queries 32 (w % 2) .. + 31
-// against the keys of row tile w / 2 of every stage, with a softmax state of
-// its own, and the two key halves of a query are merged at the end.
+// Key halves per stage. A query cluster of 64 is two wavefronts of 32
+// queries; with d = 128 its double-buffered stages (64 KB) let two workgroups
+// share a CU, one wavefront per SIMD with nothing to overlap one wave's matrix
+// products with, and with d = 64 LDS allows two and a half. Splitting every
+// stage's keys in two gives four wavefronts per workgroup in the same LDS:
+// wavefront w takes queries 32 (w % 2) .. + 31 against the keys of row tile
+// w / 2 of every stage, with a softmax state of its own, and the two key
+// halves of a query are merged at the end. (For query clusters of 128 the
+// split measured slower: eight wavefronts with half the work each, and one
+// workgroup per CU.)
 template <int D, int CQ, int CK>
 constexpr int attn_key_split() {
-  return D == 128 && CQ == 64 ? 2 : 1;
+  return CQ == 64 ? 2 : 1;
 }
 template <int D, int CQ, int CK>
 constexpr int attn_waves() {
@@ -101,8 +104,8 @@ __global__ __launch_bounds__((64 * attn_waves<D, CQ, CK>()), (attn_waves_per_sim
   // Where two or more waves share a SIMD, VALU instructions are what the loop
   // is short of: the logits' starting value -m_ref then sits in 16 registers
   // of its own, refreshed only when the reference moves (no per-stage
-  // register fill). The key-split kernels (d = 128, query clusters of 64)
-  // keep the fill: their 256 registers have no room for the copy.
+  // register fill). The key-split kernels (query clusters of 64) keep the
+  // fill: the copy would cost them a wave per SIMD (d = 64) or spill (d = 128).
   constexpr bool LEAN = attn_waves_per_simd<D, CQ, CK>() > 1 && attn_key_split<D, CQ, CK>() == 1;
   constexpr int SUB = CK / HK;                      // stages per key cluster
   constexpr int MT = HK / 32;   // row tiles of a stage
@@ -514,30 +517,37 @@ __global__ __launch_bounds__((64 * attn_waves<D, CQ, CK>()), (attn_waves_per_sim
     // reference of the halves that hold any key.
     static_assert(KSPL == 2, "two key halves");
     constexpr int NV = 2 + 16 * DT;  // floats per lane
-    static_assert(QW * NV * 64 * 4 <= 2 * STAGE, "merge buffer");
-    float* mb = (float*)smem + qw * NV * 64 + lane;  // entry i at mb[64 i]
-    __syncthreads();  // every wavefront is done with the stage buffers
-    if (kh == 1) {
-      mb[0] = m_ref;
-      mb[64] = l_tot;
+    // query tiles per round: as many as the stage buffers hold
+    constexpr int QR = (2 * STAGE) / (NV * 64 * 4) < QW ? (2 * STAGE) / (NV * 64 * 4) : QW;
+    static_assert(QR >= 1, "merge buffer");
+    for (int q0 = 0; q0 < QW; q0 += QR) {
+      const bool mine = qw >= q0 && qw < q0 + QR;
+      float* mb = (float*)smem + (qw - q0) * NV * 64 + lane;  // entry i at mb[64 i] (if mine)
+      __syncthreads();  // every wavefront is done with the stage buffers
+      if (kh == 1 && mine) {
+        mb[0] = m_ref;
+        mb[64] = l_tot;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
+        for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mb[64 * (2 + 16 * dt + r)] = oacc[dt][r];
+          for (int r = 0; r < 16; ++r) mb[64 * (2 + 16 * dt + r)] = oacc[dt][r];
+      }
+      __syncthreads();
+      if (kh == 0 && mine) {
+        const float lb = mb[64];
+        const float ma = l_tot > 0.f ? m_ref : -INFINITY, mbb = lb > 0.f ? mb[0] : -INFINITY;
+        const float m = fmaxf(ma, mbb);
+        const float mu = m == -INFINITY ? 0.f : m;
+        const float sa = __builtin_amdgcn_exp2f(ma - mu), sb = __builtin_amdgcn_exp2f(mbb - mu);
+        l_tot = l_tot * sa + lb * sb;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[dt][r] = oacc[dt][r] * sa + mb[64 * (2 + 16 * dt + r)] * sb;
+        m_fin = mu;
+      }
     }
-    __syncthreads();
     if (kh == 1) return;
-    const float lb = mb[64];
-    const float ma = l_tot > 0.f ? m_ref : -INFINITY, mbb = lb > 0.f ? mb[0] : -INFINITY;
-    const float m = fmaxf(ma, mbb);
-    const float mu = m == -INFINITY ? 0.f : m;
-    const float sa = __builtin_amdgcn_exp2f(ma - mu), sb = __builtin_amdgcn_exp2f(mbb - mu);
-    l_tot = l_tot * sa + lb * sb;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[dt][r] = oacc[dt][r] * sa + mb[64 * (2 + 16 * dt + r)] * sb;
-    m_fin = mu;
   }
   const float inv = 1.f / l_tot;
   if constexpr (FUSED) {
