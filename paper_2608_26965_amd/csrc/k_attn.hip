@@ -42,32 +42,39 @@ constexpr int attn_stage_keys() {
   return CK == 128 ? 64 : CK;
 }
 
-// Key halves per stage. A query cluster of 64 is two wavefronts of 32
-// queries; with d = 128 its double-buffered stages (64 KB) let two workgroups
-// share a CU, one wavefront per SIMD with nothing to overlap one wave's matrix
-// products with, and with d = 64 LDS allows two and a half. Splitting every
-// stage's keys in two gives four wavefronts per workgroup in the same LDS:
-// wavefront w takes queries 32 (w % 2) .. + 31 against the keys of row tile
-// w / 2 of every stage, with a softmax state of its own, and the two key
-// halves of a query are merged at the end. (For query clusters of 128 the
-// split measured slower: eight wavefronts with half the work each, and one
-// workgroup per CU.)
-template <int D, int CQ, int CK>
+// Key halves per stage (SPLIT, query clusters of 64 only). A query cluster of
+// 64 is two wavefronts of 32 queries; with d = 128 its double-buffered stages
+// (64 KB) let two workgroups share a CU, one wavefront per SIMD with nothing
+// to overlap one wave's matrix products with, and with d = 64 LDS allows two
+// and a half. Splitting every stage's keys in two gives four wavefronts per
+// workgroup in the same LDS: wavefront w takes queries 32 (w % 2) .. + 31
+// against the keys of row tile w / 2 of every stage, with a softmax state of
+// its own, and the two key halves of a query are merged at the end. The
+// launch takes it where a query cluster's selected tiles fit in one XCD's L2
+// (4 MiB): beyond that it measured slower than two wavefronts. (For query
+// clusters of 128 it measured slower everywhere: eight wavefronts with half
+// the work each, and one workgroup per CU.)
+template <int D, int CQ, int CK, bool SPLIT>
 constexpr int attn_key_split() {
-  return CQ == 64 ? 2 : 1;
+  return CQ == 64 && SPLIT ? 2 : 1;
 }
-template <int D, int CQ, int CK>
+template <int D, int CQ, int CK, bool SPLIT>
 constexpr int attn_waves() {
-  return CQ / 32 * attn_key_split<D, CQ, CK>();
+  return CQ / 32 * attn_key_split<D, CQ, CK, SPLIT>();
+}
+// the key-split kernel for k selected clusters per query cluster
+template <int D, int CQ, int CK>
+inline bool attn_use_split(int k) {
+  return CQ == 64 && (size_t)k * CK * D * 4 <= ((size_t)4 << 20);
 }
 
 // Waves per SIMD the bf16 kernel is compiled for (the second launch bound, a
 // minimum): as many workgroups as their double-buffered stages fit in LDS,
 // capped at two waves per SIMD, so that the MFMA of one wave overlaps the
 // softmax of another. Where registers and LDS allow, more workgroups run.
-template <int D, int CQ, int CK>
+template <int D, int CQ, int CK, bool SPLIT>
 constexpr int attn_waves_per_simd() {
-  constexpr int nw = attn_waves<D, CQ, CK>();
+  constexpr int nw = attn_waves<D, CQ, CK, SPLIT>();
   constexpr int by_lds = (160 * 1024) / (8 * D * attn_stage_keys<D, CQ, CK>());
   constexpr int by_waves = 8 / nw;
   constexpr int blocks = by_lds < by_waves ? (by_lds < 1 ? 1 : by_lds) : by_waves;
@@ -89,15 +96,16 @@ struct FusedArgs {
   Lay lo;
 };
 
-template <int D, int CQ, int CK, bool FUSED = false>
-__global__ __launch_bounds__((64 * attn_waves<D, CQ, CK>()), (attn_waves_per_simd<D, CQ, CK>())) void attn_bf16_kernel(
+template <int D, int CQ, int CK, bool FUSED, bool SPLIT>
+__global__ __launch_bounds__((64 * attn_waves<D, CQ, CK, SPLIT>()),
+                             (attn_waves_per_simd<D, CQ, CK, SPLIT>())) void attn_bf16_kernel(
     const bf16* __restrict__ qp, const bf16* __restrict__ kp, const bf16* __restrict__ vp,
     const int32_t* __restrict__ count_k, const int32_t* __restrict__ lists,
     const int32_t* __restrict__ lens, int nqc, int nkc, int k, float sl2, bf16* __restrict__ op,
     float* __restrict__ lse, int total, const int32_t* __restrict__ sched, int cap,
     FusedArgs fa = FusedArgs{}) {
   constexpr int QW = CQ / 32;                       // query tiles
-  constexpr int KSPL = attn_key_split<D, CQ, CK>();  // key halves
+  constexpr int KSPL = attn_key_split<D, CQ, CK, SPLIT>();  // key halves
   constexpr int NW = QW * KSPL;                      // wavefronts
   constexpr int NT = 64 * NW;
   constexpr int HK = attn_stage_keys<D, CQ, CK>();  // keys per stage
@@ -106,7 +114,7 @@ __global__ __launch_bounds__((64 * attn_waves<D, CQ, CK>()), (attn_waves_per_sim
   // of its own, refreshed only when the reference moves (no per-stage
   // register fill). The key-split kernels (query clusters of 64) keep the
   // fill: the copy would cost them a wave per SIMD (d = 64) or spill (d = 128).
-  constexpr bool LEAN = attn_waves_per_simd<D, CQ, CK>() > 1 && attn_key_split<D, CQ, CK>() == 1;
+  constexpr bool LEAN = attn_waves_per_simd<D, CQ, CK, SPLIT>() > 1 && KSPL == 1;
   constexpr int SUB = CK / HK;                      // stages per key cluster
   constexpr int MT = HK / 32;   // row tiles of a stage
   constexpr int MW = MT / KSPL;  // row tiles of a stage per wavefront
@@ -766,12 +774,22 @@ hipError_t run_bf16(const Prob& P, const void* qp, const void* kp, const void* v
   } else {
     sched = nullptr;
   }
-  hipLaunchKernelGGL((attn_bf16_kernel<D, CQ, CK, FUSED>),
-                     dim3(sched ? 8 * cap : 8 * ((P.nqc + 7) / 8) * P.BH),
-                     dim3(64 * attn_waves<D, CQ, CK>()),
-                     0, st, (const bf16*)qp, (const bf16*)kp, (const bf16*)vp, count_k, lists,
-                     lens, P.nqc, P.nkc, k, scale * kLog2e, (bf16*)op, lse, total,
-                     (const int32_t*)sched, cap, fa);
+  auto launch = [&](auto split_tag) {
+    constexpr bool SPLIT = decltype(split_tag)::value;
+    hipLaunchKernelGGL((attn_bf16_kernel<D, CQ, CK, FUSED, SPLIT>),
+                       dim3(sched ? 8 * cap : 8 * ((P.nqc + 7) / 8) * P.BH),
+                       dim3(64 * attn_waves<D, CQ, CK, SPLIT>()), 0, st, (const bf16*)qp,
+                       (const bf16*)kp, (const bf16*)vp, count_k, lists, lens, P.nqc, P.nkc, k,
+                       scale * kLog2e, (bf16*)op, lse, total, (const int32_t*)sched, cap, fa);
+  };
+  if constexpr (CQ == 64) {
+    if (attn_use_split<D, CQ, CK>(k))
+      launch(std::true_type{});
+    else
+      launch(std::false_type{});
+  } else {
+    launch(std::false_type{});
+  }
   return hipGetLastError();
 }
 

@@ -22,6 +22,10 @@ CASES = [
     ("bf16", 128, 128, 128, 1111, 2),
     ("bf16", 64, 128, 64, 900, 6),
     ("bf16", 128, 64, 128, 777, 7),
+    # query clusters of 64 with lists long enough for the two-wavefront kernel
+    # (their selected tiles exceed 4 MiB)
+    ("bf16", 128, 64, 64, 9000, 130),
+    ("bf16", 64, 64, 128, 33000, 130),
     ("f32", 64, 64, 64, 1000, 4),
     ("f32", 32, 32, 16, 333, 5),
     ("f32", 128, 16, 64, 300, 2),
@@ -130,27 +134,28 @@ def test_logit_jump_after_first_stage(d, cq, ck, n, k):
 
 
 SHORT_FIRST = [
-    # d, cq, ck, n: the last key cluster holds n % ck <= 32 keys
-    (128, 64, 64, 650),
-    (128, 64, 128, 777),
-    (64, 128, 128, 918),
-    (64, 64, 64, 980),
+    # d, cq, ck, n, k: the last key cluster holds n % ck <= 32 keys
+    (128, 64, 64, 650, 4),
+    (128, 64, 128, 777, 4),
+    (64, 128, 128, 918, 4),
+    (64, 64, 64, 980, 4),
+    (128, 64, 64, 8970, 130),  # the two-wavefront kernel for 64-query clusters
 ]
 
 
-@pytest.mark.parametrize("d,cq,ck,n", SHORT_FIRST)
-def test_short_cluster_first(d, cq, ck, n):
+@pytest.mark.parametrize("d,cq,ck,n,k", SHORT_FIRST)
+def test_short_cluster_first(d, cq, ck, n, k):
     """The last key cluster (at most 32 real keys, so the second 32-key row
     tile of its first stage is all padding) comes first in every list: every
     third query cluster uses it alone (list length 1), the others follow it
-    with three more clusters, in both calls against the oracle. Where a
+    with k - 1 more clusters, in both calls against the oracle. Where a
     wavefront takes half of a stage's keys, one half then sees only padding in
     its first stage, or in every stage."""
     import torch
     import paper_2608_26965_amd as ca
     from tests import gpu_util as G
-    G.flush(f"short cluster first d={d} cq={cq} ck={ck} n={n}")
-    H, k = 2, 4
+    G.flush(f"short cluster first d={d} cq={cq} ck={ck} n={n} k={k}")
+    H = 2
     Q, K, V = mixture_inputs(41, H, n, d, "bf16", centres=8, sigma=0.4)
     rng = np.random.default_rng(42)
     p = ca.Problem(1, H, n, n, d, cq, ck, torch.bfloat16)

@@ -57,7 +57,9 @@ def _compare(a, b, what):
 @pytest.mark.parametrize("d,cq,ck,n,keep", [
     (64, 128, 128, 3000, 0.2), (64, 64, 64, 2500, 0.25), (64, 64, 128, 2900, 0.3),
     (64, 128, 64, 3100, 0.2), (128, 64, 64, 2600, 0.25), (128, 128, 128, 4100, 0.3),
-    (128, 64, 128, 3000, 0.2), (128, 128, 64, 3300, 0.25)])
+    (128, 64, 128, 3000, 0.2), (128, 128, 64, 3300, 0.25),
+    # lists long enough for the two-wavefront kernel of 64-query clusters
+    (128, 64, 64, 12000, 0.75), (64, 64, 128, 20000, 0.9)])
 def test_fused_matches_separate(d, cq, ck, n, keep):
     import paper_2608_26965_amd as ca
     from tests import gpu_util as G
