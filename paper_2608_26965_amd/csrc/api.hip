@@ -191,7 +191,8 @@ void plan_workspace(const Prob& P, Workspace* W) {
   };
   const size_t BH = P.BH, d = P.d;
   const int nmax = P.nq > P.nk ? P.nq : P.nk;
-  W->nblk_mom = (nmax + kMomRows - 1) / kMomRows;
+  W->mom_rows = moment_rows(nmax, P.dtype, 2 * P.BH);
+  W->nblk_mom = (nmax + W->mom_rows - 1) / W->mom_rows;
   W->levels_q = num_levels(P.nq, P.cq);
   W->levels_k = num_levels(P.nk, P.ck);
   // Basic splitting runs every level with the multi-block kernels.

@@ -123,6 +123,7 @@ struct Workspace {
   size_t total;
   // derived split parameters
   int nblk_mom;             // row blocks per tensor for moment partials
+  int mom_rows;             // rows per moment-partial block
   int levels_q, levels_k;   // split levels per side
   int big_q, big_k;         // levels done by the multi-block kernels
   int max_big_nodes;        // nodes at the deepest multi-block level
@@ -145,9 +146,24 @@ constexpr int kNodeInts = 16;
 constexpr int kBins = 4096;       // linear bins of the multi-block split select
 constexpr int kChunk = 4096;      // tokens per block in the multi-block split passes
 constexpr int kTail = 2048;       // nodes of at most this size finish in one workgroup
-constexpr int kMomRows = 4096;    // rows per moment-partial block
+constexpr int kMomRows = 4096;    // rows per moment-partial block (at most)
 constexpr int kCompTile = 128;    // centroids per tile of the bf16 compensation kernel
 constexpr int kMaskWords = 2048;  // selection bitmap words in LDS: up to 65536 key clusters
+
+// Rows per moment-partial block: kMomRows, or fewer where the launch (one
+// workgroup per block and tensor) would otherwise have fewer than 512
+// workgroups, two per CU: each block is one workgroup's serial loop over its
+// rows, so few blocks of a short sequence are latency-bound, while more
+// blocks than that only add partials to write and sum. In multiples of the
+// rows the passes take per step (128 for the MFMA passes, 32 for the fp32
+// ones); tensors = 2 BH.
+inline int moment_rows(int nmax, int dtype, int tensors) {
+  const int g = dtype == CA_BF16 ? 128 : 32;
+  const int want = (512 + tensors - 1) / tensors;  // blocks per tensor
+  int r = (nmax + want - 1) / want;
+  r = (r + g - 1) / g * g;
+  return r < kMomRows ? r : kMomRows;
+}
 
 // Bytes of one bf16 compensation tile: kCompTile centroid key rows [kCompTile][d]
 // bf16, the centroid values transposed [d][kCompTile] bf16, and kCompTile fp32

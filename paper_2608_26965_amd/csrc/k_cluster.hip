@@ -51,7 +51,7 @@ struct Ctx {
   float* cent_v;
   void* vp;         // value tiles [BH][nkc][d][ck]
   Lay lv;           // strides of the values
-  int BH, H, d, dtype, xf, nmax, nblk;
+  int BH, H, d, dtype, xf, nmax, nblk, mom_rows;
   float* mats;      // [BH][kMats][d][d]
   float* vecs;      // [BH][kVecs][d]
   float* inv_q;     // [BH][nq]
@@ -142,7 +142,7 @@ __global__ __launch_bounds__(256) void moments_partial_kernel(Ctx C) {
   const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH, blk = blockIdx.x;
   const Side& S = C.s[side];
   const int d = C.d, d4 = (d + 3) / 4;
-  const int r0 = blk * kMomRows, r1 = min(S.n, r0 + kMomRows);
+  const int r0 = blk * C.mom_rows, r1 = min(S.n, r0 + C.mom_rows);
   float acc[4][16];
 #pragma unroll
   for (int q = 0; q < 4; ++q)
@@ -1091,7 +1091,7 @@ __global__ __launch_bounds__(256) void qnorm_partial_kernel(Ctx C) {
     const int t = e / (4 * d4), j = e % (4 * d4);
     Sk[t * kDP + j] = j < d ? Skg[t * d + j] : 0.f;
   }
-  const int r0 = blk * kMomRows, r1 = min(S.n, r0 + kMomRows);
+  const int r0 = blk * C.mom_rows, r1 = min(S.n, r0 + C.mom_rows);
   float acc[4][16];
 #pragma unroll
   for (int q = 0; q < 4; ++q)
@@ -1384,7 +1384,7 @@ __global__ __launch_bounds__(256) void moments_mfma_kernel(Ctx C) {
   const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH, blk = blockIdx.x;
   const Side& S = C.s[side];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
-  const int r0 = blk * kMomRows, r1 = min(S.n, r0 + kMomRows);
+  const int r0 = blk * C.mom_rows, r1 = min(S.n, r0 + C.mom_rows);
   bf16x8 id[2];
   ident_ops(l32, h, id);
   f32x16 g[NT];
@@ -1442,7 +1442,7 @@ __global__ __launch_bounds__(256) void qnorm_mfma_kernel(Ctx C) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
   stage_wops<D>(wop(C, bh, O_FK), wl);
   __syncthreads();
-  const int r0 = blk * kMomRows, r1 = min(S.n, r0 + kMomRows);
+  const int r0 = blk * C.mom_rows, r1 = min(S.n, r0 + C.mom_rows);
   bf16x8 id[2];
   ident_ops(l32, h, id);
   f32x16 g[NT];
@@ -3110,6 +3110,7 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
   C.xf = P.xf;
   C.nmax = P.nq > P.nk ? P.nq : P.nk;
   C.nblk = W.nblk_mom;
+  C.mom_rows = W.mom_rows;
   C.v = v;
   C.cent_v = out->cent_v;
   C.vp = out->vp;
