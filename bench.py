@@ -43,7 +43,7 @@ PEAK_HBM_GBS = 8000.0
 # plain-copy calibration (FETCH_SIZE x 2, WRITE_SIZE x 1; the traffic summaries
 # under profiles/ give the commands), valid for the kernel sources with the
 # given fingerprint only (else reported as null).
-ATTN_TRAFFIC = {"fingerprint": "7d982d07771bd546", "bytes": 8.4638e10}
+ATTN_TRAFFIC = {"fingerprint": "a52413eaa913dbe2", "bytes": 8.4638e10}
 CLUSTER_TRAFFIC = {"fingerprint": "78f42e41dceae9d9", "bytes": 1.8441e10}
 
 

@@ -598,11 +598,18 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
     const int32_t* __restrict__ count_k, const int32_t* __restrict__ lists,
     const int32_t* __restrict__ lens, int nqc, int nkc, int cq, int ck, int d, int k, float scale,
     float* __restrict__ op, float* __restrict__ lse) {
-  constexpr int KC = 32;
+  // 256 threads: query i of the cluster (qpad = cq rounded up to 64) and key
+  // part part = tid / qpad of parts = 256 / qpad; part p takes keys p, p +
+  // parts, ... of every staged chunk with a softmax state of its own, and the
+  // parts are merged at the end (32 queries at a time through LDS).
+  constexpr int KC = 32, QB = 32;
   __shared__ float Ksh[KC][DP + 1];
   __shared__ float Vsh[KC][DP + 1];
-  const int a = blockIdx.x, bh = blockIdx.y, i = threadIdx.x;
-  const bool active = i < cq;
+  __shared__ float mrg[(DP + 2) * QB];  // [field][query of the round]
+  const int a = blockIdx.x, bh = blockIdx.y;
+  const int qpad = (cq + 63) / 64 * 64, parts = 256 / qpad;
+  const int i = threadIdx.x % qpad, part = threadIdx.x / qpad;
+  const bool active = i < cq && part < parts;
   const size_t qrow = ((size_t)bh * nqc + a) * cq + (active ? i : 0);
   const size_t nk_pad = (size_t)nkc * ck;
   float q[DP], o[DP];
@@ -631,11 +638,17 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
         Vsh[kk][t] = (kk < nk && t < d) ? vp[(((size_t)bh * nkc + b) * d + t) * ck + k0 + kk] : 0.f;
       }
       __syncthreads();
-      for (int kk = 0; kk < nk; ++kk) {
-        float s = 0.f;
+      for (int kk = part; kk < nk; kk += parts) {
+        // four partial sums: four short dependency chains instead of one
+        float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
 #pragma unroll
-        for (int t = 0; t < DP; ++t) s = __builtin_fmaf(q[t], Ksh[kk][t], s);
-        s *= scale;
+        for (int t = 0; t < DP; t += 4) {
+          s0 = __builtin_fmaf(q[t], Ksh[kk][t], s0);
+          s1 = __builtin_fmaf(q[t + 1], Ksh[kk][t + 1], s1);
+          s2 = __builtin_fmaf(q[t + 2], Ksh[kk][t + 2], s2);
+          s3 = __builtin_fmaf(q[t + 3], Ksh[kk][t + 3], s3);
+        }
+        const float s = ((s0 + s1) + (s2 + s3)) * scale;
         if (s > m) {
           const float al = expf(m - s);
 #pragma unroll
@@ -650,7 +663,34 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
       }
     }
   }
-  if (active) {
+  // merge the key parts into part 0 (a part without keys has l = 0)
+  for (int q0 = 0; q0 < qpad; q0 += QB) {
+    const bool inq = i >= q0 && i < q0 + QB;
+    for (int pp = 1; pp < parts; ++pp) {
+      __syncthreads();
+      if (active && inq && part == pp) {
+        const int j = i - q0;
+        mrg[j] = m;
+        mrg[QB + j] = l;
+#pragma unroll
+        for (int t = 0; t < DP; ++t) mrg[(2 + t) * QB + j] = o[t];
+      }
+      __syncthreads();
+      if (active && inq && part == 0) {
+        const int j = i - q0;
+        const float lb = mrg[QB + j];
+        const float ma = l > 0.f ? m : -INFINITY, mb = lb > 0.f ? mrg[j] : -INFINITY;
+        const float mm = fmaxf(ma, mb);
+        const float mu = mm == -INFINITY ? 0.f : mm;
+        const float sa = expf(ma - mu), sb = expf(mb - mu);
+        l = l * sa + lb * sb;
+#pragma unroll
+        for (int t = 0; t < DP; ++t) o[t] = o[t] * sa + mrg[(2 + t) * QB + j] * sb;
+        m = mu;
+      }
+    }
+  }
+  if (active && part == 0) {
     const float inv = 1.f / l;
     // unrolled over DP with a guard: a loop to d would index o[] at run time
     // and move it to scratch memory
@@ -814,7 +854,7 @@ hipError_t launch_attn(const Prob& P, const void* qp, const void* kp, const void
     return hipErrorInvalidValue;
   }
   dim3 grid(P.nqc, P.BH);
-  int threads = ((P.cq + 63) / 64) * 64;
+  const int threads = 256;  // (cq rounded up to 64) x key parts
   if (P.d <= 32) {
     hipLaunchKernelGGL(attn_f32_kernel<32>, grid, dim3(threads), 0, st, (const float*)qp,
                        (const float*)kp, (const float*)vp, count_k, lists, lens, P.nqc, P.nkc,
