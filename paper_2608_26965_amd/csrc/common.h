@@ -150,19 +150,21 @@ constexpr int kMomRows = 4096;    // rows per moment-partial block (at most)
 constexpr int kCompTile = 128;    // centroids per tile of the bf16 compensation kernel
 constexpr int kMaskWords = 2048;  // selection bitmap words in LDS: up to 65536 key clusters
 
-// Rows per moment-partial block: kMomRows, or fewer where the launch (one
-// workgroup per block and tensor) would otherwise have fewer than 512
-// workgroups, two per CU: each block is one workgroup's serial loop over its
-// rows, so few blocks of a short sequence are latency-bound, while more
-// blocks than that only add partials to write and sum. In multiples of the
-// rows the passes take per step (128 for the MFMA passes, 32 for the fp32
-// ones); tensors = 2 BH.
-inline int moment_rows(int nmax, int dtype, int tensors) {
-  const int g = dtype == CA_BF16 ? 128 : 32;
+// Rows per block of a pass over the rows of `tensors` tensors of n rows, one
+// workgroup per block: cap, or fewer (in multiples of gran, the rows the pass
+// takes per step) where the launch would otherwise have fewer than 512
+// workgroups, two per CU. Each block is one workgroup's serial loop over its
+// rows, so a short sequence in a few blocks is latency-bound, while more
+// blocks than that only add per-block work (the moment passes' partials).
+inline int rows_per_block(int n, int gran, int cap, int tensors) {
   const int want = (512 + tensors - 1) / tensors;  // blocks per tensor
-  int r = (nmax + want - 1) / want;
-  r = (r + g - 1) / g * g;
-  return r < kMomRows ? r : kMomRows;
+  int r = (n + want - 1) / want;
+  r = (r + gran - 1) / gran * gran;
+  return r < cap ? r : cap;
+}
+// moment partials: 128 rows per step for the MFMA passes, 32 for the fp32 ones
+inline int moment_rows(int nmax, int dtype, int tensors) {
+  return rows_per_block(nmax, dtype == CA_BF16 ? 128 : 32, kMomRows, tensors);
 }
 
 // Bytes of one bf16 compensation tile: kCompTile centroid key rows [kCompTile][d]

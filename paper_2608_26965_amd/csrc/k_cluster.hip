@@ -51,7 +51,7 @@ struct Ctx {
   float* cent_v;
   void* vp;         // value tiles [BH][nkc][d][ck]
   Lay lv;           // strides of the values
-  int BH, H, d, dtype, xf, nmax, nblk, mom_rows;
+  int BH, H, d, dtype, xf, nmax, nblk, mom_rows, proj_rows;
   float* mats;      // [BH][kMats][d][d]
   float* vecs;      // [BH][kVecs][d]
   float* inv_q;     // [BH][nq]
@@ -1172,7 +1172,7 @@ __global__ __launch_bounds__(256) void qnorm_finish_kernel(Ctx C) {
 // Projection Y = X T (fp32), or Y = X for the raw-coordinate mode.
 // ---------------------------------------------------------------------------
 
-constexpr int kProjRows = 256;
+constexpr int kProjRows = 256;  // rows per projection block (at most)
 
 // Pseudo-random split coordinate in [0, 1) of the random-cluster control:
 // output number c (counting from 0) of splitmix64 (S. Vigna's generator,
@@ -1193,7 +1193,7 @@ __global__ __launch_bounds__(256) void project_kernel(Ctx C) {
   const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH;
   const Side& S = C.s[side];
   const int d = C.d, d4 = (d + 3) / 4;
-  const int r0 = blockIdx.x * kProjRows, r1 = min(S.n, r0 + kProjRows);
+  const int r0 = blockIdx.x * C.proj_rows, r1 = min(S.n, r0 + C.proj_rows);
   if (r0 >= r1) return;
   float* Y = S.y + (size_t)bh * S.n * d;
   if (C.xf == CA_XF_NONE) {
@@ -1521,7 +1521,7 @@ __global__ __launch_bounds__(256, 2) void project_mfma_kernel(Ctx C) {
   const int pid = blockIdx.y, side = pid / C.BH, bh = pid % C.BH;
   const Side& S = C.s[side];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
-  const int r0 = blockIdx.x * kProjRows, r1 = min(S.n, r0 + kProjRows);
+  const int r0 = blockIdx.x * C.proj_rows, r1 = min(S.n, r0 + C.proj_rows);
   if (r0 >= r1) return;
   stage_wops<D>(wop(C, bh, side == 0 ? O_TQ : O_TK), wl);
   __syncthreads();
@@ -3111,6 +3111,7 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
   C.nmax = P.nq > P.nk ? P.nq : P.nk;
   C.nblk = W.nblk_mom;
   C.mom_rows = W.mom_rows;
+  C.proj_rows = kProjRows;  // set for the projection launch below
   C.v = v;
   C.cent_v = out->cent_v;
   C.vp = out->vp;
@@ -3236,7 +3237,9 @@ hipError_t launch_cluster(const Prob& P, const void* q, const void* k, const voi
   {
     const int nmax = C.nmax;
     const size_t plds = kProjLds;
-    const dim3 pgrid((nmax + kProjRows - 1) / kProjRows, 2 * BH);
+    // the MFMA pass takes 128 rows per step, the fp32 one 32
+    C.proj_rows = rows_per_block(nmax, mfma && transformed ? 128 : 32, kProjRows, 2 * BH);
+    const dim3 pgrid((nmax + C.proj_rows - 1) / C.proj_rows, 2 * BH);
     if (mfma && transformed && d == 64)
       hipLaunchKernelGGL(project_mfma_kernel<64>, pgrid, dim3(256), 0, st, C);
     else if (mfma && transformed)
