@@ -23,6 +23,7 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import math
 import os
@@ -43,8 +44,8 @@ PEAK_HBM_GBS = 8000.0
 # plain-copy calibration (FETCH_SIZE x 2, WRITE_SIZE x 1; the traffic summaries
 # under profiles/ give the commands), valid for the kernel sources with the
 # given fingerprint only (else reported as null).
-ATTN_TRAFFIC = {"fingerprint": "a52413eaa913dbe2", "bytes": 8.4638e10}
-CLUSTER_TRAFFIC = {"fingerprint": "78f42e41dceae9d9", "bytes": 1.8441e10}
+ATTN_TRAFFIC = {"fingerprint": "4e609afc1da9508f", "bytes": 8.4878e10}
+CLUSTER_TRAFFIC = {"fingerprint": "ee7b6a8dec29e18b", "bytes": 1.8445e10}
 
 
 def _fingerprint(files):
@@ -127,16 +128,25 @@ def _timed(torch, step, n_ev, steps, warmup):
     """Run step() warmup times, then steps times with n_ev HIP events each
     (recorded by step on the stream the calls are enqueued on); returns (ms
     per step by the host clock between two synchronisations, mean ms between
-    consecutive events)."""
+    consecutive events). Python's garbage collector is run before and kept
+    off during the timed steps, so that no collection pause (the host issues
+    every launch) lands inside the timed region."""
     for _ in range(warmup):
         step()
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for s in range(steps):
-        step(evs[s])
-    torch.cuda.synchronize()
-    ms = (time.perf_counter() - t0) * 1e3 / steps
+    gc.collect()
+    gc_was_on = gc.isenabled()
+    gc.disable()
+    try:
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for s in range(steps):
+            step(evs[s])
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / steps
+    finally:
+        if gc_was_on:
+            gc.enable()
     calls = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(n_ev - 1)] for e in evs])
     return ms, calls.mean(axis=0)
 
