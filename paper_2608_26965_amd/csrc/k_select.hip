@@ -707,19 +707,36 @@ __global__ __launch_bounds__(64 * NWV, 4) void topk_block_kernel(const float* __
   // order: counts per wavefront first, then per float4 group in lane order
   const uint32_t thr = prefix;
   const int need_eq = rank + 1;
-  int eq_w = 0;
+  // Per wavefront: keys equal to the threshold and keys below it; it selects
+  // those below and its share of the first need_eq equal ones in index order
+  // (equal ranks eq_run .. eq_run + eq_w - 1), so one exchange of the two
+  // counts gives every wavefront its base in the list.
+  int eq_w = 0, lt_w = 0;
 #pragma unroll
-  for (int j = 0; j < VPL; ++j) eq_w += desc_key(v[j]) == thr;
+  for (int j = 0; j < VPL; ++j) {
+    const uint32_t u = desc_key(v[j]);
+    eq_w += u == thr;
+    lt_w += u < thr;
+  }
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) eq_w += __shfl_xor(eq_w, o, 64);
-  if (lane == 0) wcnt[0][w] = eq_w;
+  for (int o = 32; o > 0; o >>= 1) {
+    eq_w += __shfl_xor(eq_w, o, 64);
+    lt_w += __shfl_xor(lt_w, o, 64);
+  }
+  if (lane == 0) {
+    wcnt[0][w] = eq_w;
+    wcnt[1][w] = lt_w;
+  }
   __syncthreads();
-  int eq_run = 0;  // equal keys before this wavefront's range
-  for (int i = 0; i < w; ++i) eq_run += wcnt[0][i];
-  // selected per float4 group; the same walk twice: once to count, once to
-  // write (after the wavefronts' totals are known)
-  auto walk = [&](bool write, int sel_base, int32_t* out) {
-    int er = eq_run, pos_run = sel_base, sel_tot = 0;
+  int eq_run = 0, sel_base = 0;  // equal keys and selected keys before this wavefront's range
+  for (int i = 0; i < w; ++i) {
+    sel_base += wcnt[1][i] + min(max(need_eq - eq_run, 0), wcnt[0][i]);
+    eq_run += wcnt[0][i];
+  }
+  // the selected positions, per float4 group in lane order, written from
+  // the wavefront's base (the totals of the wavefronts before it)
+  auto walk = [&](int32_t* out) {
+    int er = eq_run, pos_run = sel_base;
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       uint32_t u[4];
@@ -740,7 +757,7 @@ __global__ __launch_bounds__(64 * NWV, 4) void topk_block_kernel(const float* __
         sel += take[e];
       }
       const int sel_incl = wave_incl_scan(sel, lane);
-      if (write) {
+      {
         int p = pos_run + sel_incl - sel;
 #pragma unroll
         for (int e = 0; e < 4; ++e)
@@ -749,16 +766,9 @@ __global__ __launch_bounds__(64 * NWV, 4) void topk_block_kernel(const float* __
       er += __builtin_amdgcn_readlane(eq_incl, 63);
       const int gsel = __builtin_amdgcn_readlane(sel_incl, 63);
       pos_run += gsel;
-      sel_tot += gsel;
     }
-    return sel_tot;
   };
-  const int sel_w = walk(false, 0, nullptr);
-  if (lane == 0) wcnt[1][w] = sel_w;
-  __syncthreads();
-  int sel_base = 0;
-  for (int i = 0; i < w; ++i) sel_base += wcnt[1][i];
-  walk(true, sel_base, lists + row * k);
+  walk(lists + row * k);
 }
 
 // ---------------------------------------------------------------------------
