@@ -6,9 +6,8 @@ shares no code with the HIP library.
 
 Every function works on one attention head (2-D arrays, rows = tokens) in fp64
 and cites the passage of the paper it follows. Where the paper leaves a choice
-open, the reading taken is stated in the docstring (the same readings are
-listed in the design doc). Inputs are the exact values the GPU receives (float32 or
-bf16-representable), upcast to fp64.
+open, the reading taken is stated in the docstring. Inputs are the exact
+values the GPU receives (float32 or bf16-representable), upcast to fp64.
 
 Pins: see tests/test_oracle_*.py. Parts with no independent pin are marked
 "parity unpinned" below (none at present).
