@@ -29,6 +29,9 @@ CASES = [
     ("f32", 64, 64, 64, 1000, 4),
     ("f32", 32, 32, 16, 333, 5),
     ("f32", 128, 16, 64, 300, 2),
+    # fp32 query clusters of 128 and 256: two and one key parts per query
+    ("f32", 64, 128, 64, 700, 3),
+    ("f32", 32, 256, 32, 600, 4),
 ]
 
 
