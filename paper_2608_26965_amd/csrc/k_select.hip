@@ -356,6 +356,17 @@ __device__ __forceinline__ void wave_lds_sync() {
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 }
 
+// Radix passes a candidate set can skip: every key between the smallest and
+// the largest shares their common leading bytes, so the byte passes over
+// those would only confirm them. Returns how many leading bytes are common
+// (4: all keys equal) and sets prefix to them.
+__device__ __forceinline__ int common_bytes(uint32_t kmin, uint32_t kmax, uint32_t* prefix) {
+  const uint32_t x = kmin ^ kmax;
+  const int n = x == 0u ? 4 : __builtin_clz(x) / 8;
+  *prefix = n == 0 ? 0u : (n == 4 ? kmin : kmin & (0xFFFFFFFFu << (32 - 8 * n)));
+  return n;
+}
+
 __device__ __forceinline__ int wave_incl_scan(int x, int lane) {
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
@@ -454,21 +465,33 @@ __global__ __launch_bounds__(256) void topk_wave_kernel(const float* __restrict_
     B = __builtin_amdgcn_readlane(fb, owner);
     rank = __builtin_amdgcn_readlane(fr, owner);
   }
-  // candidates: the keys of bin B
+  // candidates: the keys of bin B (and their smallest and largest key)
   int ncand = 0;
+  uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
 #pragma unroll
   for (int j = 0; j < VPL; ++j) {
     const bool hit = bin_of(v[j]) == B;
     const uint64_t m = __ballot(hit);
     const int pos = ncand + (int)__popcll(m & ((1ull << lane) - 1ull));
-    if (hit && pos < kWaveCand) ckey[pos] = desc_key(v[j]);
+    const uint32_t u = desc_key(v[j]);
+    if (hit) {
+      if (pos < kWaveCand) ckey[pos] = u;
+      kmin = min(kmin, u);
+      kmax = max(kmax, u);
+    }
     ncand += (int)__popcll(m);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, o, 64));
+    kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, o, 64));
   }
   wave_lds_sync();
   fence_row();
   const bool in_lds = ncand <= kWaveCand;
-  uint32_t prefix = 0;
-  for (int pass = 0; pass < 4; ++pass) {
+  uint32_t prefix;
+  const int p0 = common_bytes(kmin, kmax, &prefix);
+  for (int pass = p0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
     const uint32_t hmask = pass == 0 ? 0u : (0xFFFFFFFFu << (shift + 8));
     for (int i = lane; i < 256; i += 64) hist[i] = 0;
@@ -559,6 +582,7 @@ __global__ __launch_bounds__(64 * NWV, 4) void topk_block_kernel(const float* __
   __shared__ uint32_t ckey[NWV][kWaveCand];
   __shared__ float red_lo[NWV], red_hi[NWV];
   __shared__ int wcnt[2][NWV];
+  __shared__ uint32_t wkey[2][NWV];
   __shared__ int sh_over;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, tid = threadIdx.x;
   const size_t row = blockIdx.x;
@@ -644,22 +668,44 @@ __global__ __launch_bounds__(64 * NWV, 4) void topk_block_kernel(const float* __
     rank = __builtin_amdgcn_readlane(fr, owner);
   }
   // candidates of bin B: each wavefront compacts its own into its segment
+  // (and finds their smallest and largest key)
   int ncand = 0;
+  uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
 #pragma unroll
   for (int j = 0; j < VPL; ++j) {
     const bool hit = bin_of(v[j]) == B;
     const uint64_t m = __ballot(hit);
     const int pos = ncand + (int)__popcll(m & ((1ull << lane) - 1ull));
-    if (hit && pos < kWaveCand) ckey[w][pos] = desc_key(v[j]);
+    const uint32_t u = desc_key(v[j]);
+    if (hit) {
+      if (pos < kWaveCand) ckey[w][pos] = u;
+      kmin = min(kmin, u);
+      kmax = max(kmax, u);
+    }
     ncand += (int)__popcll(m);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, o, 64));
+    kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, o, 64));
   }
   if (tid == 0) sh_over = 0;
   __syncthreads();
-  if (lane == 0 && ncand > kWaveCand) sh_over = 1;
+  if (lane == 0) {
+    if (ncand > kWaveCand) sh_over = 1;
+    wkey[0][w] = kmin;
+    wkey[1][w] = kmax;
+  }
   __syncthreads();
   const bool in_lds = sh_over == 0;
-  uint32_t prefix = 0;
-  for (int pass = 0; pass < 4; ++pass) {
+#pragma unroll
+  for (int i = 0; i < NWV; ++i) {
+    kmin = min(kmin, wkey[0][i]);
+    kmax = max(kmax, wkey[1][i]);
+  }
+  uint32_t prefix;
+  const int p0 = common_bytes(kmin, kmax, &prefix);
+  for (int pass = p0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
     const uint32_t hmask = pass == 0 ? 0u : (0xFFFFFFFFu << (shift + 8));
     for (int i = tid; i < 256; i += NT) hist[i] = 0;
