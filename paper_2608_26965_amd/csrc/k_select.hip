@@ -8,6 +8,8 @@
 // order-preserving integer images of the scores (four 8-bit digit passes),
 // followed by an order-keeping compaction; it makes no floating-point
 // decision of its own, so given the scores the lists are exact.
+#include <algorithm>
+
 #include "common.h"
 
 namespace ca {
@@ -59,9 +61,9 @@ __global__ __launch_bounds__(256) void scores_kernel(const float* __restrict__ c
 // fp32 operand x is split into hi = bf16(x) and lo = bf16(x - hi), and
 // S = lo_q hi_k + hi_q lo_k + hi_q hi_k is accumulated in fp32 (the dropped
 // lo_q lo_k term is about 2^-16 of each product), so the scores keep close to
-// fp32 accuracy at the bf16 MFMA rate. One workgroup per 128 x 128 tile of
-// one head: wave w owns query rows 32 w .. 32 w + 31 and takes the four
-// 32-column key blocks in turn. v_mfma_f32_32x32x16_bf16 with the query rows
+// fp32 accuracy at the bf16 MFMA rate. Per 128 x 128 tile of one head: wave
+// w owns query rows 32 w .. 32 w + 31 and takes the four 32-column key blocks
+// in turn. v_mfma_f32_32x32x16_bf16 with the query rows
 // as the A operand and the key rows as B: lane l holds key column l % 32 of
 // the output block and query rows 8 (r / 4) + 4 (l / 32) + r % 4, so each
 // store instruction writes two 128-byte row segments.
@@ -76,13 +78,22 @@ __device__ __forceinline__ void split_hilo(const float4 x0, const float4 x1, bf1
   }
 }
 
+// A workgroup takes 128 query clusters against up to eight blocks of 128
+// key clusters (jb_per_wg). Each key block is split into bf16 hi / lo once
+// per workgroup and staged in LDS (rows padded by 16 bytes, so the 32 rows
+// one operand read touches fall in distinct banks) while the next block's
+// fp32 rows are loaded into registers.
 template <int D>
-__global__ __launch_bounds__(256) void scores_mfma_kernel(const float* __restrict__ cq,
-                                                          const float* __restrict__ ck, int nqc,
-                                                          int nkc, float* __restrict__ S) {
+__global__ __launch_bounds__(256) void scores_lds_kernel(const float* __restrict__ cq,
+                                                         const float* __restrict__ ck, int nqc,
+                                                         int nkc, int jb_per_wg,
+                                                         float* __restrict__ S) {
   constexpr int KS = D / 16;
-  const int bh = blockIdx.z, a0 = blockIdx.y * 128, b0 = blockIdx.x * 128;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, h = lane >> 5, l32 = lane & 31;
+  constexpr int RW = 2 * D + 8;  // bf16 per LDS row: hi, lo, padding
+  constexpr int NF4 = D / 8;     // float4 loads per thread and block (half a row)
+  __shared__ __attribute__((aligned(16))) __bf16 kt[128 * RW];
+  const int bh = blockIdx.z, a0 = blockIdx.y * 128;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
   const float* qh = cq + (size_t)bh * nqc * D;
   const float* kh = ck + (size_t)bh * nkc * D;
   const int arow = a0 + 32 * w + l32;
@@ -97,37 +108,60 @@ __global__ __launch_bounds__(256) void scores_mfma_kernel(const float* __restric
     }
     split_hilo(x0, x1, qhi[ks], qlo[ks]);
   }
+  // thread t stages half hf of key row r of a block
+  const int r = tid >> 1, hf = tid & 1;
+  float4 pf[NF4];
+  auto load_block = [&](int b0) __attribute__((always_inline)) {
+    const int row = b0 + r;
+#pragma unroll
+    for (int i = 0; i < NF4; ++i) {
+      pf[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (row < nkc) pf[i] = *(const float4*)(kh + (size_t)row * D + hf * (D / 2) + 4 * i);
+    }
+  };
   float* Sh = S + (size_t)bh * nqc * nkc;
-  for (int j = 0; j < 4; ++j) {
-    if (b0 + 32 * j >= nkc) break;  // uniform
-    const int bcol = b0 + 32 * j + l32;
-    bf16x8 khi[KS], klo[KS];
+  const int bfirst = blockIdx.x * jb_per_wg * 128;
+  const int bend = min(nkc, bfirst + jb_per_wg * 128);
+  load_block(bfirst);
+  for (int b0 = bfirst; b0 < bend; b0 += 128) {
+    __syncthreads();  // every wavefront is done with the previous block
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
-      if (bcol < nkc) {
-        const float4* src = (const float4*)(kh + (size_t)bcol * D + 16 * ks + 8 * h);
-        x0 = src[0];
-        x1 = src[1];
+    for (int i = 0; i < NF4; i += 2) {
+      bf16x8 hi8, lo8;
+      split_hilo(pf[i], pf[i + 1], hi8, lo8);
+      *(bf16x8*)&kt[r * RW + hf * (D / 2) + 4 * i] = hi8;
+      *(bf16x8*)&kt[r * RW + D + hf * (D / 2) + 4 * i] = lo8;
+    }
+    __syncthreads();
+    if (b0 + 128 < bend) load_block(b0 + 128);
+#pragma unroll 1
+    for (int j = 0; j < 4; ++j) {
+      if (b0 + 32 * j >= nkc) break;  // uniform
+      const int bcol = b0 + 32 * j + l32;
+      const __bf16* kr = &kt[(32 * j + l32) * RW];
+      bf16x8 khi[KS], klo[KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        khi[ks] = *(const bf16x8*)(kr + 16 * ks + 8 * h);
+        klo[ks] = *(const bf16x8*)(kr + D + 16 * ks + 8 * h);
       }
-      split_hilo(x0, x1, khi[ks], klo[ks]);
-    }
-    f32x16 acc;
+      f32x16 acc;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+      for (int q = 0; q < 16; ++q) acc[q] = 0.f;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qlo[ks], khi[ks], acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qhi[ks], klo[ks], acc, 0, 0, 0);
-    }
+      for (int ks = 0; ks < KS; ++ks) {
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qlo[ks], khi[ks], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qhi[ks], klo[ks], acc, 0, 0, 0);
+      }
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qhi[ks], khi[ks], acc, 0, 0, 0);
-    if (bcol < nkc) {
+      for (int ks = 0; ks < KS; ++ks)
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qhi[ks], khi[ks], acc, 0, 0, 0);
+      if (bcol < nkc) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int a = a0 + 32 * w + 8 * (r >> 2) + 4 * h + (r & 3);
-        if (a < nqc) Sh[(size_t)a * nkc + bcol] = acc[r];
+        for (int q = 0; q < 16; ++q) {
+          const int a = a0 + 32 * w + 8 * (q >> 2) + 4 * h + (q & 3);
+          if (a < nqc) Sh[(size_t)a * nkc + bcol] = acc[q];
+        }
       }
     }
   }
@@ -138,12 +172,17 @@ hipError_t launch_scores(const Prob& P, const float* cq, const float* ck, float*
                          hipStream_t st) {
   const bool aligned = (((uintptr_t)cq | (uintptr_t)ck) & 15) == 0;
   if (P.dtype == CA_BF16 && (P.d == 64 || P.d == 128) && aligned) {
-    const dim3 grid((P.nkc + 127) / 128, (P.nqc + 127) / 128, P.BH);
+    // key blocks per workgroup: up to eight, while the launch keeps at
+    // least 2048 workgroups
+    const int nb = (P.nkc + 127) / 128, nr = (P.nqc + 127) / 128;
+    const long wgs = (long)nb * nr * P.BH;
+    const int jb = (int)std::max(1L, std::min(8L, wgs / 2048));
+    const dim3 grid((nb + jb - 1) / jb, nr, P.BH);
     if (P.d == 64)
-      hipLaunchKernelGGL(scores_mfma_kernel<64>, grid, dim3(256), 0, st, cq, ck, P.nqc, P.nkc,
+      hipLaunchKernelGGL(scores_lds_kernel<64>, grid, dim3(256), 0, st, cq, ck, P.nqc, P.nkc, jb,
                          scores);
     else
-      hipLaunchKernelGGL(scores_mfma_kernel<128>, grid, dim3(256), 0, st, cq, ck, P.nqc, P.nkc,
+      hipLaunchKernelGGL(scores_lds_kernel<128>, grid, dim3(256), 0, st, cq, ck, P.nqc, P.nkc, jb,
                          scores);
   } else {
     const dim3 grid((P.nkc + kTileS - 1) / kTileS, (P.nqc + kTileS - 1) / kTileS, P.BH);
