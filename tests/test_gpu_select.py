@@ -85,6 +85,33 @@ def test_topk_long_rows_with_ties(nkc, k):
             assert np.array_equal(L[h, a], ref.topk(S[h, a:a + 1].astype(np.float64), k)[0]), (h, a)
 
 
+@pytest.mark.gpu
+@pytest.mark.parametrize("nkc,k", [(4096, 100), (8192, 64), (8192, 819), (6000, 3), (2052, 2052)])
+def test_topk_many_long_rows(nkc, k):
+    """A thousand rows of 2049-8192 scores (more rows than workgroups fit on
+    the device at once, one row per block of four wavefronts). Rows mix
+    continuous values, heavy ties, constant rows, subnormal ranges and far
+    outliers; every list equals the oracle's."""
+    import torch
+    import paper_2608_26965_amd as ca
+    from tests import gpu_util as G
+    G.flush(f"many long-row top-k nkc={nkc} k={k}")
+    rng = np.random.default_rng(3 * nkc + k)
+    H, nqc = 2, 500
+    S = rng.standard_normal((H, nqc, nkc)).astype(np.float32)
+    S[:, 1::5] = rng.integers(-3, 4, size=(H, len(range(1, nqc, 5)), nkc))
+    S[:, 2::5] = 0.75
+    S[:, 3::5] = (np.arange(nkc) % 7).astype(np.float32) * np.float32(1e-44)
+    S[:, 4::5, ::97] = -1e30
+    p = ca.Problem(1, H, nqc * 16, nkc * 16, 8, 16, 16, torch.float32)
+    lists, _ = ca.select(p, None, None, k, scores_in=G.dev(S))
+    torch.cuda.synchronize()
+    L = lists.cpu().numpy()
+    for h in range(H):
+        for a in range(nqc):
+            assert np.array_equal(L[h, a], ref.topk(S[h, a:a + 1].astype(np.float64), k)[0]), (h, a)
+
+
 HIST_CASES = [
     # nqc, nkc, d, min_count, mass_recall
     (16, 16, 64, 4, 0.0),
